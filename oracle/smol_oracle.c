@@ -1,0 +1,368 @@
+/*
+ * smol_oracle.c -- plain, slow, scalar CPU oracle for fused image preprocessing
+ * (Kang et al., "Jointly Optimizing Preprocessing and Inference for DNN-based
+ * Visual Analytics", PVLDB 14).
+ *
+ * TEST INFRASTRUCTURE. Only the test suite, the smoke check and the CPU-baseline
+ * leg of the benchmark load this library. The product path (the HIP library)
+ * shares no code, header, table or constant with it.
+ *
+ * What it computes is the standard ResNet preprocessing of the paper's
+ * measurement study (section 2, "Breakdown of end-to-end DNN inference",
+ * steps 2-4), applied to already-decoded pixels:
+ *   step 2  aspect-preserving resize so the short edge is S, then a central
+ *           C_h x C_w crop;
+ *   step 3  convert to float32 and normalise per channel;
+ *   step 4  rearrange to channels-first (NCHW).
+ * plus, for planar YCbCr 4:2:0 input, the colorspace conversion that the
+ * implementation appendix lists among its preprocessing methods (App. A,
+ * "Components"), done before the resize.
+ *
+ * The crop is taken in output space: resizing and cropping may be swapped
+ * (section 6.2, reordering rule 3), so the oracle evaluates the resize only at
+ * the output pixels that survive the crop. The crop offsets are Algorithm 1's
+ * l = (w' - 224)/2, t = (h' - 224)/2, generalised to C_w, C_h and floored.
+ *
+ * Readings where the paper is silent (interpolation convention, rounding of the
+ * long side, colour matrix, fp16 rounding) are fixed as follows:
+ *   - resized long side: floor(S * long / short), exact integer arithmetic;
+ *   - crop offsets: floor((W' - C_w)/2), floor((H' - C_h)/2);
+ *   - bilinear with half-pixel centres (align_corners = false), clamped at the
+ *     edges, no antialiasing; the source coordinate of output index x is the
+ *     exact rational ((2x+1)*in - out) / (2*out); its integer part is taken
+ *     exactly and only the fractional weight is rounded, once, to fp32;
+ *   - interpolation in fp32 in the lerp form a + w*(b - a), horizontal first,
+ *     every operation rounded on its own (build with -ffp-contract=off);
+ *   - normalisation (v - mean_c) / std_c in fp32 with mean and std in 0..255
+ *     units;
+ *   - fp16 output rounds to nearest, ties to even, written out below from the
+ *     IEEE-754 binary16 format;
+ *   - YCbCr: BT.601 full range (JFIF) with centred 4:2:0 chroma siting; the
+ *     chroma sample that serves luma pixel x sits at x/2 - 1/4; each channel is
+ *     clamped to [0, 255] in fp32 (no integer rounding) at every luma pixel,
+ *     before the resize.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+enum { ORACLE_OUT_F32 = 0, ORACLE_OUT_F16 = 1 };
+enum { ORACLE_OK = 0, ORACLE_ERR = -1 };
+
+/* ------------------------------------------------------------------------- */
+/* Geometry                                                                   */
+/* ------------------------------------------------------------------------- */
+
+/* Section 2, step 2: aspect-preserving resize whose short edge becomes S. The
+ * long side is floored. A square image becomes S x S. */
+void oracle_resized_dims(int64_t W, int64_t H, int64_t S, int64_t *Wr, int64_t *Hr)
+{
+    if (W <= H) {
+        *Wr = S;
+        *Hr = (S * H) / W;
+    } else {
+        *Hr = S;
+        *Wr = (S * W) / H;
+    }
+}
+
+/* Algorithm 1: l, t = (w' - C_w)/2, (h' - C_h)/2, floored. */
+void oracle_crop_offsets(int64_t Wr, int64_t Hr, int64_t Ch, int64_t Cw, int64_t *left,
+                         int64_t *top)
+{
+    *left = (Wr - Cw) / 2;
+    *top = (Hr - Ch) / 2;
+}
+
+/* One axis of the half-pixel bilinear map from an output index x (in the
+ * resized image of length `out`) to the source (length `in`):
+ *     u = (x + 1/2) * in / out - 1/2 = ((2x + 1) * in - out) / (2 * out).
+ * u below 0 clamps to 0; u at or beyond in - 1 clamps to in - 1. The two taps
+ * are floor(u) and floor(u) + 1 with weight u - floor(u) on the second. */
+void oracle_axis_tap(int64_t x, int64_t in, int64_t out, int64_t *x0, int64_t *x1, float *w)
+{
+    int64_t num = (2 * x + 1) * in - out; /* 2*out times u */
+    int64_t den = 2 * out;
+    if (num <= 0) {
+        *x0 = 0;
+        *x1 = 0;
+        *w = 0.0f;
+        return;
+    }
+    int64_t q = num / den;
+    int64_t rem = num - q * den;
+    if (q >= in - 1) {
+        *x0 = in - 1;
+        *x1 = in - 1;
+        *w = 0.0f;
+        return;
+    }
+    *x0 = q;
+    *x1 = q + 1;
+    *w = (float)rem / (float)den; /* both operands exact in fp32 (< 2^24) */
+}
+
+/* ------------------------------------------------------------------------- */
+/* Colour                                                                     */
+/* ------------------------------------------------------------------------- */
+
+/* BT.601 full-range (JFIF) YCbCr -> RGB with Kr = 0.299, Kb = 0.114:
+ *   R = Y + 2(1-Kr) (Cr-128)
+ *   G = Y - [2Kb(1-Kb)/Kg] (Cb-128) - [2Kr(1-Kr)/Kg] (Cr-128)
+ *   B = Y + 2(1-Kb) (Cb-128)
+ * Coefficients are derived in double and rounded once to fp32; the expressions
+ * are evaluated left to right in fp32; each channel is clamped to [0, 255]. */
+void oracle_ycbcr_to_rgb(float Y, float Cb, float Cr, float *rgb)
+{
+    const double kr = 0.299, kb = 0.114, kg = 1.0 - kr - kb;
+    const float r_cr = (float)(2.0 * (1.0 - kr));
+    const float g_cb = (float)(2.0 * kb * (1.0 - kb) / kg);
+    const float g_cr = (float)(2.0 * kr * (1.0 - kr) / kg);
+    const float b_cb = (float)(2.0 * (1.0 - kb));
+    float cb = Cb - 128.0f;
+    float cr = Cr - 128.0f;
+    float r = Y + r_cr * cr;
+    float g = Y - g_cb * cb;
+    g = g - g_cr * cr;
+    float b = Y + b_cb * cb;
+    rgb[0] = r < 0.0f ? 0.0f : (r > 255.0f ? 255.0f : r);
+    rgb[1] = g < 0.0f ? 0.0f : (g > 255.0f ? 255.0f : g);
+    rgb[2] = b < 0.0f ? 0.0f : (b > 255.0f ? 255.0f : b);
+}
+
+/* Centred 4:2:0 siting: the chroma coordinate of luma index x is u = x/2 - 1/4
+ * (exact in fp32 for the sizes allowed here). Same clamping as the luma map. */
+static void chroma_tap(int64_t x, int64_t n, int64_t *c0, int64_t *c1, float *w)
+{
+    float u = (float)x * 0.5f - 0.25f;
+    if (u <= 0.0f) {
+        *c0 = 0;
+        *c1 = 0;
+        *w = 0.0f;
+        return;
+    }
+    int64_t f = (int64_t)floorf(u);
+    if (f >= n - 1) {
+        *c0 = n - 1;
+        *c1 = n - 1;
+        *w = 0.0f;
+        return;
+    }
+    *c0 = f;
+    *c1 = f + 1;
+    *w = u - (float)f;
+}
+
+/* Planar I420 (Y: W x H, Cb and Cr: ceil(W/2) x ceil(H/2), tightly pitched)
+ * to an fp32 RGB image, W x H x 3 interleaved: chroma is bilinearly upsampled
+ * to every luma pixel, then converted and clamped there. */
+void oracle_yuv420_to_rgb(const uint8_t *yp, const uint8_t *cbp, const uint8_t *crp, int64_t W,
+                          int64_t H, float *rgb)
+{
+    int64_t Wc = (W + 1) / 2, Hc = (H + 1) / 2;
+    for (int64_t y = 0; y < H; ++y) {
+        int64_t r0, r1;
+        float wy;
+        chroma_tap(y, Hc, &r0, &r1, &wy);
+        for (int64_t x = 0; x < W; ++x) {
+            int64_t k0, k1;
+            float wx;
+            chroma_tap(x, Wc, &k0, &k1, &wx);
+            float c[2];
+            const uint8_t *planes[2] = {cbp, crp};
+            for (int p = 0; p < 2; ++p) {
+                const uint8_t *pl = planes[p];
+                float a = (float)pl[r0 * Wc + k0], b = (float)pl[r0 * Wc + k1];
+                float t = a + wx * (b - a);
+                a = (float)pl[r1 * Wc + k0];
+                b = (float)pl[r1 * Wc + k1];
+                float bo = a + wx * (b - a);
+                c[p] = t + wy * (bo - t);
+            }
+            oracle_ycbcr_to_rgb((float)yp[y * W + x], c[0], c[1], &rgb[(y * W + x) * 3]);
+        }
+    }
+}
+
+/* ------------------------------------------------------------------------- */
+/* fp16 rounding                                                              */
+/* ------------------------------------------------------------------------- */
+
+/* IEEE-754 binary32 -> binary16, round to nearest, ties to even. */
+uint16_t oracle_f32_to_f16(float f)
+{
+    uint32_t x;
+    memcpy(&x, &f, 4);
+    uint32_t sign = (x >> 16) & 0x8000u;
+    uint32_t e = (x >> 23) & 0xffu;
+    uint32_t m = x & 0x7fffffu;
+    if (e == 0xffu) /* inf or nan (nan keeps a set quiet bit) */
+        return (uint16_t)(sign | 0x7c00u | (m ? 0x200u | (m >> 13) : 0u));
+    int32_t he = (int32_t)e - 127 + 15; /* biased binary16 exponent */
+    if (he >= 31)                       /* too large even before rounding */
+        return (uint16_t)(sign | 0x7c00u);
+    if (he <= 0) {
+        /* binary16 subnormal (or zero): value = sig * 2^(e-150), sig = 1.m
+         * as a 24-bit integer; the result is sig * 2^(e-150) / 2^-24 =
+         * sig >> (126 - e), rounded to nearest even. */
+        if (he < -10) /* below half the smallest subnormal: rounds to zero */
+            return (uint16_t)sign;
+        uint32_t sig = m | 0x800000u;
+        uint32_t shift = (uint32_t)(126 - (int32_t)e); /* 14 .. 24 */
+        uint32_t q = sig >> shift;
+        uint32_t rest = sig & ((1u << shift) - 1u);
+        uint32_t half = 1u << (shift - 1);
+        if (rest > half || (rest == half && (q & 1u)))
+            q += 1u; /* may carry into the smallest normal: still correct */
+        return (uint16_t)(sign | q);
+    }
+    uint32_t q = ((uint32_t)he << 10) | (m >> 13);
+    uint32_t rest = m & 0x1fffu;
+    if (rest > 0x1000u || (rest == 0x1000u && (q & 1u)))
+        q += 1u; /* a carry into the exponent field is the correct result */
+    return (uint16_t)(sign | q);
+}
+
+/* ------------------------------------------------------------------------- */
+/* Resize + crop + normalise + NCHW store                                     */
+/* ------------------------------------------------------------------------- */
+
+/* rgb: fp32 image, W x H x 3 interleaved. out: 3 x Ch x Cw of the out dtype. */
+static void resample_crop_normalize(const float *rgb, int64_t W, int64_t H, int64_t S,
+                                    int64_t Ch, int64_t Cw, const float *mean, const float *stdv,
+                                    int out_dtype, void *out)
+{
+    int64_t Wr, Hr, left, top;
+    oracle_resized_dims(W, H, S, &Wr, &Hr);
+    oracle_crop_offsets(Wr, Hr, Ch, Cw, &left, &top);
+    for (int64_t yc = 0; yc < Ch; ++yc) {
+        int64_t y0, y1;
+        float wy;
+        oracle_axis_tap(yc + top, H, Hr, &y0, &y1, &wy);
+        for (int64_t xc = 0; xc < Cw; ++xc) {
+            int64_t x0, x1;
+            float wx;
+            oracle_axis_tap(xc + left, W, Wr, &x0, &x1, &wx);
+            for (int c = 0; c < 3; ++c) {
+                float p00 = rgb[(y0 * W + x0) * 3 + c];
+                float p01 = rgb[(y0 * W + x1) * 3 + c];
+                float p10 = rgb[(y1 * W + x0) * 3 + c];
+                float p11 = rgb[(y1 * W + x1) * 3 + c];
+                float t = p00 + wx * (p01 - p00);
+                float b = p10 + wx * (p11 - p10);
+                float v = t + wy * (b - t);
+                float o = (v - mean[c]) / stdv[c];
+                int64_t idx = ((int64_t)c * Ch + yc) * Cw + xc;
+                if (out_dtype == ORACLE_OUT_F32)
+                    ((float *)out)[idx] = o;
+                else
+                    ((uint16_t *)out)[idx] = oracle_f32_to_f16(o);
+            }
+        }
+    }
+}
+
+static int params_ok(int64_t W, int64_t H, int32_t S, int32_t Ch, int32_t Cw, int32_t out_dtype)
+{
+    if (W < 1 || H < 1 || S < 1 || Ch < 1 || Cw < 1)
+        return 0;
+    if (out_dtype != ORACLE_OUT_F32 && out_dtype != ORACLE_OUT_F16)
+        return 0;
+    int64_t Wr, Hr;
+    oracle_resized_dims(W, H, S, &Wr, &Hr);
+    if (Ch > Hr || Cw > Wr) /* the crop must lie inside the resized image */
+        return 0;
+    /* the fp32 weight needs 2*out < 2^24 to be formed from exact operands */
+    if (2 * Wr >= (1 << 24) || 2 * Hr >= (1 << 24))
+        return 0;
+    return 1;
+}
+
+/* One packed HWC RGB uint8 image (row pitch in bytes) -> 3 x Ch x Cw. */
+int smol_ref_preprocess_image(const uint8_t *img, int32_t W, int32_t H, int32_t pitch, int32_t S,
+                              int32_t Ch, int32_t Cw, const float *mean, const float *stdv,
+                              int32_t out_dtype, void *out)
+{
+    if (!params_ok(W, H, S, Ch, Cw, out_dtype) || pitch < 3 * W)
+        return ORACLE_ERR;
+    float *rgb = (float *)malloc((size_t)W * (size_t)H * 3 * sizeof(float));
+    if (!rgb)
+        return ORACLE_ERR;
+    for (int64_t y = 0; y < H; ++y)
+        for (int64_t x = 0; x < 3 * (int64_t)W; ++x)
+            rgb[y * 3 * W + x] = (float)img[y * (int64_t)pitch + x];
+    resample_crop_normalize(rgb, W, H, S, Ch, Cw, mean, stdv, out_dtype, out);
+    free(rgb);
+    return ORACLE_OK;
+}
+
+/* One planar I420 frame -> 3 x Ch x Cw. */
+int smol_ref_yuv420_preprocess_image(const uint8_t *yp, const uint8_t *cbp, const uint8_t *crp,
+                                     int32_t W, int32_t H, int32_t S, int32_t Ch, int32_t Cw,
+                                     const float *mean, const float *stdv, int32_t out_dtype,
+                                     void *out)
+{
+    if (!params_ok(W, H, S, Ch, Cw, out_dtype))
+        return ORACLE_ERR;
+    float *rgb = (float *)malloc((size_t)W * (size_t)H * 3 * sizeof(float));
+    if (!rgb)
+        return ORACLE_ERR;
+    oracle_yuv420_to_rgb(yp, cbp, crp, W, H, rgb);
+    resample_crop_normalize(rgb, W, H, S, Ch, Cw, mean, stdv, out_dtype, out);
+    free(rgb);
+    return ORACLE_OK;
+}
+
+static size_t out_image_bytes(int32_t Ch, int32_t Cw, int32_t out_dtype)
+{
+    return (size_t)3 * (size_t)Ch * (size_t)Cw * (out_dtype == ORACLE_OUT_F32 ? 4u : 2u);
+}
+
+/* Batch of packed HWC RGB images; image i starts at src + offsets[i] and has
+ * widths[i] x heights[i] pixels with row pitch pitches[i] bytes (NULL: 3W).
+ * out holds n x 3 x Ch x Cw elements. */
+int smol_ref_preprocess_batch(const uint8_t *src, int64_t src_bytes, const int64_t *offsets,
+                              const int32_t *widths, const int32_t *heights,
+                              const int32_t *pitches, int32_t n, int32_t S, int32_t Ch, int32_t Cw,
+                              const float *mean, const float *stdv, int32_t out_dtype, void *out)
+{
+    size_t ob = out_image_bytes(Ch, Cw, out_dtype);
+    for (int32_t i = 0; i < n; ++i) {
+        int32_t pitch = pitches ? pitches[i] : 3 * widths[i];
+        int64_t end = offsets[i] + (int64_t)(heights[i] - 1) * pitch + 3 * (int64_t)widths[i];
+        if (offsets[i] < 0 || end > src_bytes)
+            return ORACLE_ERR;
+        int rc = smol_ref_preprocess_image(src + offsets[i], widths[i], heights[i], pitch, S, Ch,
+                                           Cw, mean, stdv, out_dtype, (uint8_t *)out + ob * i);
+        if (rc)
+            return rc;
+    }
+    return ORACLE_OK;
+}
+
+/* Batch of planar I420 frames with per-frame plane offsets. */
+int smol_ref_yuv420_preprocess_batch(const uint8_t *src, int64_t src_bytes,
+                                     const int64_t *y_offsets, const int64_t *cb_offsets,
+                                     const int64_t *cr_offsets, const int32_t *widths,
+                                     const int32_t *heights, int32_t n, int32_t S, int32_t Ch,
+                                     int32_t Cw, const float *mean, const float *stdv,
+                                     int32_t out_dtype, void *out)
+{
+    size_t ob = out_image_bytes(Ch, Cw, out_dtype);
+    for (int32_t i = 0; i < n; ++i) {
+        int64_t W = widths[i], H = heights[i];
+        int64_t Wc = (W + 1) / 2, Hc = (H + 1) / 2;
+        if (y_offsets[i] < 0 || y_offsets[i] + W * H > src_bytes || cb_offsets[i] < 0 ||
+            cb_offsets[i] + Wc * Hc > src_bytes || cr_offsets[i] < 0 ||
+            cr_offsets[i] + Wc * Hc > src_bytes)
+            return ORACLE_ERR;
+        int rc = smol_ref_yuv420_preprocess_image(src + y_offsets[i], src + cb_offsets[i],
+                                                  src + cr_offsets[i], widths[i], heights[i], S,
+                                                  Ch, Cw, mean, stdv, out_dtype,
+                                                  (uint8_t *)out + ob * i);
+        if (rc)
+            return rc;
+    }
+    return ORACLE_OK;
+}

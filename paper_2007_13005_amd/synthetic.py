@@ -1,0 +1,221 @@
+"""Seeded synthetic workloads shaped like the paper's inputs.
+
+This module only *generates inputs*: pixel buffers, per-image offset and size
+tables, and the preprocessing parameters of each workload. It contains none of
+the preprocessing arithmetic, so both the HIP path and the CPU oracle can be fed
+from it without sharing any of the method.
+
+The paper's datasets (ImageNet-style full-resolution photos, 161 px thumbnails,
+1080p / 480p traffic-camera video; section 8, "Datasets") are not available, so
+five seeded stand-ins reproduce their shapes, size mix and value ranges:
+
+  c1  32 x 320x240 RGB, uniform 0..255; short side 256, crop 224, fp32 out
+  c2  256 ragged RGB, W and H each uniform in [300, 600], packed back to back
+      with no alignment; short side 256, crop 224, fp16 out
+  c3  1024 x 128x128 RGB smooth gradients + noise +-16 (natively low-res
+      thumbnails); upscale to 224x224, fp16 out
+  c4  64 x 1920x1080 RGB video frames: windows of one random base image at
+      small per-frame shifts; short side 224, crop 224, fp16 out
+  c5  128 x 1280x720 planar YCbCr 4:2:0 frames, Y in 16..235, Cb/Cr in 16..240;
+      short side 256, crop 224, fp16 out
+
+Config k draws from ``numpy.random.default_rng(13005 + k)`` (PCG64).
+The normalisation constants are the ImageNet per-channel statistics the
+standard ResNet pipeline uses (section 2, step 3), scaled to 0..255 units and
+rounded once to fp32.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+
+OUT_F32 = 0
+OUT_F16 = 1
+
+# (0.485, 0.456, 0.406) * 255 and (0.229, 0.224, 0.225) * 255, formed in double
+# and rounded once to fp32.
+IMAGENET_MEAN_255 = (np.array([0.485, 0.456, 0.406], np.float64) * 255.0).astype(np.float32)
+IMAGENET_STD_255 = (np.array([0.229, 0.224, 0.225], np.float64) * 255.0).astype(np.float32)
+
+SEED_BASE = 13005
+
+
+@dataclass
+class Workload:
+    """One batch of inputs plus the preprocessing parameters to apply."""
+
+    name: str
+    kind: str  # "rgb" (packed HWC uint8) or "yuv420" (planar I420 uint8)
+    src: np.ndarray  # flat uint8 buffer holding every image / plane
+    widths: np.ndarray  # int32 [n]
+    heights: np.ndarray  # int32 [n]
+    resize_short: int
+    crop_h: int
+    crop_w: int
+    out_dtype: int
+    offsets: np.ndarray | None = None  # int64 [n], rgb: first byte of image i
+    pitches: np.ndarray | None = None  # int32 [n], rgb: row pitch in bytes (None: 3W)
+    y_offsets: np.ndarray | None = None  # int64 [n], yuv420
+    cb_offsets: np.ndarray | None = None
+    cr_offsets: np.ndarray | None = None
+    mean: np.ndarray = field(default_factory=lambda: IMAGENET_MEAN_255.copy())
+    std: np.ndarray = field(default_factory=lambda: IMAGENET_STD_255.copy())
+    description: str = ""
+
+    @property
+    def n(self) -> int:
+        return int(len(self.widths))
+
+    @property
+    def out_elem_bytes(self) -> int:
+        return 4 if self.out_dtype == OUT_F32 else 2
+
+    def out_shape(self) -> tuple[int, int, int, int]:
+        return (self.n, 3, self.crop_h, self.crop_w)
+
+
+def _pack_rgb(images: list[np.ndarray], align: int = 1):
+    """Pack HxWx3 uint8 images back to back (offset of each rounded up to align)."""
+    offsets, cur = [], 0
+    for im in images:
+        cur = (cur + align - 1) // align * align
+        offsets.append(cur)
+        cur += im.size
+    src = np.zeros(cur, np.uint8)
+    for off, im in zip(offsets, images):
+        src[off:off + im.size] = im.reshape(-1)
+    return src, np.asarray(offsets, np.int64)
+
+
+def rgb_workload(name: str, images: list[np.ndarray], S: int, C: int | tuple[int, int],
+                 out_dtype: int, align: int = 1, description: str = "") -> Workload:
+    """Wrap a list of HxWx3 uint8 images as a packed ragged batch."""
+    ch, cw = (C, C) if isinstance(C, int) else C
+    src, offsets = _pack_rgb(images, align)
+    return Workload(name=name, kind="rgb", src=src,
+                    widths=np.asarray([im.shape[1] for im in images], np.int32),
+                    heights=np.asarray([im.shape[0] for im in images], np.int32),
+                    resize_short=S, crop_h=ch, crop_w=cw, out_dtype=out_dtype,
+                    offsets=offsets, description=description)
+
+
+def uniform_rgb_workload(name: str, batch: np.ndarray, S: int, C: int | tuple[int, int],
+                         out_dtype: int, description: str = "") -> Workload:
+    """A dense N x H x W x 3 uint8 batch (image i at offset i*H*W*3)."""
+    n, h, w, _ = batch.shape
+    ch, cw = (C, C) if isinstance(C, int) else C
+    stride = h * w * 3
+    return Workload(name=name, kind="rgb", src=np.ascontiguousarray(batch).reshape(-1),
+                    widths=np.full(n, w, np.int32), heights=np.full(n, h, np.int32),
+                    resize_short=S, crop_h=ch, crop_w=cw, out_dtype=out_dtype,
+                    offsets=np.arange(n, dtype=np.int64) * stride, description=description)
+
+
+def yuv420_workload(name: str, planes: list[tuple[np.ndarray, np.ndarray, np.ndarray]], S: int,
+                    C: int | tuple[int, int], out_dtype: int, description: str = "") -> Workload:
+    """Pack (Y, Cb, Cr) planes per frame as [Y | Cb | Cr], frames back to back."""
+    ch, cw = (C, C) if isinstance(C, int) else C
+    yo, bo, ro, cur = [], [], [], 0
+    for y, cb, cr in planes:
+        yo.append(cur)
+        cur += y.size
+        bo.append(cur)
+        cur += cb.size
+        ro.append(cur)
+        cur += cr.size
+    src = np.empty(cur, np.uint8)
+    for (y, cb, cr), a, b, c in zip(planes, yo, bo, ro):
+        src[a:a + y.size] = y.reshape(-1)
+        src[b:b + cb.size] = cb.reshape(-1)
+        src[c:c + cr.size] = cr.reshape(-1)
+    return Workload(name=name, kind="yuv420", src=src,
+                    widths=np.asarray([p[0].shape[1] for p in planes], np.int32),
+                    heights=np.asarray([p[0].shape[0] for p in planes], np.int32),
+                    resize_short=S, crop_h=ch, crop_w=cw, out_dtype=out_dtype,
+                    y_offsets=np.asarray(yo, np.int64), cb_offsets=np.asarray(bo, np.int64),
+                    cr_offsets=np.asarray(ro, np.int64), description=description)
+
+
+# ---------------------------------------------------------------------------
+# the five workloads
+# ---------------------------------------------------------------------------
+
+
+def c1(n: int = 32) -> Workload:
+    rng = np.random.default_rng(SEED_BASE + 1)
+    batch = rng.integers(0, 256, size=(n, 240, 320, 3), dtype=np.uint8)
+    return uniform_rgb_workload("c1", batch, 256, 224, OUT_F32,
+                                f"{n} x 320x240 RGB uint8 HWC, uniform 0-255; short side 256, "
+                                "center crop 224x224, NCHW fp32")
+
+
+def c2_sizes(n: int = 256) -> np.ndarray:
+    """(n, 2) int array of (W, H), each uniform in [300, 600]."""
+    rng = np.random.default_rng(SEED_BASE + 2)
+    return rng.integers(300, 601, size=(n, 2))
+
+
+def c2(n: int = 256, align: int = 1) -> Workload:
+    rng = np.random.default_rng(SEED_BASE + 2)
+    sizes = rng.integers(300, 601, size=(n, 2))
+    total = int(sum(int(w) * int(h) * 3 for w, h in sizes))
+    pix = rng.integers(0, 256, size=total, dtype=np.uint8)
+    images, cur = [], 0
+    for w, h in sizes:
+        k = int(w) * int(h) * 3
+        images.append(pix[cur:cur + k].reshape(int(h), int(w), 3))
+        cur += k
+    return rgb_workload("c2", images, 256, 224, OUT_F16, align,
+                        f"ragged {n} RGB uint8 HWC, W,H ~ U[300,600], packed with "
+                        f"{'no' if align == 1 else str(align) + ' B'} alignment; short side "
+                        "256, center crop 224x224, NCHW fp16")
+
+
+def c3(n: int = 1024) -> Workload:
+    rng = np.random.default_rng(SEED_BASE + 3)
+    size = 128
+    yy, xx = np.mgrid[0:size, 0:size].astype(np.float64)
+    alpha = rng.uniform(0.0, 255.0, size=(n, 1, 1, 3))
+    beta = rng.uniform(-1.0, 1.0, size=(n, 1, 1, 3))
+    gamma = rng.uniform(-1.0, 1.0, size=(n, 1, 1, 3))
+    noise = rng.integers(-16, 17, size=(n, size, size, 3))
+    img = alpha + beta * xx[None, :, :, None] + gamma * yy[None, :, :, None] + noise
+    batch = np.clip(np.rint(img), 0, 255).astype(np.uint8)
+    return uniform_rgb_workload("c3", batch, 224, 224, OUT_F16,
+                                f"{n} x 128x128 RGB uint8 HWC, smooth gradients + noise +-16; "
+                                "bilinear upscale to 224x224, NCHW fp16")
+
+
+def c4(n: int = 64, height: int = 1080, width: int = 1920) -> Workload:
+    rng = np.random.default_rng(SEED_BASE + 4)
+    margin = 8
+    base = rng.integers(0, 256, size=(height + 2 * margin, width + 2 * margin, 3), dtype=np.uint8)
+    shifts = rng.integers(-margin, margin + 1, size=(n, 2))
+    batch = np.empty((n, height, width, 3), np.uint8)
+    for f, (dy, dx) in enumerate(shifts):
+        y0, x0 = margin + int(dy), margin + int(dx)
+        batch[f] = base[y0:y0 + height, x0:x0 + width]
+    return uniform_rgb_workload("c4", batch, 224, 224, OUT_F16,
+                                f"{n} x {width}x{height} RGB uint8 HWC video frames (one seeded "
+                                "base image, per-frame shifts of up to 8 px); short side 224, "
+                                "center crop 224x224, NCHW fp16")
+
+
+def c5(n: int = 128, height: int = 720, width: int = 1280) -> Workload:
+    rng = np.random.default_rng(SEED_BASE + 5)
+    hc, wc = (height + 1) // 2, (width + 1) // 2
+    ys = rng.integers(16, 236, size=(n, height, width), dtype=np.uint8)
+    cbs = rng.integers(16, 241, size=(n, hc, wc), dtype=np.uint8)
+    crs = rng.integers(16, 241, size=(n, hc, wc), dtype=np.uint8)
+    return yuv420_workload("c5", [(ys[i], cbs[i], crs[i]) for i in range(n)], 256, 224, OUT_F16,
+                           f"{n} x {width}x{height} planar YCbCr 4:2:0 uint8 (Y 16-235, Cb/Cr "
+                           "16-240); BT.601 full range, short side 256, center crop 224x224, "
+                           "NCHW fp16")
+
+
+CONFIGS = {"c1": c1, "c2": c2, "c3": c3, "c4": c4, "c5": c5}
+
+
+def make(name: str, **kw) -> Workload:
+    return CONFIGS[name](**kw)
