@@ -1,0 +1,260 @@
+"""Benchmark: fused image preprocessing on one MI355X.
+
+One step = one call of the fused hot path (geometry and taps, source-row
+gather, [BT.601 conversion for I420], bilinear, normalise, NCHW store) over
+one batch of seeded synthetic input already resident in HBM. The default
+workload is the 1080p video-frame batch (64 x 1920x1080 RGB -> 224x224 fp16),
+the configuration the bandwidth target is stated on.
+
+Input/output sets are rotated so that the touched working set exceeds twice
+the 256 MB Infinity Cache: the number reported is an HBM number, not a
+cache-warm one.
+
+Prints one JSON line. ``--config c1..c5`` selects another workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "images/sec preprocessed + achieved HBM GB/s (% of MI355X peak), 1 GPU"
+HBM_PEAK_GBPS = 8000.0  # MI355X published HBM3E bandwidth
+MALL_BYTES = 256 * 1024 * 1024
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=400)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", default="c4", choices=["c1", "c2", "c3", "c4", "c5"])
+    ap.add_argument("--rotate", type=int, default=0,
+                    help="input/output sets cycled through (0: enough to defeat the MALL)")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="wall-clock budget of the CPU oracle baseline (0 disables it)")
+    ap.add_argument("--cpu-threads", type=int, default=0)
+    ap.add_argument("--band-rows", type=int, default=0, help="tuning override (0: automatic)")
+    ap.add_argument("--path", type=int, default=0, help="tuning override (0: automatic)")
+    ap.add_argument("--profile-run", action="store_true",
+                    help="no CPU baseline, fewer prints: for runs under rocprofv3")
+    ap.add_argument("--copy-probe", type=int, default=0,
+                    help="instead of the benchmark, copy this many MiB with torch several "
+                         "times (calibrates the FETCH_SIZE / WRITE_SIZE counters)")
+    return ap.parse_args()
+
+
+def algorithmic_bytes(wl, smol) -> int:
+    """Bytes the method must move per batch: for every image the source rows
+    its vertical taps read times the crop's source column span (per plane for
+    I420), plus the output."""
+    p = smol.make_params(wl.resize_short, wl.crop_h, wl.crop_w, wl.mean, wl.std, wl.out_dtype)
+    total = 0
+    cache = {}
+    for w, h in zip(wl.widths.tolist(), wl.heights.tolist()):
+        key = (w, h)
+        if key not in cache:
+            g = smol.image_geometry(w, h, p, yuv420=(wl.kind == "yuv420"))
+            span = g["src_x_last"] - g["src_x_first"] + 1
+            if wl.kind == "rgb":
+                rd = g["src_rows"] * span * 3
+            else:
+                cspan = g["chroma_x_last"] - g["chroma_x_first"] + 1
+                rd = g["src_rows"] * span + 2 * g["chroma_rows"] * cspan
+            cache[key] = rd
+        total += cache[key]
+    return total + wl.n * 3 * wl.crop_h * wl.crop_w * wl.out_elem_bytes
+
+
+def touched_bytes(wl, smol) -> int:
+    return algorithmic_bytes(wl, smol)
+
+
+def cpu_baseline(wl, seconds: float, threads: int) -> dict:
+    """The oracle, as it stands, on the host cores: images processed one per
+    task by a thread pool (ctypes releases the GIL), for about `seconds`."""
+    import concurrent.futures as cf
+
+    import numpy as np
+
+    import oracle
+
+    mean = np.ascontiguousarray(wl.mean, np.float32)
+    std = np.ascontiguousarray(wl.std, np.float32)
+    esz = wl.out_elem_bytes
+    outs = [np.empty(3 * wl.crop_h * wl.crop_w * esz, np.uint8) for _ in range(threads)]
+    base = wl.src.ctypes.data
+
+    def one(i: int, t: int) -> None:
+        o = outs[t].ctypes.data
+        if wl.kind == "rgb":
+            pitch = 3 * int(wl.widths[i]) if wl.pitches is None else int(wl.pitches[i])
+            rc = oracle.preprocess_image_into(base + int(wl.offsets[i]), int(wl.widths[i]),
+                                              int(wl.heights[i]), pitch, wl.resize_short,
+                                              wl.crop_h, wl.crop_w, mean, std, wl.out_dtype, o)
+        else:
+            rc = oracle.yuv420_preprocess_image_into(
+                base + int(wl.y_offsets[i]), base + int(wl.cb_offsets[i]),
+                base + int(wl.cr_offsets[i]), int(wl.widths[i]), int(wl.heights[i]),
+                wl.resize_short, wl.crop_h, wl.crop_w, mean, std, wl.out_dtype, o)
+        if rc != 0:
+            raise RuntimeError("oracle failed")
+
+    def worker(t: int, deadline: float, counter: list) -> None:
+        i = t
+        while time.perf_counter() < deadline:
+            one(i % wl.n, t)
+            counter[t] += 1
+            i += threads
+
+    oracle.lib()
+    counter = [0] * threads
+    t0 = time.perf_counter()
+    deadline = t0 + seconds
+    with cf.ThreadPoolExecutor(threads) as ex:
+        list(ex.map(lambda t: worker(t, deadline, counter), range(threads)))
+    elapsed = time.perf_counter() - t0
+    done = sum(counter)
+    return {"value": done / elapsed, "unit": "images/s", "cores": threads, "kind": "oracle",
+            "sample": f"{done} images of workload {wl.name} (cycling through its {wl.n} images) "
+                      f"in {elapsed:.1f} s on {threads} threads, one image per task"}
+
+
+def load_traffic(config: str) -> dict | None:
+    """HBM traffic per launch from the committed rocprofv3 counter summary,
+    valid only while the kernel sources match the ones it was taken on."""
+    import hashlib
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f).get(config)
+    except (OSError, ValueError):
+        return None
+    if not rec:
+        return None
+    h = hashlib.sha256()
+    for rel in rec.get("sources", []):
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    if h.hexdigest() != rec.get("sources_sha256"):
+        return None
+    return rec
+
+
+def copy_probe(mib: int) -> None:
+    import torch
+    n = mib * 1024 * 1024
+    a = torch.empty(n, dtype=torch.uint8, device="cuda:0")
+    b = torch.empty_like(a)
+    a.fill_(1)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": n, "copies": 5}), flush=True)
+
+
+def main() -> int:
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the fused "
+              "preprocessing path shards by image with no communication, and only the "
+              "single-GPU share is measured here.", file=sys.stderr, flush=True)
+        return 2
+    if args.copy_probe:
+        copy_probe(args.copy_probe)
+        return 0
+
+    import numpy as np
+    import torch
+
+    from paper_2007_13005_amd import smol, synthetic
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a HIP device", file=sys.stderr)
+        return 1
+    dev = torch.device("cuda:0")
+    wl = synthetic.make(args.config)
+    algo = algorithmic_bytes(wl, smol)
+    out_bytes = wl.n * 3 * wl.crop_h * wl.crop_w * wl.out_elem_bytes
+    rotate = args.rotate or max(2, -(-2 * MALL_BYTES // algo))
+    if args.band_rows or args.path:
+        smol.set_tuning(path=args.path, band_rows=args.band_rows)
+
+    src0 = torch.from_numpy(wl.src).to(dev)
+    srcs = [src0] + [src0.clone() for _ in range(rotate - 1)]
+    odt = torch.float16 if wl.out_dtype == synthetic.OUT_F16 else torch.float32
+    outs = [torch.empty((wl.n, 3, wl.crop_h, wl.crop_w), dtype=odt, device=dev)
+            for _ in range(rotate)]
+    call = smol.PreparedCall(wl)
+    stream = torch.cuda.current_stream()
+    sh = stream.cuda_stream
+    ptrs = [(s.data_ptr(), s.numel(), o.data_ptr()) for s, o in zip(srcs, outs)]
+
+    for i in range(args.warmup):
+        sp, sb, op = ptrs[i % rotate]
+        call(sp, sb, op, sh)
+    torch.cuda.synchronize()
+    plan = smol.last_plan()
+
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for i in range(args.steps):
+        sp, sb, op = ptrs[i % rotate]
+        call(sp, sb, op, sh)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gpu_ms = ev0.elapsed_time(ev1)
+    launches = args.steps * max(1, plan["launches"])
+    avg_launch_s = gpu_ms / 1e3 / launches
+    per_launch_bytes = algo / max(1, plan["launches"])
+    achieved = per_launch_bytes / avg_launch_s / 1e9
+
+    # sanity: the last output is finite
+    assert bool(torch.isfinite(outs[(args.steps - 1) % rotate]).all().item())
+
+    traffic = load_traffic(args.config)
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                "traffic": None if traffic is None else traffic["bytes_per_launch"]}
+    res = {
+        "metric": METRIC,
+        "value": round(wl.n * args.steps / wall, 1),
+        "unit": "images/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall * 1e3 / args.steps, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{wl.name}: {wl.description}", "batch": wl.n,
+                   "algorithmic_bytes_per_step": algo, "output_bytes_per_step": out_bytes,
+                   "rotation_sets": rotate, "kernel_path": plan["path"],
+                   "band_rows": plan["band_rows"], "lds_bytes": plan["lds_bytes"],
+                   "gpu_ms_per_step": round(gpu_ms / args.steps, 5),
+                   "hbm_gbps_wall": round(algo * args.steps / wall / 1e9, 1)},
+        "roofline": roofline,
+    }
+    if not args.profile_run and args.cpu_seconds > 0:
+        threads = args.cpu_threads or min(16, len(os.sched_getaffinity(0)))
+        res["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds, threads)
+    del np
+    print(json.dumps(res), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,218 @@
+/*
+ * smol.h -- C ABI of the MI355X (gfx950) fused image-preprocessing library.
+ *
+ * The library performs, in one pass of hand-written HIP kernels, the
+ * preprocessing that the Smol paper (Kang et al., PVLDB 14) identifies as the
+ * bottleneck of end-to-end DNN inference on images and video frames: the
+ * standard ResNet pipeline of section 2 ("Breakdown of end-to-end DNN
+ * inference"), steps 2-4, on already-decoded pixels --
+ *
+ *   step 2  aspect-preserving resize so the short edge becomes S, then a
+ *           central crop of C_h x C_w;
+ *   step 3  conversion to float and per-channel normalisation;
+ *   step 4  rearrangement to channels-first;
+ *
+ * fused into a single kernel as section 6.2 allows (normalisation, type
+ * conversion and channel reordering fuse; resize and crop may be swapped, so
+ * the resize is evaluated only at the cropped output pixels). For planar
+ * YCbCr 4:2:0 frames (the decoder output of JPEG and H.264 inputs, App. A
+ * "Components": colorspace conversion) the chroma upsample and BT.601
+ * conversion run in the same kernel, at every luma pixel the resize reads.
+ *
+ * Exact semantics (shared by nothing in this library but written down here):
+ *   - resized size: the short side becomes S, the long side is
+ *     floor(S * long / short); a square image becomes S x S;
+ *   - crop offsets: left = floor((W' - C_w) / 2), top = floor((H' - C_h) / 2)
+ *     (Algorithm 1's l and t);
+ *   - bilinear, half-pixel centres (align_corners = false), edge clamp, no
+ *     antialiasing: output index x maps to the source coordinate
+ *     ((2x + 1) * in - out) / (2 * out); its integer part is exact, its
+ *     fractional weight is rounded once to fp32;
+ *   - arithmetic in fp32; output (v - mean_c) / std_c, NCHW, RGB order;
+ *   - fp16 output is rounded to nearest even;
+ *   - YCbCr: BT.601 full range (Kr = 0.299, Kb = 0.114), centred 4:2:0 siting
+ *     (the chroma coordinate of luma index x is x/2 - 1/4, clamped), each
+ *     channel clamped to [0, 255] in fp32 before the resize.
+ *
+ * Threading and streams: every call enqueues work on the caller's HIP stream
+ * and returns without synchronising. Calls are thread-safe; calls from
+ * different threads on different streams may overlap. Validation is complete
+ * before anything is enqueued: a call that returns an error has enqueued
+ * nothing. Device faults (only possible if the caller's buffers are smaller
+ * than declared) surface at the caller's next synchronisation.
+ */
+#ifndef SMOL_H
+#define SMOL_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+#define SMOL_OK 0
+#define SMOL_ERR_INVALID_ARG (-1) /* a null pointer, a size out of range, a   */
+                                  /* buffer too small for its table entries  */
+#define SMOL_ERR_UNSUPPORTED (-2) /* valid in principle, beyond this build's  */
+                                  /* limits (see the per-call notes)          */
+#define SMOL_ERR_HIP (-3)         /* the HIP runtime reported an error        */
+
+/* Output element types. */
+#define SMOL_OUT_F32 0
+#define SMOL_OUT_F16 1
+
+/* Limits. */
+#define SMOL_MAX_DIM 65535          /* max source width / height, luma pixels */
+#define SMOL_MAX_RESIZED 4194303    /* max resized width / height (< 2^22)    */
+#define SMOL_MAX_BATCH 1048576      /* max images per call                    */
+
+/* Preprocessing parameters, read during the call only.
+ *   resize_short  S, the short side after the aspect-preserving resize (>= 1)
+ *   crop_h/crop_w output height / width; the crop must fit inside the resized
+ *                 image of every image in the batch
+ *   out_dtype     SMOL_OUT_F32 or SMOL_OUT_F16
+ *   mean, std     per channel R, G, B in 0..255 pixel units; finite, std != 0
+ *                 (the ImageNet statistics are (0.485, 0.456, 0.406) * 255 and
+ *                 (0.229, 0.224, 0.225) * 255) */
+typedef struct smol_params {
+    int32_t resize_short;
+    int32_t crop_h;
+    int32_t crop_w;
+    int32_t out_dtype;
+    float mean[3];
+    float std[3];
+} smol_params;
+
+/* Per-image geometry as the kernels use it (host-side query).
+ *   resized_w/h     W', H'
+ *   crop_left/top   Algorithm 1's l, t
+ *   src_x_first/last  first and last source column any output pixel reads
+ *                     (inclusive; luma columns for YUV input)
+ *   src_rows        number of distinct source rows the vertical taps read
+ *                   (luma rows for YUV input)
+ *   chroma_x_first/last, chroma_rows  the same for each chroma plane of a
+ *                   YUV 4:2:0 frame (0 for RGB queries) */
+typedef struct smol_geometry {
+    int32_t resized_w;
+    int32_t resized_h;
+    int32_t crop_left;
+    int32_t crop_top;
+    int32_t src_x_first;
+    int32_t src_x_last;
+    int32_t src_rows;
+    int32_t chroma_x_first;
+    int32_t chroma_x_last;
+    int32_t chroma_rows;
+} smol_geometry;
+
+/* smol_preprocess_batch -- packed HWC RGB uint8 images -> NCHW.
+ *
+ * Section 2, steps 2-4, fused per section 6.2.
+ *
+ *   src        DEVICE pointer, caller-owned: every image's bytes. No alignment
+ *              requirement.
+ *   src_bytes  size of the src buffer in bytes; every image must lie inside.
+ *   offsets    HOST [n]: byte offset in src of image i's first pixel (>= 0).
+ *   widths, heights  HOST [n]: image i is widths[i] x heights[i] pixels,
+ *              1 .. SMOL_MAX_DIM each.
+ *   row_pitch  HOST [n]: bytes between rows of image i (>= 3 * widths[i]),
+ *              or NULL for tightly packed rows (3 * widths[i]).
+ *   n          number of images, 0 .. SMOL_MAX_BATCH (0 enqueues nothing).
+ *   p          parameters (HOST).
+ *   out        DEVICE pointer, caller-owned, 16-byte aligned:
+ *              n x 3 x crop_h x crop_w elements of p->out_dtype, dense.
+ *   stream     hipStream_t of the current device, or NULL for the default
+ *              stream.
+ *
+ * Host tables and p are read before the call returns. When the images do not
+ * share one size and a constant offset stride, the call uploads a per-image
+ * descriptor table (64 bytes per image) through a pinned staging buffer that
+ * the library keeps per device and reuses in stream order.
+ *
+ * Returns SMOL_OK, SMOL_ERR_INVALID_ARG (nothing enqueued),
+ * SMOL_ERR_UNSUPPORTED (resized side beyond SMOL_MAX_RESIZED) or SMOL_ERR_HIP.
+ */
+int smol_preprocess_batch(const uint8_t *src, int64_t src_bytes, const int64_t *offsets,
+                          const int32_t *widths, const int32_t *heights,
+                          const int32_t *row_pitch, int32_t n, const smol_params *p, void *out,
+                          void *stream);
+
+/* smol_yuv420_preprocess_batch -- planar YCbCr 4:2:0 (I420) uint8 frames ->
+ * NCHW RGB.
+ *
+ * App. A "Components" (colorspace conversion) followed by section 2,
+ * steps 2-4, all in one kernel.
+ *
+ *   src         DEVICE pointer, caller-owned, no alignment requirement.
+ *   src_bytes   size of src in bytes; every plane must lie inside.
+ *   y_offsets, cb_offsets, cr_offsets  HOST [n]: byte offsets in src of frame
+ *               i's Y plane (widths[i] x heights[i]) and Cb and Cr planes
+ *               (ceil(W/2) x ceil(H/2) each); all planes tightly pitched.
+ *   widths, heights  HOST [n]: luma size, 1 .. SMOL_MAX_DIM.
+ *   n, p, out, stream  as for smol_preprocess_batch.
+ *
+ * Returns as smol_preprocess_batch.
+ */
+int smol_yuv420_preprocess_batch(const uint8_t *src, int64_t src_bytes, const int64_t *y_offsets,
+                                 const int64_t *cb_offsets, const int64_t *cr_offsets,
+                                 const int32_t *widths, const int32_t *heights, int32_t n,
+                                 const smol_params *p, void *out, void *stream);
+
+/* smol_image_geometry -- the geometry the kernels use for one image of
+ * width x height (luma size for yuv420 != 0) under p. Host only; touches no
+ * device. Returns SMOL_OK or SMOL_ERR_INVALID_ARG / SMOL_ERR_UNSUPPORTED. */
+int smol_image_geometry(int32_t width, int32_t height, int32_t yuv420, const smol_params *p,
+                        smol_geometry *g);
+
+/* Tuning and testing knobs, process-wide, applied to later calls. Zero in any
+ * field means "automatic".
+ *   path        1: always the direct-gather kernels (taps read from global
+ *               memory); 2: always the LDS-staged kernels (a call whose
+ *               source span cannot be staged then fails with
+ *               SMOL_ERR_UNSUPPORTED); 0: LDS-staged whenever it fits
+ *   band_rows   output rows per workgroup in the LDS-staged kernels (1..64)
+ *   lds_budget  bytes of LDS one workgroup may use (4096..65536) */
+typedef struct smol_tuning {
+    int32_t path;
+    int32_t band_rows;
+    int32_t lds_budget;
+    int32_t reserved;
+} smol_tuning;
+
+/* Set the knobs (NULL resets to automatic). SMOL_ERR_INVALID_ARG if a field
+ * is out of range. */
+int smol_set_tuning(const smol_tuning *t);
+
+/* How the calling thread's last successful batch call ran.
+ *   path        1 direct-gather, 2 LDS-staged
+ *   band_rows   output rows per workgroup (LDS-staged) or 0
+ *   lds_bytes   dynamic LDS per workgroup
+ *   launches    kernel launches the call made
+ *   uploaded_descriptors  1 if a per-image descriptor table was uploaded
+ *               (ragged batch), 0 if the batch was uniform */
+typedef struct smol_plan {
+    int32_t path;
+    int32_t band_rows;
+    int32_t lds_bytes;
+    int32_t launches;
+    int32_t uploaded_descriptors;
+    int32_t reserved[3];
+} smol_plan;
+
+int smol_last_plan(smol_plan *plan);
+
+/* Static description of a status code. */
+const char *smol_status_string(int status);
+
+/* Detail of the last error returned on the calling thread ("" if none). */
+const char *smol_last_error(void);
+
+/* Library ABI version (major * 10000 + minor * 100 + patch). */
+int smol_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SMOL_H */

@@ -1,0 +1,672 @@
+// smol_host.cpp -- C ABI of libsmol: validation, per-image geometry,
+// descriptor staging and kernel dispatch. Everything per element runs in the
+// kernels (smol_kernels.hip); this file handles per-image scalars only.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <atomic>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "smol.h"
+#include "smol_internal.h"
+
+namespace {
+
+using smol::BatchArgs;
+using smol::Desc;
+
+thread_local std::string g_last_error;
+thread_local smol_plan g_last_plan = {};
+
+int fail(int code, const char *fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return code;
+}
+
+std::atomic<int> g_path{0}, g_band_rows{0}, g_lds_budget{0};
+
+constexpr int kDefaultLdsBudget = 64 * 1024;
+constexpr int kMaxBandRows = 64;
+constexpr int kThreads = 256;
+// Keep every launch below 2^31 work-items.
+constexpr long long kMaxWorkgroupsPerLaunch = (1LL << 31) / kThreads;
+
+// ---------------------------------------------------------------------------
+// Geometry (section 2 step 2; Algorithm 1 for the crop offsets)
+// ---------------------------------------------------------------------------
+
+struct Geo {
+    int64_t Wr, Hr, left, top;
+};
+
+// Short side -> S, long side floor(S * long / short).
+void resized(int64_t W, int64_t H, int64_t S, int64_t *Wr, int64_t *Hr)
+{
+    if (W <= H) {
+        *Wr = S;
+        *Hr = S * H / W;
+    } else {
+        *Hr = S;
+        *Wr = S * W / H;
+    }
+}
+
+// Host copy of the half-pixel tap (integer part only) for footprint queries
+// and LDS planning: floor of ((2x+1)*in - out) / (2*out), clamped.
+void tap_index(int64_t x, int64_t in, int64_t out, int64_t *x0, int64_t *x1)
+{
+    const int64_t num = (2 * x + 1) * in - out;
+    if (num <= 0) {
+        *x0 = *x1 = 0;
+        return;
+    }
+    const int64_t q = num / (2 * out);
+    if (q >= in - 1) {
+        *x0 = *x1 = in - 1;
+        return;
+    }
+    *x0 = q;
+    *x1 = q + 1;
+}
+
+// Chroma tap index for luma index x: floor((2x - 1) / 4), clamped to [0, n-1].
+void chroma_index(int64_t x, int64_t n, int64_t *c0, int64_t *c1)
+{
+    const int64_t num = 2 * x - 1;
+    if (num <= 0) {
+        *c0 = *c1 = 0;
+        return;
+    }
+    const int64_t q = num >> 2;
+    if (q >= n - 1) {
+        *c0 = *c1 = n - 1;
+        return;
+    }
+    *c0 = q;
+    *c1 = q + 1;
+}
+
+int check_params(const smol_params *p)
+{
+    if (!p)
+        return fail(SMOL_ERR_INVALID_ARG, "params is NULL");
+    if (p->resize_short < 1 || p->resize_short > SMOL_MAX_RESIZED)
+        return fail(SMOL_ERR_INVALID_ARG, "resize_short %d out of range", p->resize_short);
+    if (p->crop_h < 1 || p->crop_w < 1)
+        return fail(SMOL_ERR_INVALID_ARG, "crop %dx%d must be positive", p->crop_h, p->crop_w);
+    if (p->out_dtype != SMOL_OUT_F32 && p->out_dtype != SMOL_OUT_F16)
+        return fail(SMOL_ERR_INVALID_ARG, "out_dtype %d unknown", p->out_dtype);
+    for (int c = 0; c < 3; ++c) {
+        if (!std::isfinite(p->mean[c]) || !std::isfinite(p->std[c]) || p->std[c] == 0.0f)
+            return fail(SMOL_ERR_INVALID_ARG, "mean/std of channel %d not finite or std == 0", c);
+        const double s = 1.0 / (double)p->std[c];
+        if (!std::isfinite((float)s) || !std::isfinite((float)(-(double)p->mean[c] * s)))
+            return fail(SMOL_ERR_INVALID_ARG, "1/std or mean/std of channel %d overflows", c);
+    }
+    return SMOL_OK;
+}
+
+int image_geo(int64_t W, int64_t H, const smol_params *p, Geo *g, int64_t i)
+{
+    if (W < 1 || H < 1 || W > SMOL_MAX_DIM || H > SMOL_MAX_DIM)
+        return fail(SMOL_ERR_INVALID_ARG, "image %lld: size %lldx%lld outside 1..%d",
+                    (long long)i, (long long)W, (long long)H, SMOL_MAX_DIM);
+    resized(W, H, p->resize_short, &g->Wr, &g->Hr);
+    if (g->Wr > SMOL_MAX_RESIZED || g->Hr > SMOL_MAX_RESIZED)
+        return fail(SMOL_ERR_UNSUPPORTED, "image %lld: resized size %lldx%lld beyond %d",
+                    (long long)i, (long long)g->Wr, (long long)g->Hr, SMOL_MAX_RESIZED);
+    if (p->crop_w > g->Wr || p->crop_h > g->Hr)
+        return fail(SMOL_ERR_INVALID_ARG, "image %lld: crop %dx%d larger than resized %lldx%lld",
+                    (long long)i, p->crop_w, p->crop_h, (long long)g->Wr, (long long)g->Hr);
+    g->left = (g->Wr - p->crop_w) / 2;
+    g->top = (g->Hr - p->crop_h) / 2;
+    return SMOL_OK;
+}
+
+// Source columns [x_first, x_last] read by the crop's columns.
+void x_span(const Desc &d, int Cw, int64_t *first, int64_t *last)
+{
+    int64_t a, b;
+    tap_index(d.left, d.W, d.Wr, first, &a);
+    tap_index(d.left + Cw - 1, d.W, d.Wr, &b, last);
+}
+
+int64_t distinct_rows(int64_t top, int64_t Ch, int64_t H, int64_t Hr)
+{
+    int64_t count = 0, last = -1;
+    for (int64_t r = 0; r < Ch; ++r) {
+        int64_t y0, y1;
+        tap_index(top + r, H, Hr, &y0, &y1);
+        if (y0 > last) {
+            ++count;
+            last = y0;
+        }
+        if (y1 > last) {
+            ++count;
+            last = y1;
+        }
+    }
+    return count;
+}
+
+// ---------------------------------------------------------------------------
+// Per-device descriptor staging: pinned host ring + device ring, slots reused
+// once the event recorded after the kernel that read them has completed.
+// ---------------------------------------------------------------------------
+
+struct Staging {
+    static constexpr int kSlots = 16;
+    std::mutex mu;
+    size_t slot_cap = 0;
+    uint8_t *host = nullptr;
+    uint8_t *dev = nullptr;
+    hipEvent_t ev[kSlots] = {};
+    bool pending[kSlots] = {};
+    int next = 0;
+};
+
+std::mutex g_staging_mu;
+std::vector<Staging *> g_staging;  // by device ordinal; never freed
+
+Staging *staging_for(int device)
+{
+    std::lock_guard<std::mutex> lk(g_staging_mu);
+    if ((int)g_staging.size() <= device)
+        g_staging.resize(device + 1, nullptr);
+    if (!g_staging[device])
+        g_staging[device] = new Staging();
+    return g_staging[device];
+}
+
+// Grow the ring so each slot holds `bytes`. Caller holds st->mu.
+hipError_t staging_reserve(Staging *st, size_t bytes)
+{
+    if (bytes <= st->slot_cap)
+        return hipSuccess;
+    for (int i = 0; i < Staging::kSlots; ++i)
+        if (st->pending[i]) {
+            hipError_t e = hipEventSynchronize(st->ev[i]);
+            if (e != hipSuccess)
+                return e;
+            st->pending[i] = false;
+        }
+    if (st->host)
+        (void)hipHostFree(st->host);
+    if (st->dev)
+        (void)hipFree(st->dev);
+    st->host = nullptr;
+    st->dev = nullptr;
+    st->slot_cap = 0;
+    size_t cap = 64 * 1024;
+    while (cap < bytes)
+        cap *= 2;
+    hipError_t e = hipHostMalloc((void **)&st->host, cap * Staging::kSlots, hipHostMallocDefault);
+    if (e != hipSuccess)
+        return e;
+    e = hipMalloc((void **)&st->dev, cap * Staging::kSlots);
+    if (e != hipSuccess)
+        return e;
+    for (int i = 0; i < Staging::kSlots; ++i)
+        if (!st->ev[i]) {
+            e = hipEventCreateWithFlags(&st->ev[i], hipEventDisableTiming);
+            if (e != hipSuccess)
+                return e;
+        }
+    st->slot_cap = cap;
+    return hipSuccess;
+}
+
+// ---------------------------------------------------------------------------
+// Planning and launch
+// ---------------------------------------------------------------------------
+
+struct Plan {
+    int path;  // smol::PATH_DIRECT or smol::PATH_LDS
+    int R;
+    size_t lds_bytes;
+};
+
+size_t align16(size_t v) { return (v + 15) & ~(size_t)15; }
+
+// LDS layout of the RGB kernel: colx/colw [Cw], ty0/ty1/twy [R], smap/rowa
+// [2R], then 2R row slots of slot_bytes.
+size_t rgb_lds_bytes(int Cw, int R, int slot_bytes, int *slots_off)
+{
+    const size_t head = align16((size_t)8 * Cw + (size_t)28 * R);
+    *slots_off = (int)head;
+    return head + (size_t)2 * R * slot_bytes;
+}
+
+int slot_bytes_for(int64_t span_bytes)
+{
+    // aligned-down start adds up to 15 bytes; 16 more cover the dword reads
+    // past the last pixel pair.
+    return (int)(16 * ((span_bytes + 15 + 15) / 16) + 16);
+}
+
+Plan plan_rgb(int64_t max_span_bytes, int Ch, int Cw, int *slot_bytes, int *slots_off)
+{
+    Plan pl{smol::PATH_DIRECT, 0, 0};
+    const int forced = g_path.load();
+    if (forced == smol::PATH_DIRECT)
+        return pl;
+    const int budget = g_lds_budget.load() > 0 ? g_lds_budget.load() : kDefaultLdsBudget;
+    if (max_span_bytes > (1 << 20))
+        return pl;
+    const int sb = slot_bytes_for(max_span_bytes);
+    int R = g_band_rows.load();
+    if (R <= 0) {
+        R = 16;
+        int off;
+        while (R > 1 && rgb_lds_bytes(Cw, R, sb, &off) > (size_t)budget)
+            --R;
+    }
+    R = std::min(R, Ch);
+    int off;
+    const size_t bytes = rgb_lds_bytes(Cw, R, sb, &off);
+    if (bytes > (size_t)budget)
+        return pl;
+    pl.path = smol::PATH_LDS;
+    pl.R = R;
+    pl.lds_bytes = bytes;
+    *slot_bytes = sb;
+    *slots_off = off;
+    return pl;
+}
+
+void fill_scale_bias(const smol_params *p, BatchArgs &a)
+{
+    for (int c = 0; c < 3; ++c) {
+        const double s = 1.0 / (double)p->std[c];
+        a.scale[c] = (float)s;
+        a.bias[c] = (float)(-(double)p->mean[c] * s);
+    }
+}
+
+int hip_fail(hipError_t e, const char *what)
+{
+    return fail(SMOL_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Shared tail of both entry points: uniform-batch detection, descriptor
+// upload for ragged batches, chunked launches.
+template <class Launch>
+int run_batch(std::vector<Desc> &descs, bool uniform, int64_t stride, BatchArgs a, int n,
+              const Plan &pl, void *stream, Launch launch)
+{
+    hipStream_t s = (hipStream_t)stream;
+    int device = 0;
+    hipError_t e = hipGetDevice(&device);
+    if (e != hipSuccess)
+        return hip_fail(e, "hipGetDevice");
+
+    const long long per_image_wg = pl.path == smol::PATH_LDS ? a.bands : 1;
+    long long chunk = pl.path == smol::PATH_LDS ? kMaxWorkgroupsPerLaunch / per_image_wg
+                                                : (long long)SMOL_MAX_BATCH;
+    if (chunk < 1)
+        chunk = 1;
+
+    smol_plan info = {};
+    info.path = pl.path;
+    info.band_rows = pl.path == smol::PATH_LDS ? pl.R : 0;
+    info.lds_bytes = (int)pl.lds_bytes;
+    info.uploaded_descriptors = uniform ? 0 : 1;
+
+    Staging *st = nullptr;
+    std::unique_lock<std::mutex> lk;
+    int slot = -1;
+    if (!uniform) {
+        st = staging_for(device);
+        lk = std::unique_lock<std::mutex>(st->mu);
+        const size_t bytes = sizeof(Desc) * (size_t)n;
+        e = staging_reserve(st, bytes);
+        if (e != hipSuccess)
+            return hip_fail(e, "descriptor staging allocation");
+        slot = st->next;
+        st->next = (st->next + 1) % Staging::kSlots;
+        if (st->pending[slot]) {
+            e = hipEventSynchronize(st->ev[slot]);
+            if (e != hipSuccess)
+                return hip_fail(e, "hipEventSynchronize");
+            st->pending[slot] = false;
+        }
+        uint8_t *h = st->host + (size_t)slot * st->slot_cap;
+        uint8_t *dv = st->dev + (size_t)slot * st->slot_cap;
+        std::memcpy(h, descs.data(), bytes);
+        e = hipMemcpyAsync(dv, h, bytes, hipMemcpyHostToDevice, s);
+        if (e != hipSuccess)
+            return hip_fail(e, "hipMemcpyAsync(descriptors)");
+        a.table = (const Desc *)dv;
+    } else {
+        a.table = nullptr;
+        a.uni = descs[0];
+        a.stride = stride;
+    }
+
+    const Desc *table0 = a.table;
+    const Desc uni0 = a.uni;
+    for (long long i0 = 0; i0 < n; i0 += chunk) {
+        const int cnt = (int)std::min<long long>(chunk, n - i0);
+        a.n = cnt;
+        a.img_base = (int)i0;
+        if (table0) {
+            a.table = table0 + i0;
+        } else {
+            a.uni = uni0;
+            for (int k = 0; k < 3; ++k)
+                a.uni.off[k] += i0 * stride;
+        }
+        const int rc = launch(a, pl, stream);
+        if (rc != (int)hipSuccess)
+            return hip_fail((hipError_t)rc, "kernel launch");
+        ++info.launches;
+    }
+    if (st) {
+        e = hipEventRecord(st->ev[slot], s);
+        if (e != hipSuccess)
+            return hip_fail(e, "hipEventRecord");
+        st->pending[slot] = true;
+    }
+    g_last_plan = info;
+    return SMOL_OK;
+}
+
+bool is_uniform(const std::vector<Desc> &d, int nofs, int64_t *stride)
+{
+    *stride = 0;
+    const int n = (int)d.size();
+    if (n <= 1)
+        return true;
+    const int64_t st = d[1].off[0] - d[0].off[0];
+    for (int i = 0; i < n; ++i) {
+        const Desc &x = d[i];
+        if (x.W != d[0].W || x.H != d[0].H || x.pitch != d[0].pitch)
+            return false;
+        for (int k = 0; k < nofs; ++k)
+            if (x.off[k] != d[0].off[k] + (int64_t)i * st)
+                return false;
+    }
+    *stride = st;
+    return true;
+}
+
+int common_checks(const void *src, int64_t src_bytes, const void *out, int32_t n,
+                  const smol_params *p)
+{
+    int rc = check_params(p);
+    if (rc)
+        return rc;
+    if (n < 0 || n > SMOL_MAX_BATCH)
+        return fail(SMOL_ERR_INVALID_ARG, "n = %d outside 0..%d", n, SMOL_MAX_BATCH);
+    if (n == 0)
+        return SMOL_OK;
+    if (!src || !out)
+        return fail(SMOL_ERR_INVALID_ARG, "src or out is NULL");
+    if (src_bytes < 1)
+        return fail(SMOL_ERR_INVALID_ARG, "src_bytes must be positive");
+    if (((uintptr_t)out & 15) != 0)
+        return fail(SMOL_ERR_INVALID_ARG, "out must be 16-byte aligned");
+    return SMOL_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int smol_preprocess_batch(const uint8_t *src, int64_t src_bytes, const int64_t *offsets,
+                          const int32_t *widths, const int32_t *heights,
+                          const int32_t *row_pitch, int32_t n, const smol_params *p, void *out,
+                          void *stream)
+{
+    g_last_error.clear();
+    int rc = common_checks(src, src_bytes, out, n, p);
+    if (rc || n == 0)
+        return rc;
+    if (!offsets || !widths || !heights)
+        return fail(SMOL_ERR_INVALID_ARG, "offsets, widths or heights is NULL");
+
+    std::vector<Desc> descs((size_t)n);
+    int64_t max_span = 0;
+    for (int32_t i = 0; i < n; ++i) {
+        Geo g;
+        rc = image_geo(widths[i], heights[i], p, &g, i);
+        if (rc)
+            return rc;
+        const int64_t W = widths[i], H = heights[i];
+        const int64_t pitch = row_pitch ? row_pitch[i] : 3 * W;
+        if (pitch < 3 * W || pitch > INT32_MAX)
+            return fail(SMOL_ERR_INVALID_ARG, "image %d: row pitch %lld < 3*width", i,
+                        (long long)pitch);
+        if (offsets[i] < 0 || offsets[i] > src_bytes ||
+            (H - 1) * pitch + 3 * W > src_bytes - offsets[i])
+            return fail(SMOL_ERR_INVALID_ARG, "image %d: bytes [%lld, +%lld) outside src (%lld)",
+                        i, (long long)offsets[i], (long long)((H - 1) * pitch + 3 * W),
+                        (long long)src_bytes);
+        Desc &d = descs[i];
+        std::memset(&d, 0, sizeof d);
+        d.off[0] = offsets[i];
+        d.W = (int32_t)W;
+        d.H = (int32_t)H;
+        d.pitch = (int32_t)pitch;
+        d.Wr = (int32_t)g.Wr;
+        d.Hr = (int32_t)g.Hr;
+        d.left = (int32_t)g.left;
+        d.top = (int32_t)g.top;
+        int64_t xf, xl;
+        x_span(d, p->crop_w, &xf, &xl);
+        max_span = std::max(max_span, 3 * (xl - xf + 1));
+    }
+    int64_t stride = 0;
+    const bool uniform = is_uniform(descs, 1, &stride);
+
+    BatchArgs a;
+    std::memset(&a, 0, sizeof a);
+    a.src = src;
+    a.src_bytes = src_bytes;
+    a.out = out;
+    a.Ch = p->crop_h;
+    a.Cw = p->crop_w;
+    fill_scale_bias(p, a);
+    int slot_bytes = 0, slots_off = 0;
+    Plan pl = plan_rgb(max_span, p->crop_h, p->crop_w, &slot_bytes, &slots_off);
+    if (g_path.load() == smol::PATH_LDS && pl.path != smol::PATH_LDS)
+        return fail(SMOL_ERR_UNSUPPORTED, "LDS path forced but the source span does not fit");
+    if (pl.path == smol::PATH_LDS) {
+        a.R = pl.R;
+        a.bands = (p->crop_h + pl.R - 1) / pl.R;
+        a.slot_bytes = slot_bytes;
+        a.slots_off = slots_off;
+    }
+    const int f16 = p->out_dtype == SMOL_OUT_F16;
+    return run_batch(descs, uniform, stride, a, n, pl, stream,
+                     [f16](const BatchArgs &x, const Plan &q, void *s) {
+                         return q.path == smol::PATH_LDS
+                                    ? smol::launch_rgb_lds(x, f16, q.lds_bytes, s)
+                                    : smol::launch_rgb_direct(x, f16, s);
+                     });
+}
+
+int smol_yuv420_preprocess_batch(const uint8_t *src, int64_t src_bytes, const int64_t *y_offsets,
+                                 const int64_t *cb_offsets, const int64_t *cr_offsets,
+                                 const int32_t *widths, const int32_t *heights, int32_t n,
+                                 const smol_params *p, void *out, void *stream)
+{
+    g_last_error.clear();
+    int rc = common_checks(src, src_bytes, out, n, p);
+    if (rc || n == 0)
+        return rc;
+    if (!y_offsets || !cb_offsets || !cr_offsets || !widths || !heights)
+        return fail(SMOL_ERR_INVALID_ARG, "an offset table, widths or heights is NULL");
+
+    std::vector<Desc> descs((size_t)n);
+    for (int32_t i = 0; i < n; ++i) {
+        Geo g;
+        rc = image_geo(widths[i], heights[i], p, &g, i);
+        if (rc)
+            return rc;
+        const int64_t W = widths[i], H = heights[i];
+        const int64_t cbytes = ((W + 1) / 2) * ((H + 1) / 2);
+        const int64_t offs[3] = {y_offsets[i], cb_offsets[i], cr_offsets[i]};
+        const int64_t sizes[3] = {W * H, cbytes, cbytes};
+        for (int k = 0; k < 3; ++k)
+            if (offs[k] < 0 || offs[k] > src_bytes || sizes[k] > src_bytes - offs[k])
+                return fail(SMOL_ERR_INVALID_ARG, "frame %d: plane %d [%lld, +%lld) outside src",
+                            i, k, (long long)offs[k], (long long)sizes[k]);
+        Desc &d = descs[i];
+        std::memset(&d, 0, sizeof d);
+        for (int k = 0; k < 3; ++k)
+            d.off[k] = offs[k];
+        d.W = (int32_t)W;
+        d.H = (int32_t)H;
+        d.pitch = (int32_t)W;
+        d.Wr = (int32_t)g.Wr;
+        d.Hr = (int32_t)g.Hr;
+        d.left = (int32_t)g.left;
+        d.top = (int32_t)g.top;
+    }
+    int64_t stride = 0;
+    const bool uniform = is_uniform(descs, 3, &stride);
+
+    BatchArgs a;
+    std::memset(&a, 0, sizeof a);
+    a.src = src;
+    a.src_bytes = src_bytes;
+    a.out = out;
+    a.Ch = p->crop_h;
+    a.Cw = p->crop_w;
+    fill_scale_bias(p, a);
+    if (g_path.load() == smol::PATH_LDS)
+        return fail(SMOL_ERR_UNSUPPORTED, "no LDS-staged I420 kernel in this build");
+    Plan pl{smol::PATH_DIRECT, 0, 0};
+    const int f16 = p->out_dtype == SMOL_OUT_F16;
+    return run_batch(descs, uniform, stride, a, n, pl, stream,
+                     [f16](const BatchArgs &x, const Plan &, void *s) {
+                         return smol::launch_yuv_direct(x, f16, s);
+                     });
+}
+
+int smol_image_geometry(int32_t width, int32_t height, int32_t yuv420, const smol_params *p,
+                        smol_geometry *g)
+{
+    g_last_error.clear();
+    int rc = check_params(p);
+    if (rc)
+        return rc;
+    if (!g)
+        return fail(SMOL_ERR_INVALID_ARG, "geometry output is NULL");
+    Geo geo;
+    rc = image_geo(width, height, p, &geo, 0);
+    if (rc)
+        return rc;
+    std::memset(g, 0, sizeof *g);
+    g->resized_w = (int32_t)geo.Wr;
+    g->resized_h = (int32_t)geo.Hr;
+    g->crop_left = (int32_t)geo.left;
+    g->crop_top = (int32_t)geo.top;
+    Desc d;
+    std::memset(&d, 0, sizeof d);
+    d.W = width;
+    d.H = height;
+    d.Wr = (int32_t)geo.Wr;
+    d.Hr = (int32_t)geo.Hr;
+    d.left = (int32_t)geo.left;
+    d.top = (int32_t)geo.top;
+    int64_t xf, xl;
+    x_span(d, p->crop_w, &xf, &xl);
+    g->src_x_first = (int32_t)xf;
+    g->src_x_last = (int32_t)xl;
+    g->src_rows = (int32_t)distinct_rows(geo.top, p->crop_h, height, geo.Hr);
+    if (yuv420) {
+        const int64_t Wc = (width + 1) / 2, Hc = (height + 1) / 2;
+        int64_t c0, c1, e0, e1;
+        chroma_index(xf, Wc, &c0, &c1);
+        chroma_index(xl, Wc, &e0, &e1);
+        g->chroma_x_first = (int32_t)c0;
+        g->chroma_x_last = (int32_t)e1;
+        // distinct chroma rows over every luma row the vertical taps read
+        int64_t count = 0, last = -1;
+        for (int64_t r = 0; r < p->crop_h; ++r) {
+            int64_t y0, y1;
+            tap_index(geo.top + r, height, geo.Hr, &y0, &y1);
+            const int64_t ys[2] = {y0, y1};
+            for (int k = 0; k < 2; ++k) {
+                int64_t a, b;
+                chroma_index(ys[k], Hc, &a, &b);
+                if (a > last) {
+                    ++count;
+                    last = a;
+                }
+                if (b > last) {
+                    ++count;
+                    last = b;
+                }
+            }
+        }
+        g->chroma_rows = (int32_t)count;
+    }
+    return SMOL_OK;
+}
+
+int smol_set_tuning(const smol_tuning *t)
+{
+    g_last_error.clear();
+    if (!t) {
+        g_path = 0;
+        g_band_rows = 0;
+        g_lds_budget = 0;
+        return SMOL_OK;
+    }
+    if (t->path < 0 || t->path > 2)
+        return fail(SMOL_ERR_INVALID_ARG, "path %d unknown", t->path);
+    if (t->band_rows < 0 || t->band_rows > kMaxBandRows)
+        return fail(SMOL_ERR_INVALID_ARG, "band_rows %d outside 0..%d", t->band_rows,
+                    kMaxBandRows);
+    if (t->lds_budget != 0 && (t->lds_budget < 4096 || t->lds_budget > 65536))
+        return fail(SMOL_ERR_INVALID_ARG, "lds_budget %d outside 4096..65536", t->lds_budget);
+    g_path = t->path;
+    g_band_rows = t->band_rows;
+    g_lds_budget = t->lds_budget;
+    return SMOL_OK;
+}
+
+int smol_last_plan(smol_plan *plan)
+{
+    if (!plan)
+        return SMOL_ERR_INVALID_ARG;
+    *plan = g_last_plan;
+    return SMOL_OK;
+}
+
+const char *smol_status_string(int status)
+{
+    switch (status) {
+    case SMOL_OK:
+        return "ok";
+    case SMOL_ERR_INVALID_ARG:
+        return "invalid argument";
+    case SMOL_ERR_UNSUPPORTED:
+        return "unsupported by this build";
+    case SMOL_ERR_HIP:
+        return "HIP runtime error";
+    default:
+        return "unknown status";
+    }
+}
+
+const char *smol_last_error(void) { return g_last_error.c_str(); }
+
+int smol_version(void) { return 100; }
+
+}  // extern "C"

@@ -1,0 +1,50 @@
+// smol_internal.h -- types shared by the host side and the kernels of libsmol.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+namespace smol {
+
+// Per-image descriptor, 64 bytes. For RGB input off[0] is the byte offset of
+// the first pixel; for I420 input off[0..2] are the Y, Cb and Cr plane offsets.
+// Wr/Hr are the resized sizes and left/top the crop offsets (host-computed
+// per image; per-element taps are computed by the kernels).
+struct alignas(16) Desc {
+    int64_t off[3];
+    int32_t W, H, pitch, Wr, Hr, left, top, pad0;
+    int32_t pad1[2];
+};
+static_assert(sizeof(Desc) == 64, "descriptor must be 64 bytes");
+
+// Kernel arguments (passed by value). When `table` is null every image shares
+// `uni` and image i's offsets are uni.off[k] + i * stride.
+struct BatchArgs {
+    const uint8_t *src;
+    int64_t src_bytes;
+    const Desc *table;
+    Desc uni;
+    int64_t stride;
+    void *out;
+    int32_t n;
+    int32_t Ch, Cw;
+    int32_t R;       // output rows per workgroup band (LDS kernels)
+    int32_t bands;   // ceil(Ch / R)
+    int32_t slot_bytes;  // bytes per staged source-row slot (LDS kernels)
+    int32_t slots_off;   // byte offset of the first slot in dynamic LDS
+    int32_t cslot_bytes; // bytes per staged chroma-row slot (I420 LDS kernel)
+    int32_t cslots_off;
+    int32_t img_base;    // index of this launch's first image in the output
+    float scale[3];  // 1 / std_c
+    float bias[3];   // -mean_c / std_c
+};
+
+enum Path { PATH_AUTO = 0, PATH_DIRECT = 1, PATH_LDS = 2 };
+
+// Launchers (smol_kernels.hip). Return a hipError_t as int.
+int launch_rgb_direct(const BatchArgs &a, int out_f16, void *stream);
+int launch_rgb_lds(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream);
+int launch_yuv_direct(const BatchArgs &a, int out_f16, void *stream);
+int launch_yuv_lds(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream);
+
+}  // namespace smol

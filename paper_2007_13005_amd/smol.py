@@ -1,0 +1,257 @@
+"""Thin ctypes binding over libsmol.so (the C ABI declared in include/smol.h).
+
+Argument marshalling only: every step of the preprocessing runs in the HIP
+kernels behind the C ABI. torch supplies device memory and the stream. If the
+library has not been built this module raises on first use; there is no CPU
+fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libsmol.so")
+
+OK = 0
+ERR_INVALID_ARG = -1
+ERR_UNSUPPORTED = -2
+ERR_HIP = -3
+
+OUT_F32 = 0
+OUT_F16 = 1
+
+PATH_AUTO = 0
+PATH_DIRECT = 1
+PATH_LDS = 2
+
+MAX_DIM = 65535
+MAX_RESIZED = 4194303
+MAX_BATCH = 1048576
+
+
+class Params(ctypes.Structure):
+    _fields_ = [("resize_short", ctypes.c_int32), ("crop_h", ctypes.c_int32),
+                ("crop_w", ctypes.c_int32), ("out_dtype", ctypes.c_int32),
+                ("mean", ctypes.c_float * 3), ("std", ctypes.c_float * 3)]
+
+
+class Geometry(ctypes.Structure):
+    _fields_ = [(name, ctypes.c_int32) for name in (
+        "resized_w", "resized_h", "crop_left", "crop_top", "src_x_first", "src_x_last",
+        "src_rows", "chroma_x_first", "chroma_x_last", "chroma_rows")]
+
+    def as_dict(self) -> dict:
+        return {name: getattr(self, name) for name, _ in self._fields_}
+
+
+class Tuning(ctypes.Structure):
+    _fields_ = [("path", ctypes.c_int32), ("band_rows", ctypes.c_int32),
+                ("lds_budget", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+class Plan(ctypes.Structure):
+    _fields_ = [("path", ctypes.c_int32), ("band_rows", ctypes.c_int32),
+                ("lds_bytes", ctypes.c_int32), ("launches", ctypes.c_int32),
+                ("uploaded_descriptors", ctypes.c_int32), ("reserved", ctypes.c_int32 * 3)]
+
+    def as_dict(self) -> dict:
+        return {name: getattr(self, name) for name, _ in self._fields_ if name != "reserved"}
+
+
+# Every symbol include/smol.h declares, with its ctypes signature.
+_vp = ctypes.c_void_p
+SIGNATURES = {
+    "smol_preprocess_batch": (ctypes.c_int, [_vp, ctypes.c_int64, _vp, _vp, _vp, _vp,
+                                             ctypes.c_int32, ctypes.POINTER(Params), _vp, _vp]),
+    "smol_yuv420_preprocess_batch": (ctypes.c_int, [_vp, ctypes.c_int64, _vp, _vp, _vp, _vp, _vp,
+                                                    ctypes.c_int32, ctypes.POINTER(Params), _vp,
+                                                    _vp]),
+    "smol_image_geometry": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                           ctypes.POINTER(Params), ctypes.POINTER(Geometry)]),
+    "smol_set_tuning": (ctypes.c_int, [ctypes.POINTER(Tuning)]),
+    "smol_last_plan": (ctypes.c_int, [ctypes.POINTER(Plan)]),
+    "smol_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "smol_last_error": (ctypes.c_char_p, []),
+    "smol_version": (ctypes.c_int, []),
+}
+
+_lib = None
+
+
+class SmolError(RuntimeError):
+    def __init__(self, status: int, detail: str):
+        self.status = status
+        super().__init__(f"smol status {status}: {detail}")
+
+
+def lib() -> ctypes.CDLL:
+    """Load libsmol.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                           "`python -m paper_2007_13005_amd.build` (needs hipcc)")
+    handle = ctypes.CDLL(LIB_PATH)
+    for name, (res, args) in SIGNATURES.items():
+        fn = getattr(handle, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = handle
+    return handle
+
+
+def _check(status: int) -> None:
+    if status != OK:
+        detail = lib().smol_last_error().decode() or lib().smol_status_string(status).decode()
+        raise SmolError(status, detail)
+
+
+def make_params(resize_short: int, crop_h: int, crop_w: int, mean, std, out_dtype: int) -> Params:
+    p = Params()
+    p.resize_short, p.crop_h, p.crop_w, p.out_dtype = resize_short, crop_h, crop_w, out_dtype
+    m = np.asarray(mean, np.float32).reshape(3)
+    s = np.asarray(std, np.float32).reshape(3)
+    for c in range(3):
+        p.mean[c] = float(m[c])
+        p.std[c] = float(s[c])
+    return p
+
+
+def image_geometry(width: int, height: int, params: Params, yuv420: bool = False) -> dict:
+    g = Geometry()
+    _check(lib().smol_image_geometry(width, height, int(bool(yuv420)), ctypes.byref(params),
+                                     ctypes.byref(g)))
+    return g.as_dict()
+
+
+def set_tuning(path: int = 0, band_rows: int = 0, lds_budget: int = 0) -> None:
+    t = Tuning(path, band_rows, lds_budget, 0)
+    _check(lib().smol_set_tuning(ctypes.byref(t)))
+
+
+def reset_tuning() -> None:
+    _check(lib().smol_set_tuning(None))
+
+
+def last_plan() -> dict:
+    p = Plan()
+    _check(lib().smol_last_plan(ctypes.byref(p)))
+    return p.as_dict()
+
+
+def version() -> int:
+    return int(lib().smol_version())
+
+
+def _table(v, dtype) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(v), dtype=dtype)
+
+
+def _stream_handle(stream) -> int | None:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _out_tensor(out, n: int, params: Params, device):
+    import torch
+    dtype = torch.float16 if params.out_dtype == OUT_F16 else torch.float32
+    shape = (n, 3, params.crop_h, params.crop_w)
+    if out is None:
+        return torch.empty(shape, dtype=dtype, device=device)
+    if tuple(out.shape) != shape or out.dtype != dtype or not out.is_contiguous():
+        raise ValueError(f"out must be a contiguous {dtype} tensor of shape {shape}")
+    return out
+
+
+def preprocess_batch(src, offsets, widths, heights, params: Params, pitches=None, out=None,
+                     stream=None):
+    """Packed HWC RGB uint8 images in the device tensor ``src`` -> NCHW tensor.
+
+    ``offsets`` / ``widths`` / ``heights`` / ``pitches`` are host sequences.
+    """
+    if src.dtype.itemsize != 1 or not src.is_cuda or not src.is_contiguous():
+        raise ValueError("src must be a contiguous uint8 device tensor")
+    off = _table(offsets, np.int64)
+    w = _table(widths, np.int32)
+    h = _table(heights, np.int32)
+    pt = None if pitches is None else _table(pitches, np.int32)
+    n = len(off)
+    if not (len(w) == len(h) == n and (pt is None or len(pt) == n)):
+        raise ValueError("table lengths differ")
+    out = _out_tensor(out, n, params, src.device)
+    _check(lib().smol_preprocess_batch(src.data_ptr(), src.numel(), off.ctypes.data,
+                                       w.ctypes.data, h.ctypes.data,
+                                       None if pt is None else pt.ctypes.data, n,
+                                       ctypes.byref(params), out.data_ptr(),
+                                       _stream_handle(stream)))
+    return out
+
+
+def yuv420_preprocess_batch(src, y_offsets, cb_offsets, cr_offsets, widths, heights,
+                            params: Params, out=None, stream=None):
+    """Planar I420 uint8 frames in the device tensor ``src`` -> NCHW RGB tensor."""
+    if src.dtype.itemsize != 1 or not src.is_cuda or not src.is_contiguous():
+        raise ValueError("src must be a contiguous uint8 device tensor")
+    yo = _table(y_offsets, np.int64)
+    bo = _table(cb_offsets, np.int64)
+    ro = _table(cr_offsets, np.int64)
+    w = _table(widths, np.int32)
+    h = _table(heights, np.int32)
+    n = len(yo)
+    if not (len(bo) == len(ro) == len(w) == len(h) == n):
+        raise ValueError("table lengths differ")
+    out = _out_tensor(out, n, params, src.device)
+    _check(lib().smol_yuv420_preprocess_batch(src.data_ptr(), src.numel(), yo.ctypes.data,
+                                              bo.ctypes.data, ro.ctypes.data, w.ctypes.data,
+                                              h.ctypes.data, n, ctypes.byref(params),
+                                              out.data_ptr(), _stream_handle(stream)))
+    return out
+
+
+def run_workload(wl, src_dev, out=None, stream=None):
+    """Run a ``synthetic.Workload`` whose ``src`` already sits on the device."""
+    p = make_params(wl.resize_short, wl.crop_h, wl.crop_w, wl.mean, wl.std, wl.out_dtype)
+    if wl.kind == "rgb":
+        return preprocess_batch(src_dev, wl.offsets, wl.widths, wl.heights, p, wl.pitches, out,
+                                stream)
+    return yuv420_preprocess_batch(src_dev, wl.y_offsets, wl.cb_offsets, wl.cr_offsets,
+                                   wl.widths, wl.heights, p, out, stream)
+
+
+class PreparedCall:
+    """A batch call with every host-side argument marshalled once, for tight
+    launch loops: ``call(src_ptr, src_bytes, out_ptr, stream_handle)``."""
+
+    def __init__(self, wl):
+        self.params = make_params(wl.resize_short, wl.crop_h, wl.crop_w, wl.mean, wl.std,
+                                  wl.out_dtype)
+        self.kind = wl.kind
+        self.n = wl.n
+        self._keep = []
+        if wl.kind == "rgb":
+            tabs = [_table(wl.offsets, np.int64), _table(wl.widths, np.int32),
+                    _table(wl.heights, np.int32)]
+            pt = None if wl.pitches is None else _table(wl.pitches, np.int32)
+            self._keep = tabs + [pt]
+            self._args = [t.ctypes.data for t in tabs] + [None if pt is None else pt.ctypes.data]
+            self._fn = lib().smol_preprocess_batch
+        else:
+            tabs = [_table(wl.y_offsets, np.int64), _table(wl.cb_offsets, np.int64),
+                    _table(wl.cr_offsets, np.int64), _table(wl.widths, np.int32),
+                    _table(wl.heights, np.int32)]
+            self._keep = tabs
+            self._args = [t.ctypes.data for t in tabs]
+            self._fn = lib().smol_yuv420_preprocess_batch
+        self._pref = ctypes.byref(self.params)
+
+    def __call__(self, src_ptr: int, src_bytes: int, out_ptr: int, stream_handle) -> None:
+        _check(self._fn(src_ptr, src_bytes, *self._args, self.n, self._pref, out_ptr,
+                        stream_handle))

@@ -1,0 +1,82 @@
+"""Helpers for the GPU parity tests: run a workload through the C ABI and
+through the oracle, and compare to the stated tolerances.
+
+Tolerances: fp32 outputs within 1e-5 absolute of the oracle; fp16 outputs
+within 1 unit in the last place of the oracle's round-to-nearest-even fp16
+(distance measured on the ordered binary16 encoding).
+"""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+
+import oracle
+from paper_2007_13005_amd import smol, synthetic
+
+F32_TOL = 1e-5
+F16_ULP = 1
+
+
+def note(msg: str) -> None:
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def run_oracle(wl: synthetic.Workload) -> np.ndarray:
+    if wl.kind == "rgb":
+        return oracle.preprocess_batch(wl.src, wl.offsets, wl.widths, wl.heights, wl.pitches,
+                                       wl.resize_short, wl.crop_h, wl.crop_w, wl.mean, wl.std,
+                                       wl.out_dtype)
+    return oracle.yuv420_preprocess_batch(wl.src, wl.y_offsets, wl.cb_offsets, wl.cr_offsets,
+                                          wl.widths, wl.heights, wl.resize_short, wl.crop_h,
+                                          wl.crop_w, wl.mean, wl.std, wl.out_dtype)
+
+
+def upload(wl: synthetic.Workload, pad_front: int = 0):
+    """Copy wl.src to the device. pad_front > 0 places it at a byte offset in a
+    larger allocation (to exercise unaligned src pointers)."""
+    import torch
+    buf = torch.empty(wl.src.size + pad_front, dtype=torch.uint8, device="cuda:0")
+    view = buf[pad_front:]
+    view.copy_(torch.from_numpy(wl.src))
+    return buf, view
+
+
+def run_gpu(wl: synthetic.Workload, pad_front: int = 0, stream=None) -> np.ndarray:
+    import torch
+    note(f"[gpu] {wl.name}: n={wl.n} kind={wl.kind} S={wl.resize_short} "
+         f"crop={wl.crop_h}x{wl.crop_w} dtype={'f16' if wl.out_dtype else 'f32'}")
+    _, src = upload(wl, pad_front)
+    out = smol.run_workload(wl, src, stream=stream)
+    torch.cuda.synchronize()
+    res = out.cpu().numpy()
+    return res
+
+
+def f16_ordered(bits: np.ndarray) -> np.ndarray:
+    b = bits.astype(np.int32)
+    mag = b & 0x7FFF
+    return np.where(b & 0x8000, -mag, mag)
+
+
+def assert_parity(gpu: np.ndarray, ref: np.ndarray, out_dtype: int, what: str = "") -> dict:
+    assert gpu.shape == ref.shape, (gpu.shape, ref.shape)
+    if out_dtype == smol.OUT_F32:
+        assert gpu.dtype == np.float32 and ref.dtype == np.float32
+        assert np.all(np.isfinite(gpu)), what
+        err = np.abs(gpu.astype(np.float64) - ref.astype(np.float64))
+        worst = float(err.max()) if err.size else 0.0
+        if worst > F32_TOL:
+            i = np.unravel_index(int(err.argmax()), err.shape)
+            raise AssertionError(f"{what}: max |gpu - oracle| = {worst:.3e} > {F32_TOL} at {i}: "
+                                 f"gpu {gpu[i]!r} oracle {ref[i]!r}")
+        return {"max_abs": worst, "exact_frac": float(np.mean(err == 0)) if err.size else 1.0}
+    assert gpu.dtype == np.float16 and ref.dtype == np.float16
+    d = np.abs(f16_ordered(gpu.view(np.uint16)) - f16_ordered(ref.view(np.uint16)))
+    worst = int(d.max()) if d.size else 0
+    if worst > F16_ULP:
+        i = np.unravel_index(int(d.argmax()), d.shape)
+        raise AssertionError(f"{what}: fp16 distance {worst} ulp > {F16_ULP} at {i}: "
+                             f"gpu {gpu[i]!r} oracle {ref[i]!r}")
+    return {"max_ulp": worst, "exact_frac": float(np.mean(d == 0)) if d.size else 1.0}

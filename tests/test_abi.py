@@ -1,0 +1,201 @@
+"""C-ABI checks that need no GPU: symbols, argument validation, geometry.
+
+Validation runs before the library makes any HIP call, so every call here is
+rejected on the host; no call reaches a device.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2007_13005_amd import smol, synthetic
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include",
+                      "smol.h")
+MEAN, STD = synthetic.IMAGENET_MEAN_255, synthetic.IMAGENET_STD_255
+
+
+def _declared_functions() -> list[str]:
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(smol_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = smol.lib()
+    declared = _declared_functions()
+    assert declared, "no declarations found"
+    assert set(declared) == set(smol.SIGNATURES), "binding and header disagree"
+    for name in declared:
+        assert hasattr(lib, name), name
+
+
+def test_status_strings_and_version():
+    lib = smol.lib()
+    for code in (smol.OK, smol.ERR_INVALID_ARG, smol.ERR_UNSUPPORTED, smol.ERR_HIP):
+        assert lib.smol_status_string(code)
+    assert lib.smol_status_string(12345) == b"unknown status"
+    assert smol.version() >= 100
+
+
+def _params(**kw):
+    base = dict(resize_short=256, crop_h=224, crop_w=224, mean=MEAN, std=STD,
+                out_dtype=smol.OUT_F16)
+    base.update(kw)
+    return smol.make_params(base["resize_short"], base["crop_h"], base["crop_w"], base["mean"],
+                            base["std"], base["out_dtype"])
+
+
+FAKE_SRC = 0x10000   # never dereferenced: every call below fails validation
+FAKE_OUT = 0x20000
+
+
+def _rgb_call(n=1, src=FAKE_SRC, src_bytes=10**9, offsets=(0,), widths=(320,), heights=(240,),
+              pitches=None, params=None, out=FAKE_OUT):
+    p = params or _params()
+    off = np.asarray(offsets, np.int64)
+    w = np.asarray(widths, np.int32)
+    h = np.asarray(heights, np.int32)
+    pt = None if pitches is None else np.asarray(pitches, np.int32)
+    rc = smol.lib().smol_preprocess_batch(src, src_bytes, off.ctypes.data, w.ctypes.data,
+                                          h.ctypes.data, None if pt is None else pt.ctypes.data,
+                                          n, ctypes.byref(p), out, None)
+    return rc, smol.lib().smol_last_error().decode()
+
+
+@pytest.mark.parametrize("kw,needle", [
+    (dict(n=-1), "n = -1"),
+    (dict(src=0), "NULL"),
+    (dict(out=0), "NULL"),
+    (dict(out=FAKE_OUT + 4), "aligned"),
+    (dict(widths=(0,)), "size"),
+    (dict(heights=(70000,)), "size"),
+    (dict(src_bytes=320 * 240 * 3 - 1), "outside src"),
+    (dict(offsets=(-1,)), "outside src"),
+    (dict(offsets=(5,), src_bytes=320 * 240 * 3 + 4), "outside src"),
+    (dict(pitches=(959,)), "pitch"),
+])
+def test_rgb_validation_rejects(kw, needle):
+    rc, msg = _rgb_call(**kw)
+    assert rc == smol.ERR_INVALID_ARG, (rc, msg)
+    assert needle in msg
+
+
+@pytest.mark.parametrize("kw,needle", [
+    (dict(out_dtype=7), "out_dtype"),
+    (dict(resize_short=0), "resize_short"),
+    (dict(crop_h=0), "crop"),
+    (dict(crop_w=342), "larger than resized"),
+    (dict(std=(1.0, 0.0, 1.0)), "std"),
+    (dict(mean=(np.inf, 0, 0)), "mean"),
+    (dict(std=(1e-45, 1, 1)), "overflow"),
+])
+def test_param_validation_rejects(kw, needle):
+    rc, msg = _rgb_call(params=_params(**kw))
+    assert rc == smol.ERR_INVALID_ARG, (rc, msg)
+    assert needle in msg
+
+
+def test_unsupported_resized_size():
+    # 65535 x 1 with S = 256: the long side would become 256 * 65535
+    rc, msg = _rgb_call(widths=(65535,), heights=(1,), params=_params(crop_h=1, crop_w=1))
+    assert rc == smol.ERR_UNSUPPORTED, msg
+
+
+def test_ragged_table_checked_entry_by_entry():
+    # second image runs past the end of src
+    rc, msg = _rgb_call(n=2, offsets=(0, 1000), widths=(300, 300), heights=(300, 300),
+                        src_bytes=300 * 300 * 3 + 999)
+    assert rc == smol.ERR_INVALID_ARG and "image 1" in msg
+
+
+def test_empty_batch_is_a_no_op():
+    rc, _ = _rgb_call(n=0, src=0, out=0)
+    assert rc == smol.OK
+
+
+def test_yuv_validation_rejects():
+    p = _params()
+    z = np.zeros(1, np.int64)
+    w = np.asarray([64], np.int32)
+    h = np.asarray([64], np.int32)
+    cb = np.asarray([64 * 64], np.int64)
+    cr = np.asarray([64 * 64 + 32 * 32], np.int64)
+    lib = smol.lib()
+    # src too small for the Cr plane
+    rc = lib.smol_yuv420_preprocess_batch(FAKE_SRC, 64 * 64 + 2 * 32 * 32 - 1, z.ctypes.data,
+                                          cb.ctypes.data, cr.ctypes.data, w.ctypes.data,
+                                          h.ctypes.data, 1, ctypes.byref(_params(resize_short=64,
+                                                                                 crop_h=64,
+                                                                                 crop_w=64)),
+                                          FAKE_OUT, None)
+    assert rc == smol.ERR_INVALID_ARG and "plane 2" in lib.smol_last_error().decode()
+    rc = lib.smol_yuv420_preprocess_batch(FAKE_SRC, 10**6, None, cb.ctypes.data, cr.ctypes.data,
+                                          w.ctypes.data, h.ctypes.data, 1, ctypes.byref(p),
+                                          FAKE_OUT, None)
+    assert rc == smol.ERR_INVALID_ARG
+
+
+def test_tuning_validation():
+    with pytest.raises(smol.SmolError):
+        smol.set_tuning(path=3)
+    with pytest.raises(smol.SmolError):
+        smol.set_tuning(band_rows=65)
+    with pytest.raises(smol.SmolError):
+        smol.set_tuning(lds_budget=100)
+    smol.set_tuning(path=1, band_rows=8, lds_budget=32768)
+    smol.reset_tuning()
+
+
+# ---------------------------------------------------------------------------
+# geometry: the library's per-image geometry against the oracle, bit for bit
+# ---------------------------------------------------------------------------
+
+
+def test_geometry_matches_oracle():
+    rng = np.random.default_rng(21)
+    cases = [(320, 240, 256, 224, 224), (1920, 1080, 224, 224, 224), (128, 128, 224, 224, 224),
+             (1280, 720, 256, 224, 224), (1, 1, 1, 1, 1), (2000, 260, 256, 224, 224)]
+    for _ in range(500):
+        W, H = (int(v) for v in rng.integers(1, 4000, size=2))
+        S = int(rng.integers(1, 700))
+        Ch, Cw = (int(v) for v in rng.integers(1, S + 1, size=2))
+        cases.append((W, H, S, Ch, Cw))
+    for W, H, S, Ch, Cw in cases:
+        g = smol.image_geometry(W, H, _params(resize_short=S, crop_h=Ch, crop_w=Cw))
+        Wr, Hr = oracle.resized_dims(W, H, S)
+        left, top = oracle.crop_offsets(Wr, Hr, Ch, Cw)
+        assert (g["resized_w"], g["resized_h"], g["crop_left"], g["crop_top"]) == (Wr, Hr, left,
+                                                                                   top)
+        # footprint: first/last source column and distinct rows, from the oracle's taps
+        assert g["src_x_first"] == oracle.axis_tap(left, W, Wr)[0]
+        assert g["src_x_last"] == oracle.axis_tap(left + Cw - 1, W, Wr)[1]
+        if Ch <= 64:
+            rows = set()
+            for r in range(Ch):
+                y0, y1, _ = oracle.axis_tap(top + r, H, Hr)
+                rows.update((y0, y1))
+            assert g["src_rows"] == len(rows)
+
+
+@pytest.mark.parametrize("cfg,rows,span", [
+    # per-config footprints worked out from the half-pixel map (source rows
+    # touched by the 224 output rows; source columns spanned by the crop)
+    ("c1", 212, 211), ("c3", 128, 128), ("c4", 448, 1078)])
+def test_config_footprints(cfg, rows, span):
+    W, H, S = {"c1": (320, 240, 256), "c3": (128, 128, 224), "c4": (1920, 1080, 224)}[cfg]
+    g = smol.image_geometry(W, H, _params(resize_short=S))
+    assert g["src_rows"] == rows
+    assert g["src_x_last"] - g["src_x_first"] + 1 == span
+
+
+def test_yuv_footprint_c5():
+    g = smol.image_geometry(1280, 720, _params(resize_short=256), yuv420=True)
+    assert (g["resized_w"], g["resized_h"], g["crop_left"], g["crop_top"]) == (455, 256, 115, 16)
+    assert g["src_rows"] == 448 and g["src_x_last"] - g["src_x_first"] + 1 == 629
+    assert g["chroma_rows"] == 316 and g["chroma_x_last"] - g["chroma_x_first"] + 1 == 316

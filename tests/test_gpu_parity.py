@@ -1,0 +1,237 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle, element
+by element, on seeded inputs (marked gpu; run on an MI355X).
+
+Covers the five workloads at full size in the launch configuration the
+benchmark uses, both kernel paths (LDS-staged and direct gather) on reduced
+batches, and the edge cases: tiny and odd sizes, extreme aspect ratios,
+crops that are not multiples of the store width, bands with a ragged tail,
+unaligned source pointers and offsets, non-tight pitches, a source buffer
+that ends exactly at the last image, determinism, and a non-default stream.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+from paper_2007_13005_amd import smol, synthetic
+from tests.gpu_util import assert_parity, note, run_gpu, run_oracle
+
+pytestmark = pytest.mark.gpu
+
+F32, F16 = synthetic.OUT_F32, synthetic.OUT_F16
+
+
+@pytest.fixture(autouse=True)
+def _reset_tuning():
+    smol.reset_tuning()
+    yield
+    smol.reset_tuning()
+
+
+def _check(wl, **kw):
+    ref = run_oracle(wl)
+    got = run_gpu(wl, **kw)
+    stats = assert_parity(got, ref, wl.out_dtype, wl.name)
+    note(f"    {wl.name}: {stats} plan={smol.last_plan()}")
+    return got, ref
+
+
+# ---------------------------------------------------------------------------
+# the five workloads, full size, default (benchmark) launch configuration
+# ---------------------------------------------------------------------------
+
+
+@pytest.mark.parametrize("cfg", ["c1", "c2", "c3", "c4", "c5"])
+def test_full_config_parity(cfg):
+    wl = synthetic.make(cfg)
+    _check(wl)
+    plan = smol.last_plan()
+    if wl.kind == "rgb":
+        assert plan["path"] == smol.PATH_LDS
+    assert plan["uploaded_descriptors"] == (1 if cfg == "c2" else 0)
+
+
+# ---------------------------------------------------------------------------
+# both kernel paths on reduced batches
+# ---------------------------------------------------------------------------
+
+SMALL = {"c1": dict(n=6), "c2": dict(n=40), "c3": dict(n=24), "c4": dict(n=3), "c5": dict(n=3)}
+
+
+@pytest.mark.parametrize("cfg", ["c1", "c2", "c3", "c4"])
+@pytest.mark.parametrize("path", [smol.PATH_DIRECT, smol.PATH_LDS])
+def test_rgb_paths(cfg, path):
+    smol.set_tuning(path=path)
+    wl = synthetic.make(cfg, **SMALL[cfg])
+    _check(wl)
+    assert smol.last_plan()["path"] == path
+
+
+@pytest.mark.parametrize("band_rows", [1, 3, 7, 16, 19])
+def test_band_rows_with_ragged_tail(band_rows):
+    """224 output rows split into bands of R rows, the last band short."""
+    smol.set_tuning(path=smol.PATH_LDS, band_rows=band_rows, lds_budget=65536)
+    wl = synthetic.c2(n=12)
+    wl.out_dtype = F32
+    _check(wl)
+    assert smol.last_plan()["band_rows"] == band_rows
+
+
+def test_c2_aligned_offsets_variant():
+    _check(synthetic.c2(n=64, align=256))
+
+
+# ---------------------------------------------------------------------------
+# edge cases
+# ---------------------------------------------------------------------------
+
+
+def _rgb(name, sizes, S, C, out_dtype, seed, align=1, pattern="noise"):
+    rng = np.random.default_rng(seed)
+    imgs = []
+    for w, h in sizes:
+        if pattern == "noise":
+            imgs.append(rng.integers(0, 256, size=(h, w, 3), dtype=np.uint8))
+        else:
+            yy, xx = np.mgrid[0:h, 0:w]
+            base = (xx * 255 // max(w - 1, 1) + yy * 255 // max(h - 1, 1)) // 2
+            imgs.append(np.repeat(base[:, :, None], 3, axis=2).astype(np.uint8))
+    return synthetic.rgb_workload(name, imgs, S, C, out_dtype, align)
+
+
+EDGE = [
+    ("1x1", [(1, 1)], 8, 8),
+    ("2x2", [(2, 2)], 2, 2),
+    ("3x5", [(3, 5)], 4, 3),
+    ("identity", [(64, 64)], 64, 64),
+    ("2x-down", [(448, 448)], 224, 224),
+    ("3x-down", [(21, 21)], 7, 7),
+    ("square", [(300, 300)], 256, 224),
+    ("extreme-wide", [(2000, 260)], 256, 224),
+    ("extreme-tall", [(260, 2000)], 256, 224),
+    ("odd-crop", [(640, 480)], 256, (199, 227)),
+    ("crop-is-resized", [(50, 37)], 40, (40, 54)),
+    ("one-row-crop", [(97, 53)], 30, (1, 30)),
+    ("one-col-crop", [(53, 97)], 30, (30, 1)),
+    ("upscale-8x", [(16, 12)], 96, 96),
+    ("mixed", [(31, 17), (17, 31), (64, 64), (5, 90), (600, 300), (1, 1)], 24, (20, 22)),
+]
+
+
+@pytest.mark.parametrize("dtype", [F32, F16])
+@pytest.mark.parametrize("path", [smol.PATH_DIRECT, smol.PATH_AUTO])
+@pytest.mark.parametrize("name,sizes,S,C", EDGE, ids=[e[0] for e in EDGE])
+def test_rgb_edge_cases(name, sizes, S, C, path, dtype):
+    smol.set_tuning(path=path)
+    _check(_rgb(name, sizes, S, C, dtype, seed=len(name)))
+
+
+def test_direct_fallback_for_wide_spans():
+    """A crop span too wide to stage in LDS goes to the direct-gather kernel."""
+    wl = _rgb("wide-span", [(20000, 100)], 100, (2, 12000), F16, seed=3)
+    _check(wl)
+    assert smol.last_plan()["path"] == smol.PATH_DIRECT
+
+
+@pytest.mark.parametrize("pad", [1, 3, 15])
+def test_unaligned_src_pointer(pad):
+    wl = synthetic.c1(n=3)
+    _check(wl, pad_front=pad)
+
+
+def test_unaligned_offsets_and_pitch():
+    rng = np.random.default_rng(31)
+    sizes = [(37, 29), (300, 211), (64, 64), (129, 257)]
+    chunks, offs, pitches, cur = [], [], [], 5
+    for w, h in sizes:
+        p = 3 * w + int(rng.integers(1, 40))
+        buf = rng.integers(0, 256, size=(h, p), dtype=np.uint8)
+        offs.append(cur)
+        pitches.append(p)
+        chunks.append(buf.reshape(-1))
+        cur += buf.size + int(rng.integers(0, 7))
+        chunks.append(rng.integers(0, 256, size=cur - offs[-1] - buf.size, dtype=np.uint8))
+    src = np.concatenate([rng.integers(0, 256, size=5, dtype=np.uint8)] + chunks)
+    wl = synthetic.Workload("pitched", "rgb", src, np.asarray([w for w, _ in sizes], np.int32),
+                            np.asarray([h for _, h in sizes], np.int32), 64, 56, 60, F32,
+                            offsets=np.asarray(offs, np.int64),
+                            pitches=np.asarray(pitches, np.int32))
+    for path in (smol.PATH_DIRECT, smol.PATH_LDS):
+        smol.set_tuning(path=path)
+        _check(wl)
+
+
+def test_src_ends_at_last_image():
+    """src_bytes is exactly the packed size (odd), so the last rows' 16-byte
+    chunks straddle the end of the buffer."""
+    wl = _rgb("tight-end", [(33, 21), (41, 20)], 16, 16, F32, seed=4)
+    assert wl.src.size % 16 != 0
+    _check(wl)
+
+
+def test_constant_images_are_exact():
+    imgs = [np.full((h, w, 3), k, np.uint8) for (w, h), k in [((320, 240), 0), ((97, 301), 131),
+                                                              ((1920, 1080), 255)]]
+    wl = synthetic.rgb_workload("const", imgs, 224, 224, F32)
+    got, _ = _check(wl)
+    for i in range(got.shape[0]):
+        for c in range(3):
+            assert np.all(got[i, c] == got[i, c, 0, 0]), (i, c)
+
+
+def test_deterministic():
+    wl = synthetic.c2(n=16)
+    a = run_gpu(wl)
+    b = run_gpu(wl)
+    np.testing.assert_array_equal(a.view(np.uint16), b.view(np.uint16))
+
+
+def test_non_default_stream():
+    import torch
+    s = torch.cuda.Stream()
+    wl = synthetic.c3(n=8)
+    ref = run_oracle(wl)
+    with torch.cuda.stream(s):
+        got = run_gpu(wl, stream=s)
+    assert_parity(got, ref, wl.out_dtype, "stream")
+
+
+# ---------------------------------------------------------------------------
+# YUV 4:2:0
+# ---------------------------------------------------------------------------
+
+
+def _yuv(name, sizes, S, C, out_dtype, seed, lo=0, hi=256):
+    rng = np.random.default_rng(seed)
+    planes = []
+    for w, h in sizes:
+        planes.append((rng.integers(lo, hi, size=(h, w), dtype=np.uint8),
+                       rng.integers(lo, hi, size=((h + 1) // 2, (w + 1) // 2), dtype=np.uint8),
+                       rng.integers(lo, hi, size=((h + 1) // 2, (w + 1) // 2), dtype=np.uint8)))
+    return synthetic.yuv420_workload(name, planes, S, C, out_dtype)
+
+
+YUV_EDGE = [
+    ("1x1", [(1, 1)], 4, 4),
+    ("odd", [(33, 21)], 20, (17, 19)),
+    ("identity", [(48, 48)], 48, 48),
+    ("upscale", [(40, 30)], 120, 112),
+    ("ragged", [(1280, 720), (641, 359), (300, 600), (2, 3)], 256, 224),
+]
+
+
+@pytest.mark.parametrize("dtype", [F32, F16])
+@pytest.mark.parametrize("name,sizes,S,C", YUV_EDGE, ids=[e[0] for e in YUV_EDGE])
+def test_yuv_edge_cases(name, sizes, S, C, dtype):
+    _check(_yuv(name, sizes, S, C, dtype, seed=len(name)))
+
+
+def test_yuv_neutral_chroma_equals_rgb_path_on_gpu():
+    rng = np.random.default_rng(41)
+    y = rng.integers(0, 256, size=(123, 201), dtype=np.uint8)
+    c = np.full((62, 101), 128, np.uint8)
+    wy = synthetic.yuv420_workload("neutral", [(y, c, c)], 100, 90, F32)
+    wr = synthetic.rgb_workload("grey", [np.repeat(y[:, :, None], 3, axis=2)], 100, 90, F32)
+    a = run_gpu(wy)
+    b = run_gpu(wr)
+    assert_parity(a, b, F32, "yuv-vs-rgb")
