@@ -18,6 +18,8 @@ LIB = os.path.join(PKG, "libsmol.so")
 SOURCES = ["smol_kernels.hip", "smol_host.cpp"]
 HEADERS = ["smol_internal.h"]
 
+# -ffp-contract=off: the kernels round every multiply and add on their own, as
+# the definition does; fused multiply-adds are never formed implicitly.
 # Packed fp32 VALU ops are disabled for the device code (the compiler would
 # otherwise form v_pk_fma/mul/add_f32 from ordinary float code). The host pass
 # warns that it does not know the feature; that warning is harmless.
@@ -28,6 +30,7 @@ HIPCC_FLAGS = [
     "-fPIC",
     "-shared",
     "-Wall",
+    "-ffp-contract=off",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
 ]
 

@@ -286,12 +286,11 @@ Plan plan_rgb(int64_t max_span_bytes, int Ch, int Cw, int *slot_bytes, int *slot
     return pl;
 }
 
-void fill_scale_bias(const smol_params *p, BatchArgs &a)
+void fill_norm(const smol_params *p, BatchArgs &a)
 {
     for (int c = 0; c < 3; ++c) {
-        const double s = 1.0 / (double)p->std[c];
-        a.scale[c] = (float)s;
-        a.bias[c] = (float)(-(double)p->mean[c] * s);
+        a.mean[c] = p->mean[c];
+        a.stdv[c] = p->std[c];
     }
 }
 
@@ -478,7 +477,7 @@ int smol_preprocess_batch(const uint8_t *src, int64_t src_bytes, const int64_t *
     a.out = out;
     a.Ch = p->crop_h;
     a.Cw = p->crop_w;
-    fill_scale_bias(p, a);
+    fill_norm(p, a);
     int slot_bytes = 0, slots_off = 0;
     Plan pl = plan_rgb(max_span, p->crop_h, p->crop_w, &slot_bytes, &slots_off);
     if (g_path.load() == smol::PATH_LDS && pl.path != smol::PATH_LDS)
@@ -546,7 +545,7 @@ int smol_yuv420_preprocess_batch(const uint8_t *src, int64_t src_bytes, const in
     a.out = out;
     a.Ch = p->crop_h;
     a.Cw = p->crop_w;
-    fill_scale_bias(p, a);
+    fill_norm(p, a);
     if (g_path.load() == smol::PATH_LDS)
         return fail(SMOL_ERR_UNSUPPORTED, "no LDS-staged I420 kernel in this build");
     Plan pl{smol::PATH_DIRECT, 0, 0};

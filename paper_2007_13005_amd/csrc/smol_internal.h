@@ -35,8 +35,8 @@ struct BatchArgs {
     int32_t cslot_bytes; // bytes per staged chroma-row slot (I420 LDS kernel)
     int32_t cslots_off;
     int32_t img_base;    // index of this launch's first image in the output
-    float scale[3];  // 1 / std_c
-    float bias[3];   // -mean_c / std_c
+    float mean[3];   // per channel, 0..255 units
+    float stdv[3];
 };
 
 enum Path { PATH_AUTO = 0, PATH_DIRECT = 1, PATH_LDS = 2 };

@@ -12,6 +12,13 @@
 // LDS kernels stage exactly the source rows the vertical taps use, over the
 // crop's column span, with wavefront-wide 16-byte direct-to-LDS loads; the
 // bilinear taps then read those rows from LDS as aligned dwords.
+//
+// Arithmetic follows the definition operation for operation: each lerp is
+// a + w * (b - a) with every operation rounded on its own (this file is built
+// with -ffp-contract=off), horizontal before vertical, and the normalisation
+// is (v - mean) / std with an IEEE division. The fp32 results are therefore
+// the correctly rounded values of that sequence, and fp16 outputs are their
+// round-to-nearest-even.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -108,7 +115,9 @@ __device__ __forceinline__ void ycbcr_to_rgb(float y, float cb, float cr, float 
     b = clamp255(y + kBCb * cb);
 }
 
-__device__ __forceinline__ float lerp(float a, float b, float w) { return fmaf(w, b - a, a); }
+__device__ __forceinline__ float lerp(float a, float b, float w) { return a + w * (b - a); }
+
+__device__ __forceinline__ float normalize(float v, float mean, float stdv) { return (v - mean) / stdv; }
 
 __device__ __forceinline__ uint32_t f16_bits(float v)
 {
@@ -325,7 +334,7 @@ __global__ void __launch_bounds__(kThreads) rgb_lds_kernel(BatchArgs a)
             for (int ch = 0; ch < 3; ++ch) {
                 const float t = lerp(p[ch], p[ch + 3], wx);
                 const float b = lerp(q[ch], q[ch + 3], wx);
-                o[ch][j] = fmaf(lerp(t, b, wy), a.scale[ch], a.bias[ch]);
+                o[ch][j] = normalize(lerp(t, b, wy), a.mean[ch], a.stdv[ch]);
             }
         }
         const int valid = min(8, Cw - c0);
@@ -363,7 +372,7 @@ __global__ void __launch_bounds__(kThreads) rgb_direct_kernel(BatchArgs a)
             const float p00 = r0[3 * tx.x0 + ch], p01 = r0[3 * tx.x1 + ch];
             const float p10 = r1[3 * tx.x0 + ch], p11 = r1[3 * tx.x1 + ch];
             const float v = lerp(lerp(p00, p01, tx.w), lerp(p10, p11, tx.w), ty.w);
-            store1<F16>(a.out, base + ch * plane, fmaf(v, a.scale[ch], a.bias[ch]));
+            store1<F16>(a.out, base + ch * plane, normalize(v, a.mean[ch], a.stdv[ch]));
         }
     }
 }
@@ -418,7 +427,7 @@ __global__ void __launch_bounds__(kThreads) yuv_direct_kernel(BatchArgs a)
         for (int ch = 0; ch < 3; ++ch) {
             const float v = lerp(lerp(rgb[0][0][ch], rgb[0][1][ch], tx.w),
                                  lerp(rgb[1][0][ch], rgb[1][1][ch], tx.w), ty.w);
-            store1<F16>(a.out, base + ch * plane, fmaf(v, a.scale[ch], a.bias[ch]));
+            store1<F16>(a.out, base + ch * plane, normalize(v, a.mean[ch], a.stdv[ch]));
         }
     }
 }

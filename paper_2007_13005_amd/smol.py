@@ -95,13 +95,29 @@ def lib() -> ctypes.CDLL:
     if not os.path.exists(LIB_PATH):
         raise RuntimeError(f"{LIB_PATH} is missing: build it with "
                            "`python -m paper_2007_13005_amd.build` (needs hipcc)")
+    # torch ships its own HIP runtime with the same soname (libamdhip64.so.7).
+    # Loading torch first makes libsmol bind to that runtime, so that torch's
+    # device pointers and streams and libsmol's launches share one runtime.
+    import torch  # noqa: F401
     handle = ctypes.CDLL(LIB_PATH)
+    runtimes = _mapped_hip_runtimes()
+    if len(runtimes) > 1:
+        raise RuntimeError(f"two HIP runtimes are loaded in this process: {runtimes}")
     for name, (res, args) in SIGNATURES.items():
         fn = getattr(handle, name)
         fn.restype = res
         fn.argtypes = args
     _lib = handle
     return handle
+
+
+def _mapped_hip_runtimes() -> list[str]:
+    try:
+        with open("/proc/self/maps") as f:
+            paths = {line.split()[-1] for line in f if "libamdhip64" in line}
+    except OSError:
+        return []
+    return sorted({os.path.realpath(p) for p in paths})
 
 
 def _check(status: int) -> None:
