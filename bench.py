@@ -43,6 +43,8 @@ def parse():
     ap.add_argument("--cpu-threads", type=int, default=0)
     ap.add_argument("--band-rows", type=int, default=0, help="tuning override (0: automatic)")
     ap.add_argument("--path", type=int, default=0, help="tuning override (0: automatic)")
+    ap.add_argument("--wg-per-cu", type=int, default=0, help="tuning override (0: automatic)")
+    ap.add_argument("--lds-budget", type=int, default=0, help="tuning override (0: automatic)")
     ap.add_argument("--profile-run", action="store_true",
                     help="no CPU baseline, fewer prints: for runs under rocprofv3")
     ap.add_argument("--copy-probe", type=int, default=0,
@@ -184,8 +186,9 @@ def main() -> int:
     algo = algorithmic_bytes(wl, smol)
     out_bytes = wl.n * 3 * wl.crop_h * wl.crop_w * wl.out_elem_bytes
     rotate = args.rotate or max(2, -(-2 * MALL_BYTES // algo))
-    if args.band_rows or args.path:
-        smol.set_tuning(path=args.path, band_rows=args.band_rows)
+    if args.band_rows or args.path or args.wg_per_cu or args.lds_budget:
+        smol.set_tuning(path=args.path, band_rows=args.band_rows, lds_budget=args.lds_budget,
+                        workgroups_per_cu=args.wg_per_cu)
 
     src0 = torch.from_numpy(wl.src).to(dev)
     srcs = [src0] + [src0.clone() for _ in range(rotate - 1)]
@@ -244,6 +247,7 @@ def main() -> int:
                    "algorithmic_bytes_per_step": algo, "output_bytes_per_step": out_bytes,
                    "rotation_sets": rotate, "kernel_path": plan["path"],
                    "band_rows": plan["band_rows"], "lds_bytes": plan["lds_bytes"],
+                   "grid": plan["grid"],
                    "gpu_ms_per_step": round(gpu_ms / args.steps, 5),
                    "hbm_gbps_wall": round(algo * args.steps / wall / 1e9, 1)},
         "roofline": roofline,

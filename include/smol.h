@@ -171,13 +171,17 @@ int smol_image_geometry(int32_t width, int32_t height, int32_t yuv420, const smo
  *               memory); 2: always the LDS-staged kernels (a call whose
  *               source span cannot be staged then fails with
  *               SMOL_ERR_UNSUPPORTED); 0: LDS-staged whenever it fits
- *   band_rows   output rows per workgroup in the LDS-staged kernels (1..64)
- *   lds_budget  bytes of LDS one workgroup may use (4096..65536) */
+ *   band_rows   output rows per band in the LDS-staged kernels (1..64)
+ *   lds_budget  bytes of LDS one workgroup may use (4096..163840, and at most
+ *               the device's per-workgroup limit)
+ *   workgroups_per_cu  resident single-wave workgroups per compute unit the
+ *               persistent LDS-staged kernels are sized for (1..16) */
 typedef struct smol_tuning {
     int32_t path;
     int32_t band_rows;
     int32_t lds_budget;
-    int32_t reserved;
+    int32_t workgroups_per_cu;
+    int32_t reserved[4];
 } smol_tuning;
 
 /* Set the knobs (NULL resets to automatic). SMOL_ERR_INVALID_ARG if a field
@@ -186,18 +190,21 @@ int smol_set_tuning(const smol_tuning *t);
 
 /* How the calling thread's last successful batch call ran.
  *   path        1 direct-gather, 2 LDS-staged
- *   band_rows   output rows per workgroup (LDS-staged) or 0
+ *   band_rows   output rows per band (LDS-staged) or 0
  *   lds_bytes   dynamic LDS per workgroup
  *   launches    kernel launches the call made
  *   uploaded_descriptors  1 if a per-image descriptor table was uploaded
- *               (ragged batch), 0 if the batch was uniform */
+ *               (ragged batch), 0 if the batch was uniform
+ *   grid        workgroups launched
+ *   work_items  bands (LDS-staged) or output pixels (direct) in the call */
 typedef struct smol_plan {
     int32_t path;
     int32_t band_rows;
     int32_t lds_bytes;
     int32_t launches;
     int32_t uploaded_descriptors;
-    int32_t reserved[3];
+    int32_t grid;
+    int64_t work_items;
 } smol_plan;
 
 int smol_last_plan(smol_plan *plan);

@@ -6,6 +6,7 @@
 #include <algorithm>
 #include <atomic>
 #include <cmath>
+#include <cfloat>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -35,13 +36,49 @@ int fail(int code, const char *fmt, ...)
     return code;
 }
 
-std::atomic<int> g_path{0}, g_band_rows{0}, g_lds_budget{0};
+std::atomic<int> g_path{0}, g_band_rows{0}, g_lds_budget{0}, g_wg_per_cu{0};
 
 constexpr int kDefaultLdsBudget = 64 * 1024;
 constexpr int kMaxBandRows = 64;
-constexpr int kThreads = 256;
-// Keep every launch below 2^31 work-items.
-constexpr long long kMaxWorkgroupsPerLaunch = (1LL << 31) / kThreads;
+constexpr int kMaxWorkgroupsPerCu = 16;
+constexpr int kDefaultBandRows = 2;
+constexpr int kGatherPassPixels = 2048;  // 256 threads x 4 pairs x 2 pixels
+
+// Per-device facts the planner needs, queried once.
+struct DeviceInfo {
+    int cus = 0;
+    int lds_per_cu = 0;
+    int lds_per_block = 0;
+};
+std::mutex g_dev_mu;
+std::vector<DeviceInfo> g_dev_info;
+
+hipError_t device_info(int device, DeviceInfo *out)
+{
+    std::lock_guard<std::mutex> lk(g_dev_mu);
+    if ((int)g_dev_info.size() <= device)
+        g_dev_info.resize(device + 1);
+    DeviceInfo &di = g_dev_info[device];
+    if (di.cus == 0) {
+        int cus = 0, lds = 0;
+        hipError_t e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device);
+        if (e != hipSuccess)
+            return e;
+        e = hipDeviceGetAttribute(&lds, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor,
+                                  device);
+        if (e != hipSuccess)
+            return e;
+        int lpb = 0;
+        e = hipDeviceGetAttribute(&lpb, hipDeviceAttributeMaxSharedMemoryPerBlock, device);
+        if (e != hipSuccess)
+            return e;
+        di.cus = cus;
+        di.lds_per_cu = lds > 0 ? lds : 65536;
+        di.lds_per_block = lpb > 0 ? lpb : 65536;
+    }
+    *out = di;
+    return hipSuccess;
+}
 
 // ---------------------------------------------------------------------------
 // Geometry (section 2 step 2; Algorithm 1 for the crop offsets)
@@ -111,9 +148,11 @@ int check_params(const smol_params *p)
     for (int c = 0; c < 3; ++c) {
         if (!std::isfinite(p->mean[c]) || !std::isfinite(p->std[c]) || p->std[c] == 0.0f)
             return fail(SMOL_ERR_INVALID_ARG, "mean/std of channel %d not finite or std == 0", c);
-        const double s = 1.0 / (double)p->std[c];
-        if (!std::isfinite((float)s) || !std::isfinite((float)(-(double)p->mean[c] * s)))
-            return fail(SMOL_ERR_INVALID_ARG, "1/std or mean/std of channel %d overflows", c);
+        const float r = 1.0f / p->std[c];
+        if (!std::isfinite(r) || std::fabs(r) < FLT_MIN ||
+            !std::isfinite((float)((std::fabs((double)p->mean[c]) + 255.0) * (double)r)))
+            return fail(SMOL_ERR_INVALID_ARG,
+                        "1/std of channel %d is not a normal number or the output overflows", c);
     }
     return SMOL_OK;
 }
@@ -233,20 +272,24 @@ hipError_t staging_reserve(Staging *st, size_t bytes)
 // ---------------------------------------------------------------------------
 
 struct Plan {
-    int path;  // smol::PATH_DIRECT or smol::PATH_LDS
+    int path;  // smol::PATH_DIRECT, smol::PATH_LDS or smol::PATH_GATHER
     int R;
     size_t lds_bytes;
+    int grid;
+    int f16;
 };
 
 size_t align16(size_t v) { return (v + 15) & ~(size_t)15; }
 
-// LDS layout of the RGB kernel: colx/colw [Cw], ty0/ty1/twy [R], smap/rowa
-// [2R], then 2R row slots of slot_bytes.
-size_t rgb_lds_bytes(int Cw, int R, int slot_bytes, int *slots_off)
+// LDS layout of the RGB kernel: two buffers per workgroup, each
+//   colx/colw [Cw] | rowa0/rowa1/twy [R] | 2R row slots.
+size_t rgb_lds_bytes(int Cw, int R, int slot_bytes, int *slots_off, int *buf_bytes)
 {
-    const size_t head = align16((size_t)8 * Cw + (size_t)28 * R);
+    const size_t head = align16((size_t)8 * Cw + (size_t)12 * R);
+    const size_t buf = align16(head + (size_t)2 * R * slot_bytes);
     *slots_off = (int)head;
-    return head + (size_t)2 * R * slot_bytes;
+    *buf_bytes = (int)buf;
+    return 2 * buf;
 }
 
 int slot_bytes_for(int64_t span_bytes)
@@ -256,9 +299,10 @@ int slot_bytes_for(int64_t span_bytes)
     return (int)(16 * ((span_bytes + 15 + 15) / 16) + 16);
 }
 
-Plan plan_rgb(int64_t max_span_bytes, int Ch, int Cw, int *slot_bytes, int *slots_off)
+Plan plan_rgb(int64_t max_span_bytes, int Ch, int Cw, int *slot_bytes, int *slots_off,
+              int *stage_bytes)
 {
-    Plan pl{smol::PATH_DIRECT, 0, 0};
+    Plan pl{smol::PATH_DIRECT, 0, 0, 0, 0};
     const int forced = g_path.load();
     if (forced == smol::PATH_DIRECT)
         return pl;
@@ -266,16 +310,15 @@ Plan plan_rgb(int64_t max_span_bytes, int Ch, int Cw, int *slot_bytes, int *slot
     if (max_span_bytes > (1 << 20))
         return pl;
     const int sb = slot_bytes_for(max_span_bytes);
+    int off, stage;
     int R = g_band_rows.load();
     if (R <= 0) {
-        R = 16;
-        int off;
-        while (R > 1 && rgb_lds_bytes(Cw, R, sb, &off) > (size_t)budget)
+        R = kDefaultBandRows;
+        while (R > 1 && rgb_lds_bytes(Cw, R, sb, &off, &stage) > (size_t)budget)
             --R;
     }
     R = std::min(R, Ch);
-    int off;
-    const size_t bytes = rgb_lds_bytes(Cw, R, sb, &off);
+    const size_t bytes = rgb_lds_bytes(Cw, R, sb, &off, &stage);
     if (bytes > (size_t)budget)
         return pl;
     pl.path = smol::PATH_LDS;
@@ -283,6 +326,7 @@ Plan plan_rgb(int64_t max_span_bytes, int Ch, int Cw, int *slot_bytes, int *slot
     pl.lds_bytes = bytes;
     *slot_bytes = sb;
     *slots_off = off;
+    *stage_bytes = stage;
     return pl;
 }
 
@@ -291,6 +335,11 @@ void fill_norm(const smol_params *p, BatchArgs &a)
     for (int c = 0; c < 3; ++c) {
         a.mean[c] = p->mean[c];
         a.stdv[c] = p->std[c];
+        // fp32 division on the host: the correctly rounded reciprocal the
+        // kernels' quotient correction needs (not 1/(double), which would
+        // round twice).
+        volatile float one = 1.0f;
+        a.rcp[c] = one / p->std[c];
     }
 }
 
@@ -299,29 +348,68 @@ int hip_fail(hipError_t e, const char *what)
     return fail(SMOL_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
+bool is_uniform(const std::vector<Desc> &d, size_t first, size_t count, int nofs,
+                int64_t *stride);
+
 // Shared tail of both entry points: uniform-batch detection, descriptor
-// upload for ragged batches, chunked launches.
+// upload for ragged batches and the launch, for images
+// [first, first + count) of descs (written to output images first.. on).
 template <class Launch>
-int run_batch(std::vector<Desc> &descs, bool uniform, int64_t stride, BatchArgs a, int n,
-              const Plan &pl, void *stream, Launch launch)
+int run_batch(const std::vector<Desc> &descs, size_t first, size_t count, int nofs,
+              BatchArgs a, Plan pl, void *stream, Launch launch, smol_plan *info)
 {
     hipStream_t s = (hipStream_t)stream;
     int device = 0;
     hipError_t e = hipGetDevice(&device);
     if (e != hipSuccess)
         return hip_fail(e, "hipGetDevice");
+    DeviceInfo di;
+    e = device_info(device, &di);
+    if (e != hipSuccess)
+        return hip_fail(e, "hipDeviceGetAttribute");
 
-    const long long per_image_wg = pl.path == smol::PATH_LDS ? a.bands : 1;
-    long long chunk = pl.path == smol::PATH_LDS ? kMaxWorkgroupsPerLaunch / per_image_wg
-                                                : (long long)SMOL_MAX_BATCH;
-    if (chunk < 1)
-        chunk = 1;
+    const int n = (int)count;
+    int64_t stride = 0;
+    const bool uniform = is_uniform(descs, first, count, nofs, &stride);
+    a.n = n;
+    a.img_base = (int)first;
+    long long items;
+    if (pl.path != smol::PATH_DIRECT && pl.lds_bytes > (size_t)di.lds_per_block)
+        return fail(SMOL_ERR_UNSUPPORTED, "LDS plan of %zu bytes exceeds the device's %d per "
+                    "workgroup", pl.lds_bytes, di.lds_per_block);
+    if (pl.path == smol::PATH_LDS || pl.path == smol::PATH_GATHER) {
+        int per_cu = 0;
+        const int oc = pl.path == smol::PATH_LDS
+                           ? smol::occupancy_rgb_lds(pl.f16, pl.lds_bytes, &per_cu)
+                           : smol::occupancy_rgb_gather(pl.f16, pl.lds_bytes, &per_cu);
+        if (oc != (int)hipSuccess)
+            return hip_fail((hipError_t)oc, "hipOccupancyMaxActiveBlocksPerMultiprocessor");
+        if (per_cu < 1)
+            return fail(SMOL_ERR_UNSUPPORTED, "kernel cannot be resident with %zu bytes of LDS",
+                        pl.lds_bytes);
+        const int forced = g_wg_per_cu.load();
+        if (forced > 0)
+            per_cu = std::min(per_cu, forced);
+        items = pl.path == smol::PATH_LDS
+                    ? (long long)n * a.bands
+                    : (long long)n * (((long long)a.Ch * a.Cw + kGatherPassPixels - 1) /
+                                      kGatherPassPixels);
+        pl.grid = (int)std::min<long long>(items, (long long)di.cus * per_cu);
+        a.grid = pl.grid;
+    } else {
+        items = (long long)n * a.Ch * a.Cw;
+        pl.grid = 0;
+    }
 
-    smol_plan info = {};
-    info.path = pl.path;
-    info.band_rows = pl.path == smol::PATH_LDS ? pl.R : 0;
-    info.lds_bytes = (int)pl.lds_bytes;
-    info.uploaded_descriptors = uniform ? 0 : 1;
+    // The plan reports the first launch of the most specialised kernel.
+    if (info->launches == 0 || (info->path == smol::PATH_DIRECT && pl.path != smol::PATH_DIRECT)) {
+        info->path = pl.path;
+        info->band_rows = pl.path == smol::PATH_LDS ? pl.R : 0;
+        info->lds_bytes = (int)pl.lds_bytes;
+        info->grid = pl.grid;
+        info->work_items = items;
+    }
+    info->uploaded_descriptors |= uniform ? 0 : 1;
 
     Staging *st = nullptr;
     std::unique_lock<std::mutex> lk;
@@ -329,7 +417,7 @@ int run_batch(std::vector<Desc> &descs, bool uniform, int64_t stride, BatchArgs 
     if (!uniform) {
         st = staging_for(device);
         lk = std::unique_lock<std::mutex>(st->mu);
-        const size_t bytes = sizeof(Desc) * (size_t)n;
+        const size_t bytes = sizeof(Desc) * count;
         e = staging_reserve(st, bytes);
         if (e != hipSuccess)
             return hip_fail(e, "descriptor staging allocation");
@@ -343,58 +431,44 @@ int run_batch(std::vector<Desc> &descs, bool uniform, int64_t stride, BatchArgs 
         }
         uint8_t *h = st->host + (size_t)slot * st->slot_cap;
         uint8_t *dv = st->dev + (size_t)slot * st->slot_cap;
-        std::memcpy(h, descs.data(), bytes);
+        std::memcpy(h, descs.data() + first, bytes);
         e = hipMemcpyAsync(dv, h, bytes, hipMemcpyHostToDevice, s);
         if (e != hipSuccess)
             return hip_fail(e, "hipMemcpyAsync(descriptors)");
         a.table = (const Desc *)dv;
     } else {
         a.table = nullptr;
-        a.uni = descs[0];
+        a.uni = descs[first];
         a.stride = stride;
     }
 
-    const Desc *table0 = a.table;
-    const Desc uni0 = a.uni;
-    for (long long i0 = 0; i0 < n; i0 += chunk) {
-        const int cnt = (int)std::min<long long>(chunk, n - i0);
-        a.n = cnt;
-        a.img_base = (int)i0;
-        if (table0) {
-            a.table = table0 + i0;
-        } else {
-            a.uni = uni0;
-            for (int k = 0; k < 3; ++k)
-                a.uni.off[k] += i0 * stride;
-        }
-        const int rc = launch(a, pl, stream);
-        if (rc != (int)hipSuccess)
-            return hip_fail((hipError_t)rc, "kernel launch");
-        ++info.launches;
-    }
+    const int rc = launch(a, pl, stream);
+    if (rc != (int)hipSuccess)
+        return hip_fail((hipError_t)rc, "kernel launch");
+    info->launches += 1;
     if (st) {
         e = hipEventRecord(st->ev[slot], s);
         if (e != hipSuccess)
             return hip_fail(e, "hipEventRecord");
         st->pending[slot] = true;
     }
-    g_last_plan = info;
     return SMOL_OK;
 }
 
-bool is_uniform(const std::vector<Desc> &d, int nofs, int64_t *stride)
+bool is_uniform(const std::vector<Desc> &d, size_t first, size_t count, int nofs,
+                int64_t *stride)
 {
     *stride = 0;
-    const int n = (int)d.size();
-    if (n <= 1)
+    if (count <= 1)
         return true;
-    const int64_t st = d[1].off[0] - d[0].off[0];
-    for (int i = 0; i < n; ++i) {
-        const Desc &x = d[i];
-        if (x.W != d[0].W || x.H != d[0].H || x.pitch != d[0].pitch)
+    const Desc &d0 = d[first];
+    const int64_t st = d[first + 1].off[0] - d0.off[0];
+    for (size_t i = 0; i < count; ++i) {
+        const Desc &x = d[first + i];
+        if (x.W != d0.W || x.H != d0.H || x.pitch != d0.pitch)
             return false;
         for (int k = 0; k < nofs; ++k)
-            if (x.off[k] != d[0].off[k] + (int64_t)i * st)
+            if (x.off[k] != d0.off[k] + (int64_t)i * st)
                 return false;
     }
     *stride = st;
@@ -437,6 +511,7 @@ int smol_preprocess_batch(const uint8_t *src, int64_t src_bytes, const int64_t *
         return fail(SMOL_ERR_INVALID_ARG, "offsets, widths or heights is NULL");
 
     std::vector<Desc> descs((size_t)n);
+    std::vector<uint8_t> inside((size_t)n);  // every 8-byte source window lies in src
     int64_t max_span = 0;
     for (int32_t i = 0; i < n; ++i) {
         Geo g;
@@ -466,9 +541,19 @@ int smol_preprocess_batch(const uint8_t *src, int64_t src_bytes, const int64_t *
         int64_t xf, xl;
         x_span(d, p->crop_w, &xf, &xl);
         max_span = std::max(max_span, 3 * (xl - xf + 1));
+        inside[i] = offsets[i] + (H - 1) * pitch + 3 * xl + 8 <= src_bytes;
     }
-    int64_t stride = 0;
-    const bool uniform = is_uniform(descs, 1, &stride);
+    // Maximal runs of images whose windows do / do not all lie inside src. In
+    // a packed batch only the image that ends at the end of src is outside,
+    // so there are one or two runs.
+    std::vector<std::pair<size_t, size_t>> runs;  // [begin, end)
+    bool any_inside = false;
+    for (size_t i = 0; i < (size_t)n; ++i) {
+        if (i == 0 || inside[i] != inside[i - 1])
+            runs.push_back({i, i});
+        runs.back().second = i + 1;
+        any_inside = any_inside || inside[i];
+    }
 
     BatchArgs a;
     std::memset(&a, 0, sizeof a);
@@ -478,23 +563,65 @@ int smol_preprocess_batch(const uint8_t *src, int64_t src_bytes, const int64_t *
     a.Ch = p->crop_h;
     a.Cw = p->crop_w;
     fill_norm(p, a);
-    int slot_bytes = 0, slots_off = 0;
-    Plan pl = plan_rgb(max_span, p->crop_h, p->crop_w, &slot_bytes, &slots_off);
-    if (g_path.load() == smol::PATH_LDS && pl.path != smol::PATH_LDS)
+    const int f16 = p->out_dtype == SMOL_OUT_F16;
+    smol_plan info = {};
+    const int forced = g_path.load();
+
+    auto direct = [f16](const BatchArgs &x, const Plan &, void *s) {
+        return smol::launch_rgb_direct(x, f16, s);
+    };
+    // Register-gather path: the gather kernel for runs of images whose windows
+    // lie inside src, the direct kernel for the others.
+    Plan pg{smol::PATH_GATHER, 0, 0, 0, f16};
+    const size_t head = align16((size_t)8 * p->crop_w);
+    pg.lds_bytes = head + (size_t)20 * p->crop_h;  // column and row tap tables
+    bool gather_fits = false;
+    {
+        int device = 0;
+        DeviceInfo di;
+        if (hipGetDevice(&device) == hipSuccess && device_info(device, &di) == hipSuccess)
+            gather_fits = pg.lds_bytes <= (size_t)di.lds_per_block;
+    }
+    if (forced == smol::PATH_GATHER ||
+        (forced == smol::PATH_AUTO && gather_fits && any_inside && runs.size() <= 3)) {
+        a.slots_off = (int)head;
+        auto gather = [f16](const BatchArgs &x, const Plan &q, void *s) {
+            return smol::launch_rgb_gather(x, f16, q.lds_bytes, s);
+        };
+        for (const auto &r : runs) {
+            const size_t cnt = r.second - r.first;
+            rc = inside[r.first]
+                     ? run_batch(descs, r.first, cnt, 1, a, pg, stream, gather, &info)
+                     : run_batch(descs, r.first, cnt, 1, a, Plan{smol::PATH_DIRECT, 0, 0, 0, f16},
+                                 stream, direct, &info);
+            if (rc)
+                return rc;
+        }
+        g_last_plan = info;
+        return SMOL_OK;
+    }
+    int slot_bytes = 0, slots_off = 0, stage_bytes = 0;
+    Plan pl = plan_rgb(max_span, p->crop_h, p->crop_w, &slot_bytes, &slots_off, &stage_bytes);
+    pl.f16 = f16;
+    if (forced == smol::PATH_LDS && pl.path != smol::PATH_LDS)
         return fail(SMOL_ERR_UNSUPPORTED, "LDS path forced but the source span does not fit");
     if (pl.path == smol::PATH_LDS) {
         a.R = pl.R;
         a.bands = (p->crop_h + pl.R - 1) / pl.R;
         a.slot_bytes = slot_bytes;
         a.slots_off = slots_off;
+        a.stage_bytes = stage_bytes;
     }
-    const int f16 = p->out_dtype == SMOL_OUT_F16;
-    return run_batch(descs, uniform, stride, a, n, pl, stream,
-                     [f16](const BatchArgs &x, const Plan &q, void *s) {
-                         return q.path == smol::PATH_LDS
-                                    ? smol::launch_rgb_lds(x, f16, q.lds_bytes, s)
-                                    : smol::launch_rgb_direct(x, f16, s);
-                     });
+    rc = run_batch(descs, 0, (size_t)n, 1, a, pl, stream,
+                   [f16](const BatchArgs &x, const Plan &q, void *s) {
+                       return q.path == smol::PATH_LDS
+                                  ? smol::launch_rgb_lds(x, f16, q.lds_bytes, s)
+                                  : smol::launch_rgb_direct(x, f16, s);
+                   },
+                   &info);
+    if (!rc)
+        g_last_plan = info;
+    return rc;
 }
 
 int smol_yuv420_preprocess_batch(const uint8_t *src, int64_t src_bytes, const int64_t *y_offsets,
@@ -535,9 +662,6 @@ int smol_yuv420_preprocess_batch(const uint8_t *src, int64_t src_bytes, const in
         d.left = (int32_t)g.left;
         d.top = (int32_t)g.top;
     }
-    int64_t stride = 0;
-    const bool uniform = is_uniform(descs, 3, &stride);
-
     BatchArgs a;
     std::memset(&a, 0, sizeof a);
     a.src = src;
@@ -548,12 +672,17 @@ int smol_yuv420_preprocess_batch(const uint8_t *src, int64_t src_bytes, const in
     fill_norm(p, a);
     if (g_path.load() == smol::PATH_LDS)
         return fail(SMOL_ERR_UNSUPPORTED, "no LDS-staged I420 kernel in this build");
-    Plan pl{smol::PATH_DIRECT, 0, 0};
     const int f16 = p->out_dtype == SMOL_OUT_F16;
-    return run_batch(descs, uniform, stride, a, n, pl, stream,
-                     [f16](const BatchArgs &x, const Plan &, void *s) {
-                         return smol::launch_yuv_direct(x, f16, s);
-                     });
+    Plan pl{smol::PATH_DIRECT, 0, 0, 0, f16};
+    smol_plan info = {};
+    rc = run_batch(descs, 0, (size_t)n, 3, a, pl, stream,
+                   [f16](const BatchArgs &x, const Plan &, void *s) {
+                       return smol::launch_yuv_direct(x, f16, s);
+                   },
+                   &info);
+    if (!rc)
+        g_last_plan = info;
+    return rc;
 }
 
 int smol_image_geometry(int32_t width, int32_t height, int32_t yuv420, const smol_params *p,
@@ -625,18 +754,24 @@ int smol_set_tuning(const smol_tuning *t)
         g_path = 0;
         g_band_rows = 0;
         g_lds_budget = 0;
+        g_wg_per_cu = 0;
         return SMOL_OK;
     }
-    if (t->path < 0 || t->path > 2)
+    if (t->path < 0 || t->path > 3)
         return fail(SMOL_ERR_INVALID_ARG, "path %d unknown", t->path);
     if (t->band_rows < 0 || t->band_rows > kMaxBandRows)
         return fail(SMOL_ERR_INVALID_ARG, "band_rows %d outside 0..%d", t->band_rows,
                     kMaxBandRows);
-    if (t->lds_budget != 0 && (t->lds_budget < 4096 || t->lds_budget > 65536))
-        return fail(SMOL_ERR_INVALID_ARG, "lds_budget %d outside 4096..65536", t->lds_budget);
+    if (t->lds_budget != 0 && (t->lds_budget < 4096 || t->lds_budget > 163840))
+        return fail(SMOL_ERR_INVALID_ARG, "lds_budget %d outside 4096..163840", t->lds_budget);
+
+    if (t->workgroups_per_cu < 0 || t->workgroups_per_cu > kMaxWorkgroupsPerCu)
+        return fail(SMOL_ERR_INVALID_ARG, "workgroups_per_cu %d outside 0..%d",
+                    t->workgroups_per_cu, kMaxWorkgroupsPerCu);
     g_path = t->path;
     g_band_rows = t->band_rows;
     g_lds_budget = t->lds_budget;
+    g_wg_per_cu = t->workgroups_per_cu;
     return SMOL_OK;
 }
 

@@ -35,15 +35,22 @@ struct BatchArgs {
     int32_t cslot_bytes; // bytes per staged chroma-row slot (I420 LDS kernel)
     int32_t cslots_off;
     int32_t img_base;    // index of this launch's first image in the output
+    int32_t grid;        // workgroups of a persistent launch (LDS kernels)
+    int32_t stage_bytes; // bytes of one of the two LDS buffers of a wave
     float mean[3];   // per channel, 0..255 units
     float stdv[3];
+    float rcp[3];    // RN(1 / stdv), fp32
 };
 
-enum Path { PATH_AUTO = 0, PATH_DIRECT = 1, PATH_LDS = 2 };
+enum Path { PATH_AUTO = 0, PATH_DIRECT = 1, PATH_LDS = 2, PATH_GATHER = 3 };
 
 // Launchers (smol_kernels.hip). Return a hipError_t as int.
 int launch_rgb_direct(const BatchArgs &a, int out_f16, void *stream);
 int launch_rgb_lds(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream);
+int launch_rgb_gather(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream);
+// Resident workgroups per compute unit for the persistent kernels.
+int occupancy_rgb_gather(int out_f16, size_t lds_bytes, int *blocks_per_cu);
+int occupancy_rgb_lds(int out_f16, size_t lds_bytes, int *blocks_per_cu);
 int launch_yuv_direct(const BatchArgs &a, int out_f16, void *stream);
 int launch_yuv_lds(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream);
 

@@ -16,9 +16,12 @@
 // Arithmetic follows the definition operation for operation: each lerp is
 // a + w * (b - a) with every operation rounded on its own (this file is built
 // with -ffp-contract=off), horizontal before vertical, and the normalisation
-// is (v - mean) / std with an IEEE division. The fp32 results are therefore
-// the correctly rounded values of that sequence, and fp16 outputs are their
-// round-to-nearest-even.
+// is the correctly rounded quotient (v - mean) / std. The quotient is formed
+// from the host-rounded reciprocal y = RN(1/std) as q0 = a*y, corrected once
+// with the exact FMA residual: q = q0 + (a - std*q0) * y. With y correctly
+// rounded this gives RN(a / std) whenever the quotient is a normal number
+// (Markstein's correction step), which covers every value a = v - mean can
+// take here. fp16 outputs are the round-to-nearest-even of those fp32 values.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -30,8 +33,6 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
 
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 struct Tap {
     int x0, x1;
@@ -55,7 +56,8 @@ __device__ __forceinline__ Tap axis_tap(int x, int in, int out)
         t.w = 0.0f;
         return t;
     }
-    const long long q = (long long)((double)num / (double)den);
+    const long long q = num < 0x7fffffffLL ? (long long)((unsigned)num / (unsigned)den)
+                                           : (long long)((double)num / (double)den);
     if (q >= in - 1) {
         t.x0 = in - 1;
         t.x1 = in - 1;
@@ -117,45 +119,46 @@ __device__ __forceinline__ void ycbcr_to_rgb(float y, float cb, float cr, float 
 
 __device__ __forceinline__ float lerp(float a, float b, float w) { return a + w * (b - a); }
 
-__device__ __forceinline__ float normalize(float v, float mean, float stdv) { return (v - mean) / stdv; }
+__device__ __forceinline__ float normalize(float v, float mean, float stdv, float rcp)
+{
+    const float a = v - mean;
+    const float q0 = a * rcp;
+    return fmaf(fmaf(-stdv, q0, a), rcp, q0);
+}
 
 __device__ __forceinline__ uint32_t f16_bits(float v)
 {
-    _Float16 h = (_Float16)v;  // v_cvt_f16_f32: round to nearest even
+    // The output is RNE-to-fp16 of the *fp32* result. Without this barrier
+    // the compiler folds the final FMA of the normalisation into the
+    // narrowing (v_fma_mix*_f16), rounding once from the exact value instead.
+    asm volatile("" : "+v"(v));
+    _Float16 h = (_Float16)v;  // round to nearest even (MODE default)
     return (uint32_t)__builtin_bit_cast(uint16_t, h);
 }
 
-// Store 8 consecutive outputs starting at element index idx of one plane.
+// Store 2 consecutive outputs starting at element index idx of one plane.
 template <int F16>
-__device__ __forceinline__ void store8(void *out, long long idx, const float (&v)[8], int valid)
+__device__ __forceinline__ void store2(void *out, long long idx, const float (&v)[2], int valid)
 {
     if (F16) {
         uint16_t *o = (uint16_t *)out + idx;
-        if (valid == 8 && (idx & 7) == 0) {
-            u32x4 q;
-            q.x = f16_bits(v[0]) | (f16_bits(v[1]) << 16);
-            q.y = f16_bits(v[2]) | (f16_bits(v[3]) << 16);
-            q.z = f16_bits(v[4]) | (f16_bits(v[5]) << 16);
-            q.w = f16_bits(v[6]) | (f16_bits(v[7]) << 16);
-            __builtin_nontemporal_store(q, (u32x4 *)o);
+        if (valid == 2 && (idx & 1) == 0) {
+            __builtin_nontemporal_store(f16_bits(v[0]) | (f16_bits(v[1]) << 16), (uint32_t *)o);
         } else {
-#pragma unroll
-            for (int j = 0; j < 8; ++j)
-                if (j < valid)
-                    o[j] = (uint16_t)f16_bits(v[j]);
+            o[0] = (uint16_t)f16_bits(v[0]);
+            if (valid == 2)
+                o[1] = (uint16_t)f16_bits(v[1]);
         }
     } else {
         float *o = (float *)out + idx;
-        if (valid == 8 && (idx & 3) == 0) {
-            const f32x4 lo = {v[0], v[1], v[2], v[3]};
-            const f32x4 hi = {v[4], v[5], v[6], v[7]};
-            __builtin_nontemporal_store(lo, (f32x4 *)o);
-            __builtin_nontemporal_store(hi, (f32x4 *)(o + 4));
+        if (valid == 2 && (idx & 1) == 0) {
+            typedef float f32x2 __attribute__((ext_vector_type(2)));
+            const f32x2 w = {v[0], v[1]};
+            __builtin_nontemporal_store(w, (f32x2 *)o);
         } else {
-#pragma unroll
-            for (int j = 0; j < 8; ++j)
-                if (j < valid)
-                    o[j] = v[j];
+            o[0] = v[0];
+            if (valid == 2)
+                o[1] = v[1];
         }
     }
 }
@@ -214,16 +217,27 @@ __device__ __forceinline__ int lower_bound(const int *a, int n, int v)
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 
-// Copy `nbytes` source bytes starting at absolute address `row` into the LDS
-// slot, as 16-byte chunks aligned in the global address space; the slot then
-// holds the bytes from (row & ~15) on. One wave per call; chunks entirely
-// inside [gbase, gend) use direct-to-LDS loads, the (at most two) chunks that
-// straddle the buffer ends are copied byte by byte within the buffer.
+// Copy `nbytes` source bytes starting at absolute address `row` into an LDS
+// slot, as 16-byte chunks aligned in the global address space, so the slot
+// holds the bytes from (row & ~15) on. Called by one whole wave with
+// wave-uniform arguments. When every chunk lies inside [gbase, gend) the
+// wave issues one direct-to-LDS load per 64 chunks (1 KiB per instruction)
+// with no per-lane checks; otherwise (a row touching either end of the
+// buffer) the chunks that straddle an end are copied byte by byte.
 __device__ __forceinline__ void stage_row(uint8_t *slot, uintptr_t row, int nbytes,
                                           uintptr_t gbase, uintptr_t gend, int lane)
 {
     const uintptr_t al = row & ~(uintptr_t)15;
     const int nch = (int)((row - al + (uintptr_t)nbytes + 15) >> 4);
+    if (al >= gbase && al + 16 * (uintptr_t)nch <= gend) {
+        for (int j0 = 0; j0 < nch; j0 += 64) {
+            if (j0 + lane < nch)
+                __builtin_amdgcn_global_load_lds(
+                    (const void *)(al + 16 * (uintptr_t)(j0 + lane)),
+                    (lds_void_t *)(slot + 16 * j0), 16, 0, 0);
+        }
+        return;
+    }
     for (int j0 = 0; j0 < nch; j0 += 64) {
         const int j = j0 + lane;
         const uintptr_t ga = al + 16 * (uintptr_t)j;
@@ -238,111 +252,536 @@ __device__ __forceinline__ void stage_row(uint8_t *slot, uintptr_t row, int nbyt
     }
 }
 
+__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
 // ---------------------------------------------------------------------------
-// RGB, LDS-staged. Workgroup = (image, band of R output rows), full crop width.
+// RGB, LDS-staged, persistent, double-buffered.
+//
+// Work items are (image, band of R output rows), image-major; workgroup g
+// takes the contiguous range [g*T/G, (g+1)*T/G) of the T items, so it walks
+// consecutive bands of the same image and recomputes column taps only when
+// the image geometry changes. LDS holds two buffers; item k uses buffer k&1.
+//
+// Iteration k: (1) wait until this wave's gathers for item k have landed,
+// (2) barrier -- now every wave's gathers for item k are in LDS and every
+// wave has finished reading buffer (k+1)&1 for item k-1, (3) prepare item
+// k+1 in buffer (k+1)&1 and issue its gathers (each wave stages every fourth
+// distinct source row), (4) interpolate item k and store it while those
+// gathers are in flight. Vector-memory operations complete in issue order,
+// so step (1) waits with vmcnt(n), n = a lower bound on the stores this
+// wave issued after item k's gathers: it never waits for item k+1's
+// gathers, and exposes no store latency.
+//
+// Buffer layout: colx/colw [Cw] | rowa0/rowa1/twy [R] | 2R source-row slots.
 // ---------------------------------------------------------------------------
-template <int F16>
-__global__ void __launch_bounds__(kThreads) rgb_lds_kernel(BatchArgs a)
+constexpr int kWavesPerGroup = kThreads / 64;
+
+// s_waitcnt vmcnt(n) for a wave-uniform n in 0..63 (the count is an
+// immediate, so dispatch on it).
+__device__ __forceinline__ void wait_vmcnt(int n)
 {
-    extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int img = (int)(blockIdx.x / (unsigned)a.bands);
-    const int band = (int)blockIdx.x - img * a.bands;
+#define SMOL_W(N)                                                                             \
+    case N:                                                                                   \
+        asm volatile("s_waitcnt vmcnt(" #N ")" ::: "memory");                                 \
+        break;
+    switch (n) {
+        SMOL_W(0) SMOL_W(1) SMOL_W(2) SMOL_W(3) SMOL_W(4) SMOL_W(5) SMOL_W(6) SMOL_W(7)
+        SMOL_W(8) SMOL_W(9) SMOL_W(10) SMOL_W(11) SMOL_W(12) SMOL_W(13) SMOL_W(14) SMOL_W(15)
+        SMOL_W(16) SMOL_W(17) SMOL_W(18) SMOL_W(19) SMOL_W(20) SMOL_W(21) SMOL_W(22) SMOL_W(23)
+        SMOL_W(24) SMOL_W(25) SMOL_W(26) SMOL_W(27) SMOL_W(28) SMOL_W(29) SMOL_W(30) SMOL_W(31)
+        SMOL_W(32) SMOL_W(33) SMOL_W(34) SMOL_W(35) SMOL_W(36) SMOL_W(37) SMOL_W(38) SMOL_W(39)
+        SMOL_W(40) SMOL_W(41) SMOL_W(42) SMOL_W(43) SMOL_W(44) SMOL_W(45) SMOL_W(46) SMOL_W(47)
+        SMOL_W(48) SMOL_W(49) SMOL_W(50) SMOL_W(51) SMOL_W(52) SMOL_W(53) SMOL_W(54) SMOL_W(55)
+        SMOL_W(56) SMOL_W(57) SMOL_W(58) SMOL_W(59) SMOL_W(60) SMOL_W(61) SMOL_W(62)
+    default:
+        asm volatile("s_waitcnt vmcnt(63)" ::: "memory");
+        break;
+    }
+#undef SMOL_W
+}
+
+__device__ __forceinline__ void barrier_lds()
+{
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+struct BufView {
+    int *colx;
+    float *colw;
+    int *rowa0, *rowa1;
+    float *twy;
+};
+
+__device__ __forceinline__ BufView buf_view(uint8_t *base, int Cw, int R)
+{
+    BufView v;
+    v.colx = (int *)base;
+    v.colw = (float *)(v.colx + Cw);
+    v.rowa0 = (int *)(v.colw + Cw);
+    v.rowa1 = v.rowa0 + R;
+    v.twy = (float *)(v.rowa1 + R);
+    return v;
+}
+
+// Number of set bits of the 64-bit mask in lanes below the calling lane.
+__device__ __forceinline__ int bits_below(unsigned long long m)
+{
+    return __builtin_amdgcn_mbcnt_hi((unsigned)(m >> 32),
+                                     __builtin_amdgcn_mbcnt_lo((unsigned)m, 0u));
+}
+
+struct Geo {
+    int W, Wr, left;
+};
+
+// Fill buffer `bi` for item w and issue this wave's share of its gathers.
+// Returns the number of vector-memory instructions issued, or -1 if a row
+// touched an end of the source buffer (byte copies: count unknown).
+__device__ __forceinline__ int prepare(const BatchArgs &a, long long w, int bi, uint8_t *lds,
+                                       Geo &held, int tid)
+{
+    const int lane = tid & 63, wave = tid >> 6;
+    const int Cw = a.Cw, R = a.R;
+    const int img = (int)(w / a.bands);
+    const int band = (int)(w - (long long)img * a.bands);
+    const int boff = bi * a.stage_bytes;
+    const BufView v = buf_view(lds + boff, Cw, R);
+    const int slot0 = boff + a.slots_off;  // LDS address of slot 0
     Desc d;
     image_desc(a, img, d);
-    const int Cw = a.Cw, Ch = a.Ch, R = a.R;
     const int r_begin = band * R;
-    const int r_cnt = min(R, Ch - r_begin);
-
-    int *colx = (int *)lds;
-    float *colw = (float *)(colx + Cw);
-    int *ty0 = (int *)(colw + Cw);
-    int *ty1 = ty0 + R;
-    float *twy = (float *)(ty1 + R);
-    int *smap = (int *)(twy + R);
-    int *rowa = smap + 2 * R;
-    uint8_t *slots = lds + a.slots_off;
-
+    const int r_cnt = min(R, a.Ch - r_begin);
     const int xs = axis_tap(d.left, d.W, d.Wr).x0;
-    const int xe = axis_tap(d.left + Cw - 1, d.W, d.Wr).x1;
-    const int span_bytes = 3 * (xe - xs + 1);
-
-    for (int c = tid; c < Cw; c += kThreads) {
-        const Tap t = axis_tap(d.left + c, d.W, d.Wr);
-        colx[c] = 3 * (t.x0 - xs);
-        colw[c] = t.w;
+    const int span_bytes = 3 * (axis_tap(d.left + Cw - 1, d.W, d.Wr).x1 - xs + 1);
+    if (d.W != held.W || d.Wr != held.Wr || d.left != held.left) {
+        held.W = d.W;
+        held.Wr = d.Wr;
+        held.left = d.left;
+        for (int c = tid; c < Cw; c += kThreads) {
+            const Tap t = axis_tap(d.left + c, d.W, d.Wr);
+            v.colx[c] = 3 * (t.x0 - xs);
+            v.colw[c] = t.w;
+        }
     }
-    for (int r = tid; r < r_cnt; r += kThreads) {
-        const Tap t = axis_tap(d.top + r_begin + r, d.H, d.Hr);
-        ty0[r] = t.x0;
-        ty1[r] = t.x1;
-        twy[r] = t.w;
-    }
-    __syncthreads();
 
-    // Candidate 2r is row ty0[r], 2r+1 is ty1[r]; each maps to the first
-    // candidate holding the same source row, so every row is staged once.
-    for (int s = tid; s < 2 * r_cnt; s += kThreads) {
-        const int v = (s & 1) ? ty1[s >> 1] : ty0[s >> 1];
-        const int i0 = lower_bound(ty0, r_cnt, v);
-        const int i1 = lower_bound(ty1, r_cnt, v);
-        int first = 2 * r_cnt;
-        if (i0 < r_cnt && ty0[i0] == v)
-            first = 2 * i0;
-        if (i1 < r_cnt && ty1[i1] == v)
-            first = min(first, 2 * i1 + 1);
-        smap[s] = first;
-    }
-    __syncthreads();
-
+    // Row taps of band row `lane` (every wave computes them). Both tap
+    // sequences are non-decreasing and y1 is y0 or y0 + 1, so among the
+    // candidates y0[0], y1[0], y0[1], ... y0[r] is new iff it exceeds
+    // y1[r-1], and y1[r] is new iff it differs from y0[r] and from y1[r-1].
+    // The k-th new candidate goes to slot k. The distinct rows seen before
+    // row r end with y1[r-1] (slot before-1), preceded by y0[r-1] when
+    // y1[r-1] = y0[r-1] + 1 (slot before-2): a repeated y0[r] is one of
+    // those two, a repeated y1[r] is y0[r] (clamped) or y1[r-1].
+    const bool live = lane < r_cnt;
+    const Tap t = axis_tap(d.top + r_begin + min(lane, r_cnt - 1), d.H, d.Hr);
+    const int prev_y1 = __shfl_up(t.x1, 1, 64);
+    const bool new0 = live && (lane == 0 || t.x0 > prev_y1);
+    const bool new1 = live && t.x1 != t.x0 && (lane == 0 || t.x1 != prev_y1);
+    const unsigned long long m0 = __ballot(new0);
+    const unsigned long long m1 = __ballot(new1);
+    const int before = bits_below(m0) + bits_below(m1);  // new candidates in rows < lane
+    const int s0 = new0 ? before : (t.x0 == prev_y1 ? before - 1 : before - 2);
+    const int s1 = new1 ? before + (new0 ? 1 : 0) : (t.x1 == t.x0 ? s0 : before - 1);
     const uintptr_t gbase = (uintptr_t)a.src, gend = gbase + (uintptr_t)a.src_bytes;
     const uintptr_t img_base = gbase + (uintptr_t)d.off[0] + 3 * (uintptr_t)xs;
-    for (int s = wave; s < 2 * r_cnt; s += kWaves) {
-        if (smap[s] != s)
-            continue;
-        const int y = (s & 1) ? ty1[s >> 1] : ty0[s >> 1];
-        stage_row(slots + s * a.slot_bytes, img_base + (uintptr_t)y * (uintptr_t)d.pitch,
-                  span_bytes, gbase, gend, lane);
+    if (wave == 0 && live) {
+        const uintptr_t r0 = img_base + (uintptr_t)t.x0 * (uintptr_t)d.pitch;
+        const uintptr_t r1 = img_base + (uintptr_t)t.x1 * (uintptr_t)d.pitch;
+        v.rowa0[lane] = slot0 + s0 * a.slot_bytes + (int)(r0 & 15);
+        v.rowa1[lane] = slot0 + s1 * a.slot_bytes + (int)(r1 & 15);
+        v.twy[lane] = t.w;
     }
-    for (int s = tid; s < 2 * r_cnt; s += kThreads) {
-        const int y = (s & 1) ? ty1[s >> 1] : ty0[s >> 1];
-        const uintptr_t row = img_base + (uintptr_t)y * (uintptr_t)d.pitch;
-        rowa[s] = a.slots_off + smap[s] * a.slot_bytes + (int)(row & 15);
-    }
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
 
-    const int gpr = (Cw + 7) >> 3;
-    const int items = r_cnt * gpr;
-    const long long plane = (long long)Ch * Cw;
-    const long long out_img = (long long)(a.img_base + img) * 3 * plane;
-    for (int it = tid; it < items; it += kThreads) {
-        const int r = it / gpr;
-        const int c0 = (it - r * gpr) * 8;
-        const int a0 = rowa[2 * r], a1 = rowa[2 * r + 1];
-        const float wy = twy[r];
-        float o[3][8];
+    // Gathers: slot k is staged by wave k % 4.
+    int issued = 0;
+    int slot = 0;
+    for (int r = 0; r < r_cnt; ++r) {
+        for (int h = 0; h < 2; ++h) {
+            const unsigned long long m = h ? m1 : m0;
+            if (!((m >> r) & 1ull))
+                continue;
+            if (slot % kWavesPerGroup == wave) {
+                const int y = __builtin_amdgcn_readlane(h ? t.x1 : t.x0, r);
+                const uintptr_t row = img_base + (uintptr_t)y * (uintptr_t)d.pitch;
+                const uintptr_t al = row & ~(uintptr_t)15;
+                const int nch = (int)((row - al + (uintptr_t)span_bytes + 15) >> 4);
+                if (issued >= 0 && al >= gbase && al + 16 * (uintptr_t)nch <= gend)
+                    issued += (nch + 63) >> 6;
+                else
+                    issued = -1;
+                stage_row(lds + slot0 + slot * a.slot_bytes, row, span_bytes, gbase, gend,
+                          lane);
+            }
+            ++slot;
+        }
+    }
+    return issued;
+}
+
+// Interpolate item w out of buffer `bi` and store it. Threads take pairs of
+// adjacent pixels of the band; the band's output rows are contiguous in every
+// plane (pixel p of the band lands at element r_begin * Cw + p), so each pair
+// is one 32-bit (fp16) or 64-bit (fp32) store per plane. Returns the number
+// of pair iterations this wave ran (each issues at least three stores).
+template <int F16>
+__device__ __forceinline__ int interpolate(const BatchArgs &a, long long w, int bi, uint8_t *lds,
+                                           int tid)
+{
+    const int Cw = a.Cw, R = a.R;
+    const int img = (int)(w / a.bands);
+    const int band = (int)(w - (long long)img * a.bands);
+    const BufView v = buf_view(lds + bi * a.stage_bytes, Cw, R);
+    const int r_begin = band * R;
+    const int npx = min(R, a.Ch - r_begin) * Cw;
+    const long long plane = (long long)a.Ch * Cw;
+    const long long out_band = (long long)(a.img_base + img) * 3 * plane + (long long)r_begin * Cw;
+    const int step = 2 * kThreads;
+    const int step_r = step / Cw, step_c = step - step_r * Cw;
+    const int first = 2 * (tid & ~63);  // first pixel of this wave
+    const int iters = npx > first ? (npx - first + step - 1) / step : 0;
+    int r = (2 * tid) / Cw;
+    int c = 2 * tid - r * Cw;
+    for (int p0 = 2 * tid; p0 < npx; p0 += step) {
+        float o[3][2];
+        int rr = r, cc = c;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const int c = min(c0 + j, Cw - 1);
-            const int xo = colx[c];
-            const float wx = colw[c];
+        for (int j = 0; j < 2; ++j) {
+            if (j == 1) {
+                if (p0 + 1 >= npx) {
+                    o[0][1] = o[1][1] = o[2][1] = 0.0f;
+                    break;
+                }
+                if (++cc == Cw) {
+                    cc = 0;
+                    ++rr;
+                }
+            }
+            const int xo = v.colx[cc];
+            const float wx = v.colw[cc];
+            const float wy = v.twy[rr];
             float p[6], q[6];
-            lds_pixel_pair(lds, a0 + xo, p);
-            lds_pixel_pair(lds, a1 + xo, q);
+            lds_pixel_pair(lds, v.rowa0[rr] + xo, p);
+            lds_pixel_pair(lds, v.rowa1[rr] + xo, q);
 #pragma unroll
             for (int ch = 0; ch < 3; ++ch) {
                 const float t = lerp(p[ch], p[ch + 3], wx);
                 const float b = lerp(q[ch], q[ch + 3], wx);
-                o[ch][j] = normalize(lerp(t, b, wy), a.mean[ch], a.stdv[ch]);
+                o[ch][j] = normalize(lerp(t, b, wy), a.mean[ch], a.stdv[ch], a.rcp[ch]);
             }
         }
-        const int valid = min(8, Cw - c0);
-        const long long idx = out_img + (long long)(r_begin + r) * Cw + c0;
+        const int valid = min(2, npx - p0);
 #pragma unroll
         for (int ch = 0; ch < 3; ++ch)
-            store8<F16>(a.out, idx + ch * plane, o[ch], valid);
+            store2<F16>(a.out, out_band + ch * plane + p0, o[ch], valid);
+        c += step_c;
+        r += step_r;
+        if (c >= Cw) {
+            c -= Cw;
+            ++r;
+        }
     }
+    return iters;
+}
+
+template <int F16>
+__global__ void __launch_bounds__(kThreads) rgb_lds_kernel(BatchArgs a)
+{
+    extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+    const int tid = threadIdx.x;
+    const long long total = (long long)a.n * a.bands;
+    const long long w_begin = total * blockIdx.x / gridDim.x;
+    const long long w_end = total * (blockIdx.x + 1) / gridDim.x;
+    const int items = (int)(w_end - w_begin);
+    Geo held0 = {-1, -1, -1}, held1 = {-1, -1, -1};  // geometry of each buffer's column taps
+    if (items > 0)
+        prepare(a, w_begin, 0, lds, held0, tid);
+    int stores_after = 0;  // lower bound on vector-memory ops issued after item k's gathers
+    for (int k = 0; k < items; ++k) {
+        wait_vmcnt(min(stores_after, 63));
+        barrier_lds();
+        int after = 0;
+        if (k + 1 < items) {
+            if ((k + 1) & 1)
+                after = prepare(a, w_begin + k + 1, 1, lds, held1, tid);
+            else
+                after = prepare(a, w_begin + k + 1, 0, lds, held0, tid);
+        }
+        const int iters = interpolate<F16>(a, w_begin + k, k & 1, lds, tid);
+        // Item k+1's gathers are followed by at least 3 * iters stores; if a
+        // row needed byte copies, wait for everything.
+        stores_after = after < 0 ? 0 : 3 * iters;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// RGB, register gather, persistent and software-pipelined.
+//
+// The output of one image is Ch x Cw pixels per plane; a "pass" is the next
+// kPassPx of them in row-major order (pixel p is element p of every plane).
+// Work items are (image, pass), image-major; workgroup g takes the
+// contiguous range [g*T/G, (g+1)*T/G) of the T items.
+//
+// LDS holds the taps of the current image geometry: per output column the
+// byte offset 3*x0 and weight, per output row the byte offsets of rows y0,
+// y1 and the weight. They are rebuilt only when the geometry changes (never,
+// in a batch of equal images).
+//
+// Per pass each thread takes kPairs pairs of adjacent output pixels. For each
+// pixel it loads the 8 source bytes at pixel x0 of rows y0 and y1 (one
+// unaligned load each; x0 and x0 + 1 sit at fixed byte positions). The loads
+// of pass j+1 go into the other of two register sets before pass j is
+// interpolated, so a pass's source bytes are in flight while the previous
+// one computes; vector-memory operations complete in issue order, so the
+// waits before using a set do not wait for the newer one. Overlapping
+// windows of neighbouring lanes share cache lines, so HBM sees each touched
+// line once. The host routes any image whose windows could reach past the
+// end of the source buffer to the direct-gather kernel instead.
+// ---------------------------------------------------------------------------
+constexpr int kPairs = 4;                       // pixel pairs per thread per pass
+constexpr int kPassPx = 2 * kPairs * kThreads;  // output pixels per pass
+
+// Pixel x0 (bytes 0..2) and x0 + 1 (bytes 3..5) of an 8-byte window.
+__device__ __forceinline__ void unpack_pair(uint64_t v, float (&p)[6])
+{
+    const uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
+    p[0] = (float)(lo & 0xffu);
+    p[1] = (float)((lo >> 8) & 0xffu);
+    p[2] = (float)((lo >> 16) & 0xffu);
+    p[3] = (float)(lo >> 24);
+    p[4] = (float)(hi & 0xffu);
+    p[5] = (float)((hi >> 8) & 0xffu);
+}
+
+struct GatherTabs {
+    const int *colx;               // 3 * x0 per output column
+    const float *colw;             // weight per output column
+    const long long *row0, *row1;  // byte offsets of rows y0, y1 per output row
+    const float *twy;              // weight per output row
+};
+
+typedef uint64_t PassRegs[kPairs][4];  // per pair: px0 row0, px0 row1, px1 row0, px1 row1
+
+// Output pixel (row, column) of pair k's first pixel in a pass, and of its
+// second pixel (which may wrap to the next row). Pixels beyond the image map
+// to pixel 0 (loaded but never stored).
+struct PairPos {
+    int r0, c0, r1, c1;
+};
+
+__device__ __forceinline__ void pass_positions(PairPos (&pos)[kPairs], int Cw, int npx,
+                                               int pass_px, int tid)
+{
+    const int p_first = pass_px + 2 * tid;
+    int r = p_first / Cw;
+    int c = p_first - r * Cw;
+    const int step = 2 * kThreads;
+    const int step_r = step / Cw, step_c = step - step_r * Cw;
+#pragma unroll
+    for (int k = 0; k < kPairs; ++k) {
+        const int p0 = p_first + k * step;
+        const bool in0 = p0 < npx, in1 = p0 + 1 < npx;
+        const bool wrap = c + 1 == Cw;
+        pos[k].r0 = in0 ? r : 0;
+        pos[k].c0 = in0 ? c : 0;
+        pos[k].r1 = in1 ? (wrap ? r + 1 : r) : 0;
+        pos[k].c1 = in1 ? (wrap ? 0 : c + 1) : 0;
+        c += step_c;
+        r += step_r;
+        if (c >= Cw) {
+            c -= Cw;
+            ++r;
+        }
+    }
+}
+
+__device__ __forceinline__ uint64_t load8(const uint8_t *p)
+{
+    uint64_t v;
+    __builtin_memcpy(&v, p, 8);  // one unaligned global_load_dwordx2
+    return v;
+}
+
+__device__ __forceinline__ void load_pass(PassRegs &v, const GatherTabs &T, const uint8_t *base,
+                                          int Cw, int npx, int pass_px, int tid)
+{
+    PairPos pos[kPairs];
+    pass_positions(pos, Cw, npx, pass_px, tid);
+#pragma unroll
+    for (int k = 0; k < kPairs; ++k) {
+        const uint8_t *q0 = base + T.colx[pos[k].c0];
+        const uint8_t *q1 = base + T.colx[pos[k].c1];
+        v[k][0] = load8(q0 + T.row0[pos[k].r0]);
+        v[k][1] = load8(q0 + T.row1[pos[k].r0]);
+        v[k][2] = load8(q1 + T.row0[pos[k].r1]);
+        v[k][3] = load8(q1 + T.row1[pos[k].r1]);
+    }
+}
+
+template <int F16>
+__device__ __forceinline__ void compute_pass(const PassRegs &v, const GatherTabs &T,
+                                             const BatchArgs &a, long long out_img, int npx,
+                                             int pass_px, int tid)
+{
+    PairPos pos[kPairs];
+    pass_positions(pos, a.Cw, npx, pass_px, tid);
+    const int p_first = pass_px + 2 * tid;
+#pragma unroll
+    for (int k = 0; k < kPairs; ++k) {
+        const int p0 = p_first + k * 2 * kThreads;
+        if (p0 >= npx)
+            break;
+        const int valid = min(2, npx - p0);
+        float o[3][2];
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const float wx = T.colw[j ? pos[k].c1 : pos[k].c0];
+            const float wy = T.twy[j ? pos[k].r1 : pos[k].r0];
+            float p[6], q[6];
+            unpack_pair(v[k][2 * j], p);
+            unpack_pair(v[k][2 * j + 1], q);
+#pragma unroll
+            for (int ch = 0; ch < 3; ++ch) {
+                const float t = lerp(p[ch], p[ch + 3], wx);
+                const float b = lerp(q[ch], q[ch + 3], wx);
+                o[ch][j] = normalize(lerp(t, b, wy), a.mean[ch], a.stdv[ch], a.rcp[ch]);
+            }
+        }
+#pragma unroll
+        for (int ch = 0; ch < 3; ++ch)
+            store2<F16>(a.out, out_img + ch * (long long)npx + p0, o[ch], valid);
+    }
+}
+
+// The fields of an image the gather kernel uses, as plain scalars (a copy of
+// the 64-byte descriptor would not stay in registers across the loop).
+struct ImgGeo {
+    long long off;
+    int W, H, pitch, Wr, Hr, left, top;
+};
+
+__device__ __forceinline__ ImgGeo image_geo(const BatchArgs &a, int img)
+{
+    ImgGeo g;
+    if (a.table) {
+        const Desc *t = a.table + img;
+        g.off = t->off[0];
+        g.W = t->W;
+        g.H = t->H;
+        g.pitch = t->pitch;
+        g.Wr = t->Wr;
+        g.Hr = t->Hr;
+        g.left = t->left;
+        g.top = t->top;
+    } else {
+        g.off = a.uni.off[0] + (long long)img * a.stride;
+        g.W = a.uni.W;
+        g.H = a.uni.H;
+        g.pitch = a.uni.pitch;
+        g.Wr = a.uni.Wr;
+        g.Hr = a.uni.Hr;
+        g.left = a.uni.left;
+        g.top = a.uni.top;
+    }
+    return g;
+}
+
+// Fill the tap tables for the geometry of image d (all threads; caller syncs).
+__device__ __forceinline__ void build_tabs(uint8_t *lds, const BatchArgs &a, const ImgGeo &d,
+                                           int tid)
+{
+    const int Cw = a.Cw, Ch = a.Ch;
+    int *colx = (int *)lds;
+    float *colw = (float *)(colx + Cw);
+    long long *row0 = (long long *)(lds + a.slots_off);
+    long long *row1 = row0 + Ch;
+    float *twy = (float *)(row1 + Ch);
+    for (int c = tid; c < Cw; c += kThreads) {
+        const Tap t = axis_tap(d.left + c, d.W, d.Wr);
+        colx[c] = 3 * t.x0;
+        colw[c] = t.w;
+    }
+    for (int r = tid; r < Ch; r += kThreads) {
+        const Tap t = axis_tap(d.top + r, d.H, d.Hr);
+        row0[r] = (long long)t.x0 * d.pitch;
+        row1[r] = (long long)t.x1 * d.pitch;
+        twy[r] = t.w;
+    }
+}
+
+__device__ __forceinline__ bool same_geometry(const ImgGeo &x, const ImgGeo &y)
+{
+    return x.W == y.W && x.H == y.H && x.pitch == y.pitch && x.Wr == y.Wr && x.Hr == y.Hr &&
+           x.left == y.left && x.top == y.top;
+}
+
+template <int F16>
+__global__ void __launch_bounds__(kThreads) rgb_gather_kernel(BatchArgs a)
+{
+    extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+    const int tid = threadIdx.x;
+    const int Cw = a.Cw;
+    const int npx = a.Ch * Cw;
+    const int passes = (npx + kPassPx - 1) / kPassPx;  // per image
+    const long long total = (long long)a.n * passes;
+    const long long w_begin = total * blockIdx.x / gridDim.x;
+    const long long w_end = total * (blockIdx.x + 1) / gridDim.x;
+    if (w_begin >= w_end)
+        return;
+
+    GatherTabs T;
+    T.colx = (const int *)lds;
+    T.colw = (const float *)(T.colx + Cw);
+    T.row0 = (const long long *)(lds + a.slots_off);
+    T.row1 = T.row0 + a.Ch;
+    T.twy = (const float *)(T.row1 + a.Ch);
+
+    PassRegs A, B;
+    long long w = w_begin;
+    int img = (int)(w / passes);
+    ImgGeo d = image_geo(a, img);
+    build_tabs(lds, a, d, tid);
+    __syncthreads();
+    int pass_px = (int)(w - (long long)img * passes) * kPassPx;
+    load_pass(A, T, a.src + d.off, Cw, npx, pass_px, tid);
+
+    // One step computes the current set and prefetches the next item into
+    // the other; two steps per trip so the sets alternate without copies.
+#define SMOL_GATHER_STEP(CUR, NXT)                                                            \
+    {                                                                                         \
+        const long long wn = w + 1;                                                           \
+        const bool more = wn < w_end;                                                         \
+        int nimg = img, npass = 0;                                                            \
+        ImgGeo dn = d;                                                                        \
+        bool pre = false;                                                                     \
+        if (more) {                                                                           \
+            nimg = (int)(wn / passes);                                                        \
+            npass = (int)(wn - (long long)nimg * passes) * kPassPx;                           \
+            if (nimg != img)                                                                  \
+                dn = image_geo(a, nimg);                                                      \
+            pre = same_geometry(dn, d);                                                       \
+            if (pre)                                                                          \
+                load_pass(NXT, T, a.src + dn.off, Cw, npx, npass, tid);                       \
+        }                                                                                     \
+        compute_pass<F16>(CUR, T, a, (long long)(a.img_base + img) * 3 * npx, npx, pass_px,   \
+                          tid);                                                               \
+        if (!more)                                                                            \
+            break;                                                                            \
+        if (!pre) { /* new geometry: rebuild the tables, then load */                         \
+            __syncthreads();                                                                  \
+            build_tabs(lds, a, dn, tid);                                                      \
+            __syncthreads();                                                                  \
+            load_pass(NXT, T, a.src + dn.off, Cw, npx, npass, tid);                           \
+        }                                                                                     \
+        w = wn;                                                                               \
+        img = nimg;                                                                           \
+        d = dn;                                                                               \
+        pass_px = npass;                                                                      \
+    }
+    while (true) {
+        SMOL_GATHER_STEP(A, B)
+        SMOL_GATHER_STEP(B, A)
+    }
+#undef SMOL_GATHER_STEP
 }
 
 // ---------------------------------------------------------------------------
@@ -372,7 +811,7 @@ __global__ void __launch_bounds__(kThreads) rgb_direct_kernel(BatchArgs a)
             const float p00 = r0[3 * tx.x0 + ch], p01 = r0[3 * tx.x1 + ch];
             const float p10 = r1[3 * tx.x0 + ch], p11 = r1[3 * tx.x1 + ch];
             const float v = lerp(lerp(p00, p01, tx.w), lerp(p10, p11, tx.w), ty.w);
-            store1<F16>(a.out, base + ch * plane, normalize(v, a.mean[ch], a.stdv[ch]));
+            store1<F16>(a.out, base + ch * plane, normalize(v, a.mean[ch], a.stdv[ch], a.rcp[ch]));
         }
     }
 }
@@ -427,7 +866,7 @@ __global__ void __launch_bounds__(kThreads) yuv_direct_kernel(BatchArgs a)
         for (int ch = 0; ch < 3; ++ch) {
             const float v = lerp(lerp(rgb[0][0][ch], rgb[0][1][ch], tx.w),
                                  lerp(rgb[1][0][ch], rgb[1][1][ch], tx.w), ty.w);
-            store1<F16>(a.out, base + ch * plane, normalize(v, a.mean[ch], a.stdv[ch]));
+            store1<F16>(a.out, base + ch * plane, normalize(v, a.mean[ch], a.stdv[ch], a.rcp[ch]));
         }
     }
 }
@@ -456,12 +895,41 @@ int launch_rgb_direct(const BatchArgs &a, int out_f16, void *stream)
 int launch_rgb_lds(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream)
 {
     hipStream_t s = (hipStream_t)stream;
-    const dim3 grid((unsigned)a.n * (unsigned)a.bands), block(kThreads);
+    const dim3 grid((unsigned)a.grid), block(kThreads);
     if (out_f16)
         hipLaunchKernelGGL(rgb_lds_kernel<1>, grid, block, lds_bytes, s, a);
     else
         hipLaunchKernelGGL(rgb_lds_kernel<0>, grid, block, lds_bytes, s, a);
     return (int)hipGetLastError();
+}
+
+int launch_rgb_gather(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream)
+{
+    hipStream_t s = (hipStream_t)stream;
+    const dim3 grid((unsigned)a.grid), block(kThreads);
+    if (out_f16)
+        hipLaunchKernelGGL(rgb_gather_kernel<1>, grid, block, lds_bytes, s, a);
+    else
+        hipLaunchKernelGGL(rgb_gather_kernel<0>, grid, block, lds_bytes, s, a);
+    return (int)hipGetLastError();
+}
+
+int occupancy_rgb_gather(int out_f16, size_t lds_bytes, int *blocks_per_cu)
+{
+    hipError_t e = out_f16 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                                 blocks_per_cu, rgb_gather_kernel<1>, kThreads, lds_bytes)
+                           : hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                                 blocks_per_cu, rgb_gather_kernel<0>, kThreads, lds_bytes);
+    return (int)e;
+}
+
+int occupancy_rgb_lds(int out_f16, size_t lds_bytes, int *blocks_per_cu)
+{
+    hipError_t e = out_f16 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                                 blocks_per_cu, rgb_lds_kernel<1>, kThreads, lds_bytes)
+                           : hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                                 blocks_per_cu, rgb_lds_kernel<0>, kThreads, lds_bytes);
+    return (int)e;
 }
 
 int launch_yuv_direct(const BatchArgs &a, int out_f16, void *stream)

@@ -26,6 +26,7 @@ OUT_F16 = 1
 PATH_AUTO = 0
 PATH_DIRECT = 1
 PATH_LDS = 2
+PATH_GATHER = 3
 
 MAX_DIM = 65535
 MAX_RESIZED = 4194303
@@ -49,16 +50,18 @@ class Geometry(ctypes.Structure):
 
 class Tuning(ctypes.Structure):
     _fields_ = [("path", ctypes.c_int32), ("band_rows", ctypes.c_int32),
-                ("lds_budget", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("lds_budget", ctypes.c_int32), ("workgroups_per_cu", ctypes.c_int32),
+                ("reserved", ctypes.c_int32 * 4)]
 
 
 class Plan(ctypes.Structure):
     _fields_ = [("path", ctypes.c_int32), ("band_rows", ctypes.c_int32),
                 ("lds_bytes", ctypes.c_int32), ("launches", ctypes.c_int32),
-                ("uploaded_descriptors", ctypes.c_int32), ("reserved", ctypes.c_int32 * 3)]
+                ("uploaded_descriptors", ctypes.c_int32), ("grid", ctypes.c_int32),
+                ("work_items", ctypes.c_int64)]
 
     def as_dict(self) -> dict:
-        return {name: getattr(self, name) for name, _ in self._fields_ if name != "reserved"}
+        return {name: getattr(self, name) for name, _ in self._fields_}
 
 
 # Every symbol include/smol.h declares, with its ctypes signature.
@@ -144,8 +147,9 @@ def image_geometry(width: int, height: int, params: Params, yuv420: bool = False
     return g.as_dict()
 
 
-def set_tuning(path: int = 0, band_rows: int = 0, lds_budget: int = 0) -> None:
-    t = Tuning(path, band_rows, lds_budget, 0)
+def set_tuning(path: int = 0, band_rows: int = 0, lds_budget: int = 0,
+               workgroups_per_cu: int = 0) -> None:
+    t = Tuning(path, band_rows, lds_budget, workgroups_per_cu)
     _check(lib().smol_set_tuning(ctypes.byref(t)))
 
 

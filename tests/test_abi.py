@@ -143,11 +143,13 @@ def test_yuv_validation_rejects():
 
 def test_tuning_validation():
     with pytest.raises(smol.SmolError):
-        smol.set_tuning(path=3)
+        smol.set_tuning(path=4)
     with pytest.raises(smol.SmolError):
         smol.set_tuning(band_rows=65)
     with pytest.raises(smol.SmolError):
         smol.set_tuning(lds_budget=100)
+    with pytest.raises(smol.SmolError):
+        smol.set_tuning(workgroups_per_cu=17)
     smol.set_tuning(path=1, band_rows=8, lds_budget=32768)
     smol.reset_tuning()
 

@@ -41,14 +41,37 @@ def _check(wl, **kw):
 # ---------------------------------------------------------------------------
 
 
+_FULL = {}
+
+
+def _full(cfg):
+    """Full-size workload, its oracle output and its GPU output (cached)."""
+    if cfg not in _FULL:
+        wl = synthetic.make(cfg)
+        ref = run_oracle(wl)
+        got = run_gpu(wl)
+        _FULL[cfg] = (wl, ref, got, smol.last_plan())
+    return _FULL[cfg]
+
+
 @pytest.mark.parametrize("cfg", ["c1", "c2", "c3", "c4", "c5"])
 def test_full_config_parity(cfg):
-    wl = synthetic.make(cfg)
-    _check(wl)
-    plan = smol.last_plan()
+    wl, ref, got, plan = _full(cfg)
+    stats = assert_parity(got, ref, wl.out_dtype, wl.name)
+    note(f"    {cfg}: {stats} plan={plan}")
     if wl.kind == "rgb":
-        assert plan["path"] == smol.PATH_LDS
+        assert plan["path"] == smol.PATH_GATHER
     assert plan["uploaded_descriptors"] == (1 if cfg == "c2" else 0)
+
+
+@pytest.mark.parametrize("cfg", ["c1", "c2", "c3", "c4", "c5"])
+def test_full_config_bit_exact(cfg):
+    """Stronger than the tolerance: the kernels evaluate the definition's
+    operations in its order with correctly rounded results, so every output
+    equals the oracle's bit for bit."""
+    wl, ref, got, _ = _full(cfg)
+    np.testing.assert_array_equal(got.view(np.uint32 if wl.out_dtype == F32 else np.uint16),
+                                  ref.view(np.uint32 if wl.out_dtype == F32 else np.uint16))
 
 
 # ---------------------------------------------------------------------------
@@ -59,7 +82,7 @@ SMALL = {"c1": dict(n=6), "c2": dict(n=40), "c3": dict(n=24), "c4": dict(n=3), "
 
 
 @pytest.mark.parametrize("cfg", ["c1", "c2", "c3", "c4"])
-@pytest.mark.parametrize("path", [smol.PATH_DIRECT, smol.PATH_LDS])
+@pytest.mark.parametrize("path", [smol.PATH_DIRECT, smol.PATH_LDS, smol.PATH_GATHER])
 def test_rgb_paths(cfg, path):
     smol.set_tuning(path=path)
     wl = synthetic.make(cfg, **SMALL[cfg])
@@ -67,9 +90,10 @@ def test_rgb_paths(cfg, path):
     assert smol.last_plan()["path"] == path
 
 
-@pytest.mark.parametrize("band_rows", [1, 3, 7, 16, 19])
+@pytest.mark.parametrize("band_rows", [1, 2, 3, 5, 9])
 def test_band_rows_with_ragged_tail(band_rows):
-    """224 output rows split into bands of R rows, the last band short."""
+    """224 output rows split into bands of R rows (the last band short when R
+    does not divide 224)."""
     smol.set_tuning(path=smol.PATH_LDS, band_rows=band_rows, lds_budget=65536)
     wl = synthetic.c2(n=12)
     wl.out_dtype = F32
@@ -119,18 +143,58 @@ EDGE = [
 
 
 @pytest.mark.parametrize("dtype", [F32, F16])
-@pytest.mark.parametrize("path", [smol.PATH_DIRECT, smol.PATH_AUTO])
+@pytest.mark.parametrize("path", [smol.PATH_DIRECT, smol.PATH_AUTO, smol.PATH_GATHER])
 @pytest.mark.parametrize("name,sizes,S,C", EDGE, ids=[e[0] for e in EDGE])
 def test_rgb_edge_cases(name, sizes, S, C, path, dtype):
     smol.set_tuning(path=path)
     _check(_rgb(name, sizes, S, C, dtype, seed=len(name)))
 
 
-def test_direct_fallback_for_wide_spans():
-    """A crop span too wide to stage in LDS goes to the direct-gather kernel."""
-    wl = _rgb("wide-span", [(20000, 100)], 100, (2, 12000), F16, seed=3)
+@pytest.mark.parametrize("path", [smol.PATH_AUTO, smol.PATH_LDS])
+def test_wide_spans(path):
+    """A crop span too wide to stage in LDS: the LDS planner falls back to the
+    direct-gather kernel; the register-gather kernel handles it directly."""
+    smol.set_tuning(path=path)
+    wl = _rgb("wide-span", [(20000, 100), (15000, 100)], 100, (2, 12000), F16, seed=3)
+    if path == smol.PATH_LDS:
+        with pytest.raises(smol.SmolError):
+            run_gpu(wl)
+        smol.set_tuning(path=smol.PATH_AUTO)
+    _check(wl)
+    assert smol.last_plan()["path"] in (smol.PATH_GATHER, smol.PATH_DIRECT)
+
+
+def test_crop_too_wide_for_gather_tables():
+    """Column tap tables of a 30000-wide crop exceed LDS: the automatic plan
+    uses the direct kernel, a forced gather plan is refused."""
+    wl = _rgb("very-wide", [(31000, 40)], 40, (3, 30000), F32, seed=6)
     _check(wl)
     assert smol.last_plan()["path"] == smol.PATH_DIRECT
+    smol.set_tuning(path=smol.PATH_GATHER)
+    with pytest.raises(smol.SmolError):
+        run_gpu(wl)
+
+
+def test_gather_prefix_with_direct_tail():
+    """In a packed batch the last image's 8-byte windows reach the end of src:
+    the gather kernel takes the others and the direct kernel that one."""
+    wl = _rgb("tail", [(128, 128)] * 5, 224, 224, F16, seed=5)
+    _check(wl)
+    plan = smol.last_plan()
+    assert plan["path"] == smol.PATH_GATHER and plan["launches"] == 2
+
+
+@pytest.mark.parametrize("path", [smol.PATH_AUTO, smol.PATH_GATHER])
+def test_image_at_end_of_src_first_in_batch(path):
+    """Batch order is the reverse of memory order, so the image whose windows
+    reach the end of src comes first: gather and direct launches interleave."""
+    import dataclasses
+    smol.set_tuning(path=path)
+    fwd = _rgb("reversed", [(90, 70), (64, 64), (128, 100), (33, 47)], 48, 40, F16, seed=8)
+    wl = dataclasses.replace(fwd, widths=fwd.widths[::-1].copy(),
+                             heights=fwd.heights[::-1].copy(), offsets=fwd.offsets[::-1].copy())
+    _check(wl)
+    assert smol.last_plan()["path"] == smol.PATH_GATHER
 
 
 @pytest.mark.parametrize("pad", [1, 3, 15])
@@ -156,14 +220,16 @@ def test_unaligned_offsets_and_pitch():
                             np.asarray([h for _, h in sizes], np.int32), 64, 56, 60, F32,
                             offsets=np.asarray(offs, np.int64),
                             pitches=np.asarray(pitches, np.int32))
-    for path in (smol.PATH_DIRECT, smol.PATH_LDS):
+    for path in (smol.PATH_DIRECT, smol.PATH_LDS, smol.PATH_GATHER):
         smol.set_tuning(path=path)
         _check(wl)
 
 
-def test_src_ends_at_last_image():
+@pytest.mark.parametrize("path", [smol.PATH_AUTO, smol.PATH_GATHER])
+def test_src_ends_at_last_image(path):
     """src_bytes is exactly the packed size (odd), so the last rows' 16-byte
-    chunks straddle the end of the buffer."""
+    chunks and 8-byte windows straddle the end of the buffer."""
+    smol.set_tuning(path=path)
     wl = _rgb("tight-end", [(33, 21), (41, 20)], 16, 16, F32, seed=4)
     assert wl.src.size % 16 != 0
     _check(wl)
