@@ -167,15 +167,22 @@ int smol_image_geometry(int32_t width, int32_t height, int32_t yuv420, const smo
 
 /* Tuning and testing knobs, process-wide, applied to later calls. Zero in any
  * field means "automatic".
- *   path        1: always the direct-gather kernels (taps read from global
- *               memory); 2: always the LDS-staged kernels (a call whose
- *               source span cannot be staged then fails with
- *               SMOL_ERR_UNSUPPORTED); 0: LDS-staged whenever it fits
+ *   path        1: always the direct-gather kernels (one thread per output
+ *               pixel, taps read from global memory); 2: always the
+ *               LDS-staged kernels (a call whose source span cannot be staged
+ *               then fails with SMOL_ERR_UNSUPPORTED); 3: the persistent
+ *               register-gather RGB kernel, with per-image tap tables in LDS
+ *               (images whose last 8-byte source window reaches the end of
+ *               src, and YUV calls, use the direct kernel; a crop too wide
+ *               for the tap tables fails with SMOL_ERR_UNSUPPORTED);
+ *               0: automatic (RGB: register-gather when its tables fit,
+ *               else LDS-staged when the span fits, else direct; YUV: direct)
  *   band_rows   output rows per band in the LDS-staged kernels (1..64)
  *   lds_budget  bytes of LDS one workgroup may use (4096..163840, and at most
  *               the device's per-workgroup limit)
- *   workgroups_per_cu  resident single-wave workgroups per compute unit the
- *               persistent LDS-staged kernels are sized for (1..16) */
+ *   workgroups_per_cu  cap on the resident single-wave workgroups per
+ *               compute unit the persistent kernels (paths 2 and 3) are
+ *               sized for (1..16); by default as many as can be resident */
 typedef struct smol_tuning {
     int32_t path;
     int32_t band_rows;
@@ -189,14 +196,16 @@ typedef struct smol_tuning {
 int smol_set_tuning(const smol_tuning *t);
 
 /* How the calling thread's last successful batch call ran.
- *   path        1 direct-gather, 2 LDS-staged
+ *   path        1 direct-gather, 2 LDS-staged, 3 register-gather (the most
+ *               specialised kernel the call launched)
  *   band_rows   output rows per band (LDS-staged) or 0
- *   lds_bytes   dynamic LDS per workgroup
- *   launches    kernel launches the call made
+ *   lds_bytes   dynamic LDS per workgroup of that kernel
+ *   launches    kernel launches the call made (all kernels)
  *   uploaded_descriptors  1 if a per-image descriptor table was uploaded
  *               (ragged batch), 0 if the batch was uniform
- *   grid        workgroups launched
- *   work_items  bands (LDS-staged) or output pixels (direct) in the call */
+ *   grid        workgroups of that kernel's first launch (0 for direct)
+ *   work_items  of that launch: bands (LDS-staged), passes of 2048 output
+ *               pixels (register-gather) or output pixels (direct) */
 typedef struct smol_plan {
     int32_t path;
     int32_t band_rows;
