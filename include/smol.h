@@ -174,21 +174,34 @@ int smol_image_geometry(int32_t width, int32_t height, int32_t yuv420, const smo
  *               register-gather RGB kernel, with per-image tap tables in LDS
  *               (images whose last 8-byte source window reaches the end of
  *               src, and YUV calls, use the direct kernel; a crop too wide
- *               for the tap tables fails with SMOL_ERR_UNSUPPORTED);
- *               0: automatic (RGB: register-gather when its tables fit,
- *               else LDS-staged when the span fits, else direct; YUV: direct)
- *   band_rows   output rows per band in the LDS-staged kernels (1..64)
+ *               for the tap tables fails with SMOL_ERR_UNSUPPORTED); 4: the
+ *               row-streaming RGB kernel (crops up to 512 columns whose
+ *               source span plus 32 bytes is at most 4 KiB and fits the LDS
+ *               budget twice, else SMOL_ERR_UNSUPPORTED; images whose 16-byte
+ *               source chunks cross an end of src use the direct kernel);
+ *               0: automatic (RGB: row-streaming when it fits, else
+ *               register-gather when its tables fit, else LDS-staged when
+ *               the span fits, else direct; YUV: direct)
+ *   band_rows   output rows per band in the LDS-staged kernels (1..64); for
+ *               the row-streaming kernel, 1 or 2 sets how many output rows
+ *               ahead of the interpolated one each wave loads
  *   lds_budget  bytes of LDS one workgroup may use (4096..163840, and at most
  *               the device's per-workgroup limit)
- *   workgroups_per_cu  cap on the resident single-wave workgroups per
- *               compute unit the persistent kernels (paths 2 and 3) are
- *               sized for (1..16); by default as many as can be resident */
+ *   workgroups_per_cu  cap on the resident workgroups per compute unit
+ *               the persistent kernels (paths 2-4) are sized for (1..16);
+ *               by default as many as can be resident
+ *   exact       1: the row-streaming kernel evaluates every multiply, add
+ *               and the normalising division with its own fp32 rounding, in
+ *               the definition's order (bit-identical to a scalar fp32
+ *               evaluation; the other kernels always do); 0 (default): it
+ *               uses fused multiply-adds and 1/std, within 2e-6 of that */
 typedef struct smol_tuning {
     int32_t path;
     int32_t band_rows;
     int32_t lds_budget;
     int32_t workgroups_per_cu;
-    int32_t reserved[4];
+    int32_t exact;
+    int32_t reserved[3];
 } smol_tuning;
 
 /* Set the knobs (NULL resets to automatic). SMOL_ERR_INVALID_ARG if a field
@@ -196,8 +209,8 @@ typedef struct smol_tuning {
 int smol_set_tuning(const smol_tuning *t);
 
 /* How the calling thread's last successful batch call ran.
- *   path        1 direct-gather, 2 LDS-staged, 3 register-gather (the most
- *               specialised kernel the call launched)
+ *   path        1 direct-gather, 2 LDS-staged, 3 register-gather, 4 row
+ *               streaming (the most specialised kernel the call launched)
  *   band_rows   output rows per band (LDS-staged) or 0
  *   lds_bytes   dynamic LDS per workgroup of that kernel
  *   launches    kernel launches the call made (all kernels)
@@ -205,7 +218,8 @@ int smol_set_tuning(const smol_tuning *t);
  *               (ragged batch), 0 if the batch was uniform
  *   grid        workgroups of that kernel's first launch (0 for direct)
  *   work_items  of that launch: bands (LDS-staged), passes of 2048 output
- *               pixels (register-gather) or output pixels (direct) */
+ *               pixels (register-gather), output rows (row streaming) or
+ *               output pixels (direct) */
 typedef struct smol_plan {
     int32_t path;
     int32_t band_rows;

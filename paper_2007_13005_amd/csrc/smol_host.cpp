@@ -36,13 +36,17 @@ int fail(int code, const char *fmt, ...)
     return code;
 }
 
-std::atomic<int> g_path{0}, g_band_rows{0}, g_lds_budget{0}, g_wg_per_cu{0};
+std::atomic<int> g_path{0}, g_band_rows{0}, g_lds_budget{0}, g_wg_per_cu{0}, g_exact{0};
 
 constexpr int kDefaultLdsBudget = 64 * 1024;
 constexpr int kMaxBandRows = 64;
 constexpr int kMaxWorkgroupsPerCu = 16;
 constexpr int kDefaultBandRows = 2;
 constexpr int kGatherPassPixels = 2048;  // 256 threads x 4 pairs x 2 pixels
+// Row-streaming waves per compute unit for long staged rows (4 KiB chunk
+// groups): more waves would each walk fewer rows, and every wave pays its
+// column taps and one exposed load latency to start.
+constexpr int kRowsWavesPerCu = 8;
 
 // Per-device facts the planner needs, queried once.
 struct DeviceInfo {
@@ -272,7 +276,8 @@ hipError_t staging_reserve(Staging *st, size_t bytes)
 // ---------------------------------------------------------------------------
 
 struct Plan {
-    int path;  // smol::PATH_DIRECT, smol::PATH_LDS or smol::PATH_GATHER
+    int path;  // smol::PATH_DIRECT, _LDS, _GATHER or _ROWS
+    // R: output rows per band (LDS) or row-pair slots per wave (ROWS)
     int R;
     size_t lds_bytes;
     int grid;
@@ -340,7 +345,9 @@ void fill_norm(const smol_params *p, BatchArgs &a)
         // round twice).
         volatile float one = 1.0f;
         a.rcp[c] = one / p->std[c];
+        a.bias[c] = (float)(-(double)p->mean[c] / (double)p->std[c]);
     }
+    a.exact = g_exact.load();
 }
 
 int hip_fail(hipError_t e, const char *what)
@@ -377,11 +384,13 @@ int run_batch(const std::vector<Desc> &descs, size_t first, size_t count, int no
     if (pl.path != smol::PATH_DIRECT && pl.lds_bytes > (size_t)di.lds_per_block)
         return fail(SMOL_ERR_UNSUPPORTED, "LDS plan of %zu bytes exceeds the device's %d per "
                     "workgroup", pl.lds_bytes, di.lds_per_block);
-    if (pl.path == smol::PATH_LDS || pl.path == smol::PATH_GATHER) {
+    if (pl.path == smol::PATH_LDS || pl.path == smol::PATH_GATHER || pl.path == smol::PATH_ROWS) {
         int per_cu = 0;
         const int oc = pl.path == smol::PATH_LDS
                            ? smol::occupancy_rgb_lds(pl.f16, pl.lds_bytes, &per_cu)
-                           : smol::occupancy_rgb_gather(pl.f16, pl.lds_bytes, &per_cu);
+                       : pl.path == smol::PATH_GATHER
+                           ? smol::occupancy_rgb_gather(pl.f16, pl.lds_bytes, &per_cu)
+                           : smol::occupancy_rgb_rows(a, pl.f16, pl.lds_bytes, &per_cu);
         if (oc != (int)hipSuccess)
             return hip_fail((hipError_t)oc, "hipOccupancyMaxActiveBlocksPerMultiprocessor");
         if (per_cu < 1)
@@ -390,10 +399,13 @@ int run_batch(const std::vector<Desc> &descs, size_t first, size_t count, int no
         const int forced = g_wg_per_cu.load();
         if (forced > 0)
             per_cu = std::min(per_cu, forced);
-        items = pl.path == smol::PATH_LDS
-                    ? (long long)n * a.bands
-                    : (long long)n * (((long long)a.Ch * a.Cw + kGatherPassPixels - 1) /
-                                      kGatherPassPixels);
+        else if (pl.path == smol::PATH_ROWS && a.row_groups >= 4)
+            per_cu = std::min(per_cu, kRowsWavesPerCu);
+        items = pl.path == smol::PATH_LDS      ? (long long)n * a.bands
+                : pl.path == smol::PATH_ROWS ? (long long)n * a.Ch
+                                             : (long long)n * (((long long)a.Ch * a.Cw +
+                                                                kGatherPassPixels - 1) /
+                                                               kGatherPassPixels);
         pl.grid = (int)std::min<long long>(items, (long long)di.cus * per_cu);
         a.grid = pl.grid;
     } else {
@@ -540,6 +552,19 @@ int smol_preprocess_batch(const uint8_t *src, int64_t src_bytes, const int64_t *
         d.top = (int32_t)g.top;
         int64_t xf, xl;
         x_span(d, p->crop_w, &xf, &xl);
+        d.xf = (int32_t)xf;
+        d.span = (int32_t)std::min<int64_t>(3 * (xl - xf + 1), INT32_MAX);
+        {
+            // every 16-byte chunk holding a staged byte lies inside src
+            int64_t yf, yd, yd2, yl;
+            tap_index(g.top, H, g.Hr, &yf, &yd);
+            tap_index(g.top + p->crop_h - 1, H, g.Hr, &yd2, &yl);
+            const uintptr_t base = (uintptr_t)src + (uintptr_t)offsets[i] + 3 * (uintptr_t)xf;
+            const uintptr_t first = (base + (uintptr_t)yf * (uintptr_t)pitch) & ~(uintptr_t)15;
+            const uintptr_t last = base + (uintptr_t)yl * (uintptr_t)pitch + 3 * (uintptr_t)(xl - xf + 1);
+            const uintptr_t end = (last + 15) & ~(uintptr_t)15;
+            d.safe = first >= (uintptr_t)src && end <= (uintptr_t)src + (uintptr_t)src_bytes;
+        }
         max_span = std::max(max_span, 3 * (xl - xf + 1));
         inside[i] = offsets[i] + (H - 1) * pitch + 3 * xl + 8 <= src_bytes;
     }
@@ -572,6 +597,71 @@ int smol_preprocess_batch(const uint8_t *src, int64_t src_bytes, const int64_t *
     };
     // Register-gather path: the gather kernel for runs of images whose windows
     // lie inside src, the direct kernel for the others.
+    // Row-streaming path: the row-streaming kernel for runs of images whose
+    // staged chunks lie inside src, the direct kernel for the others.
+    {
+        int device = 0;
+        DeviceInfo di;
+        const bool have_dev =
+            hipGetDevice(&device) == hipSuccess && device_info(device, &di) == hipSuccess;
+        const int col_iters = p->crop_w <= 128 ? 1 : p->crop_w <= 256 ? 2 : 4;
+        // A staged row: up to 15 bytes before the span (16-byte aligned
+        // chunks), the span, and the 12-byte read of the last column's taps,
+        // in groups of 64 chunks (1 KiB).
+        const int64_t groups = (max_span + 32 + 1023) / 1024;
+        const int64_t lds_bytes = 2 * 1024 * (groups <= 1 ? 1 : groups <= 2 ? 2 : 4);
+        const int64_t budget = std::min<int64_t>(
+            have_dev ? di.lds_per_block : 65536,
+            g_lds_budget.load() > 0 ? g_lds_budget.load() : INT64_MAX);
+        bool any_safe = false, runs_ok = true;
+        size_t nruns = 0;
+        for (int32_t i = 0; i < n; ++i) {
+            any_safe = any_safe || descs[(size_t)i].safe;
+            nruns += (i == 0 || descs[(size_t)i].safe != descs[(size_t)i - 1].safe) ? 1 : 0;
+        }
+        runs_ok = nruns <= 3;
+        const bool rows_ok = have_dev && p->crop_w <= 128 * smol::kRowsMaxColIters &&
+                             groups <= smol::kRowsMaxGroups && lds_bytes <= budget;
+        if (forced == smol::PATH_ROWS && !rows_ok)
+            return fail(SMOL_ERR_UNSUPPORTED, "row-streaming path forced but the crop width or "
+                        "source span does not fit (crop_w <= %d, span + 32 <= %d bytes, "
+                        "%lld bytes of LDS)",
+                        128 * smol::kRowsMaxColIters, 1024 * smol::kRowsMaxGroups,
+                        (long long)lds_bytes);
+        if (rows_ok && (forced == smol::PATH_ROWS ||
+                        (forced == smol::PATH_AUTO && any_safe && runs_ok))) {
+            Plan pr{smol::PATH_ROWS, 0, (size_t)lds_bytes, 0, f16};
+            a.col_iters = col_iters;
+            a.row_groups = (int)(lds_bytes / 2048);
+            // Prefetch depth (band_rows 1 or 2 forces it): long staged rows
+            // keep one row in flight per wave, short ones two.
+            const int br = g_band_rows.load();
+            a.prefetch = br == 1 || br == 2 ? br : a.row_groups >= 4 ? 1 : 2;
+            auto rows = [f16](const BatchArgs &x, const Plan &q, void *s) {
+                return smol::launch_rgb_rows(x, f16, q.lds_bytes, s);
+            };
+            auto direct_run = [f16](const BatchArgs &x, const Plan &, void *s) {
+                return smol::launch_rgb_direct(x, f16, s);
+            };
+            for (int32_t b = 0; b < n;) {
+                int32_t e = b + 1;
+                while (e < n && descs[(size_t)e].safe == descs[(size_t)b].safe)
+                    ++e;
+                rc = descs[(size_t)b].safe
+                         ? run_batch(descs, (size_t)b, (size_t)(e - b), 1, a, pr, stream, rows,
+                                     &info)
+                         : run_batch(descs, (size_t)b, (size_t)(e - b), 1, a,
+                                     Plan{smol::PATH_DIRECT, 0, 0, 0, f16}, stream, direct_run,
+                                     &info);
+                if (rc)
+                    return rc;
+                b = e;
+            }
+            g_last_plan = info;
+            return SMOL_OK;
+        }
+    }
+
     Plan pg{smol::PATH_GATHER, 0, 0, 0, f16};
     const size_t head = align16((size_t)8 * p->crop_w);
     pg.lds_bytes = head + (size_t)20 * p->crop_h;  // column and row tap tables
@@ -755,9 +845,10 @@ int smol_set_tuning(const smol_tuning *t)
         g_band_rows = 0;
         g_lds_budget = 0;
         g_wg_per_cu = 0;
+        g_exact = 0;
         return SMOL_OK;
     }
-    if (t->path < 0 || t->path > 3)
+    if (t->path < 0 || t->path > 4)
         return fail(SMOL_ERR_INVALID_ARG, "path %d unknown", t->path);
     if (t->band_rows < 0 || t->band_rows > kMaxBandRows)
         return fail(SMOL_ERR_INVALID_ARG, "band_rows %d outside 0..%d", t->band_rows,
@@ -768,10 +859,13 @@ int smol_set_tuning(const smol_tuning *t)
     if (t->workgroups_per_cu < 0 || t->workgroups_per_cu > kMaxWorkgroupsPerCu)
         return fail(SMOL_ERR_INVALID_ARG, "workgroups_per_cu %d outside 0..%d",
                     t->workgroups_per_cu, kMaxWorkgroupsPerCu);
+    if (t->exact != 0 && t->exact != 1)
+        return fail(SMOL_ERR_INVALID_ARG, "exact %d is neither 0 nor 1", t->exact);
     g_path = t->path;
     g_band_rows = t->band_rows;
     g_lds_budget = t->lds_budget;
     g_wg_per_cu = t->workgroups_per_cu;
+    g_exact = t->exact;
     return SMOL_OK;
 }
 

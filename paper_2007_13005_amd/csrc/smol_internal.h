@@ -9,11 +9,15 @@ namespace smol {
 // Per-image descriptor, 64 bytes. For RGB input off[0] is the byte offset of
 // the first pixel; for I420 input off[0..2] are the Y, Cb and Cr plane offsets.
 // Wr/Hr are the resized sizes and left/top the crop offsets (host-computed
-// per image; per-element taps are computed by the kernels).
+// per image; per-element taps are computed by the kernels). xf is the first
+// source column any output pixel reads and span the bytes from that column's
+// first byte to the end of the last source column read; safe is 1 when every
+// 16-byte aligned chunk that holds a byte of a staged source row lies inside
+// src (RGB only).
 struct alignas(16) Desc {
     int64_t off[3];
-    int32_t W, H, pitch, Wr, Hr, left, top, pad0;
-    int32_t pad1[2];
+    int32_t W, H, pitch, Wr, Hr, left, top, xf;
+    int32_t span, safe;
 };
 static_assert(sizeof(Desc) == 64, "descriptor must be 64 bytes");
 
@@ -37,17 +41,29 @@ struct BatchArgs {
     int32_t img_base;    // index of this launch's first image in the output
     int32_t grid;        // workgroups of a persistent launch (LDS kernels)
     int32_t stage_bytes; // bytes of one of the two LDS buffers of a wave
+    int32_t row_groups;  // 1 KiB chunk groups per staged source row (row-streaming kernel)
+    int32_t col_iters;   // column pairs per lane: 1, 2 or 4 (row-streaming kernel)
+    int32_t prefetch;    // rows loaded ahead of the one interpolated: 1 or 2 (row streaming)
+    int32_t exact;       // 1: operation-by-operation fp32 arithmetic (row-streaming kernel)
     float mean[3];   // per channel, 0..255 units
     float stdv[3];
     float rcp[3];    // RN(1 / stdv), fp32
+    float bias[3];   // RN(-mean / stdv), fp32
 };
 
-enum Path { PATH_AUTO = 0, PATH_DIRECT = 1, PATH_LDS = 2, PATH_GATHER = 3 };
+enum Path { PATH_AUTO = 0, PATH_DIRECT = 1, PATH_LDS = 2, PATH_GATHER = 3, PATH_ROWS = 4 };
+
+// Row-streaming kernel limits: crops up to 2 * 64 * kRowsMaxColIters columns,
+// staged source rows (span + 32 bytes) up to kRowsMaxGroups KiB.
+constexpr int kRowsMaxColIters = 4;
+constexpr int kRowsMaxGroups = 4;
 
 // Launchers (smol_kernels.hip). Return a hipError_t as int.
 int launch_rgb_direct(const BatchArgs &a, int out_f16, void *stream);
 int launch_rgb_lds(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream);
 int launch_rgb_gather(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream);
+int launch_rgb_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream);
+int occupancy_rgb_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, int *blocks_per_cu);
 // Resident workgroups per compute unit for the persistent kernels.
 int occupancy_rgb_gather(int out_f16, size_t lds_bytes, int *blocks_per_cu);
 int occupancy_rgb_lds(int out_f16, size_t lds_bytes, int *blocks_per_cu);

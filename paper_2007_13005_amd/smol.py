@@ -27,6 +27,7 @@ PATH_AUTO = 0
 PATH_DIRECT = 1
 PATH_LDS = 2
 PATH_GATHER = 3
+PATH_ROWS = 4
 
 MAX_DIM = 65535
 MAX_RESIZED = 4194303
@@ -51,7 +52,7 @@ class Geometry(ctypes.Structure):
 class Tuning(ctypes.Structure):
     _fields_ = [("path", ctypes.c_int32), ("band_rows", ctypes.c_int32),
                 ("lds_budget", ctypes.c_int32), ("workgroups_per_cu", ctypes.c_int32),
-                ("reserved", ctypes.c_int32 * 4)]
+                ("exact", ctypes.c_int32), ("reserved", ctypes.c_int32 * 3)]
 
 
 class Plan(ctypes.Structure):
@@ -148,8 +149,8 @@ def image_geometry(width: int, height: int, params: Params, yuv420: bool = False
 
 
 def set_tuning(path: int = 0, band_rows: int = 0, lds_budget: int = 0,
-               workgroups_per_cu: int = 0) -> None:
-    t = Tuning(path, band_rows, lds_budget, workgroups_per_cu)
+               workgroups_per_cu: int = 0, exact: int = 0) -> None:
+    t = Tuning(path, band_rows, lds_budget, workgroups_per_cu, exact)
     _check(lib().smol_set_tuning(ctypes.byref(t)))
 
 

@@ -143,14 +143,17 @@ def test_yuv_validation_rejects():
 
 def test_tuning_validation():
     with pytest.raises(smol.SmolError):
-        smol.set_tuning(path=4)
+        smol.set_tuning(path=5)
     with pytest.raises(smol.SmolError):
         smol.set_tuning(band_rows=65)
     with pytest.raises(smol.SmolError):
         smol.set_tuning(lds_budget=100)
     with pytest.raises(smol.SmolError):
         smol.set_tuning(workgroups_per_cu=17)
+    with pytest.raises(smol.SmolError):
+        smol.set_tuning(exact=2)
     smol.set_tuning(path=1, band_rows=8, lds_budget=32768)
+    smol.set_tuning(path=4, exact=1)
     smol.reset_tuning()
 
 

@@ -42,16 +42,20 @@ def _check(wl, **kw):
 
 
 _FULL = {}
+_REF = {}
 
 
-def _full(cfg):
-    """Full-size workload, its oracle output and its GPU output (cached)."""
-    if cfg not in _FULL:
+def _full(cfg, exact=0):
+    """Full-size workload, its oracle output and its GPU output (cached), in
+    the default arithmetic or the operation-by-operation one."""
+    if (cfg, exact) not in _FULL:
         wl = synthetic.make(cfg)
-        ref = run_oracle(wl)
+        if cfg not in _REF:
+            _REF[cfg] = run_oracle(wl)
+        smol.set_tuning(exact=exact)
         got = run_gpu(wl)
-        _FULL[cfg] = (wl, ref, got, smol.last_plan())
-    return _FULL[cfg]
+        _FULL[(cfg, exact)] = (wl, _REF[cfg], got, smol.last_plan())
+    return _FULL[(cfg, exact)]
 
 
 @pytest.mark.parametrize("cfg", ["c1", "c2", "c3", "c4", "c5"])
@@ -60,16 +64,18 @@ def test_full_config_parity(cfg):
     stats = assert_parity(got, ref, wl.out_dtype, wl.name)
     note(f"    {cfg}: {stats} plan={plan}")
     if wl.kind == "rgb":
-        assert plan["path"] == smol.PATH_GATHER
+        assert plan["path"] == smol.PATH_ROWS
     assert plan["uploaded_descriptors"] == (1 if cfg == "c2" else 0)
 
 
 @pytest.mark.parametrize("cfg", ["c1", "c2", "c3", "c4", "c5"])
 def test_full_config_bit_exact(cfg):
-    """Stronger than the tolerance: the kernels evaluate the definition's
-    operations in its order with correctly rounded results, so every output
-    equals the oracle's bit for bit."""
-    wl, ref, got, _ = _full(cfg)
+    """Stronger than the tolerance: with exact arithmetic selected the kernels
+    evaluate the definition's operations in its order with correctly rounded
+    results, so every output equals the oracle's bit for bit."""
+    wl, ref, got, plan = _full(cfg, exact=1)
+    if wl.kind == "rgb":
+        assert plan["path"] == smol.PATH_ROWS
     np.testing.assert_array_equal(got.view(np.uint32 if wl.out_dtype == F32 else np.uint16),
                                   ref.view(np.uint32 if wl.out_dtype == F32 else np.uint16))
 
@@ -82,7 +88,8 @@ SMALL = {"c1": dict(n=6), "c2": dict(n=40), "c3": dict(n=24), "c4": dict(n=3), "
 
 
 @pytest.mark.parametrize("cfg", ["c1", "c2", "c3", "c4"])
-@pytest.mark.parametrize("path", [smol.PATH_DIRECT, smol.PATH_LDS, smol.PATH_GATHER])
+@pytest.mark.parametrize("path", [smol.PATH_DIRECT, smol.PATH_LDS, smol.PATH_GATHER,
+                                  smol.PATH_ROWS])
 def test_rgb_paths(cfg, path):
     smol.set_tuning(path=path)
     wl = synthetic.make(cfg, **SMALL[cfg])
@@ -99,6 +106,56 @@ def test_band_rows_with_ragged_tail(band_rows):
     wl.out_dtype = F32
     _check(wl)
     assert smol.last_plan()["band_rows"] == band_rows
+
+
+@pytest.mark.parametrize("dtype", [F32, F16])
+@pytest.mark.parametrize("sizes,S,C", [
+    ([(320, 240)] * 5, 256, 224),       # span 633 B: one 1 KiB chunk group per row
+    ([(900, 600), (700, 700)], 256, 224),  # spans 1.6-2.3 KiB: two groups
+    ([(1920, 1080)] * 3, 224, 224),     # span 3.2 KiB: four groups
+    ([(1200, 400)] * 2, 300, (60, 300)),  # crop 300 wide: four column iterations
+], ids=["g1", "g2", "g4", "j4"])
+def test_row_streaming_chunk_groups(sizes, S, C, dtype):
+    """Staged rows of one, two and four 1 KiB chunk groups, crops needing one
+    to four column iterations per lane."""
+    smol.set_tuning(path=smol.PATH_ROWS)
+    _check(_rgb("groups", sizes, S, C, dtype, seed=11))
+    assert smol.last_plan()["path"] == smol.PATH_ROWS
+
+
+@pytest.mark.parametrize("prefetch", [1, 2])
+@pytest.mark.parametrize("cfg", ["c2", "c4"])
+def test_row_streaming_prefetch_depths(cfg, prefetch):
+    """One or two output rows loaded ahead of the interpolated one."""
+    smol.set_tuning(path=smol.PATH_ROWS, band_rows=prefetch)
+    _check(synthetic.make(cfg, n=7 if cfg == "c2" else 3))
+    assert smol.last_plan()["path"] == smol.PATH_ROWS
+
+
+def test_row_streaming_small_lds_budget():
+    """A 1080p span needs 8 KiB of LDS: a 4 KiB budget refuses the forced
+    row-streaming plan, the automatic plan takes another kernel."""
+    wl = _rgb("budget", [(1920, 1080)] * 2, 224, 224, F16, seed=2)
+    smol.set_tuning(path=smol.PATH_ROWS, lds_budget=4096)
+    with pytest.raises(smol.SmolError):
+        run_gpu(wl)
+    smol.set_tuning(lds_budget=4096)
+    _check(wl)
+    assert smol.last_plan()["path"] != smol.PATH_ROWS
+
+
+@pytest.mark.parametrize("wg", [1, 2, 5])
+def test_row_streaming_few_waves(wg):
+    """Few resident waves: each wave walks many rows and several images."""
+    smol.set_tuning(path=smol.PATH_ROWS, workgroups_per_cu=wg)
+    _check(synthetic.c2(n=30))
+
+
+def test_row_streaming_single_row_ranges():
+    """More waves than rows: ranges of one row (the prologue's second load
+    repeats the first row)."""
+    smol.set_tuning(path=smol.PATH_ROWS)
+    _check(_rgb("one-row", [(64, 48)], 8, (3, 8), F32, seed=12))
 
 
 def test_c2_aligned_offsets_variant():
@@ -143,20 +200,33 @@ EDGE = [
 
 
 @pytest.mark.parametrize("dtype", [F32, F16])
-@pytest.mark.parametrize("path", [smol.PATH_DIRECT, smol.PATH_AUTO, smol.PATH_GATHER])
+@pytest.mark.parametrize("path", [smol.PATH_DIRECT, smol.PATH_AUTO, smol.PATH_GATHER,
+                                  smol.PATH_ROWS])
 @pytest.mark.parametrize("name,sizes,S,C", EDGE, ids=[e[0] for e in EDGE])
 def test_rgb_edge_cases(name, sizes, S, C, path, dtype):
     smol.set_tuning(path=path)
     _check(_rgb(name, sizes, S, C, dtype, seed=len(name)))
 
 
-@pytest.mark.parametrize("path", [smol.PATH_AUTO, smol.PATH_LDS])
+@pytest.mark.parametrize("dtype", [F32, F16])
+@pytest.mark.parametrize("name,sizes,S,C", EDGE, ids=[e[0] for e in EDGE])
+def test_row_streaming_exact_edge_cases(name, sizes, S, C, dtype):
+    """Exact arithmetic in the row-streaming kernel: bit-identical to the
+    oracle on every edge case."""
+    smol.set_tuning(path=smol.PATH_ROWS, exact=1)
+    got, ref = _check(_rgb(name, sizes, S, C, dtype, seed=len(name)))
+    np.testing.assert_array_equal(got.view(np.uint32 if dtype == F32 else np.uint16),
+                                  ref.view(np.uint32 if dtype == F32 else np.uint16))
+
+
+@pytest.mark.parametrize("path", [smol.PATH_AUTO, smol.PATH_LDS, smol.PATH_ROWS])
 def test_wide_spans(path):
-    """A crop span too wide to stage in LDS: the LDS planner falls back to the
-    direct-gather kernel; the register-gather kernel handles it directly."""
+    """A crop span too wide to stage in LDS, and wider than the row-streaming
+    kernel's 512 columns: forced LDS or row-streaming plans are refused, the
+    automatic plan uses the register-gather kernel."""
     smol.set_tuning(path=path)
     wl = _rgb("wide-span", [(20000, 100), (15000, 100)], 100, (2, 12000), F16, seed=3)
-    if path == smol.PATH_LDS:
+    if path in (smol.PATH_LDS, smol.PATH_ROWS):
         with pytest.raises(smol.SmolError):
             run_gpu(wl)
         smol.set_tuning(path=smol.PATH_AUTO)
@@ -178,13 +248,14 @@ def test_crop_too_wide_for_gather_tables():
 def test_gather_prefix_with_direct_tail():
     """In a packed batch the last image's 8-byte windows reach the end of src:
     the gather kernel takes the others and the direct kernel that one."""
+    smol.set_tuning(path=smol.PATH_GATHER)
     wl = _rgb("tail", [(128, 128)] * 5, 224, 224, F16, seed=5)
     _check(wl)
     plan = smol.last_plan()
     assert plan["path"] == smol.PATH_GATHER and plan["launches"] == 2
 
 
-@pytest.mark.parametrize("path", [smol.PATH_AUTO, smol.PATH_GATHER])
+@pytest.mark.parametrize("path", [smol.PATH_AUTO, smol.PATH_GATHER, smol.PATH_ROWS])
 def test_image_at_end_of_src_first_in_batch(path):
     """Batch order is the reverse of memory order, so the image whose windows
     reach the end of src comes first: gather and direct launches interleave."""
@@ -194,7 +265,7 @@ def test_image_at_end_of_src_first_in_batch(path):
     wl = dataclasses.replace(fwd, widths=fwd.widths[::-1].copy(),
                              heights=fwd.heights[::-1].copy(), offsets=fwd.offsets[::-1].copy())
     _check(wl)
-    assert smol.last_plan()["path"] == smol.PATH_GATHER
+    assert smol.last_plan()["path"] == (smol.PATH_ROWS if path == smol.PATH_AUTO else path)
 
 
 @pytest.mark.parametrize("pad", [1, 3, 15])
@@ -220,12 +291,12 @@ def test_unaligned_offsets_and_pitch():
                             np.asarray([h for _, h in sizes], np.int32), 64, 56, 60, F32,
                             offsets=np.asarray(offs, np.int64),
                             pitches=np.asarray(pitches, np.int32))
-    for path in (smol.PATH_DIRECT, smol.PATH_LDS, smol.PATH_GATHER):
+    for path in (smol.PATH_DIRECT, smol.PATH_LDS, smol.PATH_GATHER, smol.PATH_ROWS):
         smol.set_tuning(path=path)
         _check(wl)
 
 
-@pytest.mark.parametrize("path", [smol.PATH_AUTO, smol.PATH_GATHER])
+@pytest.mark.parametrize("path", [smol.PATH_AUTO, smol.PATH_GATHER, smol.PATH_ROWS])
 def test_src_ends_at_last_image(path):
     """src_bytes is exactly the packed size (odd), so the last rows' 16-byte
     chunks and 8-byte windows straddle the end of the buffer."""
