@@ -384,13 +384,16 @@ int run_batch(const std::vector<Desc> &descs, size_t first, size_t count, int no
     if (pl.path != smol::PATH_DIRECT && pl.lds_bytes > (size_t)di.lds_per_block)
         return fail(SMOL_ERR_UNSUPPORTED, "LDS plan of %zu bytes exceeds the device's %d per "
                     "workgroup", pl.lds_bytes, di.lds_per_block);
-    if (pl.path == smol::PATH_LDS || pl.path == smol::PATH_GATHER || pl.path == smol::PATH_ROWS) {
+    const bool rows = pl.path == smol::PATH_ROWS || pl.path == smol::PATH_YUV_ROWS;
+    if (pl.path == smol::PATH_LDS || pl.path == smol::PATH_GATHER || rows) {
         int per_cu = 0;
         const int oc = pl.path == smol::PATH_LDS
                            ? smol::occupancy_rgb_lds(pl.f16, pl.lds_bytes, &per_cu)
                        : pl.path == smol::PATH_GATHER
                            ? smol::occupancy_rgb_gather(pl.f16, pl.lds_bytes, &per_cu)
-                           : smol::occupancy_rgb_rows(a, pl.f16, pl.lds_bytes, &per_cu);
+                       : pl.path == smol::PATH_ROWS
+                           ? smol::occupancy_rgb_rows(a, pl.f16, pl.lds_bytes, &per_cu)
+                           : smol::occupancy_yuv_rows(a, pl.f16, pl.lds_bytes, &per_cu);
         if (oc != (int)hipSuccess)
             return hip_fail((hipError_t)oc, "hipOccupancyMaxActiveBlocksPerMultiprocessor");
         if (per_cu < 1)
@@ -401,8 +404,8 @@ int run_batch(const std::vector<Desc> &descs, size_t first, size_t count, int no
             per_cu = std::min(per_cu, forced);
         else if (pl.path == smol::PATH_ROWS && a.row_groups >= 4)
             per_cu = std::min(per_cu, kRowsWavesPerCu);
-        items = pl.path == smol::PATH_LDS      ? (long long)n * a.bands
-                : pl.path == smol::PATH_ROWS ? (long long)n * a.Ch
+        items = pl.path == smol::PATH_LDS ? (long long)n * a.bands
+                : rows                    ? (long long)n * a.Ch
                                              : (long long)n * (((long long)a.Ch * a.Cw +
                                                                 kGatherPassPixels - 1) /
                                                                kGatherPassPixels);
@@ -415,7 +418,7 @@ int run_batch(const std::vector<Desc> &descs, size_t first, size_t count, int no
 
     // The plan reports the first launch of the most specialised kernel.
     if (info->launches == 0 || (info->path == smol::PATH_DIRECT && pl.path != smol::PATH_DIRECT)) {
-        info->path = pl.path;
+        info->path = pl.path == smol::PATH_YUV_ROWS ? smol::PATH_ROWS : pl.path;
         info->band_rows = pl.path == smol::PATH_LDS ? pl.R : 0;
         info->lds_bytes = (int)pl.lds_bytes;
         info->grid = pl.grid;
@@ -727,6 +730,7 @@ int smol_yuv420_preprocess_batch(const uint8_t *src, int64_t src_bytes, const in
         return fail(SMOL_ERR_INVALID_ARG, "an offset table, widths or heights is NULL");
 
     std::vector<Desc> descs((size_t)n);
+    int64_t max_yspan = 0, max_cspan = 0;
     for (int32_t i = 0; i < n; ++i) {
         Geo g;
         rc = image_geo(widths[i], heights[i], p, &g, i);
@@ -751,6 +755,23 @@ int smol_yuv420_preprocess_batch(const uint8_t *src, int64_t src_bytes, const in
         d.Hr = (int32_t)g.Hr;
         d.left = (int32_t)g.left;
         d.top = (int32_t)g.top;
+        int64_t xf, xl, c0, c1, e0, e1;
+        x_span(d, p->crop_w, &xf, &xl);
+        chroma_index(xf, (W + 1) / 2, &c0, &c1);
+        chroma_index(xl, (W + 1) / 2, &e0, &e1);
+        d.xf = (int32_t)xf;
+        d.span = (int32_t)(xl - xf + 1);
+        max_yspan = std::max(max_yspan, xl - xf + 1);
+        max_cspan = std::max(max_cspan, e1 - c0 + 1);
+        // every 16-byte chunk of every plane lies inside src
+        bool safe = true;
+        for (int k = 0; k < 3; ++k) {
+            const uintptr_t b = (uintptr_t)src + (uintptr_t)offs[k];
+            safe = safe && (b & ~(uintptr_t)15) >= (uintptr_t)src &&
+                   ((b + (uintptr_t)sizes[k] + 15) & ~(uintptr_t)15) <=
+                       (uintptr_t)src + (uintptr_t)src_bytes;
+        }
+        d.safe = safe;
     }
     BatchArgs a;
     std::memset(&a, 0, sizeof a);
@@ -760,16 +781,46 @@ int smol_yuv420_preprocess_batch(const uint8_t *src, int64_t src_bytes, const in
     a.Ch = p->crop_h;
     a.Cw = p->crop_w;
     fill_norm(p, a);
-    if (g_path.load() == smol::PATH_LDS)
-        return fail(SMOL_ERR_UNSUPPORTED, "no LDS-staged I420 kernel in this build");
+    const int forced = g_path.load();
+    if (forced == smol::PATH_LDS || forced == smol::PATH_GATHER)
+        return fail(SMOL_ERR_UNSUPPORTED, "no LDS-staged or register-gather I420 kernel");
     const int f16 = p->out_dtype == SMOL_OUT_F16;
-    Plan pl{smol::PATH_DIRECT, 0, 0, 0, f16};
     smol_plan info = {};
-    rc = run_batch(descs, 0, (size_t)n, 3, a, pl, stream,
-                   [f16](const BatchArgs &x, const Plan &, void *s) {
-                       return smol::launch_yuv_direct(x, f16, s);
-                   },
-                   &info);
+    auto direct = [f16](const BatchArgs &x, const Plan &, void *s) {
+        return smol::launch_yuv_direct(x, f16, s);
+    };
+    // Row-streaming kernel: staged luma and chroma rows of at most 1 KiB
+    // (span + 32 bytes), crops up to 512 columns; frames whose planes' chunks
+    // cross an end of src go to the direct kernel.
+    const bool rows_ok = p->crop_w <= 128 * smol::kRowsMaxColIters && max_yspan + 32 <= 1024 &&
+                         max_cspan + 32 <= 1024;
+    if (forced == smol::PATH_ROWS && !rows_ok)
+        return fail(SMOL_ERR_UNSUPPORTED, "row-streaming I420 path forced but the crop is wider "
+                    "than %d columns or a source span exceeds 992 bytes",
+                    128 * smol::kRowsMaxColIters);
+    if (rows_ok && (forced == smol::PATH_ROWS || forced == smol::PATH_AUTO)) {
+        a.col_iters = p->crop_w <= 128 ? 1 : p->crop_w <= 256 ? 2 : 4;
+        const Plan pr{smol::PATH_YUV_ROWS, 0, 8 * 1024, 0, f16};
+        auto rows = [f16](const BatchArgs &x, const Plan &q, void *s) {
+            return smol::launch_yuv_rows(x, f16, q.lds_bytes, s);
+        };
+        for (int32_t b = 0; b < n;) {
+            int32_t e = b + 1;
+            while (e < n && descs[(size_t)e].safe == descs[(size_t)b].safe)
+                ++e;
+            rc = descs[(size_t)b].safe
+                     ? run_batch(descs, (size_t)b, (size_t)(e - b), 3, a, pr, stream, rows, &info)
+                     : run_batch(descs, (size_t)b, (size_t)(e - b), 3, a,
+                                 Plan{smol::PATH_DIRECT, 0, 0, 0, f16}, stream, direct, &info);
+            if (rc)
+                return rc;
+            b = e;
+        }
+        g_last_plan = info;
+        return SMOL_OK;
+    }
+    rc = run_batch(descs, 0, (size_t)n, 3, a, Plan{smol::PATH_DIRECT, 0, 0, 0, f16}, stream,
+                   direct, &info);
     if (!rc)
         g_last_plan = info;
     return rc;

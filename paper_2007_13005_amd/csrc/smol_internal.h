@@ -53,6 +53,9 @@ struct BatchArgs {
 
 enum Path { PATH_AUTO = 0, PATH_DIRECT = 1, PATH_LDS = 2, PATH_GATHER = 3, PATH_ROWS = 4 };
 
+// Pseudo path of the I420 row-streaming kernel in run_batch (reported as PATH_ROWS).
+constexpr int PATH_YUV_ROWS = 5;
+
 // Row-streaming kernel limits: crops up to 2 * 64 * kRowsMaxColIters columns,
 // staged source rows (span + 32 bytes) up to kRowsMaxGroups KiB.
 constexpr int kRowsMaxColIters = 4;
@@ -68,6 +71,7 @@ int occupancy_rgb_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, int *b
 int occupancy_rgb_gather(int out_f16, size_t lds_bytes, int *blocks_per_cu);
 int occupancy_rgb_lds(int out_f16, size_t lds_bytes, int *blocks_per_cu);
 int launch_yuv_direct(const BatchArgs &a, int out_f16, void *stream);
-int launch_yuv_lds(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream);
+int launch_yuv_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream);
+int occupancy_yuv_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, int *blocks_per_cu);
 
 }  // namespace smol

@@ -1291,6 +1291,398 @@ __global__ void __launch_bounds__(64) rgb_rows_kernel(BatchArgs a)
 }
 
 // ---------------------------------------------------------------------------
+// I420, row streaming: one wave per workgroup, the scheme of the RGB kernel.
+//
+// For each output row the wave loads eight row segments into registers and
+// then into its LDS slot (1 KiB each): luma rows y0 and y1 over the crop's
+// luma column span and, for each chroma plane, the chroma rows that the
+// vertical chroma taps of y0 and y1 read over the matching chroma span. Those
+// are at most three rows: the first chroma row of y1 is always one of the two
+// of y0 (y1 = y0 + 1 or the clamped y0).
+//
+// Every luma tap is converted as defined: chroma bilinear at centred siting,
+// BT.601 full range, clamp; then the four converted taps are interpolated
+// and normalised. The chroma weights are 0, 1/4 and 3/4, so each chroma
+// interpolation step is exact in fp32 (multiples of 1/16 below 256) and a
+// fused multiply-add gives the value the separately rounded form gives.
+//
+// Lane l computes output columns c = 2l + 128j and c + 1 (j < J). Per column
+// it keeps: the luma tap (offset of x0 in the staged luma span, weight), and
+// for its two luma columns x0, x1 the chroma taps as the offset of the first
+// chroma column they read and a byte selector that picks the chroma samples
+// (x0's pair, x1's pair) out of the four bytes read there.
+// ---------------------------------------------------------------------------
+struct YuvImg {
+    long long off[3];
+    int W, H, Wr, Hr, left, top, xf, span;
+};
+
+__device__ __forceinline__ YuvImg yuv_img(const BatchArgs &a, int img)
+{
+    YuvImg g;
+    if (a.table) {
+        const ConstDesc *t = (const ConstDesc *)a.table + img;
+        g.off[0] = t->off[0];
+        g.off[1] = t->off[1];
+        g.off[2] = t->off[2];
+        g.W = t->W;
+        g.H = t->H;
+        g.Wr = t->Wr;
+        g.Hr = t->Hr;
+        g.left = t->left;
+        g.top = t->top;
+        g.xf = t->xf;
+        g.span = t->span;
+    } else {
+        g.off[0] = a.uni.off[0] + (long long)img * a.stride;
+        g.off[1] = a.uni.off[1] + (long long)img * a.stride;
+        g.off[2] = a.uni.off[2] + (long long)img * a.stride;
+        g.W = a.uni.W;
+        g.H = a.uni.H;
+        g.Wr = a.uni.Wr;
+        g.Hr = a.uni.Hr;
+        g.left = a.uni.left;
+        g.top = a.uni.top;
+        g.xf = a.uni.xf;
+        g.span = a.uni.span;
+    }
+    return g;
+}
+
+// Load cursor over the output rows of I420 frames.
+struct YuvCursor {
+    int img, rr;
+    VCursor v;               // luma vertical map
+    uintptr_t base[3];       // first staged byte of row 0 of Y, Cb, Cr
+    int W, Wc, Hc, yspan, cspan;
+};
+
+__device__ __forceinline__ void yuv_cursor_image(YuvCursor &c, const BatchArgs &a, int img, int rr)
+{
+    const YuvImg g = yuv_img(a, img);
+    c.img = img;
+    c.rr = rr;
+    VCursor v;
+    v.H = g.H;
+    v.den = 2 * g.Hr;
+    const long long n = (long long)(2 * (g.top + rr) + 1) * g.H - g.Hr;
+    const long long q = n >= 0 ? n / v.den : -((-n + v.den - 1) / v.den);
+    v.q = (int)q;
+    v.rem = (int)(n - q * v.den);
+    v.qs = (2 * g.H) / v.den;
+    v.rs = 2 * g.H - v.qs * v.den;
+    c.v = v;
+    c.W = g.W;
+    c.Wc = (g.W + 1) >> 1;
+    c.Hc = (g.H + 1) >> 1;
+    const int xl = g.xf + g.span - 1;
+    const int cxf = chroma_tap(g.xf, c.Wc).x0;
+    const int cxl = chroma_tap(xl, c.Wc).x1;
+    c.yspan = g.span;
+    c.cspan = cxl - cxf + 1;
+    c.base[0] = (uintptr_t)(a.src + g.off[0]) + (uintptr_t)g.xf;
+    c.base[1] = (uintptr_t)(a.src + g.off[1]) + (uintptr_t)cxf;
+    c.base[2] = (uintptr_t)(a.src + g.off[2]) + (uintptr_t)cxf;
+}
+
+__device__ __forceinline__ void yuv_cursor_next(YuvCursor &c, const BatchArgs &a)
+{
+    vcursor_next(c.v);
+    if (++c.rr == a.Ch && c.img + 1 < a.n)
+        yuv_cursor_image(c, a, c.img + 1, 0);
+}
+
+// One output row's eight segments in registers: Y y0, Y y1, Cb r0, Cb r1,
+// Cb r2, Cr r0, Cr r1, Cr r2 (r0, r1: the chroma rows of y0; r2: the second
+// chroma row of y1), with each segment's offset in its first chunk, the luma
+// vertical weight, the chroma vertical weights of y0 and y1, and which of r0,
+// r1 is y1's first chroma row.
+struct YuvStaged {
+    u32x4 c[8];
+    int sh[8];
+    float wy, wc0, wc1;
+    int b0;
+};
+
+__device__ __forceinline__ void yuv_load(YuvStaged &st, const YuvCursor &c, int lane)
+{
+    int y0, y1;
+    vcursor_tap(c.v, y0, y1, st.wy);
+    const Tap t0 = chroma_tap(y0, c.Hc), t1 = chroma_tap(y1, c.Hc);
+    st.wc0 = t0.w;
+    st.wc1 = t1.w;
+    st.b0 = t1.x0 == t0.x0 ? 0 : 1;
+    const uintptr_t row[8] = {
+        c.base[0] + (uintptr_t)y0 * (uintptr_t)c.W,   c.base[0] + (uintptr_t)y1 * (uintptr_t)c.W,
+        c.base[1] + (uintptr_t)t0.x0 * (uintptr_t)c.Wc, c.base[1] + (uintptr_t)t0.x1 * (uintptr_t)c.Wc,
+        c.base[1] + (uintptr_t)t1.x1 * (uintptr_t)c.Wc, c.base[2] + (uintptr_t)t0.x0 * (uintptr_t)c.Wc,
+        c.base[2] + (uintptr_t)t0.x1 * (uintptr_t)c.Wc, c.base[2] + (uintptr_t)t1.x1 * (uintptr_t)c.Wc};
+    typedef __attribute__((address_space(1))) const uint8_t GlobalByte;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+        st.sh[s] = (int)(row[s] & 15);
+        const int last = (st.sh[s] + (s < 2 ? c.yspan : c.cspan) - 1) >> 4;
+        GlobalByte *p = (GlobalByte *)(row[s] - (uintptr_t)st.sh[s]);
+        st.c[s] = __builtin_nontemporal_load(
+            (const __attribute__((address_space(1))) u32x4 *)(p + 16u * (uint32_t)min(lane, last)));
+    }
+}
+
+__device__ __forceinline__ void yuv_write(uint8_t *slot, const YuvStaged &st, int lane)
+{
+#pragma unroll
+    for (int s = 0; s < 8; ++s)
+        ((u32x4 *)(slot + 1024 * s))[lane] = st.c[s];
+}
+
+// Per-lane column taps of the I420 kernel.
+template <int J>
+struct YuvCols {
+    int ox[J][2];        // luma x0 - xf
+    float wx[J][2];      // luma weight
+    int oc[J][2];        // first chroma column read - cxf
+    uint32_t sel[J][2];  // v_perm selector: bytes (x0 pair, x1 pair) of the 4 read
+    float wc0[J][2], wc1[J][2];  // chroma weights of luma columns x0 and x1
+};
+
+template <int J>
+__device__ __forceinline__ void yuv_cols(YuvCols<J> &k, const YuvImg &g, int Cw, int lane)
+{
+    const int Wc = (g.W + 1) >> 1;
+    const int cxf = chroma_tap(g.xf, Wc).x0;
+#pragma unroll
+    for (int j = 0; j < J; ++j)
+#pragma unroll
+        for (int px = 0; px < 2; ++px) {
+            const int c = min(2 * lane + 128 * j + px, Cw - 1);
+            const Tap t = axis_tap(g.left + c, g.W, g.Wr);
+            const Tap a0 = chroma_tap(t.x0, Wc), a1 = chroma_tap(t.x1, Wc);
+            k.ox[j][px] = t.x0 - g.xf;
+            k.wx[j][px] = t.w;
+            k.oc[j][px] = a0.x0 - cxf;
+            k.sel[j][px] = (uint32_t)(a0.x1 - a0.x0) << 8 | (uint32_t)(a1.x0 - a0.x0) << 16 |
+                           (uint32_t)(a1.x1 - a0.x0) << 24;
+            k.wc0[j][px] = a0.w;
+            k.wc1[j][px] = a1.w;
+        }
+}
+
+// Dword-aligned reads of N byte groups (at LDS byte addresses A), realigned:
+// bytes A .. A + 3 of each group.
+template <int N>
+__device__ __forceinline__ void lds_read_quads(const uint32_t (&A)[N], uint32_t (&q)[N]);
+
+#define SMOL_RD2(D, A) "ds_read2_b32 " D ", " A " offset1:1\n\t"
+template <>
+__device__ __forceinline__ void lds_read_quads<8>(const uint32_t (&A)[8], uint32_t (&q)[8])
+{
+    uint32_t ad[8];
+    u32x2 d[8];
+#pragma unroll
+    for (int t = 0; t < 8; ++t)
+        ad[t] = A[t] & ~3u;
+    asm volatile(SMOL_RD2("%0", "%8") SMOL_RD2("%1", "%9") SMOL_RD2("%2", "%10")
+                 SMOL_RD2("%3", "%11") SMOL_RD2("%4", "%12") SMOL_RD2("%5", "%13")
+                 SMOL_RD2("%6", "%14") SMOL_RD2("%7", "%15") "s_waitcnt lgkmcnt(0)"
+                 : "=&v"(d[0]), "=&v"(d[1]), "=&v"(d[2]), "=&v"(d[3]), "=&v"(d[4]),
+                   "=&v"(d[5]), "=&v"(d[6]), "=&v"(d[7])
+                 : "v"(ad[0]), "v"(ad[1]), "v"(ad[2]), "v"(ad[3]), "v"(ad[4]), "v"(ad[5]),
+                   "v"(ad[6]), "v"(ad[7])
+                 : "memory");
+#pragma unroll
+    for (int t = 0; t < 8; ++t)
+        q[t] = __builtin_amdgcn_alignbyte(d[t].y, d[t].x, A[t]);
+}
+#undef SMOL_RD2
+
+// Chroma of luma columns x0, x1 at one chroma row: (horizontal lerps).
+__device__ __forceinline__ void chroma_h(uint32_t quad, uint32_t sel, float w0, float w1, float &h0,
+                                         float &h1)
+{
+    const uint32_t b = __builtin_amdgcn_perm(0u, quad, sel);  // x0 pair, x1 pair
+    const float a0 = cvt_ubyte0(b), a1 = cvt_ubyte2(b);
+    h0 = fmaf(w0, cvt_ubyte1(b) - a0, a0);  // exact (see above)
+    h1 = fmaf(w1, cvt_ubyte3(b) - a1, a1);
+}
+
+template <int F16, int J, int EXACT>
+__device__ __forceinline__ void yuv_compute(const BatchArgs &a, const NormK &nk, uint8_t *orow,
+                                            uint32_t slot, const int (&sh)[8], float wy,
+                                            float wc0, float wc1, int b0, const YuvCols<J> &k,
+                                            int lane)
+{
+    const int Cw = a.Cw;
+    constexpr int kEsz = F16 ? 2 : 4;
+    const long long plane = (long long)a.Ch * Cw * kEsz;
+    const bool pairs = (Cw & 1) == 0;
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+        float o[3][2];
+#pragma unroll
+        for (int px = 0; px < 2; ++px) {
+            // reads: Y y0, Y y1, Cb r0..r2, Cr r0..r2
+            uint32_t A[8], q[8];
+#pragma unroll
+            for (int s = 0; s < 8; ++s)
+                A[s] = slot + 1024u * s + (uint32_t)sh[s] +
+                       (uint32_t)(s < 2 ? k.ox[j][px] : k.oc[j][px]);
+            lds_read_quads<8>(A, q);
+            // chroma at (x0, x1) x (y0, y1) for both planes
+            float cc[2][2][2];  // [plane][luma row][luma col]
+#pragma unroll
+            for (int pl = 0; pl < 2; ++pl) {
+                float h[3][2];
+#pragma unroll
+                for (int r = 0; r < 3; ++r)
+                    chroma_h(q[2 + 3 * pl + r], k.sel[j][px], k.wc0[j][px], k.wc1[j][px], h[r][0],
+                             h[r][1]);
+#pragma unroll
+                for (int xi = 0; xi < 2; ++xi) {
+                    cc[pl][0][xi] = fmaf(wc0, h[1][xi] - h[0][xi], h[0][xi]);
+                    const float hb = b0 ? h[1][xi] : h[0][xi];
+                    cc[pl][1][xi] = fmaf(wc1, h[2][xi] - hb, hb);
+                }
+            }
+            float rgb[2][2][3];  // [luma row][luma col][channel]
+#pragma unroll
+            for (int yi = 0; yi < 2; ++yi)
+#pragma unroll
+                for (int xi = 0; xi < 2; ++xi) {
+                    const float Y = xi ? cvt_ubyte1(q[yi]) : cvt_ubyte0(q[yi]);
+                    ycbcr_to_rgb(Y, cc[0][yi][xi], cc[1][yi][xi], rgb[yi][xi][0], rgb[yi][xi][1],
+                                 rgb[yi][xi][2]);
+                }
+#pragma unroll
+            for (int ch = 0; ch < 3; ++ch)
+                o[ch][px] = normalize_k<EXACT>(
+                    nk, ch,
+                    lerp(lerp(rgb[0][0][ch], rgb[0][1][ch], k.wx[j][px]),
+                         lerp(rgb[1][0][ch], rgb[1][1][ch], k.wx[j][px]), wy));
+        }
+        const int c = 2 * lane + 128 * j;
+        if (c < Cw) {
+            const uint32_t lo = (uint32_t)c * kEsz;
+            if (pairs) {
+#pragma unroll
+                for (int ch = 0; ch < 3; ++ch) {
+                    uint8_t *dst = orow + ch * plane + lo;
+                    if (F16 && !EXACT) {
+                        typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+                        const f16x2 h = {(_Float16)o[ch][0], (_Float16)o[ch][1]};
+                        __builtin_nontemporal_store(__builtin_bit_cast(uint32_t, h),
+                                                    (uint32_t *)dst);
+                    } else if (F16) {
+                        __builtin_nontemporal_store(f16_bits(o[ch][0]) | (f16_bits(o[ch][1]) << 16),
+                                                    (uint32_t *)dst);
+                    } else {
+                        typedef float f32x2 __attribute__((ext_vector_type(2)));
+                        const f32x2 w = {o[ch][0], o[ch][1]};
+                        __builtin_nontemporal_store(w, (f32x2 *)dst);
+                    }
+                }
+            } else {
+                const bool second = c + 1 < Cw;
+#pragma unroll
+                for (int ch = 0; ch < 3; ++ch) {
+                    uint8_t *dst = orow + ch * plane + lo;
+                    if (F16) {
+                        ((uint16_t *)dst)[0] = (uint16_t)f16_bits(o[ch][0]);
+                        if (second)
+                            ((uint16_t *)dst)[1] = (uint16_t)f16_bits(o[ch][1]);
+                    } else {
+                        ((float *)dst)[0] = o[ch][0];
+                        if (second)
+                            ((float *)dst)[1] = o[ch][1];
+                    }
+                }
+            }
+        }
+    }
+}
+
+template <int F16, int J, int EXACT>
+__global__ void __launch_bounds__(64) yuv_rows_kernel(BatchArgs a)
+{
+    extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+    const int lane = threadIdx.x;
+    const int Ch = a.Ch;
+    const long long T = (long long)a.n * Ch;
+    const long long r_begin = T * blockIdx.x / gridDim.x;
+    const long long r_end = T * (blockIdx.x + 1) / gridDim.x;
+    if (r_begin >= r_end)
+        return;
+    constexpr int kEsz = F16 ? 2 : 4;
+    const int n_rows = (int)(r_end - r_begin);
+    const int img0 = (int)(r_begin / Ch);
+    const int rr0 = (int)(r_begin - (long long)img0 * Ch);
+
+    YuvCursor lc;
+    yuv_cursor_image(lc, a, img0, rr0);
+    int c_img = img0, c_rr = rr0;
+    uint8_t *orow = (uint8_t *)a.out +
+                    ((long long)(a.img_base + c_img) * 3 * Ch + c_rr) * (long long)a.Cw * kEsz;
+    YuvCols<J> cols;
+    int cW, cWr, cleft;
+    {
+        const YuvImg g = yuv_img(a, img0);
+        yuv_cols<J>(cols, g, a.Cw, lane);
+        cW = g.W;
+        cWr = g.Wr;
+        cleft = g.left;
+    }
+    const NormK nk = norm_consts(a);
+    const uint32_t lds0 = lds_addr(lds);
+
+    // One register set: row k + 1 is loaded before row k is interpolated
+    // (the loads past the wave's last row repeat that row).
+    int lrow = 0;
+    YuvStaged R;
+    yuv_load(R, lc, lane);
+    if (lrow + 1 < n_rows) {
+        yuv_cursor_next(lc, a);
+        ++lrow;
+    }
+    yuv_write(lds, R, lane);
+    int csh[8];
+#pragma unroll
+    for (int s = 0; s < 8; ++s)
+        csh[s] = R.sh[s];
+    float cwy = R.wy, cwc0 = R.wc0, cwc1 = R.wc1;
+    int cb0 = R.b0;
+    for (int k = 0;;) {
+        yuv_load(R, lc, lane);
+        if (lrow + 1 < n_rows) {
+            yuv_cursor_next(lc, a);
+            ++lrow;
+        }
+        yuv_compute<F16, J, EXACT>(a, nk, orow, lds0, csh, cwy, cwc0, cwc1, cb0, cols, lane);
+        if (++k == n_rows)
+            break;
+        yuv_write(lds, R, lane);
+#pragma unroll
+        for (int s = 0; s < 8; ++s)
+            csh[s] = R.sh[s];
+        cwy = R.wy;
+        cwc0 = R.wc0;
+        cwc1 = R.wc1;
+        cb0 = R.b0;
+        orow += (long long)a.Cw * kEsz;
+        if (++c_rr == Ch) {
+            c_rr = 0;
+            ++c_img;
+            orow += 2 * (long long)Ch * a.Cw * kEsz;  // skip planes 1 and 2
+            const YuvImg g = yuv_img(a, c_img);
+            if (g.W != cW || g.Wr != cWr || g.left != cleft) {
+                cW = g.W;
+                cWr = g.Wr;
+                cleft = g.left;
+                yuv_cols<J>(cols, g, a.Cw, lane);
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // RGB, direct gather: one thread per output pixel, taps read from global
 // memory. Used when the crop's source span does not fit the LDS budget.
 // ---------------------------------------------------------------------------
@@ -1490,9 +1882,32 @@ int launch_yuv_direct(const BatchArgs &a, int out_f16, void *stream)
     return (int)hipGetLastError();
 }
 
-int launch_yuv_lds(const BatchArgs &, int, size_t, void *)
+template <int F16, int EXACT>
+const void *yuv_rows_kernel_e(int col_iters)
 {
-    return (int)hipErrorNotSupported;
+    return col_iters <= 1   ? (const void *)yuv_rows_kernel<F16, 1, EXACT>
+           : col_iters <= 2 ? (const void *)yuv_rows_kernel<F16, 2, EXACT>
+                            : (const void *)yuv_rows_kernel<F16, 4, EXACT>;
+}
+
+const void *yuv_rows_kernel_for(const BatchArgs &a, int f16)
+{
+    return f16 ? (a.exact ? yuv_rows_kernel_e<1, 1>(a.col_iters) : yuv_rows_kernel_e<1, 0>(a.col_iters))
+               : (a.exact ? yuv_rows_kernel_e<0, 1>(a.col_iters) : yuv_rows_kernel_e<0, 0>(a.col_iters));
+}
+
+int launch_yuv_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream)
+{
+    hipStream_t s = (hipStream_t)stream;
+    const dim3 grid((unsigned)a.grid), block(64);
+    void *args[] = {(void *)&a};
+    return (int)hipLaunchKernel(yuv_rows_kernel_for(a, out_f16), grid, block, args, lds_bytes, s);
+}
+
+int occupancy_yuv_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, int *blocks_per_cu)
+{
+    return (int)hipOccupancyMaxActiveBlocksPerMultiprocessor(
+        blocks_per_cu, yuv_rows_kernel_for(a, out_f16), 64, lds_bytes);
 }
 
 }  // namespace smol

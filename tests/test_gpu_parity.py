@@ -358,9 +358,49 @@ YUV_EDGE = [
 
 
 @pytest.mark.parametrize("dtype", [F32, F16])
+@pytest.mark.parametrize("path", [smol.PATH_AUTO, smol.PATH_DIRECT, smol.PATH_ROWS])
 @pytest.mark.parametrize("name,sizes,S,C", YUV_EDGE, ids=[e[0] for e in YUV_EDGE])
-def test_yuv_edge_cases(name, sizes, S, C, dtype):
+def test_yuv_edge_cases(name, sizes, S, C, path, dtype):
+    smol.set_tuning(path=path)
     _check(_yuv(name, sizes, S, C, dtype, seed=len(name)))
+
+
+@pytest.mark.parametrize("dtype", [F32, F16])
+@pytest.mark.parametrize("name,sizes,S,C", YUV_EDGE, ids=[e[0] for e in YUV_EDGE])
+def test_yuv_row_streaming_exact(name, sizes, S, C, dtype):
+    """Exact arithmetic in the I420 row-streaming kernel: bit-identical to the
+    oracle (the frames the direct kernel takes are exact as well)."""
+    smol.set_tuning(path=smol.PATH_ROWS, exact=1)
+    got, ref = _check(_yuv(name, sizes, S, C, dtype, seed=len(name)))
+    np.testing.assert_array_equal(got.view(np.uint32 if dtype == F32 else np.uint16),
+                                  ref.view(np.uint32 if dtype == F32 else np.uint16))
+
+
+@pytest.mark.parametrize("path", [smol.PATH_AUTO, smol.PATH_ROWS])
+def test_yuv_frame_at_end_of_src_first_in_batch(path):
+    """Batch order reverses memory order: the frame whose planes end at the
+    end of src comes first, so direct and row-streaming launches alternate."""
+    import dataclasses
+    smol.set_tuning(path=path)
+    fwd = _yuv("rev", [(96, 64), (130, 90), (64, 64)], 48, 40, F16, seed=9)
+    rev = lambda x: x[::-1].copy()
+    wl = dataclasses.replace(fwd, widths=rev(fwd.widths), heights=rev(fwd.heights),
+                             y_offsets=rev(fwd.y_offsets), cb_offsets=rev(fwd.cb_offsets),
+                             cr_offsets=rev(fwd.cr_offsets))
+    _check(wl)
+    assert smol.last_plan()["path"] == smol.PATH_ROWS
+
+
+def test_yuv_wide_span_uses_direct_kernel():
+    """A luma span past 992 bytes: forced row streaming is refused, the
+    automatic plan uses the direct kernel."""
+    wl = _yuv("wide", [(4000, 200)], 80, (2, 400), F32, seed=10)
+    smol.set_tuning(path=smol.PATH_ROWS)
+    with pytest.raises(smol.SmolError):
+        run_gpu(wl)
+    smol.set_tuning(path=smol.PATH_AUTO)
+    _check(wl)
+    assert smol.last_plan()["path"] == smol.PATH_DIRECT
 
 
 def test_yuv_neutral_chroma_equals_rgb_path_on_gpu():
