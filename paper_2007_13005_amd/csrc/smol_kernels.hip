@@ -999,8 +999,12 @@ __device__ __forceinline__ void cursor_image(RowCursor &c, const BatchArgs &a, i
     c.span = g.span;
 }
 
+// `repeat`: the row was loaded already (past the end of the wave's range);
+// every lane then loads the rows' first chunk, so the instruction stream is
+// unchanged but almost nothing is fetched.
 template <int G>
-__device__ __forceinline__ void load_rows(StagedRows<G> &st, const RowCursor &c, int lane)
+__device__ __forceinline__ void load_rows(StagedRows<G> &st, const RowCursor &c, int lane,
+                                          bool repeat)
 {
     int y0, y1;
     vcursor_tap(c.v, y0, y1, st.wy);
@@ -1008,7 +1012,8 @@ __device__ __forceinline__ void load_rows(StagedRows<G> &st, const RowCursor &c,
     const uintptr_t r1 = c.base + (uintptr_t)y1 * (uintptr_t)c.pitch;
     st.sh0 = (int)(r0 & 15);
     st.sh1 = (int)(r1 & 15);
-    const int last0 = (st.sh0 + c.span - 1) >> 4, last1 = (st.sh1 + c.span - 1) >> 4;
+    const int last0 = repeat ? 0 : (st.sh0 + c.span - 1) >> 4;
+    const int last1 = repeat ? 0 : (st.sh1 + c.span - 1) >> 4;
     // global address space: a generic (flat) load would also count against
     // the LDS counter and make every LDS access wait for it
     // (a uniform base and a 32-bit lane offset: the loads take the base from
@@ -1230,10 +1235,13 @@ __global__ void __launch_bounds__(64) rgb_rows_kernel(BatchArgs a)
     // repeat that row, so every step issues the same loads and the compiler
     // can count exactly what is outstanding when a row is written to LDS.
     int lrow = 0;
+    bool at_end = false;  // the cursor sits on the wave's last row, already loaded
     auto advance = [&]() {
         if (lrow + 1 < n_rows) {
             cursor_next(lc, a);
             ++lrow;
+        } else {
+            at_end = true;
         }
     };
     int k = 0;
@@ -1242,10 +1250,10 @@ __global__ void __launch_bounds__(64) rgb_rows_kernel(BatchArgs a)
     // trip so the register sets rotate without copies. P = 1: one register
     // set, loaded with row k + 1 before row k is interpolated.
     StagedRows<G> A, B, C;
-    load_rows<G>(A, lc, lane);
+    load_rows<G>(A, lc, lane, false);
     advance();
     if (P == 2) {
-        load_rows<G>(B, lc, lane);
+        load_rows<G>(B, lc, lane, at_end);
         advance();
     }
     write_rows<G>(lds, A, lane);
@@ -1253,7 +1261,7 @@ __global__ void __launch_bounds__(64) rgb_rows_kernel(BatchArgs a)
     float cwy = A.wy;
 #define SMOL_ROWS_STEP(CUR, NXT, FUT)                                                         \
     {                                                                                         \
-        load_rows<G>(FUT, lc, lane);                                                          \
+        load_rows<G>(FUT, lc, lane, at_end);                                                  \
         advance();                                                                            \
         rows_compute<F16, J, EXACT>(a, nk, orow, lds0 + (uint32_t)csh0,                       \
                                     lds0 + (uint32_t)(1024 * G + csh1), cwy, cx, cw, lane);   \
@@ -1404,7 +1412,7 @@ struct YuvStaged {
     int b0;
 };
 
-__device__ __forceinline__ void yuv_load(YuvStaged &st, const YuvCursor &c, int lane)
+__device__ __forceinline__ void yuv_load(YuvStaged &st, const YuvCursor &c, int lane, bool repeat)
 {
     int y0, y1;
     vcursor_tap(c.v, y0, y1, st.wy);
@@ -1421,7 +1429,7 @@ __device__ __forceinline__ void yuv_load(YuvStaged &st, const YuvCursor &c, int 
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
         st.sh[s] = (int)(row[s] & 15);
-        const int last = (st.sh[s] + (s < 2 ? c.yspan : c.cspan) - 1) >> 4;
+        const int last = repeat ? 0 : (st.sh[s] + (s < 2 ? c.yspan : c.cspan) - 1) >> 4;
         GlobalByte *p = (GlobalByte *)(row[s] - (uintptr_t)st.sh[s]);
         st.c[s] = __builtin_nontemporal_load(
             (const __attribute__((address_space(1))) u32x4 *)(p + 16u * (uint32_t)min(lane, last)));
@@ -1636,12 +1644,18 @@ __global__ void __launch_bounds__(64) yuv_rows_kernel(BatchArgs a)
     // One register set: row k + 1 is loaded before row k is interpolated
     // (the loads past the wave's last row repeat that row).
     int lrow = 0;
+    bool at_end = false;  // the cursor sits on the wave's last row, already loaded
+    auto advance = [&]() {
+        if (lrow + 1 < n_rows) {
+            yuv_cursor_next(lc, a);
+            ++lrow;
+        } else {
+            at_end = true;
+        }
+    };
     YuvStaged R;
-    yuv_load(R, lc, lane);
-    if (lrow + 1 < n_rows) {
-        yuv_cursor_next(lc, a);
-        ++lrow;
-    }
+    yuv_load(R, lc, lane, false);
+    advance();
     yuv_write(lds, R, lane);
     int csh[8];
 #pragma unroll
@@ -1650,11 +1664,8 @@ __global__ void __launch_bounds__(64) yuv_rows_kernel(BatchArgs a)
     float cwy = R.wy, cwc0 = R.wc0, cwc1 = R.wc1;
     int cb0 = R.b0;
     for (int k = 0;;) {
-        yuv_load(R, lc, lane);
-        if (lrow + 1 < n_rows) {
-            yuv_cursor_next(lc, a);
-            ++lrow;
-        }
+        yuv_load(R, lc, lane, at_end);
+        advance();
         yuv_compute<F16, J, EXACT>(a, nk, orow, lds0, csh, cwy, cwc0, cwc1, cb0, cols, lane);
         if (++k == n_rows)
             break;
