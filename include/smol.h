@@ -173,15 +173,18 @@ int smol_image_geometry(int32_t width, int32_t height, int32_t yuv420, const smo
  *               then fails with SMOL_ERR_UNSUPPORTED); 3: the persistent
  *               register-gather RGB kernel, with per-image tap tables in LDS
  *               (images whose last 8-byte source window reaches the end of
- *               src, and YUV calls, use the direct kernel; a crop too wide
- *               for the tap tables fails with SMOL_ERR_UNSUPPORTED); 4: the
+ *               src use the direct kernel; a crop too wide for the tap
+ *               tables fails with SMOL_ERR_UNSUPPORTED); 4: the
  *               row-streaming RGB kernel (crops up to 512 columns whose
  *               source span plus 32 bytes is at most 4 KiB and fits the LDS
  *               budget twice, else SMOL_ERR_UNSUPPORTED; images whose 16-byte
  *               source chunks cross an end of src use the direct kernel);
  *               0: automatic (RGB: row-streaming when it fits, else
  *               register-gather when its tables fit, else LDS-staged when
- *               the span fits, else direct; YUV: direct)
+ *               the span fits, else direct; I420: row-streaming when the
+ *               crop is at most 512 columns and the luma and chroma spans at
+ *               most 992 bytes, else direct). For I420 only 0, 1 and 4 are
+ *               valid; 4 fails with SMOL_ERR_UNSUPPORTED past those limits
  *   band_rows   output rows per band in the LDS-staged kernels (1..64); for
  *               the row-streaming kernel, 1 or 2 sets how many output rows
  *               ahead of the interpolated one each wave loads
@@ -189,12 +192,16 @@ int smol_image_geometry(int32_t width, int32_t height, int32_t yuv420, const smo
  *               the device's per-workgroup limit)
  *   workgroups_per_cu  cap on the resident workgroups per compute unit
  *               the persistent kernels (paths 2-4) are sized for (1..16);
- *               by default as many as can be resident
- *   exact       1: the row-streaming kernel evaluates every multiply, add
- *               and the normalising division with its own fp32 rounding, in
- *               the definition's order (bit-identical to a scalar fp32
- *               evaluation; the other kernels always do); 0 (default): it
- *               uses fused multiply-adds and 1/std, within 2e-6 of that */
+ *               by default as many as can be resident (row streaming with
+ *               4 KiB staged rows: 8)
+ *   exact       1: the row-streaming kernels form the normalisation as the
+ *               correctly rounded quotient (v - mean) / std and round to
+ *               fp16 from that fp32 value, bit-identical to a scalar fp32
+ *               evaluation of the definition (the other kernels always do);
+ *               0 (default): they multiply v - mean by RN(1/std), at most
+ *               one fp32 ulp from the quotient, and may round that product
+ *               to fp16 directly (within one fp16 ulp). Every interpolation
+ *               and colour-conversion step is exact in both modes. */
 typedef struct smol_tuning {
     int32_t path;
     int32_t band_rows;
