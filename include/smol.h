@@ -201,14 +201,20 @@ int smol_image_geometry(int32_t width, int32_t height, int32_t yuv420, const smo
  *               0 (default): they multiply v - mean by RN(1/std), at most
  *               one fp32 ulp from the quotient, and may round that product
  *               to fp16 directly (within one fp16 ulp). Every interpolation
- *               and colour-conversion step is exact in both modes. */
+ *               and colour-conversion step is exact in both modes.
+ *   row_order   row-streaming kernels: 1 each wave takes a contiguous range
+ *               of output rows; 2 wave q of G takes rows q, q + G, ...
+ *               (concurrently running waves stream neighbouring rows);
+ *               0 (default): 2 for uniform RGB batches whose staged rows
+ *               exceed 2 KiB, else 1 */
 typedef struct smol_tuning {
     int32_t path;
     int32_t band_rows;
     int32_t lds_budget;
     int32_t workgroups_per_cu;
     int32_t exact;
-    int32_t reserved[3];
+    int32_t row_order;
+    int32_t reserved[2];
 } smol_tuning;
 
 /* Set the knobs (NULL resets to automatic). SMOL_ERR_INVALID_ARG if a field

@@ -8,6 +8,7 @@ import os
 import shutil
 import subprocess
 import sys
+import tempfile
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
@@ -15,8 +16,19 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libsmol.so")
 
-SOURCES = ["smol_kernels.hip", "smol_host.cpp"]
-HEADERS = ["smol_internal.h"]
+# The row-streaming kernels are split into parts (input, output type, row
+# walk) so that the compiler runs on the parts in parallel.
+SOURCES = [
+    "smol_kernels.hip",
+    "smol_rows_rgb_f16_range.hip",
+    "smol_rows_rgb_f16_stride.hip",
+    "smol_rows_rgb_f32_range.hip",
+    "smol_rows_rgb_f32_stride.hip",
+    "smol_rows_yuv_range.hip",
+    "smol_rows_yuv_stride.hip",
+    "smol_host.cpp",
+]
+HEADERS = ["smol_internal.h", "smol_device.h", "smol_rows.h"]
 
 # -ffp-contract=off: the kernels round every multiply and add on their own, as
 # the definition does; fused multiply-adds are never formed implicitly.
@@ -28,11 +40,11 @@ HIPCC_FLAGS = [
     "-O3",
     "-std=c++17",
     "-fPIC",
-    "-shared",
     "-Wall",
     "-ffp-contract=off",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
 ]
+LINK_FLAGS = ["--offload-arch=gfx950", "-shared", "-fPIC"]
 
 
 def hipcc() -> str:
@@ -42,19 +54,53 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found; ROCm is required to build libsmol")
 
 
-def build(verbose: bool = False) -> str:
-    tmp = LIB + ".tmp"
-    cmd = [hipcc(), *HIPCC_FLAGS, "-I", INCLUDE, "-I", CSRC, "-o", tmp,
-           *[os.path.join(CSRC, s) for s in SOURCES]]
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    res = subprocess.run(cmd, capture_output=True, text=True)
+def _jobs() -> int:
+    try:
+        n = int(os.environ.get("MAX_JOBS", ""))
+    except ValueError:
+        n = 0
+    return max(1, min(n or (os.cpu_count() or 4), 16))
+
+
+def _noise_free(stderr: str) -> str:
     noise = "is not a recognized feature for this target"
-    err = "\n".join(line for line in res.stderr.splitlines() if noise not in line)
-    if res.returncode != 0:
-        raise RuntimeError(f"hipcc failed ({res.returncode}):\n{err}")
-    if verbose and err.strip():
-        print(err, file=sys.stderr)
+    return "\n".join(line for line in stderr.splitlines() if noise not in line)
+
+
+def build(verbose: bool = False) -> str:
+    cc = hipcc()
+    tmp = LIB + ".tmp"
+    with tempfile.TemporaryDirectory(prefix="smol_build_") as objdir:
+        cmds = []
+        for src in SOURCES:
+            obj = os.path.join(objdir, os.path.splitext(src)[0] + ".o")
+            cmds.append((obj, [cc, *HIPCC_FLAGS, "-I", INCLUDE, "-I", CSRC, "-c", "-o", obj,
+                               os.path.join(CSRC, src)]))
+        pending = list(cmds)
+        running = []
+        errors = []
+        while pending or running:
+            while pending and len(running) < _jobs():
+                obj, cmd = pending.pop(0)
+                if verbose:
+                    print(" ".join(cmd), flush=True)
+                running.append((cmd, subprocess.Popen(cmd, stdout=subprocess.PIPE,
+                                                      stderr=subprocess.PIPE, text=True)))
+            cmd, proc = running.pop(0)
+            _, err = proc.communicate()
+            err = _noise_free(err)
+            if proc.returncode != 0:
+                errors.append(f"{cmd[-1]} ({proc.returncode}):\n{err}")
+            elif verbose and err.strip():
+                print(err, file=sys.stderr)
+        if errors:
+            raise RuntimeError("hipcc failed:\n" + "\n".join(errors))
+        link = [cc, *LINK_FLAGS, "-o", tmp, *[obj for obj, _ in cmds]]
+        if verbose:
+            print(" ".join(link), flush=True)
+        res = subprocess.run(link, capture_output=True, text=True)
+        if res.returncode != 0:
+            raise RuntimeError(f"link failed ({res.returncode}):\n{_noise_free(res.stderr)}")
     os.replace(tmp, LIB)
     return LIB
 

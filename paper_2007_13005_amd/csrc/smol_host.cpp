@@ -36,7 +36,8 @@ int fail(int code, const char *fmt, ...)
     return code;
 }
 
-std::atomic<int> g_path{0}, g_band_rows{0}, g_lds_budget{0}, g_wg_per_cu{0}, g_exact{0};
+std::atomic<int> g_path{0}, g_band_rows{0}, g_lds_budget{0}, g_wg_per_cu{0}, g_exact{0},
+    g_row_order{0};
 
 constexpr int kDefaultLdsBudget = 64 * 1024;
 constexpr int kMaxBandRows = 64;
@@ -455,6 +456,14 @@ int run_batch(const std::vector<Desc> &descs, size_t first, size_t count, int no
         a.table = nullptr;
         a.uni = descs[first];
         a.stride = stride;
+    }
+    {
+        // Row order of the row-streaming kernels: interleaved across waves
+        // for uniform batches of long staged rows (memory-bound: the waves
+        // then stream neighbouring rows), contiguous ranges otherwise.
+        const int order = g_row_order.load();
+        a.interleave = order == 2 || (order == 0 && uniform && pl.path == smol::PATH_ROWS &&
+                                      a.row_groups >= 4);
     }
 
     const int rc = launch(a, pl, stream);
@@ -897,6 +906,7 @@ int smol_set_tuning(const smol_tuning *t)
         g_lds_budget = 0;
         g_wg_per_cu = 0;
         g_exact = 0;
+        g_row_order = 0;
         return SMOL_OK;
     }
     if (t->path < 0 || t->path > 4)
@@ -912,11 +922,14 @@ int smol_set_tuning(const smol_tuning *t)
                     t->workgroups_per_cu, kMaxWorkgroupsPerCu);
     if (t->exact != 0 && t->exact != 1)
         return fail(SMOL_ERR_INVALID_ARG, "exact %d is neither 0 nor 1", t->exact);
+    if (t->row_order < 0 || t->row_order > 2)
+        return fail(SMOL_ERR_INVALID_ARG, "row_order %d outside 0..2", t->row_order);
     g_path = t->path;
     g_band_rows = t->band_rows;
     g_lds_budget = t->lds_budget;
     g_wg_per_cu = t->workgroups_per_cu;
     g_exact = t->exact;
+    g_row_order = t->row_order;
     return SMOL_OK;
 }
 

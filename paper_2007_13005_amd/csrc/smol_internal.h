@@ -44,6 +44,7 @@ struct BatchArgs {
     int32_t row_groups;  // 1 KiB chunk groups per staged source row (row-streaming kernel)
     int32_t col_iters;   // column pairs per lane: 1, 2 or 4 (row-streaming kernel)
     int32_t prefetch;    // rows loaded ahead of the one interpolated: 1 or 2 (row streaming)
+    int32_t interleave;  // row streaming: wave q takes rows q, q + G, ... (else a range)
     int32_t exact;       // 1: operation-by-operation fp32 arithmetic (row-streaming kernel)
     float mean[3];   // per channel, 0..255 units
     float stdv[3];
@@ -73,5 +74,14 @@ int occupancy_rgb_lds(int out_f16, size_t lds_bytes, int *blocks_per_cu);
 int launch_yuv_direct(const BatchArgs &a, int out_f16, void *stream);
 int launch_yuv_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream);
 int occupancy_yuv_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, int *blocks_per_cu);
+
+// Row-streaming kernels for the plan in the arguments (the file of each part:
+// smol_rows_<input>_<output>_<walk>.hip); `interleave` picks the walk.
+const void *rows_rgb_f16_range(const BatchArgs &a);
+const void *rows_rgb_f16_stride(const BatchArgs &a);
+const void *rows_rgb_f32_range(const BatchArgs &a);
+const void *rows_rgb_f32_stride(const BatchArgs &a);
+const void *rows_yuv_range(const BatchArgs &a, int f16);
+const void *rows_yuv_stride(const BatchArgs &a, int f16);
 
 }  // namespace smol

@@ -152,6 +152,8 @@ def test_tuning_validation():
         smol.set_tuning(workgroups_per_cu=17)
     with pytest.raises(smol.SmolError):
         smol.set_tuning(exact=2)
+    with pytest.raises(smol.SmolError):
+        smol.set_tuning(row_order=3)
     smol.set_tuning(path=1, band_rows=8, lds_budget=32768)
     smol.set_tuning(path=4, exact=1)
     smol.reset_tuning()

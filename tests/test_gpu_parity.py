@@ -132,6 +132,16 @@ def test_row_streaming_prefetch_depths(cfg, prefetch):
     assert smol.last_plan()["path"] == smol.PATH_ROWS
 
 
+@pytest.mark.parametrize("order", [1, 2])
+@pytest.mark.parametrize("cfg", ["c1", "c2", "c4", "c5"])
+def test_row_streaming_row_orders(cfg, order):
+    """Contiguous row ranges and rows interleaved across waves, on uniform
+    (incremental vertical taps, wrapping across images) and ragged batches."""
+    smol.set_tuning(row_order=order)
+    _check(synthetic.make(cfg, n={"c1": 9, "c2": 11, "c4": 3, "c5": 4}[cfg]))
+    assert smol.last_plan()["path"] == smol.PATH_ROWS
+
+
 def test_row_streaming_small_lds_budget():
     """A 1080p span needs 8 KiB of LDS: a 4 KiB budget refuses the forced
     row-streaming plan, the automatic plan takes another kernel."""
