@@ -117,17 +117,57 @@ def cpu_baseline(wl, seconds: float, threads: int) -> dict:
             counter[t] += 1
             i += threads
 
+    def timed(nthreads: int, secs: float) -> tuple[int, float]:
+        counter = [0] * nthreads
+        t0 = time.perf_counter()
+        deadline = t0 + secs
+        if nthreads == 1:
+            worker(0, deadline, counter)
+        else:
+            with cf.ThreadPoolExecutor(nthreads) as ex:
+                list(ex.map(lambda t: worker(t, deadline, counter), range(nthreads)))
+        return sum(counter), time.perf_counter() - t0
+
     oracle.lib()
-    counter = [0] * threads
-    t0 = time.perf_counter()
-    deadline = t0 + seconds
-    with cf.ThreadPoolExecutor(threads) as ex:
-        list(ex.map(lambda t: worker(t, deadline, counter), range(threads)))
-    elapsed = time.perf_counter() - t0
-    done = sum(counter)
+    done, elapsed = timed(threads, seconds)
+    done1, elapsed1 = timed(1, seconds / 4)
     return {"value": done / elapsed, "unit": "images/s", "cores": threads, "kind": "oracle",
             "sample": f"{done} images of workload {wl.name} (cycling through its {wl.n} images) "
-                      f"in {elapsed:.1f} s on {threads} threads, one image per task"}
+                      f"in {elapsed:.1f} s on {threads} threads, one image per task",
+            "single_thread_value": done1 / elapsed1,
+            "single_thread_sample": f"{done1} images in {elapsed1:.1f} s on 1 thread",
+            "cpu_model": cpu_model()}
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def copy_ceiling_gbps(torch, mib: int = 512, reps: int = 10) -> float:
+    """Read + write GB/s of a plain device-to-device copy (torch's copy
+    kernel) of `mib` MiB, the streaming ceiling the kernel is compared with."""
+    n = mib * 1024 * 1024
+    a = torch.empty(n, dtype=torch.uint8, device="cuda:0")
+    b = torch.empty_like(a)
+    a.fill_(1)
+    for _ in range(2):
+        b.copy_(a)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(reps):
+        b.copy_(a)
+    e1.record()
+    torch.cuda.synchronize()
+    return 2 * n * reps / (e0.elapsed_time(e1) / 1e3) / 1e9
 
 
 def load_traffic(config: str) -> dict | None:
@@ -207,18 +247,25 @@ def main() -> int:
     torch.cuda.synchronize()
     plan = smol.last_plan()
 
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
+    # The timed region, split into 5 repetitions by events on the launch
+    # stream (the median per-batch time is reported beside the average).
+    reps = 5
+    bounds = [args.steps * r // reps for r in range(reps + 1)]
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    ev0.record(stream)
-    for i in range(args.steps):
-        sp, sb, op = ptrs[i % rotate]
-        call(sp, sb, op, sh)
-    ev1.record(stream)
+    evs[0].record(stream)
+    for r in range(reps):
+        for i in range(bounds[r], bounds[r + 1]):
+            sp, sb, op = ptrs[i % rotate]
+            call(sp, sb, op, sh)
+        evs[r + 1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    gpu_ms = ev0.elapsed_time(ev1)
+    gpu_ms = evs[0].elapsed_time(evs[-1])
+    rep_us = sorted(1e3 * evs[r].elapsed_time(evs[r + 1]) / max(1, bounds[r + 1] - bounds[r])
+                    for r in range(reps) if bounds[r + 1] > bounds[r])
+    median_us = rep_us[len(rep_us) // 2]
     launches = args.steps * max(1, plan["launches"])
     avg_launch_s = gpu_ms / 1e3 / launches
     per_launch_bytes = algo / max(1, plan["launches"])
@@ -226,6 +273,21 @@ def main() -> int:
 
     # sanity: the last output is finite
     assert bool(torch.isfinite(outs[(args.steps - 1) % rotate]).all().item())
+
+    # Labelled separately: the same launches on one input/output set, which
+    # then stays resident in the 256 MB Infinity Cache (MALL) when it fits.
+    sp, sb, op = ptrs[0]
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    for _ in range(args.warmup):
+        call(sp, sb, op, sh)
+    e0.record(stream)
+    for _ in range(args.steps):
+        call(sp, sb, op, sh)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    mall_us = 1e3 * e0.elapsed_time(e1) / args.steps
+    copy_gbps = None if args.profile_run else copy_ceiling_gbps(torch)
 
     traffic = load_traffic(args.config)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
@@ -250,7 +312,13 @@ def main() -> int:
                    "band_rows": plan["band_rows"], "lds_bytes": plan["lds_bytes"],
                    "grid": plan["grid"],
                    "gpu_ms_per_step": round(gpu_ms / args.steps, 5),
-                   "hbm_gbps_wall": round(algo * args.steps / wall / 1e9, 1)},
+                   "gpu_us_per_step_median_of_5": round(median_us, 3),
+                   "gpu_us_per_step_reps": [round(x, 3) for x in rep_us],
+                   "hbm_gbps_wall": round(algo * args.steps / wall / 1e9, 1),
+                   "mall_warm_us_per_step_one_set": round(mall_us, 3),
+                   "copy_ceiling_gbps": None if copy_gbps is None else round(copy_gbps, 1),
+                   "achieved_frac_of_copy_ceiling":
+                       None if copy_gbps is None else round(achieved / copy_gbps, 4)},
         "roofline": roofline,
     }
     if not args.profile_run and args.cpu_seconds > 0:

@@ -192,8 +192,10 @@ int smol_image_geometry(int32_t width, int32_t height, int32_t yuv420, const smo
  *               the device's per-workgroup limit)
  *   workgroups_per_cu  cap on the resident workgroups per compute unit
  *               the persistent kernels (paths 2-4) are sized for (1..16);
- *               by default as many as can be resident (row streaming with
- *               4 KiB staged rows: 8)
+ *               for the row-streaming kernels, whose workgroups hold 1, 2
+ *               or 4 independent waves, the cap counts waves; by default as
+ *               many as can be resident (row streaming with 4 KiB staged
+ *               rows: 8 waves)
  *   exact       1: the row-streaming kernels form the normalisation as the
  *               correctly rounded quotient (v - mean) / std and round to
  *               fp16 from that fp32 value, bit-identical to a scalar fp32

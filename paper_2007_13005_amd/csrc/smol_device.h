@@ -93,6 +93,18 @@ __device__ __forceinline__ void ycbcr_to_rgb(float y, float cb, float cr, float 
     b = clamp255(y + kBCb * cb);
 }
 
+// The same conversion from cb16 = 16 * (cb - 128) and cr16 = 16 * (cr - 128):
+// with the coefficients divided by 16 (exact) each product is the same real
+// number as above, so every rounded value is identical.
+__device__ __forceinline__ void ycbcr16_to_rgb(float y, float cb16, float cr16, float &r,
+                                               float &g, float &b)
+{
+    constexpr float s = 0.0625f;
+    r = clamp255(y + (kRCr * s) * cr16);
+    g = clamp255((y - (kGCb * s) * cb16) - (kGCr * s) * cr16);
+    b = clamp255(y + (kBCb * s) * cb16);
+}
+
 __device__ __forceinline__ float lerp(float a, float b, float w) { return a + w * (b - a); }
 
 __device__ __forceinline__ float normalize(float v, float mean, float stdv, float rcp)

@@ -387,6 +387,7 @@ int run_batch(const std::vector<Desc> &descs, size_t first, size_t count, int no
                     "workgroup", pl.lds_bytes, di.lds_per_block);
     const bool rows = pl.path == smol::PATH_ROWS || pl.path == smol::PATH_YUV_ROWS;
     if (pl.path == smol::PATH_LDS || pl.path == smol::PATH_GATHER || rows) {
+        a.wpg = rows ? smol::kRowsMaxWavesPerGroup : 1;
         int per_cu = 0;
         const int oc = pl.path == smol::PATH_LDS
                            ? smol::occupancy_rgb_lds(pl.f16, pl.lds_bytes, &per_cu)
@@ -401,16 +402,32 @@ int run_batch(const std::vector<Desc> &descs, size_t first, size_t count, int no
             return fail(SMOL_ERR_UNSUPPORTED, "kernel cannot be resident with %zu bytes of LDS",
                         pl.lds_bytes);
         const int forced = g_wg_per_cu.load();
-        if (forced > 0)
-            per_cu = std::min(per_cu, forced);
-        else if (pl.path == smol::PATH_ROWS && a.row_groups >= 4)
-            per_cu = std::min(per_cu, kRowsWavesPerCu);
-        items = pl.path == smol::PATH_LDS ? (long long)n * a.bands
-                : rows                    ? (long long)n * a.Ch
-                                             : (long long)n * (((long long)a.Ch * a.Cw +
-                                                                kGatherPassPixels - 1) /
-                                                               kGatherPassPixels);
-        pl.grid = (int)std::min<long long>(items, (long long)di.cus * per_cu);
+        if (rows) {
+            // Waves per compute unit (the tuning knob counts waves here).
+            int waves = per_cu * a.wpg;
+            if (forced > 0)
+                waves = std::min(waves, forced);
+            else if (pl.path == smol::PATH_ROWS && a.row_groups >= 4)
+                waves = std::min(waves, kRowsWavesPerCu);
+            // Workgroups of 4 (or 2) waves when that count allows, so each
+            // compute unit still holds at most `waves` of them.
+            a.wpg = waves % 4 == 0 ? 4 : waves % 2 == 0 ? 2 : 1;
+            items = (long long)n * a.Ch;
+            long long w = std::min<long long>(items, (long long)di.cus * waves);
+            if (w >= a.wpg)
+                w -= w % a.wpg;
+            else
+                a.wpg = 1;
+            pl.grid = (int)w;
+        } else {
+            if (forced > 0)
+                per_cu = std::min(per_cu, forced);
+            items = pl.path == smol::PATH_LDS ? (long long)n * a.bands
+                                              : (long long)n * (((long long)a.Ch * a.Cw +
+                                                                 kGatherPassPixels - 1) /
+                                                                kGatherPassPixels);
+            pl.grid = (int)std::min<long long>(items, (long long)di.cus * per_cu);
+        }
         a.grid = pl.grid;
     } else {
         items = (long long)n * a.Ch * a.Cw;

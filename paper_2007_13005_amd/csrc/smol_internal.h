@@ -46,6 +46,7 @@ struct BatchArgs {
     int32_t prefetch;    // rows loaded ahead of the one interpolated: 1 or 2 (row streaming)
     int32_t interleave;  // row streaming: wave q takes rows q, q + G, ... (else a range)
     int32_t exact;       // 1: operation-by-operation fp32 arithmetic (row-streaming kernel)
+    int32_t wpg;         // row streaming: waves per workgroup (grid = waves / wpg)
     float mean[3];   // per channel, 0..255 units
     float stdv[3];
     float rcp[3];    // RN(1 / stdv), fp32
@@ -61,12 +62,17 @@ constexpr int PATH_YUV_ROWS = 5;
 // staged source rows (span + 32 bytes) up to kRowsMaxGroups KiB.
 constexpr int kRowsMaxColIters = 4;
 constexpr int kRowsMaxGroups = 4;
+// Waves per workgroup of the row-streaming kernels (each wave independent).
+constexpr int kRowsMaxWavesPerGroup = 4;
 
 // Launchers (smol_kernels.hip). Return a hipError_t as int.
 int launch_rgb_direct(const BatchArgs &a, int out_f16, void *stream);
 int launch_rgb_lds(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream);
 int launch_rgb_gather(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream);
+// Row-streaming launches: `lds_bytes` is one wave's slot; a workgroup holds
+// a.wpg waves and a.grid is the number of waves (a multiple of a.wpg).
 int launch_rgb_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream);
+// Resident workgroups of a.wpg waves per compute unit.
 int occupancy_rgb_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, int *blocks_per_cu);
 // Resident workgroups per compute unit for the persistent kernels.
 int occupancy_rgb_gather(int out_f16, size_t lds_bytes, int *blocks_per_cu);

@@ -760,15 +760,15 @@ const void *rows_kernel(const BatchArgs &a, int f16)
 int launch_rgb_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream)
 {
     hipStream_t s = (hipStream_t)stream;
-    const dim3 grid((unsigned)a.grid), block(64);
+    const dim3 grid((unsigned)(a.grid / a.wpg)), block(64 * a.wpg);
     void *args[] = {(void *)&a};
-    return (int)hipLaunchKernel(rows_kernel(a, out_f16), grid, block, args, lds_bytes, s);
+    return (int)hipLaunchKernel(rows_kernel(a, out_f16), grid, block, args, lds_bytes * a.wpg, s);
 }
 
 int occupancy_rgb_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, int *blocks_per_cu)
 {
     return (int)hipOccupancyMaxActiveBlocksPerMultiprocessor(
-        blocks_per_cu, rows_kernel(a, out_f16), 64, lds_bytes);
+        blocks_per_cu, rows_kernel(a, out_f16), 64 * a.wpg, lds_bytes * a.wpg);
 }
 
 int occupancy_rgb_gather(int out_f16, size_t lds_bytes, int *blocks_per_cu)
@@ -808,15 +808,15 @@ const void *yuv_rows_kernel_for(const BatchArgs &a, int f16)
 int launch_yuv_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream)
 {
     hipStream_t s = (hipStream_t)stream;
-    const dim3 grid((unsigned)a.grid), block(64);
+    const dim3 grid((unsigned)(a.grid / a.wpg)), block(64 * a.wpg);
     void *args[] = {(void *)&a};
-    return (int)hipLaunchKernel(yuv_rows_kernel_for(a, out_f16), grid, block, args, lds_bytes, s);
+    return (int)hipLaunchKernel(yuv_rows_kernel_for(a, out_f16), grid, block, args, lds_bytes * a.wpg, s);
 }
 
 int occupancy_yuv_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, int *blocks_per_cu)
 {
     return (int)hipOccupancyMaxActiveBlocksPerMultiprocessor(
-        blocks_per_cu, yuv_rows_kernel_for(a, out_f16), 64, lds_bytes);
+        blocks_per_cu, yuv_rows_kernel_for(a, out_f16), 64 * a.wpg, lds_bytes * a.wpg);
 }
 
 }  // namespace smol

@@ -213,6 +213,24 @@ __device__ __forceinline__ int xcd_position(int g, int G)
     return G % 8 == 0 ? (g % 8) * (G / 8) + g / 8 : g;
 }
 
+// A workgroup holds blockDim.x / 64 independent waves (no barriers), each
+// with its own LDS slot of `slot_bytes`; several waves per workgroup cut the
+// cost of dispatching the grid. Returns the wave's slot and sets its lane,
+// the number of waves and the wave's rows.
+template <int STRIDE>
+__device__ __forceinline__ uint8_t *rows_wave(uint8_t *lds_all, int slot_bytes, long long T,
+                                              int &lane, int &nw, long long &r0, int &n_rows)
+{
+    const int wpg = (int)(blockDim.x >> 6);
+    const int wid = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+    lane = (int)(threadIdx.x & 63);
+    const int ng = (int)gridDim.x;
+    nw = ng * wpg;
+    const int g = STRIDE ? xcd_position((int)blockIdx.x, ng) : (int)blockIdx.x;
+    wave_rows<STRIDE>(T, g * wpg + wid, nw, r0, n_rows);
+    return lds_all + wid * slot_bytes;
+}
+
 __device__ __forceinline__ void floor_divmod(long long n, int d, int &q, int &r)
 {
     const long long qq = n >= 0 ? n / d : -((-n + d - 1) / d);
@@ -512,17 +530,15 @@ __device__ __forceinline__ void rows_compute(const BatchArgs &a, const NormK &nk
 }
 
 template <int F16, int J, int EXACT, int G, int P, int STRIDE>
-__global__ void __launch_bounds__(64) rgb_rows_kernel(BatchArgs a)
+__global__ void __launch_bounds__(64 * kRowsMaxWavesPerGroup) rgb_rows_kernel(BatchArgs a)
 {
-    extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
-    const int lane = threadIdx.x;
-    const int Ch = a.Ch;
-    const int nw = (int)gridDim.x;
+    extern __shared__ __attribute__((aligned(16))) uint8_t lds_all[];
+    int lane, nw;
     long long r0;
     int n_rows;
-    wave_rows<STRIDE>((long long)a.n * Ch, STRIDE ? xcd_position((int)blockIdx.x, nw)
-                                                  : (int)blockIdx.x,
-                      nw, r0, n_rows);
+    const int Ch = a.Ch;
+    uint8_t *const lds = rows_wave<STRIDE>(lds_all, 2048 * G, (long long)a.n * Ch, lane, nw, r0,
+                                           n_rows);
     if (n_rows <= 0)
         return;
     const RowStep step = row_step_of<STRIDE>(nw, Ch);
@@ -564,11 +580,13 @@ __global__ void __launch_bounds__(64) rgb_rows_kernel(BatchArgs a)
             at_end = true;
         }
     };
-    int k = 0;
-    // P = 2: one step loads row k + 2 into FUT, interpolates row k (staged
-    // from CUR), writes row k + 1 (in NXT) into the slot; three steps per
-    // trip so the register sets rotate without copies. P = 1: one register
-    // set, loaded with row k + 1 before row k is interpolated.
+    // P = 2: a step loads row k + 2 into FUT, interpolates row k (staged in
+    // LDS), writes row k + 1 (in NXT) into the slot; the three register sets
+    // rotate over three steps without copies. P = 1: one register set, loaded
+    // with row k + 1 before row k is interpolated. The loop runs the n_rows - 1
+    // steps that stage a next row and leaves only at its end, with nothing
+    // outstanding but the prefetched row; the last row is interpolated after
+    // it.
     StagedRows<G> A, B, C;
     load_rows<G>(A, lc, lane, false);
     advance();
@@ -579,14 +597,12 @@ __global__ void __launch_bounds__(64) rgb_rows_kernel(BatchArgs a)
     write_rows<G>(lds, A, lane);
     int csh0 = A.sh0, csh1 = A.sh1;
     float cwy = A.wy;
-#define SMOL_ROWS_STEP(CUR, NXT, FUT)                                                         \
+#define SMOL_ROWS_STEP(NXT, FUT)                                                              \
     {                                                                                         \
         load_rows<G>(FUT, lc, lane, at_end);                                                  \
         advance();                                                                            \
         rows_compute<F16, J, EXACT>(a, nk, orow, lds0 + (uint32_t)csh0,                       \
                                     lds0 + (uint32_t)(1024 * G + csh1), cwy, cx, cw, lane);   \
-        if (++k == n_rows)                                                                    \
-            break;                                                                            \
         write_rows<G>(lds, NXT, lane);                                                        \
         csh0 = NXT.sh0;                                                                       \
         csh1 = NXT.sh1;                                                                       \
@@ -610,17 +626,24 @@ __global__ void __launch_bounds__(64) rgb_rows_kernel(BatchArgs a)
             }                                                                                 \
         }                                                                                     \
     }
+    int left = n_rows - 1;
     if (P == 2) {
-        while (true) {
-            SMOL_ROWS_STEP(A, B, C)
-            SMOL_ROWS_STEP(B, C, A)
-            SMOL_ROWS_STEP(C, A, B)
+        for (; left >= 3; left -= 3) {
+            SMOL_ROWS_STEP(B, C)
+            SMOL_ROWS_STEP(C, A)
+            SMOL_ROWS_STEP(A, B)
         }
+        if (left >= 1)
+            SMOL_ROWS_STEP(B, C)
+        if (left >= 2)
+            SMOL_ROWS_STEP(C, A)
     } else {
-        while (true)
-            SMOL_ROWS_STEP(A, A, A)
+        for (; left > 0; --left)
+            SMOL_ROWS_STEP(A, A)
     }
 #undef SMOL_ROWS_STEP
+    rows_compute<F16, J, EXACT>(a, nk, orow, lds0 + (uint32_t)csh0,
+                                lds0 + (uint32_t)(1024 * G + csh1), cwy, cx, cw, lane);
 }
 
 // ---------------------------------------------------------------------------
@@ -635,15 +658,20 @@ __global__ void __launch_bounds__(64) rgb_rows_kernel(BatchArgs a)
 //
 // Every luma tap is converted as defined: chroma bilinear at centred siting,
 // BT.601 full range, clamp; then the four converted taps are interpolated
-// and normalised. The chroma weights are 0, 1/4 and 3/4, so each chroma
-// interpolation step is exact in fp32 (multiples of 1/16 below 256) and a
-// fused multiply-add gives the value the separately rounded form gives.
+// and normalised. The chroma weights are 0, 1/4 and 3/4, so the chroma value
+// at a luma tap is S / 16 with S = the sum of its four chroma samples times
+// integer weights (4 - fy or fy) * (4 - fx or fx), fx, fy in {0, 1, 3}: every
+// interpolation step of the definition is exact, and so is S. One v_dot4
+// forms S - 2048 = 16 * (chroma - 128) from the four sample bytes and the four
+// weight bytes; the BT.601 products then use the coefficients divided by 16,
+// which gives the same real products and so the same rounded values.
 //
 // Lane l computes output columns c = 2l + 128j and c + 1 (j < J). Per column
 // it keeps: the luma tap (offset of x0 in the staged luma span, weight), and
-// for its two luma columns x0, x1 the chroma taps as the offset of the first
-// chroma column they read and a byte selector that picks the chroma samples
-// (x0's pair, x1's pair) out of the four bytes read there.
+// for its two luma columns x0, x1 the offset of the first chroma column they
+// read, per luma column a v_perm selector that picks its two chroma samples
+// from each of two chroma rows, and its horizontal weight bytes
+// (4 - fx, fx).
 // ---------------------------------------------------------------------------
 struct YuvImg {
     long long off[3];
@@ -690,7 +718,8 @@ __device__ __forceinline__ YuvImg yuv_img(const BatchArgs &a, int img)
 struct YuvStaged {
     u32x4 c[8];
     int sh[8];
-    float wy, wc0, wc1;
+    float wy;
+    int fy0, fy1;  // vertical chroma weights of luma rows y0, y1, in quarters
     int b0;
 };
 
@@ -762,8 +791,8 @@ __device__ __forceinline__ void yuv_load(YuvStaged &st, const YuvCursor &c, int 
     int y0, y1;
     vcursor_tap(c.v, y0, y1, st.wy);
     const Tap t0 = chroma_tap(y0, c.Hc), t1 = chroma_tap(y1, c.Hc);
-    st.wc0 = t0.w;
-    st.wc1 = t1.w;
+    st.fy0 = (int)(4.0f * t0.w);  // exact: 0, 1 or 3
+    st.fy1 = (int)(4.0f * t1.w);
     st.b0 = t1.x0 == t0.x0 ? 0 : 1;
     const uintptr_t row[8] = {
         c.base[0] + (uintptr_t)y0 * (uintptr_t)c.W,     c.base[0] + (uintptr_t)y1 * (uintptr_t)c.W,
@@ -793,9 +822,9 @@ template <int J>
 struct YuvCols {
     int ox[J][2];        // luma x0 - xf
     float wx[J][2];      // luma weight
-    int oc[J][2];        // first chroma column read - cxf
-    uint32_t sel[J][2];  // v_perm selector: bytes (x0 pair, x1 pair) of the 4 read
-    float wc0[J][2], wc1[J][2];  // chroma weights of luma columns x0 and x1
+    int oc[J][2];            // first chroma column read - cxf
+    uint32_t sel[J][2][2];   // per luma column: v_perm selector of its 2 x 2 chroma samples
+    uint32_t hw[J][2][2];    // per luma column: horizontal weight bytes (4 - fx, fx)
 };
 
 template <int J>
@@ -813,10 +842,18 @@ __device__ __forceinline__ void yuv_cols(YuvCols<J> &k, const YuvImg &g, int Cw,
             k.ox[j][px] = t.x0 - g.xf;
             k.wx[j][px] = t.w;
             k.oc[j][px] = a0.x0 - cxf;
-            k.sel[j][px] = (uint32_t)(a0.x1 - a0.x0) << 8 | (uint32_t)(a1.x0 - a0.x0) << 16 |
-                           (uint32_t)(a1.x1 - a0.x0) << 24;
-            k.wc0[j][px] = a0.w;
-            k.wc1[j][px] = a1.w;
+            // the samples of luma column xi are bytes d0, d1 of the 4 read
+            // from each chroma row; perm(row b, row a) yields a[d0], a[d1],
+            // b[d0], b[d1]
+            const Tap ax[2] = {a0, a1};
+#pragma unroll
+            for (int xi = 0; xi < 2; ++xi) {
+                const uint32_t d0 = (uint32_t)(ax[xi].x0 - a0.x0);
+                const uint32_t d1 = (uint32_t)(ax[xi].x1 - a0.x0);
+                k.sel[j][px][xi] = d0 | d1 << 8 | (4 + d0) << 16 | (4 + d1) << 24;
+                const uint32_t fx = (uint32_t)(4.0f * ax[xi].w);  // exact: 0, 1 or 3
+                k.hw[j][px][xi] = (4 - fx) | fx << 8;
+            }
         }
 }
 
@@ -848,22 +885,24 @@ __device__ __forceinline__ void lds_read_quads<8>(const uint32_t (&A)[8], uint32
 }
 #undef SMOL_RD2
 
-// Chroma of luma columns x0, x1 at one chroma row: (horizontal lerps).
-__device__ __forceinline__ void chroma_h(uint32_t quad, uint32_t sel, float w0, float w1, float &h0,
-                                         float &h1)
+// 16 * (chroma - 128) at one luma tap: the tap's four chroma samples
+// (selected from chroma rows ra and rb) dotted with its weight bytes, minus
+// 2048, exact in integers.
+__device__ __forceinline__ float chroma16(uint32_t ra, uint32_t rb, uint32_t sel, uint32_t wts)
 {
-    const uint32_t b = __builtin_amdgcn_perm(0u, quad, sel);  // x0 pair, x1 pair
-    const float a0 = cvt_ubyte0(b), a1 = cvt_ubyte2(b);
-    h0 = fmaf(w0, cvt_ubyte1(b) - a0, a0);  // exact (see above)
-    h1 = fmaf(w1, cvt_ubyte3(b) - a1, a1);
+    const uint32_t smp = __builtin_amdgcn_perm(rb, ra, sel);
+    return (float)(int)__builtin_amdgcn_udot4(smp, wts, (uint32_t)-2048, false);
 }
 
 template <int F16, int J, int EXACT>
 __device__ __forceinline__ void yuv_compute(const BatchArgs &a, const NormK &nk, uint8_t *orow,
                                             uint32_t slot, const int (&sh)[8], float wy,
-                                            float wc0, float wc1, int b0, const YuvCols<J> &k,
+                                            int fy0, int fy1, int b0, const YuvCols<J> &k,
                                             int lane)
 {
+    // weight bytes of luma row yi and column xi: hw(xi) * (4 + 65535 fy(yi))
+    // = (4 - fy) * [4 - fx, fx, 0, 0] + fy * [0, 0, 4 - fx, fx] (no carries)
+    const uint32_t vm[2] = {4u + 65535u * (uint32_t)fy0, 4u + 65535u * (uint32_t)fy1};
     const int Cw = a.Cw;
     constexpr int kEsz = F16 ? 2 : 4;
     const long long plane = (long long)a.Ch * Cw * kEsz;
@@ -880,20 +919,18 @@ __device__ __forceinline__ void yuv_compute(const BatchArgs &a, const NormK &nk,
                 A[s] = slot + 1024u * s + (uint32_t)sh[s] +
                        (uint32_t)(s < 2 ? k.ox[j][px] : k.oc[j][px]);
             lds_read_quads<8>(A, q);
-            // chroma at (x0, x1) x (y0, y1) for both planes
+            // 16 * (chroma - 128) at (y0, y1) x (x0, x1) for both planes:
+            // luma row y0 reads chroma rows r0, r1; y1 reads r0 or r1 (b0),
+            // and r2
             float cc[2][2][2];  // [plane][luma row][luma col]
 #pragma unroll
             for (int pl = 0; pl < 2; ++pl) {
-                float h[3][2];
-#pragma unroll
-                for (int r = 0; r < 3; ++r)
-                    chroma_h(q[2 + 3 * pl + r], k.sel[j][px], k.wc0[j][px], k.wc1[j][px], h[r][0],
-                             h[r][1]);
+                const uint32_t r0 = q[2 + 3 * pl], r1 = q[3 + 3 * pl], r2 = q[4 + 3 * pl];
+                const uint32_t ra1 = b0 ? r1 : r0;
 #pragma unroll
                 for (int xi = 0; xi < 2; ++xi) {
-                    cc[pl][0][xi] = fmaf(wc0, h[1][xi] - h[0][xi], h[0][xi]);
-                    const float hb = b0 ? h[1][xi] : h[0][xi];
-                    cc[pl][1][xi] = fmaf(wc1, h[2][xi] - hb, hb);
+                    cc[pl][0][xi] = chroma16(r0, r1, k.sel[j][px][xi], __umul24(k.hw[j][px][xi], vm[0]));
+                    cc[pl][1][xi] = chroma16(ra1, r2, k.sel[j][px][xi], __umul24(k.hw[j][px][xi], vm[1]));
                 }
             }
             float rgb[2][2][3];  // [luma row][luma col][channel]
@@ -902,8 +939,8 @@ __device__ __forceinline__ void yuv_compute(const BatchArgs &a, const NormK &nk,
 #pragma unroll
                 for (int xi = 0; xi < 2; ++xi) {
                     const float Y = xi ? cvt_ubyte1(q[yi]) : cvt_ubyte0(q[yi]);
-                    ycbcr_to_rgb(Y, cc[0][yi][xi], cc[1][yi][xi], rgb[yi][xi][0], rgb[yi][xi][1],
-                                 rgb[yi][xi][2]);
+                    ycbcr16_to_rgb(Y, cc[0][yi][xi], cc[1][yi][xi], rgb[yi][xi][0],
+                                   rgb[yi][xi][1], rgb[yi][xi][2]);
                 }
 #pragma unroll
             for (int ch = 0; ch < 3; ++ch)
@@ -954,17 +991,16 @@ __device__ __forceinline__ void yuv_compute(const BatchArgs &a, const NormK &nk,
 }
 
 template <int F16, int J, int EXACT, int STRIDE>
-__global__ void __launch_bounds__(64) yuv_rows_kernel(BatchArgs a)
+__global__ void __launch_bounds__(64 * kRowsMaxWavesPerGroup) __attribute__((amdgpu_waves_per_eu(J <= 2 ? 3 : 1)))
+yuv_rows_kernel(BatchArgs a)
 {
-    extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
-    const int lane = threadIdx.x;
-    const int Ch = a.Ch;
-    const int nw = (int)gridDim.x;
+    extern __shared__ __attribute__((aligned(16))) uint8_t lds_all[];
+    int lane, nw;
     long long r0;
     int n_rows;
-    wave_rows<STRIDE>((long long)a.n * Ch, STRIDE ? xcd_position((int)blockIdx.x, nw)
-                                                  : (int)blockIdx.x,
-                      nw, r0, n_rows);
+    const int Ch = a.Ch;
+    uint8_t *const lds = rows_wave<STRIDE>(lds_all, 8192, (long long)a.n * Ch, lane, nw, r0,
+                                           n_rows);
     if (n_rows <= 0)
         return;
     const RowStep step = row_step_of<STRIDE>(nw, Ch);
@@ -989,17 +1025,14 @@ __global__ void __launch_bounds__(64) yuv_rows_kernel(BatchArgs a)
     const NormK nk = norm_consts(a);
     const uint32_t lds0 = lds_addr(lds);
 
-    // One register set: row k + 1 is loaded before row k is interpolated
-    // (the loads past the wave's last row repeat that row, fetching one
-    // chunk per segment).
+    // One register set: row k + 1 is loaded before row k is interpolated.
+    // The loop runs the n_rows - 1 steps that stage a next row and leaves
+    // only at its end; the last row is interpolated after it.
     int lrow = 0;
-    bool at_end = false;
     auto advance = [&]() {
         if (lrow + 1 < n_rows) {
             yuv_cursor_next<STRIDE>(lc, a, step);
             ++lrow;
-        } else {
-            at_end = true;
         }
     };
     YuvStaged R;
@@ -1010,21 +1043,20 @@ __global__ void __launch_bounds__(64) yuv_rows_kernel(BatchArgs a)
 #pragma unroll
     for (int s = 0; s < 8; ++s)
         csh[s] = R.sh[s];
-    float cwy = R.wy, cwc0 = R.wc0, cwc1 = R.wc1;
+    float cwy = R.wy;
+    int cfy0 = R.fy0, cfy1 = R.fy1;
     int cb0 = R.b0;
-    for (int k = 0;;) {
-        yuv_load(R, lc, lane, at_end);
+    for (int left = n_rows - 1; left > 0; --left) {
+        yuv_load(R, lc, lane, false);
         advance();
-        yuv_compute<F16, J, EXACT>(a, nk, orow, lds0, csh, cwy, cwc0, cwc1, cb0, cols, lane);
-        if (++k == n_rows)
-            break;
+        yuv_compute<F16, J, EXACT>(a, nk, orow, lds0, csh, cwy, cfy0, cfy1, cb0, cols, lane);
         yuv_write(lds, R, lane);
 #pragma unroll
         for (int s = 0; s < 8; ++s)
             csh[s] = R.sh[s];
         cwy = R.wy;
-        cwc0 = R.wc0;
-        cwc1 = R.wc1;
+        cfy0 = R.fy0;
+        cfy1 = R.fy1;
         cb0 = R.b0;
         const int pimg = c_img;
         c_img += step.di;
@@ -1045,6 +1077,7 @@ __global__ void __launch_bounds__(64) yuv_rows_kernel(BatchArgs a)
             }
         }
     }
+    yuv_compute<F16, J, EXACT>(a, nk, orow, lds0, csh, cwy, cfy0, cfy1, cb0, cols, lane);
 }
 
 
