@@ -87,6 +87,18 @@ __device__ __forceinline__ RowImg row_img(const BatchArgs &a, int img)
     return g;
 }
 
+// First output column of the pair lane `lane` computes in column iteration
+// j: 2 * lane + 128 * j, clamped to the last pair (Cw - 2 for even Cw, the
+// last column for odd Cw). Lanes past the crop thus compute and store a
+// copy of the last pair, the same values to the same addresses: every lane
+// runs the same stores, with no branch around them, and the compiler can
+// count the memory operations in flight exactly (a branch that might skip
+// the stores would make it wait for them before every write to LDS).
+__device__ __forceinline__ int pair_col(int lane, int j, int Cw)
+{
+    return min(2 * lane + 128 * j, Cw - 2 + (Cw & 1));
+}
+
 template <int J>
 __device__ __forceinline__ void row_taps(const RowImg &g, const int Cw, int (&cx)[J][2],
                                          float (&cw)[J][2], int lane)
@@ -95,14 +107,10 @@ __device__ __forceinline__ void row_taps(const RowImg &g, const int Cw, int (&cx
     for (int j = 0; j < J; ++j)
 #pragma unroll
         for (int px = 0; px < 2; ++px) {
-            const int c = 2 * lane + 128 * j + px;
-            cx[j][px] = 0;
-            cw[j][px] = 0.0f;
-            if (c < Cw) {
-                const Tap t = axis_tap(g.left + c, g.W, g.Wr);
-                cx[j][px] = 3 * (t.x0 - g.xf);
-                cw[j][px] = t.w;
-            }
+            const int col = min(pair_col(lane, j, Cw) + px, Cw - 1);
+            const Tap t = axis_tap(g.left + col, g.W, g.Wr);
+            cx[j][px] = 3 * (t.x0 - g.xf);
+            cw[j][px] = t.w;
         }
 }
 
@@ -174,6 +182,7 @@ struct StagedRows {
     u32x4 c0[G], c1[G];
     int sh0, sh1;
     float wy;
+    int y0, y1;  // the source rows
 };
 
 // The rows a wave walks: batch rows r0, r0 + d, r0 + 2d, ... as (image, crop
@@ -351,6 +360,8 @@ __device__ __forceinline__ void load_rows(StagedRows<G> &st, const RowCursor &c,
 {
     int y0, y1;
     vcursor_tap(c.v, y0, y1, st.wy);
+    st.y0 = y0;
+    st.y1 = y1;
     const uintptr_t r0 = c.base + (uintptr_t)y0 * (uintptr_t)c.pitch;
     const uintptr_t r1 = c.base + (uintptr_t)y1 * (uintptr_t)c.pitch;
     st.sh0 = (int)(r0 & 15);
@@ -425,7 +436,41 @@ __device__ __forceinline__ void lds_read_taps8(const uint32_t (&ad)[8], u32x2 (&
                    "v"(ad[6]), "v"(ad[7])
                  : "memory");
 }
+__device__ __forceinline__ void lds_read_taps2(const uint32_t (&ad)[2], u32x2 (&lo)[2],
+                                               uint32_t (&hi)[2])
+{
+    asm volatile(SMOL_RD3("%0", "%2", "%4") SMOL_RD3("%1", "%3", "%5") "s_waitcnt lgkmcnt(0)"
+                 : "=&v"(lo[0]), "=&v"(lo[1]), "=&v"(hi[0]), "=&v"(hi[1])
+                 : "v"(ad[0]), "v"(ad[1])
+                 : "memory");
+}
 #undef SMOL_RD3
+
+// The 2J tap pairs of one staged row (pixel c and c + 1 of every column
+// iteration), realigned to 8-byte values: tap 2j + px.
+template <int J>
+__device__ __forceinline__ void read_row_taps(uint32_t row, const int (&cx)[J][2],
+                                              uint64_t (&v)[2 * J])
+{
+    constexpr int N = 2 * J;
+    uint32_t A[N], ad[N], hi[N];
+    u32x2 lo[N];
+#pragma unroll
+    for (int t = 0; t < N; ++t) {
+        A[t] = row + (uint32_t)cx[t / 2][t & 1];
+        ad[t] = A[t] & ~3u;
+    }
+    if constexpr (N == 8)
+        lds_read_taps8(ad, lo, hi);
+    else if constexpr (N == 4)
+        lds_read_taps4(ad, lo, hi);
+    else
+        lds_read_taps2(ad, lo, hi);
+#pragma unroll
+    for (int t = 0; t < N; ++t)
+        v[t] = (uint64_t)__builtin_amdgcn_alignbyte(lo[t].y, lo[t].x, A[t]) |
+               ((uint64_t)__builtin_amdgcn_alignbyte(hi[t], lo[t].y, A[t]) << 32);
+}
 
 // The tap pairs of column iterations j0 .. j0 + N/4 - 1 (pixel c, c + 1 of
 // rows 0 and 1 each), realigned to 8-byte values.
@@ -451,21 +496,89 @@ __device__ __forceinline__ void read_taps(uint32_t row0, uint32_t row1, const in
                ((uint64_t)__builtin_amdgcn_alignbyte(hi[t], lo[t].y, A[t]) << 32);
 }
 
+// One output row's values of a lane, ready to store: per column iteration
+// and channel the pair (c, c + 1) as one dword (fp16) or two (fp32).
+//
+// A row's stores are issued after the next row's chunks are written to LDS,
+// not before: the wait for those chunks' loads then never includes the
+// completion of this row's stores (the compiler cannot count stores among
+// the loads they may overtake, so a wait for a load issued before a store
+// lasts until the store is done as well).
+template <int F16, int J>
+struct RowOut {
+    uint32_t w[J][3][F16 ? 1 : 2];
+};
+
+template <int F16, int EXACT, int J>
+__device__ __forceinline__ void pack_pair(RowOut<F16, J> &out, int j, const float (&o)[3][2])
+{
+#pragma unroll
+    for (int ch = 0; ch < 3; ++ch) {
+        if (F16 && !EXACT) {
+            // The conversion may fuse with the last product (one rounding
+            // to fp16 instead of two).
+            typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+            const f16x2 h = {(_Float16)o[ch][0], (_Float16)o[ch][1]};
+            out.w[j][ch][0] = __builtin_bit_cast(uint32_t, h);
+        } else if (F16) {
+            out.w[j][ch][0] = f16_bits(o[ch][0]) | (f16_bits(o[ch][1]) << 16);
+        } else {
+            out.w[j][ch][0] = __builtin_bit_cast(uint32_t, o[ch][0]);
+            out.w[j][ch][F16 ? 0 : 1] = __builtin_bit_cast(uint32_t, o[ch][1]);
+        }
+    }
+}
+
+// Store a lane's pairs of one output row (three planes).
+template <int F16, int J>
+__device__ __forceinline__ void store_row(uint8_t *orow, long long plane, int Cw, int lane,
+                                          const RowOut<F16, J> &out)
+{
+    constexpr int kEsz = F16 ? 2 : 4;
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+        const int c = pair_col(lane, j, Cw);
+        const uint32_t lo = (uint32_t)c * kEsz;
+        if ((Cw & 1) == 0) {  // every pair is whole and 2-element aligned
+#pragma unroll
+            for (int ch = 0; ch < 3; ++ch) {
+                uint8_t *dst = orow + ch * plane + lo;
+                if (F16) {
+                    __builtin_nontemporal_store(out.w[j][ch][0], (uint32_t *)dst);
+                } else {
+                    typedef uint32_t u32x2v __attribute__((ext_vector_type(2)));
+                    const u32x2v w = {out.w[j][ch][0], out.w[j][ch][F16 ? 0 : 1]};
+                    __builtin_nontemporal_store(w, (u32x2v *)dst);
+                }
+            }
+        } else {
+            // odd Cw: element c + 1 is the last column again past the end
+            // (its value is that column's too)
+            const uint32_t lo1 = (uint32_t)min(c + 1, Cw - 1) * kEsz;
+#pragma unroll
+            for (int ch = 0; ch < 3; ++ch) {
+                uint8_t *dst = orow + ch * plane;
+                if (F16) {
+                    *(uint16_t *)(dst + lo) = (uint16_t)out.w[j][ch][0];
+                    *(uint16_t *)(dst + lo1) = (uint16_t)(out.w[j][ch][0] >> 16);
+                } else {
+                    *(uint32_t *)(dst + lo) = out.w[j][ch][0];
+                    *(uint32_t *)(dst + lo1) = out.w[j][ch][F16 ? 0 : 1];
+                }
+            }
+        }
+    }
+}
+
 // Interpolate, normalise and store one output row from its staged rows
 // (row 0 at byte `row0` of lds, row 1 at `row1`, both including the offset
 // of the first byte in its chunk).
 template <int F16, int J, int EXACT>
-__device__ __forceinline__ void rows_compute(const BatchArgs &a, const NormK &nk, uint8_t *orow,
-                                             uint32_t row0, uint32_t row1, float wy,
-                                             const int (&cx)[J][2], const float (&cw)[J][2],
-                                             int lane)
+__device__ __forceinline__ void rows_compute(const NormK &nk, uint32_t row0, uint32_t row1,
+                                             float wy, const int (&cx)[J][2],
+                                             const float (&cw)[J][2], RowOut<F16, J> &out)
 {
-    const int Cw = a.Cw;
-    constexpr int kEsz = F16 ? 2 : 4;
-    const long long plane = (long long)a.Ch * Cw * kEsz;
-    const bool pairs = (Cw & 1) == 0;  // every pair is whole and 2-element aligned
     // tap pairs, 4 per column iteration: pixel c and c + 1 of row 0, then row 1
-    // (lanes past the crop read column 0 and store nothing)
     constexpr int kN = J == 1 ? 4 : 8;
     uint64_t v[J * 4];
 #pragma unroll
@@ -473,60 +586,90 @@ __device__ __forceinline__ void rows_compute(const BatchArgs &a, const NormK &nk
         read_taps<J, kN>(row0, row1, cx, j0, *(uint64_t(*)[kN]) & v[4 * j0]);
 #pragma unroll
     for (int j = 0; j < J; ++j) {
-        const int c = 2 * lane + 128 * j;
-        if (c < Cw) {
-            float o[3][2];
+        float o[3][2];
 #pragma unroll
-            for (int px = 0; px < 2; ++px) {
-                float pa[3], pd[3], qa[3], qd[3];
-                unpack_ad(v[4 * j + px], pa, pd);
-                unpack_ad(v[4 * j + 2 + px], qa, qd);
+        for (int px = 0; px < 2; ++px) {
+            float pa[3], pd[3], qa[3], qd[3];
+            unpack_ad(v[4 * j + px], pa, pd);
+            unpack_ad(v[4 * j + 2 + px], qa, qd);
 #pragma unroll
-                for (int ch = 0; ch < 3; ++ch) {
-                    const float top = lerp_ad(pa[ch], pd[ch], cw[j][px]);
-                    const float bot = lerp_ad(qa[ch], qd[ch], cw[j][px]);
-                    o[ch][px] = normalize_k<EXACT>(nk, ch, lerp(top, bot, wy));
-                }
-            }
-            const uint32_t lo = (uint32_t)c * kEsz;
-            if (pairs) {
-#pragma unroll
-                for (int ch = 0; ch < 3; ++ch) {
-                    uint8_t *dst = orow + ch * plane + lo;
-                    if (F16 && !EXACT) {
-                        // The conversion may fuse with the last product (one
-                        // rounding to fp16 instead of two).
-                        typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
-                        const f16x2 h = {(_Float16)o[ch][0], (_Float16)o[ch][1]};
-                        __builtin_nontemporal_store(__builtin_bit_cast(uint32_t, h),
-                                                    (uint32_t *)dst);
-                    } else if (F16) {
-                        __builtin_nontemporal_store(f16_bits(o[ch][0]) | (f16_bits(o[ch][1]) << 16),
-                                                    (uint32_t *)dst);
-                    } else {
-                        typedef float f32x2 __attribute__((ext_vector_type(2)));
-                        const f32x2 w = {o[ch][0], o[ch][1]};
-                        __builtin_nontemporal_store(w, (f32x2 *)dst);
-                    }
-                }
-            } else {
-                const bool second = c + 1 < Cw;
-#pragma unroll
-                for (int ch = 0; ch < 3; ++ch) {
-                    uint8_t *dst = orow + ch * plane + lo;
-                    if (F16) {
-                        ((uint16_t *)dst)[0] = (uint16_t)f16_bits(o[ch][0]);
-                        if (second)
-                            ((uint16_t *)dst)[1] = (uint16_t)f16_bits(o[ch][1]);
-                    } else {
-                        ((float *)dst)[0] = o[ch][0];
-                        if (second)
-                            ((float *)dst)[1] = o[ch][1];
-                    }
-                }
+            for (int ch = 0; ch < 3; ++ch) {
+                const float top = lerp_ad(pa[ch], pd[ch], cw[j][px]);
+                const float bot = lerp_ad(qa[ch], qd[ch], cw[j][px]);
+                o[ch][px] = normalize_k<EXACT>(nk, ch, lerp(top, bot, wy));
             }
         }
+        pack_pair<F16, EXACT, J>(out, j, o);
     }
+}
+
+// Horizontal lerps of one staged row at the lane's columns: h[j][px][ch].
+template <int J>
+__device__ __forceinline__ void rows_horizontal(uint32_t row, const int (&cx)[J][2],
+                                                const float (&cw)[J][2], float (&h)[J][2][3])
+{
+    uint64_t v[2 * J];
+    read_row_taps<J>(row, cx, v);
+#pragma unroll
+    for (int j = 0; j < J; ++j)
+#pragma unroll
+        for (int px = 0; px < 2; ++px) {
+            float pa[3], pd[3];
+            unpack_ad(v[2 * j + px], pa, pd);
+#pragma unroll
+            for (int ch = 0; ch < 3; ++ch)
+                h[j][px][ch] = lerp_ad(pa[ch], pd[ch], cw[j][px]);
+        }
+}
+
+// Vertical lerp of two rows of horizontal lerps, normalise, store.
+template <int F16, int J, int EXACT>
+__device__ __forceinline__ void rows_vertical(const NormK &nk, const float (&h0)[J][2][3],
+                                              const float (&h1)[J][2][3], float wy,
+                                              RowOut<F16, J> &out)
+{
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+        float o[3][2];
+#pragma unroll
+        for (int px = 0; px < 2; ++px)
+#pragma unroll
+            for (int ch = 0; ch < 3; ++ch)
+                o[ch][px] = normalize_k<EXACT>(nk, ch, lerp(h0[j][px][ch], h1[j][px][ch], wy));
+        pack_pair<F16, EXACT, J>(out, j, o);
+    }
+}
+
+// One output row with horizontal lerps kept across rows (contiguous row
+// ranges): a wave walking consecutive output rows of an upscale, or of a
+// downscale by less than 2, meets the same source row again, and its
+// horizontal lerps at the same columns are the same numbers. (py0, py1) are
+// the source rows whose lerps h0, h1 hold, -1 when none (a new image or new
+// column taps).
+template <int F16, int J, int EXACT>
+__device__ __forceinline__ void rows_compute_reuse(const NormK &nk, uint32_t row0, uint32_t row1,
+                                                   float wy, int y0, int y1, int &py0, int &py1,
+                                                   float (&h0)[J][2][3], float (&h1)[J][2][3],
+                                                   const int (&cx)[J][2],
+                                                   const float (&cw)[J][2], RowOut<F16, J> &out)
+{
+    const bool same = y0 == py0 && y1 == py1;
+    if (!same && y0 == py1) {
+#pragma unroll
+        for (int j = 0; j < J; ++j)
+#pragma unroll
+            for (int px = 0; px < 2; ++px)
+#pragma unroll
+                for (int ch = 0; ch < 3; ++ch)
+                    h0[j][px][ch] = h1[j][px][ch];
+    } else if (!same) {
+        rows_horizontal<J>(row0, cx, cw, h0);
+    }
+    if (!same)
+        rows_horizontal<J>(row1, cx, cw, h1);
+    py0 = y0;
+    py1 = y1;
+    rows_vertical<F16, J, EXACT>(nk, h0, h1, wy, out);
 }
 
 template <int F16, int J, int EXACT, int G, int P, int STRIDE>
@@ -595,17 +738,35 @@ __global__ void __launch_bounds__(64 * kRowsMaxWavesPerGroup) rgb_rows_kernel(Ba
         advance();
     }
     write_rows<G>(lds, A, lane);
-    int csh0 = A.sh0, csh1 = A.sh1;
+    int csh0 = A.sh0, csh1 = A.sh1, cy0 = A.y0, cy1 = A.y1;
     float cwy = A.wy;
+    // Contiguous ranges keep the horizontal lerps of the last two source
+    // rows (see rows_compute_reuse); J = 4 would need 48 more registers.
+    constexpr bool kReuse = STRIDE == 0 && J <= 2;
+    float h0[J][2][3], h1[J][2][3];
+    int py0 = -1, py1 = -1;
+    const long long plane = (long long)Ch * a.Cw * kEsz;
+    RowOut<F16, J> out;
+    auto compute = [&]() {
+        if constexpr (kReuse)
+            rows_compute_reuse<F16, J, EXACT>(nk, lds0 + (uint32_t)csh0,
+                                              lds0 + (uint32_t)(1024 * G + csh1), cwy, cy0, cy1,
+                                              py0, py1, h0, h1, cx, cw, out);
+        else
+            rows_compute<F16, J, EXACT>(nk, lds0 + (uint32_t)csh0,
+                                        lds0 + (uint32_t)(1024 * G + csh1), cwy, cx, cw, out);
+    };
 #define SMOL_ROWS_STEP(NXT, FUT)                                                              \
     {                                                                                         \
         load_rows<G>(FUT, lc, lane, at_end);                                                  \
         advance();                                                                            \
-        rows_compute<F16, J, EXACT>(a, nk, orow, lds0 + (uint32_t)csh0,                       \
-                                    lds0 + (uint32_t)(1024 * G + csh1), cwy, cx, cw, lane);   \
+        compute();                                                                            \
         write_rows<G>(lds, NXT, lane);                                                        \
+        store_row<F16, J>(orow, plane, a.Cw, lane, out);                                      \
         csh0 = NXT.sh0;                                                                       \
         csh1 = NXT.sh1;                                                                       \
+        cy0 = NXT.y0;                                                                         \
+        cy1 = NXT.y1;                                                                         \
         cwy = NXT.wy;                                                                         \
         const int pimg = c_img;                                                               \
         c_img += step.di;                                                                     \
@@ -617,6 +778,7 @@ __global__ void __launch_bounds__(64 * kRowsMaxWavesPerGroup) rgb_rows_kernel(Ba
             orow += owrap;                                                                    \
         }                                                                                     \
         if (c_img != pimg) {                                                                  \
+            py0 = py1 = -1; /* another image's rows */                                        \
             const RowImg g = row_img(a, c_img);                                               \
             if (g.W != cW || g.Wr != cWr || g.left != cleft) {                                \
                 cW = g.W;                                                                     \
@@ -642,8 +804,8 @@ __global__ void __launch_bounds__(64 * kRowsMaxWavesPerGroup) rgb_rows_kernel(Ba
             SMOL_ROWS_STEP(A, A)
     }
 #undef SMOL_ROWS_STEP
-    rows_compute<F16, J, EXACT>(a, nk, orow, lds0 + (uint32_t)csh0,
-                                lds0 + (uint32_t)(1024 * G + csh1), cwy, cx, cw, lane);
+    compute();
+    store_row<F16, J>(orow, plane, a.Cw, lane, out);
 }
 
 // ---------------------------------------------------------------------------
@@ -836,7 +998,7 @@ __device__ __forceinline__ void yuv_cols(YuvCols<J> &k, const YuvImg &g, int Cw,
     for (int j = 0; j < J; ++j)
 #pragma unroll
         for (int px = 0; px < 2; ++px) {
-            const int c = min(2 * lane + 128 * j + px, Cw - 1);
+            const int c = min(pair_col(lane, j, Cw) + px, Cw - 1);
             const Tap t = axis_tap(g.left + c, g.W, g.Wr);
             const Tap a0 = chroma_tap(t.x0, Wc), a1 = chroma_tap(t.x1, Wc);
             k.ox[j][px] = t.x0 - g.xf;
@@ -895,18 +1057,13 @@ __device__ __forceinline__ float chroma16(uint32_t ra, uint32_t rb, uint32_t sel
 }
 
 template <int F16, int J, int EXACT>
-__device__ __forceinline__ void yuv_compute(const BatchArgs &a, const NormK &nk, uint8_t *orow,
-                                            uint32_t slot, const int (&sh)[8], float wy,
-                                            int fy0, int fy1, int b0, const YuvCols<J> &k,
-                                            int lane)
+__device__ __forceinline__ void yuv_compute(const NormK &nk, uint32_t slot, const int (&sh)[8],
+                                            float wy, int fy0, int fy1, int b0,
+                                            const YuvCols<J> &k, RowOut<F16, J> &out)
 {
     // weight bytes of luma row yi and column xi: hw(xi) * (4 + 65535 fy(yi))
     // = (4 - fy) * [4 - fx, fx, 0, 0] + fy * [0, 0, 4 - fx, fx] (no carries)
     const uint32_t vm[2] = {4u + 65535u * (uint32_t)fy0, 4u + 65535u * (uint32_t)fy1};
-    const int Cw = a.Cw;
-    constexpr int kEsz = F16 ? 2 : 4;
-    const long long plane = (long long)a.Ch * Cw * kEsz;
-    const bool pairs = (Cw & 1) == 0;
 #pragma unroll
     for (int j = 0; j < J; ++j) {
         float o[3][2];
@@ -949,44 +1106,7 @@ __device__ __forceinline__ void yuv_compute(const BatchArgs &a, const NormK &nk,
                     lerp(lerp(rgb[0][0][ch], rgb[0][1][ch], k.wx[j][px]),
                          lerp(rgb[1][0][ch], rgb[1][1][ch], k.wx[j][px]), wy));
         }
-        const int c = 2 * lane + 128 * j;
-        if (c < Cw) {
-            const uint32_t lo = (uint32_t)c * kEsz;
-            if (pairs) {
-#pragma unroll
-                for (int ch = 0; ch < 3; ++ch) {
-                    uint8_t *dst = orow + ch * plane + lo;
-                    if (F16 && !EXACT) {
-                        typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
-                        const f16x2 h = {(_Float16)o[ch][0], (_Float16)o[ch][1]};
-                        __builtin_nontemporal_store(__builtin_bit_cast(uint32_t, h),
-                                                    (uint32_t *)dst);
-                    } else if (F16) {
-                        __builtin_nontemporal_store(f16_bits(o[ch][0]) | (f16_bits(o[ch][1]) << 16),
-                                                    (uint32_t *)dst);
-                    } else {
-                        typedef float f32x2 __attribute__((ext_vector_type(2)));
-                        const f32x2 w = {o[ch][0], o[ch][1]};
-                        __builtin_nontemporal_store(w, (f32x2 *)dst);
-                    }
-                }
-            } else {
-                const bool second = c + 1 < Cw;
-#pragma unroll
-                for (int ch = 0; ch < 3; ++ch) {
-                    uint8_t *dst = orow + ch * plane + lo;
-                    if (F16) {
-                        ((uint16_t *)dst)[0] = (uint16_t)f16_bits(o[ch][0]);
-                        if (second)
-                            ((uint16_t *)dst)[1] = (uint16_t)f16_bits(o[ch][1]);
-                    } else {
-                        ((float *)dst)[0] = o[ch][0];
-                        if (second)
-                            ((float *)dst)[1] = o[ch][1];
-                    }
-                }
-            }
-        }
+        pack_pair<F16, EXACT, J>(out, j, o);
     }
 }
 
@@ -1035,6 +1155,8 @@ yuv_rows_kernel(BatchArgs a)
             ++lrow;
         }
     };
+    const long long plane = (long long)Ch * a.Cw * kEsz;
+    RowOut<F16, J> out;
     YuvStaged R;
     yuv_load(R, lc, lane, false);
     advance();
@@ -1049,8 +1171,9 @@ yuv_rows_kernel(BatchArgs a)
     for (int left = n_rows - 1; left > 0; --left) {
         yuv_load(R, lc, lane, false);
         advance();
-        yuv_compute<F16, J, EXACT>(a, nk, orow, lds0, csh, cwy, cfy0, cfy1, cb0, cols, lane);
+        yuv_compute<F16, J, EXACT>(nk, lds0, csh, cwy, cfy0, cfy1, cb0, cols, out);
         yuv_write(lds, R, lane);
+        store_row<F16, J>(orow, plane, a.Cw, lane, out);
 #pragma unroll
         for (int s = 0; s < 8; ++s)
             csh[s] = R.sh[s];
@@ -1077,7 +1200,8 @@ yuv_rows_kernel(BatchArgs a)
             }
         }
     }
-    yuv_compute<F16, J, EXACT>(a, nk, orow, lds0, csh, cwy, cfy0, cfy1, cb0, cols, lane);
+    yuv_compute<F16, J, EXACT>(nk, lds0, csh, cwy, cfy0, cfy1, cb0, cols, out);
+    store_row<F16, J>(orow, plane, a.Cw, lane, out);
 }
 
 
