@@ -150,24 +150,29 @@ def cpu_model() -> str:
     return "unknown"
 
 
-def copy_ceiling_gbps(torch, mib: int = 512, reps: int = 10) -> float:
-    """Read + write GB/s of a plain device-to-device copy (torch's copy
-    kernel) of `mib` MiB, the streaming ceiling the kernel is compared with."""
+def stream_ceilings_gbps(torch, mib: int = 512, reps: int = 10) -> dict:
+    """GB/s of plain streaming kernels over `mib` MiB buffers: a device copy
+    (read + write bytes) and a fill (write), ceilings the kernel's traffic
+    mix is compared with."""
     n = mib * 1024 * 1024
     a = torch.empty(n, dtype=torch.uint8, device="cuda:0")
     b = torch.empty_like(a)
     a.fill_(1)
-    for _ in range(2):
-        b.copy_(a)
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    e0.record()
-    for _ in range(reps):
-        b.copy_(a)
-    e1.record()
-    torch.cuda.synchronize()
-    return 2 * n * reps / (e0.elapsed_time(e1) / 1e3) / 1e9
+
+    def rate(fn, nbytes: int) -> float:
+        for _ in range(2):
+            fn()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return nbytes * reps / (e0.elapsed_time(e1) / 1e3) / 1e9
+
+    return {"copy": rate(lambda: b.copy_(a), 2 * n), "write": rate(lambda: b.fill_(3), n)}
 
 
 def load_traffic(config: str) -> dict | None:
@@ -287,7 +292,8 @@ def main() -> int:
     e1.record(stream)
     torch.cuda.synchronize()
     mall_us = 1e3 * e0.elapsed_time(e1) / args.steps
-    copy_gbps = None if args.profile_run else copy_ceiling_gbps(torch)
+    ceil = None if args.profile_run else stream_ceilings_gbps(torch)
+    copy_gbps = None if ceil is None else ceil["copy"]
 
     traffic = load_traffic(args.config)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
@@ -317,6 +323,7 @@ def main() -> int:
                    "hbm_gbps_wall": round(algo * args.steps / wall / 1e9, 1),
                    "mall_warm_us_per_step_one_set": round(mall_us, 3),
                    "copy_ceiling_gbps": None if copy_gbps is None else round(copy_gbps, 1),
+                   "write_ceiling_gbps": None if ceil is None else round(ceil["write"], 1),
                    "achieved_frac_of_copy_ceiling":
                        None if copy_gbps is None else round(achieved / copy_gbps, 4)},
         "roofline": roofline,
