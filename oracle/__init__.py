@@ -25,6 +25,12 @@ _LIB_PATH = os.path.join(_HERE, "libsmol_oracle.so")
 
 OUT_F32 = 0
 OUT_F16 = 1
+RESIZE_SHORT_CROP = 0
+RESIZE_DIRECT = 1
+NCHW = 0
+NHWC = 1
+CHROMA_CENTER = 0
+CHROMA_LEFT = 1
 
 # No -ffast-math, no -march: x86-64 SSE arithmetic is exact IEEE binary32, and
 # -ffp-contract=off keeps every multiply and add rounded on its own.
@@ -116,6 +122,17 @@ def _load():
         ctypes.c_void_p,
     ]
     lib.smol_ref_yuv420_preprocess_batch.restype = ctypes.c_int
+    P, I32, I64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    lib.oracle_yuv420_to_rgb_sited.argtypes = [P, P, P, I64, I64, I32, P]
+    lib.oracle_yuv420_to_rgb_sited.restype = None
+    lib.oracle_output_geometry.argtypes = [I64] * 5 + [I32] + [_i64p] * 4
+    lib.oracle_output_geometry.restype = None
+    lib.smol_ref_preprocess_batch_ex.argtypes = [P, I64, P, P, P, P, P, I32, I32, I32, I32, P, P,
+                                                 I32, I32, I32, P]
+    lib.smol_ref_preprocess_batch_ex.restype = ctypes.c_int
+    lib.smol_ref_yuv420_preprocess_batch_ex.argtypes = [P, I64, P, P, P, P, P, P, I32, I32, I32,
+                                                        I32, P, P, I32, I32, I32, I32, P]
+    lib.smol_ref_yuv420_preprocess_batch_ex.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -262,6 +279,97 @@ def yuv420_preprocess_batch(src: np.ndarray, y_offsets, cb_offsets, cr_offsets, 
                                                   bo.ctypes.data, ro.ctypes.data, w.ctypes.data,
                                                   h.ctypes.data, n, S, Ch, Cw, m.ctypes.data,
                                                   s.ctypes.data, out_dtype, out.ctypes.data)
+    if rc != 0:
+        raise ValueError("oracle rejected the arguments")
+    return _finish(out, out_dtype)
+
+
+# --------------------------------------------------------------------------
+# variants: region of interest, direct resize, NHWC, left-sited chroma
+# --------------------------------------------------------------------------
+
+
+def output_geometry(W: int, H: int, S: int, Ch: int, Cw: int,
+                    resize_mode: int = RESIZE_SHORT_CROP) -> tuple[int, int, int, int]:
+    """(Wr, Hr, left, top) of a W x H image (or ROI)."""
+    v = [ctypes.c_int64() for _ in range(4)]
+    _load().oracle_output_geometry(W, H, S, Ch, Cw, resize_mode, *[ctypes.byref(x) for x in v])
+    return tuple(x.value for x in v)
+
+
+def yuv420_to_rgb_sited(y: np.ndarray, cb: np.ndarray, cr: np.ndarray,
+                        siting: int = CHROMA_CENTER) -> np.ndarray:
+    """As ``yuv420_to_rgb`` with the chroma siting chosen."""
+    H, W = y.shape
+    y = np.ascontiguousarray(y, np.uint8)
+    cb = np.ascontiguousarray(cb, np.uint8)
+    cr = np.ascontiguousarray(cr, np.uint8)
+    assert cb.shape == ((H + 1) // 2, (W + 1) // 2) and cr.shape == cb.shape
+    out = np.empty((H, W, 3), np.float32)
+    _load().oracle_yuv420_to_rgb_sited(y.ctypes.data, cb.ctypes.data, cr.ctypes.data, W, H,
+                                       siting, out.ctypes.data)
+    return out
+
+
+def _out_array_ex(n: int, Ch: int, Cw: int, out_dtype: int, layout: int) -> np.ndarray:
+    shape = (n, Ch, Cw, 3) if layout == NHWC else (n, 3, Ch, Cw)
+    if out_dtype == OUT_F32:
+        return np.empty(shape, np.float32)
+    if out_dtype == OUT_F16:
+        return np.empty(shape, np.uint16)
+    raise ValueError("out_dtype must be OUT_F32 or OUT_F16")
+
+
+def _rois(rois, n: int):
+    if rois is None:
+        return None
+    r = np.ascontiguousarray(rois, np.int32).reshape(n, 4)
+    return r
+
+
+def preprocess_batch_ex(src: np.ndarray, offsets, widths, heights, pitches, rois, S: int,
+                        Ch: int, Cw: int, mean, std, out_dtype: int,
+                        resize_mode: int = RESIZE_SHORT_CROP, layout: int = NCHW) -> np.ndarray:
+    """RGB batch with an optional ROI per image ((x, y, w, h) rows), the
+    resize mode and the output layout."""
+    src = np.ascontiguousarray(src, np.uint8).reshape(-1)
+    n = len(offsets)
+    off = np.ascontiguousarray(offsets, np.int64)
+    w = np.ascontiguousarray(widths, np.int32)
+    h = np.ascontiguousarray(heights, np.int32)
+    p = None if pitches is None else np.ascontiguousarray(pitches, np.int32)
+    r = _rois(rois, n)
+    m, s = _vec3(mean), _vec3(std)
+    out = _out_array_ex(n, Ch, Cw, out_dtype, layout)
+    rc = _load().smol_ref_preprocess_batch_ex(
+        src.ctypes.data, src.size, off.ctypes.data, w.ctypes.data, h.ctypes.data,
+        None if p is None else p.ctypes.data, None if r is None else r.ctypes.data, n, S, Ch, Cw,
+        m.ctypes.data, s.ctypes.data, out_dtype, resize_mode, layout, out.ctypes.data)
+    if rc != 0:
+        raise ValueError("oracle rejected the arguments")
+    return _finish(out, out_dtype)
+
+
+def yuv420_preprocess_batch_ex(src: np.ndarray, y_offsets, cb_offsets, cr_offsets, widths,
+                               heights, rois, S: int, Ch: int, Cw: int, mean, std, out_dtype: int,
+                               resize_mode: int = RESIZE_SHORT_CROP, layout: int = NCHW,
+                               siting: int = CHROMA_CENTER) -> np.ndarray:
+    """I420 batch with an optional ROI per frame, resize mode, layout and
+    chroma siting."""
+    src = np.ascontiguousarray(src, np.uint8).reshape(-1)
+    n = len(y_offsets)
+    yo = np.ascontiguousarray(y_offsets, np.int64)
+    bo = np.ascontiguousarray(cb_offsets, np.int64)
+    ro = np.ascontiguousarray(cr_offsets, np.int64)
+    w = np.ascontiguousarray(widths, np.int32)
+    h = np.ascontiguousarray(heights, np.int32)
+    r = _rois(rois, n)
+    m, s = _vec3(mean), _vec3(std)
+    out = _out_array_ex(n, Ch, Cw, out_dtype, layout)
+    rc = _load().smol_ref_yuv420_preprocess_batch_ex(
+        src.ctypes.data, src.size, yo.ctypes.data, bo.ctypes.data, ro.ctypes.data, w.ctypes.data,
+        h.ctypes.data, None if r is None else r.ctypes.data, n, S, Ch, Cw, m.ctypes.data,
+        s.ctypes.data, out_dtype, resize_mode, layout, siting, out.ctypes.data)
     if rc != 0:
         raise ValueError("oracle rejected the arguments")
     return _finish(out, out_dtype)

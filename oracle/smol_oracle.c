@@ -41,6 +41,22 @@
  *     chroma sample that serves luma pixel x sits at x/2 - 1/4; each channel is
  *     clamped to [0, 255] in fp32 (no integer rounding) at every luma pixel,
  *     before the resize.
+ *
+ * Variants (the "_ex" calls), each a reading of a passage the paper leaves
+ * open:
+ *   - region of interest: the paper's partial-decoding discussion (section
+ *     5.3, "Leveraging partial decoding") lets a caller pass an ROI per image,
+ *     e.g. a face or detection crop, and only the ROI is processed. The ROI
+ *     (x, y, w, h) is cut out of the decoded image first and then treated as
+ *     a w x h image: the resize taps clamp at the ROI's edges. For I420 the
+ *     frame is converted to RGB first (chroma taps in frame coordinates,
+ *     clamped at the frame's chroma planes), then the ROI is cut;
+ *   - direct resize: the network's fixed input size (the section cites
+ *     224 x 224) reached without keeping the aspect ratio: the image (or ROI)
+ *     is resized to C_w x C_h and nothing is cropped;
+ *   - channels-last (NHWC) output instead of step 4's channels-first;
+ *   - left (co-sited) 4:2:0 chroma, as MPEG-2 / H.264 decoders emit: the
+ *     chroma sample of luma column x sits at x/2 (rows stay centred).
  */
 #include <math.h>
 #include <stdint.h>
@@ -48,6 +64,9 @@
 #include <string.h>
 
 enum { ORACLE_OUT_F32 = 0, ORACLE_OUT_F16 = 1 };
+enum { ORACLE_RESIZE_SHORT_CROP = 0, ORACLE_RESIZE_DIRECT = 1 };
+enum { ORACLE_NCHW = 0, ORACLE_NHWC = 1 };
+enum { ORACLE_CHROMA_CENTER = 0, ORACLE_CHROMA_LEFT = 1 };
 enum { ORACLE_OK = 0, ORACLE_ERR = -1 };
 
 /* ------------------------------------------------------------------------- */
@@ -154,11 +173,28 @@ static void chroma_tap(int64_t x, int64_t n, int64_t *c0, int64_t *c1, float *w)
     *w = u - (float)f;
 }
 
+/* Left (co-sited) siting, horizontal axis: the chroma coordinate of luma
+ * column x is u = x/2. */
+static void chroma_tap_left(int64_t x, int64_t n, int64_t *c0, int64_t *c1, float *w)
+{
+    float u = (float)x * 0.5f;
+    int64_t f = (int64_t)floorf(u);
+    if (f >= n - 1) {
+        *c0 = n - 1;
+        *c1 = n - 1;
+        *w = 0.0f;
+        return;
+    }
+    *c0 = f;
+    *c1 = f + 1;
+    *w = u - (float)f;
+}
+
 /* Planar I420 (Y: W x H, Cb and Cr: ceil(W/2) x ceil(H/2), tightly pitched)
  * to an fp32 RGB image, W x H x 3 interleaved: chroma is bilinearly upsampled
  * to every luma pixel, then converted and clamped there. */
-void oracle_yuv420_to_rgb(const uint8_t *yp, const uint8_t *cbp, const uint8_t *crp, int64_t W,
-                          int64_t H, float *rgb)
+void oracle_yuv420_to_rgb_sited(const uint8_t *yp, const uint8_t *cbp, const uint8_t *crp,
+                                int64_t W, int64_t H, int32_t siting, float *rgb)
 {
     int64_t Wc = (W + 1) / 2, Hc = (H + 1) / 2;
     for (int64_t y = 0; y < H; ++y) {
@@ -168,7 +204,10 @@ void oracle_yuv420_to_rgb(const uint8_t *yp, const uint8_t *cbp, const uint8_t *
         for (int64_t x = 0; x < W; ++x) {
             int64_t k0, k1;
             float wx;
-            chroma_tap(x, Wc, &k0, &k1, &wx);
+            if (siting == ORACLE_CHROMA_LEFT)
+                chroma_tap_left(x, Wc, &k0, &k1, &wx);
+            else
+                chroma_tap(x, Wc, &k0, &k1, &wx);
             float c[2];
             const uint8_t *planes[2] = {cbp, crp};
             for (int p = 0; p < 2; ++p) {
@@ -183,6 +222,12 @@ void oracle_yuv420_to_rgb(const uint8_t *yp, const uint8_t *cbp, const uint8_t *
             oracle_ycbcr_to_rgb((float)yp[y * W + x], c[0], c[1], &rgb[(y * W + x) * 3]);
         }
     }
+}
+
+void oracle_yuv420_to_rgb(const uint8_t *yp, const uint8_t *cbp, const uint8_t *crp, int64_t W,
+                          int64_t H, float *rgb)
+{
+    oracle_yuv420_to_rgb_sited(yp, cbp, crp, W, H, ORACLE_CHROMA_CENTER, rgb);
 }
 
 /* ------------------------------------------------------------------------- */
@@ -228,14 +273,32 @@ uint16_t oracle_f32_to_f16(float f)
 /* Resize + crop + normalise + NCHW store                                     */
 /* ------------------------------------------------------------------------- */
 
-/* rgb: fp32 image, W x H x 3 interleaved. out: 3 x Ch x Cw of the out dtype. */
-static void resample_crop_normalize(const float *rgb, int64_t W, int64_t H, int64_t S,
-                                    int64_t Ch, int64_t Cw, const float *mean, const float *stdv,
-                                    int out_dtype, void *out)
+/* Resized size and crop offsets of a W x H image: step 2's short-side resize
+ * and central crop, or the direct resize to C_w x C_h (no crop). */
+void oracle_output_geometry(int64_t W, int64_t H, int64_t S, int64_t Ch, int64_t Cw,
+                            int32_t resize_mode, int64_t *Wr, int64_t *Hr, int64_t *left,
+                            int64_t *top)
+{
+    if (resize_mode == ORACLE_RESIZE_DIRECT) {
+        *Wr = Cw;
+        *Hr = Ch;
+        *left = 0;
+        *top = 0;
+        return;
+    }
+    oracle_resized_dims(W, H, S, Wr, Hr);
+    oracle_crop_offsets(*Wr, *Hr, Ch, Cw, left, top);
+}
+
+/* rgb: fp32 image, W x H x 3 interleaved (rows `rstride` floats apart).
+ * out: 3 x Ch x Cw (NCHW) or Ch x Cw x 3 (NHWC) of the out dtype. */
+static void resample_crop_normalize(const float *rgb, int64_t rstride, int64_t W, int64_t H,
+                                    int64_t S, int64_t Ch, int64_t Cw, const float *mean,
+                                    const float *stdv, int out_dtype, int32_t resize_mode,
+                                    int32_t layout, void *out)
 {
     int64_t Wr, Hr, left, top;
-    oracle_resized_dims(W, H, S, &Wr, &Hr);
-    oracle_crop_offsets(Wr, Hr, Ch, Cw, &left, &top);
+    oracle_output_geometry(W, H, S, Ch, Cw, resize_mode, &Wr, &Hr, &left, &top);
     for (int64_t yc = 0; yc < Ch; ++yc) {
         int64_t y0, y1;
         float wy;
@@ -245,15 +308,16 @@ static void resample_crop_normalize(const float *rgb, int64_t W, int64_t H, int6
             float wx;
             oracle_axis_tap(xc + left, W, Wr, &x0, &x1, &wx);
             for (int c = 0; c < 3; ++c) {
-                float p00 = rgb[(y0 * W + x0) * 3 + c];
-                float p01 = rgb[(y0 * W + x1) * 3 + c];
-                float p10 = rgb[(y1 * W + x0) * 3 + c];
-                float p11 = rgb[(y1 * W + x1) * 3 + c];
+                float p00 = rgb[y0 * rstride + x0 * 3 + c];
+                float p01 = rgb[y0 * rstride + x1 * 3 + c];
+                float p10 = rgb[y1 * rstride + x0 * 3 + c];
+                float p11 = rgb[y1 * rstride + x1 * 3 + c];
                 float t = p00 + wx * (p01 - p00);
                 float b = p10 + wx * (p11 - p10);
                 float v = t + wy * (b - t);
                 float o = (v - mean[c]) / stdv[c];
-                int64_t idx = ((int64_t)c * Ch + yc) * Cw + xc;
+                int64_t idx = layout == ORACLE_NHWC ? (yc * Cw + xc) * 3 + c
+                                                    : ((int64_t)c * Ch + yc) * Cw + xc;
                 if (out_dtype == ORACLE_OUT_F32)
                     ((float *)out)[idx] = o;
                 else
@@ -263,14 +327,18 @@ static void resample_crop_normalize(const float *rgb, int64_t W, int64_t H, int6
     }
 }
 
-static int params_ok(int64_t W, int64_t H, int32_t S, int32_t Ch, int32_t Cw, int32_t out_dtype)
+static int params_ok_ex(int64_t W, int64_t H, int32_t S, int32_t Ch, int32_t Cw,
+                        int32_t out_dtype, int32_t resize_mode, int32_t layout)
 {
     if (W < 1 || H < 1 || S < 1 || Ch < 1 || Cw < 1)
         return 0;
     if (out_dtype != ORACLE_OUT_F32 && out_dtype != ORACLE_OUT_F16)
         return 0;
-    int64_t Wr, Hr;
-    oracle_resized_dims(W, H, S, &Wr, &Hr);
+    if ((resize_mode != ORACLE_RESIZE_SHORT_CROP && resize_mode != ORACLE_RESIZE_DIRECT) ||
+        (layout != ORACLE_NCHW && layout != ORACLE_NHWC))
+        return 0;
+    int64_t Wr, Hr, left, top;
+    oracle_output_geometry(W, H, S, Ch, Cw, resize_mode, &Wr, &Hr, &left, &top);
     if (Ch > Hr || Cw > Wr) /* the crop must lie inside the resized image */
         return 0;
     /* the fp32 weight needs 2*out < 2^24 to be formed from exact operands */
@@ -279,20 +347,64 @@ static int params_ok(int64_t W, int64_t H, int32_t S, int32_t Ch, int32_t Cw, in
     return 1;
 }
 
+/* A region of interest inside a W x H image. */
+static int roi_ok(int64_t W, int64_t H, int32_t rx, int32_t ry, int32_t rw, int32_t rh)
+{
+    return rx >= 0 && ry >= 0 && rw >= 1 && rh >= 1 && rx + (int64_t)rw <= W &&
+           ry + (int64_t)rh <= H;
+}
+
+/* One packed HWC RGB uint8 image (row pitch in bytes): the ROI (rx, ry, rw,
+ * rh) cut out, resized, cropped, normalised, in the given layout. */
+int smol_ref_preprocess_image_ex(const uint8_t *img, int32_t W, int32_t H, int32_t pitch,
+                                 int32_t rx, int32_t ry, int32_t rw, int32_t rh, int32_t S,
+                                 int32_t Ch, int32_t Cw, const float *mean, const float *stdv,
+                                 int32_t out_dtype, int32_t resize_mode, int32_t layout,
+                                 void *out)
+{
+    if (W < 1 || H < 1 || pitch < 3 * W || !roi_ok(W, H, rx, ry, rw, rh) ||
+        !params_ok_ex(rw, rh, S, Ch, Cw, out_dtype, resize_mode, layout))
+        return ORACLE_ERR;
+    float *rgb = (float *)malloc((size_t)rw * (size_t)rh * 3 * sizeof(float));
+    if (!rgb)
+        return ORACLE_ERR;
+    for (int64_t y = 0; y < rh; ++y)
+        for (int64_t x = 0; x < 3 * (int64_t)rw; ++x)
+            rgb[y * 3 * rw + x] = (float)img[(ry + y) * (int64_t)pitch + 3 * (int64_t)rx + x];
+    resample_crop_normalize(rgb, 3 * (int64_t)rw, rw, rh, S, Ch, Cw, mean, stdv, out_dtype,
+                            resize_mode, layout, out);
+    free(rgb);
+    return ORACLE_OK;
+}
+
 /* One packed HWC RGB uint8 image (row pitch in bytes) -> 3 x Ch x Cw. */
 int smol_ref_preprocess_image(const uint8_t *img, int32_t W, int32_t H, int32_t pitch, int32_t S,
                               int32_t Ch, int32_t Cw, const float *mean, const float *stdv,
                               int32_t out_dtype, void *out)
 {
-    if (!params_ok(W, H, S, Ch, Cw, out_dtype) || pitch < 3 * W)
+    return smol_ref_preprocess_image_ex(img, W, H, pitch, 0, 0, W, H, S, Ch, Cw, mean, stdv,
+                                        out_dtype, ORACLE_RESIZE_SHORT_CROP, ORACLE_NCHW, out);
+}
+
+/* One planar I420 frame: converted to RGB at every luma pixel (chroma sited
+ * as given), the ROI cut out of that, then resized, cropped, normalised. */
+int smol_ref_yuv420_preprocess_image_ex(const uint8_t *yp, const uint8_t *cbp,
+                                        const uint8_t *crp, int32_t W, int32_t H, int32_t rx,
+                                        int32_t ry, int32_t rw, int32_t rh, int32_t S, int32_t Ch,
+                                        int32_t Cw, const float *mean, const float *stdv,
+                                        int32_t out_dtype, int32_t resize_mode, int32_t layout,
+                                        int32_t siting, void *out)
+{
+    if (W < 1 || H < 1 || !roi_ok(W, H, rx, ry, rw, rh) ||
+        !params_ok_ex(rw, rh, S, Ch, Cw, out_dtype, resize_mode, layout) ||
+        (siting != ORACLE_CHROMA_CENTER && siting != ORACLE_CHROMA_LEFT))
         return ORACLE_ERR;
     float *rgb = (float *)malloc((size_t)W * (size_t)H * 3 * sizeof(float));
     if (!rgb)
         return ORACLE_ERR;
-    for (int64_t y = 0; y < H; ++y)
-        for (int64_t x = 0; x < 3 * (int64_t)W; ++x)
-            rgb[y * 3 * W + x] = (float)img[y * (int64_t)pitch + x];
-    resample_crop_normalize(rgb, W, H, S, Ch, Cw, mean, stdv, out_dtype, out);
+    oracle_yuv420_to_rgb_sited(yp, cbp, crp, W, H, siting, rgb);
+    resample_crop_normalize(rgb + ((int64_t)ry * W + rx) * 3, 3 * (int64_t)W, rw, rh, S, Ch, Cw,
+                            mean, stdv, out_dtype, resize_mode, layout, out);
     free(rgb);
     return ORACLE_OK;
 }
@@ -303,20 +415,71 @@ int smol_ref_yuv420_preprocess_image(const uint8_t *yp, const uint8_t *cbp, cons
                                      const float *mean, const float *stdv, int32_t out_dtype,
                                      void *out)
 {
-    if (!params_ok(W, H, S, Ch, Cw, out_dtype))
-        return ORACLE_ERR;
-    float *rgb = (float *)malloc((size_t)W * (size_t)H * 3 * sizeof(float));
-    if (!rgb)
-        return ORACLE_ERR;
-    oracle_yuv420_to_rgb(yp, cbp, crp, W, H, rgb);
-    resample_crop_normalize(rgb, W, H, S, Ch, Cw, mean, stdv, out_dtype, out);
-    free(rgb);
-    return ORACLE_OK;
+    return smol_ref_yuv420_preprocess_image_ex(yp, cbp, crp, W, H, 0, 0, W, H, S, Ch, Cw, mean,
+                                               stdv, out_dtype, ORACLE_RESIZE_SHORT_CROP,
+                                               ORACLE_NCHW, ORACLE_CHROMA_CENTER, out);
 }
 
 static size_t out_image_bytes(int32_t Ch, int32_t Cw, int32_t out_dtype)
 {
     return (size_t)3 * (size_t)Ch * (size_t)Cw * (out_dtype == ORACLE_OUT_F32 ? 4u : 2u);
+}
+
+/* Batch of packed HWC RGB images with an optional ROI table (rois: n x
+ * {x, y, w, h}, or NULL for whole images). */
+int smol_ref_preprocess_batch_ex(const uint8_t *src, int64_t src_bytes, const int64_t *offsets,
+                                 const int32_t *widths, const int32_t *heights,
+                                 const int32_t *pitches, const int32_t *rois, int32_t n,
+                                 int32_t S, int32_t Ch, int32_t Cw, const float *mean,
+                                 const float *stdv, int32_t out_dtype, int32_t resize_mode,
+                                 int32_t layout, void *out)
+{
+    size_t ob = out_image_bytes(Ch, Cw, out_dtype);
+    for (int32_t i = 0; i < n; ++i) {
+        int32_t pitch = pitches ? pitches[i] : 3 * widths[i];
+        int64_t end = offsets[i] + (int64_t)(heights[i] - 1) * pitch + 3 * (int64_t)widths[i];
+        if (offsets[i] < 0 || end > src_bytes)
+            return ORACLE_ERR;
+        const int32_t *r = rois ? rois + 4 * (size_t)i : NULL;
+        int rc = smol_ref_preprocess_image_ex(src + offsets[i], widths[i], heights[i], pitch,
+                                              r ? r[0] : 0, r ? r[1] : 0, r ? r[2] : widths[i],
+                                              r ? r[3] : heights[i], S, Ch, Cw, mean, stdv,
+                                              out_dtype, resize_mode, layout,
+                                              (uint8_t *)out + ob * i);
+        if (rc)
+            return rc;
+    }
+    return ORACLE_OK;
+}
+
+/* Batch of planar I420 frames with per-frame plane offsets and an optional
+ * ROI table. */
+int smol_ref_yuv420_preprocess_batch_ex(const uint8_t *src, int64_t src_bytes,
+                                        const int64_t *y_offsets, const int64_t *cb_offsets,
+                                        const int64_t *cr_offsets, const int32_t *widths,
+                                        const int32_t *heights, const int32_t *rois, int32_t n,
+                                        int32_t S, int32_t Ch, int32_t Cw, const float *mean,
+                                        const float *stdv, int32_t out_dtype,
+                                        int32_t resize_mode, int32_t layout, int32_t siting,
+                                        void *out)
+{
+    size_t ob = out_image_bytes(Ch, Cw, out_dtype);
+    for (int32_t i = 0; i < n; ++i) {
+        int64_t W = widths[i], H = heights[i];
+        int64_t Wc = (W + 1) / 2, Hc = (H + 1) / 2;
+        if (y_offsets[i] < 0 || y_offsets[i] + W * H > src_bytes || cb_offsets[i] < 0 ||
+            cb_offsets[i] + Wc * Hc > src_bytes || cr_offsets[i] < 0 ||
+            cr_offsets[i] + Wc * Hc > src_bytes)
+            return ORACLE_ERR;
+        const int32_t *r = rois ? rois + 4 * (size_t)i : NULL;
+        int rc = smol_ref_yuv420_preprocess_image_ex(
+            src + y_offsets[i], src + cb_offsets[i], src + cr_offsets[i], widths[i], heights[i],
+            r ? r[0] : 0, r ? r[1] : 0, r ? r[2] : widths[i], r ? r[3] : heights[i], S, Ch, Cw,
+            mean, stdv, out_dtype, resize_mode, layout, siting, (uint8_t *)out + ob * i);
+        if (rc)
+            return rc;
+    }
+    return ORACLE_OK;
 }
 
 /* Batch of packed HWC RGB images; image i starts at src + offsets[i] and has
