@@ -35,7 +35,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=400)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--config", default="c4", choices=["c1", "c2", "c3", "c4", "c5"])
+    ap.add_argument("--config", default="c4", choices=["c1", "c2", "c3", "c4", "c5", "c6"])
     ap.add_argument("--rotate", type=int, default=0,
                     help="input/output sets cycled through (0: enough to defeat the MALL)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
@@ -59,12 +59,15 @@ def algorithmic_bytes(wl, smol) -> int:
     its vertical taps read times the crop's source column span (per plane for
     I420), plus the output."""
     p = smol.make_params(wl.resize_short, wl.crop_h, wl.crop_w, wl.mean, wl.std, wl.out_dtype)
+    opts = smol.make_options(wl.resize_mode, wl.layout, wl.siting)
+    rois = [None] * wl.n if wl.rois is None else [tuple(r) for r in wl.rois.tolist()]
     total = 0
     cache = {}
-    for w, h in zip(wl.widths.tolist(), wl.heights.tolist()):
-        key = (w, h)
+    for w, h, roi in zip(wl.widths.tolist(), wl.heights.tolist(), rois):
+        key = (w, h, roi)
         if key not in cache:
-            g = smol.image_geometry(w, h, p, yuv420=(wl.kind == "yuv420"))
+            g = smol.image_geometry_ex(w, h, p, yuv420=(wl.kind == "yuv420"), roi=roi,
+                                       options=opts)
             span = g["src_x_last"] - g["src_x_first"] + 1
             if wl.kind == "rgb":
                 rd = g["src_rows"] * span * 3
@@ -97,7 +100,21 @@ def cpu_baseline(wl, seconds: float, threads: int) -> dict:
 
     def one(i: int, t: int) -> None:
         o = outs[t].ctypes.data
-        if wl.kind == "rgb":
+        if wl.variant:
+            W, H = int(wl.widths[i]), int(wl.heights[i])
+            roi = (0, 0, W, H) if wl.rois is None else tuple(int(v) for v in wl.rois[i])
+            if wl.kind == "rgb":
+                pitch = 3 * W if wl.pitches is None else int(wl.pitches[i])
+                rc = oracle.preprocess_image_ex_into(base + int(wl.offsets[i]), W, H, pitch, roi,
+                                                     wl.resize_short, wl.crop_h, wl.crop_w, mean,
+                                                     std, wl.out_dtype, wl.resize_mode,
+                                                     wl.layout, o)
+            else:
+                rc = oracle.yuv420_preprocess_image_ex_into(
+                    base + int(wl.y_offsets[i]), base + int(wl.cb_offsets[i]),
+                    base + int(wl.cr_offsets[i]), W, H, roi, wl.resize_short, wl.crop_h,
+                    wl.crop_w, mean, std, wl.out_dtype, wl.resize_mode, wl.layout, wl.siting, o)
+        elif wl.kind == "rgb":
             pitch = 3 * int(wl.widths[i]) if wl.pitches is None else int(wl.pitches[i])
             rc = oracle.preprocess_image_into(base + int(wl.offsets[i]), int(wl.widths[i]),
                                               int(wl.heights[i]), pitch, wl.resize_short,
@@ -239,8 +256,7 @@ def main() -> int:
     src0 = torch.from_numpy(wl.src).to(dev)
     srcs = [src0] + [src0.clone() for _ in range(rotate - 1)]
     odt = torch.float16 if wl.out_dtype == synthetic.OUT_F16 else torch.float32
-    outs = [torch.empty((wl.n, 3, wl.crop_h, wl.crop_w), dtype=odt, device=dev)
-            for _ in range(rotate)]
+    outs = [torch.empty(wl.out_shape(), dtype=odt, device=dev) for _ in range(rotate)]
     call = smol.PreparedCall(wl)
     stream = torch.cuda.current_stream()
     sh = stream.cuda_stream

@@ -127,7 +127,7 @@ typedef struct smol_geometry {
  *
  * Host tables and p are read before the call returns. When the images do not
  * share one size and a constant offset stride, the call uploads a per-image
- * descriptor table (64 bytes per image) through a pinned staging buffer that
+ * descriptor table (80 bytes per image) through a pinned staging buffer that
  * the library keeps per device and reuses in stream order.
  *
  * Returns SMOL_OK, SMOL_ERR_INVALID_ARG (nothing enqueued),
@@ -164,6 +164,85 @@ int smol_yuv420_preprocess_batch(const uint8_t *src, int64_t src_bytes, const in
  * device. Returns SMOL_OK or SMOL_ERR_INVALID_ARG / SMOL_ERR_UNSUPPORTED. */
 int smol_image_geometry(int32_t width, int32_t height, int32_t yuv420, const smol_params *p,
                         smol_geometry *g);
+
+/* ------------------------------------------------------------------------
+ * Variants: region of interest, direct resize, channels-last, chroma siting.
+ *
+ * Section 5.3 ("Leveraging partial decoding") lets a caller give an ROI per
+ * image (a face, a detection box, the central crop) so that only the ROI is
+ * processed, and notes that networks take fixed input sizes (224 x 224 for
+ * ResNet-50). Semantics:
+ *   - ROI (x, y, w, h), luma pixels for I420: 0 <= x, 0 <= y, w, h >= 1,
+ *     x + w <= width, y + h <= height. The ROI is cut out of the decoded image
+ *     and processed as a w x h image: the resize taps clamp at the ROI's
+ *     edges. For I420 the frame is converted first: chroma taps use frame
+ *     coordinates and clamp at the frame's chroma planes.
+ *   - resize_mode SMOL_RESIZE_SHORT_CROP: step 2 as above (short side to S,
+ *     central crop); SMOL_RESIZE_DIRECT: the image (or ROI) is resized to
+ *     crop_w x crop_h, aspect ratio not kept, nothing cropped (resize_short
+ *     is then not used, but must still be valid).
+ *   - layout SMOL_LAYOUT_NCHW (step 4) or SMOL_LAYOUT_NHWC: n x crop_h x
+ *     crop_w x 3, channels last.
+ *   - chroma_siting (I420 only) SMOL_CHROMA_CENTER: chroma of luma column x
+ *     at x/2 - 1/4 (JPEG); SMOL_CHROMA_LEFT: at x/2 (co-sited, as MPEG-2 and
+ *     H.264 decoders emit). Rows are centred (y/2 - 1/4) in both.
+ * NHWC output runs on the row-streaming and direct kernels only: with it,
+ * a forced LDS-staged or register-gather path fails with
+ * SMOL_ERR_UNSUPPORTED. */
+#define SMOL_RESIZE_SHORT_CROP 0
+#define SMOL_RESIZE_DIRECT 1
+#define SMOL_LAYOUT_NCHW 0
+#define SMOL_LAYOUT_NHWC 1
+#define SMOL_CHROMA_CENTER 0
+#define SMOL_CHROMA_LEFT 1
+
+/* Options of the _ex calls (NULL: all zero, the calls above). reserved must
+ * be zero. */
+typedef struct smol_options {
+    int32_t resize_mode;
+    int32_t layout;
+    int32_t chroma_siting;
+    int32_t reserved[5];
+} smol_options;
+
+/* smol_preprocess_batch_ex -- smol_preprocess_batch with an ROI per image
+ * and options.
+ *
+ * Section 2 steps 2-4 on the ROI (section 5.3), fused per section 6.2.
+ *
+ *   rois   HOST [n][4] int32: x, y, w, h of image i's ROI, or NULL for whole
+ *          images.
+ *   opts   HOST, or NULL.
+ *   out    n x 3 x crop_h x crop_w (NCHW) or n x crop_h x crop_w x 3 (NHWC)
+ *          elements of p->out_dtype, 16-byte aligned.
+ *   Every other argument as for smol_preprocess_batch; the whole image i
+ *   must lie inside src, as there. Returns as smol_preprocess_batch. */
+int smol_preprocess_batch_ex(const uint8_t *src, int64_t src_bytes, const int64_t *offsets,
+                             const int32_t *widths, const int32_t *heights,
+                             const int32_t *row_pitch, const int32_t *rois, int32_t n,
+                             const smol_params *p, const smol_options *opts, void *out,
+                             void *stream);
+
+/* smol_yuv420_preprocess_batch_ex -- smol_yuv420_preprocess_batch with an
+ * ROI per frame (luma pixels) and options.
+ *
+ * App. A "Components" (colorspace conversion, chroma sited per
+ * opts->chroma_siting), then section 2 steps 2-4 on the ROI (section 5.3).
+ * Arguments as for smol_yuv420_preprocess_batch, plus rois and opts as for
+ * smol_preprocess_batch_ex. Returns as smol_preprocess_batch. */
+int smol_yuv420_preprocess_batch_ex(const uint8_t *src, int64_t src_bytes,
+                                    const int64_t *y_offsets, const int64_t *cb_offsets,
+                                    const int64_t *cr_offsets, const int32_t *widths,
+                                    const int32_t *heights, const int32_t *rois, int32_t n,
+                                    const smol_params *p, const smol_options *opts, void *out,
+                                    void *stream);
+
+/* smol_image_geometry_ex -- smol_image_geometry of an ROI (HOST int32[4], or
+ * NULL for the whole image) under opts (NULL: defaults). resized_w/h and
+ * crop_left/top are those of the ROI; src_x_first/last, chroma_x_first/last
+ * are in image (frame) coordinates. */
+int smol_image_geometry_ex(int32_t width, int32_t height, int32_t yuv420, const int32_t *roi,
+                           const smol_params *p, const smol_options *opts, smol_geometry *g);
 
 /* Tuning and testing knobs, process-wide, applied to later calls. Zero in any
  * field means "automatic".

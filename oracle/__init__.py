@@ -133,6 +133,11 @@ def _load():
     lib.smol_ref_yuv420_preprocess_batch_ex.argtypes = [P, I64, P, P, P, P, P, P, I32, I32, I32,
                                                         I32, P, P, I32, I32, I32, I32, P]
     lib.smol_ref_yuv420_preprocess_batch_ex.restype = ctypes.c_int
+    lib.smol_ref_preprocess_image_ex.argtypes = [P] + [I32] * 11 + [P, P, I32, I32, I32, P]
+    lib.smol_ref_preprocess_image_ex.restype = ctypes.c_int
+    lib.smol_ref_yuv420_preprocess_image_ex.argtypes = [P, P, P] + [I32] * 11 + [P, P, I32, I32,
+                                                                                   I32, I32, P]
+    lib.smol_ref_yuv420_preprocess_image_ex.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -373,3 +378,25 @@ def yuv420_preprocess_batch_ex(src: np.ndarray, y_offsets, cb_offsets, cr_offset
     if rc != 0:
         raise ValueError("oracle rejected the arguments")
     return _finish(out, out_dtype)
+
+
+def preprocess_image_ex_into(img_ptr: int, W: int, H: int, pitch: int, roi, S: int, Ch: int,
+                             Cw: int, mean: np.ndarray, std: np.ndarray, out_dtype: int,
+                             resize_mode: int, layout: int, out_ptr: int) -> int:
+    """Raw-pointer form of one RGB image with its ROI (x, y, w, h) and options."""
+    x, y, w, h = roi
+    return _load().smol_ref_preprocess_image_ex(img_ptr, W, H, pitch, x, y, w, h, S, Ch, Cw,
+                                                mean.ctypes.data, std.ctypes.data, out_dtype,
+                                                resize_mode, layout, out_ptr)
+
+
+def yuv420_preprocess_image_ex_into(y_ptr: int, cb_ptr: int, cr_ptr: int, W: int, H: int, roi,
+                                    S: int, Ch: int, Cw: int, mean: np.ndarray, std: np.ndarray,
+                                    out_dtype: int, resize_mode: int, layout: int, siting: int,
+                                    out_ptr: int) -> int:
+    """Raw-pointer form of one I420 frame with its ROI and options."""
+    x, y, w, h = roi
+    return _load().smol_ref_yuv420_preprocess_image_ex(y_ptr, cb_ptr, cr_ptr, W, H, x, y, w, h,
+                                                       S, Ch, Cw, mean.ctypes.data,
+                                                       std.ctypes.data, out_dtype, resize_mode,
+                                                       layout, siting, out_ptr)

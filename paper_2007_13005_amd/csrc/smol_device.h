@@ -47,12 +47,14 @@ __device__ __forceinline__ Tap axis_tap(int x, int in, int out)
     return t;
 }
 
-// Centred 4:2:0 chroma siting: luma index x samples chroma at
-// u = x/2 - 1/4 = (2x - 1)/4, clamped like the luma map; the weight is 1/4 or
-// 3/4 in the interior.
-__device__ __forceinline__ Tap chroma_tap(int x, int n)
+// Chroma tap of luma index x over n chroma samples, in quarters of a
+// sample: centred 4:2:0 siting puts luma x at chroma u = x/2 - 1/4
+// (4u = 2x - 1), co-sited (left) siting at u = x/2 (4u = 2x). Taps floor(u)
+// and floor(u) + 1 with weight frac(u) (a multiple of 1/4, exact), clamped at
+// both ends like the luma map.
+__device__ __forceinline__ Tap chroma_tap(int x, int n, int left = 0)
 {
-    const int num = 2 * x - 1;
+    const int num = 2 * x - 1 + left;
     Tap t;
     if (num <= 0) {
         t.x0 = 0;

@@ -123,10 +123,11 @@ void tap_index(int64_t x, int64_t in, int64_t out, int64_t *x0, int64_t *x1)
     *x1 = q + 1;
 }
 
-// Chroma tap index for luma index x: floor((2x - 1) / 4), clamped to [0, n-1].
-void chroma_index(int64_t x, int64_t n, int64_t *c0, int64_t *c1)
+// Chroma tap index for luma index x: floor((2x - 1) / 4) for centred siting,
+// floor(2x / 4) for co-sited (left), clamped to [0, n-1].
+void chroma_index(int64_t x, int64_t n, int64_t *c0, int64_t *c1, int left = 0)
 {
-    const int64_t num = 2 * x - 1;
+    const int64_t num = 2 * x - 1 + left;
     if (num <= 0) {
         *c0 = *c1 = 0;
         return;
@@ -162,11 +163,61 @@ int check_params(const smol_params *p)
     return SMOL_OK;
 }
 
-int image_geo(int64_t W, int64_t H, const smol_params *p, Geo *g, int64_t i)
+int check_options(const smol_options *o, smol_options *out)
+{
+    std::memset(out, 0, sizeof *out);
+    if (!o)
+        return SMOL_OK;
+    if (o->resize_mode != SMOL_RESIZE_SHORT_CROP && o->resize_mode != SMOL_RESIZE_DIRECT)
+        return fail(SMOL_ERR_INVALID_ARG, "resize_mode %d unknown", o->resize_mode);
+    if (o->layout != SMOL_LAYOUT_NCHW && o->layout != SMOL_LAYOUT_NHWC)
+        return fail(SMOL_ERR_INVALID_ARG, "layout %d unknown", o->layout);
+    if (o->chroma_siting != SMOL_CHROMA_CENTER && o->chroma_siting != SMOL_CHROMA_LEFT)
+        return fail(SMOL_ERR_INVALID_ARG, "chroma_siting %d unknown", o->chroma_siting);
+    for (int k = 0; k < 5; ++k)
+        if (o->reserved[k] != 0)
+            return fail(SMOL_ERR_INVALID_ARG, "options: reserved[%d] is not zero", k);
+    *out = *o;
+    return SMOL_OK;
+}
+
+// The processed region of image i: its ROI (rois[4i..4i+3]) or the whole
+// W x H image.
+int region(const int32_t *rois, int64_t i, int64_t W, int64_t H, int64_t *rx, int64_t *ry,
+           int64_t *rw, int64_t *rh)
+{
+    if (!rois) {
+        *rx = *ry = 0;
+        *rw = W;
+        *rh = H;
+        return SMOL_OK;
+    }
+    const int32_t *r = rois + 4 * i;
+    if (r[0] < 0 || r[1] < 0 || r[2] < 1 || r[3] < 1 || (int64_t)r[0] + r[2] > W ||
+        (int64_t)r[1] + r[3] > H)
+        return fail(SMOL_ERR_INVALID_ARG, "image %lld: ROI (%d, %d, %d, %d) not inside %lldx%lld",
+                    (long long)i, r[0], r[1], r[2], r[3], (long long)W, (long long)H);
+    *rx = r[0];
+    *ry = r[1];
+    *rw = r[2];
+    *rh = r[3];
+    return SMOL_OK;
+}
+
+int image_geo(int64_t W, int64_t H, const smol_params *p, int mode, Geo *g, int64_t i)
 {
     if (W < 1 || H < 1 || W > SMOL_MAX_DIM || H > SMOL_MAX_DIM)
         return fail(SMOL_ERR_INVALID_ARG, "image %lld: size %lldx%lld outside 1..%d",
                     (long long)i, (long long)W, (long long)H, SMOL_MAX_DIM);
+    if (mode == SMOL_RESIZE_DIRECT) {
+        if (p->crop_w > SMOL_MAX_RESIZED || p->crop_h > SMOL_MAX_RESIZED)
+            return fail(SMOL_ERR_UNSUPPORTED, "output %dx%d beyond %d", p->crop_w, p->crop_h,
+                        SMOL_MAX_RESIZED);
+        g->Wr = p->crop_w;
+        g->Hr = p->crop_h;
+        g->left = g->top = 0;
+        return SMOL_OK;
+    }
     resized(W, H, p->resize_short, &g->Wr, &g->Hr);
     if (g->Wr > SMOL_MAX_RESIZED || g->Hr > SMOL_MAX_RESIZED)
         return fail(SMOL_ERR_UNSUPPORTED, "image %lld: resized size %lldx%lld beyond %d",
@@ -506,7 +557,8 @@ bool is_uniform(const std::vector<Desc> &d, size_t first, size_t count, int nofs
     const int64_t st = d[first + 1].off[0] - d0.off[0];
     for (size_t i = 0; i < count; ++i) {
         const Desc &x = d[first + i];
-        if (x.W != d0.W || x.H != d0.H || x.pitch != d0.pitch)
+        if (x.W != d0.W || x.H != d0.H || x.pitch != d0.pitch || x.rx != d0.rx ||
+            x.ry != d0.ry || x.fh != d0.fh)
             return false;
         for (int k = 0; k < nofs; ++k)
             if (x.off[k] != d0.off[k] + (int64_t)i * st)
@@ -539,14 +591,20 @@ int common_checks(const void *src, int64_t src_bytes, const void *out, int32_t n
 
 extern "C" {
 
-int smol_preprocess_batch(const uint8_t *src, int64_t src_bytes, const int64_t *offsets,
-                          const int32_t *widths, const int32_t *heights,
-                          const int32_t *row_pitch, int32_t n, const smol_params *p, void *out,
-                          void *stream)
+// RGB batch: the whole image i must lie inside src; its region (ROI or the
+// whole image) becomes the descriptor's image.
+static int rgb_batch(const uint8_t *src, int64_t src_bytes, const int64_t *offsets,
+                     const int32_t *widths, const int32_t *heights, const int32_t *row_pitch,
+                     const int32_t *rois, int32_t n, const smol_params *p,
+                     const smol_options *opts, void *out, void *stream)
 {
     g_last_error.clear();
     int rc = common_checks(src, src_bytes, out, n, p);
     if (rc || n == 0)
+        return rc;
+    smol_options o;
+    rc = check_options(opts, &o);
+    if (rc)
         return rc;
     if (!offsets || !widths || !heights)
         return fail(SMOL_ERR_INVALID_ARG, "offsets, widths or heights is NULL");
@@ -556,22 +614,31 @@ int smol_preprocess_batch(const uint8_t *src, int64_t src_bytes, const int64_t *
     int64_t max_span = 0;
     for (int32_t i = 0; i < n; ++i) {
         Geo g;
-        rc = image_geo(widths[i], heights[i], p, &g, i);
-        if (rc)
-            return rc;
-        const int64_t W = widths[i], H = heights[i];
-        const int64_t pitch = row_pitch ? row_pitch[i] : 3 * W;
-        if (pitch < 3 * W || pitch > INT32_MAX)
+        const int64_t FW = widths[i], FH = heights[i];
+        if (FW < 1 || FH < 1 || FW > SMOL_MAX_DIM || FH > SMOL_MAX_DIM)
+            return fail(SMOL_ERR_INVALID_ARG, "image %d: size %lldx%lld outside 1..%d", i,
+                        (long long)FW, (long long)FH, SMOL_MAX_DIM);
+        const int64_t pitch = row_pitch ? row_pitch[i] : 3 * FW;
+        if (pitch < 3 * FW || pitch > INT32_MAX)
             return fail(SMOL_ERR_INVALID_ARG, "image %d: row pitch %lld < 3*width", i,
                         (long long)pitch);
         if (offsets[i] < 0 || offsets[i] > src_bytes ||
-            (H - 1) * pitch + 3 * W > src_bytes - offsets[i])
+            (FH - 1) * pitch + 3 * FW > src_bytes - offsets[i])
             return fail(SMOL_ERR_INVALID_ARG, "image %d: bytes [%lld, +%lld) outside src (%lld)",
-                        i, (long long)offsets[i], (long long)((H - 1) * pitch + 3 * W),
+                        i, (long long)offsets[i], (long long)((FH - 1) * pitch + 3 * FW),
                         (long long)src_bytes);
+        int64_t rx, ry, W, H;
+        rc = region(rois, i, FW, FH, &rx, &ry, &W, &H);
+        if (rc)
+            return rc;
+        rc = image_geo(W, H, p, o.resize_mode, &g, i);
+        if (rc)
+            return rc;
+        const int64_t off = offsets[i] + ry * pitch + 3 * rx;  // the region's first pixel
         Desc &d = descs[i];
         std::memset(&d, 0, sizeof d);
-        d.off[0] = offsets[i];
+        d.off[0] = off;
+        d.fh = (int32_t)H;
         d.W = (int32_t)W;
         d.H = (int32_t)H;
         d.pitch = (int32_t)pitch;
@@ -588,14 +655,14 @@ int smol_preprocess_batch(const uint8_t *src, int64_t src_bytes, const int64_t *
             int64_t yf, yd, yd2, yl;
             tap_index(g.top, H, g.Hr, &yf, &yd);
             tap_index(g.top + p->crop_h - 1, H, g.Hr, &yd2, &yl);
-            const uintptr_t base = (uintptr_t)src + (uintptr_t)offsets[i] + 3 * (uintptr_t)xf;
+            const uintptr_t base = (uintptr_t)src + (uintptr_t)off + 3 * (uintptr_t)xf;
             const uintptr_t first = (base + (uintptr_t)yf * (uintptr_t)pitch) & ~(uintptr_t)15;
             const uintptr_t last = base + (uintptr_t)yl * (uintptr_t)pitch + 3 * (uintptr_t)(xl - xf + 1);
             const uintptr_t end = (last + 15) & ~(uintptr_t)15;
             d.safe = first >= (uintptr_t)src && end <= (uintptr_t)src + (uintptr_t)src_bytes;
         }
         max_span = std::max(max_span, 3 * (xl - xf + 1));
-        inside[i] = offsets[i] + (H - 1) * pitch + 3 * xl + 8 <= src_bytes;
+        inside[i] = off + (H - 1) * pitch + 3 * xl + 8 <= src_bytes;
     }
     // Maximal runs of images whose windows do / do not all lie inside src. In
     // a packed batch only the image that ends at the end of src is outside,
@@ -616,10 +683,14 @@ int smol_preprocess_batch(const uint8_t *src, int64_t src_bytes, const int64_t *
     a.out = out;
     a.Ch = p->crop_h;
     a.Cw = p->crop_w;
+    a.nhwc = o.layout == SMOL_LAYOUT_NHWC;
     fill_norm(p, a);
     const int f16 = p->out_dtype == SMOL_OUT_F16;
     smol_plan info = {};
     const int forced = g_path.load();
+    if (a.nhwc && (forced == smol::PATH_LDS || forced == smol::PATH_GATHER))
+        return fail(SMOL_ERR_UNSUPPORTED, "NHWC output runs on the row-streaming and direct "
+                    "kernels only");
 
     auto direct = [f16](const BatchArgs &x, const Plan &, void *s) {
         return smol::launch_rgb_direct(x, f16, s);
@@ -701,6 +772,13 @@ int smol_preprocess_batch(const uint8_t *src, int64_t src_bytes, const int64_t *
         if (hipGetDevice(&device) == hipSuccess && device_info(device, &di) == hipSuccess)
             gather_fits = pg.lds_bytes <= (size_t)di.lds_per_block;
     }
+    if (a.nhwc) {
+        rc = run_batch(descs, 0, (size_t)n, 1, a, Plan{smol::PATH_DIRECT, 0, 0, 0, f16}, stream,
+                       direct, &info);
+        if (!rc)
+            g_last_plan = info;
+        return rc;
+    }
     if (forced == smol::PATH_GATHER ||
         (forced == smol::PATH_AUTO && gather_fits && any_inside && runs.size() <= 3)) {
         a.slots_off = (int)head;
@@ -743,29 +821,43 @@ int smol_preprocess_batch(const uint8_t *src, int64_t src_bytes, const int64_t *
     return rc;
 }
 
-int smol_yuv420_preprocess_batch(const uint8_t *src, int64_t src_bytes, const int64_t *y_offsets,
-                                 const int64_t *cb_offsets, const int64_t *cr_offsets,
-                                 const int32_t *widths, const int32_t *heights, int32_t n,
-                                 const smol_params *p, void *out, void *stream)
+// I420 batch: every plane of frame i must lie inside src; the descriptor
+// holds the frame's planes and the processed region (ROI or whole frame).
+static int yuv_batch(const uint8_t *src, int64_t src_bytes, const int64_t *y_offsets,
+                     const int64_t *cb_offsets, const int64_t *cr_offsets, const int32_t *widths,
+                     const int32_t *heights, const int32_t *rois, int32_t n, const smol_params *p,
+                     const smol_options *opts, void *out, void *stream)
 {
     g_last_error.clear();
     int rc = common_checks(src, src_bytes, out, n, p);
     if (rc || n == 0)
         return rc;
+    smol_options o;
+    rc = check_options(opts, &o);
+    if (rc)
+        return rc;
     if (!y_offsets || !cb_offsets || !cr_offsets || !widths || !heights)
         return fail(SMOL_ERR_INVALID_ARG, "an offset table, widths or heights is NULL");
+    const int left = o.chroma_siting == SMOL_CHROMA_LEFT;
 
     std::vector<Desc> descs((size_t)n);
     int64_t max_yspan = 0, max_cspan = 0;
     for (int32_t i = 0; i < n; ++i) {
         Geo g;
-        rc = image_geo(widths[i], heights[i], p, &g, i);
+        const int64_t FW = widths[i], FH = heights[i];
+        if (FW < 1 || FH < 1 || FW > SMOL_MAX_DIM || FH > SMOL_MAX_DIM)
+            return fail(SMOL_ERR_INVALID_ARG, "frame %d: size %lldx%lld outside 1..%d", i,
+                        (long long)FW, (long long)FH, SMOL_MAX_DIM);
+        int64_t rx, ry, W, H;
+        rc = region(rois, i, FW, FH, &rx, &ry, &W, &H);
         if (rc)
             return rc;
-        const int64_t W = widths[i], H = heights[i];
-        const int64_t cbytes = ((W + 1) / 2) * ((H + 1) / 2);
+        rc = image_geo(W, H, p, o.resize_mode, &g, i);
+        if (rc)
+            return rc;
+        const int64_t cbytes = ((FW + 1) / 2) * ((FH + 1) / 2);
         const int64_t offs[3] = {y_offsets[i], cb_offsets[i], cr_offsets[i]};
-        const int64_t sizes[3] = {W * H, cbytes, cbytes};
+        const int64_t sizes[3] = {FW * FH, cbytes, cbytes};
         for (int k = 0; k < 3; ++k)
             if (offs[k] < 0 || offs[k] > src_bytes || sizes[k] > src_bytes - offs[k])
                 return fail(SMOL_ERR_INVALID_ARG, "frame %d: plane %d [%lld, +%lld) outside src",
@@ -776,15 +868,18 @@ int smol_yuv420_preprocess_batch(const uint8_t *src, int64_t src_bytes, const in
             d.off[k] = offs[k];
         d.W = (int32_t)W;
         d.H = (int32_t)H;
-        d.pitch = (int32_t)W;
+        d.pitch = (int32_t)FW;
+        d.fh = (int32_t)FH;
+        d.rx = (int32_t)rx;
+        d.ry = (int32_t)ry;
         d.Wr = (int32_t)g.Wr;
         d.Hr = (int32_t)g.Hr;
         d.left = (int32_t)g.left;
         d.top = (int32_t)g.top;
         int64_t xf, xl, c0, c1, e0, e1;
         x_span(d, p->crop_w, &xf, &xl);
-        chroma_index(xf, (W + 1) / 2, &c0, &c1);
-        chroma_index(xl, (W + 1) / 2, &e0, &e1);
+        chroma_index(rx + xf, (FW + 1) / 2, &c0, &c1, left);
+        chroma_index(rx + xl, (FW + 1) / 2, &e0, &e1, left);
         d.xf = (int32_t)xf;
         d.span = (int32_t)(xl - xf + 1);
         max_yspan = std::max(max_yspan, xl - xf + 1);
@@ -806,6 +901,8 @@ int smol_yuv420_preprocess_batch(const uint8_t *src, int64_t src_bytes, const in
     a.out = out;
     a.Ch = p->crop_h;
     a.Cw = p->crop_w;
+    a.nhwc = o.layout == SMOL_LAYOUT_NHWC;
+    a.siting = left;
     fill_norm(p, a);
     const int forced = g_path.load();
     if (forced == smol::PATH_LDS || forced == smol::PATH_GATHER)
@@ -852,17 +949,30 @@ int smol_yuv420_preprocess_batch(const uint8_t *src, int64_t src_bytes, const in
     return rc;
 }
 
-int smol_image_geometry(int32_t width, int32_t height, int32_t yuv420, const smol_params *p,
-                        smol_geometry *g)
+int smol_image_geometry_ex(int32_t frame_w, int32_t frame_h, int32_t yuv420, const int32_t *roi,
+                           const smol_params *p, const smol_options *opts, smol_geometry *g)
 {
     g_last_error.clear();
     int rc = check_params(p);
     if (rc)
         return rc;
+    smol_options o;
+    rc = check_options(opts, &o);
+    if (rc)
+        return rc;
     if (!g)
         return fail(SMOL_ERR_INVALID_ARG, "geometry output is NULL");
+    if (frame_w < 1 || frame_h < 1 || frame_w > SMOL_MAX_DIM || frame_h > SMOL_MAX_DIM)
+        return fail(SMOL_ERR_INVALID_ARG, "size %dx%d outside 1..%d", frame_w, frame_h,
+                    SMOL_MAX_DIM);
+    int64_t rx, ry, rw, rh;
+    rc = region(roi, 0, frame_w, frame_h, &rx, &ry, &rw, &rh);
+    if (rc)
+        return rc;
+    const int32_t width = (int32_t)rw, height = (int32_t)rh;
+    const int left = o.chroma_siting == SMOL_CHROMA_LEFT;
     Geo geo;
-    rc = image_geo(width, height, p, &geo, 0);
+    rc = image_geo(width, height, p, o.resize_mode, &geo, 0);
     if (rc)
         return rc;
     std::memset(g, 0, sizeof *g);
@@ -880,14 +990,14 @@ int smol_image_geometry(int32_t width, int32_t height, int32_t yuv420, const smo
     d.top = (int32_t)geo.top;
     int64_t xf, xl;
     x_span(d, p->crop_w, &xf, &xl);
-    g->src_x_first = (int32_t)xf;
-    g->src_x_last = (int32_t)xl;
+    g->src_x_first = (int32_t)(rx + xf);
+    g->src_x_last = (int32_t)(rx + xl);
     g->src_rows = (int32_t)distinct_rows(geo.top, p->crop_h, height, geo.Hr);
     if (yuv420) {
-        const int64_t Wc = (width + 1) / 2, Hc = (height + 1) / 2;
+        const int64_t Wc = (frame_w + 1) / 2, Hc = (frame_h + 1) / 2;
         int64_t c0, c1, e0, e1;
-        chroma_index(xf, Wc, &c0, &c1);
-        chroma_index(xl, Wc, &e0, &e1);
+        chroma_index(rx + xf, Wc, &c0, &c1, left);
+        chroma_index(rx + xl, Wc, &e0, &e1, left);
         g->chroma_x_first = (int32_t)c0;
         g->chroma_x_last = (int32_t)e1;
         // distinct chroma rows over every luma row the vertical taps read
@@ -895,7 +1005,7 @@ int smol_image_geometry(int32_t width, int32_t height, int32_t yuv420, const smo
         for (int64_t r = 0; r < p->crop_h; ++r) {
             int64_t y0, y1;
             tap_index(geo.top + r, height, geo.Hr, &y0, &y1);
-            const int64_t ys[2] = {y0, y1};
+            const int64_t ys[2] = {ry + y0, ry + y1};
             for (int k = 0; k < 2; ++k) {
                 int64_t a, b;
                 chroma_index(ys[k], Hc, &a, &b);
@@ -912,6 +1022,51 @@ int smol_image_geometry(int32_t width, int32_t height, int32_t yuv420, const smo
         g->chroma_rows = (int32_t)count;
     }
     return SMOL_OK;
+}
+
+int smol_image_geometry(int32_t width, int32_t height, int32_t yuv420, const smol_params *p,
+                        smol_geometry *g)
+{
+    return smol_image_geometry_ex(width, height, yuv420, nullptr, p, nullptr, g);
+}
+
+int smol_preprocess_batch(const uint8_t *src, int64_t src_bytes, const int64_t *offsets,
+                          const int32_t *widths, const int32_t *heights,
+                          const int32_t *row_pitch, int32_t n, const smol_params *p, void *out,
+                          void *stream)
+{
+    return rgb_batch(src, src_bytes, offsets, widths, heights, row_pitch, nullptr, n, p, nullptr,
+                     out, stream);
+}
+
+int smol_preprocess_batch_ex(const uint8_t *src, int64_t src_bytes, const int64_t *offsets,
+                             const int32_t *widths, const int32_t *heights,
+                             const int32_t *row_pitch, const int32_t *rois, int32_t n,
+                             const smol_params *p, const smol_options *opts, void *out,
+                             void *stream)
+{
+    return rgb_batch(src, src_bytes, offsets, widths, heights, row_pitch, rois, n, p, opts, out,
+                     stream);
+}
+
+int smol_yuv420_preprocess_batch(const uint8_t *src, int64_t src_bytes, const int64_t *y_offsets,
+                                 const int64_t *cb_offsets, const int64_t *cr_offsets,
+                                 const int32_t *widths, const int32_t *heights, int32_t n,
+                                 const smol_params *p, void *out, void *stream)
+{
+    return yuv_batch(src, src_bytes, y_offsets, cb_offsets, cr_offsets, widths, heights, nullptr,
+                     n, p, nullptr, out, stream);
+}
+
+int smol_yuv420_preprocess_batch_ex(const uint8_t *src, int64_t src_bytes,
+                                    const int64_t *y_offsets, const int64_t *cb_offsets,
+                                    const int64_t *cr_offsets, const int32_t *widths,
+                                    const int32_t *heights, const int32_t *rois, int32_t n,
+                                    const smol_params *p, const smol_options *opts, void *out,
+                                    void *stream)
+{
+    return yuv_batch(src, src_bytes, y_offsets, cb_offsets, cr_offsets, widths, heights, rois, n,
+                     p, opts, out, stream);
 }
 
 int smol_set_tuning(const smol_tuning *t)

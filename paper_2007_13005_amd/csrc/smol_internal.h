@@ -6,20 +6,24 @@
 
 namespace smol {
 
-// Per-image descriptor, 64 bytes. For RGB input off[0] is the byte offset of
-// the first pixel; for I420 input off[0..2] are the Y, Cb and Cr plane offsets.
-// Wr/Hr are the resized sizes and left/top the crop offsets (host-computed
-// per image; per-element taps are computed by the kernels). xf is the first
-// source column any output pixel reads and span the bytes from that column's
-// first byte to the end of the last source column read; safe is 1 when every
-// 16-byte aligned chunk that holds a byte of a staged source row lies inside
-// src (RGB only).
+// Per-image descriptor, 80 bytes. For RGB input off[0] is the byte offset of
+// the first pixel of the processed region (the image, or its ROI) and W x H
+// its size; for I420 input off[0..2] are the Y, Cb and Cr plane offsets of
+// the frame, W x H the size of the processed region, (rx, ry) its origin in
+// the frame, pitch the frame's luma width and fh its luma height. Wr/Hr are
+// the resized sizes and left/top the crop offsets (host-computed per image;
+// per-element taps are computed by the kernels). xf is the first column of
+// the region any output pixel reads and span the bytes from that column's
+// first byte to the end of the last column read (luma bytes for I420); safe
+// is 1 when every 16-byte aligned chunk that holds a byte of a staged row
+// lies inside src.
 struct alignas(16) Desc {
     int64_t off[3];
     int32_t W, H, pitch, Wr, Hr, left, top, xf;
     int32_t span, safe;
+    int32_t rx, ry, fh, pad;
 };
-static_assert(sizeof(Desc) == 64, "descriptor must be 64 bytes");
+static_assert(sizeof(Desc) == 80, "descriptor must be 80 bytes");
 
 // Kernel arguments (passed by value). When `table` is null every image shares
 // `uni` and image i's offsets are uni.off[k] + i * stride.
@@ -47,6 +51,8 @@ struct BatchArgs {
     int32_t interleave;  // row streaming: wave q takes rows q, q + G, ... (else a range)
     int32_t exact;       // 1: operation-by-operation fp32 arithmetic (row-streaming kernel)
     int32_t wpg;         // row streaming: waves per workgroup (grid = waves / wpg)
+    int32_t nhwc;        // 1: output n x Ch x Cw x 3 (row-streaming and direct kernels)
+    int32_t siting;      // I420 chroma columns: 0 centred (x/2 - 1/4), 1 co-sited (x/2)
     float mean[3];   // per channel, 0..255 units
     float stdv[3];
     float rcp[3];    // RN(1 / stdv), fp32

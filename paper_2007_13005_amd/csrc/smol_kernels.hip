@@ -489,7 +489,7 @@ __device__ __forceinline__ void compute_pass(const PassRegs &v, const GatherTabs
 }
 
 // The fields of an image the gather kernel uses, as plain scalars (a copy of
-// the 64-byte descriptor would not stay in registers across the loop).
+// the 80-byte descriptor would not stay in registers across the loop).
 struct ImgGeo {
     long long off;
     int W, H, pitch, Wr, Hr, left, top;
@@ -642,13 +642,15 @@ __global__ void __launch_bounds__(kThreads) rgb_direct_kernel(BatchArgs a)
         const Tap ty = axis_tap(d.top + yc, d.H, d.Hr);
         const uint8_t *r0 = a.src + d.off[0] + (long long)ty.x0 * d.pitch;
         const uint8_t *r1 = a.src + d.off[0] + (long long)ty.x1 * d.pitch;
-        const long long base = (long long)(a.img_base + img) * 3 * plane + pix;
+        // element of channel ch: NCHW base + ch * plane, NHWC base + ch
+        const long long base = (long long)(a.img_base + img) * 3 * plane + (a.nhwc ? 3 * pix : pix);
+        const long long cstep = a.nhwc ? 1 : plane;
 #pragma unroll
         for (int ch = 0; ch < 3; ++ch) {
             const float p00 = r0[3 * tx.x0 + ch], p01 = r0[3 * tx.x1 + ch];
             const float p10 = r1[3 * tx.x0 + ch], p11 = r1[3 * tx.x1 + ch];
             const float v = lerp(lerp(p00, p01, tx.w), lerp(p10, p11, tx.w), ty.w);
-            store1<F16>(a.out, base + ch * plane, normalize(v, a.mean[ch], a.stdv[ch], a.rcp[ch]));
+            store1<F16>(a.out, base + ch * cstep, normalize(v, a.mean[ch], a.stdv[ch], a.rcp[ch]));
         }
     }
 }
@@ -678,8 +680,10 @@ __global__ void __launch_bounds__(kThreads) yuv_direct_kernel(BatchArgs a)
         const int xc = (int)(pix - (long long)yc * a.Cw);
         Desc d;
         image_desc(a, img, d);
-        const int Wc = (d.W + 1) >> 1, Hc = (d.H + 1) >> 1;
-        const uint8_t *yp = a.src + d.off[0];
+        // the region (d.W x d.H at (rx, ry)) inside a frame of pitch x fh;
+        // chroma taps in frame coordinates
+        const int Wc = (d.pitch + 1) >> 1, Hc = (d.fh + 1) >> 1;
+        const uint8_t *yp = a.src + d.off[0] + (long long)d.ry * d.pitch + d.rx;
         const uint8_t *cbp = a.src + d.off[1];
         const uint8_t *crp = a.src + d.off[2];
         const Tap tx = axis_tap(d.left + xc, d.W, d.Wr);
@@ -689,21 +693,22 @@ __global__ void __launch_bounds__(kThreads) yuv_direct_kernel(BatchArgs a)
         float rgb[2][2][3];
 #pragma unroll
         for (int i = 0; i < 2; ++i) {
-            const Tap cy = chroma_tap(yy[i], Hc);
+            const Tap cy = chroma_tap(d.ry + yy[i], Hc);
 #pragma unroll
             for (int k = 0; k < 2; ++k) {
-                const Tap cx = chroma_tap(xx[k], Wc);
-                const float Y = (float)yp[(long long)yy[i] * d.W + xx[k]];
+                const Tap cx = chroma_tap(d.rx + xx[k], Wc, a.siting);
+                const float Y = (float)yp[(long long)yy[i] * d.pitch + xx[k]];
                 ycbcr_to_rgb(Y, chroma_at(cbp, Wc, cx, cy), chroma_at(crp, Wc, cx, cy),
                              rgb[i][k][0], rgb[i][k][1], rgb[i][k][2]);
             }
         }
-        const long long base = (long long)(a.img_base + img) * 3 * plane + pix;
+        const long long base = (long long)(a.img_base + img) * 3 * plane + (a.nhwc ? 3 * pix : pix);
+        const long long cstep = a.nhwc ? 1 : plane;
 #pragma unroll
         for (int ch = 0; ch < 3; ++ch) {
             const float v = lerp(lerp(rgb[0][0][ch], rgb[0][1][ch], tx.w),
                                  lerp(rgb[1][0][ch], rgb[1][1][ch], tx.w), ty.w);
-            store1<F16>(a.out, base + ch * plane, normalize(v, a.mean[ch], a.stdv[ch], a.rcp[ch]));
+            store1<F16>(a.out, base + ch * cstep, normalize(v, a.mean[ch], a.stdv[ch], a.rcp[ch]));
         }
     }
 }

@@ -529,12 +529,54 @@ __device__ __forceinline__ void pack_pair(RowOut<F16, J> &out, int j, const floa
     }
 }
 
-// Store a lane's pairs of one output row (three planes).
+// Store a lane's pairs of one output row: three planes (NCHW), or the six
+// interleaved elements of the two pixels (NHWC).
 template <int F16, int J>
 __device__ __forceinline__ void store_row(uint8_t *orow, long long plane, int Cw, int lane,
-                                          const RowOut<F16, J> &out)
+                                          const RowOut<F16, J> &out, int nhwc)
 {
     constexpr int kEsz = F16 ? 2 : 4;
+    if (nhwc) {
+#pragma unroll
+        for (int j = 0; j < J; ++j) {
+            const int c = pair_col(lane, j, Cw);
+            uint8_t *dst = orow + (long long)3 * c * kEsz;
+            if ((Cw & 1) == 0) {
+                // c even: 6 c bytes (fp16) is a multiple of 4, 12 c (fp32) of 8
+                if (F16) {
+                    const uint32_t w0 = out.w[j][0][0], w1 = out.w[j][1][0], w2 = out.w[j][2][0];
+                    __builtin_nontemporal_store((w0 & 0xffffu) | (w1 << 16), (uint32_t *)dst);
+                    __builtin_nontemporal_store((w2 & 0xffffu) | (w0 & 0xffff0000u),
+                                                (uint32_t *)dst + 1);
+                    __builtin_nontemporal_store((w1 >> 16) | (w2 & 0xffff0000u),
+                                                (uint32_t *)dst + 2);
+                } else {
+                    typedef uint32_t u32x2v __attribute__((ext_vector_type(2)));
+                    const u32x2v q0 = {out.w[j][0][0], out.w[j][1][0]};
+                    const u32x2v q1 = {out.w[j][2][0], out.w[j][0][F16 ? 0 : 1]};
+                    const u32x2v q2 = {out.w[j][1][F16 ? 0 : 1], out.w[j][2][F16 ? 0 : 1]};
+                    __builtin_nontemporal_store(q0, (u32x2v *)dst);
+                    __builtin_nontemporal_store(q1, (u32x2v *)dst + 1);
+                    __builtin_nontemporal_store(q2, (u32x2v *)dst + 2);
+                }
+            } else {
+                // odd Cw: element by element, pixel c + 1 is the last
+                // column again past the end
+                uint8_t *dst1 = orow + (long long)3 * min(c + 1, Cw - 1) * kEsz;
+#pragma unroll
+                for (int ch = 0; ch < 3; ++ch) {
+                    if (F16) {
+                        ((uint16_t *)dst)[ch] = (uint16_t)out.w[j][ch][0];
+                        ((uint16_t *)dst1)[ch] = (uint16_t)(out.w[j][ch][0] >> 16);
+                    } else {
+                        ((uint32_t *)dst)[ch] = out.w[j][ch][0];
+                        ((uint32_t *)dst1)[ch] = out.w[j][ch][F16 ? 0 : 1];
+                    }
+                }
+            }
+        }
+        return;
+    }
 #pragma unroll
     for (int j = 0; j < J; ++j) {
         const int c = pair_col(lane, j, Cw);
@@ -692,10 +734,12 @@ __global__ void __launch_bounds__(64 * kRowsMaxWavesPerGroup) rgb_rows_kernel(Ba
 
     // Output row pointer of the row to interpolate: a step adds 3 Ch di + dr
     // rows, plus 2 Ch (planes 1 and 2 of the image left) when it wraps.
-    const long long rb = (long long)a.Cw * kEsz;
-    uint8_t *orow =
-        (uint8_t *)a.out + ((long long)(a.img_base + c_img) * 3 * Ch + c_rr) * rb;
-    const long long ostep = (3LL * Ch * step.di + step.dr) * rb, owrap = 2LL * Ch * rb;
+    // bytes between an image's output rows: Cw elements per plane (NCHW) or
+    // 3 Cw (NHWC); a wrap to the next image skips the rest of the image.
+    const long long rb = (long long)a.Cw * kEsz, rowb = a.nhwc ? 3 * rb : rb;
+    const long long imgb = 3LL * Ch * rb;
+    uint8_t *orow = (uint8_t *)a.out + (long long)(a.img_base + c_img) * imgb + c_rr * rowb;
+    const long long ostep = step.di * imgb + step.dr * rowb, owrap = imgb - Ch * rowb;
     int cx[J][2];
     float cw[J][2];
     int cW, cWr, cleft;
@@ -762,7 +806,7 @@ __global__ void __launch_bounds__(64 * kRowsMaxWavesPerGroup) rgb_rows_kernel(Ba
         advance();                                                                            \
         compute();                                                                            \
         write_rows<G>(lds, NXT, lane);                                                        \
-        store_row<F16, J>(orow, plane, a.Cw, lane, out);                                      \
+        store_row<F16, J>(orow, plane, a.Cw, lane, out, a.nhwc);                              \
         csh0 = NXT.sh0;                                                                       \
         csh1 = NXT.sh1;                                                                       \
         cy0 = NXT.y0;                                                                         \
@@ -805,7 +849,7 @@ __global__ void __launch_bounds__(64 * kRowsMaxWavesPerGroup) rgb_rows_kernel(Ba
     }
 #undef SMOL_ROWS_STEP
     compute();
-    store_row<F16, J>(orow, plane, a.Cw, lane, out);
+    store_row<F16, J>(orow, plane, a.Cw, lane, out, a.nhwc);
 }
 
 // ---------------------------------------------------------------------------
@@ -835,9 +879,12 @@ __global__ void __launch_bounds__(64 * kRowsMaxWavesPerGroup) rgb_rows_kernel(Ba
 // from each of two chroma rows, and its horizontal weight bytes
 // (4 - fx, fx).
 // ---------------------------------------------------------------------------
+// A frame's plane offsets and the processed region: W x H luma pixels at
+// (rx, ry) in a frame of fw x fh (chroma taps use frame coordinates).
 struct YuvImg {
     long long off[3];
     int W, H, Wr, Hr, left, top, xf, span;
+    int rx, ry, fw, fh;
 };
 
 __device__ __forceinline__ YuvImg yuv_img(const BatchArgs &a, int img)
@@ -856,10 +903,18 @@ __device__ __forceinline__ YuvImg yuv_img(const BatchArgs &a, int img)
         g.top = t->top;
         g.xf = t->xf;
         g.span = t->span;
+        g.rx = t->rx;
+        g.ry = t->ry;
+        g.fw = t->pitch;
+        g.fh = t->fh;
     } else {
         g.off[0] = a.uni.off[0] + (long long)img * a.stride;
         g.off[1] = a.uni.off[1] + (long long)img * a.stride;
         g.off[2] = a.uni.off[2] + (long long)img * a.stride;
+        g.rx = a.uni.rx;
+        g.ry = a.uni.ry;
+        g.fw = a.uni.pitch;
+        g.fh = a.uni.fh;
         g.W = a.uni.W;
         g.H = a.uni.H;
         g.Wr = a.uni.Wr;
@@ -889,9 +944,10 @@ struct YuvStaged {
 // cursor, with the three plane bases).
 struct YuvCursor {
     int img, rr;
-    VCursor v;          // luma vertical map
-    uintptr_t base[3];  // first staged byte of row 0 of Y, Cb, Cr
-    int W, Wc, Hc, yspan, cspan;
+    VCursor v;          // luma vertical map over the region's rows
+    uintptr_t base[3];  // first staged byte of the region's row 0 (Y), of chroma row 0 (Cb, Cr)
+    int W, Wc, Hc, yspan, cspan;  // frame luma pitch, chroma pitch and rows
+    int ry;             // the region's first frame row
 };
 
 template <int STRIDE>
@@ -906,14 +962,16 @@ __device__ __forceinline__ void yuv_cursor_image(YuvCursor &c, const BatchArgs &
     lg.Hr = g.Hr;
     lg.top = g.top;
     vcursor_init<STRIDE>(c.v, lg, rr, s);
-    c.W = g.W;
-    c.Wc = (g.W + 1) >> 1;
-    c.Hc = (g.H + 1) >> 1;
-    const int cxf = chroma_tap(g.xf, c.Wc).x0;
-    const int cxl = chroma_tap(g.xf + g.span - 1, c.Wc).x1;
+    c.W = g.fw;
+    c.Wc = (g.fw + 1) >> 1;
+    c.Hc = (g.fh + 1) >> 1;
+    c.ry = g.ry;
+    const int cxf = chroma_tap(g.rx + g.xf, c.Wc, a.siting).x0;
+    const int cxl = chroma_tap(g.rx + g.xf + g.span - 1, c.Wc, a.siting).x1;
     c.yspan = g.span;
     c.cspan = cxl - cxf + 1;
-    c.base[0] = (uintptr_t)(a.src + g.off[0]) + (uintptr_t)g.xf;
+    c.base[0] = (uintptr_t)(a.src + g.off[0]) + (uintptr_t)g.ry * (uintptr_t)g.fw +
+                (uintptr_t)(g.rx + g.xf);
     c.base[1] = (uintptr_t)(a.src + g.off[1]) + (uintptr_t)cxf;
     c.base[2] = (uintptr_t)(a.src + g.off[2]) + (uintptr_t)cxf;
 }
@@ -952,7 +1010,7 @@ __device__ __forceinline__ void yuv_load(YuvStaged &st, const YuvCursor &c, int 
 {
     int y0, y1;
     vcursor_tap(c.v, y0, y1, st.wy);
-    const Tap t0 = chroma_tap(y0, c.Hc), t1 = chroma_tap(y1, c.Hc);
+    const Tap t0 = chroma_tap(c.ry + y0, c.Hc), t1 = chroma_tap(c.ry + y1, c.Hc);
     st.fy0 = (int)(4.0f * t0.w);  // exact: 0, 1 or 3
     st.fy1 = (int)(4.0f * t1.w);
     st.b0 = t1.x0 == t0.x0 ? 0 : 1;
@@ -990,17 +1048,19 @@ struct YuvCols {
 };
 
 template <int J>
-__device__ __forceinline__ void yuv_cols(YuvCols<J> &k, const YuvImg &g, int Cw, int lane)
+__device__ __forceinline__ void yuv_cols(YuvCols<J> &k, const YuvImg &g, int Cw, int lane,
+                                         int siting)
 {
-    const int Wc = (g.W + 1) >> 1;
-    const int cxf = chroma_tap(g.xf, Wc).x0;
+    const int Wc = (g.fw + 1) >> 1;
+    const int cxf = chroma_tap(g.rx + g.xf, Wc, siting).x0;
 #pragma unroll
     for (int j = 0; j < J; ++j)
 #pragma unroll
         for (int px = 0; px < 2; ++px) {
             const int c = min(pair_col(lane, j, Cw) + px, Cw - 1);
             const Tap t = axis_tap(g.left + c, g.W, g.Wr);
-            const Tap a0 = chroma_tap(t.x0, Wc), a1 = chroma_tap(t.x1, Wc);
+            const Tap a0 = chroma_tap(g.rx + t.x0, Wc, siting),
+                      a1 = chroma_tap(g.rx + t.x1, Wc, siting);
             k.ox[j][px] = t.x0 - g.xf;
             k.wx[j][px] = t.w;
             k.oc[j][px] = a0.x0 - cxf;
@@ -1013,7 +1073,7 @@ __device__ __forceinline__ void yuv_cols(YuvCols<J> &k, const YuvImg &g, int Cw,
                 const uint32_t d0 = (uint32_t)(ax[xi].x0 - a0.x0);
                 const uint32_t d1 = (uint32_t)(ax[xi].x1 - a0.x0);
                 k.sel[j][px][xi] = d0 | d1 << 8 | (4 + d0) << 16 | (4 + d1) << 24;
-                const uint32_t fx = (uint32_t)(4.0f * ax[xi].w);  // exact: 0, 1 or 3
+                const uint32_t fx = (uint32_t)(4.0f * ax[xi].w);  // exact: 0 .. 3
                 k.hw[j][px][xi] = (4 - fx) | fx << 8;
             }
         }
@@ -1128,16 +1188,18 @@ yuv_rows_kernel(BatchArgs a)
     int c_img = (int)(r0 / Ch), c_rr = (int)(r0 - (long long)c_img * Ch);  // row to interpolate
     YuvCursor lc;                                                          // next row to load
     yuv_cursor_image<STRIDE>(lc, a, c_img, c_rr, step);
-    const long long rb = (long long)a.Cw * kEsz;
-    uint8_t *orow =
-        (uint8_t *)a.out + ((long long)(a.img_base + c_img) * 3 * Ch + c_rr) * rb;
-    const long long ostep = (3LL * Ch * step.di + step.dr) * rb, owrap = 2LL * Ch * rb;
+    // bytes between an image's output rows: Cw elements per plane (NCHW) or
+    // 3 Cw (NHWC); a wrap to the next image skips the rest of the image.
+    const long long rb = (long long)a.Cw * kEsz, rowb = a.nhwc ? 3 * rb : rb;
+    const long long imgb = 3LL * Ch * rb;
+    uint8_t *orow = (uint8_t *)a.out + (long long)(a.img_base + c_img) * imgb + c_rr * rowb;
+    const long long ostep = step.di * imgb + step.dr * rowb, owrap = imgb - Ch * rowb;
 
     YuvCols<J> cols;
     int cW, cWr, cleft;
     {
         const YuvImg g = yuv_img(a, c_img);
-        yuv_cols<J>(cols, g, a.Cw, lane);
+        yuv_cols<J>(cols, g, a.Cw, lane, a.siting);
         cW = g.W;
         cWr = g.Wr;
         cleft = g.left;
@@ -1173,7 +1235,7 @@ yuv_rows_kernel(BatchArgs a)
         advance();
         yuv_compute<F16, J, EXACT>(nk, lds0, csh, cwy, cfy0, cfy1, cb0, cols, out);
         yuv_write(lds, R, lane);
-        store_row<F16, J>(orow, plane, a.Cw, lane, out);
+        store_row<F16, J>(orow, plane, a.Cw, lane, out, a.nhwc);
 #pragma unroll
         for (int s = 0; s < 8; ++s)
             csh[s] = R.sh[s];
@@ -1196,12 +1258,12 @@ yuv_rows_kernel(BatchArgs a)
                 cW = g.W;
                 cWr = g.Wr;
                 cleft = g.left;
-                yuv_cols<J>(cols, g, a.Cw, lane);
+                yuv_cols<J>(cols, g, a.Cw, lane, a.siting);
             }
         }
     }
     yuv_compute<F16, J, EXACT>(nk, lds0, csh, cwy, cfy0, cfy1, cb0, cols, out);
-    store_row<F16, J>(orow, plane, a.Cw, lane, out);
+    store_row<F16, J>(orow, plane, a.Cw, lane, out, a.nhwc);
 }
 
 

@@ -29,6 +29,13 @@ PATH_LDS = 2
 PATH_GATHER = 3
 PATH_ROWS = 4
 
+RESIZE_SHORT_CROP = 0
+RESIZE_DIRECT = 1
+LAYOUT_NCHW = 0
+LAYOUT_NHWC = 1
+CHROMA_CENTER = 0
+CHROMA_LEFT = 1
+
 MAX_DIM = 65535
 MAX_RESIZED = 4194303
 MAX_BATCH = 1048576
@@ -47,6 +54,11 @@ class Geometry(ctypes.Structure):
 
     def as_dict(self) -> dict:
         return {name: getattr(self, name) for name, _ in self._fields_}
+
+
+class Options(ctypes.Structure):
+    _fields_ = [("resize_mode", ctypes.c_int32), ("layout", ctypes.c_int32),
+                ("chroma_siting", ctypes.c_int32), ("reserved", ctypes.c_int32 * 5)]
 
 
 class Tuning(ctypes.Structure):
@@ -76,6 +88,16 @@ SIGNATURES = {
                                                     _vp]),
     "smol_image_geometry": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                            ctypes.POINTER(Params), ctypes.POINTER(Geometry)]),
+    "smol_preprocess_batch_ex": (ctypes.c_int, [_vp, ctypes.c_int64, _vp, _vp, _vp, _vp, _vp,
+                                                ctypes.c_int32, ctypes.POINTER(Params),
+                                                ctypes.POINTER(Options), _vp, _vp]),
+    "smol_yuv420_preprocess_batch_ex": (ctypes.c_int, [_vp, ctypes.c_int64, _vp, _vp, _vp, _vp,
+                                                       _vp, _vp, ctypes.c_int32,
+                                                       ctypes.POINTER(Params),
+                                                       ctypes.POINTER(Options), _vp, _vp]),
+    "smol_image_geometry_ex": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _vp,
+                                              ctypes.POINTER(Params), ctypes.POINTER(Options),
+                                              ctypes.POINTER(Geometry)]),
     "smol_set_tuning": (ctypes.c_int, [ctypes.POINTER(Tuning)]),
     "smol_last_plan": (ctypes.c_int, [ctypes.POINTER(Plan)]),
     "smol_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -142,6 +164,25 @@ def make_params(resize_short: int, crop_h: int, crop_w: int, mean, std, out_dtyp
     return p
 
 
+def make_options(resize_mode: int = RESIZE_SHORT_CROP, layout: int = LAYOUT_NCHW,
+                 chroma_siting: int = CHROMA_CENTER) -> Options:
+    o = Options()
+    o.resize_mode, o.layout, o.chroma_siting = resize_mode, layout, chroma_siting
+    return o
+
+
+def image_geometry_ex(width: int, height: int, params: Params, yuv420: bool = False,
+                      roi=None, options: Options | None = None) -> dict:
+    """Geometry of an ROI (x, y, w, h) of a width x height image under options."""
+    g = Geometry()
+    r = None if roi is None else _table(roi, np.int32).reshape(4)
+    _check(lib().smol_image_geometry_ex(width, height, int(bool(yuv420)),
+                                        None if r is None else r.ctypes.data, ctypes.byref(params),
+                                        None if options is None else ctypes.byref(options),
+                                        ctypes.byref(g)))
+    return g.as_dict()
+
+
 def image_geometry(width: int, height: int, params: Params, yuv420: bool = False) -> dict:
     g = Geometry()
     _check(lib().smol_image_geometry(width, height, int(bool(yuv420)), ctypes.byref(params),
@@ -182,10 +223,11 @@ def _stream_handle(stream) -> int | None:
     return stream.cuda_stream
 
 
-def _out_tensor(out, n: int, params: Params, device):
+def _out_tensor(out, n: int, params: Params, device, layout: int = LAYOUT_NCHW):
     import torch
     dtype = torch.float16 if params.out_dtype == OUT_F16 else torch.float32
-    shape = (n, 3, params.crop_h, params.crop_w)
+    shape = ((n, params.crop_h, params.crop_w, 3) if layout == LAYOUT_NHWC
+             else (n, 3, params.crop_h, params.crop_w))
     if out is None:
         return torch.empty(shape, dtype=dtype, device=device)
     if tuple(out.shape) != shape or out.dtype != dtype or not out.is_contiguous():
@@ -193,11 +235,23 @@ def _out_tensor(out, n: int, params: Params, device):
     return out
 
 
-def preprocess_batch(src, offsets, widths, heights, params: Params, pitches=None, out=None,
-                     stream=None):
-    """Packed HWC RGB uint8 images in the device tensor ``src`` -> NCHW tensor.
+def _rois(rois, n: int):
+    if rois is None:
+        return None
+    r = _table(rois, np.int32)
+    if r.shape != (n, 4):
+        raise ValueError("rois must be an (n, 4) table of x, y, w, h")
+    return r
 
-    ``offsets`` / ``widths`` / ``heights`` / ``pitches`` are host sequences.
+
+def preprocess_batch(src, offsets, widths, heights, params: Params, pitches=None, out=None,
+                     stream=None, rois=None, options: Options | None = None):
+    """Packed HWC RGB uint8 images in the device tensor ``src`` -> NCHW (or,
+    with options, NHWC) tensor. With ``rois`` ((n, 4): x, y, w, h) or
+    ``options`` the call goes through ``smol_preprocess_batch_ex``.
+
+    ``offsets`` / ``widths`` / ``heights`` / ``pitches`` / ``rois`` are host
+    sequences.
     """
     if src.dtype.itemsize != 1 or not src.is_cuda or not src.is_contiguous():
         raise ValueError("src must be a contiguous uint8 device tensor")
@@ -208,18 +262,28 @@ def preprocess_batch(src, offsets, widths, heights, params: Params, pitches=None
     n = len(off)
     if not (len(w) == len(h) == n and (pt is None or len(pt) == n)):
         raise ValueError("table lengths differ")
-    out = _out_tensor(out, n, params, src.device)
-    _check(lib().smol_preprocess_batch(src.data_ptr(), src.numel(), off.ctypes.data,
-                                       w.ctypes.data, h.ctypes.data,
-                                       None if pt is None else pt.ctypes.data, n,
-                                       ctypes.byref(params), out.data_ptr(),
-                                       _stream_handle(stream)))
+    r = _rois(rois, n)
+    out = _out_tensor(out, n, params, src.device, options.layout if options else LAYOUT_NCHW)
+    if r is None and options is None:
+        _check(lib().smol_preprocess_batch(src.data_ptr(), src.numel(), off.ctypes.data,
+                                           w.ctypes.data, h.ctypes.data,
+                                           None if pt is None else pt.ctypes.data, n,
+                                           ctypes.byref(params), out.data_ptr(),
+                                           _stream_handle(stream)))
+    else:
+        _check(lib().smol_preprocess_batch_ex(
+            src.data_ptr(), src.numel(), off.ctypes.data, w.ctypes.data, h.ctypes.data,
+            None if pt is None else pt.ctypes.data, None if r is None else r.ctypes.data, n,
+            ctypes.byref(params), None if options is None else ctypes.byref(options),
+            out.data_ptr(), _stream_handle(stream)))
     return out
 
 
 def yuv420_preprocess_batch(src, y_offsets, cb_offsets, cr_offsets, widths, heights,
-                            params: Params, out=None, stream=None):
-    """Planar I420 uint8 frames in the device tensor ``src`` -> NCHW RGB tensor."""
+                            params: Params, out=None, stream=None, rois=None,
+                            options: Options | None = None):
+    """Planar I420 uint8 frames in the device tensor ``src`` -> NCHW (or NHWC)
+    RGB tensor; ``rois`` / ``options`` as for ``preprocess_batch``."""
     if src.dtype.itemsize != 1 or not src.is_cuda or not src.is_contiguous():
         raise ValueError("src must be a contiguous uint8 device tensor")
     yo = _table(y_offsets, np.int64)
@@ -230,22 +294,37 @@ def yuv420_preprocess_batch(src, y_offsets, cb_offsets, cr_offsets, widths, heig
     n = len(yo)
     if not (len(bo) == len(ro) == len(w) == len(h) == n):
         raise ValueError("table lengths differ")
-    out = _out_tensor(out, n, params, src.device)
-    _check(lib().smol_yuv420_preprocess_batch(src.data_ptr(), src.numel(), yo.ctypes.data,
-                                              bo.ctypes.data, ro.ctypes.data, w.ctypes.data,
-                                              h.ctypes.data, n, ctypes.byref(params),
-                                              out.data_ptr(), _stream_handle(stream)))
+    r = _rois(rois, n)
+    out = _out_tensor(out, n, params, src.device, options.layout if options else LAYOUT_NCHW)
+    if r is None and options is None:
+        _check(lib().smol_yuv420_preprocess_batch(src.data_ptr(), src.numel(), yo.ctypes.data,
+                                                  bo.ctypes.data, ro.ctypes.data, w.ctypes.data,
+                                                  h.ctypes.data, n, ctypes.byref(params),
+                                                  out.data_ptr(), _stream_handle(stream)))
+    else:
+        _check(lib().smol_yuv420_preprocess_batch_ex(
+            src.data_ptr(), src.numel(), yo.ctypes.data, bo.ctypes.data, ro.ctypes.data,
+            w.ctypes.data, h.ctypes.data, None if r is None else r.ctypes.data, n,
+            ctypes.byref(params), None if options is None else ctypes.byref(options),
+            out.data_ptr(), _stream_handle(stream)))
     return out
+
+
+def _workload_options(wl) -> Options | None:
+    if not wl.variant:
+        return None
+    return make_options(wl.resize_mode, wl.layout, wl.siting)
 
 
 def run_workload(wl, src_dev, out=None, stream=None):
     """Run a ``synthetic.Workload`` whose ``src`` already sits on the device."""
     p = make_params(wl.resize_short, wl.crop_h, wl.crop_w, wl.mean, wl.std, wl.out_dtype)
+    o = _workload_options(wl)
     if wl.kind == "rgb":
         return preprocess_batch(src_dev, wl.offsets, wl.widths, wl.heights, p, wl.pitches, out,
-                                stream)
+                                stream, wl.rois, o)
     return yuv420_preprocess_batch(src_dev, wl.y_offsets, wl.cb_offsets, wl.cr_offsets,
-                                   wl.widths, wl.heights, p, out, stream)
+                                   wl.widths, wl.heights, p, out, stream, wl.rois, o)
 
 
 class PreparedCall:
@@ -258,22 +337,29 @@ class PreparedCall:
         self.kind = wl.kind
         self.n = wl.n
         self._keep = []
+        self.options = _workload_options(wl)
+        ex = self.options is not None
+        r = None if wl.rois is None else _rois(wl.rois, wl.n)
         if wl.kind == "rgb":
             tabs = [_table(wl.offsets, np.int64), _table(wl.widths, np.int32),
                     _table(wl.heights, np.int32)]
             pt = None if wl.pitches is None else _table(wl.pitches, np.int32)
-            self._keep = tabs + [pt]
+            self._keep = tabs + [pt, r]
             self._args = [t.ctypes.data for t in tabs] + [None if pt is None else pt.ctypes.data]
-            self._fn = lib().smol_preprocess_batch
+            self._fn = lib().smol_preprocess_batch_ex if ex else lib().smol_preprocess_batch
         else:
             tabs = [_table(wl.y_offsets, np.int64), _table(wl.cb_offsets, np.int64),
                     _table(wl.cr_offsets, np.int64), _table(wl.widths, np.int32),
                     _table(wl.heights, np.int32)]
-            self._keep = tabs
+            self._keep = tabs + [r]
             self._args = [t.ctypes.data for t in tabs]
-            self._fn = lib().smol_yuv420_preprocess_batch
+            self._fn = (lib().smol_yuv420_preprocess_batch_ex if ex
+                        else lib().smol_yuv420_preprocess_batch)
+        if ex:
+            self._args.append(None if r is None else r.ctypes.data)
         self._pref = ctypes.byref(self.params)
+        self._tail = [ctypes.byref(self.options)] if ex else []
 
     def __call__(self, src_ptr: int, src_bytes: int, out_ptr: int, stream_handle) -> None:
-        _check(self._fn(src_ptr, src_bytes, *self._args, self.n, self._pref, out_ptr,
-                        stream_handle))
+        _check(self._fn(src_ptr, src_bytes, *self._args, self.n, self._pref, *self._tail,
+                        out_ptr, stream_handle))

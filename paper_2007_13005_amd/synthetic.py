@@ -18,6 +18,9 @@ five seeded stand-ins reproduce their shapes, size mix and value ranges:
       small per-frame shifts; short side 224, crop 224, fp16 out
   c5  128 x 1280x720 planar YCbCr 4:2:0 frames, Y in 16..235, Cb/Cr in 16..240;
       short side 256, crop 224, fp16 out
+  c6  256 regions of interest (64..512 px boxes) in 16 1080p RGB frames,
+      resized directly to 112x112, channels-last fp16 (detection / face crops,
+      the ROI use of section 5.3)
 
 Config k draws from ``numpy.random.default_rng(13005 + k)`` (PCG64).
 The normalisation constants are the ImageNet per-channel statistics the
@@ -62,6 +65,18 @@ class Workload:
     mean: np.ndarray = field(default_factory=lambda: IMAGENET_MEAN_255.copy())
     std: np.ndarray = field(default_factory=lambda: IMAGENET_STD_255.copy())
     description: str = ""
+    # variants: an ROI per image (int32 [n, 4]: x, y, w, h), the resize mode
+    # (0 short side + centre crop, 1 direct), the layout (0 NCHW, 1 NHWC) and
+    # the I420 chroma siting (0 centred, 1 co-sited)
+    rois: np.ndarray | None = None
+    resize_mode: int = 0
+    layout: int = 0
+    siting: int = 0
+
+    @property
+    def variant(self) -> bool:
+        return (self.rois is not None or self.resize_mode != 0 or self.layout != 0 or
+                self.siting != 0)
 
     @property
     def n(self) -> int:
@@ -72,6 +87,8 @@ class Workload:
         return 4 if self.out_dtype == OUT_F32 else 2
 
     def out_shape(self) -> tuple[int, int, int, int]:
+        if self.layout == 1:
+            return (self.n, self.crop_h, self.crop_w, 3)
         return (self.n, 3, self.crop_h, self.crop_w)
 
 
@@ -214,7 +231,34 @@ def c5(n: int = 128, height: int = 720, width: int = 1280) -> Workload:
                            "NCHW fp16")
 
 
-CONFIGS = {"c1": c1, "c2": c2, "c3": c3, "c4": c4, "c5": c5}
+def c6(n: int = 256, height: int = 1080, width: int = 1920) -> Workload:
+    """Detection / face crops: one ROI per 1080p frame (square-ish boxes of
+    64..512 px at random positions), each resized directly to 112x112, fp16,
+    channels last -- the shape of a second-stage recogniser's input."""
+    rng = np.random.default_rng(SEED_BASE + 6)
+    frames = 16  # the ROIs index a smaller set of frames, several per frame
+    base = rng.integers(0, 256, size=(frames, height, width, 3), dtype=np.uint8)
+    side = rng.integers(64, 513, size=n)
+    aspect = rng.uniform(0.75, 1.33, size=n)
+    w = np.clip(np.rint(side * np.sqrt(aspect)), 16, width).astype(np.int64)
+    h = np.clip(np.rint(side / np.sqrt(aspect)), 16, height).astype(np.int64)
+    x = (rng.random(n) * (width - w + 1)).astype(np.int64)
+    y = (rng.random(n) * (height - h + 1)).astype(np.int64)
+    fi = rng.integers(0, frames, size=n)
+    stride = height * width * 3
+    wl = Workload(name="c6", kind="rgb", src=base.reshape(-1),
+                  widths=np.full(n, width, np.int32), heights=np.full(n, height, np.int32),
+                  resize_short=112, crop_h=112, crop_w=112, out_dtype=OUT_F16,
+                  offsets=fi.astype(np.int64) * stride,
+                  description=f"{n} ROIs (64..512 px boxes) in {frames} x {width}x{height} RGB "
+                              "uint8 frames; direct resize to 112x112, NHWC fp16")
+    wl.rois = np.stack([x, y, w, h], axis=1).astype(np.int32)
+    wl.resize_mode = 1
+    wl.layout = 1
+    return wl
+
+
+CONFIGS = {"c1": c1, "c2": c2, "c3": c3, "c4": c4, "c5": c5, "c6": c6}
 
 
 def make(name: str, **kw) -> Workload:

@@ -24,6 +24,17 @@ def note(msg: str) -> None:
 
 
 def run_oracle(wl: synthetic.Workload) -> np.ndarray:
+    if wl.variant:
+        if wl.kind == "rgb":
+            return oracle.preprocess_batch_ex(wl.src, wl.offsets, wl.widths, wl.heights,
+                                              wl.pitches, wl.rois, wl.resize_short, wl.crop_h,
+                                              wl.crop_w, wl.mean, wl.std, wl.out_dtype,
+                                              wl.resize_mode, wl.layout)
+        return oracle.yuv420_preprocess_batch_ex(wl.src, wl.y_offsets, wl.cb_offsets,
+                                                 wl.cr_offsets, wl.widths, wl.heights, wl.rois,
+                                                 wl.resize_short, wl.crop_h, wl.crop_w, wl.mean,
+                                                 wl.std, wl.out_dtype, wl.resize_mode, wl.layout,
+                                                 wl.siting)
     if wl.kind == "rgb":
         return oracle.preprocess_batch(wl.src, wl.offsets, wl.widths, wl.heights, wl.pitches,
                                        wl.resize_short, wl.crop_h, wl.crop_w, wl.mean, wl.std,

@@ -206,3 +206,97 @@ def test_yuv_footprint_c5():
     assert (g["resized_w"], g["resized_h"], g["crop_left"], g["crop_top"]) == (455, 256, 115, 16)
     assert g["src_rows"] == 448 and g["src_x_last"] - g["src_x_first"] + 1 == 629
     assert g["chroma_rows"] == 316 and g["chroma_x_last"] - g["chroma_x_first"] + 1 == 316
+
+
+# ---------------------------------------------------------------------------
+# variants: ROI, options (validation on the host, geometry against the oracle)
+# ---------------------------------------------------------------------------
+
+
+def _rgb_ex_call(rois=None, opts=None, widths=(320,), heights=(240,), params=None):
+    p = params or _params()
+    off = np.zeros(1, np.int64)
+    w = np.asarray(widths, np.int32)
+    h = np.asarray(heights, np.int32)
+    r = None if rois is None else np.asarray(rois, np.int32).reshape(-1, 4)
+    rc = smol.lib().smol_preprocess_batch_ex(
+        FAKE_SRC, 10**9, off.ctypes.data, w.ctypes.data, h.ctypes.data, None,
+        None if r is None else r.ctypes.data, 1, ctypes.byref(p),
+        None if opts is None else ctypes.byref(opts), FAKE_OUT, None)
+    return rc, smol.lib().smol_last_error().decode()
+
+
+def _opts(**kw):
+    o = smol.make_options()
+    for k, v in kw.items():
+        if k == "reserved":
+            o.reserved[0] = v
+        else:
+            setattr(o, k, v)
+    return o
+
+
+@pytest.mark.parametrize("kw,needle", [
+    (dict(opts=_opts(resize_mode=2)), "resize_mode"),
+    (dict(opts=_opts(layout=5)), "layout"),
+    (dict(opts=_opts(chroma_siting=-1)), "chroma_siting"),
+    (dict(opts=_opts(reserved=1)), "reserved"),
+    (dict(rois=(-1, 0, 10, 10)), "ROI"),
+    (dict(rois=(0, 0, 0, 10)), "ROI"),
+    (dict(rois=(300, 0, 21, 10)), "ROI"),
+    (dict(rois=(0, 200, 10, 41)), "ROI"),
+    # a 100 x 100 ROI cannot hold a 224 crop after a short-side resize to 160
+    (dict(rois=(0, 0, 100, 100), params=_params(resize_short=160)), "larger than resized"),
+])
+def test_variant_validation_rejects(kw, needle):
+    rc, msg = _rgb_ex_call(**kw)
+    assert rc == smol.ERR_INVALID_ARG, (rc, msg)
+    assert needle in msg
+
+
+def test_nhwc_refuses_forced_lds_and_gather_paths():
+    for path in (smol.PATH_LDS, smol.PATH_GATHER):
+        smol.set_tuning(path=path)
+        try:
+            rc, msg = _rgb_ex_call(opts=_opts(layout=smol.LAYOUT_NHWC))
+        finally:
+            smol.reset_tuning()
+        assert rc == smol.ERR_UNSUPPORTED and "NHWC" in msg
+
+
+def test_geometry_ex_matches_oracle():
+    """ROI geometry: resized size and crop offsets of the ROI (oracle), columns
+    in image coordinates; direct resize: the output size, no crop."""
+    rng = np.random.default_rng(22)
+    for _ in range(300):
+        W, H = (int(v) for v in rng.integers(8, 3000, size=2))
+        rw, rh = int(rng.integers(1, W + 1)), int(rng.integers(1, H + 1))
+        rx, ry = int(rng.integers(0, W - rw + 1)), int(rng.integers(0, H - rh + 1))
+        Ch, Cw = (int(v) for v in rng.integers(1, 300, size=2))
+        mode = int(rng.integers(0, 2))
+        S = max(Ch, Cw) + int(rng.integers(0, 50))
+        p = _params(resize_short=S, crop_h=Ch, crop_w=Cw)
+        Wr, Hr, left, top = oracle.output_geometry(rw, rh, S, Ch, Cw, mode)
+        if Cw > Wr or Ch > Hr:
+            continue
+        g = smol.image_geometry_ex(W, H, p, roi=(rx, ry, rw, rh),
+                                   options=smol.make_options(resize_mode=mode))
+        assert (g["resized_w"], g["resized_h"], g["crop_left"], g["crop_top"]) == (Wr, Hr, left,
+                                                                                   top)
+        assert g["src_x_first"] == rx + oracle.axis_tap(left, rw, Wr)[0]
+        assert g["src_x_last"] == rx + oracle.axis_tap(left + Cw - 1, rw, Wr)[1]
+
+
+def test_left_siting_chroma_footprint():
+    """Co-sited chroma: luma columns x0 .. x1 read chroma columns x0 // 2 ..
+    min(x1 // 2 + 1, Wc - 1) (the centred map reads one column further left)."""
+    p = _params(resize_short=112, crop_h=112, crop_w=112)
+    roi = (101, 37, 300, 300)
+    gc = smol.image_geometry_ex(640, 480, p, yuv420=True, roi=roi,
+                                options=smol.make_options(resize_mode=1))
+    gl = smol.image_geometry_ex(640, 480, p, yuv420=True, roi=roi,
+                                options=smol.make_options(resize_mode=1,
+                                                          chroma_siting=smol.CHROMA_LEFT))
+    x0, x1 = gl["src_x_first"], gl["src_x_last"]
+    assert (gl["chroma_x_first"], gl["chroma_x_last"]) == (x0 // 2, min(x1 // 2 + 1, 319))
+    assert gc["chroma_x_first"] == (2 * x0 - 1) // 4
