@@ -17,15 +17,21 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libsmol.so")
 
 # The row-streaming kernels are split into parts (input, output type, row
-# walk) so that the compiler runs on the parts in parallel.
+# walk, output layout) so that the compiler runs on the parts in parallel.
 SOURCES = [
     "smol_kernels.hip",
     "smol_rows_rgb_f16_range.hip",
+    "smol_rows_rgb_f16_range_nhwc.hip",
     "smol_rows_rgb_f16_stride.hip",
+    "smol_rows_rgb_f16_stride_nhwc.hip",
     "smol_rows_rgb_f32_range.hip",
+    "smol_rows_rgb_f32_range_nhwc.hip",
     "smol_rows_rgb_f32_stride.hip",
+    "smol_rows_rgb_f32_stride_nhwc.hip",
     "smol_rows_yuv_range.hip",
+    "smol_rows_yuv_range_nhwc.hip",
     "smol_rows_yuv_stride.hip",
+    "smol_rows_yuv_stride_nhwc.hip",
     "smol_host.cpp",
 ]
 HEADERS = ["smol_internal.h", "smol_device.h", "smol_rows.h"]

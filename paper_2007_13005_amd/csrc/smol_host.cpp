@@ -257,8 +257,12 @@ int64_t distinct_rows(int64_t top, int64_t Ch, int64_t H, int64_t Hr)
 }
 
 // ---------------------------------------------------------------------------
-// Per-device descriptor staging: pinned host ring + device ring, slots reused
-// once the event recorded after the kernel that read them has completed.
+// Per-device descriptor staging: pinned host ring + device ring. A ragged
+// batch's table is copied on the library's own copy stream (a DMA engine, so
+// the copy runs while the caller's stream is still busy with earlier work);
+// the caller's stream waits for that copy before the kernel. A slot is
+// reused once the kernel that read it has completed (the host waits for
+// that kernel's event; the kernel itself waited for the slot's copy).
 // ---------------------------------------------------------------------------
 
 struct Staging {
@@ -267,8 +271,11 @@ struct Staging {
     size_t slot_cap = 0;
     uint8_t *host = nullptr;
     uint8_t *dev = nullptr;
-    hipEvent_t ev[kSlots] = {};
+    hipStream_t copy = nullptr;      // default priority, non-blocking
+    hipEvent_t ev[kSlots] = {};      // after the kernel that read slot k
     bool pending[kSlots] = {};
+    hipEvent_t up[kSlots] = {};      // after the copy into slot k
+    bool up_pending[kSlots] = {};
     int next = 0;
 };
 
@@ -285,18 +292,31 @@ Staging *staging_for(int device)
     return g_staging[device];
 }
 
-// Grow the ring so each slot holds `bytes`. Caller holds st->mu.
+// Grow the ring so each slot holds `bytes` (and create the copy stream on
+// first use). Caller holds st->mu.
 hipError_t staging_reserve(Staging *st, size_t bytes)
 {
+    if (!st->copy) {
+        hipError_t e = hipStreamCreateWithFlags(&st->copy, hipStreamNonBlocking);
+        if (e != hipSuccess)
+            return e;
+    }
     if (bytes <= st->slot_cap)
         return hipSuccess;
-    for (int i = 0; i < Staging::kSlots; ++i)
+    for (int i = 0; i < Staging::kSlots; ++i) {
         if (st->pending[i]) {
             hipError_t e = hipEventSynchronize(st->ev[i]);
             if (e != hipSuccess)
                 return e;
             st->pending[i] = false;
         }
+        if (st->up_pending[i]) {
+            hipError_t e = hipEventSynchronize(st->up[i]);
+            if (e != hipSuccess)
+                return e;
+            st->up_pending[i] = false;
+        }
+    }
     if (st->host)
         (void)hipHostFree(st->host);
     if (st->dev)
@@ -313,12 +333,18 @@ hipError_t staging_reserve(Staging *st, size_t bytes)
     e = hipMalloc((void **)&st->dev, cap * Staging::kSlots);
     if (e != hipSuccess)
         return e;
-    for (int i = 0; i < Staging::kSlots; ++i)
+    for (int i = 0; i < Staging::kSlots; ++i) {
         if (!st->ev[i]) {
             e = hipEventCreateWithFlags(&st->ev[i], hipEventDisableTiming);
             if (e != hipSuccess)
                 return e;
         }
+        if (!st->up[i]) {
+            e = hipEventCreateWithFlags(&st->up[i], hipEventDisableTiming);
+            if (e != hipSuccess)
+                return e;
+        }
+    }
     st->slot_cap = cap;
     return hipSuccess;
 }
@@ -507,18 +533,30 @@ int run_batch(const std::vector<Desc> &descs, size_t first, size_t count, int no
             return hip_fail(e, "descriptor staging allocation");
         slot = st->next;
         st->next = (st->next + 1) % Staging::kSlots;
+        // The slot's last kernel waited for the slot's last copy, so once that
+        // kernel is done both the host and the device slot are free. (Waiting
+        // on the kernel's event, not on the copy's, keeps the host on the
+        // compute queue's completion signal.)
         if (st->pending[slot]) {
             e = hipEventSynchronize(st->ev[slot]);
             if (e != hipSuccess)
                 return hip_fail(e, "hipEventSynchronize");
             st->pending[slot] = false;
+            st->up_pending[slot] = false;
         }
         uint8_t *h = st->host + (size_t)slot * st->slot_cap;
         uint8_t *dv = st->dev + (size_t)slot * st->slot_cap;
         std::memcpy(h, descs.data() + first, bytes);
-        e = hipMemcpyAsync(dv, h, bytes, hipMemcpyHostToDevice, s);
+        e = hipMemcpyAsync(dv, h, bytes, hipMemcpyHostToDevice, st->copy);
         if (e != hipSuccess)
             return hip_fail(e, "hipMemcpyAsync(descriptors)");
+        e = hipEventRecord(st->up[slot], st->copy);
+        if (e != hipSuccess)
+            return hip_fail(e, "hipEventRecord(copy)");
+        st->up_pending[slot] = true;
+        e = hipStreamWaitEvent(s, st->up[slot], 0);
+        if (e != hipSuccess)
+            return hip_fail(e, "hipStreamWaitEvent");
         a.table = (const Desc *)dv;
     } else {
         a.table = nullptr;

@@ -88,12 +88,19 @@ int launch_yuv_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, void *str
 int occupancy_yuv_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, int *blocks_per_cu);
 
 // Row-streaming kernels for the plan in the arguments (the file of each part:
-// smol_rows_<input>_<output>_<walk>.hip); `interleave` picks the walk.
+// smol_rows_<input>_<walk>[_nhwc].hip); `interleave` picks the walk, `nhwc`
+// the output layout.
 const void *rows_rgb_f16_range(const BatchArgs &a);
+const void *rows_rgb_f16_range_nhwc(const BatchArgs &a);
 const void *rows_rgb_f16_stride(const BatchArgs &a);
+const void *rows_rgb_f16_stride_nhwc(const BatchArgs &a);
 const void *rows_rgb_f32_range(const BatchArgs &a);
+const void *rows_rgb_f32_range_nhwc(const BatchArgs &a);
 const void *rows_rgb_f32_stride(const BatchArgs &a);
+const void *rows_rgb_f32_stride_nhwc(const BatchArgs &a);
 const void *rows_yuv_range(const BatchArgs &a, int f16);
+const void *rows_yuv_range_nhwc(const BatchArgs &a, int f16);
 const void *rows_yuv_stride(const BatchArgs &a, int f16);
+const void *rows_yuv_stride_nhwc(const BatchArgs &a, int f16);
 
 }  // namespace smol

@@ -758,6 +758,9 @@ int launch_rgb_gather(const BatchArgs &a, int out_f16, size_t lds_bytes, void *s
 
 const void *rows_kernel(const BatchArgs &a, int f16)
 {
+    if (a.nhwc)
+        return f16 ? (a.interleave ? rows_rgb_f16_stride_nhwc(a) : rows_rgb_f16_range_nhwc(a))
+                   : (a.interleave ? rows_rgb_f32_stride_nhwc(a) : rows_rgb_f32_range_nhwc(a));
     return f16 ? (a.interleave ? rows_rgb_f16_stride(a) : rows_rgb_f16_range(a))
                : (a.interleave ? rows_rgb_f32_stride(a) : rows_rgb_f32_range(a));
 }
@@ -807,6 +810,8 @@ int launch_yuv_direct(const BatchArgs &a, int out_f16, void *stream)
 
 const void *yuv_rows_kernel_for(const BatchArgs &a, int f16)
 {
+    if (a.nhwc)
+        return a.interleave ? rows_yuv_stride_nhwc(a, f16) : rows_yuv_range_nhwc(a, f16);
     return a.interleave ? rows_yuv_stride(a, f16) : rows_yuv_range(a, f16);
 }
 

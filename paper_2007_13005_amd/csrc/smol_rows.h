@@ -1,6 +1,6 @@
 // smol_rows.h -- the row-streaming kernels (RGB and I420) as templates. Each
-// smol_*_rows*.hip file instantiates one part of them, so the parts build in
-// parallel.
+// smol_rows_*.hip file instantiates one part of them (input, output type, row
+// walk, output layout), so the parts build in parallel.
 #pragma once
 
 #include "smol_device.h"
@@ -714,7 +714,7 @@ __device__ __forceinline__ void rows_compute_reuse(const NormK &nk, uint32_t row
     rows_vertical<F16, J, EXACT>(nk, h0, h1, wy, out);
 }
 
-template <int F16, int J, int EXACT, int G, int P, int STRIDE>
+template <int F16, int J, int EXACT, int G, int P, int STRIDE, int NHWC>
 __global__ void __launch_bounds__(64 * kRowsMaxWavesPerGroup) rgb_rows_kernel(BatchArgs a)
 {
     extern __shared__ __attribute__((aligned(16))) uint8_t lds_all[];
@@ -736,7 +736,7 @@ __global__ void __launch_bounds__(64 * kRowsMaxWavesPerGroup) rgb_rows_kernel(Ba
     // rows, plus 2 Ch (planes 1 and 2 of the image left) when it wraps.
     // bytes between an image's output rows: Cw elements per plane (NCHW) or
     // 3 Cw (NHWC); a wrap to the next image skips the rest of the image.
-    const long long rb = (long long)a.Cw * kEsz, rowb = a.nhwc ? 3 * rb : rb;
+    const long long rb = (long long)a.Cw * kEsz, rowb = NHWC ? 3 * rb : rb;
     const long long imgb = 3LL * Ch * rb;
     uint8_t *orow = (uint8_t *)a.out + (long long)(a.img_base + c_img) * imgb + c_rr * rowb;
     const long long ostep = step.di * imgb + step.dr * rowb, owrap = imgb - Ch * rowb;
@@ -806,7 +806,7 @@ __global__ void __launch_bounds__(64 * kRowsMaxWavesPerGroup) rgb_rows_kernel(Ba
         advance();                                                                            \
         compute();                                                                            \
         write_rows<G>(lds, NXT, lane);                                                        \
-        store_row<F16, J>(orow, plane, a.Cw, lane, out, a.nhwc);                              \
+        store_row<F16, J>(orow, plane, a.Cw, lane, out, NHWC);                              \
         csh0 = NXT.sh0;                                                                       \
         csh1 = NXT.sh1;                                                                       \
         cy0 = NXT.y0;                                                                         \
@@ -849,7 +849,7 @@ __global__ void __launch_bounds__(64 * kRowsMaxWavesPerGroup) rgb_rows_kernel(Ba
     }
 #undef SMOL_ROWS_STEP
     compute();
-    store_row<F16, J>(orow, plane, a.Cw, lane, out, a.nhwc);
+    store_row<F16, J>(orow, plane, a.Cw, lane, out, NHWC);
 }
 
 // ---------------------------------------------------------------------------
@@ -1170,7 +1170,7 @@ __device__ __forceinline__ void yuv_compute(const NormK &nk, uint32_t slot, cons
     }
 }
 
-template <int F16, int J, int EXACT, int STRIDE>
+template <int F16, int J, int EXACT, int STRIDE, int NHWC>
 __global__ void __launch_bounds__(64 * kRowsMaxWavesPerGroup) __attribute__((amdgpu_waves_per_eu(J <= 2 ? 3 : 1)))
 yuv_rows_kernel(BatchArgs a)
 {
@@ -1190,7 +1190,7 @@ yuv_rows_kernel(BatchArgs a)
     yuv_cursor_image<STRIDE>(lc, a, c_img, c_rr, step);
     // bytes between an image's output rows: Cw elements per plane (NCHW) or
     // 3 Cw (NHWC); a wrap to the next image skips the rest of the image.
-    const long long rb = (long long)a.Cw * kEsz, rowb = a.nhwc ? 3 * rb : rb;
+    const long long rb = (long long)a.Cw * kEsz, rowb = NHWC ? 3 * rb : rb;
     const long long imgb = 3LL * Ch * rb;
     uint8_t *orow = (uint8_t *)a.out + (long long)(a.img_base + c_img) * imgb + c_rr * rowb;
     const long long ostep = step.di * imgb + step.dr * rowb, owrap = imgb - Ch * rowb;
@@ -1235,7 +1235,7 @@ yuv_rows_kernel(BatchArgs a)
         advance();
         yuv_compute<F16, J, EXACT>(nk, lds0, csh, cwy, cfy0, cfy1, cb0, cols, out);
         yuv_write(lds, R, lane);
-        store_row<F16, J>(orow, plane, a.Cw, lane, out, a.nhwc);
+        store_row<F16, J>(orow, plane, a.Cw, lane, out, NHWC);
 #pragma unroll
         for (int s = 0; s < 8; ++s)
             csh[s] = R.sh[s];
@@ -1263,52 +1263,54 @@ yuv_rows_kernel(BatchArgs a)
         }
     }
     yuv_compute<F16, J, EXACT>(nk, lds0, csh, cwy, cfy0, cfy1, cb0, cols, out);
-    store_row<F16, J>(orow, plane, a.Cw, lane, out, a.nhwc);
+    store_row<F16, J>(orow, plane, a.Cw, lane, out, NHWC);
 }
 
 
 // Kernel for a plan: output type, arithmetic mode, chunk groups, column
 // pairs per lane and prefetch depth from the launch arguments.
-template <int F16, int EXACT, int G, int STRIDE>
+template <int F16, int EXACT, int G, int STRIDE, int NHWC>
 const void *rgb_rows_g(int col_iters, int prefetch)
 {
     if (prefetch == 1)
-        return col_iters <= 1   ? (const void *)rgb_rows_kernel<F16, 1, EXACT, G, 1, STRIDE>
-               : col_iters <= 2 ? (const void *)rgb_rows_kernel<F16, 2, EXACT, G, 1, STRIDE>
-                                : (const void *)rgb_rows_kernel<F16, 4, EXACT, G, 1, STRIDE>;
-    return col_iters <= 1   ? (const void *)rgb_rows_kernel<F16, 1, EXACT, G, 2, STRIDE>
-           : col_iters <= 2 ? (const void *)rgb_rows_kernel<F16, 2, EXACT, G, 2, STRIDE>
-                            : (const void *)rgb_rows_kernel<F16, 4, EXACT, G, 2, STRIDE>;
+        return col_iters <= 1   ? (const void *)rgb_rows_kernel<F16, 1, EXACT, G, 1, STRIDE, NHWC>
+               : col_iters <= 2 ? (const void *)rgb_rows_kernel<F16, 2, EXACT, G, 1, STRIDE, NHWC>
+                                : (const void *)rgb_rows_kernel<F16, 4, EXACT, G, 1, STRIDE, NHWC>;
+    return col_iters <= 1   ? (const void *)rgb_rows_kernel<F16, 1, EXACT, G, 2, STRIDE, NHWC>
+           : col_iters <= 2 ? (const void *)rgb_rows_kernel<F16, 2, EXACT, G, 2, STRIDE, NHWC>
+                            : (const void *)rgb_rows_kernel<F16, 4, EXACT, G, 2, STRIDE, NHWC>;
 }
 
-template <int F16, int EXACT, int STRIDE>
+template <int F16, int EXACT, int STRIDE, int NHWC>
 const void *rgb_rows_e(int col_iters, int groups, int prefetch)
 {
-    return groups <= 1   ? rgb_rows_g<F16, EXACT, 1, STRIDE>(col_iters, prefetch)
-           : groups <= 2 ? rgb_rows_g<F16, EXACT, 2, STRIDE>(col_iters, prefetch)
-                         : rgb_rows_g<F16, EXACT, 4, STRIDE>(col_iters, prefetch);
+    return groups <= 1   ? rgb_rows_g<F16, EXACT, 1, STRIDE, NHWC>(col_iters, prefetch)
+           : groups <= 2 ? rgb_rows_g<F16, EXACT, 2, STRIDE, NHWC>(col_iters, prefetch)
+                         : rgb_rows_g<F16, EXACT, 4, STRIDE, NHWC>(col_iters, prefetch);
 }
 
-template <int F16, int STRIDE>
+template <int F16, int STRIDE, int NHWC>
 const void *rgb_rows_table(const BatchArgs &a)
 {
-    return a.exact ? rgb_rows_e<F16, 1, STRIDE>(a.col_iters, a.row_groups, a.prefetch)
-                   : rgb_rows_e<F16, 0, STRIDE>(a.col_iters, a.row_groups, a.prefetch);
+    return a.exact ? rgb_rows_e<F16, 1, STRIDE, NHWC>(a.col_iters, a.row_groups, a.prefetch)
+                   : rgb_rows_e<F16, 0, STRIDE, NHWC>(a.col_iters, a.row_groups, a.prefetch);
 }
 
-template <int F16, int EXACT, int STRIDE>
+template <int F16, int EXACT, int STRIDE, int NHWC>
 const void *yuv_rows_e(int col_iters)
 {
-    return col_iters <= 1   ? (const void *)yuv_rows_kernel<F16, 1, EXACT, STRIDE>
-           : col_iters <= 2 ? (const void *)yuv_rows_kernel<F16, 2, EXACT, STRIDE>
-                            : (const void *)yuv_rows_kernel<F16, 4, EXACT, STRIDE>;
+    return col_iters <= 1   ? (const void *)yuv_rows_kernel<F16, 1, EXACT, STRIDE, NHWC>
+           : col_iters <= 2 ? (const void *)yuv_rows_kernel<F16, 2, EXACT, STRIDE, NHWC>
+                            : (const void *)yuv_rows_kernel<F16, 4, EXACT, STRIDE, NHWC>;
 }
 
-template <int STRIDE>
+template <int STRIDE, int NHWC>
 const void *yuv_rows_table(const BatchArgs &a, int f16)
 {
-    return f16 ? (a.exact ? yuv_rows_e<1, 1, STRIDE>(a.col_iters) : yuv_rows_e<1, 0, STRIDE>(a.col_iters))
-               : (a.exact ? yuv_rows_e<0, 1, STRIDE>(a.col_iters) : yuv_rows_e<0, 0, STRIDE>(a.col_iters));
+    return f16 ? (a.exact ? yuv_rows_e<1, 1, STRIDE, NHWC>(a.col_iters)
+                          : yuv_rows_e<1, 0, STRIDE, NHWC>(a.col_iters))
+               : (a.exact ? yuv_rows_e<0, 1, STRIDE, NHWC>(a.col_iters)
+                          : yuv_rows_e<0, 0, STRIDE, NHWC>(a.col_iters));
 }
 
 }  // namespace

@@ -1,8 +1,8 @@
-// smol_rows_rgb_f32_stride.hip -- RGB row-streaming kernels, fp32 output, rows strided across waves.
+// smol_rows_rgb_f32_stride.hip -- RGB row-streaming kernels, fp32 output, rows strided across waves, NCHW output.
 #include "smol_rows.h"
 
 namespace smol {
 
-const void *rows_rgb_f32_stride(const BatchArgs &a) { return rgb_rows_table<0, 1>(a); }
+const void *rows_rgb_f32_stride(const BatchArgs &a) { return rgb_rows_table<0, 1, 0>(a); }
 
 }  // namespace smol

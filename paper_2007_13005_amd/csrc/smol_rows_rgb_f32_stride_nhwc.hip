@@ -1,0 +1,8 @@
+// smol_rows_rgb_f32_stride_nhwc.hip -- RGB row-streaming kernels, fp32 output, rows strided across waves, NHWC output.
+#include "smol_rows.h"
+
+namespace smol {
+
+const void *rows_rgb_f32_stride_nhwc(const BatchArgs &a) { return rgb_rows_table<0, 1, 1>(a); }
+
+}  // namespace smol

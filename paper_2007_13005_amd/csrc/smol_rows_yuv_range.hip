@@ -1,8 +1,8 @@
-// smol_rows_yuv_range.hip -- I420 row-streaming kernels, contiguous row ranges.
+// smol_rows_yuv_range.hip -- I420 row-streaming kernels, contiguous row ranges, NCHW output.
 #include "smol_rows.h"
 
 namespace smol {
 
-const void *rows_yuv_range(const BatchArgs &a, int f16) { return yuv_rows_table<0>(a, f16); }
+const void *rows_yuv_range(const BatchArgs &a, int f16) { return yuv_rows_table<0, 0>(a, f16); }
 
 }  // namespace smol
