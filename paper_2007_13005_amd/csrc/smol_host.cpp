@@ -463,6 +463,15 @@ int run_batch(const std::vector<Desc> &descs, size_t first, size_t count, int no
         return fail(SMOL_ERR_UNSUPPORTED, "LDS plan of %zu bytes exceeds the device's %d per "
                     "workgroup", pl.lds_bytes, di.lds_per_block);
     const bool rows = pl.path == smol::PATH_ROWS || pl.path == smol::PATH_YUV_ROWS;
+    {
+        // Row order of the row-streaming kernels: interleaved across waves
+        // for uniform batches of long staged rows (memory-bound: the waves
+        // then stream neighbouring rows), contiguous ranges otherwise. (Set
+        // before the occupancy query: the two walks are different kernels.)
+        const int order = g_row_order.load();
+        a.interleave = order == 2 || (order == 0 && uniform && pl.path == smol::PATH_ROWS &&
+                                      a.row_groups >= 4);
+    }
     if (pl.path == smol::PATH_LDS || pl.path == smol::PATH_GATHER || rows) {
         a.wpg = rows ? smol::kRowsMaxWavesPerGroup : 1;
         int per_cu = 0;
@@ -562,14 +571,6 @@ int run_batch(const std::vector<Desc> &descs, size_t first, size_t count, int no
         a.table = nullptr;
         a.uni = descs[first];
         a.stride = stride;
-    }
-    {
-        // Row order of the row-streaming kernels: interleaved across waves
-        // for uniform batches of long staged rows (memory-bound: the waves
-        // then stream neighbouring rows), contiguous ranges otherwise.
-        const int order = g_row_order.load();
-        a.interleave = order == 2 || (order == 0 && uniform && pl.path == smol::PATH_ROWS &&
-                                      a.row_groups >= 4);
     }
 
     const int rc = launch(a, pl, stream);

@@ -25,6 +25,10 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <map>
+#include <mutex>
+#include <tuple>
+
 #include "smol_device.h"
 
 namespace smol {
@@ -773,28 +777,49 @@ int launch_rgb_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, void *str
     return (int)hipLaunchKernel(rows_kernel(a, out_f16), grid, block, args, lds_bytes * a.wpg, s);
 }
 
+// Resident workgroups per compute unit of a kernel at a block size and LDS
+// size, queried once per device and remembered (the query costs more than
+// the rest of a call's host work).
+static int occupancy(const void *fn, int block, size_t lds, int *blocks_per_cu)
+{
+    static std::mutex mu;
+    static std::map<std::tuple<int, const void *, int, size_t>, int> cache;
+    int device = 0;
+    hipError_t e = hipGetDevice(&device);
+    if (e != hipSuccess)
+        return (int)e;
+    const auto key = std::make_tuple(device, fn, block, lds);
+    {
+        std::lock_guard<std::mutex> lk(mu);
+        const auto it = cache.find(key);
+        if (it != cache.end()) {
+            *blocks_per_cu = it->second;
+            return (int)hipSuccess;
+        }
+    }
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, fn, block, lds);
+    if (e == hipSuccess) {
+        std::lock_guard<std::mutex> lk(mu);
+        cache[key] = *blocks_per_cu;
+    }
+    return (int)e;
+}
+
 int occupancy_rgb_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, int *blocks_per_cu)
 {
-    return (int)hipOccupancyMaxActiveBlocksPerMultiprocessor(
-        blocks_per_cu, rows_kernel(a, out_f16), 64 * a.wpg, lds_bytes * a.wpg);
+    return occupancy(rows_kernel(a, out_f16), 64 * a.wpg, lds_bytes * a.wpg, blocks_per_cu);
 }
 
 int occupancy_rgb_gather(int out_f16, size_t lds_bytes, int *blocks_per_cu)
 {
-    hipError_t e = out_f16 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                                 blocks_per_cu, rgb_gather_kernel<1>, kThreads, lds_bytes)
-                           : hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                                 blocks_per_cu, rgb_gather_kernel<0>, kThreads, lds_bytes);
-    return (int)e;
+    return occupancy(out_f16 ? (const void *)rgb_gather_kernel<1> : (const void *)rgb_gather_kernel<0>,
+                     kThreads, lds_bytes, blocks_per_cu);
 }
 
 int occupancy_rgb_lds(int out_f16, size_t lds_bytes, int *blocks_per_cu)
 {
-    hipError_t e = out_f16 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                                 blocks_per_cu, rgb_lds_kernel<1>, kThreads, lds_bytes)
-                           : hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                                 blocks_per_cu, rgb_lds_kernel<0>, kThreads, lds_bytes);
-    return (int)e;
+    return occupancy(out_f16 ? (const void *)rgb_lds_kernel<1> : (const void *)rgb_lds_kernel<0>,
+                     kThreads, lds_bytes, blocks_per_cu);
 }
 
 int launch_yuv_direct(const BatchArgs &a, int out_f16, void *stream)
@@ -825,8 +850,8 @@ int launch_yuv_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, void *str
 
 int occupancy_yuv_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, int *blocks_per_cu)
 {
-    return (int)hipOccupancyMaxActiveBlocksPerMultiprocessor(
-        blocks_per_cu, yuv_rows_kernel_for(a, out_f16), 64 * a.wpg, lds_bytes * a.wpg);
+    return occupancy(yuv_rows_kernel_for(a, out_f16), 64 * a.wpg, lds_bytes * a.wpg,
+                     blocks_per_cu);
 }
 
 }  // namespace smol
