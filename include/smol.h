@@ -168,7 +168,7 @@ int smol_image_geometry(int32_t width, int32_t height, int32_t yuv420, const smo
 /* ------------------------------------------------------------------------
  * Variants: region of interest, direct resize, channels-last, chroma siting.
  *
- * Section 5.3 ("Leveraging partial decoding") lets a caller give an ROI per
+ * Section 6.4 ("Leveraging partial decoding") lets a caller give an ROI per
  * image (a face, a detection box, the central crop) so that only the ROI is
  * processed, and notes that networks take fixed input sizes (224 x 224 for
  * ResNet-50). Semantics:
@@ -208,7 +208,7 @@ typedef struct smol_options {
 /* smol_preprocess_batch_ex -- smol_preprocess_batch with an ROI per image
  * and options.
  *
- * Section 2 steps 2-4 on the ROI (section 5.3), fused per section 6.2.
+ * Section 2 steps 2-4 on the ROI (section 6.4), fused per section 6.2.
  *
  *   rois   HOST [n][4] int32: x, y, w, h of image i's ROI, or NULL for whole
  *          images.
@@ -227,7 +227,7 @@ int smol_preprocess_batch_ex(const uint8_t *src, int64_t src_bytes, const int64_
  * ROI per frame (luma pixels) and options.
  *
  * App. A "Components" (colorspace conversion, chroma sited per
- * opts->chroma_siting), then section 2 steps 2-4 on the ROI (section 5.3).
+ * opts->chroma_siting), then section 2 steps 2-4 on the ROI (section 6.4).
  * Arguments as for smol_yuv420_preprocess_batch, plus rois and opts as for
  * smol_preprocess_batch_ex. Returns as smol_preprocess_batch. */
 int smol_yuv420_preprocess_batch_ex(const uint8_t *src, int64_t src_bytes,

@@ -9,7 +9,8 @@ What is computed, and which passage each step follows, is documented at the top
 of ``smol_oracle.c``: the standard ResNet preprocessing of the paper's section 2
 ("Breakdown of end-to-end DNN inference", steps 2-4), the crop taken in output
 space (section 6.2, reordering rule 3) at Algorithm 1's offsets, and the
-colorspace conversion listed in App. A ("Components").
+colorspace conversion listed in App. A ("Components"); and the variants and
+the low-resolution augmentation (section 5.3) described there too.
 """
 from __future__ import annotations
 
@@ -25,6 +26,7 @@ _LIB_PATH = os.path.join(_HERE, "libsmol_oracle.so")
 
 OUT_F32 = 0
 OUT_F16 = 1
+OUT_U8 = 2
 RESIZE_SHORT_CROP = 0
 RESIZE_DIRECT = 1
 NCHW = 0
@@ -138,6 +140,16 @@ def _load():
     lib.smol_ref_yuv420_preprocess_image_ex.argtypes = [P, P, P] + [I32] * 11 + [P, P, I32, I32,
                                                                                    I32, I32, P]
     lib.smol_ref_yuv420_preprocess_image_ex.restype = ctypes.c_int
+    lib.smol_ref_lowres_preprocess_batch.argtypes = [P, I64, P, P, P, P] + [I32] * 5 + [P, P, I32,
+                                                                                        P]
+    lib.smol_ref_lowres_preprocess_batch.restype = ctypes.c_int
+    lib.smol_ref_yuv420_lowres_preprocess_batch.argtypes = [P, I64, P, P, P, P, P] + [I32] * 5 + [
+        P, P, I32, P]
+    lib.smol_ref_yuv420_lowres_preprocess_batch.restype = ctypes.c_int
+    lib.smol_ref_lowres_preprocess_image.argtypes = [P] + [I32] * 7 + [P, P, I32, P]
+    lib.smol_ref_lowres_preprocess_image.restype = ctypes.c_int
+    lib.smol_ref_yuv420_lowres_preprocess_image.argtypes = [P, P, P] + [I32] * 6 + [P, P, I32, P]
+    lib.smol_ref_yuv420_lowres_preprocess_image.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -207,6 +219,9 @@ def _out_array(n: int, Ch: int, Cw: int, out_dtype: int) -> np.ndarray:
 
 def _finish(out: np.ndarray, out_dtype: int) -> np.ndarray:
     return out.view(np.float16) if out_dtype == OUT_F16 else out
+
+
+_ELEM = {OUT_F32: np.float32, OUT_F16: np.uint16, OUT_U8: np.uint8}
 
 
 def _vec3(v) -> np.ndarray:
@@ -318,11 +333,9 @@ def yuv420_to_rgb_sited(y: np.ndarray, cb: np.ndarray, cr: np.ndarray,
 
 def _out_array_ex(n: int, Ch: int, Cw: int, out_dtype: int, layout: int) -> np.ndarray:
     shape = (n, Ch, Cw, 3) if layout == NHWC else (n, 3, Ch, Cw)
-    if out_dtype == OUT_F32:
-        return np.empty(shape, np.float32)
-    if out_dtype == OUT_F16:
-        return np.empty(shape, np.uint16)
-    raise ValueError("out_dtype must be OUT_F32 or OUT_F16")
+    if out_dtype not in _ELEM:
+        raise ValueError("out_dtype must be OUT_F32, OUT_F16 or OUT_U8")
+    return np.empty(shape, _ELEM[out_dtype])
 
 
 def _rois(rois, n: int):
@@ -400,3 +413,68 @@ def yuv420_preprocess_image_ex_into(y_ptr: int, cb_ptr: int, cr_ptr: int, W: int
                                                        S, Ch, Cw, mean.ctypes.data,
                                                        std.ctypes.data, out_dtype, resize_mode,
                                                        layout, siting, out_ptr)
+
+
+# --------------------------------------------------------------------------
+# low-resolution-aware augmentation (section 5.3)
+# --------------------------------------------------------------------------
+
+
+def lowres_preprocess_batch(src: np.ndarray, offsets, widths, heights, pitches, r: int, S: int,
+                            Ch: int, Cw: int, mean, std, out_dtype: int) -> np.ndarray:
+    """RGB batch: each image reduced to the r x r uint8 image, then steps 2-4."""
+    src = np.ascontiguousarray(src, np.uint8).reshape(-1)
+    n = len(offsets)
+    off = np.ascontiguousarray(offsets, np.int64)
+    w = np.ascontiguousarray(widths, np.int32)
+    h = np.ascontiguousarray(heights, np.int32)
+    p = None if pitches is None else np.ascontiguousarray(pitches, np.int32)
+    m, s = _vec3(mean), _vec3(std)
+    out = _out_array(n, Ch, Cw, out_dtype)
+    rc = _load().smol_ref_lowres_preprocess_batch(
+        src.ctypes.data, src.size, off.ctypes.data, w.ctypes.data, h.ctypes.data,
+        None if p is None else p.ctypes.data, n, r, S, Ch, Cw, m.ctypes.data, s.ctypes.data,
+        out_dtype, out.ctypes.data)
+    if rc != 0:
+        raise ValueError("oracle rejected the arguments")
+    return _finish(out, out_dtype)
+
+
+def yuv420_lowres_preprocess_batch(src: np.ndarray, y_offsets, cb_offsets, cr_offsets, widths,
+                                   heights, r: int, S: int, Ch: int, Cw: int, mean, std,
+                                   out_dtype: int) -> np.ndarray:
+    """I420 batch: each frame converted and reduced to the r x r uint8 RGB
+    image, then steps 2-4."""
+    src = np.ascontiguousarray(src, np.uint8).reshape(-1)
+    n = len(y_offsets)
+    yo = np.ascontiguousarray(y_offsets, np.int64)
+    bo = np.ascontiguousarray(cb_offsets, np.int64)
+    ro = np.ascontiguousarray(cr_offsets, np.int64)
+    w = np.ascontiguousarray(widths, np.int32)
+    h = np.ascontiguousarray(heights, np.int32)
+    m, s = _vec3(mean), _vec3(std)
+    out = _out_array(n, Ch, Cw, out_dtype)
+    rc = _load().smol_ref_yuv420_lowres_preprocess_batch(
+        src.ctypes.data, src.size, yo.ctypes.data, bo.ctypes.data, ro.ctypes.data, w.ctypes.data,
+        h.ctypes.data, n, r, S, Ch, Cw, m.ctypes.data, s.ctypes.data, out_dtype, out.ctypes.data)
+    if rc != 0:
+        raise ValueError("oracle rejected the arguments")
+    return _finish(out, out_dtype)
+
+
+def lowres_preprocess_image_into(img_ptr: int, W: int, H: int, pitch: int, r: int, S: int,
+                                 Ch: int, Cw: int, mean: np.ndarray, std: np.ndarray,
+                                 out_dtype: int, out_ptr: int) -> int:
+    """Raw-pointer form of one RGB image (the threaded CPU baseline)."""
+    return _load().smol_ref_lowres_preprocess_image(img_ptr, W, H, pitch, r, S, Ch, Cw,
+                                                    mean.ctypes.data, std.ctypes.data, out_dtype,
+                                                    out_ptr)
+
+
+def yuv420_lowres_preprocess_image_into(y_ptr: int, cb_ptr: int, cr_ptr: int, W: int, H: int,
+                                        r: int, S: int, Ch: int, Cw: int, mean: np.ndarray,
+                                        std: np.ndarray, out_dtype: int, out_ptr: int) -> int:
+    """Raw-pointer form of one I420 frame."""
+    return _load().smol_ref_yuv420_lowres_preprocess_image(y_ptr, cb_ptr, cr_ptr, W, H, r, S, Ch,
+                                                           Cw, mean.ctypes.data, std.ctypes.data,
+                                                           out_dtype, out_ptr)

@@ -45,7 +45,7 @@
  * Variants (the "_ex" calls), each a reading of a passage the paper leaves
  * open:
  *   - region of interest: the paper's partial-decoding discussion (section
- *     5.3, "Leveraging partial decoding") lets a caller pass an ROI per image,
+ *     6.4, "Leveraging partial decoding") lets a caller pass an ROI per image,
  *     e.g. a face or detection crop, and only the ROI is processed. The ROI
  *     (x, y, w, h) is cut out of the decoded image first and then treated as
  *     a w x h image: the resize taps clamp at the ROI's edges. For I420 the
@@ -57,13 +57,22 @@
  *   - channels-last (NHWC) output instead of step 4's channels-first;
  *   - left (co-sited) 4:2:0 chroma, as MPEG-2 / H.264 decoders emit: the
  *     chroma sample of luma column x sits at x/2 (rows stay centred).
+ *
+ * Low-resolution-aware augmentation (section 5.3, "Training DNNs for
+ * Low-resolution Visual Data"): at training time the full-resolution input is
+ * downsampled to the target resolution r and upsampled back to the network's
+ * input size. Readings: the low-resolution image is what a stored
+ * low-resolution copy would hold -- the standard step 2 geometry with S = r
+ * and an r x r central crop, each resized value rounded to the nearest
+ * integer (ties to even) as uint8 ("uint8 output", no normalisation) -- and
+ * that r x r image then goes through steps 2-4 like any other image.
  */
 #include <math.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
 
-enum { ORACLE_OUT_F32 = 0, ORACLE_OUT_F16 = 1 };
+enum { ORACLE_OUT_F32 = 0, ORACLE_OUT_F16 = 1, ORACLE_OUT_U8 = 2 };
 enum { ORACLE_RESIZE_SHORT_CROP = 0, ORACLE_RESIZE_DIRECT = 1 };
 enum { ORACLE_NCHW = 0, ORACLE_NHWC = 1 };
 enum { ORACLE_CHROMA_CENTER = 0, ORACLE_CHROMA_LEFT = 1 };
@@ -290,8 +299,21 @@ void oracle_output_geometry(int64_t W, int64_t H, int64_t S, int64_t Ch, int64_t
     oracle_crop_offsets(*Wr, *Hr, Ch, Cw, left, top);
 }
 
+/* A resized value v (in [0, 255]) as uint8: the nearest integer, ties to
+ * even. v - floor(v) is exact in fp32, so the comparison with 1/2 decides. */
+static uint8_t round_u8(float v)
+{
+    float f = floorf(v);
+    float d = v - f;
+    int64_t k = (int64_t)f;
+    if (d > 0.5f || (d == 0.5f && (k & 1)))
+        ++k;
+    return (uint8_t)(k < 0 ? 0 : k > 255 ? 255 : k);
+}
+
 /* rgb: fp32 image, W x H x 3 interleaved (rows `rstride` floats apart).
- * out: 3 x Ch x Cw (NCHW) or Ch x Cw x 3 (NHWC) of the out dtype. */
+ * out: 3 x Ch x Cw (NCHW) or Ch x Cw x 3 (NHWC) of the out dtype; uint8
+ * output holds the resized values rounded, not normalised. */
 static void resample_crop_normalize(const float *rgb, int64_t rstride, int64_t W, int64_t H,
                                     int64_t S, int64_t Ch, int64_t Cw, const float *mean,
                                     const float *stdv, int out_dtype, int32_t resize_mode,
@@ -315,9 +337,13 @@ static void resample_crop_normalize(const float *rgb, int64_t rstride, int64_t W
                 float t = p00 + wx * (p01 - p00);
                 float b = p10 + wx * (p11 - p10);
                 float v = t + wy * (b - t);
-                float o = (v - mean[c]) / stdv[c];
                 int64_t idx = layout == ORACLE_NHWC ? (yc * Cw + xc) * 3 + c
                                                     : ((int64_t)c * Ch + yc) * Cw + xc;
+                if (out_dtype == ORACLE_OUT_U8) {
+                    ((uint8_t *)out)[idx] = round_u8(v);
+                    continue;
+                }
+                float o = (v - mean[c]) / stdv[c];
                 if (out_dtype == ORACLE_OUT_F32)
                     ((float *)out)[idx] = o;
                 else
@@ -332,7 +358,7 @@ static int params_ok_ex(int64_t W, int64_t H, int32_t S, int32_t Ch, int32_t Cw,
 {
     if (W < 1 || H < 1 || S < 1 || Ch < 1 || Cw < 1)
         return 0;
-    if (out_dtype != ORACLE_OUT_F32 && out_dtype != ORACLE_OUT_F16)
+    if (out_dtype != ORACLE_OUT_F32 && out_dtype != ORACLE_OUT_F16 && out_dtype != ORACLE_OUT_U8)
         return 0;
     if ((resize_mode != ORACLE_RESIZE_SHORT_CROP && resize_mode != ORACLE_RESIZE_DIRECT) ||
         (layout != ORACLE_NCHW && layout != ORACLE_NHWC))
@@ -422,7 +448,8 @@ int smol_ref_yuv420_preprocess_image(const uint8_t *yp, const uint8_t *cbp, cons
 
 static size_t out_image_bytes(int32_t Ch, int32_t Cw, int32_t out_dtype)
 {
-    return (size_t)3 * (size_t)Ch * (size_t)Cw * (out_dtype == ORACLE_OUT_F32 ? 4u : 2u);
+    return (size_t)3 * (size_t)Ch * (size_t)Cw *
+           (out_dtype == ORACLE_OUT_F32 ? 4u : out_dtype == ORACLE_OUT_F16 ? 2u : 1u);
 }
 
 /* Batch of packed HWC RGB images with an optional ROI table (rois: n x
@@ -524,6 +551,100 @@ int smol_ref_yuv420_preprocess_batch(const uint8_t *src, int64_t src_bytes,
                                                   src + cr_offsets[i], widths[i], heights[i], S,
                                                   Ch, Cw, mean, stdv, out_dtype,
                                                   (uint8_t *)out + ob * i);
+        if (rc)
+            return rc;
+    }
+    return ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Low-resolution-aware augmentation (section 5.3)                           */
+/* ------------------------------------------------------------------------- */
+
+/* One packed HWC RGB image: reduced to the r x r uint8 image (short side r,
+ * central r x r crop, rounded), which then goes through steps 2-4. */
+int smol_ref_lowres_preprocess_image(const uint8_t *img, int32_t W, int32_t H, int32_t pitch,
+                                     int32_t r, int32_t S, int32_t Ch, int32_t Cw,
+                                     const float *mean, const float *stdv, int32_t out_dtype,
+                                     void *out)
+{
+    if (r < 1 || out_dtype == ORACLE_OUT_U8)
+        return ORACLE_ERR;
+    uint8_t *low = (uint8_t *)malloc((size_t)r * (size_t)r * 3);
+    if (!low)
+        return ORACLE_ERR;
+    int rc = smol_ref_preprocess_image_ex(img, W, H, pitch, 0, 0, W, H, r, r, r, mean, stdv,
+                                          ORACLE_OUT_U8, ORACLE_RESIZE_SHORT_CROP, ORACLE_NHWC,
+                                          low);
+    if (rc == ORACLE_OK)
+        rc = smol_ref_preprocess_image(low, r, r, 3 * r, S, Ch, Cw, mean, stdv, out_dtype, out);
+    free(low);
+    return rc;
+}
+
+/* One planar I420 frame: converted (centred chroma) and reduced to the r x r
+ * uint8 RGB image, which then goes through steps 2-4. */
+int smol_ref_yuv420_lowres_preprocess_image(const uint8_t *yp, const uint8_t *cbp,
+                                            const uint8_t *crp, int32_t W, int32_t H, int32_t r,
+                                            int32_t S, int32_t Ch, int32_t Cw, const float *mean,
+                                            const float *stdv, int32_t out_dtype, void *out)
+{
+    if (r < 1 || out_dtype == ORACLE_OUT_U8)
+        return ORACLE_ERR;
+    uint8_t *low = (uint8_t *)malloc((size_t)r * (size_t)r * 3);
+    if (!low)
+        return ORACLE_ERR;
+    int rc = smol_ref_yuv420_preprocess_image_ex(yp, cbp, crp, W, H, 0, 0, W, H, r, r, r, mean,
+                                                 stdv, ORACLE_OUT_U8, ORACLE_RESIZE_SHORT_CROP,
+                                                 ORACLE_NHWC, ORACLE_CHROMA_CENTER, low);
+    if (rc == ORACLE_OK)
+        rc = smol_ref_preprocess_image(low, r, r, 3 * r, S, Ch, Cw, mean, stdv, out_dtype, out);
+    free(low);
+    return rc;
+}
+
+/* Batch forms (tables as in smol_ref_preprocess_batch and
+ * smol_ref_yuv420_preprocess_batch). */
+int smol_ref_lowres_preprocess_batch(const uint8_t *src, int64_t src_bytes,
+                                     const int64_t *offsets, const int32_t *widths,
+                                     const int32_t *heights, const int32_t *pitches, int32_t n,
+                                     int32_t r, int32_t S, int32_t Ch, int32_t Cw,
+                                     const float *mean, const float *stdv, int32_t out_dtype,
+                                     void *out)
+{
+    size_t ob = out_image_bytes(Ch, Cw, out_dtype);
+    for (int32_t i = 0; i < n; ++i) {
+        int32_t pitch = pitches ? pitches[i] : 3 * widths[i];
+        int64_t end = offsets[i] + (int64_t)(heights[i] - 1) * pitch + 3 * (int64_t)widths[i];
+        if (offsets[i] < 0 || end > src_bytes)
+            return ORACLE_ERR;
+        int rc = smol_ref_lowres_preprocess_image(src + offsets[i], widths[i], heights[i], pitch,
+                                                  r, S, Ch, Cw, mean, stdv, out_dtype,
+                                                  (uint8_t *)out + ob * i);
+        if (rc)
+            return rc;
+    }
+    return ORACLE_OK;
+}
+
+int smol_ref_yuv420_lowres_preprocess_batch(const uint8_t *src, int64_t src_bytes,
+                                            const int64_t *y_offsets, const int64_t *cb_offsets,
+                                            const int64_t *cr_offsets, const int32_t *widths,
+                                            const int32_t *heights, int32_t n, int32_t r,
+                                            int32_t S, int32_t Ch, int32_t Cw, const float *mean,
+                                            const float *stdv, int32_t out_dtype, void *out)
+{
+    size_t ob = out_image_bytes(Ch, Cw, out_dtype);
+    for (int32_t i = 0; i < n; ++i) {
+        int64_t W = widths[i], H = heights[i];
+        int64_t Wc = (W + 1) / 2, Hc = (H + 1) / 2;
+        if (y_offsets[i] < 0 || y_offsets[i] + W * H > src_bytes || cb_offsets[i] < 0 ||
+            cb_offsets[i] + Wc * Hc > src_bytes || cr_offsets[i] < 0 ||
+            cr_offsets[i] + Wc * Hc > src_bytes)
+            return ORACLE_ERR;
+        int rc = smol_ref_yuv420_lowres_preprocess_image(
+            src + y_offsets[i], src + cb_offsets[i], src + cr_offsets[i], widths[i], heights[i],
+            r, S, Ch, Cw, mean, stdv, out_dtype, (uint8_t *)out + ob * i);
         if (rc)
             return rc;
     }

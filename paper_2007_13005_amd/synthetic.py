@@ -20,7 +20,7 @@ five seeded stand-ins reproduce their shapes, size mix and value ranges:
       short side 256, crop 224, fp16 out
   c6  256 regions of interest (64..512 px boxes) in 16 1080p RGB frames,
       resized directly to 112x112, channels-last fp16 (detection / face crops,
-      the ROI use of section 5.3)
+      the ROI use of section 6.4)
 
 Config k draws from ``numpy.random.default_rng(13005 + k)`` (PCG64).
 The normalisation constants are the ImageNet per-channel statistics the
