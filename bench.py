@@ -10,7 +10,9 @@ Input/output sets are rotated so that the touched working set exceeds twice
 the 256 MB Infinity Cache: the number reported is an HBM number, not a
 cache-warm one.
 
-Prints one JSON line. ``--config c1..c5`` selects another workload.
+Prints one JSON line. ``--config c1..c7`` selects another workload (c7, the
+low-resolution augmentation, is two launches per step: the roofline figure
+then covers both).
 """
 from __future__ import annotations
 
@@ -35,7 +37,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=400)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--config", default="c4", choices=["c1", "c2", "c3", "c4", "c5", "c6"])
+    ap.add_argument("--config", default="c4", choices=["c1", "c2", "c3", "c4", "c5", "c6", "c7"])
     ap.add_argument("--rotate", type=int, default=0,
                     help="input/output sets cycled through (0: enough to defeat the MALL)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
@@ -54,10 +56,43 @@ def parse():
     return ap.parse_args()
 
 
+def _read_bytes(g: dict, kind: str) -> int:
+    span = g["src_x_last"] - g["src_x_first"] + 1
+    if kind == "rgb":
+        return g["src_rows"] * span * 3
+    cspan = g["chroma_x_last"] - g["chroma_x_first"] + 1
+    return g["src_rows"] * span + 2 * g["chroma_rows"] * cspan
+
+
+def lowres_algorithmic_bytes(wl, smol) -> int:
+    """The augmentation's two launches: the reduction reads the source rows
+    and columns its taps touch and writes the r x r uint8 images; the second
+    launch reads what its taps touch of those and writes the output."""
+    r = wl.low_res
+    p1 = smol.make_params(r, r, r, wl.mean, wl.std, synthetic_u8())
+    p2 = smol.make_params(wl.resize_short, wl.crop_h, wl.crop_w, wl.mean, wl.std, wl.out_dtype)
+    total, cache = 0, {}
+    for w, h in zip(wl.widths.tolist(), wl.heights.tolist()):
+        if (w, h) not in cache:
+            cache[(w, h)] = _read_bytes(smol.image_geometry(w, h, p1, wl.kind == "yuv420"),
+                                        wl.kind)
+        total += cache[(w, h)]
+    step2 = _read_bytes(smol.image_geometry(r, r, p2), "rgb")
+    return (total + wl.n * 3 * r * r + wl.n * step2 +
+            wl.n * 3 * wl.crop_h * wl.crop_w * wl.out_elem_bytes)
+
+
+def synthetic_u8() -> int:
+    from paper_2007_13005_amd import synthetic
+    return synthetic.OUT_U8
+
+
 def algorithmic_bytes(wl, smol) -> int:
     """Bytes the method must move per batch: for every image the source rows
     its vertical taps read times the crop's source column span (per plane for
     I420), plus the output."""
+    if wl.low_res:
+        return lowres_algorithmic_bytes(wl, smol)
     p = smol.make_params(wl.resize_short, wl.crop_h, wl.crop_w, wl.mean, wl.std, wl.out_dtype)
     opts = smol.make_options(wl.resize_mode, wl.layout, wl.siting)
     rois = [None] * wl.n if wl.rois is None else [tuple(r) for r in wl.rois.tolist()]
@@ -68,13 +103,7 @@ def algorithmic_bytes(wl, smol) -> int:
         if key not in cache:
             g = smol.image_geometry_ex(w, h, p, yuv420=(wl.kind == "yuv420"), roi=roi,
                                        options=opts)
-            span = g["src_x_last"] - g["src_x_first"] + 1
-            if wl.kind == "rgb":
-                rd = g["src_rows"] * span * 3
-            else:
-                cspan = g["chroma_x_last"] - g["chroma_x_first"] + 1
-                rd = g["src_rows"] * span + 2 * g["chroma_rows"] * cspan
-            cache[key] = rd
+            cache[key] = _read_bytes(g, wl.kind)
         total += cache[key]
     return total + wl.n * 3 * wl.crop_h * wl.crop_w * wl.out_elem_bytes
 
@@ -100,7 +129,19 @@ def cpu_baseline(wl, seconds: float, threads: int) -> dict:
 
     def one(i: int, t: int) -> None:
         o = outs[t].ctypes.data
-        if wl.variant:
+        if wl.low_res:
+            W, H = int(wl.widths[i]), int(wl.heights[i])
+            if wl.kind == "rgb":
+                pitch = 3 * W if wl.pitches is None else int(wl.pitches[i])
+                rc = oracle.lowres_preprocess_image_into(base + int(wl.offsets[i]), W, H, pitch,
+                                                         wl.low_res, wl.resize_short, wl.crop_h,
+                                                         wl.crop_w, mean, std, wl.out_dtype, o)
+            else:
+                rc = oracle.yuv420_lowres_preprocess_image_into(
+                    base + int(wl.y_offsets[i]), base + int(wl.cb_offsets[i]),
+                    base + int(wl.cr_offsets[i]), W, H, wl.low_res, wl.resize_short, wl.crop_h,
+                    wl.crop_w, mean, std, wl.out_dtype, o)
+        elif wl.variant:
             W, H = int(wl.widths[i]), int(wl.heights[i])
             roi = (0, 0, W, H) if wl.rois is None else tuple(int(v) for v in wl.rois[i])
             if wl.kind == "rgb":
@@ -255,7 +296,8 @@ def main() -> int:
 
     src0 = torch.from_numpy(wl.src).to(dev)
     srcs = [src0] + [src0.clone() for _ in range(rotate - 1)]
-    odt = torch.float16 if wl.out_dtype == synthetic.OUT_F16 else torch.float32
+    odt = {synthetic.OUT_F16: torch.float16, synthetic.OUT_U8: torch.uint8}.get(wl.out_dtype,
+                                                                             torch.float32)
     outs = [torch.empty(wl.out_shape(), dtype=odt, device=dev) for _ in range(rotate)]
     call = smol.PreparedCall(wl)
     stream = torch.cuda.current_stream()
@@ -293,7 +335,7 @@ def main() -> int:
     achieved = per_launch_bytes / avg_launch_s / 1e9
 
     # sanity: the last output is finite
-    assert bool(torch.isfinite(outs[(args.steps - 1) % rotate]).all().item())
+    assert bool(torch.isfinite(outs[(args.steps - 1) % rotate].float()).all().item())
 
     # Labelled separately: the same launches on one input/output set, which
     # then stays resident in the 256 MB Infinity Cache (MALL) when it fits.
@@ -332,7 +374,7 @@ def main() -> int:
                    "algorithmic_bytes_per_step": algo, "output_bytes_per_step": out_bytes,
                    "rotation_sets": rotate, "kernel_path": plan["path"],
                    "band_rows": plan["band_rows"], "lds_bytes": plan["lds_bytes"],
-                   "grid": plan["grid"],
+                   "grid": plan["grid"], "launches_per_step": plan["launches"],
                    "gpu_ms_per_step": round(gpu_ms / args.steps, 5),
                    "gpu_us_per_step_median_of_5": round(median_us, 3),
                    "gpu_us_per_step_reps": [round(x, 3) for x in rep_us],

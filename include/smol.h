@@ -58,9 +58,14 @@ extern "C" {
                                   /* limits (see the per-call notes)          */
 #define SMOL_ERR_HIP (-3)         /* the HIP runtime reported an error        */
 
-/* Output element types. */
+/* Output element types. SMOL_OUT_U8 holds the resized value itself, rounded
+ * to the nearest integer with ties to even (no normalisation; mean and std
+ * are then not used). It runs on the direct kernels only: with it, a forced
+ * LDS-staged, register-gather or row-streaming path fails with
+ * SMOL_ERR_UNSUPPORTED. */
 #define SMOL_OUT_F32 0
 #define SMOL_OUT_F16 1
+#define SMOL_OUT_U8 2
 
 /* Limits. */
 #define SMOL_MAX_DIM 65535          /* max source width / height, luma pixels */
@@ -71,8 +76,9 @@ extern "C" {
  *   resize_short  S, the short side after the aspect-preserving resize (>= 1)
  *   crop_h/crop_w output height / width; the crop must fit inside the resized
  *                 image of every image in the batch
- *   out_dtype     SMOL_OUT_F32 or SMOL_OUT_F16
+ *   out_dtype     SMOL_OUT_F32, SMOL_OUT_F16 or SMOL_OUT_U8
  *   mean, std     per channel R, G, B in 0..255 pixel units; finite, std != 0
+ *                 (not used, and not checked, with SMOL_OUT_U8)
  *                 (the ImageNet statistics are (0.485, 0.456, 0.406) * 255 and
  *                 (0.229, 0.224, 0.225) * 255) */
 typedef struct smol_params {
@@ -236,6 +242,56 @@ int smol_yuv420_preprocess_batch_ex(const uint8_t *src, int64_t src_bytes,
                                     const int32_t *heights, const int32_t *rois, int32_t n,
                                     const smol_params *p, const smol_options *opts, void *out,
                                     void *stream);
+
+/* ------------------------------------------------------------------------
+ * Low-resolution-aware augmentation (section 5.3, "Training DNNs for
+ * Low-resolution Visual Data"): at training time an input is downsampled to
+ * the target resolution and upsampled back to the network's input size, so
+ * that the network learns the artifacts of stored low-resolution data (the
+ * section's example: 161 x 161 thumbnails upscaled to 224 x 224).
+ *
+ * Two launches of the resize kernels on `stream`:
+ *   1. each image (or I420 frame, centred chroma) is reduced to an r x r
+ *      uint8 RGB image -- short side resized to r, central r x r crop, values
+ *      rounded to nearest, ties to even (SMOL_OUT_U8, NHWC) -- packed in the
+ *      workspace, image i at byte i * 3 * r * r;
+ *   2. those n r x r images go through smol_preprocess_batch with p.
+ * ------------------------------------------------------------------------ */
+
+/* Bytes of workspace the augmentation needs: n * 3 * low_res^2 rounded up to
+ * a multiple of 16, plus 16 (0 for n < 1 or low_res < 1). */
+int64_t smol_lowres_workspace_bytes(int32_t n, int32_t low_res);
+
+/* smol_lowres_preprocess_batch -- RGB images reduced to low_res x low_res,
+ * then preprocessed.
+ *
+ *   low_res    r, 1 .. SMOL_MAX_DIM.
+ *   workspace  DEVICE pointer, caller-owned, 16-byte aligned, at least
+ *              smol_lowres_workspace_bytes(n, low_res) bytes; overlaps
+ *              neither src nor out. Holds the r x r images when the stream
+ *              reaches the second launch; the caller may reuse it once the
+ *              call's work on the stream is done.
+ *   p          parameters of the second step; p->out_dtype SMOL_OUT_F32 or
+ *              SMOL_OUT_F16 (SMOL_OUT_U8: SMOL_ERR_INVALID_ARG).
+ *   out        n x 3 x crop_h x crop_w elements, as for
+ *              smol_preprocess_batch.
+ *   Every other argument as for smol_preprocess_batch. Both steps are
+ *   validated before the first launch (the crop must fit the r x r image
+ *   resized to p->resize_short). Returns as smol_preprocess_batch. */
+int smol_lowres_preprocess_batch(const uint8_t *src, int64_t src_bytes, const int64_t *offsets,
+                                 const int32_t *widths, const int32_t *heights,
+                                 const int32_t *row_pitch, int32_t n, int32_t low_res,
+                                 const smol_params *p, void *workspace, int64_t workspace_bytes,
+                                 void *out, void *stream);
+
+/* smol_yuv420_lowres_preprocess_batch -- the same for I420 frames (tables as
+ * for smol_yuv420_preprocess_batch). */
+int smol_yuv420_lowres_preprocess_batch(const uint8_t *src, int64_t src_bytes,
+                                        const int64_t *y_offsets, const int64_t *cb_offsets,
+                                        const int64_t *cr_offsets, const int32_t *widths,
+                                        const int32_t *heights, int32_t n, int32_t low_res,
+                                        const smol_params *p, void *workspace,
+                                        int64_t workspace_bytes, void *out, void *stream);
 
 /* smol_image_geometry_ex -- smol_image_geometry of an ROI (HOST int32[4], or
  * NULL for the whole image) under opts (NULL: defaults). resized_w/h and

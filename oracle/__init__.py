@@ -135,10 +135,10 @@ def _load():
     lib.smol_ref_yuv420_preprocess_batch_ex.argtypes = [P, I64, P, P, P, P, P, P, I32, I32, I32,
                                                         I32, P, P, I32, I32, I32, I32, P]
     lib.smol_ref_yuv420_preprocess_batch_ex.restype = ctypes.c_int
-    lib.smol_ref_preprocess_image_ex.argtypes = [P] + [I32] * 11 + [P, P, I32, I32, I32, P]
+    lib.smol_ref_preprocess_image_ex.argtypes = [P] + [I32] * 10 + [P, P, I32, I32, I32, P]
     lib.smol_ref_preprocess_image_ex.restype = ctypes.c_int
-    lib.smol_ref_yuv420_preprocess_image_ex.argtypes = [P, P, P] + [I32] * 11 + [P, P, I32, I32,
-                                                                                   I32, I32, P]
+    lib.smol_ref_yuv420_preprocess_image_ex.argtypes = [P, P, P] + [I32] * 9 + [P, P, I32, I32,
+                                                                                  I32, I32, P]
     lib.smol_ref_yuv420_preprocess_image_ex.restype = ctypes.c_int
     lib.smol_ref_lowres_preprocess_batch.argtypes = [P, I64, P, P, P, P] + [I32] * 5 + [P, P, I32,
                                                                                         P]
@@ -210,11 +210,9 @@ def yuv420_to_rgb(y: np.ndarray, cb: np.ndarray, cr: np.ndarray) -> np.ndarray:
 
 
 def _out_array(n: int, Ch: int, Cw: int, out_dtype: int) -> np.ndarray:
-    if out_dtype == OUT_F32:
-        return np.empty((n, 3, Ch, Cw), np.float32)
-    if out_dtype == OUT_F16:
-        return np.empty((n, 3, Ch, Cw), np.uint16)
-    raise ValueError("out_dtype must be OUT_F32 or OUT_F16")
+    if out_dtype not in _ELEM:
+        raise ValueError("out_dtype must be OUT_F32, OUT_F16 or OUT_U8")
+    return np.empty((n, 3, Ch, Cw), _ELEM[out_dtype])
 
 
 def _finish(out: np.ndarray, out_dtype: int) -> np.ndarray:

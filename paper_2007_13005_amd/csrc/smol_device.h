@@ -162,6 +162,18 @@ __device__ __forceinline__ void store1(void *out, long long idx, float v)
         ((float *)out)[idx] = v;
 }
 
+// Output element for channel ch of resized value v: OUT 0 / 1 the normalised
+// value as fp32 / fp16; OUT 2 (uint8 output) v itself rounded to the nearest
+// integer, ties to even (v_rndne_f32), clamped to 0..255, not normalised.
+template <int OUT>
+__device__ __forceinline__ void emit1(const BatchArgs &a, long long idx, int ch, float v)
+{
+    if (OUT == 2)
+        ((uint8_t *)a.out)[idx] = (uint8_t)__builtin_rintf(clamp255(v));
+    else
+        store1<OUT>(a.out, idx, normalize(v, a.mean[ch], a.stdv[ch], a.rcp[ch]));
+}
+
 __device__ __forceinline__ void image_desc(const BatchArgs &a, int img, Desc &d)
 {
     if (a.table) {

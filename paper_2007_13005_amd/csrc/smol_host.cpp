@@ -149,8 +149,11 @@ int check_params(const smol_params *p)
         return fail(SMOL_ERR_INVALID_ARG, "resize_short %d out of range", p->resize_short);
     if (p->crop_h < 1 || p->crop_w < 1)
         return fail(SMOL_ERR_INVALID_ARG, "crop %dx%d must be positive", p->crop_h, p->crop_w);
-    if (p->out_dtype != SMOL_OUT_F32 && p->out_dtype != SMOL_OUT_F16)
+    if (p->out_dtype != SMOL_OUT_F32 && p->out_dtype != SMOL_OUT_F16 &&
+        p->out_dtype != SMOL_OUT_U8)
         return fail(SMOL_ERR_INVALID_ARG, "out_dtype %d unknown", p->out_dtype);
+    if (p->out_dtype == SMOL_OUT_U8)
+        return SMOL_OK;  // mean and std are not used
     for (int c = 0; c < 3; ++c) {
         if (!std::isfinite(p->mean[c]) || !std::isfinite(p->std[c]) || p->std[c] == 0.0f)
             return fail(SMOL_ERR_INVALID_ARG, "mean/std of channel %d not finite or std == 0", c);
@@ -734,6 +737,19 @@ static int rgb_batch(const uint8_t *src, int64_t src_bytes, const int64_t *offse
     auto direct = [f16](const BatchArgs &x, const Plan &, void *s) {
         return smol::launch_rgb_direct(x, f16, s);
     };
+    if (p->out_dtype == SMOL_OUT_U8) {
+        // uint8 output: the direct kernel only
+        if (forced != smol::PATH_AUTO && forced != smol::PATH_DIRECT)
+            return fail(SMOL_ERR_UNSUPPORTED, "uint8 output runs on the direct kernels only");
+        rc = run_batch(descs, 0, (size_t)n, 1, a, Plan{smol::PATH_DIRECT, 0, 0, 0, 0}, stream,
+                       [](const BatchArgs &x, const Plan &, void *s) {
+                           return smol::launch_rgb_direct(x, SMOL_OUT_U8, s);
+                       },
+                       &info);
+        if (!rc)
+            g_last_plan = info;
+        return rc;
+    }
     // Register-gather path: the gather kernel for runs of images whose windows
     // lie inside src, the direct kernel for the others.
     // Row-streaming path: the row-streaming kernel for runs of images whose
@@ -951,6 +967,18 @@ static int yuv_batch(const uint8_t *src, int64_t src_bytes, const int64_t *y_off
     auto direct = [f16](const BatchArgs &x, const Plan &, void *s) {
         return smol::launch_yuv_direct(x, f16, s);
     };
+    if (p->out_dtype == SMOL_OUT_U8) {
+        if (forced != smol::PATH_AUTO && forced != smol::PATH_DIRECT)
+            return fail(SMOL_ERR_UNSUPPORTED, "uint8 output runs on the direct kernels only");
+        rc = run_batch(descs, 0, (size_t)n, 3, a, Plan{smol::PATH_DIRECT, 0, 0, 0, 0}, stream,
+                       [](const BatchArgs &x, const Plan &, void *s) {
+                           return smol::launch_yuv_direct(x, SMOL_OUT_U8, s);
+                       },
+                       &info);
+        if (!rc)
+            g_last_plan = info;
+        return rc;
+    }
     // Row-streaming kernel: staged luma and chroma rows of at most 1 KiB
     // (span + 32 bytes), crops up to 512 columns; frames whose planes' chunks
     // cross an end of src go to the direct kernel.
@@ -1106,6 +1134,99 @@ int smol_yuv420_preprocess_batch_ex(const uint8_t *src, int64_t src_bytes,
 {
     return yuv_batch(src, src_bytes, y_offsets, cb_offsets, cr_offsets, widths, heights, rois, n,
                      p, opts, out, stream);
+}
+
+int64_t smol_lowres_workspace_bytes(int32_t n, int32_t low_res)
+{
+    if (n < 1 || low_res < 1)
+        return 0;
+    // the images, then 16-byte chunks past the last one so that the second
+    // step reads the last image like the others
+    return (((int64_t)n * 3 * low_res * low_res + 15) & ~(int64_t)15) + 16;
+}
+
+// Low-resolution augmentation, shared checks and the second step: the r x r
+// uint8 HWC images packed in the workspace, preprocessed as one uniform
+// batch.
+static int lowres_check(int32_t n, int32_t low_res, const smol_params *p, const void *workspace,
+                        int64_t workspace_bytes, smol_params *lo)
+{
+    g_last_error.clear();
+    int rc = check_params(p);
+    if (rc)
+        return rc;
+    if (p->out_dtype == SMOL_OUT_U8)
+        return fail(SMOL_ERR_INVALID_ARG, "the augmented output is normalised: out_dtype must be "
+                    "SMOL_OUT_F32 or SMOL_OUT_F16");
+    if (low_res < 1 || low_res > SMOL_MAX_DIM)
+        return fail(SMOL_ERR_INVALID_ARG, "low_res %d outside 1..%d", low_res, SMOL_MAX_DIM);
+    if (n < 0 || n > SMOL_MAX_BATCH)
+        return fail(SMOL_ERR_INVALID_ARG, "n = %d outside 0..%d", n, SMOL_MAX_BATCH);
+    const int64_t need = smol_lowres_workspace_bytes(n, low_res);
+    if (n > 0 && (!workspace || workspace_bytes < need))
+        return fail(SMOL_ERR_INVALID_ARG, "workspace of %lld bytes, %lld needed",
+                    (long long)workspace_bytes, (long long)need);
+    if (((uintptr_t)workspace & 15) != 0)
+        return fail(SMOL_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
+    Geo g;  // the second step's geometry, checked before the first launch
+    rc = image_geo(low_res, low_res, p, SMOL_RESIZE_SHORT_CROP, &g, 0);
+    if (rc)
+        return rc;
+    *lo = *p;
+    lo->resize_short = low_res;
+    lo->crop_h = lo->crop_w = low_res;
+    lo->out_dtype = SMOL_OUT_U8;
+    return SMOL_OK;
+}
+
+static int lowres_upsample(const void *workspace, int64_t workspace_bytes, int32_t n,
+                           int32_t low_res, const smol_params *p, void *out, void *stream)
+{
+    const int launches = g_last_plan.launches;
+    std::vector<int64_t> offs((size_t)n);
+    std::vector<int32_t> side((size_t)n, low_res);
+    const int64_t each = (int64_t)3 * low_res * low_res;
+    for (int32_t i = 0; i < n; ++i)
+        offs[(size_t)i] = (int64_t)i * each;
+    const int rc = rgb_batch((const uint8_t *)workspace, workspace_bytes, offs.data(),
+                             side.data(), side.data(), nullptr, nullptr, n, p, nullptr, out,
+                             stream);
+    if (!rc)
+        g_last_plan.launches += launches;
+    return rc;
+}
+
+int smol_lowres_preprocess_batch(const uint8_t *src, int64_t src_bytes, const int64_t *offsets,
+                                 const int32_t *widths, const int32_t *heights,
+                                 const int32_t *row_pitch, int32_t n, int32_t low_res,
+                                 const smol_params *p, void *workspace, int64_t workspace_bytes,
+                                 void *out, void *stream)
+{
+    smol_params lo;
+    int rc = lowres_check(n, low_res, p, workspace, workspace_bytes, &lo);
+    if (rc || n == 0)
+        return rc;
+    const smol_options o = {SMOL_RESIZE_SHORT_CROP, SMOL_LAYOUT_NHWC, SMOL_CHROMA_CENTER, {0}};
+    rc = rgb_batch(src, src_bytes, offsets, widths, heights, row_pitch, nullptr, n, &lo, &o,
+                   workspace, stream);
+    return rc ? rc : lowres_upsample(workspace, workspace_bytes, n, low_res, p, out, stream);
+}
+
+int smol_yuv420_lowres_preprocess_batch(const uint8_t *src, int64_t src_bytes,
+                                        const int64_t *y_offsets, const int64_t *cb_offsets,
+                                        const int64_t *cr_offsets, const int32_t *widths,
+                                        const int32_t *heights, int32_t n, int32_t low_res,
+                                        const smol_params *p, void *workspace,
+                                        int64_t workspace_bytes, void *out, void *stream)
+{
+    smol_params lo;
+    int rc = lowres_check(n, low_res, p, workspace, workspace_bytes, &lo);
+    if (rc || n == 0)
+        return rc;
+    const smol_options o = {SMOL_RESIZE_SHORT_CROP, SMOL_LAYOUT_NHWC, SMOL_CHROMA_CENTER, {0}};
+    rc = yuv_batch(src, src_bytes, y_offsets, cb_offsets, cr_offsets, widths, heights, nullptr, n,
+                   &lo, &o, workspace, stream);
+    return rc ? rc : lowres_upsample(workspace, workspace_bytes, n, low_res, p, out, stream);
 }
 
 int smol_set_tuning(const smol_tuning *t)

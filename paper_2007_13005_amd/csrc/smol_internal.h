@@ -72,7 +72,8 @@ constexpr int kRowsMaxGroups = 4;
 constexpr int kRowsMaxWavesPerGroup = 4;
 
 // Launchers (smol_kernels.hip). Return a hipError_t as int.
-int launch_rgb_direct(const BatchArgs &a, int out_f16, void *stream);
+// Direct kernels: out_type 0 fp32, 1 fp16, 2 uint8 (rounded, not normalised).
+int launch_rgb_direct(const BatchArgs &a, int out_type, void *stream);
 int launch_rgb_lds(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream);
 int launch_rgb_gather(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream);
 // Row-streaming launches: `lds_bytes` is one wave's slot; a workgroup holds
@@ -83,7 +84,7 @@ int occupancy_rgb_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, int *b
 // Resident workgroups per compute unit for the persistent kernels.
 int occupancy_rgb_gather(int out_f16, size_t lds_bytes, int *blocks_per_cu);
 int occupancy_rgb_lds(int out_f16, size_t lds_bytes, int *blocks_per_cu);
-int launch_yuv_direct(const BatchArgs &a, int out_f16, void *stream);
+int launch_yuv_direct(const BatchArgs &a, int out_type, void *stream);
 int launch_yuv_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream);
 int occupancy_yuv_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, int *blocks_per_cu);
 

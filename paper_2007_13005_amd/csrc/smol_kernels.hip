@@ -626,35 +626,38 @@ __global__ void __launch_bounds__(kThreads) rgb_gather_kernel(BatchArgs a)
 
 
 // ---------------------------------------------------------------------------
-// RGB, direct gather: one thread per output pixel, taps read from global
-// memory. Used when the crop's source span does not fit the LDS budget.
+// RGB, direct gather: a workgroup per output row (the image's descriptor and
+// the row's vertical taps once per row), a thread per output pixel, taps
+// read from global memory. Used for images whose staged rows would cross an
+// end of src, NHWC and uint8 outputs, and spans beyond the LDS budgets.
 // ---------------------------------------------------------------------------
-template <int F16>
+template <int OUT>
 __global__ void __launch_bounds__(kThreads) rgb_direct_kernel(BatchArgs a)
 {
     const long long plane = (long long)a.Ch * a.Cw;
-    const long long total = plane * a.n;
-    for (long long gid = (long long)blockIdx.x * kThreads + threadIdx.x; gid < total;
-         gid += (long long)gridDim.x * kThreads) {
-        const int img = (int)(gid / plane);
-        const long long pix = gid - (long long)img * plane;
-        const int yc = (int)(pix / a.Cw);
-        const int xc = (int)(pix - (long long)yc * a.Cw);
+    const long long rows = (long long)a.Ch * a.n;
+    for (long long row = blockIdx.x; row < rows; row += gridDim.x) {
+        const int img = (int)(row / a.Ch);
+        const int yc = (int)(row - (long long)img * a.Ch);
         Desc d;
         image_desc(a, img, d);
-        const Tap tx = axis_tap(d.left + xc, d.W, d.Wr);
         const Tap ty = axis_tap(d.top + yc, d.H, d.Hr);
         const uint8_t *r0 = a.src + d.off[0] + (long long)ty.x0 * d.pitch;
         const uint8_t *r1 = a.src + d.off[0] + (long long)ty.x1 * d.pitch;
-        // element of channel ch: NCHW base + ch * plane, NHWC base + ch
-        const long long base = (long long)(a.img_base + img) * 3 * plane + (a.nhwc ? 3 * pix : pix);
-        const long long cstep = a.nhwc ? 1 : plane;
+        const long long ibase = (long long)(a.img_base + img) * 3 * plane;
+        const long long pix0 = (long long)yc * a.Cw;  // first pixel of the row in the crop
+        for (int xc = threadIdx.x; xc < a.Cw; xc += blockDim.x) {
+            const Tap tx = axis_tap(d.left + xc, d.W, d.Wr);
+            // element of channel ch: NCHW base + ch * plane, NHWC base + ch
+            const long long base = ibase + (a.nhwc ? 3 * (pix0 + xc) : pix0 + xc);
+            const long long cstep = a.nhwc ? 1 : plane;
 #pragma unroll
-        for (int ch = 0; ch < 3; ++ch) {
-            const float p00 = r0[3 * tx.x0 + ch], p01 = r0[3 * tx.x1 + ch];
-            const float p10 = r1[3 * tx.x0 + ch], p11 = r1[3 * tx.x1 + ch];
-            const float v = lerp(lerp(p00, p01, tx.w), lerp(p10, p11, tx.w), ty.w);
-            store1<F16>(a.out, base + ch * cstep, normalize(v, a.mean[ch], a.stdv[ch], a.rcp[ch]));
+            for (int ch = 0; ch < 3; ++ch) {
+                const float p00 = r0[3 * tx.x0 + ch], p01 = r0[3 * tx.x1 + ch];
+                const float p10 = r1[3 * tx.x0 + ch], p11 = r1[3 * tx.x1 + ch];
+                const float v = lerp(lerp(p00, p01, tx.w), lerp(p10, p11, tx.w), ty.w);
+                emit1<OUT>(a, base + ch * cstep, ch, v);
+            }
         }
     }
 }
@@ -671,17 +674,14 @@ __device__ __forceinline__ float chroma_at(const uint8_t *pl, int Wc, const Tap 
     return lerp(t, b, cy.w);
 }
 
-template <int F16>
+template <int OUT>
 __global__ void __launch_bounds__(kThreads) yuv_direct_kernel(BatchArgs a)
 {
     const long long plane = (long long)a.Ch * a.Cw;
-    const long long total = plane * a.n;
-    for (long long gid = (long long)blockIdx.x * kThreads + threadIdx.x; gid < total;
-         gid += (long long)gridDim.x * kThreads) {
-        const int img = (int)(gid / plane);
-        const long long pix = gid - (long long)img * plane;
-        const int yc = (int)(pix / a.Cw);
-        const int xc = (int)(pix - (long long)yc * a.Cw);
+    const long long rows = (long long)a.Ch * a.n;
+    for (long long row = blockIdx.x; row < rows; row += gridDim.x) {
+        const int img = (int)(row / a.Ch);
+        const int yc = (int)(row - (long long)img * a.Ch);
         Desc d;
         image_desc(a, img, d);
         // the region (d.W x d.H at (rx, ry)) inside a frame of pitch x fh;
@@ -690,48 +690,62 @@ __global__ void __launch_bounds__(kThreads) yuv_direct_kernel(BatchArgs a)
         const uint8_t *yp = a.src + d.off[0] + (long long)d.ry * d.pitch + d.rx;
         const uint8_t *cbp = a.src + d.off[1];
         const uint8_t *crp = a.src + d.off[2];
-        const Tap tx = axis_tap(d.left + xc, d.W, d.Wr);
         const Tap ty = axis_tap(d.top + yc, d.H, d.Hr);
-        const int xx[2] = {tx.x0, tx.x1};
         const int yy[2] = {ty.x0, ty.x1};
-        float rgb[2][2][3];
+        const Tap cy[2] = {chroma_tap(d.ry + yy[0], Hc), chroma_tap(d.ry + yy[1], Hc)};
+        const long long ibase = (long long)(a.img_base + img) * 3 * plane;
+        const long long pix0 = (long long)yc * a.Cw;  // first pixel of the row in the crop
+        for (int xc = threadIdx.x; xc < a.Cw; xc += blockDim.x) {
+            const Tap tx = axis_tap(d.left + xc, d.W, d.Wr);
+            const int xx[2] = {tx.x0, tx.x1};
+            float rgb[2][2][3];
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const Tap cy = chroma_tap(d.ry + yy[i], Hc);
+            for (int i = 0; i < 2; ++i) {
 #pragma unroll
-            for (int k = 0; k < 2; ++k) {
-                const Tap cx = chroma_tap(d.rx + xx[k], Wc, a.siting);
-                const float Y = (float)yp[(long long)yy[i] * d.pitch + xx[k]];
-                ycbcr_to_rgb(Y, chroma_at(cbp, Wc, cx, cy), chroma_at(crp, Wc, cx, cy),
-                             rgb[i][k][0], rgb[i][k][1], rgb[i][k][2]);
+                for (int k = 0; k < 2; ++k) {
+                    const Tap cx = chroma_tap(d.rx + xx[k], Wc, a.siting);
+                    const float Y = (float)yp[(long long)yy[i] * d.pitch + xx[k]];
+                    ycbcr_to_rgb(Y, chroma_at(cbp, Wc, cx, cy[i]), chroma_at(crp, Wc, cx, cy[i]),
+                                 rgb[i][k][0], rgb[i][k][1], rgb[i][k][2]);
+                }
             }
-        }
-        const long long base = (long long)(a.img_base + img) * 3 * plane + (a.nhwc ? 3 * pix : pix);
-        const long long cstep = a.nhwc ? 1 : plane;
+            const long long base = ibase + (a.nhwc ? 3 * (pix0 + xc) : pix0 + xc);
+            const long long cstep = a.nhwc ? 1 : plane;
 #pragma unroll
-        for (int ch = 0; ch < 3; ++ch) {
-            const float v = lerp(lerp(rgb[0][0][ch], rgb[0][1][ch], tx.w),
-                                 lerp(rgb[1][0][ch], rgb[1][1][ch], tx.w), ty.w);
-            store1<F16>(a.out, base + ch * cstep, normalize(v, a.mean[ch], a.stdv[ch], a.rcp[ch]));
+            for (int ch = 0; ch < 3; ++ch) {
+                const float v = lerp(lerp(rgb[0][0][ch], rgb[0][1][ch], tx.w),
+                                     lerp(rgb[1][0][ch], rgb[1][1][ch], tx.w), ty.w);
+                emit1<OUT>(a, base + ch * cstep, ch, v);
+            }
         }
     }
 }
 
-unsigned direct_grid(const BatchArgs &a)
+// Direct kernels: a workgroup per output row, 64 to 256 threads (whole
+// waves covering the crop's width where it is narrower than 256), at most
+// 2^20 workgroups looping over the rows.
+dim3 direct_grid(const BatchArgs &a)
 {
-    const long long total = (long long)a.Ch * a.Cw * a.n;
-    long long blocks = (total + kThreads - 1) / kThreads;
+    const long long rows = (long long)a.Ch * a.n;
     const long long cap = 1 << 20;
-    return (unsigned)(blocks < cap ? blocks : cap);
+    return dim3((unsigned)(rows < cap ? rows : cap));
+}
+
+dim3 direct_block(const BatchArgs &a)
+{
+    const int waves = (a.Cw + 63) / 64;
+    return dim3(64 * (waves < kThreads / 64 ? waves : kThreads / 64));
 }
 
 }  // namespace
 
-int launch_rgb_direct(const BatchArgs &a, int out_f16, void *stream)
+int launch_rgb_direct(const BatchArgs &a, int out_type, void *stream)
 {
     hipStream_t s = (hipStream_t)stream;
-    const dim3 grid(direct_grid(a)), block(kThreads);
-    if (out_f16)
+    const dim3 grid = direct_grid(a), block = direct_block(a);
+    if (out_type == 2)
+        hipLaunchKernelGGL(rgb_direct_kernel<2>, grid, block, 0, s, a);
+    else if (out_type == 1)
         hipLaunchKernelGGL(rgb_direct_kernel<1>, grid, block, 0, s, a);
     else
         hipLaunchKernelGGL(rgb_direct_kernel<0>, grid, block, 0, s, a);
@@ -822,11 +836,13 @@ int occupancy_rgb_lds(int out_f16, size_t lds_bytes, int *blocks_per_cu)
                      kThreads, lds_bytes, blocks_per_cu);
 }
 
-int launch_yuv_direct(const BatchArgs &a, int out_f16, void *stream)
+int launch_yuv_direct(const BatchArgs &a, int out_type, void *stream)
 {
     hipStream_t s = (hipStream_t)stream;
-    const dim3 grid(direct_grid(a)), block(kThreads);
-    if (out_f16)
+    const dim3 grid = direct_grid(a), block = direct_block(a);
+    if (out_type == 2)
+        hipLaunchKernelGGL(yuv_direct_kernel<2>, grid, block, 0, s, a);
+    else if (out_type == 1)
         hipLaunchKernelGGL(yuv_direct_kernel<1>, grid, block, 0, s, a);
     else
         hipLaunchKernelGGL(yuv_direct_kernel<0>, grid, block, 0, s, a);

@@ -22,6 +22,7 @@ ERR_HIP = -3
 
 OUT_F32 = 0
 OUT_F16 = 1
+OUT_U8 = 2
 
 PATH_AUTO = 0
 PATH_DIRECT = 1
@@ -98,6 +99,15 @@ SIGNATURES = {
     "smol_image_geometry_ex": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _vp,
                                               ctypes.POINTER(Params), ctypes.POINTER(Options),
                                               ctypes.POINTER(Geometry)]),
+    "smol_lowres_workspace_bytes": (ctypes.c_int64, [ctypes.c_int32, ctypes.c_int32]),
+    "smol_lowres_preprocess_batch": (ctypes.c_int, [_vp, ctypes.c_int64, _vp, _vp, _vp, _vp,
+                                                    ctypes.c_int32, ctypes.c_int32,
+                                                    ctypes.POINTER(Params), _vp, ctypes.c_int64,
+                                                    _vp, _vp]),
+    "smol_yuv420_lowres_preprocess_batch": (ctypes.c_int, [_vp, ctypes.c_int64, _vp, _vp, _vp,
+                                                           _vp, _vp, ctypes.c_int32,
+                                                           ctypes.c_int32, ctypes.POINTER(Params),
+                                                           _vp, ctypes.c_int64, _vp, _vp]),
     "smol_set_tuning": (ctypes.c_int, [ctypes.POINTER(Tuning)]),
     "smol_last_plan": (ctypes.c_int, [ctypes.POINTER(Plan)]),
     "smol_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -225,7 +235,7 @@ def _stream_handle(stream) -> int | None:
 
 def _out_tensor(out, n: int, params: Params, device, layout: int = LAYOUT_NCHW):
     import torch
-    dtype = torch.float16 if params.out_dtype == OUT_F16 else torch.float32
+    dtype = {OUT_F16: torch.float16, OUT_U8: torch.uint8}.get(params.out_dtype, torch.float32)
     shape = ((n, params.crop_h, params.crop_w, 3) if layout == LAYOUT_NHWC
              else (n, 3, params.crop_h, params.crop_w))
     if out is None:
@@ -310,6 +320,67 @@ def yuv420_preprocess_batch(src, y_offsets, cb_offsets, cr_offsets, widths, heig
     return out
 
 
+def lowres_workspace_bytes(n: int, low_res: int) -> int:
+    return int(lib().smol_lowres_workspace_bytes(n, low_res))
+
+
+def _workspace(workspace, n: int, low_res: int, device):
+    import torch
+    need = lowres_workspace_bytes(n, low_res)
+    if workspace is None:
+        return torch.empty(max(need, 16), dtype=torch.uint8, device=device)
+    if workspace.dtype != torch.uint8 or not workspace.is_contiguous() or workspace.numel() < need:
+        raise ValueError(f"workspace must be a contiguous uint8 tensor of >= {need} bytes")
+    return workspace
+
+
+def lowres_preprocess_batch(src, offsets, widths, heights, params: Params, low_res: int,
+                            pitches=None, out=None, workspace=None, stream=None):
+    """Low-resolution augmentation of packed HWC RGB uint8 images: each image
+    reduced to low_res x low_res uint8, then preprocessed with ``params``
+    (``smol_lowres_preprocess_batch``). ``workspace`` (uint8 device tensor of
+    ``lowres_workspace_bytes(n, low_res)`` bytes) is allocated if omitted."""
+    if src.dtype.itemsize != 1 or not src.is_cuda or not src.is_contiguous():
+        raise ValueError("src must be a contiguous uint8 device tensor")
+    off = _table(offsets, np.int64)
+    w = _table(widths, np.int32)
+    h = _table(heights, np.int32)
+    pt = None if pitches is None else _table(pitches, np.int32)
+    n = len(off)
+    if not (len(w) == len(h) == n and (pt is None or len(pt) == n)):
+        raise ValueError("table lengths differ")
+    out = _out_tensor(out, n, params, src.device)
+    ws = _workspace(workspace, n, low_res, src.device)
+    _check(lib().smol_lowres_preprocess_batch(
+        src.data_ptr(), src.numel(), off.ctypes.data, w.ctypes.data, h.ctypes.data,
+        None if pt is None else pt.ctypes.data, n, low_res, ctypes.byref(params), ws.data_ptr(),
+        ws.numel(), out.data_ptr(), _stream_handle(stream)))
+    return out
+
+
+def yuv420_lowres_preprocess_batch(src, y_offsets, cb_offsets, cr_offsets, widths, heights,
+                                   params: Params, low_res: int, out=None, workspace=None,
+                                   stream=None):
+    """As ``lowres_preprocess_batch`` for planar I420 frames."""
+    if src.dtype.itemsize != 1 or not src.is_cuda or not src.is_contiguous():
+        raise ValueError("src must be a contiguous uint8 device tensor")
+    yo = _table(y_offsets, np.int64)
+    bo = _table(cb_offsets, np.int64)
+    ro = _table(cr_offsets, np.int64)
+    w = _table(widths, np.int32)
+    h = _table(heights, np.int32)
+    n = len(yo)
+    if not (len(bo) == len(ro) == len(w) == len(h) == n):
+        raise ValueError("table lengths differ")
+    out = _out_tensor(out, n, params, src.device)
+    ws = _workspace(workspace, n, low_res, src.device)
+    _check(lib().smol_yuv420_lowres_preprocess_batch(
+        src.data_ptr(), src.numel(), yo.ctypes.data, bo.ctypes.data, ro.ctypes.data,
+        w.ctypes.data, h.ctypes.data, n, low_res, ctypes.byref(params), ws.data_ptr(),
+        ws.numel(), out.data_ptr(), _stream_handle(stream)))
+    return out
+
+
 def _workload_options(wl) -> Options | None:
     if not wl.variant:
         return None
@@ -319,6 +390,15 @@ def _workload_options(wl) -> Options | None:
 def run_workload(wl, src_dev, out=None, stream=None):
     """Run a ``synthetic.Workload`` whose ``src`` already sits on the device."""
     p = make_params(wl.resize_short, wl.crop_h, wl.crop_w, wl.mean, wl.std, wl.out_dtype)
+    if wl.low_res:
+        if wl.variant:
+            raise ValueError("the low-resolution augmentation takes no ROI or options")
+        if wl.kind == "rgb":
+            return lowres_preprocess_batch(src_dev, wl.offsets, wl.widths, wl.heights, p,
+                                           wl.low_res, wl.pitches, out, None, stream)
+        return yuv420_lowres_preprocess_batch(src_dev, wl.y_offsets, wl.cb_offsets,
+                                              wl.cr_offsets, wl.widths, wl.heights, p,
+                                              wl.low_res, out, None, stream)
     o = _workload_options(wl)
     if wl.kind == "rgb":
         return preprocess_batch(src_dev, wl.offsets, wl.widths, wl.heights, p, wl.pitches, out,
@@ -339,6 +419,15 @@ class PreparedCall:
         self._keep = []
         self.options = _workload_options(wl)
         ex = self.options is not None
+        self._low = None
+        if wl.low_res:
+            if ex:
+                raise ValueError("the low-resolution augmentation takes no ROI or options")
+            import torch
+            ws = torch.empty(max(lowres_workspace_bytes(wl.n, wl.low_res), 16),
+                             dtype=torch.uint8, device="cuda")
+            self._low = (ctypes.c_int32(wl.low_res), ws, ctypes.c_void_p(ws.data_ptr()),
+                         ctypes.c_int64(ws.numel()))
         r = None if wl.rois is None else _rois(wl.rois, wl.n)
         if wl.kind == "rgb":
             tabs = [_table(wl.offsets, np.int64), _table(wl.widths, np.int32),
@@ -346,14 +435,16 @@ class PreparedCall:
             pt = None if wl.pitches is None else _table(wl.pitches, np.int32)
             self._keep = tabs + [pt, r]
             self._args = [t.ctypes.data for t in tabs] + [None if pt is None else pt.ctypes.data]
-            self._fn = lib().smol_preprocess_batch_ex if ex else lib().smol_preprocess_batch
+            self._fn = (lib().smol_lowres_preprocess_batch if self._low else
+                        lib().smol_preprocess_batch_ex if ex else lib().smol_preprocess_batch)
         else:
             tabs = [_table(wl.y_offsets, np.int64), _table(wl.cb_offsets, np.int64),
                     _table(wl.cr_offsets, np.int64), _table(wl.widths, np.int32),
                     _table(wl.heights, np.int32)]
             self._keep = tabs + [r]
             self._args = [t.ctypes.data for t in tabs]
-            self._fn = (lib().smol_yuv420_preprocess_batch_ex if ex
+            self._fn = (lib().smol_yuv420_lowres_preprocess_batch if self._low else
+                        lib().smol_yuv420_preprocess_batch_ex if ex
                         else lib().smol_yuv420_preprocess_batch)
         if ex:
             self._args.append(None if r is None else r.ctypes.data)
@@ -361,5 +452,10 @@ class PreparedCall:
         self._tail = [ctypes.byref(self.options)] if ex else []
 
     def __call__(self, src_ptr: int, src_bytes: int, out_ptr: int, stream_handle) -> None:
+        if self._low:
+            low, _, ws, ws_bytes = self._low
+            _check(self._fn(src_ptr, src_bytes, *self._args, self.n, low, self._pref, ws,
+                            ws_bytes, out_ptr, stream_handle))
+            return
         _check(self._fn(src_ptr, src_bytes, *self._args, self.n, self._pref, *self._tail,
                         out_ptr, stream_handle))

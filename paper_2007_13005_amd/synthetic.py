@@ -7,7 +7,7 @@ from it without sharing any of the method.
 
 The paper's datasets (ImageNet-style full-resolution photos, 161 px thumbnails,
 1080p / 480p traffic-camera video; section 8, "Datasets") are not available, so
-five seeded stand-ins reproduce their shapes, size mix and value ranges:
+seeded stand-ins reproduce their shapes, size mix and value ranges:
 
   c1  32 x 320x240 RGB, uniform 0..255; short side 256, crop 224, fp32 out
   c2  256 ragged RGB, W and H each uniform in [300, 600], packed back to back
@@ -21,6 +21,9 @@ five seeded stand-ins reproduce their shapes, size mix and value ranges:
   c6  256 regions of interest (64..512 px boxes) in 16 1080p RGB frames,
       resized directly to 112x112, channels-last fp16 (detection / face crops,
       the ROI use of section 6.4)
+  c7  256 ragged RGB as c2, low-resolution augmentation: reduced to 161x161
+      (the thumbnail size of section 5.2) then upsampled to 224x224 (short
+      side 224, crop 224), fp16 out (the training augmentation of section 5.3)
 
 Config k draws from ``numpy.random.default_rng(13005 + k)`` (PCG64).
 The normalisation constants are the ImageNet per-channel statistics the
@@ -35,6 +38,7 @@ import numpy as np
 
 OUT_F32 = 0
 OUT_F16 = 1
+OUT_U8 = 2
 
 # (0.485, 0.456, 0.406) * 255 and (0.229, 0.224, 0.225) * 255, formed in double
 # and rounded once to fp32.
@@ -72,6 +76,9 @@ class Workload:
     resize_mode: int = 0
     layout: int = 0
     siting: int = 0
+    # low-resolution augmentation: each image first reduced to low_res x
+    # low_res (0: off)
+    low_res: int = 0
 
     @property
     def variant(self) -> bool:
@@ -84,7 +91,7 @@ class Workload:
 
     @property
     def out_elem_bytes(self) -> int:
-        return 4 if self.out_dtype == OUT_F32 else 2
+        return {OUT_F32: 4, OUT_F16: 2, OUT_U8: 1}[self.out_dtype]
 
     def out_shape(self) -> tuple[int, int, int, int]:
         if self.layout == 1:
@@ -258,7 +265,22 @@ def c6(n: int = 256, height: int = 1080, width: int = 1920) -> Workload:
     return wl
 
 
-CONFIGS = {"c1": c1, "c2": c2, "c3": c3, "c4": c4, "c5": c5, "c6": c6}
+def c7(n: int = 256, low_res: int = 161) -> Workload:
+    """Low-resolution-aware training augmentation over ImageNet-sized photos:
+    every image reduced to low_res x low_res, then upsampled to the network's
+    224 x 224 input."""
+    rng = np.random.default_rng(SEED_BASE + 7)
+    sizes = rng.integers(300, 601, size=(n, 2))
+    images = [rng.integers(0, 256, size=(int(h), int(w), 3), dtype=np.uint8) for w, h in sizes]
+    wl = rgb_workload("c7", images, 224, 224, OUT_F16, 1,
+                      f"ragged {n} RGB uint8 HWC, W,H ~ U[300,600]; reduced to "
+                      f"{low_res}x{low_res} uint8, then short side 224, center crop 224x224, "
+                      "NCHW fp16")
+    wl.low_res = low_res
+    return wl
+
+
+CONFIGS = {"c1": c1, "c2": c2, "c3": c3, "c4": c4, "c5": c5, "c6": c6, "c7": c7}
 
 
 def make(name: str, **kw) -> Workload:

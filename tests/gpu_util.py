@@ -3,7 +3,8 @@ through the oracle, and compare to the stated tolerances.
 
 Tolerances: fp32 outputs within 1e-5 absolute of the oracle; fp16 outputs
 within 1 unit in the last place of the oracle's round-to-nearest-even fp16
-(distance measured on the ordered binary16 encoding).
+(distance measured on the ordered binary16 encoding); uint8 outputs (a
+rounding decision taken in fp32 on both sides) bit for bit.
 """
 from __future__ import annotations
 
@@ -24,6 +25,16 @@ def note(msg: str) -> None:
 
 
 def run_oracle(wl: synthetic.Workload) -> np.ndarray:
+    if wl.low_res:
+        if wl.kind == "rgb":
+            return oracle.lowres_preprocess_batch(wl.src, wl.offsets, wl.widths, wl.heights,
+                                                  wl.pitches, wl.low_res, wl.resize_short,
+                                                  wl.crop_h, wl.crop_w, wl.mean, wl.std,
+                                                  wl.out_dtype)
+        return oracle.yuv420_lowres_preprocess_batch(wl.src, wl.y_offsets, wl.cb_offsets,
+                                                     wl.cr_offsets, wl.widths, wl.heights,
+                                                     wl.low_res, wl.resize_short, wl.crop_h,
+                                                     wl.crop_w, wl.mean, wl.std, wl.out_dtype)
     if wl.variant:
         if wl.kind == "rgb":
             return oracle.preprocess_batch_ex(wl.src, wl.offsets, wl.widths, wl.heights,
@@ -57,7 +68,8 @@ def upload(wl: synthetic.Workload, pad_front: int = 0):
 def run_gpu(wl: synthetic.Workload, pad_front: int = 0, stream=None) -> np.ndarray:
     import torch
     note(f"[gpu] {wl.name}: n={wl.n} kind={wl.kind} S={wl.resize_short} "
-         f"crop={wl.crop_h}x{wl.crop_w} dtype={'f16' if wl.out_dtype else 'f32'}")
+         f"crop={wl.crop_h}x{wl.crop_w} dtype={('f32', 'f16', 'u8')[wl.out_dtype]} "
+         f"low_res={wl.low_res}")
     _, src = upload(wl, pad_front)
     out = smol.run_workload(wl, src, stream=stream)
     torch.cuda.synchronize()
@@ -73,6 +85,14 @@ def f16_ordered(bits: np.ndarray) -> np.ndarray:
 
 def assert_parity(gpu: np.ndarray, ref: np.ndarray, out_dtype: int, what: str = "") -> dict:
     assert gpu.shape == ref.shape, (gpu.shape, ref.shape)
+    if out_dtype == smol.OUT_U8:
+        assert gpu.dtype == np.uint8 and ref.dtype == np.uint8
+        bad = np.argwhere(gpu != ref)
+        if bad.size:
+            i = tuple(bad[0])
+            raise AssertionError(f"{what}: {len(bad)} uint8 outputs differ, first at {i}: "
+                                 f"gpu {gpu[i]} oracle {ref[i]}")
+        return {"exact_frac": 1.0}
     if out_dtype == smol.OUT_F32:
         assert gpu.dtype == np.float32 and ref.dtype == np.float32
         assert np.all(np.isfinite(gpu)), what

@@ -300,3 +300,54 @@ def test_left_siting_chroma_footprint():
     x0, x1 = gl["src_x_first"], gl["src_x_last"]
     assert (gl["chroma_x_first"], gl["chroma_x_last"]) == (x0 // 2, min(x1 // 2 + 1, 319))
     assert gc["chroma_x_first"] == (2 * x0 - 1) // 4
+
+
+def test_u8_output_refuses_forced_tiled_paths():
+    for path in (smol.PATH_LDS, smol.PATH_GATHER, smol.PATH_ROWS):
+        smol.set_tuning(path=path)
+        try:
+            rc, msg = _rgb_call(params=_params(out_dtype=smol.OUT_U8))
+        finally:
+            smol.reset_tuning()
+        assert rc == smol.ERR_UNSUPPORTED and "uint8" in msg, (path, rc, msg)
+
+
+def test_lowres_workspace_bytes():
+    f = smol.lib().smol_lowres_workspace_bytes
+    assert f(256, 161) == 256 * 3 * 161 * 161 + 16
+    assert f(1, 3) == 32 + 16
+    assert f(0, 161) == 0 and f(-1, 4) == 0 and f(4, 0) == 0
+
+
+def _lowres_call(n=1, low_res=64, params=None, ws=FAKE_OUT + 4096, ws_bytes=None):
+    p = params or _params()
+    off = np.zeros(1, np.int64)
+    w = np.asarray([320], np.int32)
+    h = np.asarray([240], np.int32)
+    need = smol.lib().smol_lowres_workspace_bytes(n, low_res)
+    rc = smol.lib().smol_lowres_preprocess_batch(
+        FAKE_SRC, 10**9, off.ctypes.data, w.ctypes.data, h.ctypes.data, None, n, low_res,
+        ctypes.byref(p), ws, need if ws_bytes is None else ws_bytes, FAKE_OUT, None)
+    return rc, smol.lib().smol_last_error().decode()
+
+
+@pytest.mark.parametrize("kw,needle", [
+    (dict(low_res=0), "low_res"),
+    (dict(low_res=70000), "low_res"),
+    (dict(ws_bytes=64 * 64 * 3 + 15), "workspace"),
+    (dict(ws=0), "workspace"),
+    (dict(ws=FAKE_OUT + 8), "aligned"),
+    (dict(params=_params(out_dtype=smol.OUT_U8)), "normalised"),
+    # the 64 x 64 image resized to 256 cannot hold a 300 x 300 crop
+    (dict(params=_params(crop_h=300, crop_w=300)), "larger than resized"),
+    (dict(n=-1), "n = -1"),
+])
+def test_lowres_validation_rejects(kw, needle):
+    rc, msg = _lowres_call(**kw)
+    assert rc == smol.ERR_INVALID_ARG, (rc, msg)
+    assert needle in msg
+
+
+def test_lowres_empty_batch_is_a_no_op():
+    rc, _ = _lowres_call(n=0, ws=0)
+    assert rc == smol.OK

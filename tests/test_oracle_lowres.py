@@ -138,3 +138,45 @@ def test_lowres_rejects_bad_arguments():
     with pytest.raises(ValueError):
         flat, offs, ws, hs = _flat([img])
         oracle.lowres_preprocess_batch(flat, offs, ws, hs, None, 4, 8, 8, 8, MEAN, STD, U8)
+
+
+def test_single_image_entry_points_match_the_batch_calls():
+    """The raw-pointer single-image calls (used by the CPU baseline) give the
+    batch calls' bytes."""
+    rng = np.random.default_rng(26)
+    img = rng.integers(0, 256, (45, 62, 3), dtype=np.uint8)
+    flat, offs, ws, hs = _flat([img])
+    out = np.empty((3, 20, 24), np.uint16)
+    rc = oracle.preprocess_image_ex_into(flat.ctypes.data, 62, 45, 186, (5, 3, 40, 30), 1, 20,
+                                         24, MEAN, STD, F16, oracle.RESIZE_DIRECT, oracle.NCHW,
+                                         out.ctypes.data)
+    exp = oracle.preprocess_batch_ex(flat, offs, ws, hs, None, [(5, 3, 40, 30)], 1, 20, 24, MEAN,
+                                     STD, F16, oracle.RESIZE_DIRECT, oracle.NCHW)
+    assert rc == 0 and np.array_equal(out, exp[0].view(np.uint16))
+    o1 = np.empty((3, 28, 28), np.uint16)
+    rc = oracle.lowres_preprocess_image_into(flat.ctypes.data, 62, 45, 186, 17, 32, 28, 28, MEAN,
+                                             STD, F16, o1.ctypes.data)
+    exp = oracle.lowres_preprocess_batch(flat, offs, ws, hs, None, 17, 32, 28, 28, MEAN, STD, F16)
+    assert rc == 0 and np.array_equal(o1, exp[0].view(np.uint16))
+
+    W, H = 33, 21
+    y = rng.integers(16, 236, (H, W), dtype=np.uint8)
+    cb = rng.integers(16, 241, ((H + 1) // 2, (W + 1) // 2), dtype=np.uint8)
+    cr = rng.integers(16, 241, ((H + 1) // 2, (W + 1) // 2), dtype=np.uint8)
+    o2 = np.empty((10, 12, 3), np.float32)
+    rc = oracle.yuv420_preprocess_image_ex_into(y.ctypes.data, cb.ctypes.data, cr.ctypes.data, W,
+                                                H, (1, 1, 30, 19), 1, 10, 12, MEAN, STD, F32,
+                                                oracle.RESIZE_DIRECT, oracle.NHWC,
+                                                oracle.CHROMA_LEFT, o2.ctypes.data)
+    yuv = np.concatenate([y.reshape(-1), cb.reshape(-1), cr.reshape(-1)])
+    exp = oracle.yuv420_preprocess_batch_ex(yuv, [0], [W * H], [W * H + cb.size], [W], [H],
+                                            [(1, 1, 30, 19)], 1, 10, 12, MEAN, STD, F32,
+                                            oracle.RESIZE_DIRECT, oracle.NHWC, oracle.CHROMA_LEFT)
+    assert rc == 0 and np.array_equal(o2, exp[0])
+    o3 = np.empty((3, 16, 16), np.float32)
+    rc = oracle.yuv420_lowres_preprocess_image_into(y.ctypes.data, cb.ctypes.data, cr.ctypes.data,
+                                                    W, H, 9, 20, 16, 16, MEAN, STD, F32,
+                                                    o3.ctypes.data)
+    exp = oracle.yuv420_lowres_preprocess_batch(yuv, [0], [W * H], [W * H + cb.size], [W], [H], 9,
+                                                20, 16, 16, MEAN, STD, F32)
+    assert rc == 0 and np.array_equal(o3, exp[0])
