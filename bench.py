@@ -235,7 +235,8 @@ def stream_ceilings_gbps(torch, mib: int = 512, reps: int = 10) -> dict:
 
 def load_traffic(config: str) -> dict | None:
     """HBM traffic per launch from the committed rocprofv3 counter summary,
-    valid only while the kernel sources match the ones it was taken on."""
+    valid only while the kernel sources (device code and launchers) match the
+    ones it was taken on; the caller also checks the launch grid."""
     import hashlib
     try:
         with open(TRAFFIC_FILE) as f:
@@ -354,6 +355,8 @@ def main() -> int:
     copy_gbps = None if ceil is None else ceil["copy"]
 
     traffic = load_traffic(args.config)
+    if traffic is not None and traffic.get("grid") != plan["grid"]:
+        traffic = None  # counters taken on another launch shape
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                 "traffic": None if traffic is None else traffic["bytes_per_launch"]}
