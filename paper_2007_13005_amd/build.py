@@ -33,6 +33,7 @@ SOURCES = [
     "smol_rows_yuv_stride.hip",
     "smol_rows_yuv_stride_nhwc.hip",
     "smol_host.cpp",
+    "smol_pipeline.cpp",
 ]
 HEADERS = ["smol_internal.h", "smol_device.h", "smol_rows.h"]
 
@@ -115,7 +116,8 @@ def sources_newer_than_lib() -> bool:
     if not os.path.exists(LIB):
         return True
     t = os.path.getmtime(LIB)
-    files = [os.path.join(CSRC, f) for f in SOURCES + HEADERS] + [os.path.join(INCLUDE, "smol.h")]
+    files = [os.path.join(CSRC, f) for f in SOURCES + HEADERS] + [
+        os.path.join(INCLUDE, f) for f in os.listdir(INCLUDE) if f.endswith(".h")]
     return any(os.path.getmtime(f) > t for f in files)
 
 

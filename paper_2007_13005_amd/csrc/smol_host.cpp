@@ -1294,3 +1294,16 @@ const char *smol_last_error(void) { return g_last_error.c_str(); }
 int smol_version(void) { return 100; }
 
 }  // extern "C"
+
+int smol::set_error(int code, const char *fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return code;
+}
+
+void smol::clear_error() { g_last_error.clear(); }

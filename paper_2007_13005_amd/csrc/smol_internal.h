@@ -71,6 +71,11 @@ constexpr int kRowsMaxGroups = 4;
 // Waves per workgroup of the row-streaming kernels (each wave independent).
 constexpr int kRowsMaxWavesPerGroup = 4;
 
+// The calling thread's smol_last_error() message (smol_host.cpp): set_error
+// formats it and returns `code`; clear_error empties it.
+int set_error(int code, const char *fmt, ...);
+void clear_error();
+
 // Launchers (smol_kernels.hip). Return a hipError_t as int.
 // Direct kernels: out_type 0 fp32, 1 fp16, 2 uint8 (rounded, not normalised).
 int launch_rgb_direct(const BatchArgs &a, int out_type, void *stream);

@@ -79,7 +79,26 @@ class Plan(ctypes.Structure):
         return {name: getattr(self, name) for name, _ in self._fields_}
 
 
-# Every symbol include/smol.h declares, with its ctypes signature.
+class PipelineConfig(ctypes.Structure):
+    _fields_ = [("slots", ctypes.c_int32), ("streams", ctypes.c_int32),
+                ("input_bytes", ctypes.c_int64), ("output_bytes", ctypes.c_int64),
+                ("reserved", ctypes.c_int32 * 4)]
+
+
+class PipelineStats(ctypes.Structure):
+    _fields_ = [("submitted", ctypes.c_int64), ("completed", ctypes.c_int64),
+                ("images", ctypes.c_int64), ("bytes_copied", ctypes.c_int64),
+                ("acquire_waits", ctypes.c_int64), ("reserved", ctypes.c_int64 * 3)]
+
+    def as_dict(self) -> dict:
+        return {name: getattr(self, name) for name, _ in self._fields_ if name != "reserved"}
+
+
+# smol_consumer_fn: int (*)(void *user, const void *output, int32_t n, void *stream)
+CONSUMER = ctypes.CFUNCTYPE(ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                            ctypes.c_void_p)
+
+# Every symbol include/*.h declares, with its ctypes signature.
 _vp = ctypes.c_void_p
 SIGNATURES = {
     "smol_preprocess_batch": (ctypes.c_int, [_vp, ctypes.c_int64, _vp, _vp, _vp, _vp,
@@ -108,6 +127,22 @@ SIGNATURES = {
                                                            _vp, _vp, ctypes.c_int32,
                                                            ctypes.c_int32, ctypes.POINTER(Params),
                                                            _vp, ctypes.c_int64, _vp, _vp]),
+    "smol_pipeline_create": (ctypes.c_int, [ctypes.POINTER(PipelineConfig),
+                                            ctypes.POINTER(ctypes.c_void_p)]),
+    "smol_pipeline_destroy": (ctypes.c_int, [_vp]),
+    "smol_pipeline_acquire": (ctypes.c_int, [_vp, ctypes.POINTER(ctypes.c_int32),
+                                             ctypes.POINTER(ctypes.c_void_p),
+                                             ctypes.POINTER(ctypes.c_void_p)]),
+    "smol_pipeline_release": (ctypes.c_int, [_vp, ctypes.c_int32]),
+    "smol_pipeline_submit": (ctypes.c_int, [_vp, ctypes.c_int32, ctypes.c_int64, _vp, _vp, _vp,
+                                            _vp, _vp, ctypes.c_int32, ctypes.POINTER(Params),
+                                            ctypes.POINTER(Options), CONSUMER, _vp]),
+    "smol_pipeline_submit_yuv420": (ctypes.c_int, [_vp, ctypes.c_int32, ctypes.c_int64, _vp, _vp,
+                                                   _vp, _vp, _vp, _vp, ctypes.c_int32,
+                                                   ctypes.POINTER(Params),
+                                                   ctypes.POINTER(Options), CONSUMER, _vp]),
+    "smol_pipeline_drain": (ctypes.c_int, [_vp]),
+    "smol_pipeline_get_stats": (ctypes.c_int, [_vp, ctypes.POINTER(PipelineStats)]),
     "smol_set_tuning": (ctypes.c_int, [ctypes.POINTER(Tuning)]),
     "smol_last_plan": (ctypes.c_int, [ctypes.POINTER(Plan)]),
     "smol_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -155,6 +190,29 @@ def _mapped_hip_runtimes() -> list[str]:
     except OSError:
         return []
     return sorted({os.path.realpath(p) for p in paths})
+
+
+_hip = None
+
+
+def hip_runtime() -> ctypes.CDLL:
+    """The HIP runtime this library is bound to (the one torch loaded), with
+    ``hipMemcpyAsync`` typed: for consumers that enqueue their own copies."""
+    global _hip
+    if _hip is None:
+        lib()
+        rt = _mapped_hip_runtimes()
+        if not rt:
+            raise RuntimeError("no HIP runtime is loaded")
+        h = ctypes.CDLL(rt[0])
+        h.hipMemcpyAsync.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+                                     ctypes.c_int, ctypes.c_void_p]
+        h.hipMemcpyAsync.restype = ctypes.c_int
+        _hip = h
+    return _hip
+
+
+HIP_MEMCPY_DEVICE_TO_DEVICE = 3
 
 
 def _check(status: int) -> None:
@@ -459,3 +517,95 @@ class PreparedCall:
             return
         _check(self._fn(src_ptr, src_bytes, *self._args, self.n, self._pref, *self._tail,
                         out_ptr, stream_handle))
+
+
+class Pipeline:
+    """Pipelined ingest (``include/smol_pipeline.h``): ``slots`` reused buffer
+    sets (pinned host input, device input, device output) and ``streams`` HIP
+    streams. Producer threads ``acquire`` a slot, fill ``host_view(slot)`` with
+    a batch and ``submit`` it; the copy, the preprocessing and the optional
+    consumer (a ``CONSUMER`` callback that enqueues the DNN on the given
+    stream) run in stream order while other slots are filled."""
+
+    def __init__(self, slots: int, streams: int, input_bytes: int, output_bytes: int):
+        cfg = PipelineConfig()
+        cfg.slots, cfg.streams = slots, streams
+        cfg.input_bytes, cfg.output_bytes = input_bytes, output_bytes
+        h = ctypes.c_void_p()
+        _check(lib().smol_pipeline_create(ctypes.byref(cfg), ctypes.byref(h)))
+        self._h = h
+        self.input_bytes = input_bytes
+        self.output_bytes = output_bytes
+        self._host = {}
+
+    def acquire(self) -> tuple[int, int, int]:
+        """(slot, host pointer, device output pointer)."""
+        slot, host, out = ctypes.c_int32(), ctypes.c_void_p(), ctypes.c_void_p()
+        _check(lib().smol_pipeline_acquire(self._h, ctypes.byref(slot), ctypes.byref(host),
+                                           ctypes.byref(out)))
+        self._host[slot.value] = host.value
+        return slot.value, host.value, out.value
+
+    def host_view(self, slot: int) -> np.ndarray:
+        """The acquired slot's pinned input buffer as a uint8 array."""
+        buf = (ctypes.c_uint8 * self.input_bytes).from_address(self._host[slot])
+        return np.ctypeslib.as_array(buf)
+
+    def release(self, slot: int) -> None:
+        _check(lib().smol_pipeline_release(self._h, slot))
+
+    def submit(self, slot: int, nbytes: int, offsets, widths, heights, params: Params,
+               pitches=None, rois=None, options: Options | None = None, consumer=None,
+               user: int | None = None) -> None:
+        off = _table(offsets, np.int64)
+        w = _table(widths, np.int32)
+        h = _table(heights, np.int32)
+        pt = None if pitches is None else _table(pitches, np.int32)
+        n = len(off)
+        r = _rois(rois, n)
+        _check(lib().smol_pipeline_submit(
+            self._h, slot, nbytes, off.ctypes.data, w.ctypes.data, h.ctypes.data,
+            None if pt is None else pt.ctypes.data, None if r is None else r.ctypes.data, n,
+            ctypes.byref(params), None if options is None else ctypes.byref(options),
+            CONSUMER() if consumer is None else consumer, user))
+
+    def submit_yuv420(self, slot: int, nbytes: int, y_offsets, cb_offsets, cr_offsets, widths,
+                      heights, params: Params, rois=None, options: Options | None = None,
+                      consumer=None, user: int | None = None) -> None:
+        yo = _table(y_offsets, np.int64)
+        bo = _table(cb_offsets, np.int64)
+        ro = _table(cr_offsets, np.int64)
+        w = _table(widths, np.int32)
+        h = _table(heights, np.int32)
+        n = len(yo)
+        r = _rois(rois, n)
+        _check(lib().smol_pipeline_submit_yuv420(
+            self._h, slot, nbytes, yo.ctypes.data, bo.ctypes.data, ro.ctypes.data, w.ctypes.data,
+            h.ctypes.data, None if r is None else r.ctypes.data, n, ctypes.byref(params),
+            None if options is None else ctypes.byref(options),
+            CONSUMER() if consumer is None else consumer, user))
+
+    def drain(self) -> None:
+        _check(lib().smol_pipeline_drain(self._h))
+
+    def stats(self) -> dict:
+        st = PipelineStats()
+        _check(lib().smol_pipeline_get_stats(self._h, ctypes.byref(st)))
+        return st.as_dict()
+
+    def close(self) -> None:
+        if self._h is not None and self._h.value:
+            h, self._h = self._h, None
+            _check(lib().smol_pipeline_destroy(h))
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -15,13 +15,13 @@ import pytest
 import oracle
 from paper_2007_13005_amd import smol, synthetic
 
-HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include",
-                      "smol.h")
+INCLUDE = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include")
+HEADERS = sorted(os.path.join(INCLUDE, f) for f in os.listdir(INCLUDE) if f.endswith(".h"))
 MEAN, STD = synthetic.IMAGENET_MEAN_255, synthetic.IMAGENET_STD_255
 
 
 def _declared_functions() -> list[str]:
-    text = open(HEADER).read()
+    text = "\n".join(open(h).read() for h in HEADERS)
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(smol_[a-z0-9_]+)\s*\(", text)))
 
@@ -351,3 +351,35 @@ def test_lowres_validation_rejects(kw, needle):
 def test_lowres_empty_batch_is_a_no_op():
     rc, _ = _lowres_call(n=0, ws=0)
     assert rc == smol.OK
+
+
+@pytest.mark.parametrize("kw,needle", [
+    (dict(slots=0), "slots"), (dict(slots=65), "slots"), (dict(streams=0), "streams"),
+    (dict(streams=17), "streams"), (dict(input_bytes=0), "input_bytes"),
+    (dict(output_bytes=8), "output_bytes"), (dict(reserved=1), "reserved"),
+])
+def test_pipeline_config_validation(kw, needle):
+    cfg = smol.PipelineConfig()
+    cfg.slots, cfg.streams, cfg.input_bytes, cfg.output_bytes = 2, 1, 1024, 1024
+    for k, v in kw.items():
+        if k == "reserved":
+            cfg.reserved[0] = v
+        else:
+            setattr(cfg, k, v)
+    h = ctypes.c_void_p(1)
+    rc = smol.lib().smol_pipeline_create(ctypes.byref(cfg), ctypes.byref(h))
+    assert rc == smol.ERR_INVALID_ARG and h.value is None
+    assert needle in smol.lib().smol_last_error().decode()
+
+
+def test_pipeline_null_handles_are_rejected():
+    lib = smol.lib()
+    slot, host, out = ctypes.c_int32(), ctypes.c_void_p(), ctypes.c_void_p()
+    assert lib.smol_pipeline_acquire(None, ctypes.byref(slot), ctypes.byref(host),
+                                     ctypes.byref(out)) == smol.ERR_INVALID_ARG
+    assert lib.smol_pipeline_release(None, 0) == smol.ERR_INVALID_ARG
+    assert lib.smol_pipeline_drain(None) == smol.ERR_INVALID_ARG
+    assert lib.smol_pipeline_destroy(None) == smol.OK
+    p = smol.make_params(256, 224, 224, MEAN, STD, smol.OUT_F16)
+    assert lib.smol_pipeline_submit(None, 0, 1, None, None, None, None, None, 0, ctypes.byref(p),
+                                    None, smol.CONSUMER(), None) == smol.ERR_INVALID_ARG
