@@ -10,13 +10,15 @@ Input/output sets are rotated so that the touched working set exceeds twice
 the 256 MB Infinity Cache: the number reported is an HBM number, not a
 cache-warm one.
 
-Prints one JSON line. ``--config c1..c7`` selects another workload (c7, the
+Prints one JSON line. ``--pipeline`` runs the pipelined-ingest experiment
+instead (one JSON line as well). ``--config c1..c7`` selects another workload (c7, the
 low-resolution augmentation, is two launches per step: the roofline figure
 then covers both).
 """
 from __future__ import annotations
 
 import argparse
+import ctypes
 import json
 import os
 import sys
@@ -50,6 +52,11 @@ def parse():
     ap.add_argument("--row-order", type=int, default=0, help="tuning override (0: automatic)")
     ap.add_argument("--profile-run", action="store_true",
                     help="no CPU baseline, fewer prints: for runs under rocprofv3")
+    ap.add_argument("--pipeline", action="store_true",
+                    help="instead of the benchmark, the pipelined-ingest experiment: pipelined "
+                         "throughput against the minimum of the stage throughputs (Eq. 4)")
+    ap.add_argument("--pipeline-seconds", type=float, default=2.0,
+                    help="duration of each timed phase of --pipeline")
     ap.add_argument("--copy-probe", type=int, default=0,
                     help="instead of the benchmark, copy this many MiB with torch several "
                          "times (calibrates the FETCH_SIZE / WRITE_SIZE counters)")
@@ -267,6 +274,222 @@ def copy_probe(mib: int) -> None:
     print(json.dumps({"copy_probe_bytes": n, "copies": 5}), flush=True)
 
 
+class CopyConsumer:
+    """The consumer stage of the pipeline experiment: a memory-bound stand-in
+    for the DNN that reads each preprocessed batch ``reps`` times (device to
+    device copies into one resident scratch buffer, on the batch's stream).
+    It calls only the HIP runtime, no framework code, from the callback."""
+
+    def __init__(self, torch, smol, wl, reps: int):
+        self.smol, self.reps = smol, reps
+        self.nbytes = wl.n * 3 * wl.crop_h * wl.crop_w * wl.out_elem_bytes
+        self.dst = torch.empty(self.nbytes, dtype=torch.uint8, device="cuda:0")
+        self.rt = smol.hip_runtime()
+        self.fn = smol.CONSUMER(self._consume)
+
+    def enqueue(self, output: int, stream: int) -> int:
+        for _ in range(self.reps):
+            rc = self.rt.hipMemcpyAsync(self.dst.data_ptr(), output, self.nbytes,
+                                        self.smol.HIP_MEMCPY_DEVICE_TO_DEVICE, stream)
+            if rc:
+                return rc
+        return 0
+
+    def _consume(self, user, output, n, stream):
+        try:
+            return self.enqueue(output, stream)
+        except Exception:  # noqa: BLE001 -- reported as a failed consumer
+            return 1
+
+
+class KernelConsumer:
+    """A compute-bound stand-in for the DNN: ``reps`` launches of this
+    library's resize kernel that read the batch's output on its stream. Each
+    output image's 3*C_h*C_w elements are read as the bytes of a small RGB
+    image (3*C_h*C_w*e = 3*W*H bytes) that is resized to 112 x 112 fp16 into
+    a resident scratch buffer: shader work that reads all of the output, on
+    the compute units rather than the copy engines."""
+
+    def __init__(self, torch, smol, wl, reps: int):
+        import numpy as np
+        self.smol, self.reps, self.n = smol, reps, wl.n
+        per = 3 * wl.crop_h * wl.crop_w * wl.out_elem_bytes  # bytes of one output image
+        self.h = wl.crop_h
+        self.w = per // (3 * self.h)
+        assert 3 * self.w * self.h == per
+        self.nbytes = wl.n * per
+        self.off = np.arange(wl.n, dtype=np.int64) * per
+        self.ws = np.full(wl.n, self.w, np.int32)
+        self.hs = np.full(wl.n, self.h, np.int32)
+        self.p = smol.make_params(112, 112, 112, wl.mean, wl.std, smol.OUT_F16)
+        self.dst = torch.empty(wl.n * 3 * 112 * 112, dtype=torch.float16, device="cuda:0")
+        self.fn = smol.CONSUMER(self._consume)
+        self._lib = smol.lib()
+        self._pref = ctypes.byref(self.p)
+
+    def enqueue(self, output: int, stream: int) -> int:
+        for _ in range(self.reps):
+            rc = self._lib.smol_preprocess_batch(output, self.nbytes, self.off.ctypes.data,
+                                                 self.ws.ctypes.data, self.hs.ctypes.data, None,
+                                                 self.n, self._pref, self.dst.data_ptr(), stream)
+            if rc:
+                return rc
+        return 0
+
+    def _consume(self, user, output, n, stream):
+        try:
+            return self.enqueue(output, stream)
+        except Exception:  # noqa: BLE001 -- reported as a failed consumer
+            return 1
+
+
+def pipeline_experiment(args) -> int:
+    """Section 4's corrected throughput estimate (Eq. 4) checked on one GPU:
+    each stage's throughput is measured alone -- producers filling pinned
+    slots (the decoder's place), host-to-device copies, the preprocessing
+    kernel, the consumer -- then the stages run pipelined through the library's
+    pipeline, and the measured rate is set against the minimum."""
+    import threading
+
+    import torch
+
+    from paper_2007_13005_amd import smol, synthetic
+
+    wl = synthetic.make(args.config)
+    if wl.kind != "rgb" or wl.variant or wl.low_res:
+        print("--pipeline runs plain RGB workloads", file=sys.stderr)
+        return 2
+    secs = args.pipeline_seconds
+    # slots: every producer holds one while it fills it, and the batches in
+    # flight need the rest (section 6.1: over-allocate so that producers do
+    # not wait on consumers)
+    slots, streams, copy_streams = 16, 3, 1
+    nbytes = wl.src.size
+    out_bytes = wl.n * 3 * wl.crop_h * wl.crop_w * wl.out_elem_bytes
+    src_host = wl.src  # the "decoded" batch the producers copy into a slot
+    params = smol.make_params(wl.resize_short, wl.crop_h, wl.crop_w, wl.mean, wl.std,
+                              wl.out_dtype)
+    strs = [torch.cuda.Stream() for _ in range(streams)]
+
+    def images_per_s(batches: int, seconds: float) -> float:
+        return batches * wl.n / seconds
+
+    def timed_threads(threads: int, body) -> float:
+        counts = [0] * threads
+        deadline = time.perf_counter() + secs
+
+        def run(t):
+            while time.perf_counter() < deadline:
+                body()
+                counts[t] += 1
+        t0 = time.perf_counter()
+        ts = [threading.Thread(target=run, args=(t,)) for t in range(threads)]
+        for t in ts:
+            t.start()
+        for t in ts:
+            t.join()
+        return sum(counts), time.perf_counter() - t0
+
+    # preprocessing alone: inputs resident, launches on the pipeline's streams
+    src_dev = torch.from_numpy(src_host).to("cuda:0")
+    outs = [torch.empty(wl.out_shape(), dtype=torch.float16, device="cuda:0")
+            for _ in range(streams)]
+    call = smol.PreparedCall(wl)
+
+    def rate_on_streams(enqueue, reps: int, count: int = streams) -> float:
+        for i in range(count):
+            enqueue(i)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(reps):
+            enqueue(i % count)
+        torch.cuda.synchronize()
+        return images_per_s(reps, time.perf_counter() - t0)
+
+    g_rate = rate_on_streams(lambda i: call(src_dev.data_ptr(), nbytes, outs[i].data_ptr(),
+                                            strs[i].cuda_stream), 300)
+    # copies alone: pinned host buffer to device on as many streams as the
+    # pipeline has copy streams
+    pinned = torch.from_numpy(src_host).pin_memory()
+    dsts = [torch.empty(nbytes, dtype=torch.uint8, device="cuda:0") for _ in range(streams)]
+
+    def h2d(i):
+        with torch.cuda.stream(strs[i]):
+            dsts[i].copy_(pinned, non_blocking=True)
+    reps_h2d = max(6, int(secs / max(1e-4, nbytes / 50e9)))
+    h_rate = rate_on_streams(h2d, reps_h2d, copy_streams)
+
+    # (name, producer threads, consumer class, consumer repetitions)
+    scenarios = [("producer-bound", 1, None, 0), ("copy-bound", 8, None, 0),
+                 ("kernel-consumer-bound", 8, KernelConsumer, 250),
+                 ("copy-consumer-bound", 8, CopyConsumer, 200)]
+    results = []
+    with smol.Pipeline(slots, streams, nbytes, out_bytes, copy_streams) as pl:
+        for name, producers, kind, reps in scenarios:
+            print(f"[pipeline] {name}: stage rates", file=sys.stderr, flush=True)
+            dnn = kind(torch, smol, wl, reps) if kind else None
+            e_rate = None
+            if reps:
+                # alone, over as many output buffers as the pipeline has slots
+                # (so that they do not stay in the 256 MB MALL either)
+                c_outs = [torch.empty(out_bytes, dtype=torch.uint8, device="cuda:0")
+                          for _ in range(slots)]
+                k = [0]
+
+                def consume_alone(i):
+                    k[0] += 1
+                    dnn.enqueue(c_outs[k[0] % slots].data_ptr(), strs[i].cuda_stream)
+                e_rate = rate_on_streams(consume_alone, max(6, 4 * slots))
+                del c_outs
+
+            def fill_only():
+                slot, host, _ = pl.acquire()
+                ctypes.memmove(host, src_host.ctypes.data, nbytes)
+                pl.release(slot)
+            done, el = timed_threads(producers, fill_only)
+            p_rate = images_per_s(done, el)
+
+            def produce():
+                slot, host, _ = pl.acquire()
+                ctypes.memmove(host, src_host.ctypes.data, nbytes)
+                pl.submit(slot, nbytes, wl.offsets, wl.widths, wl.heights, params,
+                          consumer=dnn.fn if reps else None)
+            pl.drain()
+            print(f"[pipeline] {name}: pipelined run", file=sys.stderr, flush=True)
+            before = pl.stats()["completed"]
+            t0 = time.perf_counter()
+            done, _ = timed_threads(producers, produce)
+            pl.drain()
+            el = time.perf_counter() - t0
+            assert pl.stats()["completed"] - before == done
+            measured = images_per_s(done, el)
+            stages = {"producer": p_rate, "h2d": h_rate, "preprocess": g_rate}
+            if e_rate is not None:
+                stages["consumer"] = e_rate
+            bottleneck = min(stages, key=stages.get)
+            results.append({"scenario": name, "producer_threads": producers,
+                            "consumer": kind.__name__ if kind else None,
+                            "consumer_reps": reps,
+                            "stage_images_per_s": {k: round(v, 1) for k, v in stages.items()},
+                            "predicted_images_per_s": round(stages[bottleneck], 1),
+                            "predicted_bottleneck": bottleneck,
+                            "measured_images_per_s": round(measured, 1),
+                            "measured_over_predicted": round(measured / stages[bottleneck], 3),
+                            "batches": done})
+            print(f"[pipeline] {results[-1]}", file=sys.stderr, flush=True)
+    print(json.dumps({
+        "metric": "pipelined images/s against the minimum of the stage throughputs (Eq. 4)",
+        "unit": "images/s", "n_gpus": 1, "data": "synthetic",
+        "config": {"workload": f"{wl.name}: {wl.description}", "batch": wl.n,
+                   "batch_input_bytes": nbytes, "slots": slots, "streams": streams,
+                   "copy_streams": copy_streams,
+                   "phase_seconds": secs,
+                   "consumers": {"KernelConsumer": KernelConsumer.__doc__.split(":")[0],
+                                 "CopyConsumer": CopyConsumer.__doc__.split(".")[0]}},
+        "scenarios": results}), flush=True)
+    return 0
+
+
 def main() -> int:
     args = parse()
     if args.gpus != 1:
@@ -277,6 +500,8 @@ def main() -> int:
     if args.copy_probe:
         copy_probe(args.copy_probe)
         return 0
+    if args.pipeline:
+        return pipeline_experiment(args)
 
     import numpy as np
     import torch

@@ -14,14 +14,17 @@
  *
  * Model. A pipeline owns `slots` buffer sets, each a pinned host input buffer
  * of `input_bytes`, a device input buffer of the same size and a device output
- * buffer of `output_bytes`, and `streams` HIP streams (default priority) on
- * the device current at creation. A producer thread acquires a free slot,
- * writes a batch of images into its host buffer (the decoder's output) and
- * submits it; the submission enqueues, on the next stream in round-robin
- * order, the copy of the batch's bytes to the device, the preprocessing call
- * into the slot's device output, and then the consumer, and returns. A slot
- * becomes free again when all three have completed on the device; acquiring
- * a slot when none is free waits for the oldest submission.
+ * buffer of `output_bytes`, `streams` compute streams and `copy_streams`
+ * copy streams (HIP streams of default priority on the device current at
+ * creation). A producer thread acquires a free slot, writes a batch of
+ * images into its host buffer (the decoder's output) and submits it; the
+ * submission enqueues the copy of the batch's bytes to the device on the
+ * next copy stream, and on the next compute stream (both in round-robin
+ * order) a wait for that copy, the preprocessing call into the slot's device
+ * output and then the consumer, and returns. Copies of later batches thus
+ * run while earlier batches are preprocessed and consumed. A slot becomes
+ * free again when all of its work has completed on the device; acquiring a
+ * slot when none is free waits for the oldest submission.
  *
  * Threading. Every call is thread-safe: any number of producer threads may
  * acquire and submit concurrently (the queue is multi-producer; the streams
@@ -51,9 +54,10 @@ typedef struct smol_pipeline smol_pipeline;
 /* Pipeline sizes.
  *   slots         buffer sets, 1 .. 64 (more than `streams` lets producers
  *                 fill one while the others are in flight)
- *   streams       HIP streams, 1 .. 16
+ *   streams       compute streams, 1 .. 16
  *   input_bytes   bytes of each host / device input buffer, >= 1
  *   output_bytes  bytes of each device output buffer, >= 16
+ *   copy_streams  copy streams, 0 .. 4 (0: one)
  * Device memory held: slots * (input_bytes + output_bytes); pinned host
  * memory: slots * input_bytes. */
 typedef struct smol_pipeline_config {
@@ -61,7 +65,8 @@ typedef struct smol_pipeline_config {
     int32_t streams;
     int64_t input_bytes;
     int64_t output_bytes;
-    int32_t reserved[4];
+    int32_t copy_streams;
+    int32_t reserved[3];  /* must be zero */
 } smol_pipeline_config;
 
 /* The DNN stage, called on the submitting thread right after the

@@ -1,8 +1,9 @@
 // smol_pipeline.cpp -- pipelined ingest: a pool of buffer sets (pinned host
 // input, device input, device output), producer threads that acquire and
-// submit them, and several HIP streams on which each submission's copy,
-// preprocessing and consumer run in order while other streams work on other
-// batches (section 6.1; Eq. 4 is the throughput model this overlap serves).
+// submit them, copy streams that move each batch to the device, and compute
+// streams on which its preprocessing and consumer run once its copy is done,
+// while the copy streams already move later batches (section 6.1; Eq. 4 is
+// the throughput model this overlap serves).
 #include <hip/hip_runtime.h>
 
 #include <condition_variable>
@@ -24,6 +25,7 @@ struct Slot {
     uint8_t *host = nullptr;    // pinned, input_bytes
     uint8_t *dev_in = nullptr;  // input_bytes
     uint8_t *dev_out = nullptr; // output_bytes
+    hipEvent_t copied = nullptr; // after the slot's input copy
     hipEvent_t done = nullptr;  // after the slot's last consumer
     SlotState state = kFree;
     uint64_t seq = 0;           // submission number while in flight
@@ -31,6 +33,7 @@ struct Slot {
 
 constexpr int kMaxSlots = 64;
 constexpr int kMaxStreams = 16;
+constexpr int kMaxCopyStreams = 4;
 
 }  // namespace
 
@@ -38,7 +41,8 @@ struct smol_pipeline {
     int device = 0;
     int64_t input_bytes = 0;
     int64_t output_bytes = 0;
-    std::vector<hipStream_t> streams;
+    std::vector<hipStream_t> streams;       // preprocessing and consumers
+    std::vector<hipStream_t> copy_streams;  // host-to-device copies
     std::vector<Slot> slots;
     std::mutex mu;
     std::condition_variable cv;  // a slot was submitted or released
@@ -58,6 +62,8 @@ void free_all(smol_pipeline *p)
     for (Slot &s : p->slots) {
         if (s.done)
             (void)hipEventDestroy(s.done);
+        if (s.copied)
+            (void)hipEventDestroy(s.copied);
         if (s.host)
             (void)hipHostFree(s.host);
         if (s.dev_in)
@@ -68,8 +74,12 @@ void free_all(smol_pipeline *p)
     for (hipStream_t st : p->streams)
         if (st)
             (void)hipStreamDestroy(st);
+    for (hipStream_t st : p->copy_streams)
+        if (st)
+            (void)hipStreamDestroy(st);
     p->slots.clear();
     p->streams.clear();
+    p->copy_streams.clear();
 }
 
 // Marks completed in-flight slots free. Caller holds p->mu.
@@ -158,7 +168,7 @@ int submit(smol_pipeline *p, int32_t slot, int64_t bytes, int32_t n, const smol_
     if (output_bytes_of(params, n) > p->output_bytes)
         return smol::set_error(SMOL_ERR_INVALID_ARG, "output of %lld bytes exceeds the slot's %lld",
                                (long long)output_bytes_of(params, n), (long long)p->output_bytes);
-    hipStream_t s;
+    hipStream_t s, cs;
     uint64_t seq;
     {
         std::lock_guard<std::mutex> lk(p->mu);
@@ -166,14 +176,27 @@ int submit(smol_pipeline *p, int32_t slot, int64_t bytes, int32_t n, const smol_
             return smol::set_error(SMOL_ERR_INVALID_ARG, "slot %d is not acquired", slot);
         seq = p->next_seq++;
         s = p->streams[seq % p->streams.size()];
+        cs = p->copy_streams[seq % p->copy_streams.size()];
     }
     DeviceGuard dg(p->device);
     if (dg.err != hipSuccess)
         return hip_error(dg.err, "hipSetDevice");
     Slot &sl = p->slots[slot];
-    hipError_t e = hipMemcpyAsync(sl.dev_in, sl.host, (size_t)bytes, hipMemcpyHostToDevice, s);
+    // the copy on a copy stream; the compute stream waits for it
+    hipError_t e = hipMemcpyAsync(sl.dev_in, sl.host, (size_t)bytes, hipMemcpyHostToDevice, cs);
     if (e != hipSuccess)
         return hip_error(e, "hipMemcpyAsync(input)");
+    e = hipEventRecord(sl.copied, cs);
+    if (e == hipSuccess)
+        e = hipStreamWaitEvent(s, sl.copied, 0);
+    if (e != hipSuccess) {
+        // the copy is enqueued: wait for it so that the slot is free again
+        const hipError_t e2 = hipStreamSynchronize(cs);
+        std::lock_guard<std::mutex> lk(p->mu);
+        sl.state = kFree;
+        p->cv.notify_all();
+        return hip_error(e2 != hipSuccess ? e2 : e, "copy event");
+    }
     int rc = pre(sl.dev_in, bytes, sl.dev_out, s);
     std::string msg = rc ? smol_last_error() : "";
     if (!rc && consumer) {
@@ -224,10 +247,13 @@ int smol_pipeline_create(const smol_pipeline_config *c, smol_pipeline **out)
     if (c->streams < 1 || c->streams > kMaxStreams)
         return smol::set_error(SMOL_ERR_INVALID_ARG, "streams %d outside 1..%d", c->streams,
                                kMaxStreams);
+    if (c->copy_streams < 0 || c->copy_streams > kMaxCopyStreams)
+        return smol::set_error(SMOL_ERR_INVALID_ARG, "copy_streams %d outside 0..%d",
+                               c->copy_streams, kMaxCopyStreams);
     if (c->input_bytes < 1 || c->output_bytes < 16)
         return smol::set_error(SMOL_ERR_INVALID_ARG, "input_bytes %lld < 1 or output_bytes %lld "
                                "< 16", (long long)c->input_bytes, (long long)c->output_bytes);
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 3; ++i)
         if (c->reserved[i])
             return smol::set_error(SMOL_ERR_INVALID_ARG, "reserved[%d] is not zero", i);
     smol_pipeline *p = new smol_pipeline();
@@ -236,8 +262,11 @@ int smol_pipeline_create(const smol_pipeline_config *c, smol_pipeline **out)
     hipError_t e = hipGetDevice(&p->device);
     p->slots.resize((size_t)c->slots);
     p->streams.resize((size_t)c->streams, nullptr);
+    p->copy_streams.resize((size_t)(c->copy_streams ? c->copy_streams : 1), nullptr);
     for (int i = 0; e == hipSuccess && i < c->streams; ++i)
         e = hipStreamCreateWithFlags(&p->streams[i], hipStreamNonBlocking);
+    for (int i = 0; e == hipSuccess && i < (int)p->copy_streams.size(); ++i)
+        e = hipStreamCreateWithFlags(&p->copy_streams[i], hipStreamNonBlocking);
     for (int i = 0; e == hipSuccess && i < c->slots; ++i) {
         Slot &s = p->slots[i];
         e = hipHostMalloc((void **)&s.host, (size_t)c->input_bytes, hipHostMallocDefault);
@@ -247,6 +276,8 @@ int smol_pipeline_create(const smol_pipeline_config *c, smol_pipeline **out)
             e = hipMalloc((void **)&s.dev_out, (size_t)c->output_bytes);
         if (e == hipSuccess)
             e = hipEventCreateWithFlags(&s.done, hipEventDisableTiming);
+        if (e == hipSuccess)
+            e = hipEventCreateWithFlags(&s.copied, hipEventDisableTiming);
     }
     if (e != hipSuccess) {
         free_all(p);

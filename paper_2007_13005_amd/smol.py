@@ -82,7 +82,7 @@ class Plan(ctypes.Structure):
 class PipelineConfig(ctypes.Structure):
     _fields_ = [("slots", ctypes.c_int32), ("streams", ctypes.c_int32),
                 ("input_bytes", ctypes.c_int64), ("output_bytes", ctypes.c_int64),
-                ("reserved", ctypes.c_int32 * 4)]
+                ("copy_streams", ctypes.c_int32), ("reserved", ctypes.c_int32 * 3)]
 
 
 class PipelineStats(ctypes.Structure):
@@ -521,15 +521,16 @@ class PreparedCall:
 
 class Pipeline:
     """Pipelined ingest (``include/smol_pipeline.h``): ``slots`` reused buffer
-    sets (pinned host input, device input, device output) and ``streams`` HIP
-    streams. Producer threads ``acquire`` a slot, fill ``host_view(slot)`` with
+    sets (pinned host input, device input, device output), ``streams`` compute
+    streams and ``copy_streams`` copy streams. Producer threads ``acquire`` a slot, fill ``host_view(slot)`` with
     a batch and ``submit`` it; the copy, the preprocessing and the optional
     consumer (a ``CONSUMER`` callback that enqueues the DNN on the given
     stream) run in stream order while other slots are filled."""
 
-    def __init__(self, slots: int, streams: int, input_bytes: int, output_bytes: int):
+    def __init__(self, slots: int, streams: int, input_bytes: int, output_bytes: int,
+                 copy_streams: int = 1):
         cfg = PipelineConfig()
-        cfg.slots, cfg.streams = slots, streams
+        cfg.slots, cfg.streams, cfg.copy_streams = slots, streams, copy_streams
         cfg.input_bytes, cfg.output_bytes = input_bytes, output_bytes
         h = ctypes.c_void_p()
         _check(lib().smol_pipeline_create(ctypes.byref(cfg), ctypes.byref(h)))

@@ -357,6 +357,7 @@ def test_lowres_empty_batch_is_a_no_op():
     (dict(slots=0), "slots"), (dict(slots=65), "slots"), (dict(streams=0), "streams"),
     (dict(streams=17), "streams"), (dict(input_bytes=0), "input_bytes"),
     (dict(output_bytes=8), "output_bytes"), (dict(reserved=1), "reserved"),
+    (dict(copy_streams=5), "copy_streams"), (dict(copy_streams=-1), "copy_streams"),
 ])
 def test_pipeline_config_validation(kw, needle):
     cfg = smol.PipelineConfig()
