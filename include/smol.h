@@ -60,9 +60,11 @@ extern "C" {
 
 /* Output element types. SMOL_OUT_U8 holds the resized value itself, rounded
  * to the nearest integer with ties to even (no normalisation; mean and std
- * are then not used). It runs on the direct kernels only: with it, a forced
- * LDS-staged, register-gather or row-streaming path fails with
- * SMOL_ERR_UNSUPPORTED. */
+ * are then not used). It runs on the row-streaming kernels (contiguous row
+ * order; the row_order knob is ignored) and the direct kernels, and for I420
+ * input on the direct kernel only: with it, a forced LDS-staged or
+ * register-gather path, or a forced row-streaming path for I420 input, fails
+ * with SMOL_ERR_UNSUPPORTED. */
 #define SMOL_OUT_F32 0
 #define SMOL_OUT_F16 1
 #define SMOL_OUT_U8 2

@@ -28,6 +28,8 @@ SOURCES = [
     "smol_rows_rgb_f32_range_nhwc.hip",
     "smol_rows_rgb_f32_stride.hip",
     "smol_rows_rgb_f32_stride_nhwc.hip",
+    "smol_rows_rgb_u8_range.hip",
+    "smol_rows_rgb_u8_range_nhwc.hip",
     "smol_rows_yuv_range.hip",
     "smol_rows_yuv_range_nhwc.hip",
     "smol_rows_yuv_stride.hip",

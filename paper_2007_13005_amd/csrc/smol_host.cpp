@@ -472,8 +472,9 @@ int run_batch(const std::vector<Desc> &descs, size_t first, size_t count, int no
         // then stream neighbouring rows), contiguous ranges otherwise. (Set
         // before the occupancy query: the two walks are different kernels.)
         const int order = g_row_order.load();
-        a.interleave = order == 2 || (order == 0 && uniform && pl.path == smol::PATH_ROWS &&
-                                      a.row_groups >= 4);
+        a.interleave = pl.f16 != SMOL_OUT_U8 &&
+                       (order == 2 || (order == 0 && uniform && pl.path == smol::PATH_ROWS &&
+                                       a.row_groups >= 4));
     }
     if (pl.path == smol::PATH_LDS || pl.path == smol::PATH_GATHER || rows) {
         a.wpg = rows ? smol::kRowsMaxWavesPerGroup : 1;
@@ -727,29 +728,21 @@ static int rgb_batch(const uint8_t *src, int64_t src_bytes, const int64_t *offse
     a.Cw = p->crop_w;
     a.nhwc = o.layout == SMOL_LAYOUT_NHWC;
     fill_norm(p, a);
-    const int f16 = p->out_dtype == SMOL_OUT_F16;
+    // output type: 0 fp32, 1 fp16, 2 uint8 (row-streaming and direct kernels)
+    const int f16 = p->out_dtype;
+    const bool u8 = p->out_dtype == SMOL_OUT_U8;
     smol_plan info = {};
     const int forced = g_path.load();
     if (a.nhwc && (forced == smol::PATH_LDS || forced == smol::PATH_GATHER))
         return fail(SMOL_ERR_UNSUPPORTED, "NHWC output runs on the row-streaming and direct "
                     "kernels only");
+    if (u8 && (forced == smol::PATH_LDS || forced == smol::PATH_GATHER))
+        return fail(SMOL_ERR_UNSUPPORTED, "uint8 output runs on the row-streaming and direct "
+                    "kernels only");
 
     auto direct = [f16](const BatchArgs &x, const Plan &, void *s) {
         return smol::launch_rgb_direct(x, f16, s);
     };
-    if (p->out_dtype == SMOL_OUT_U8) {
-        // uint8 output: the direct kernel only
-        if (forced != smol::PATH_AUTO && forced != smol::PATH_DIRECT)
-            return fail(SMOL_ERR_UNSUPPORTED, "uint8 output runs on the direct kernels only");
-        rc = run_batch(descs, 0, (size_t)n, 1, a, Plan{smol::PATH_DIRECT, 0, 0, 0, 0}, stream,
-                       [](const BatchArgs &x, const Plan &, void *s) {
-                           return smol::launch_rgb_direct(x, SMOL_OUT_U8, s);
-                       },
-                       &info);
-        if (!rc)
-            g_last_plan = info;
-        return rc;
-    }
     // Register-gather path: the gather kernel for runs of images whose windows
     // lie inside src, the direct kernel for the others.
     // Row-streaming path: the row-streaming kernel for runs of images whose
@@ -827,7 +820,7 @@ static int rgb_batch(const uint8_t *src, int64_t src_bytes, const int64_t *offse
         if (hipGetDevice(&device) == hipSuccess && device_info(device, &di) == hipSuccess)
             gather_fits = pg.lds_bytes <= (size_t)di.lds_per_block;
     }
-    if (a.nhwc) {
+    if (a.nhwc || u8) {
         rc = run_batch(descs, 0, (size_t)n, 1, a, Plan{smol::PATH_DIRECT, 0, 0, 0, f16}, stream,
                        direct, &info);
         if (!rc)

@@ -104,6 +104,8 @@ const void *rows_rgb_f32_range(const BatchArgs &a);
 const void *rows_rgb_f32_range_nhwc(const BatchArgs &a);
 const void *rows_rgb_f32_stride(const BatchArgs &a);
 const void *rows_rgb_f32_stride_nhwc(const BatchArgs &a);
+const void *rows_rgb_u8_range(const BatchArgs &a);  // uint8: contiguous ranges only
+const void *rows_rgb_u8_range_nhwc(const BatchArgs &a);
 const void *rows_yuv_range(const BatchArgs &a, int f16);
 const void *rows_yuv_range_nhwc(const BatchArgs &a, int f16);
 const void *rows_yuv_stride(const BatchArgs &a, int f16);

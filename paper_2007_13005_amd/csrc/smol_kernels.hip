@@ -774,8 +774,11 @@ int launch_rgb_gather(const BatchArgs &a, int out_f16, size_t lds_bytes, void *s
     return (int)hipGetLastError();
 }
 
+// f16: the output type, 0 fp32, 1 fp16, 2 uint8 (contiguous ranges only)
 const void *rows_kernel(const BatchArgs &a, int f16)
 {
+    if (f16 == 2)
+        return a.nhwc ? rows_rgb_u8_range_nhwc(a) : rows_rgb_u8_range(a);
     if (a.nhwc)
         return f16 ? (a.interleave ? rows_rgb_f16_stride_nhwc(a) : rows_rgb_f16_range_nhwc(a))
                    : (a.interleave ? rows_rgb_f32_stride_nhwc(a) : rows_rgb_f32_range_nhwc(a));

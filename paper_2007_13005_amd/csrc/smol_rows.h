@@ -171,6 +171,14 @@ __device__ __forceinline__ float normalize_k(const NormK &k, int ch, float v)
     return EXACT ? normalize(v, k.mean[ch], k.stdv[ch], k.rcp[ch]) : (v - k.mean[ch]) * k.rcp[ch];
 }
 
+// The value an output element holds: normalised (fp32 / fp16 output, OUT 0 /
+// 1), or the resized value itself (uint8 output, OUT 2; rounded when packed).
+template <int OUT, int EXACT>
+__device__ __forceinline__ float out_value(const NormK &k, int ch, float v)
+{
+    return OUT == 2 ? v : normalize_k<EXACT>(k, ch, v);
+}
+
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
@@ -504,6 +512,9 @@ __device__ __forceinline__ void read_taps(uint32_t row0, uint32_t row1, const in
 // completion of this row's stores (the compiler cannot count stores among
 // the loads they may overtake, so a wait for a load issued before a store
 // lasts until the store is done as well).
+// A lane's output pairs of one row: per column pair and channel two fp32
+// words (F16 0), one word of two fp16 (F16 1) or the low half-word of one
+// word holding two uint8 (F16 2, uint8 output).
 template <int F16, int J>
 struct RowOut {
     uint32_t w[J][3][F16 ? 1 : 2];
@@ -514,7 +525,12 @@ __device__ __forceinline__ void pack_pair(RowOut<F16, J> &out, int j, const floa
 {
 #pragma unroll
     for (int ch = 0; ch < 3; ++ch) {
-        if (F16 && !EXACT) {
+        if (F16 == 2) {
+            // nearest, ties to even (v_rndne_f32), of a value in [0, 255]
+            const uint32_t b0 = (uint32_t)__builtin_rintf(clamp255(o[ch][0]));
+            const uint32_t b1 = (uint32_t)__builtin_rintf(clamp255(o[ch][1]));
+            out.w[j][ch][0] = b0 | (b1 << 8);
+        } else if (F16 && !EXACT) {
             // The conversion may fuse with the last product (one rounding
             // to fp16 instead of two).
             typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
@@ -535,6 +551,44 @@ template <int F16, int J>
 __device__ __forceinline__ void store_row(uint8_t *orow, long long plane, int Cw, int lane,
                                           const RowOut<F16, J> &out, int nhwc)
 {
+    if constexpr (F16 == 2) {
+        // uint8: a pair is 6 bytes (NHWC) or 2 per plane (NCHW); with Cw even
+        // every pair starts on an even byte, so it goes out as 16-bit stores
+#pragma unroll
+        for (int j = 0; j < J; ++j) {
+            const int c = pair_col(lane, j, Cw);
+            const uint32_t r = out.w[j][0][0], g = out.w[j][1][0], b = out.w[j][2][0];
+            if (nhwc && (Cw & 1) == 0) {
+                uint16_t *dst = (uint16_t *)(orow + 3LL * c);
+                __builtin_nontemporal_store((uint16_t)((r & 0xffu) | ((g & 0xffu) << 8)), dst);
+                __builtin_nontemporal_store((uint16_t)((b & 0xffu) | (r & 0xff00u)), dst + 1);
+                __builtin_nontemporal_store((uint16_t)(((g >> 8) & 0xffu) | (b & 0xff00u)),
+                                            dst + 2);
+            } else if (nhwc) {
+                // odd Cw: pixel c + 1 is the last column again past the end
+                uint8_t *d0 = orow + 3LL * c, *d1 = orow + 3LL * min(c + 1, Cw - 1);
+                d0[0] = (uint8_t)r;
+                d0[1] = (uint8_t)g;
+                d0[2] = (uint8_t)b;
+                d1[0] = (uint8_t)(r >> 8);
+                d1[1] = (uint8_t)(g >> 8);
+                d1[2] = (uint8_t)(b >> 8);
+            } else if ((Cw & 1) == 0) {
+#pragma unroll
+                for (int ch = 0; ch < 3; ++ch)
+                    __builtin_nontemporal_store((uint16_t)out.w[j][ch][0],
+                                                (uint16_t *)(orow + ch * plane + c));
+            } else {
+                const int c1 = min(c + 1, Cw - 1);
+#pragma unroll
+                for (int ch = 0; ch < 3; ++ch) {
+                    orow[ch * plane + c] = (uint8_t)out.w[j][ch][0];
+                    orow[ch * plane + c1] = (uint8_t)(out.w[j][ch][0] >> 8);
+                }
+            }
+        }
+        return;
+    }
     constexpr int kEsz = F16 ? 2 : 4;
     if (nhwc) {
 #pragma unroll
@@ -638,7 +692,7 @@ __device__ __forceinline__ void rows_compute(const NormK &nk, uint32_t row0, uin
             for (int ch = 0; ch < 3; ++ch) {
                 const float top = lerp_ad(pa[ch], pd[ch], cw[j][px]);
                 const float bot = lerp_ad(qa[ch], qd[ch], cw[j][px]);
-                o[ch][px] = normalize_k<EXACT>(nk, ch, lerp(top, bot, wy));
+                o[ch][px] = out_value<F16, EXACT>(nk, ch, lerp(top, bot, wy));
             }
         }
         pack_pair<F16, EXACT, J>(out, j, o);
@@ -677,7 +731,8 @@ __device__ __forceinline__ void rows_vertical(const NormK &nk, const float (&h0)
         for (int px = 0; px < 2; ++px)
 #pragma unroll
             for (int ch = 0; ch < 3; ++ch)
-                o[ch][px] = normalize_k<EXACT>(nk, ch, lerp(h0[j][px][ch], h1[j][px][ch], wy));
+                o[ch][px] = out_value<F16, EXACT>(nk, ch,
+                                                  lerp(h0[j][px][ch], h1[j][px][ch], wy));
         pack_pair<F16, EXACT, J>(out, j, o);
     }
 }
@@ -727,7 +782,7 @@ __global__ void __launch_bounds__(64 * kRowsMaxWavesPerGroup) rgb_rows_kernel(Ba
     if (n_rows <= 0)
         return;
     const RowStep step = row_step_of<STRIDE>(nw, Ch);
-    constexpr int kEsz = F16 ? 2 : 4;
+    constexpr int kEsz = F16 == 2 ? 1 : F16 ? 2 : 4;
     int c_img = (int)(r0 / Ch), c_rr = (int)(r0 - (long long)c_img * Ch);  // row to interpolate
     RowCursor lc;                                                          // next row to load
     cursor_image<STRIDE>(lc, a, c_img, c_rr, step);
@@ -1184,7 +1239,7 @@ yuv_rows_kernel(BatchArgs a)
     if (n_rows <= 0)
         return;
     const RowStep step = row_step_of<STRIDE>(nw, Ch);
-    constexpr int kEsz = F16 ? 2 : 4;
+    constexpr int kEsz = F16 == 2 ? 1 : F16 ? 2 : 4;
     int c_img = (int)(r0 / Ch), c_rr = (int)(r0 - (long long)c_img * Ch);  // row to interpolate
     YuvCursor lc;                                                          // next row to load
     yuv_cursor_image<STRIDE>(lc, a, c_img, c_rr, step);

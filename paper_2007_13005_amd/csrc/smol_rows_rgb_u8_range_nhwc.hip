@@ -1,0 +1,12 @@
+// smol_rows_rgb_u8_range_nhwc.hip -- RGB row-streaming kernels, uint8 output (rounded resized values), contiguous row ranges, NHWC output.
+#include "smol_rows.h"
+
+namespace smol {
+
+// uint8 output is not normalised: the exact and the default normalisation are the same kernel
+const void *rows_rgb_u8_range_nhwc(const BatchArgs &a)
+{
+    return rgb_rows_e<2, 0, 0, 1>(a.col_iters, a.row_groups, a.prefetch);
+}
+
+}  // namespace smol

@@ -303,7 +303,7 @@ def test_left_siting_chroma_footprint():
 
 
 def test_u8_output_refuses_forced_tiled_paths():
-    for path in (smol.PATH_LDS, smol.PATH_GATHER, smol.PATH_ROWS):
+    for path in (smol.PATH_LDS, smol.PATH_GATHER):
         smol.set_tuning(path=path)
         try:
             rc, msg = _rgb_call(params=_params(out_dtype=smol.OUT_U8))

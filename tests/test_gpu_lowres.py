@@ -65,12 +65,28 @@ def _yuv(name, sizes, S, C, dtype, mode=SHORT, layout=NCHW, siting=0, seed=32):
     return wl
 
 
+@pytest.mark.parametrize("C", [(36, 40), (35, 41)], ids=["even", "odd"])
 @pytest.mark.parametrize("layout", [NCHW, NHWC])
-@pytest.mark.parametrize("path", [smol.PATH_AUTO, smol.PATH_DIRECT])
-def test_rgb_u8_short_side_crop(path, layout):
+@pytest.mark.parametrize("path", [smol.PATH_AUTO, smol.PATH_DIRECT, smol.PATH_ROWS])
+def test_rgb_u8_short_side_crop(path, layout, C):
+    """Even crop widths store pixel pairs as 16-bit words, odd ones byte by
+    byte; both kernels that write uint8."""
     smol.set_tuning(path=path)
-    _check(_rgb("u8-short", SIZES[:4], 40, (36, 40), U8, SHORT, layout))
-    assert smol.last_plan()["path"] == smol.PATH_DIRECT
+    _check(_rgb("u8-short", SIZES[:4], 41, C, U8, SHORT, layout))
+    want = smol.PATH_DIRECT if path == smol.PATH_DIRECT else smol.PATH_ROWS
+    assert smol.last_plan()["path"] == want
+
+
+@pytest.mark.parametrize("layout", [NCHW, NHWC])
+def test_rgb_u8_uniform_frames_row_streaming(layout):
+    """A uniform batch of long rows (strided row order for fp16) keeps the
+    contiguous order with uint8 output."""
+    rng = np.random.default_rng(34)
+    batch = rng.integers(0, 256, size=(4, 1080, 1920, 3), dtype=np.uint8)
+    wl = synthetic.uniform_rgb_workload("u8-frames", batch, 161, 161, U8)
+    wl.layout = layout
+    _check(wl)
+    assert smol.last_plan()["path"] == smol.PATH_ROWS
 
 
 @pytest.mark.parametrize("layout", [NCHW, NHWC])
@@ -93,10 +109,17 @@ def test_yuv_u8(layout, siting):
                 siting))
 
 
-def test_u8_forced_rows_path_is_unsupported():
+@pytest.mark.parametrize("path", [smol.PATH_LDS, smol.PATH_GATHER])
+def test_u8_forced_tiled_paths_are_unsupported(path):
+    smol.set_tuning(path=path)
+    with pytest.raises(smol.SmolError):
+        run_gpu(_rgb("u8-tiled", SIZES[:2], 40, 32, U8))
+
+
+def test_yuv_u8_forced_rows_path_is_unsupported():
     smol.set_tuning(path=smol.PATH_ROWS)
     with pytest.raises(smol.SmolError):
-        run_gpu(_rgb("u8-rows", SIZES[:2], 40, 32, U8))
+        run_gpu(_yuv("yuv-u8-rows", [(64, 48)], 24, 20, U8))
 
 
 def _lowres(name, sizes, r, S, C, dtype, seed=33):
