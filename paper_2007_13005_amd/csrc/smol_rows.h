@@ -512,6 +512,11 @@ __device__ __forceinline__ void read_taps(uint32_t row0, uint32_t row1, const in
 // completion of this row's stores (the compiler cannot count stores among
 // the loads they may overtake, so a wait for a load issued before a store
 // lasts until the store is done as well).
+// Output form of a row-streaming kernel instance (its FORM template
+// parameter): NHWC layout, odd crop width.
+constexpr int kFormNhwc = 1;
+constexpr int kFormOdd = 2;
+
 // A lane's output pairs of one row: per column pair and channel two fp32
 // words (F16 0), one word of two fp16 (F16 1) or the low half-word of one
 // word holding two uint8 (F16 2, uint8 output).
@@ -546,8 +551,11 @@ __device__ __forceinline__ void pack_pair(RowOut<F16, J> &out, int j, const floa
 }
 
 // Store a lane's pairs of one output row: three planes (NCHW), or the six
-// interleaved elements of the two pixels (NHWC).
-template <int F16, int J>
+// interleaved elements of the two pixels (NHWC). ODD is Cw & 1, a template
+// parameter so that the stores are straight-line code: the compiler then
+// counts them exactly in the vmcnt waits of the row loop (with a branch here
+// it waits for them as well when it waits for the next rows' loads).
+template <int F16, int J, int ODD>
 __device__ __forceinline__ void store_row(uint8_t *orow, long long plane, int Cw, int lane,
                                           const RowOut<F16, J> &out, int nhwc)
 {
@@ -558,7 +566,7 @@ __device__ __forceinline__ void store_row(uint8_t *orow, long long plane, int Cw
         for (int j = 0; j < J; ++j) {
             const int c = pair_col(lane, j, Cw);
             const uint32_t r = out.w[j][0][0], g = out.w[j][1][0], b = out.w[j][2][0];
-            if (nhwc && (Cw & 1) == 0) {
+            if (nhwc && !ODD) {
                 uint16_t *dst = (uint16_t *)(orow + 3LL * c);
                 __builtin_nontemporal_store((uint16_t)((r & 0xffu) | ((g & 0xffu) << 8)), dst);
                 __builtin_nontemporal_store((uint16_t)((b & 0xffu) | (r & 0xff00u)), dst + 1);
@@ -573,7 +581,7 @@ __device__ __forceinline__ void store_row(uint8_t *orow, long long plane, int Cw
                 d1[0] = (uint8_t)(r >> 8);
                 d1[1] = (uint8_t)(g >> 8);
                 d1[2] = (uint8_t)(b >> 8);
-            } else if ((Cw & 1) == 0) {
+            } else if (!ODD) {
 #pragma unroll
                 for (int ch = 0; ch < 3; ++ch)
                     __builtin_nontemporal_store((uint16_t)out.w[j][ch][0],
@@ -595,7 +603,7 @@ __device__ __forceinline__ void store_row(uint8_t *orow, long long plane, int Cw
         for (int j = 0; j < J; ++j) {
             const int c = pair_col(lane, j, Cw);
             uint8_t *dst = orow + (long long)3 * c * kEsz;
-            if ((Cw & 1) == 0) {
+            if constexpr (!ODD) {
                 // c even: 6 c bytes (fp16) is a multiple of 4, 12 c (fp32) of 8
                 if (F16) {
                     const uint32_t w0 = out.w[j][0][0], w1 = out.w[j][1][0], w2 = out.w[j][2][0];
@@ -635,7 +643,7 @@ __device__ __forceinline__ void store_row(uint8_t *orow, long long plane, int Cw
     for (int j = 0; j < J; ++j) {
         const int c = pair_col(lane, j, Cw);
         const uint32_t lo = (uint32_t)c * kEsz;
-        if ((Cw & 1) == 0) {  // every pair is whole and 2-element aligned
+        if constexpr (!ODD) {  // every pair is whole and 2-element aligned
 #pragma unroll
             for (int ch = 0; ch < 3; ++ch) {
                 uint8_t *dst = orow + ch * plane + lo;
@@ -769,9 +777,11 @@ __device__ __forceinline__ void rows_compute_reuse(const NormK &nk, uint32_t row
     rows_vertical<F16, J, EXACT>(nk, h0, h1, wy, out);
 }
 
-template <int F16, int J, int EXACT, int G, int P, int STRIDE, int NHWC>
+// FORM: bit 0 NHWC output, bit 1 odd crop width (kFormNhwc, kFormOdd).
+template <int F16, int J, int EXACT, int G, int P, int STRIDE, int FORM>
 __global__ void __launch_bounds__(64 * kRowsMaxWavesPerGroup) rgb_rows_kernel(BatchArgs a)
 {
+    constexpr int NHWC = FORM & kFormNhwc, ODD = (FORM & kFormOdd) ? 1 : 0;
     extern __shared__ __attribute__((aligned(16))) uint8_t lds_all[];
     int lane, nw;
     long long r0;
@@ -861,7 +871,7 @@ __global__ void __launch_bounds__(64 * kRowsMaxWavesPerGroup) rgb_rows_kernel(Ba
         advance();                                                                            \
         compute();                                                                            \
         write_rows<G>(lds, NXT, lane);                                                        \
-        store_row<F16, J>(orow, plane, a.Cw, lane, out, NHWC);                              \
+        store_row<F16, J, ODD>(orow, plane, a.Cw, lane, out, NHWC);                         \
         csh0 = NXT.sh0;                                                                       \
         csh1 = NXT.sh1;                                                                       \
         cy0 = NXT.y0;                                                                         \
@@ -904,7 +914,7 @@ __global__ void __launch_bounds__(64 * kRowsMaxWavesPerGroup) rgb_rows_kernel(Ba
     }
 #undef SMOL_ROWS_STEP
     compute();
-    store_row<F16, J>(orow, plane, a.Cw, lane, out, NHWC);
+    store_row<F16, J, ODD>(orow, plane, a.Cw, lane, out, NHWC);
 }
 
 // ---------------------------------------------------------------------------
@@ -1225,10 +1235,12 @@ __device__ __forceinline__ void yuv_compute(const NormK &nk, uint32_t slot, cons
     }
 }
 
-template <int F16, int J, int EXACT, int STRIDE, int NHWC>
+// FORM as for rgb_rows_kernel.
+template <int F16, int J, int EXACT, int STRIDE, int FORM>
 __global__ void __launch_bounds__(64 * kRowsMaxWavesPerGroup) __attribute__((amdgpu_waves_per_eu(J <= 2 ? 3 : 1)))
 yuv_rows_kernel(BatchArgs a)
 {
+    constexpr int NHWC = FORM & kFormNhwc, ODD = (FORM & kFormOdd) ? 1 : 0;
     extern __shared__ __attribute__((aligned(16))) uint8_t lds_all[];
     int lane, nw;
     long long r0;
@@ -1290,7 +1302,7 @@ yuv_rows_kernel(BatchArgs a)
         advance();
         yuv_compute<F16, J, EXACT>(nk, lds0, csh, cwy, cfy0, cfy1, cb0, cols, out);
         yuv_write(lds, R, lane);
-        store_row<F16, J>(orow, plane, a.Cw, lane, out, NHWC);
+        store_row<F16, J, ODD>(orow, plane, a.Cw, lane, out, NHWC);
 #pragma unroll
         for (int s = 0; s < 8; ++s)
             csh[s] = R.sh[s];
@@ -1318,54 +1330,67 @@ yuv_rows_kernel(BatchArgs a)
         }
     }
     yuv_compute<F16, J, EXACT>(nk, lds0, csh, cwy, cfy0, cfy1, cb0, cols, out);
-    store_row<F16, J>(orow, plane, a.Cw, lane, out, NHWC);
+    store_row<F16, J, ODD>(orow, plane, a.Cw, lane, out, NHWC);
 }
 
 
 // Kernel for a plan: output type, arithmetic mode, chunk groups, column
 // pairs per lane and prefetch depth from the launch arguments.
-template <int F16, int EXACT, int G, int STRIDE, int NHWC>
+template <int F16, int EXACT, int G, int STRIDE, int FORM>
 const void *rgb_rows_g(int col_iters, int prefetch)
 {
     if (prefetch == 1)
-        return col_iters <= 1   ? (const void *)rgb_rows_kernel<F16, 1, EXACT, G, 1, STRIDE, NHWC>
-               : col_iters <= 2 ? (const void *)rgb_rows_kernel<F16, 2, EXACT, G, 1, STRIDE, NHWC>
-                                : (const void *)rgb_rows_kernel<F16, 4, EXACT, G, 1, STRIDE, NHWC>;
-    return col_iters <= 1   ? (const void *)rgb_rows_kernel<F16, 1, EXACT, G, 2, STRIDE, NHWC>
-           : col_iters <= 2 ? (const void *)rgb_rows_kernel<F16, 2, EXACT, G, 2, STRIDE, NHWC>
-                            : (const void *)rgb_rows_kernel<F16, 4, EXACT, G, 2, STRIDE, NHWC>;
+        return col_iters <= 1   ? (const void *)rgb_rows_kernel<F16, 1, EXACT, G, 1, STRIDE, FORM>
+               : col_iters <= 2 ? (const void *)rgb_rows_kernel<F16, 2, EXACT, G, 1, STRIDE, FORM>
+                                : (const void *)rgb_rows_kernel<F16, 4, EXACT, G, 1, STRIDE, FORM>;
+    return col_iters <= 1   ? (const void *)rgb_rows_kernel<F16, 1, EXACT, G, 2, STRIDE, FORM>
+           : col_iters <= 2 ? (const void *)rgb_rows_kernel<F16, 2, EXACT, G, 2, STRIDE, FORM>
+                            : (const void *)rgb_rows_kernel<F16, 4, EXACT, G, 2, STRIDE, FORM>;
 }
 
-template <int F16, int EXACT, int STRIDE, int NHWC>
+template <int F16, int EXACT, int STRIDE, int FORM>
 const void *rgb_rows_e(int col_iters, int groups, int prefetch)
 {
-    return groups <= 1   ? rgb_rows_g<F16, EXACT, 1, STRIDE, NHWC>(col_iters, prefetch)
-           : groups <= 2 ? rgb_rows_g<F16, EXACT, 2, STRIDE, NHWC>(col_iters, prefetch)
-                         : rgb_rows_g<F16, EXACT, 4, STRIDE, NHWC>(col_iters, prefetch);
+    return groups <= 1   ? rgb_rows_g<F16, EXACT, 1, STRIDE, FORM>(col_iters, prefetch)
+           : groups <= 2 ? rgb_rows_g<F16, EXACT, 2, STRIDE, FORM>(col_iters, prefetch)
+                         : rgb_rows_g<F16, EXACT, 4, STRIDE, FORM>(col_iters, prefetch);
+}
+
+// The crop width's parity picks the FORM of a layout.
+template <int F16, int EXACT, int STRIDE, int NHWC>
+const void *rgb_rows_f(const BatchArgs &a)
+{
+    return (a.Cw & 1) ? rgb_rows_e<F16, EXACT, STRIDE, NHWC | kFormOdd>(a.col_iters, a.row_groups,
+                                                                       a.prefetch)
+                      : rgb_rows_e<F16, EXACT, STRIDE, NHWC>(a.col_iters, a.row_groups, a.prefetch);
 }
 
 template <int F16, int STRIDE, int NHWC>
 const void *rgb_rows_table(const BatchArgs &a)
 {
-    return a.exact ? rgb_rows_e<F16, 1, STRIDE, NHWC>(a.col_iters, a.row_groups, a.prefetch)
-                   : rgb_rows_e<F16, 0, STRIDE, NHWC>(a.col_iters, a.row_groups, a.prefetch);
+    return a.exact ? rgb_rows_f<F16, 1, STRIDE, NHWC>(a) : rgb_rows_f<F16, 0, STRIDE, NHWC>(a);
+}
+
+template <int F16, int EXACT, int STRIDE, int FORM>
+const void *yuv_rows_e(int col_iters)
+{
+    return col_iters <= 1   ? (const void *)yuv_rows_kernel<F16, 1, EXACT, STRIDE, FORM>
+           : col_iters <= 2 ? (const void *)yuv_rows_kernel<F16, 2, EXACT, STRIDE, FORM>
+                            : (const void *)yuv_rows_kernel<F16, 4, EXACT, STRIDE, FORM>;
 }
 
 template <int F16, int EXACT, int STRIDE, int NHWC>
-const void *yuv_rows_e(int col_iters)
+const void *yuv_rows_f(const BatchArgs &a)
 {
-    return col_iters <= 1   ? (const void *)yuv_rows_kernel<F16, 1, EXACT, STRIDE, NHWC>
-           : col_iters <= 2 ? (const void *)yuv_rows_kernel<F16, 2, EXACT, STRIDE, NHWC>
-                            : (const void *)yuv_rows_kernel<F16, 4, EXACT, STRIDE, NHWC>;
+    return (a.Cw & 1) ? yuv_rows_e<F16, EXACT, STRIDE, NHWC | kFormOdd>(a.col_iters)
+                      : yuv_rows_e<F16, EXACT, STRIDE, NHWC>(a.col_iters);
 }
 
 template <int STRIDE, int NHWC>
 const void *yuv_rows_table(const BatchArgs &a, int f16)
 {
-    return f16 ? (a.exact ? yuv_rows_e<1, 1, STRIDE, NHWC>(a.col_iters)
-                          : yuv_rows_e<1, 0, STRIDE, NHWC>(a.col_iters))
-               : (a.exact ? yuv_rows_e<0, 1, STRIDE, NHWC>(a.col_iters)
-                          : yuv_rows_e<0, 0, STRIDE, NHWC>(a.col_iters));
+    return f16 ? (a.exact ? yuv_rows_f<1, 1, STRIDE, NHWC>(a) : yuv_rows_f<1, 0, STRIDE, NHWC>(a))
+               : (a.exact ? yuv_rows_f<0, 1, STRIDE, NHWC>(a) : yuv_rows_f<0, 0, STRIDE, NHWC>(a));
 }
 
 }  // namespace

@@ -6,7 +6,7 @@ namespace smol {
 // uint8 output is not normalised: the exact and the default normalisation are the same kernel
 const void *rows_rgb_u8_range(const BatchArgs &a)
 {
-    return rgb_rows_e<2, 0, 0, 0>(a.col_iters, a.row_groups, a.prefetch);
+    return rgb_rows_f<2, 0, 0, 0>(a);
 }
 
 }  // namespace smol
