@@ -50,6 +50,7 @@ def parse():
     ap.add_argument("--wg-per-cu", type=int, default=0, help="tuning override (0: automatic)")
     ap.add_argument("--lds-budget", type=int, default=0, help="tuning override (0: automatic)")
     ap.add_argument("--row-order", type=int, default=0, help="tuning override (0: automatic)")
+    ap.add_argument("--upload", type=int, default=0, help="tuning override (0: automatic)")
     ap.add_argument("--profile-run", action="store_true",
                     help="no CPU baseline, fewer prints: for runs under rocprofv3")
     ap.add_argument("--pipeline", action="store_true",
@@ -516,9 +517,11 @@ def main() -> int:
     algo = algorithmic_bytes(wl, smol)
     out_bytes = wl.n * 3 * wl.crop_h * wl.crop_w * wl.out_elem_bytes
     rotate = args.rotate or max(2, -(-2 * MALL_BYTES // algo))
-    if args.band_rows or args.path or args.wg_per_cu or args.lds_budget or args.row_order:
+    if (args.band_rows or args.path or args.wg_per_cu or args.lds_budget or args.row_order or
+            args.upload):
         smol.set_tuning(path=args.path, band_rows=args.band_rows, lds_budget=args.lds_budget,
-                        workgroups_per_cu=args.wg_per_cu, row_order=args.row_order)
+                        workgroups_per_cu=args.wg_per_cu, row_order=args.row_order,
+                        upload=args.upload)
 
     src0 = torch.from_numpy(wl.src).to(dev)
     srcs = [src0] + [src0.clone() for _ in range(rotate - 1)]

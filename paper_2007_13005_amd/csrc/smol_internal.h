@@ -77,6 +77,9 @@ int set_error(int code, const char *fmt, ...);
 void clear_error();
 
 // Launchers (smol_kernels.hip). Return a hipError_t as int.
+// Copies `bytes` (a multiple of 16) from src to dst with a small kernel on
+// `stream` (src may be pinned host memory as the device addresses it).
+int launch_table_copy(const void *src, void *dst, size_t bytes, void *stream);
 // Direct kernels: out_type 0 fp32, 1 fp16, 2 uint8 (rounded, not normalised).
 int launch_rgb_direct(const BatchArgs &a, int out_type, void *stream);
 int launch_rgb_lds(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream);

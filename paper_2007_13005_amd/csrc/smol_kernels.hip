@@ -25,6 +25,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
 #include <map>
 #include <mutex>
 #include <tuple>
@@ -721,6 +722,16 @@ __global__ void __launch_bounds__(kThreads) yuv_direct_kernel(BatchArgs a)
     }
 }
 
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// A ragged batch's descriptor table, 16 bytes per thread, from the pinned
+// staging slot (read over the bus) to device memory.
+__global__ void __launch_bounds__(kThreads) table_copy_kernel(const u32x4 *src, u32x4 *dst, int n)
+{
+    for (int i = blockIdx.x * kThreads + threadIdx.x; i < n; i += gridDim.x * kThreads)
+        dst[i] = src[i];
+}
+
 // Direct kernels: a workgroup per output row, 64 to 256 threads (whole
 // waves covering the crop's width where it is narrower than 256), at most
 // 2^20 workgroups looping over the rows.
@@ -738,6 +749,15 @@ dim3 direct_block(const BatchArgs &a)
 }
 
 }  // namespace
+
+int launch_table_copy(const void *src, void *dst, size_t bytes, void *stream)
+{
+    const int n = (int)(bytes / 16);
+    const dim3 grid((unsigned)std::min(64, (n + kThreads - 1) / kThreads)), block(kThreads);
+    hipLaunchKernelGGL(table_copy_kernel, grid, block, 0, (hipStream_t)stream,
+                       (const u32x4 *)src, (u32x4 *)dst, n);
+    return (int)hipGetLastError();
+}
 
 int launch_rgb_direct(const BatchArgs &a, int out_type, void *stream)
 {

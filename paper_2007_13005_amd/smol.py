@@ -66,7 +66,7 @@ class Tuning(ctypes.Structure):
     _fields_ = [("path", ctypes.c_int32), ("band_rows", ctypes.c_int32),
                 ("lds_budget", ctypes.c_int32), ("workgroups_per_cu", ctypes.c_int32),
                 ("exact", ctypes.c_int32), ("row_order", ctypes.c_int32),
-                ("reserved", ctypes.c_int32 * 2)]
+                ("upload", ctypes.c_int32), ("reserved", ctypes.c_int32 * 1)]
 
 
 class Plan(ctypes.Structure):
@@ -259,8 +259,9 @@ def image_geometry(width: int, height: int, params: Params, yuv420: bool = False
 
 
 def set_tuning(path: int = 0, band_rows: int = 0, lds_budget: int = 0,
-               workgroups_per_cu: int = 0, exact: int = 0, row_order: int = 0) -> None:
-    t = Tuning(path, band_rows, lds_budget, workgroups_per_cu, exact, row_order)
+               workgroups_per_cu: int = 0, exact: int = 0, row_order: int = 0,
+               upload: int = 0) -> None:
+    t = Tuning(path, band_rows, lds_budget, workgroups_per_cu, exact, row_order, upload)
     _check(lib().smol_set_tuning(ctypes.byref(t)))
 
 

@@ -171,4 +171,7 @@ def test_lowres_c7_full():
     """The augmentation workload at the size the benchmark runs."""
     wl = synthetic.c7()
     _check(wl)
-    assert smol.last_plan()["launches"] == 2
+    # the reduction (descriptor copy kernel, row-streaming kernel, and the
+    # direct kernel for an image whose staged rows would cross the end of
+    # src), then the second step
+    assert smol.last_plan()["launches"] in (3, 4)

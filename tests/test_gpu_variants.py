@@ -173,3 +173,18 @@ def test_detection_crops_c6_small():
 def test_detection_crops_c6_full():
     """The detection-crop workload at the size the benchmark runs."""
     _check(synthetic.c6())
+
+
+@pytest.mark.parametrize("upload", [0, 1, 2])
+def test_descriptor_upload_paths(upload):
+    """Both ways a ragged table reaches the device (DMA on the copy stream, or
+    the copy kernel on the caller's stream) give the oracle's results, over
+    more calls than the staging ring has slots."""
+    smol.set_tuning(upload=upload)
+    wl = synthetic.c6(n=24)
+    ref = run_oracle(wl)
+    for _ in range(20):
+        got = run_gpu(wl)
+        assert_parity(got, ref, wl.out_dtype, f"c6 upload={upload}")
+    assert smol.last_plan()["uploaded_descriptors"] == 1
+    assert smol.last_plan()["launches"] == (1 if upload == 1 else 2)
