@@ -150,6 +150,14 @@ def _load():
     lib.smol_ref_lowres_preprocess_image.restype = ctypes.c_int
     lib.smol_ref_yuv420_lowres_preprocess_image.argtypes = [P, P, P] + [I32] * 6 + [P, P, I32, P]
     lib.smol_ref_yuv420_lowres_preprocess_image.restype = ctypes.c_int
+    lib.oracle_idct_block.argtypes = [P, P, P, I64, I32, I32]
+    lib.oracle_idct_block.restype = None
+    lib.oracle_jpeg_coef_count.argtypes = [I32, I32]
+    lib.oracle_jpeg_coef_count.restype = I64
+    lib.oracle_jpeg_mcu_rect.argtypes = [I32] * 6 + [P]
+    lib.oracle_jpeg_mcu_rect.restype = ctypes.c_int
+    lib.oracle_jpeg_decode_i420.argtypes = [P, P, P, I32, I32, P, P, P, P]
+    lib.oracle_jpeg_decode_i420.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -476,3 +484,53 @@ def yuv420_lowres_preprocess_image_into(y_ptr: int, cb_ptr: int, cr_ptr: int, W:
     return _load().smol_ref_yuv420_lowres_preprocess_image(y_ptr, cb_ptr, cr_ptr, W, H, r, S, Ch,
                                                            Cw, mean.ctypes.data, std.ctypes.data,
                                                            out_dtype, out_ptr)
+
+
+# --------------------------------------------------------------------------
+# partial JPEG decoding (section 6.4, "ROI decoding", Algorithm 1)
+# --------------------------------------------------------------------------
+
+
+def idct_block(coef, q) -> np.ndarray:
+    """One 8 x 8 block of int16 coefficients (natural order) dequantised by q
+    (uint16), inverse-DCT'd, level-shifted, rounded and clamped: uint8 8 x 8."""
+    c = np.ascontiguousarray(coef, np.int16).reshape(64)
+    qq = np.ascontiguousarray(q, np.uint16).reshape(64)
+    out = np.empty((8, 8), np.uint8)
+    _load().oracle_idct_block(c.ctypes.data, qq.ctypes.data, out.ctypes.data, 8, 8, 8)
+    return out
+
+
+def jpeg_coef_count(W: int, H: int) -> int:
+    """int16 coefficients of one W x H 4:2:0 frame (MCU-padded block grid)."""
+    return int(_load().oracle_jpeg_coef_count(W, H))
+
+
+def jpeg_mcu_rect(W: int, H: int, S: int, Ch: int, Cw: int,
+                  resize_mode: int = RESIZE_SHORT_CROP) -> tuple[int, int, int, int]:
+    """Algorithm 1's MCU-aligned rectangle (x, y, w, h) for a W x H frame."""
+    r = np.zeros(4, np.int32)
+    if _load().oracle_jpeg_mcu_rect(W, H, S, Ch, Cw, resize_mode, r.ctypes.data) != 0:
+        raise ValueError("oracle rejected the arguments")
+    return tuple(int(v) for v in r)
+
+
+def jpeg_decode_i420(coef, qy, qc, W: int, H: int, rect=None, fill: int | None = None):
+    """Decode the blocks of a frame that meet ``rect`` (None: all) into
+    full-size I420 planes (y, cb, cr); pixels outside stay ``fill`` (or
+    uninitialised when None)."""
+    c = np.ascontiguousarray(coef, np.int16).reshape(-1)
+    assert c.size == jpeg_coef_count(W, H)
+    qy = np.ascontiguousarray(qy, np.uint16).reshape(64)
+    qc = np.ascontiguousarray(qc, np.uint16).reshape(64)
+    Wc, Hc = (W + 1) // 2, (H + 1) // 2
+    mk = (lambda shape: np.full(shape, fill, np.uint8)) if fill is not None else (
+        lambda shape: np.empty(shape, np.uint8))
+    y, cb, cr = mk((H, W)), mk((Hc, Wc)), mk((Hc, Wc))
+    r = None if rect is None else np.ascontiguousarray(rect, np.int32)
+    rc = _load().oracle_jpeg_decode_i420(c.ctypes.data, qy.ctypes.data, qc.ctypes.data, W, H,
+                                         None if r is None else r.ctypes.data, y.ctypes.data,
+                                         cb.ctypes.data, cr.ctypes.data)
+    if rc != 0:
+        raise ValueError("oracle rejected the arguments")
+    return y, cb, cr

@@ -650,3 +650,149 @@ int smol_ref_yuv420_lowres_preprocess_batch(const uint8_t *src, int64_t src_byte
     }
     return ORACLE_OK;
 }
+
+/* ------------------------------------------------------------------------- */
+/* Partial JPEG decoding (section 6.4, "ROI decoding", Algorithm 1)          */
+/* ------------------------------------------------------------------------- */
+/*
+ * Readings (none of this is fixed by the paper, which relies on a decoder
+ * library):
+ *   - the decoder's output is baseline JPEG 4:2:0: 16 x 16 luma MCUs, each
+ *     holding four luma and one Cb and one Cr 8 x 8 block; the entropy
+ *     decoding (Huffman, zig-zag) happens on the CPU and is not modelled:
+ *     the input is the dequantisation's input, int16 coefficients per block
+ *     in natural order (row v = vertical frequency, column u), blocks in
+ *     raster order over the MCU-padded frame, luma then Cb then Cr;
+ *   - dequantisation multiplies by the table entry; the inverse DCT is
+ *     ITU-T T.81's A.3.3 formula, evaluated in fp32 as two 1-D passes
+ *     (horizontal frequencies first), each sum over the frequency index in
+ *     increasing order, every product and sum rounded on its own, with the
+ *     table c[k][n] = C(k)/2 cos((2n+1) k pi / 16) (C(0) = 1/sqrt(2), else 1)
+ *     formed in double and rounded once to fp32; then + 128, rounded to
+ *     nearest (ties to even) and clamped to 0..255;
+ *   - Algorithm 1's rectangle: the smallest MCU-aligned rectangle holding
+ *     every luma and chroma sample the resize taps read (the algorithm's
+ *     scale = min(h, w) / 224 is replaced by the exact tap footprint, as for
+ *     the crop itself), clipped to the frame.
+ */
+
+static void jpeg_idct_table(float c[64])
+{
+    const double pi = 3.14159265358979323846;
+    for (int k = 0; k < 8; ++k)
+        for (int n = 0; n < 8; ++n) {
+            double ck = k == 0 ? 1.0 / sqrt(2.0) : 1.0;
+            c[k * 8 + n] = (float)(ck / 2.0 * cos((2.0 * n + 1.0) * k * pi / 16.0));
+        }
+}
+
+/* One block: coef[v*8+u] times q[v*8+u], inverse DCT, level shift, round,
+ * clamp; the w x h top-left pixels (w, h <= 8) are written to out (row
+ * pitch `pitch` bytes). */
+void oracle_idct_block(const int16_t *coef, const uint16_t *q, uint8_t *out, int64_t pitch,
+                       int32_t w, int32_t h)
+{
+    float c[64], d[64], g[64];
+    jpeg_idct_table(c);
+    for (int i = 0; i < 64; ++i)
+        d[i] = (float)((int32_t)coef[i] * (int32_t)q[i]); /* exact: |.| < 2^24 */
+    for (int v = 0; v < 8; ++v) /* horizontal pass: row v of frequencies */
+        for (int x = 0; x < 8; ++x) {
+            float s = 0.0f;
+            for (int u = 0; u < 8; ++u)
+                s = s + c[u * 8 + x] * d[v * 8 + u];
+            g[v * 8 + x] = s;
+        }
+    for (int y = 0; y < h; ++y) /* vertical pass */
+        for (int x = 0; x < w; ++x) {
+            float s = 0.0f;
+            for (int v = 0; v < 8; ++v)
+                s = s + c[v * 8 + y] * g[v * 8 + x];
+            out[y * pitch + x] = round_u8(s + 128.0f);
+        }
+}
+
+/* Blocks of the MCU-padded frame: luma bw x bh, chroma bw/2 x bh/2 each. */
+static void jpeg_grid(int64_t W, int64_t H, int64_t *bw, int64_t *bh)
+{
+    *bw = 2 * ((W + 15) / 16);
+    *bh = 2 * ((H + 15) / 16);
+}
+
+/* Coefficients (int16 elements) of one frame. */
+int64_t oracle_jpeg_coef_count(int32_t W, int32_t H)
+{
+    int64_t bw, bh;
+    jpeg_grid(W, H, &bw, &bh);
+    return 64 * (bw * bh + 2 * (bw / 2) * (bh / 2));
+}
+
+/* The MCU-aligned rectangle (x, y, w, h in luma pixels) holding every sample
+ * the resize of a W x H I420 frame reads (centred chroma), for the short-side
+ * crop or direct resize of `mode`. */
+int oracle_jpeg_mcu_rect(int32_t W, int32_t H, int32_t S, int32_t Ch, int32_t Cw, int32_t mode,
+                         int32_t *rect)
+{
+    if (!params_ok_ex(W, H, S, Ch, Cw, ORACLE_OUT_F32, mode, ORACLE_NCHW))
+        return ORACLE_ERR;
+    int64_t Wr, Hr, left, top, a, b, xf, xl, yf, yl, c0, c1, d0, d1;
+    float w;
+    oracle_output_geometry(W, H, S, Ch, Cw, mode, &Wr, &Hr, &left, &top);
+    oracle_axis_tap(left, W, Wr, &xf, &a, &w);
+    oracle_axis_tap(left + Cw - 1, W, Wr, &b, &xl, &w);
+    oracle_axis_tap(top, H, Hr, &yf, &a, &w);
+    oracle_axis_tap(top + Ch - 1, H, Hr, &b, &yl, &w);
+    /* chroma samples of the first and last luma columns / rows, in luma units */
+    chroma_tap(xf, (W + 1) / 2, &c0, &a, &w);
+    chroma_tap(xl, (W + 1) / 2, &b, &c1, &w);
+    chroma_tap(yf, (H + 1) / 2, &d0, &a, &w);
+    chroma_tap(yl, (H + 1) / 2, &b, &d1, &w);
+    int64_t x0 = xf < 2 * c0 ? xf : 2 * c0, x1 = xl > 2 * c1 + 1 ? xl : 2 * c1 + 1;
+    int64_t y0 = yf < 2 * d0 ? yf : 2 * d0, y1 = yl > 2 * d1 + 1 ? yl : 2 * d1 + 1;
+    x0 = x0 / 16 * 16;
+    y0 = y0 / 16 * 16;
+    x1 = (x1 / 16 + 1) * 16;
+    y1 = (y1 / 16 + 1) * 16;
+    rect[0] = (int32_t)x0;
+    rect[1] = (int32_t)y0;
+    rect[2] = (int32_t)((x1 < W ? x1 : W) - x0);
+    rect[3] = (int32_t)((y1 < H ? y1 : H) - y0);
+    return ORACLE_OK;
+}
+
+/* Decode the blocks of a W x H frame that meet `rect` (x, y, w, h; NULL: the
+ * whole frame) into full-size I420 planes (Y W x H, Cb and Cr ceil(W/2) x
+ * ceil(H/2), tightly pitched); pixels of other blocks are left untouched. */
+int oracle_jpeg_decode_i420(const int16_t *coef, const uint16_t *qy, const uint16_t *qc,
+                            int32_t W, int32_t H, const int32_t *rect, uint8_t *yp, uint8_t *cbp,
+                            uint8_t *crp)
+{
+    if (W < 1 || H < 1)
+        return ORACLE_ERR;
+    int64_t bw, bh;
+    jpeg_grid(W, H, &bw, &bh);
+    int64_t rx = rect ? rect[0] : 0, ry = rect ? rect[1] : 0;
+    int64_t rw = rect ? rect[2] : W, rh = rect ? rect[3] : H;
+    if (rx < 0 || ry < 0 || rw < 1 || rh < 1 || rx + rw > W || ry + rh > H)
+        return ORACLE_ERR;
+    const int64_t Wc = (W + 1) / 2, Hc = (H + 1) / 2;
+    /* luma blocks */
+    for (int64_t by = ry / 8; by <= (ry + rh - 1) / 8; ++by)
+        for (int64_t bx = rx / 8; bx <= (rx + rw - 1) / 8; ++bx) {
+            int32_t w = (int32_t)(W - 8 * bx < 8 ? W - 8 * bx : 8);
+            int32_t h = (int32_t)(H - 8 * by < 8 ? H - 8 * by : 8);
+            oracle_idct_block(coef + 64 * (by * bw + bx), qy, yp + 8 * by * W + 8 * bx, W, w, h);
+        }
+    /* chroma blocks: the chroma samples of the rectangle's luma columns */
+    const int64_t cx0 = rx / 2, cx1 = (rx + rw - 1) / 2, cy0 = ry / 2, cy1 = (ry + rh - 1) / 2;
+    const int16_t *cb = coef + 64 * bw * bh, *cr = cb + 64 * (bw / 2) * (bh / 2);
+    for (int64_t by = cy0 / 8; by <= cy1 / 8; ++by)
+        for (int64_t bx = cx0 / 8; bx <= cx1 / 8; ++bx) {
+            int32_t w = (int32_t)(Wc - 8 * bx < 8 ? Wc - 8 * bx : 8);
+            int32_t h = (int32_t)(Hc - 8 * by < 8 ? Hc - 8 * by : 8);
+            int64_t k = by * (bw / 2) + bx;
+            oracle_idct_block(cb + 64 * k, qc, cbp + 8 * by * Wc + 8 * bx, Wc, w, h);
+            oracle_idct_block(cr + 64 * k, qc, crp + 8 * by * Wc + 8 * bx, Wc, w, h);
+        }
+    return ORACLE_OK;
+}
