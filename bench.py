@@ -39,7 +39,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=400)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--config", default="c4", choices=["c1", "c2", "c3", "c4", "c5", "c6", "c7"])
+    ap.add_argument("--config", default="c4", choices=["c1", "c2", "c3", "c4", "c5", "c6", "c7", "c8"])
     ap.add_argument("--rotate", type=int, default=0,
                     help="input/output sets cycled through (0: enough to defeat the MALL)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
@@ -95,10 +95,33 @@ def synthetic_u8() -> int:
     return synthetic.OUT_U8
 
 
+def jpeg_algorithmic_bytes(wl, smol) -> int:
+    """Partial decoding, then the I420 preprocessing: for every frame the
+    coefficient blocks of its MCU rectangle (128 bytes each) read and their
+    pixels inside the frame written, then what the preprocessing reads of
+    them and its output."""
+    import math
+    p = smol.make_params(wl.resize_short, wl.crop_h, wl.crop_w, wl.mean, wl.std, wl.out_dtype)
+    o = smol.make_options(wl.resize_mode, wl.layout, 0)
+    total, cache = 0, {}
+    for w, h in zip(wl.widths.tolist(), wl.heights.tolist()):
+        if (w, h) not in cache:
+            x, y, rw, rh = smol.jpeg_mcu_rect(w, h, p, o)
+            luma = math.ceil(rw / 8) * math.ceil(rh / 8)
+            chroma = math.ceil(math.ceil(rw / 2) / 8) * math.ceil(math.ceil(rh / 2) / 8)
+            written = rw * rh + 2 * ((rw + 1) // 2) * ((rh + 1) // 2)
+            g = smol.image_geometry_ex(w, h, p, yuv420=True, options=o)
+            cache[(w, h)] = 128 * (luma + 2 * chroma) + written + _read_bytes(g, "yuv420")
+        total += cache[(w, h)]
+    return total + wl.n * 3 * wl.crop_h * wl.crop_w * wl.out_elem_bytes
+
+
 def algorithmic_bytes(wl, smol) -> int:
     """Bytes the method must move per batch: for every image the source rows
     its vertical taps read times the crop's source column span (per plane for
     I420), plus the output."""
+    if wl.kind == "jpeg":
+        return jpeg_algorithmic_bytes(wl, smol)
     if wl.low_res:
         return lowres_algorithmic_bytes(wl, smol)
     p = smol.make_params(wl.resize_short, wl.crop_h, wl.crop_w, wl.mean, wl.std, wl.out_dtype)
@@ -137,7 +160,21 @@ def cpu_baseline(wl, seconds: float, threads: int) -> dict:
 
     def one(i: int, t: int) -> None:
         o = outs[t].ctypes.data
-        if wl.low_res:
+        if wl.kind == "jpeg":
+            # the oracle's partial decode of the frame's rectangle, then its
+            # I420 preprocessing
+            W, H = int(wl.widths[i]), int(wl.heights[i])
+            rect = oracle.jpeg_mcu_rect(W, H, wl.resize_short, wl.crop_h, wl.crop_w,
+                                        wl.resize_mode)
+            k = oracle.jpeg_coef_count(W, H)
+            c0 = int(wl.coef_offsets[i])
+            y, cb, cr = oracle.jpeg_decode_i420(wl.src.view(np.int16)[c0:c0 + k], wl.qtables[0],
+                                                wl.qtables[1], W, H, rect)
+            rc = oracle.yuv420_preprocess_image_ex_into(
+                y.ctypes.data, cb.ctypes.data, cr.ctypes.data, W, H, (0, 0, W, H),
+                wl.resize_short, wl.crop_h, wl.crop_w, mean, std, wl.out_dtype, wl.resize_mode,
+                wl.layout, oracle.CHROMA_CENTER, o)
+        elif wl.low_res:
             W, H = int(wl.widths[i]), int(wl.heights[i])
             if wl.kind == "rgb":
                 pitch = 3 * W if wl.pitches is None else int(wl.pitches[i])

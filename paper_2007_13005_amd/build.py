@@ -36,6 +36,8 @@ SOURCES = [
     "smol_rows_yuv_stride_nhwc.hip",
     "smol_host.cpp",
     "smol_pipeline.cpp",
+    "smol_jpeg_kernels.hip",
+    "smol_jpeg.cpp",
 ]
 HEADERS = ["smol_internal.h", "smol_device.h", "smol_rows.h"]
 

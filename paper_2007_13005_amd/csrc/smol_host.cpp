@@ -1323,3 +1323,39 @@ int smol::set_error(int code, const char *fmt, ...)
 }
 
 void smol::clear_error() { g_last_error.clear(); }
+
+int smol::mcu_rect(int64_t W, int64_t H, const smol_params *p, int resize_mode, int32_t rect[4])
+{
+    Geo g;
+    int rc = image_geo(W, H, p, resize_mode, &g, 0);
+    if (rc)
+        return rc;
+    int64_t xf, xl, yf, yl, a, b, c0, c1, d0, d1;
+    tap_index(g.left, W, g.Wr, &xf, &a);
+    tap_index(g.left + p->crop_w - 1, W, g.Wr, &b, &xl);
+    tap_index(g.top, H, g.Hr, &yf, &a);
+    tap_index(g.top + p->crop_h - 1, H, g.Hr, &b, &yl);
+    // the chroma samples of the first and last luma column and row (centred
+    // siting), as luma columns and rows
+    chroma_index(xf, (W + 1) / 2, &c0, &a);
+    chroma_index(xl, (W + 1) / 2, &a, &c1);
+    chroma_index(yf, (H + 1) / 2, &d0, &a);
+    chroma_index(yl, (H + 1) / 2, &a, &d1);
+    const int64_t x0 = std::min(xf, 2 * c0) / 16 * 16, y0 = std::min(yf, 2 * d0) / 16 * 16;
+    const int64_t x1 = (std::max(xl, 2 * c1 + 1) / 16 + 1) * 16;
+    const int64_t y1 = (std::max(yl, 2 * d1 + 1) / 16 + 1) * 16;
+    rect[0] = (int32_t)x0;
+    rect[1] = (int32_t)y0;
+    rect[2] = (int32_t)(std::min(x1, W) - x0);
+    rect[3] = (int32_t)(std::min(y1, H) - y0);
+    return SMOL_OK;
+}
+
+int smol::device_cus()
+{
+    int device = 0;
+    DeviceInfo di;
+    if (hipGetDevice(&device) != hipSuccess || device_info(device, &di) != hipSuccess)
+        return 0;
+    return di.cus;
+}

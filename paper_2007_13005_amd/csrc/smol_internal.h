@@ -4,6 +4,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "smol.h"
+
 namespace smol {
 
 // Per-image descriptor, 80 bytes. For RGB input off[0] is the byte offset of
@@ -70,6 +72,33 @@ constexpr int kRowsMaxColIters = 4;
 constexpr int kRowsMaxGroups = 4;
 // Waves per workgroup of the row-streaming kernels (each wave independent).
 constexpr int kRowsMaxWavesPerGroup = 4;
+
+// Block decoding of a group of 4:2:0 frames of one geometry (smol_jpeg_kernels.hip):
+// frame f's coefficients at coef + f * coef_stride (int16 elements; luma
+// blocks bw x bh, then Cb and Cr (bw/2) x (bh/2), 64 each, natural order),
+// its planes at out + f * out_stride + yoff / cboff / croff (W x H and
+// Wc x Hc, tightly pitched). Blocks lbx0 .. lbx0 + lnbx - 1 (and rows) of
+// luma and cbx0 .. of chroma are decoded.
+struct JpegArgs {
+    const int16_t *coef;
+    long long coef_stride;
+    uint8_t *out;
+    long long out_stride, yoff, cboff, croff;
+    int32_t W, H, Wc, Hc, bw, bh;
+    int32_t lbx0, lby0, lnbx, lnby, cbx0, cby0, cnbx, cnby;
+    int32_t frames;
+    int32_t q[2][64];  // luma, chroma dequantisation
+    float c[64];       // c[k * 8 + n] = fp32(C(k)/2 cos((2n + 1) k pi / 16))
+};
+int launch_jpeg_idct(const JpegArgs &a, int grid, void *stream);
+
+// The MCU-aligned rectangle (x, y, w, h) holding every luma and chroma sample
+// the preprocessing of a W x H 4:2:0 frame reads (smol_host.cpp). Returns a
+// status; fails as the batch calls would on these parameters.
+int mcu_rect(int64_t W, int64_t H, const smol_params *p, int resize_mode, int32_t rect[4]);
+
+// Device compute units (0 when unknown).
+int device_cus();
 
 // The calling thread's smol_last_error() message (smol_host.cpp): set_error
 // formats it and returns `code`; clear_error empties it.

@@ -143,6 +143,17 @@ SIGNATURES = {
                                                    ctypes.POINTER(Options), CONSUMER, _vp]),
     "smol_pipeline_drain": (ctypes.c_int, [_vp]),
     "smol_pipeline_get_stats": (ctypes.c_int, [_vp, ctypes.POINTER(PipelineStats)]),
+    "smol_jpeg_coef_count": (ctypes.c_int64, [ctypes.c_int32, ctypes.c_int32]),
+    "smol_jpeg_mcu_rect": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(Params),
+                                          ctypes.POINTER(Options), _vp]),
+    "smol_jpeg_decode_i420": (ctypes.c_int, [_vp, ctypes.c_int64, _vp, _vp, _vp, _vp, _vp,
+                                             ctypes.c_int32, _vp, ctypes.c_int64, _vp, _vp, _vp,
+                                             _vp]),
+    "smol_jpeg_workspace_bytes": (ctypes.c_int64, [ctypes.c_int32, _vp, _vp]),
+    "smol_jpeg_roi_preprocess_batch": (ctypes.c_int, [_vp, ctypes.c_int64, _vp, _vp, _vp, _vp,
+                                                      ctypes.c_int32, ctypes.POINTER(Params),
+                                                      ctypes.POINTER(Options), _vp,
+                                                      ctypes.c_int64, _vp, _vp]),
     "smol_set_tuning": (ctypes.c_int, [ctypes.POINTER(Tuning)]),
     "smol_last_plan": (ctypes.c_int, [ctypes.POINTER(Plan)]),
     "smol_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -440,6 +451,82 @@ def yuv420_lowres_preprocess_batch(src, y_offsets, cb_offsets, cr_offsets, width
     return out
 
 
+def jpeg_coef_count(width: int, height: int) -> int:
+    return int(lib().smol_jpeg_coef_count(width, height))
+
+
+def jpeg_mcu_rect(width: int, height: int, params: Params,
+                  options: Options | None = None) -> tuple[int, int, int, int]:
+    """Algorithm 1's MCU-aligned rectangle (x, y, w, h) for one frame."""
+    r = np.zeros(4, np.int32)
+    _check(lib().smol_jpeg_mcu_rect(width, height, ctypes.byref(params),
+                                    None if options is None else ctypes.byref(options),
+                                    r.ctypes.data))
+    return tuple(int(v) for v in r)
+
+
+def _qtables(qtables) -> np.ndarray:
+    q = _table(qtables, np.uint16).reshape(-1)
+    if q.size != 128:
+        raise ValueError("qtables must hold 2 x 64 entries (luma, chroma)")
+    return q
+
+
+def jpeg_decode_i420(coef, coef_offsets, qtables, widths, heights, out, y_offsets, cb_offsets,
+                     cr_offsets, rects=None, stream=None):
+    """Decode the blocks of each frame meeting its rectangle (``rects`` (n, 4)
+    or None for whole frames) from the int16 device tensor ``coef`` into the
+    uint8 device tensor ``out`` at the given plane offsets."""
+    if coef.dtype.itemsize != 2 or not coef.is_cuda or not coef.is_contiguous():
+        raise ValueError("coef must be a contiguous int16 device tensor")
+    if out.dtype.itemsize != 1 or not out.is_cuda or not out.is_contiguous():
+        raise ValueError("out must be a contiguous uint8 device tensor")
+    co = _table(coef_offsets, np.int64)
+    w, h = _table(widths, np.int32), _table(heights, np.int32)
+    yo, bo, ro = (_table(v, np.int64) for v in (y_offsets, cb_offsets, cr_offsets))
+    n = len(co)
+    r = None if rects is None else _rois(rects, n)
+    q = _qtables(qtables)
+    _check(lib().smol_jpeg_decode_i420(
+        coef.data_ptr(), coef.numel(), co.ctypes.data, q.ctypes.data, w.ctypes.data,
+        h.ctypes.data, None if r is None else r.ctypes.data, n, out.data_ptr(), out.numel(),
+        yo.ctypes.data, bo.ctypes.data, ro.ctypes.data, _stream_handle(stream)))
+
+
+def jpeg_workspace_bytes(widths, heights) -> int:
+    w, h = _table(widths, np.int32), _table(heights, np.int32)
+    return int(lib().smol_jpeg_workspace_bytes(len(w), w.ctypes.data, h.ctypes.data))
+
+
+def jpeg_roi_preprocess_batch(coef, coef_offsets, qtables, widths, heights, params: Params,
+                              options: Options | None = None, workspace=None, out=None,
+                              stream=None):
+    """Algorithm 1 end to end: only each frame's MCU rectangle decoded (into
+    ``workspace``, allocated if omitted), then the I420 preprocessing."""
+    import torch
+    if coef.dtype.itemsize != 2 or not coef.is_cuda or not coef.is_contiguous():
+        raise ValueError("coef must be a contiguous int16 device tensor")
+    co = _table(coef_offsets, np.int64)
+    w, h = _table(widths, np.int32), _table(heights, np.int32)
+    n = len(co)
+    q = _qtables(qtables)
+    need = jpeg_workspace_bytes(w, h)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=coef.device)
+    out = _out_tensor(out, n, params, coef.device, options.layout if options else LAYOUT_NCHW)
+    _check(lib().smol_jpeg_roi_preprocess_batch(
+        coef.data_ptr(), coef.numel(), co.ctypes.data, q.ctypes.data, w.ctypes.data,
+        h.ctypes.data, n, ctypes.byref(params),
+        None if options is None else ctypes.byref(options), workspace.data_ptr(),
+        workspace.numel(), out.data_ptr(), _stream_handle(stream)))
+    return out
+
+
+def torch_int16():
+    import torch
+    return torch.int16
+
+
 def _workload_options(wl) -> Options | None:
     if not wl.variant:
         return None
@@ -449,6 +536,9 @@ def _workload_options(wl) -> Options | None:
 def run_workload(wl, src_dev, out=None, stream=None):
     """Run a ``synthetic.Workload`` whose ``src`` already sits on the device."""
     p = make_params(wl.resize_short, wl.crop_h, wl.crop_w, wl.mean, wl.std, wl.out_dtype)
+    if wl.kind == "jpeg":
+        return jpeg_roi_preprocess_batch(src_dev.view(torch_int16()), wl.coef_offsets, wl.qtables, wl.widths,
+                                         wl.heights, p, _workload_options(wl), None, out, stream)
     if wl.low_res:
         if wl.variant:
             raise ValueError("the low-resolution augmentation takes no ROI or options")
@@ -479,6 +569,19 @@ class PreparedCall:
         self.options = _workload_options(wl)
         ex = self.options is not None
         self._low = None
+        self._jpeg = None
+        if wl.kind == "jpeg":
+            import torch
+            tabs = [_table(wl.coef_offsets, np.int64), _qtables(wl.qtables),
+                    _table(wl.widths, np.int32), _table(wl.heights, np.int32)]
+            ws = torch.empty(max(jpeg_workspace_bytes(wl.widths, wl.heights), 16),
+                             dtype=torch.uint8, device="cuda")
+            self._keep = tabs
+            self._jpeg = ([t.ctypes.data for t in tabs], ws, ws.data_ptr(), ws.numel())
+            self._fn = lib().smol_jpeg_roi_preprocess_batch
+            self._pref = ctypes.byref(self.params)
+            self._tail = [ctypes.byref(self.options)] if ex else [None]
+            return
         if wl.low_res:
             if ex:
                 raise ValueError("the low-resolution augmentation takes no ROI or options")
@@ -511,6 +614,11 @@ class PreparedCall:
         self._tail = [ctypes.byref(self.options)] if ex else []
 
     def __call__(self, src_ptr: int, src_bytes: int, out_ptr: int, stream_handle) -> None:
+        if self._jpeg:
+            args, _, ws, ws_bytes = self._jpeg
+            _check(self._fn(src_ptr, src_bytes // 2, *args, self.n, self._pref, *self._tail, ws,
+                            ws_bytes, out_ptr, stream_handle))
+            return
         if self._low:
             low, _, ws, ws_bytes = self._low
             _check(self._fn(src_ptr, src_bytes, *self._args, self.n, low, self._pref, ws,

@@ -21,6 +21,10 @@ seeded stand-ins reproduce their shapes, size mix and value ranges:
   c6  256 regions of interest (64..512 px boxes) in 16 1080p RGB frames,
       resized directly to 112x112, channels-last fp16 (detection / face crops,
       the ROI use of section 6.4)
+  c8  128 JPEG-coded 1280x720 4:2:0 frames as entropy-decoded coefficient
+      blocks (smooth DC field, Laplacian AC falling with frequency, synthetic
+      quantisation tables); only Algorithm 1's MCU rectangle is decoded,
+      then short side 256, crop 224, fp16 out (section 6.4, ROI decoding)
   c7  256 ragged RGB as c2, low-resolution augmentation: reduced to 161x161
       (the thumbnail size of section 5.2) then upsampled to 224x224 (short
       side 224, crop 224), fp16 out (the training augmentation of section 5.3)
@@ -79,6 +83,10 @@ class Workload:
     # low-resolution augmentation: each image first reduced to low_res x
     # low_res (0: off)
     low_res: int = 0
+    # kind "jpeg": src holds the int16 coefficients' bytes; frame i's start at
+    # element coef_offsets[i]; qtables (2, 64) uint16, luma then chroma
+    coef_offsets: np.ndarray | None = None
+    qtables: np.ndarray | None = None
 
     @property
     def variant(self) -> bool:
@@ -280,7 +288,58 @@ def c7(n: int = 256, low_res: int = 161) -> Workload:
     return wl
 
 
-CONFIGS = {"c1": c1, "c2": c2, "c3": c3, "c4": c4, "c5": c5, "c6": c6, "c7": c7}
+def jpeg_qtables() -> np.ndarray:
+    """Synthetic dequantisation tables (luma, chroma): coarser with frequency."""
+    u = np.arange(8)
+    f = u[None, :] + u[:, None]
+    return np.stack([2 + 2 * f, 3 + 3 * f]).reshape(2, 64).astype(np.uint16)
+
+
+def jpeg_coefficients(rng, W: int, H: int, q: np.ndarray) -> np.ndarray:
+    """Entropy-decoded coefficients of one W x H 4:2:0 frame (MCU-padded block
+    grid, luma then Cb then Cr, 64 per block in natural order): a smooth DC
+    field plus Laplacian AC terms whose scale falls with frequency, quantised
+    by the tables."""
+    bw, bh = 2 * ((W + 15) // 16), 2 * ((H + 15) // 16)
+    u = np.arange(8)
+    f = (u[None, :] + u[:, None]).reshape(64)
+    out = []
+    for comp, (gw, gh) in enumerate([(bw, bh), (bw // 2, bh // 2), (bw // 2, bh // 2)]):
+        qt = q[0 if comp == 0 else 1].astype(np.float64)
+        yy, xx = np.mgrid[0:gh, 0:gw].astype(np.float64)
+        a, b, ph = rng.uniform(0.02, 0.2, 2), rng.uniform(0.02, 0.2, 2), rng.uniform(0, 6.3, 2)
+        level = 128 + 70 * np.sin(a[0] * xx + b[0] * yy + ph[0]) * np.cos(a[1] * xx - b[1] * yy + ph[1])
+        blocks = rng.laplace(0.0, 1.0, size=(gh * gw, 64)) * (40.0 / (1.0 + f))[None, :]
+        blocks[:, 0] = (level.reshape(-1) - 128) * 8
+        out.append(np.rint(blocks / qt[None, :]).astype(np.int16).reshape(-1))
+    return np.concatenate(out)
+
+
+def jpeg_workload(name: str, sizes, S: int, C: int | tuple[int, int], out_dtype: int, seed: int,
+                  description: str = "") -> Workload:
+    """Frames of the given (W, H) sizes as coefficient blocks, packed."""
+    rng = np.random.default_rng(seed)
+    ch, cw = (C, C) if isinstance(C, int) else C
+    q = jpeg_qtables()
+    coefs = [jpeg_coefficients(rng, int(w), int(h), q) for w, h in sizes]
+    offs = np.cumsum([0] + [c.size for c in coefs[:-1]]).astype(np.int64)
+    coef = np.concatenate(coefs)
+    return Workload(name=name, kind="jpeg", src=coef.view(np.uint8),
+                    widths=np.asarray([w for w, _ in sizes], np.int32),
+                    heights=np.asarray([h for _, h in sizes], np.int32), resize_short=S,
+                    crop_h=ch, crop_w=cw, out_dtype=out_dtype, coef_offsets=offs, qtables=q,
+                    description=description)
+
+
+def c8(n: int = 128, height: int = 720, width: int = 1280) -> Workload:
+    return jpeg_workload("c8", [(width, height)] * n, 256, 224, OUT_F16, SEED_BASE + 8,
+                         f"{n} JPEG-coded {width}x{height} 4:2:0 frames as entropy-decoded "
+                         "coefficient blocks; only the MCU rectangle of the crop decoded "
+                         "(dequantisation, 8x8 inverse DCT), then short side 256, center crop "
+                         "224x224, NCHW fp16")
+
+
+CONFIGS = {"c1": c1, "c2": c2, "c3": c3, "c4": c4, "c5": c5, "c6": c6, "c7": c7, "c8": c8}
 
 
 def make(name: str, **kw) -> Workload:

@@ -24,7 +24,31 @@ def note(msg: str) -> None:
     sys.stdout.flush()
 
 
+def jpeg_planes(wl: synthetic.Workload):
+    """The oracle's whole-frame decode of a jpeg workload as a packed I420
+    batch: (flat buffer, y, cb, cr offsets)."""
+    coef = wl.src.view(np.int16)
+    bufs, yo, bo, ro, cur = [], [], [], [], 0
+    for i in range(wl.n):
+        W, H = int(wl.widths[i]), int(wl.heights[i])
+        k = oracle.jpeg_coef_count(W, H)
+        c = coef[int(wl.coef_offsets[i]):int(wl.coef_offsets[i]) + k]
+        y, cb, cr = oracle.jpeg_decode_i420(c, wl.qtables[0], wl.qtables[1], W, H)
+        yo.append(cur)
+        bo.append(cur + y.size)
+        ro.append(cur + y.size + cb.size)
+        cur += y.size + cb.size + cr.size
+        bufs += [y.reshape(-1), cb.reshape(-1), cr.reshape(-1)]
+    return np.concatenate(bufs), yo, bo, ro
+
+
 def run_oracle(wl: synthetic.Workload) -> np.ndarray:
+    if wl.kind == "jpeg":
+        flat, yo, bo, ro = jpeg_planes(wl)
+        return oracle.yuv420_preprocess_batch_ex(flat, yo, bo, ro, wl.widths, wl.heights, None,
+                                                 wl.resize_short, wl.crop_h, wl.crop_w, wl.mean,
+                                                 wl.std, wl.out_dtype, wl.resize_mode, wl.layout,
+                                                 oracle.CHROMA_CENTER)
     if wl.low_res:
         if wl.kind == "rgb":
             return oracle.lowres_preprocess_batch(wl.src, wl.offsets, wl.widths, wl.heights,

@@ -387,3 +387,42 @@ def test_pipeline_null_handles_are_rejected():
     p = smol.make_params(256, 224, 224, MEAN, STD, smol.OUT_F16)
     assert lib.smol_pipeline_submit(None, 0, 1, None, None, None, None, None, 0, ctypes.byref(p),
                                     None, smol.CONSUMER(), None) == smol.ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("W,H,S,C,mode", [(1920, 1080, 224, 224, 0), (1280, 720, 256, 224, 0),
+                                          (641, 359, 128, 112, 0), (17, 33, 16, 8, 0),
+                                          (640, 480, 1, 96, 1), (1000, 200, 300, 150, 0)])
+def test_jpeg_mcu_rect_matches_oracle(W, H, S, C, mode):
+    p = smol.make_params(S, C, C, MEAN, STD, smol.OUT_F16)
+    o = smol.make_options(resize_mode=mode)
+    assert smol.jpeg_mcu_rect(W, H, p, o) == oracle.jpeg_mcu_rect(W, H, S, C, C, mode)
+
+
+def test_jpeg_sizes_match_oracle():
+    for W, H in [(1, 1), (16, 16), (17, 33), (1920, 1080)]:
+        assert smol.jpeg_coef_count(W, H) == oracle.jpeg_coef_count(W, H)
+    w, h = [3, 16], [5, 16]
+    assert smol.jpeg_workspace_bytes(w, h) == ((15 + 2 * 2 * 3 + 256 + 2 * 64 + 15) // 16) * 16 + 16
+
+
+def _jpeg_decode_call(qt=None, rect=(0, 0, 16, 16), out_bytes=16 * 16 + 2 * 64, n=1):
+    q = np.ones(128, np.uint16) if qt is None else np.asarray(qt, np.uint16)
+    w = np.asarray([16], np.int32)
+    z = np.zeros(1, np.int64)
+    r = np.asarray(rect, np.int32)
+    rc = smol.lib().smol_jpeg_decode_i420(FAKE_SRC, 10**6, z.ctypes.data, q.ctypes.data,
+                                          w.ctypes.data, w.ctypes.data, r.ctypes.data, n,
+                                          FAKE_OUT, out_bytes, z.ctypes.data,
+                                          np.asarray([256], np.int64).ctypes.data,
+                                          np.asarray([320], np.int64).ctypes.data, None)
+    return rc, smol.lib().smol_last_error().decode()
+
+
+@pytest.mark.parametrize("kw,needle", [
+    (dict(qt=[0] + [1] * 127), "table entry"), (dict(qt=[1] * 127 + [256]), "table entry"),
+    (dict(rect=(1, 0, 8, 8)), "odd origin"), (dict(rect=(0, 0, 17, 16)), "rectangle"),
+    (dict(out_bytes=383), "outside out"), (dict(n=-1), "n = -1"),
+])
+def test_jpeg_decode_validation(kw, needle):
+    rc, msg = _jpeg_decode_call(**kw)
+    assert rc == smol.ERR_INVALID_ARG and needle in msg, (rc, msg)
