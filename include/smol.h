@@ -320,8 +320,8 @@ int smol_image_geometry_ex(int32_t width, int32_t height, int32_t yuv420, const 
  *               0: automatic (RGB: row-streaming when it fits, else
  *               register-gather when its tables fit, else LDS-staged when
  *               the span fits, else direct; I420: row-streaming when the
- *               crop is at most 512 columns and the luma and chroma spans at
- *               most 992 bytes, else direct). For I420 only 0, 1 and 4 are
+ *               crop is at most 512 columns, the luma span at most 2016
+ *               bytes and the chroma span at most 992, else direct). For I420 only 0, 1 and 4 are
  *               valid; 4 fails with SMOL_ERR_UNSUPPORTED past those limits
  *   band_rows   output rows per band in the LDS-staged kernels (1..64); for
  *               the row-streaming kernel, 1 or 2 sets how many output rows

@@ -991,18 +991,20 @@ static int yuv_batch(const uint8_t *src, int64_t src_bytes, const int64_t *y_off
             g_last_plan = info;
         return rc;
     }
-    // Row-streaming kernel: staged luma and chroma rows of at most 1 KiB
-    // (span + 32 bytes), crops up to 512 columns; frames whose planes' chunks
-    // cross an end of src go to the direct kernel.
-    const bool rows_ok = p->crop_w <= 128 * smol::kRowsMaxColIters && max_yspan + 32 <= 1024 &&
+    // Row-streaming kernel: staged luma rows of at most 2 KiB and chroma rows
+    // of at most 1 KiB (span + 32 bytes), crops up to 512 columns; frames
+    // whose planes' chunks cross an end of src go to the direct kernel.
+    const bool rows_ok = p->crop_w <= 128 * smol::kRowsMaxColIters && max_yspan + 32 <= 2048 &&
                          max_cspan + 32 <= 1024;
     if (forced == smol::PATH_ROWS && !rows_ok)
         return fail(SMOL_ERR_UNSUPPORTED, "row-streaming I420 path forced but the crop is wider "
-                    "than %d columns or a source span exceeds 992 bytes",
+                    "than %d columns, the luma span exceeds 2016 bytes or the chroma span 992",
                     128 * smol::kRowsMaxColIters);
     if (rows_ok && (forced == smol::PATH_ROWS || forced == smol::PATH_AUTO)) {
         a.col_iters = p->crop_w <= 128 ? 1 : p->crop_w <= 256 ? 2 : 4;
-        const Plan pr{smol::PATH_YUV_ROWS, 0, 8 * 1024, 0, f16};
+        // luma segments of 1 or 2 KiB, six chroma segments of 1 KiB per wave
+        a.row_groups = max_yspan + 32 <= 1024 ? 1 : 2;
+        const Plan pr{smol::PATH_YUV_ROWS, 0, (size_t)(2 * a.row_groups + 6) * 1024, 0, f16};
         auto rows = [f16](const BatchArgs &x, const Plan &q, void *s) {
             return smol::launch_yuv_rows(x, f16, q.lds_bytes, s);
         };

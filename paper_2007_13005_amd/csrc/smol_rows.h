@@ -996,9 +996,13 @@ __device__ __forceinline__ YuvImg yuv_img(const BatchArgs &a, int img)
 // Cb r2, Cr r0, Cr r1, Cr r2 (r0, r1: the chroma rows of y0; r2: the second
 // chroma row of y1), with each segment's offset in its first chunk, the luma
 // vertical weight, the chroma vertical weights of y0 and y1, and which of r0,
-// r1 is y1's first chroma row.
+// r1 is y1's first chroma row. A lane holds one 16-byte chunk of each
+// segment, and with GL = 2 a second chunk of each luma segment (luma rows of
+// up to 2 KiB).
+template <int GL>
 struct YuvStaged {
     u32x4 c[8];
+    u32x4 c2[2];  // second luma chunks (GL = 2)
     int sh[8];
     float wy;
     int fy0, fy1;  // vertical chroma weights of luma rows y0, y1, in quarters
@@ -1071,7 +1075,17 @@ __device__ __forceinline__ void yuv_cursor_next(YuvCursor &c, const BatchArgs &a
     }
 }
 
-__device__ __forceinline__ void yuv_load(YuvStaged &st, const YuvCursor &c, int lane, bool repeat)
+// LDS layout of a wave's slot: luma segments of 1 KiB * GL, then the six
+// chroma segments of 1 KiB.
+template <int GL>
+__device__ __forceinline__ constexpr uint32_t yuv_seg(int s)
+{
+    return s < 2 ? 1024u * GL * (uint32_t)s : 2048u * GL + 1024u * (uint32_t)(s - 2);
+}
+
+template <int GL>
+__device__ __forceinline__ void yuv_load(YuvStaged<GL> &st, const YuvCursor &c, int lane,
+                                         bool repeat)
 {
     int y0, y1;
     vcursor_tap(c.v, y0, y1, st.wy);
@@ -1092,14 +1106,22 @@ __device__ __forceinline__ void yuv_load(YuvStaged &st, const YuvCursor &c, int 
         GlobalByte *p = (GlobalByte *)(row[s] - (uintptr_t)st.sh[s]);
         st.c[s] = __builtin_nontemporal_load(
             (const __attribute__((address_space(1))) u32x4 *)(p + 16u * (uint32_t)min(lane, last)));
+        if (GL == 2 && s < 2)
+            st.c2[s] = __builtin_nontemporal_load(
+                (const __attribute__((address_space(1))) u32x4 *)(p + 16u * (uint32_t)min(64 + lane,
+                                                                                           last)));
     }
 }
 
-__device__ __forceinline__ void yuv_write(uint8_t *slot, const YuvStaged &st, int lane)
+template <int GL>
+__device__ __forceinline__ void yuv_write(uint8_t *slot, const YuvStaged<GL> &st, int lane)
 {
 #pragma unroll
-    for (int s = 0; s < 8; ++s)
-        ((u32x4 *)(slot + 1024 * s))[lane] = st.c[s];
+    for (int s = 0; s < 8; ++s) {
+        ((u32x4 *)(slot + yuv_seg<GL>(s)))[lane] = st.c[s];
+        if (GL == 2 && s < 2)
+            ((u32x4 *)(slot + yuv_seg<GL>(s)))[64 + lane] = st.c2[s];
+    }
 }
 
 // Per-lane column taps of the I420 kernel.
@@ -1181,7 +1203,7 @@ __device__ __forceinline__ float chroma16(uint32_t ra, uint32_t rb, uint32_t sel
     return (float)(int)__builtin_amdgcn_udot4(smp, wts, (uint32_t)-2048, false);
 }
 
-template <int F16, int J, int EXACT>
+template <int F16, int J, int EXACT, int GL>
 __device__ __forceinline__ void yuv_compute(const NormK &nk, uint32_t slot, const int (&sh)[8],
                                             float wy, int fy0, int fy1, int b0,
                                             const YuvCols<J> &k, RowOut<F16, J> &out)
@@ -1198,7 +1220,7 @@ __device__ __forceinline__ void yuv_compute(const NormK &nk, uint32_t slot, cons
             uint32_t A[8], q[8];
 #pragma unroll
             for (int s = 0; s < 8; ++s)
-                A[s] = slot + 1024u * s + (uint32_t)sh[s] +
+                A[s] = slot + yuv_seg<GL>(s) + (uint32_t)sh[s] +
                        (uint32_t)(s < 2 ? k.ox[j][px] : k.oc[j][px]);
             lds_read_quads<8>(A, q);
             // 16 * (chroma - 128) at (y0, y1) x (x0, x1) for both planes:
@@ -1235,8 +1257,9 @@ __device__ __forceinline__ void yuv_compute(const NormK &nk, uint32_t slot, cons
     }
 }
 
-// FORM as for rgb_rows_kernel.
-template <int F16, int J, int EXACT, int STRIDE, int FORM>
+// FORM as for rgb_rows_kernel; GL: chunks per lane of a luma segment (staged
+// luma rows of up to 1 or 2 KiB).
+template <int F16, int J, int EXACT, int STRIDE, int FORM, int GL>
 __global__ void __launch_bounds__(64 * kRowsMaxWavesPerGroup) __attribute__((amdgpu_waves_per_eu(J <= 2 ? 3 : 1)))
 yuv_rows_kernel(BatchArgs a)
 {
@@ -1246,8 +1269,8 @@ yuv_rows_kernel(BatchArgs a)
     long long r0;
     int n_rows;
     const int Ch = a.Ch;
-    uint8_t *const lds = rows_wave<STRIDE>(lds_all, 8192, (long long)a.n * Ch, lane, nw, r0,
-                                           n_rows);
+    uint8_t *const lds = rows_wave<STRIDE>(lds_all, yuv_seg<GL>(8), (long long)a.n * Ch, lane,
+                                           nw, r0, n_rows);
     if (n_rows <= 0)
         return;
     const RowStep step = row_step_of<STRIDE>(nw, Ch);
@@ -1286,10 +1309,10 @@ yuv_rows_kernel(BatchArgs a)
     };
     const long long plane = (long long)Ch * a.Cw * kEsz;
     RowOut<F16, J> out;
-    YuvStaged R;
-    yuv_load(R, lc, lane, false);
+    YuvStaged<GL> R;
+    yuv_load<GL>(R, lc, lane, false);
     advance();
-    yuv_write(lds, R, lane);
+    yuv_write<GL>(lds, R, lane);
     int csh[8];
 #pragma unroll
     for (int s = 0; s < 8; ++s)
@@ -1298,10 +1321,10 @@ yuv_rows_kernel(BatchArgs a)
     int cfy0 = R.fy0, cfy1 = R.fy1;
     int cb0 = R.b0;
     for (int left = n_rows - 1; left > 0; --left) {
-        yuv_load(R, lc, lane, false);
+        yuv_load<GL>(R, lc, lane, false);
         advance();
-        yuv_compute<F16, J, EXACT>(nk, lds0, csh, cwy, cfy0, cfy1, cb0, cols, out);
-        yuv_write(lds, R, lane);
+        yuv_compute<F16, J, EXACT, GL>(nk, lds0, csh, cwy, cfy0, cfy1, cb0, cols, out);
+        yuv_write<GL>(lds, R, lane);
         store_row<F16, J, ODD>(orow, plane, a.Cw, lane, out, NHWC);
 #pragma unroll
         for (int s = 0; s < 8; ++s)
@@ -1329,7 +1352,7 @@ yuv_rows_kernel(BatchArgs a)
             }
         }
     }
-    yuv_compute<F16, J, EXACT>(nk, lds0, csh, cwy, cfy0, cfy1, cb0, cols, out);
+    yuv_compute<F16, J, EXACT, GL>(nk, lds0, csh, cwy, cfy0, cfy1, cb0, cols, out);
     store_row<F16, J, ODD>(orow, plane, a.Cw, lane, out, NHWC);
 }
 
@@ -1371,19 +1394,27 @@ const void *rgb_rows_table(const BatchArgs &a)
     return a.exact ? rgb_rows_f<F16, 1, STRIDE, NHWC>(a) : rgb_rows_f<F16, 0, STRIDE, NHWC>(a);
 }
 
-template <int F16, int EXACT, int STRIDE, int FORM>
-const void *yuv_rows_e(int col_iters)
+template <int F16, int EXACT, int STRIDE, int FORM, int GL>
+const void *yuv_rows_g(int col_iters)
 {
-    return col_iters <= 1   ? (const void *)yuv_rows_kernel<F16, 1, EXACT, STRIDE, FORM>
-           : col_iters <= 2 ? (const void *)yuv_rows_kernel<F16, 2, EXACT, STRIDE, FORM>
-                            : (const void *)yuv_rows_kernel<F16, 4, EXACT, STRIDE, FORM>;
+    return col_iters <= 1   ? (const void *)yuv_rows_kernel<F16, 1, EXACT, STRIDE, FORM, GL>
+           : col_iters <= 2 ? (const void *)yuv_rows_kernel<F16, 2, EXACT, STRIDE, FORM, GL>
+                            : (const void *)yuv_rows_kernel<F16, 4, EXACT, STRIDE, FORM, GL>;
+}
+
+// a.row_groups: KiB per staged luma row, 1 or 2
+template <int F16, int EXACT, int STRIDE, int FORM>
+const void *yuv_rows_e(const BatchArgs &a)
+{
+    return a.row_groups >= 2 ? yuv_rows_g<F16, EXACT, STRIDE, FORM, 2>(a.col_iters)
+                             : yuv_rows_g<F16, EXACT, STRIDE, FORM, 1>(a.col_iters);
 }
 
 template <int F16, int EXACT, int STRIDE, int NHWC>
 const void *yuv_rows_f(const BatchArgs &a)
 {
-    return (a.Cw & 1) ? yuv_rows_e<F16, EXACT, STRIDE, NHWC | kFormOdd>(a.col_iters)
-                      : yuv_rows_e<F16, EXACT, STRIDE, NHWC>(a.col_iters);
+    return (a.Cw & 1) ? yuv_rows_e<F16, EXACT, STRIDE, NHWC | kFormOdd>(a)
+                      : yuv_rows_e<F16, EXACT, STRIDE, NHWC>(a);
 }
 
 template <int STRIDE, int NHWC>

@@ -402,15 +402,25 @@ def test_yuv_frame_at_end_of_src_first_in_batch(path):
 
 
 def test_yuv_wide_span_uses_direct_kernel():
-    """A luma span past 992 bytes: forced row streaming is refused, the
+    """A luma span past 2016 bytes: forced row streaming is refused, the
     automatic plan uses the direct kernel."""
-    wl = _yuv("wide", [(4000, 200)], 80, (2, 400), F32, seed=10)
+    wl = _yuv("wide", [(12000, 100)], 20, (2, 450), F32, seed=10)
     smol.set_tuning(path=smol.PATH_ROWS)
     with pytest.raises(smol.SmolError):
         run_gpu(wl)
     smol.set_tuning(path=smol.PATH_AUTO)
     _check(wl)
     assert smol.last_plan()["path"] == smol.PATH_DIRECT
+
+
+@pytest.mark.parametrize("dtype", [F32, F16])
+def test_yuv_long_luma_rows_stream(dtype):
+    """1080p frames at short side 224: luma spans of 1,078 bytes take the
+    row-streaming kernel's two-chunk luma segments (and spans of 992 to 2016
+    bytes in general, here also a ragged second frame)."""
+    wl = _yuv("hd", [(1920, 1080), (1500, 900)], 224, 224, dtype, seed=12)
+    _check(wl)
+    assert smol.last_plan()["path"] == smol.PATH_ROWS
 
 
 def test_yuv_neutral_chroma_equals_rgb_path_on_gpu():
