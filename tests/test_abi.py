@@ -426,3 +426,29 @@ def _jpeg_decode_call(qt=None, rect=(0, 0, 16, 16), out_bytes=16 * 16 + 2 * 64, 
 def test_jpeg_decode_validation(kw, needle):
     rc, msg = _jpeg_decode_call(**kw)
     assert rc == smol.ERR_INVALID_ARG and needle in msg, (rc, msg)
+
+
+def _jpeg_roi_call(opts=None, ws=FAKE_OUT + 4096, ws_bytes=None, params=None):
+    p = params or smol.make_params(32, 24, 24, MEAN, STD, smol.OUT_F16)
+    w = np.asarray([64], np.int32)
+    h = np.asarray([48], np.int32)
+    q = np.ones(128, np.uint16)
+    z = np.zeros(1, np.int64)
+    need = smol.lib().smol_jpeg_workspace_bytes(1, w.ctypes.data, h.ctypes.data)
+    rc = smol.lib().smol_jpeg_roi_preprocess_batch(
+        FAKE_SRC, 10**6, z.ctypes.data, q.ctypes.data, w.ctypes.data, h.ctypes.data, 1,
+        ctypes.byref(p), None if opts is None else ctypes.byref(opts), ws,
+        need if ws_bytes is None else ws_bytes, FAKE_OUT, None)
+    return rc, smol.lib().smol_last_error().decode()
+
+
+@pytest.mark.parametrize("kw,needle", [
+    (dict(opts=smol.make_options(chroma_siting=smol.CHROMA_LEFT)), "centred"),
+    (dict(opts=smol.make_options(layout=3)), "layout"),
+    (dict(ws_bytes=100), "workspace"),
+    (dict(ws=FAKE_OUT + 4), "aligned"),
+    (dict(params=smol.make_params(32, 40, 40, MEAN, STD, smol.OUT_F16)), "larger than resized"),
+])
+def test_jpeg_roi_preprocess_validation(kw, needle):
+    rc, msg = _jpeg_roi_call(**kw)
+    assert rc == smol.ERR_INVALID_ARG and needle in msg, (rc, msg)
