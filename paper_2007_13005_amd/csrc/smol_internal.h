@@ -73,22 +73,31 @@ constexpr int kRowsMaxGroups = 4;
 // Waves per workgroup of the row-streaming kernels (each wave independent).
 constexpr int kRowsMaxWavesPerGroup = 4;
 
-// Block decoding of a group of 4:2:0 frames of one geometry (smol_jpeg_kernels.hip):
-// frame f's coefficients at coef + f * coef_stride (int16 elements; luma
-// blocks bw x bh, then Cb and Cr (bw/2) x (bh/2), 64 each, natural order),
-// its planes at out + f * out_stride + yoff / cboff / croff (W x H and
-// Wc x Hc, tightly pitched). Blocks lbx0 .. lbx0 + lnbx - 1 (and rows) of
-// luma and cbx0 .. of chroma are decoded.
+// Block decoding (smol_jpeg_kernels.hip). A launch decodes up to
+// kJpegMaxRuns runs; a run is `frames` frames of one geometry whose
+// coefficients start at element coef (from JpegArgs::coef) and step by
+// coef_stride, and whose Y planes start at byte out (from JpegArgs::out) and
+// step by out_stride, the Cb and Cr planes cboff / croff bytes after the Y
+// plane. Coefficients: luma blocks bw x bh, then Cb and Cr (bw/2) x (bh/2),
+// 64 each, natural order; planes W x H and ceil(W/2) x ceil(H/2), tightly
+// pitched. Luma blocks lbx0 .. lbx0 + lnbx - 1 (rows likewise) and chroma
+// blocks cbx0 .. are decoded; jobs_end counts the kernel's jobs (groups of up
+// to eight blocks along a block row) of this and the earlier runs.
+constexpr int kJpegMaxRuns = 24;
+struct JpegRun {
+    long long coef, coef_stride, out, out_stride, cboff, croff;
+    int32_t W, H, bw, bh;
+    int16_t lbx0, lby0, lnbx, lnby, cbx0, cby0, cnbx, cnby;
+    int32_t frames, pad;
+    long long jobs_end;
+};
 struct JpegArgs {
     const int16_t *coef;
-    long long coef_stride;
     uint8_t *out;
-    long long out_stride, yoff, cboff, croff;
-    int32_t W, H, Wc, Hc, bw, bh;
-    int32_t lbx0, lby0, lnbx, lnby, cbx0, cby0, cnbx, cnby;
-    int32_t frames;
-    int32_t q[2][64];  // luma, chroma dequantisation
+    int32_t runs, pad;
+    uint8_t q[2][64];  // luma, chroma dequantisation (entries 1..255)
     float c[64];       // c[k * 8 + n] = fp32(C(k)/2 cos((2n + 1) k pi / 16))
+    JpegRun run[kJpegMaxRuns];
 };
 int launch_jpeg_idct(const JpegArgs &a, int grid, void *stream);
 

@@ -148,7 +148,23 @@ int smol_jpeg_decode_i420(const int16_t *coef, int64_t coef_elems, const int64_t
             a.c[k * 8 + m] = (float)((k == 0 ? 1.0 / std::sqrt(2.0) : 1.0) / 2.0 *
                                      std::cos((2.0 * m + 1.0) * k * pi / 16.0));
     const int cus = smol::device_cus();
-    // Runs of frames with one geometry and constant strides share a launch.
+    a.coef = coef;
+    a.out = out;
+    // Runs of frames with one geometry and constant strides; up to
+    // kJpegMaxRuns runs share a launch.
+    long long jobs = 0;
+    auto flush = [&]() -> int {
+        if (a.runs == 0)
+            return SMOL_OK;
+        const int grid = (int)std::min<long long>(jobs, (long long)(cus > 0 ? cus : 256) * 32);
+        const int rc = smol::launch_jpeg_idct(a, grid, stream);
+        a.runs = 0;
+        jobs = 0;
+        if (rc != (int)hipSuccess)
+            return smol::set_error(SMOL_ERR_HIP, "block decoding launch: %s",
+                                   hipGetErrorString((hipError_t)rc));
+        return SMOL_OK;
+    };
     for (int32_t b = 0; b < n;) {
         int32_t e = b + 1;
         const int64_t cs = e < n ? coef_offsets[e] - coef_offsets[b] : 0;
@@ -160,39 +176,41 @@ int smol_jpeg_decode_i420(const int16_t *coef, int64_t coef_elems, const int64_t
                cr_offsets[e] - y_offsets[e] == cr_offsets[b] - y_offsets[b])
             ++e;
         const Blocks &g = blk[(size_t)b];
-        a.coef = coef + coef_offsets[b];
-        a.coef_stride = cs;
-        a.out = out + y_offsets[b];
-        a.out_stride = os;
-        a.yoff = 0;
-        a.cboff = cb_offsets[b] - y_offsets[b];
-        a.croff = cr_offsets[b] - y_offsets[b];
-        a.W = g.W;
-        a.H = g.H;
-        a.Wc = (g.W + 1) / 2;
-        a.Hc = (g.H + 1) / 2;
-        a.bw = g.bw;
-        a.bh = g.bh;
-        a.lbx0 = g.lbx0;
-        a.lby0 = g.lby0;
-        a.lnbx = g.lnbx;
-        a.lnby = g.lnby;
-        a.cbx0 = g.cbx0;
-        a.cby0 = g.cby0;
-        a.cnbx = g.cnbx;
-        a.cnby = g.cnby;
-        a.frames = e - b;
+        smol::JpegRun &r = a.run[a.runs];
+        r.coef = coef_offsets[b];
+        r.coef_stride = cs;
+        r.out = y_offsets[b];
+        r.out_stride = os;
+        r.cboff = cb_offsets[b] - y_offsets[b];
+        r.croff = cr_offsets[b] - y_offsets[b];
+        r.W = (int32_t)g.W;
+        r.H = (int32_t)g.H;
+        r.bw = (int32_t)g.bw;
+        r.bh = (int32_t)g.bh;
+        r.lbx0 = (int16_t)g.lbx0;
+        r.lby0 = (int16_t)g.lby0;
+        r.lnbx = (int16_t)g.lnbx;
+        r.lnby = (int16_t)g.lnby;
+        r.cbx0 = (int16_t)g.cbx0;
+        r.cby0 = (int16_t)g.cby0;
+        r.cnbx = (int16_t)g.cnbx;
+        r.cnby = (int16_t)g.cnby;
+        r.frames = e - b;
+        r.pad = 0;
         // jobs of the kernel: groups of up to eight blocks along block rows
-        const long long jobs = ((long long)(g.lnbx + 7) / 8 * g.lnby +
-                                2LL * ((g.cnbx + 7) / 8) * g.cnby) *
-                               (long long)(e - b);
-        const int grid = (int)std::min<long long>(jobs, (long long)(cus > 0 ? cus : 256) * 32);
-        const int rc = smol::launch_jpeg_idct(a, grid, stream);
-        if (rc != (int)hipSuccess)
-            return smol::set_error(SMOL_ERR_HIP, "block decoding launch: %s",
-                                   hipGetErrorString((hipError_t)rc));
+        jobs += ((long long)(g.lnbx + 7) / 8 * g.lnby + 2LL * ((g.cnbx + 7) / 8) * g.cnby) *
+                (long long)(e - b);
+        r.jobs_end = jobs;
+        if (++a.runs == smol::kJpegMaxRuns) {
+            const int rc = flush();
+            if (rc != SMOL_OK)
+                return rc;
+        }
         b = e;
     }
+    const int rc = flush();
+    if (rc != SMOL_OK)
+        return rc;
     return SMOL_OK;
 }
 

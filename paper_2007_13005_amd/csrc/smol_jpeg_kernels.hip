@@ -30,53 +30,58 @@ __global__ void __launch_bounds__(64) jpeg_idct_kernel(JpegArgs a)
 #pragma unroll
     for (int k = 0; k < 8; ++k)
         cr[k] = a.c[k * 8 + row];
-    // groups of up to eight blocks along each block row of the rectangle
-    const int lg = (a.lnbx + kBlocksPerWave - 1) / kBlocksPerWave;
-    const int cg = (a.cnbx + kBlocksPerWave - 1) / kBlocksPerWave;
-    const long long lum = (long long)lg * a.lnby, chr = (long long)cg * a.cnby;
-    const long long per_frame = lum + 2 * chr;
-    const long long jobs = per_frame * a.frames;
+    const long long jobs = a.run[a.runs - 1].jobs_end;
+    int ri = 0;  // run of the current job (jobs ascend within a workgroup)
     for (long long job = blockIdx.x; job < jobs; job += gridDim.x) {
-        const int f = (int)(job / per_frame);
-        long long k = job - (long long)f * per_frame;
+        while (a.run[ri].jobs_end <= job)
+            ++ri;
+        const JpegRun &r = a.run[ri];
+        // groups of up to eight blocks along each block row of the rectangle
+        const int lg = (r.lnbx + kBlocksPerWave - 1) / kBlocksPerWave;
+        const int cg = (r.cnbx + kBlocksPerWave - 1) / kBlocksPerWave;
+        const long long lum = (long long)lg * r.lnby, chr = (long long)cg * r.cnby;
+        const long long per_frame = lum + 2 * chr;
+        const long long local = job - (ri ? a.run[ri - 1].jobs_end : 0);
+        const int f = (int)(local / per_frame);
+        long long k = local - (long long)f * per_frame;
         int comp, by, bx0, nb, gw, pw, ph;
         long long cbase, pbase;
         if (k < lum) {
             comp = 0;
-            by = a.lby0 + (int)(k / lg);
+            by = r.lby0 + (int)(k / lg);
             const int gi = (int)(k % lg);
-            bx0 = a.lbx0 + gi * kBlocksPerWave;
-            nb = min(kBlocksPerWave, a.lnbx - gi * kBlocksPerWave);
-            gw = a.bw;
+            bx0 = r.lbx0 + gi * kBlocksPerWave;
+            nb = min(kBlocksPerWave, r.lnbx - gi * kBlocksPerWave);
+            gw = r.bw;
             cbase = 0;
-            pbase = a.yoff;
-            pw = a.W;
-            ph = a.H;
+            pbase = 0;
+            pw = r.W;
+            ph = r.H;
         } else {
             k -= lum;
             comp = k < chr ? 1 : 2;
             k -= comp == 1 ? 0 : chr;
-            by = a.cby0 + (int)(k / cg);
+            by = r.cby0 + (int)(k / cg);
             const int gi = (int)(k % cg);
-            bx0 = a.cbx0 + gi * kBlocksPerWave;
-            nb = min(kBlocksPerWave, a.cnbx - gi * kBlocksPerWave);
-            gw = a.bw >> 1;
-            cbase = 64LL * a.bw * a.bh + (comp == 2 ? 64LL * (a.bw >> 1) * (a.bh >> 1) : 0);
-            pbase = comp == 1 ? a.cboff : a.croff;
-            pw = a.Wc;
-            ph = a.Hc;
+            bx0 = r.cbx0 + gi * kBlocksPerWave;
+            nb = min(kBlocksPerWave, r.cnbx - gi * kBlocksPerWave);
+            gw = r.bw >> 1;
+            cbase = 64LL * r.bw * r.bh + (comp == 2 ? 64LL * (r.bw >> 1) * (r.bh >> 1) : 0);
+            pbase = comp == 1 ? r.cboff : r.croff;
+            pw = (r.W + 1) >> 1;
+            ph = (r.H + 1) >> 1;
         }
         // lanes of blocks past the group's end repeat its last block
         const int bb = min(b, nb - 1);
-        const int16_t *blk =
-            a.coef + f * a.coef_stride + cbase + 64LL * ((long long)by * gw + bx0 + bb);
+        const int16_t *blk = a.coef + r.coef + f * r.coef_stride + cbase +
+                             64LL * ((long long)by * gw + bx0 + bb);
         typedef short short8 __attribute__((ext_vector_type(8)));
         const short8 raw = *(const short8 *)(blk + 8 * row);
-        const int *q = comp == 0 ? a.q[0] : a.q[1];
+        const uint8_t *q = comp == 0 ? a.q[0] : a.q[1];
         float d[8];
 #pragma unroll
         for (int u = 0; u < 8; ++u)
-            d[u] = (float)((int)raw[u] * q[8 * row + u]);  // exact: |.| < 2^24
+            d[u] = (float)((int)raw[u] * (int)q[8 * row + u]);  // exact: |.| < 2^24
         // horizontal pass for row v = row of block bb
 #pragma unroll
         for (int x = 0; x < 8; ++x) {
@@ -101,7 +106,7 @@ __global__ void __launch_bounds__(64) jpeg_idct_kernel(JpegArgs a)
         }
         const int gx = 8 * (bx0 + b), gy = 8 * by + row;
         if (b < nb && gy < ph) {
-            uint8_t *dst = a.out + f * a.out_stride + pbase + (long long)gy * pw + gx;
+            uint8_t *dst = a.out + r.out + f * r.out_stride + pbase + (long long)gy * pw + gx;
             if (gx + 8 <= pw && ((uintptr_t)dst & 7) == 0) {
                 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
                 *(u32x2 *)dst = u32x2{px4[0], px4[1]};

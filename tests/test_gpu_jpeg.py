@@ -78,6 +78,31 @@ def test_rectangle_decode_touches_only_its_blocks():
             assert np.array_equal(got[i][k], exp[k]), (sizes[i], r, k)
 
 
+def test_ragged_batch_spans_several_launches():
+    """Sixty frames in more runs of one geometry than one launch's table
+    holds, with and without rectangles, bit for bit."""
+    rng = np.random.default_rng(56)
+    sizes = []
+    while len(sizes) < 60:
+        W, H = int(rng.integers(1, 200)), int(rng.integers(1, 150))
+        sizes += [(W, H)] * (1 + (len(sizes) % 3 == 0) * int(rng.integers(0, 4)))
+    sizes = sizes[:60]
+    runs = 1 + sum(a != b for a, b in zip(sizes, sizes[1:]))
+    assert runs > 24, runs
+    wl = synthetic.jpeg_workload("jpeg-ragged", sizes, 16, 8, F16, 56)
+    rects = []
+    for W, H in sizes:
+        x, y = 2 * int(rng.integers(0, (W + 1) // 2)), 2 * int(rng.integers(0, (H + 1) // 2))
+        rects.append((x, y, int(rng.integers(1, W - x + 1)), int(rng.integers(1, H - y + 1))))
+    for rr in (None, rects):
+        got = _gpu_decode(wl, rr, fill=7)
+        for i in range(wl.n):
+            exp = _oracle_decode(wl, i, None if rr is None else rr[i], fill=7)
+            for k in range(3):
+                assert np.array_equal(got[i][k], exp[k]), (i, sizes[i], k)
+    note(f"    {wl.n} frames in {runs} runs decoded bit for bit")
+
+
 @pytest.mark.parametrize("layout", [smol.LAYOUT_NCHW, smol.LAYOUT_NHWC])
 @pytest.mark.parametrize("dtype", [F32, F16])
 def test_partial_decode_then_preprocess(dtype, layout):
