@@ -158,6 +158,8 @@ def _load():
     lib.oracle_jpeg_mcu_rect.restype = ctypes.c_int
     lib.oracle_jpeg_decode_i420.argtypes = [P, P, P, I32, I32, P, P, P, P]
     lib.oracle_jpeg_decode_i420.restype = ctypes.c_int
+    lib.oracle_jpeg_entropy_decode.argtypes = [P, I64, P, I64, P, P, P, P]
+    lib.oracle_jpeg_entropy_decode.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -534,3 +536,23 @@ def jpeg_decode_i420(coef, qy, qc, W: int, H: int, rect=None, fill: int | None =
     if rc != 0:
         raise ValueError("oracle rejected the arguments")
     return y, cb, cr
+
+
+def jpeg_entropy_decode(data: bytes):
+    """Entropy-decode a whole baseline 4:2:0 JPEG stream (T.81, Annex F):
+    (coefficients int16 in the library's block layout, luma table, chroma
+    table (natural order, uint16[64] each), W, H). Raises ValueError on a
+    stream outside the accepted subset or a corrupt one."""
+    buf = np.frombuffer(bytes(data), np.uint8)
+    qy, qc = np.zeros(64, np.uint16), np.zeros(64, np.uint16)
+    W, H = ctypes.c_int32(0), ctypes.c_int32(0)
+    lib_ = _load()
+    if lib_.oracle_jpeg_entropy_decode(buf.ctypes.data, buf.size, None, 0, qy.ctypes.data,
+                                       qc.ctypes.data, ctypes.byref(W), ctypes.byref(H)) != 0:
+        raise ValueError("oracle rejected the stream")
+    coef = np.zeros(jpeg_coef_count(W.value, H.value), np.int16)
+    if lib_.oracle_jpeg_entropy_decode(buf.ctypes.data, buf.size, coef.ctypes.data, coef.size,
+                                       qy.ctypes.data, qc.ctypes.data, ctypes.byref(W),
+                                       ctypes.byref(H)) != 0:
+        raise ValueError("oracle rejected the stream")
+    return coef, qy, qc, W.value, H.value

@@ -66,6 +66,10 @@
  * and an r x r central crop, each resized value rounded to the nearest
  * integer (ties to even) as uint8 ("uint8 output", no normalisation) -- and
  * that r x r image then goes through steps 2-4 like any other image.
+ *
+ * Partial JPEG decoding (section 6.4, "ROI decoding", Algorithm 1) and, ahead
+ * of it, baseline JPEG entropy decoding written from ITU-T T.81: their
+ * readings sit with the functions at the end of this file.
  */
 #include <math.h>
 #include <stdint.h>
@@ -795,4 +799,308 @@ int oracle_jpeg_decode_i420(const int16_t *coef, const uint16_t *qy, const uint1
             oracle_idct_block(cr + 64 * k, qc, crp + 8 * by * Wc + 8 * bx, Wc, w, h);
         }
     return ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Baseline JPEG entropy decoding (the CPU step ahead of section 6.4's       */
+/* partial decode), written from ITU-T T.81                                  */
+/* ------------------------------------------------------------------------- */
+/*
+ * The whole scan is decoded, always: a partial decode must produce the same
+ * coefficients for every block it keeps. Accepted streams: baseline (SOF0)
+ * or extended (SOF1) Huffman coding, 8-bit samples, three components with
+ * sampling factors 2x2, 1x1, 1x1 (4:2:0), Cb and Cr on one quantisation
+ * table, 8-bit table entries, one interleaved scan with Ss = 0, Se = 63,
+ * Ah = Al = 0, and optional restart intervals (DRI). The output is this
+ * library's coefficient layout: per block 64 values in natural order
+ * (row = vertical frequency), luma blocks in raster order over the
+ * MCU-padded frame, then Cb, then Cr.
+ */
+
+/* Zig-zag order (T.81 Figure A.6): zz_pos[k] = row * 8 + column of the k-th
+ * coefficient, generated by walking the anti-diagonals d = row + column in
+ * turn, upwards (row falling) on even d and downwards on odd d. */
+static void zigzag_positions(int zz_pos[64])
+{
+    int k = 0;
+    for (int d = 0; d < 15; ++d)
+        for (int i = 0; i < 8; ++i) {
+            int row = (d % 2 == 0) ? d - i : i;
+            int col = d - row;
+            if (row >= 0 && row < 8 && col >= 0 && col < 8)
+                zz_pos[k++] = row * 8 + col;
+        }
+}
+
+/* A Huffman table in T.81's decoder form (C.1, C.2 and F.2.2.3, Figure F.15):
+ * for each code length l, the largest code MAXCODE[l] (-1: none), the
+ * smallest MINCODE[l] and the index VALPTR[l] of its first value in HUFFVAL. */
+typedef struct {
+    int present;
+    int32_t maxcode[18], mincode[17], valptr[17];
+    uint8_t huffval[256];
+} jpeg_huff;
+
+static int huff_build(jpeg_huff *t, const uint8_t bits[16], const uint8_t *vals, int nvals)
+{
+    /* C.1: HUFFSIZE lists the code lengths in order; C.2: HUFFCODE the codes */
+    int huffsize[257], huffcode[257], k = 0;
+    for (int l = 1; l <= 16; ++l)
+        for (int i = 0; i < bits[l - 1]; ++i)
+            huffsize[k++] = l;
+    huffsize[k] = 0;
+    if (k != nvals || k > 256)
+        return 0;
+    int code = 0, si = huffsize[0];
+    for (int p = 0; p < k;) {
+        while (p < k && huffsize[p] == si)
+            huffcode[p++] = code++;
+        if ((long)code > (1L << si))
+            return 0; /* lengths that do not form a prefix code */
+        code <<= 1;
+        ++si;
+    }
+    /* F.15 */
+    int j = 0;
+    for (int l = 1; l <= 16; ++l) {
+        if (bits[l - 1] == 0) {
+            t->maxcode[l] = -1;
+            continue;
+        }
+        t->valptr[l] = j;
+        t->mincode[l] = huffcode[j];
+        j += bits[l - 1];
+        t->maxcode[l] = huffcode[j - 1];
+    }
+    t->maxcode[17] = 0x7fffffff;
+    memcpy(t->huffval, vals, (size_t)nvals);
+    t->present = 1;
+    return 1;
+}
+
+/* The entropy-coded segment as a bit source: NEXTBIT of F.2.2.5 (Figure
+ * F.18) with the stuffed zero byte after 0xFF removed; a marker ends the
+ * bits (reading past it is an error). */
+typedef struct {
+    const uint8_t *d;
+    int64_t n, pos;
+    int cnt, b, bad;
+} jpeg_bits;
+
+static int next_bit(jpeg_bits *s)
+{
+    if (s->cnt == 0) {
+        if (s->pos >= s->n) {
+            s->bad = 1;
+            return 0;
+        }
+        s->b = s->d[s->pos++];
+        s->cnt = 8;
+        if (s->b == 0xFF) {
+            if (s->pos >= s->n || s->d[s->pos] != 0x00) {
+                s->bad = 1; /* a marker inside the data */
+                return 0;
+            }
+            ++s->pos;
+        }
+    }
+    --s->cnt;
+    return (s->b >> s->cnt) & 1;
+}
+
+/* DECODE (Figure F.16) */
+static int huff_decode(jpeg_bits *s, const jpeg_huff *t)
+{
+    int32_t code = next_bit(s);
+    int l = 1;
+    while (code > t->maxcode[l]) {
+        if (l == 16) {
+            s->bad = 1;
+            return 0;
+        }
+        code = (code << 1) | next_bit(s);
+        ++l;
+    }
+    return t->huffval[t->valptr[l] + code - t->mincode[l]];
+}
+
+/* RECEIVE (Figure F.17) followed by EXTEND (Figure F.12) */
+static int32_t receive_extend(jpeg_bits *s, int ssss)
+{
+    int32_t v = 0;
+    for (int i = 0; i < ssss; ++i)
+        v = (v << 1) | next_bit(s);
+    if (ssss > 0 && v < (1 << (ssss - 1)))
+        v -= (1 << ssss) - 1;
+    return v;
+}
+
+static int be16(const uint8_t *p) { return (p[0] << 8) | p[1]; }
+
+/* Decode a whole baseline 4:2:0 JPEG stream: coefficients into coef
+ * (oracle_jpeg_coef_count(W, H) elements), tables in natural order into
+ * qy and qc (uint16[64] each), size into *W and *H. coef_elems bounds
+ * coef; pass coef = NULL to read only the headers (size and tables). */
+int oracle_jpeg_entropy_decode(const uint8_t *d, int64_t n, int16_t *coef, int64_t coef_elems,
+                               uint16_t *qy, uint16_t *qc, int32_t *Wout, int32_t *Hout)
+{
+    int zz_pos[64];
+    zigzag_positions(zz_pos);
+    uint16_t qt[4][64];
+    int qt_present[4] = {0, 0, 0, 0};
+    jpeg_huff dc[4], ac[4];
+    memset(dc, 0, sizeof dc);
+    memset(ac, 0, sizeof ac);
+    int W = 0, H = 0, comp_id[3] = {0, 0, 0}, comp_q[3] = {0, 0, 0}, have_sof = 0;
+    int64_t restart = 0;
+    if (n < 4 || d[0] != 0xFF || d[1] != 0xD8)
+        return ORACLE_ERR;
+    int64_t p = 2;
+    for (;;) {
+        if (p + 4 > n || d[p] != 0xFF)
+            return ORACLE_ERR;
+        while (p < n && d[p] == 0xFF) /* fill bytes before a marker */
+            ++p;
+        if (p + 3 > n)
+            return ORACLE_ERR;
+        const int m = d[p++];
+        if (m == 0xD9 || m == 0xD8 || (m >= 0xD0 && m <= 0xD7) || m == 0x01)
+            return ORACLE_ERR; /* EOI, SOI or RST before the scan */
+        const int len = be16(d + p);
+        if (len < 2 || p + len > n)
+            return ORACLE_ERR;
+        const uint8_t *s = d + p + 2;
+        const int64_t seg_end = p + len;
+        if (m == 0xDB) { /* DQT */
+            int64_t q = p + 2;
+            while (q < seg_end) {
+                const int pq = d[q] >> 4, tq = d[q] & 15;
+                if (pq != 0 || tq > 3 || q + 65 > seg_end)
+                    return ORACLE_ERR; /* 16-bit tables are not accepted */
+                for (int k = 0; k < 64; ++k)
+                    qt[tq][zz_pos[k]] = d[q + 1 + k];
+                qt_present[tq] = 1;
+                q += 65;
+            }
+        } else if (m == 0xC4) { /* DHT */
+            int64_t q = p + 2;
+            while (q < seg_end) {
+                if (q + 17 > seg_end)
+                    return ORACLE_ERR;
+                const int tc = d[q] >> 4, th = d[q] & 15;
+                int total = 0;
+                for (int i = 0; i < 16; ++i)
+                    total += d[q + 1 + i];
+                if (tc > 1 || th > 3 || q + 17 + total > seg_end)
+                    return ORACLE_ERR;
+                if (!huff_build(tc == 0 ? &dc[th] : &ac[th], d + q + 1, d + q + 17, total))
+                    return ORACLE_ERR;
+                q += 17 + total;
+            }
+        } else if (m == 0xDD) { /* DRI */
+            if (len != 4)
+                return ORACLE_ERR;
+            restart = be16(s);
+        } else if (m == 0xC0 || m == 0xC1) { /* SOF0, SOF1 */
+            if (len != 17 || s[0] != 8 || s[5] != 3)
+                return ORACLE_ERR;
+            H = be16(s + 1);
+            W = be16(s + 3);
+            const int want[3] = {0x22, 0x11, 0x11};
+            for (int c = 0; c < 3; ++c) {
+                comp_id[c] = s[6 + 3 * c];
+                if (s[7 + 3 * c] != want[c] || s[8 + 3 * c] > 3)
+                    return ORACLE_ERR;
+                comp_q[c] = s[8 + 3 * c];
+            }
+            if (W < 1 || H < 1 || comp_q[1] != comp_q[2])
+                return ORACLE_ERR;
+            have_sof = 1;
+        } else if (m >= 0xC2 && m <= 0xCF && m != 0xC4 && m != 0xC8 && m != 0xCC) {
+            return ORACLE_ERR; /* progressive, lossless, hierarchical, arithmetic */
+        } else if (m == 0xDA) { /* SOS */
+            if (!have_sof || !qt_present[comp_q[0]] || !qt_present[comp_q[1]])
+                return ORACLE_ERR;
+            if (len != 12 || s[0] != 3 || s[7] != 0 || s[8] != 63 || s[9] != 0)
+                return ORACLE_ERR;
+            int td[3], ta[3];
+            for (int c = 0; c < 3; ++c) {
+                if (s[1 + 2 * c] != comp_id[c])
+                    return ORACLE_ERR; /* components in frame order */
+                td[c] = s[2 + 2 * c] >> 4;
+                ta[c] = s[2 + 2 * c] & 15;
+                if (td[c] > 3 || ta[c] > 3 || !dc[td[c]].present || !ac[ta[c]].present)
+                    return ORACLE_ERR;
+            }
+            for (int k = 0; k < 64; ++k) {
+                qy[k] = qt[comp_q[0]][k];
+                qc[k] = qt[comp_q[1]][k];
+            }
+            *Wout = W;
+            *Hout = H;
+            if (!coef)
+                return ORACLE_OK;
+            if (coef_elems < oracle_jpeg_coef_count(W, H))
+                return ORACLE_ERR;
+            int64_t bw, bh;
+            jpeg_grid(W, H, &bw, &bh);
+            const int64_t mcux = bw / 2, mcuy = bh / 2, mcus = mcux * mcuy;
+            int16_t *plane[3] = {coef, coef + 64 * bw * bh, coef + 64 * bw * bh + 64 * mcus};
+            jpeg_bits bs = {d, n, seg_end, 0, 0, 0};
+            int32_t pred[3] = {0, 0, 0};
+            for (int64_t mcu = 0; mcu < mcus; ++mcu) {
+                if (restart > 0 && mcu > 0 && mcu % restart == 0) {
+                    /* the interval ends: skip the remaining bits of the byte,
+                     * then expect RST((mcu / restart - 1) mod 8) */
+                    bs.cnt = 0;
+                    const int64_t want_rst = 0xD0 + (mcu / restart - 1) % 8;
+                    if (bs.pos + 2 > n || d[bs.pos] != 0xFF || d[bs.pos + 1] != want_rst)
+                        return ORACLE_ERR;
+                    bs.pos += 2;
+                    pred[0] = pred[1] = pred[2] = 0;
+                }
+                const int64_t my = mcu / mcux, mx = mcu % mcux;
+                /* four luma blocks (left to right, top to bottom), Cb, Cr */
+                for (int b = 0; b < 6; ++b) {
+                    const int c = b < 4 ? 0 : b - 3;
+                    int64_t blk;
+                    if (c == 0)
+                        blk = (2 * my + b / 2) * bw + 2 * mx + b % 2;
+                    else
+                        blk = mcu;
+                    int16_t *z = plane[c] + 64 * blk;
+                    memset(z, 0, 64 * sizeof(int16_t));
+                    /* F.2.2.1: DC difference */
+                    const int t = huff_decode(&bs, &dc[td[c]]);
+                    if (t > 11)
+                        return ORACLE_ERR;
+                    pred[c] += receive_extend(&bs, t);
+                    if (pred[c] < -32768 || pred[c] > 32767)
+                        return ORACLE_ERR;
+                    z[0] = (int16_t)pred[c];
+                    /* F.2.2.2 (Figure F.13): AC coefficients */
+                    for (int k = 1; k < 64;) {
+                        const int rs = huff_decode(&bs, &ac[ta[c]]);
+                        const int ssss = rs & 15, rrrr = rs >> 4;
+                        if (ssss == 0) {
+                            if (rrrr != 15)
+                                break; /* end of block */
+                            k += 16;
+                            continue;
+                        }
+                        k += rrrr;
+                        if (k > 63 || ssss > 10)
+                            return ORACLE_ERR;
+                        z[zz_pos[k]] = (int16_t)receive_extend(&bs, ssss);
+                        ++k;
+                    }
+                    if (bs.bad)
+                        return ORACLE_ERR;
+                }
+            }
+            return ORACLE_OK;
+        }
+        /* APPn, COM and other segments are skipped */
+        p = seg_end;
+    }
 }

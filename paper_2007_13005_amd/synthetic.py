@@ -84,9 +84,16 @@ class Workload:
     # low_res (0: off)
     low_res: int = 0
     # kind "jpeg": src holds the int16 coefficients' bytes; frame i's start at
-    # element coef_offsets[i]; qtables (2, 64) uint16, luma then chroma
+    # element coef_offsets[i]; qtables (2, 64) uint16, luma then chroma, for
+    # every frame, or (n, 2, 64), one pair per frame
     coef_offsets: np.ndarray | None = None
     qtables: np.ndarray | None = None
+
+    def frame_qtables(self, i: int) -> tuple[np.ndarray, np.ndarray]:
+        """Frame i's (luma, chroma) dequantisation tables."""
+        q = np.asarray(self.qtables).reshape(-1, 2, 64)
+        q = q[0] if len(q) == 1 else q[i]
+        return q[0], q[1]
 
     @property
     def variant(self) -> bool:
@@ -329,6 +336,44 @@ def jpeg_workload(name: str, sizes, S: int, C: int | tuple[int, int], out_dtype:
                     heights=np.asarray([h for _, h in sizes], np.int32), resize_short=S,
                     crop_h=ch, crop_w=cw, out_dtype=out_dtype, coef_offsets=offs, qtables=q,
                     description=description)
+
+
+def photo_ycbcr(rng, W: int, H: int) -> np.ndarray:
+    """A W x H x 3 YCbCr uint8 image with photo-like structure: smooth
+    luminance and colour fields, a few hard-edged rectangles and fine
+    Gaussian grain."""
+    yy, xx = np.mgrid[0:H, 0:W].astype(np.float64)
+    img = np.empty((H, W, 3))
+    for c, amp in enumerate((70.0, 35.0, 35.0)):
+        a, b, ph = rng.uniform(0.005, 0.08, 2), rng.uniform(0.005, 0.08, 2), rng.uniform(0, 6.3, 2)
+        img[..., c] = 128 + amp * np.sin(a[0] * xx + b[0] * yy + ph[0]) * np.cos(
+            a[1] * xx - b[1] * yy + ph[1])
+    for _ in range(int(rng.integers(2, 6))):
+        x0, y0 = int(rng.integers(0, W)), int(rng.integers(0, H))
+        x1, y1 = x0 + int(rng.integers(1, max(2, W // 3))), y0 + int(rng.integers(1, max(2, H // 3)))
+        img[y0:y1, x0:x1] += rng.uniform(-50, 50, 3)
+    img += rng.normal(0.0, 4.0, img.shape)
+    return np.clip(np.rint(img), 0, 255).astype(np.uint8)
+
+
+def jpeg_files(sizes, seed: int, quality=75, restart_blocks: int = 0) -> list[bytes]:
+    """Baseline 4:2:0 JPEG streams of seeded photo-like images, encoded by
+    libjpeg through PIL, standing in for a JPEG dataset. ``quality`` is one
+    libjpeg quality for all or one per image; ``restart_blocks`` > 0 puts a
+    restart marker every that many MCUs."""
+    import io
+
+    from PIL import Image
+    rng = np.random.default_rng(seed)
+    qs = [quality] * len(sizes) if np.isscalar(quality) else list(quality)
+    out = []
+    for (W, H), q in zip(sizes, qs):
+        b = io.BytesIO()
+        kw = {"restart_marker_blocks": int(restart_blocks)} if restart_blocks else {}
+        Image.fromarray(photo_ycbcr(rng, int(W), int(H)), "YCbCr").save(
+            b, "JPEG", quality=int(q), subsampling=2, **kw)
+        out.append(b.getvalue())
+    return out
 
 
 def c8(n: int = 128, height: int = 720, width: int = 1280) -> Workload:
