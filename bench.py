@@ -58,6 +58,9 @@ def parse():
                          "throughput against the minimum of the stage throughputs (Eq. 4)")
     ap.add_argument("--pipeline-seconds", type=float, default=2.0,
                     help="duration of each timed phase of --pipeline")
+    ap.add_argument("--jpeg-files", action="store_true",
+                    help="experiment: JPEG files through host entropy decoding (whole and "
+                         "partial), the copy and the GPU stages, alone and pipelined")
     ap.add_argument("--copy-probe", type=int, default=0,
                     help="instead of the benchmark, copy this many MiB with torch several "
                          "times (calibrates the FETCH_SIZE / WRITE_SIZE counters)")
@@ -168,8 +171,8 @@ def cpu_baseline(wl, seconds: float, threads: int) -> dict:
                                         wl.resize_mode)
             k = oracle.jpeg_coef_count(W, H)
             c0 = int(wl.coef_offsets[i])
-            y, cb, cr = oracle.jpeg_decode_i420(wl.src.view(np.int16)[c0:c0 + k], wl.qtables[0],
-                                                wl.qtables[1], W, H, rect)
+            y, cb, cr = oracle.jpeg_decode_i420(wl.src.view(np.int16)[c0:c0 + k],
+                                                *wl.frame_qtables(i), W, H, rect)
             rc = oracle.yuv420_preprocess_image_ex_into(
                 y.ctypes.data, cb.ctypes.data, cr.ctypes.data, W, H, (0, 0, W, H),
                 wl.resize_short, wl.crop_h, wl.crop_w, mean, std, wl.out_dtype, wl.resize_mode,
@@ -528,6 +531,142 @@ def pipeline_experiment(args) -> int:
     return 0
 
 
+def jpeg_files_experiment(args) -> int:
+    """JPEG files (section 6.4 with Algorithm 1) stage by stage: the host
+    entropy decoding of whole streams and of only the MCUs Algorithm 1's
+    rectangles need, the copy of the coefficients to the device, the GPU's
+    partial block decoding plus fused preprocessing, and the stages pipelined
+    (host decoding of batch k + 1 while the GPU works on batch k), set against
+    the minimum of the stage rates (Eq. 4). libjpeg's full decode to RGB
+    through PIL on the same threads is printed for context."""
+    import ctypes
+    from concurrent.futures import ThreadPoolExecutor
+
+    import numpy as np
+    import torch
+
+    from paper_2007_13005_amd import smol, synthetic
+
+    files = synthetic.jpeg_file_batch()
+    n = len(files)
+    threads = args.cpu_threads or 16
+    secs = args.pipeline_seconds
+    params = smol.make_params(256, 224, 224, synthetic.IMAGENET_MEAN_255,
+                              synthetic.IMAGENET_STD_255, synthetic.OUT_F16)
+    infos = [smol.jpeg_read_info(f) for f in files]
+    w = np.asarray([i.width for i in infos], np.int32)
+    h = np.asarray([i.height for i in infos], np.int32)
+    rects = np.asarray([smol.jpeg_mcu_rect(int(a), int(b), params) for a, b in zip(w, h)],
+                       np.int32)
+    sizes = np.asarray([len(f) for f in files], np.int64)
+    offs = np.concatenate([[0], np.cumsum(sizes)[:-1]]).astype(np.int64)
+    data = np.frombuffer(b"".join(files), np.uint8)
+    counts = np.asarray([smol.jpeg_coef_count(int(a), int(b)) for a, b in zip(w, h)], np.int64)
+    co = np.concatenate([[0], np.cumsum(counts)[:-1]]).astype(np.int64)
+    total = int(counts.sum())
+    slots = [torch.zeros(total, dtype=torch.int16, pin_memory=True) for _ in range(3)]
+    q = np.zeros((n, 2, 64), np.uint16)
+    fn = smol.lib().smol_jpeg_entropy_decode_batch
+
+    def entropy(slot, rect_ptr):
+        rc = fn(data.ctypes.data, data.size, offs.ctypes.data, sizes.ctypes.data, n, rect_ptr,
+                slot.data_ptr(), total, co.ctypes.data, q.ctypes.data, threads)
+        if rc:
+            raise smol.SmolError(smol.lib().smol_last_error().decode())
+
+    def rate(body) -> tuple[float, int]:
+        body()
+        k, t0 = 0, time.perf_counter()
+        while time.perf_counter() - t0 < secs:
+            body()
+            k += 1
+        return k * n / (time.perf_counter() - t0), k
+
+    whole, _ = rate(lambda: entropy(slots[0], None))
+    partial, _ = rate(lambda: entropy(slots[0], rects.ctypes.data))
+    print(f"[jpeg-files] entropy whole {whole:.0f} partial {partial:.0f} images/s",
+          file=sys.stderr, flush=True)
+    dev = torch.empty(total, dtype=torch.int16, device="cuda:0")
+    ws = torch.empty(smol.jpeg_workspace_bytes(w, h), dtype=torch.uint8, device="cuda:0")
+    out = torch.empty((n, 3, 224, 224), dtype=torch.float16, device="cuda:0")
+    stream = torch.cuda.current_stream()
+    qp = q.copy()
+    gpu_fn = smol.lib().smol_jpeg_roi_preprocess_batch
+    pref = ctypes.byref(params)
+
+    def gpu(src):
+        rc = gpu_fn(src.data_ptr(), total, co.ctypes.data, qp.ctypes.data, n, w.ctypes.data,
+                    h.ctypes.data, n, pref, None, ws.data_ptr(), ws.numel(), out.data_ptr(),
+                    stream.cuda_stream)
+        if rc:
+            raise smol.SmolError(smol.lib().smol_last_error().decode())
+
+    def timed_gpu(body, reps=50) -> float:
+        body()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            body()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps * 1e-3
+
+    entropy(slots[0], rects.ctypes.data)
+    qp[:] = q
+    h2d_s = timed_gpu(lambda: dev.copy_(slots[0], non_blocking=True))
+    gpu_s = timed_gpu(lambda: gpu(dev))
+    stages = {"entropy_partial": partial, "h2d": n / h2d_s, "gpu_decode_preprocess": n / gpu_s}
+    # pipelined: host decoding of the next batch runs while the copy and the
+    # GPU stages of the previous ones are in flight; a slot is reused once
+    # the copy that read it has completed
+    evs = [torch.cuda.Event() for _ in slots]
+    devs = [torch.empty(total, dtype=torch.int16, device="cuda:0") for _ in slots]
+    k, t0 = 0, time.perf_counter()
+    while time.perf_counter() - t0 < secs or k < 3:
+        s_ = k % len(slots)
+        evs[s_].synchronize()
+        entropy(slots[s_], rects.ctypes.data)
+        devs[s_].copy_(slots[s_], non_blocking=True)
+        evs[s_].record()
+        gpu(devs[s_])
+        k += 1
+    torch.cuda.synchronize()
+    measured = k * n / (time.perf_counter() - t0)
+    bottleneck = min(stages, key=stages.get)
+
+    def pil_full(i):
+        from PIL import Image
+        import io
+        im = Image.open(io.BytesIO(files[i]))
+        im.convert("RGB").load()
+
+    with ThreadPoolExecutor(threads) as ex:
+        pil, _ = rate(lambda: list(ex.map(pil_full, range(n))))
+    check = out.float().abs().sum().item()
+    print(json.dumps({
+        "metric": "JPEG files: images/s per stage and pipelined against their minimum (Eq. 4)",
+        "unit": "images/s", "n_gpus": 1, "data": "synthetic",
+        "config": {"workload": f"{n} photo-like 1280x720 4:2:0 JPEG streams, libjpeg quality "
+                               "75, restart marker every MCU row; Algorithm 1's rectangles for "
+                               "short side 256, crop 224x224, NCHW fp16",
+                   "avg_stream_bytes": int(sizes.mean()), "host_threads": threads,
+                   "coef_bytes_per_batch": 2 * total, "phase_seconds": secs},
+        "entropy_whole_images_per_s": round(whole, 1),
+        "entropy_partial_images_per_s": round(partial, 1),
+        "partial_speedup": round(partial / whole, 3),
+        "gpu_decode_preprocess_us_per_batch": round(gpu_s * 1e6, 1),
+        "h2d_us_per_batch": round(h2d_s * 1e6, 1),
+        "stage_images_per_s": {a: round(b, 1) for a, b in stages.items()},
+        "predicted_images_per_s": round(stages[bottleneck], 1),
+        "predicted_bottleneck": bottleneck,
+        "measured_images_per_s": round(measured, 1),
+        "measured_over_predicted": round(measured / stages[bottleneck], 3),
+        "context_libjpeg_full_decode_rgb_images_per_s": round(pil, 1),
+        "output_checksum": round(check, 1)}), flush=True)
+    return 0
+
+
 def main() -> int:
     args = parse()
     if args.gpus != 1:
@@ -540,6 +679,8 @@ def main() -> int:
         return 0
     if args.pipeline:
         return pipeline_experiment(args)
+    if args.jpeg_files:
+        return jpeg_files_experiment(args)
 
     import numpy as np
     import torch

@@ -6,12 +6,12 @@
  *
  * Scope: baseline JPEG with 4:2:0 subsampling (16 x 16 luma MCUs holding
  * four luma blocks and one Cb and one Cr block). The entropy decoding
- * (Huffman codes, zig-zag order) runs on the CPU, as in the paper's system,
- * and is not part of this library: its calls take the entropy decoder's
- * output, int16 coefficients per block in natural order (row = vertical
- * frequency v, column = horizontal frequency u), blocks in raster order
- * over the MCU-padded frame -- 2 ceil(W/16) x 2 ceil(H/16) luma blocks, then
- * ceil(W/16) x ceil(H/16) Cb blocks, then as many Cr blocks.
+ * (Huffman codes, zig-zag order) is bit-serial and runs on the CPU, as in
+ * the paper's system (smol_jpeg_entropy_decode_batch, host threads); the GPU
+ * calls take its output, int16 coefficients per block in natural order (row
+ * = vertical frequency v, column = horizontal frequency u), blocks in raster
+ * order over the MCU-padded frame -- 2 ceil(W/16) x 2 ceil(H/16) luma
+ * blocks, then ceil(W/16) x ceil(H/16) Cb blocks, then as many Cr blocks.
  *
  * Arithmetic (one definition, also the tests' reference): dequantised value
  * = coefficient x table entry (exact in fp32); the ITU-T T.81 A.3.3 inverse
@@ -52,8 +52,9 @@ int smol_jpeg_mcu_rect(int32_t width, int32_t height, const smol_params *p,
  *                 element coef_offsets[i] (HOST [n], multiples of 8),
  *                 smol_jpeg_coef_count of its size, all inside coef_elems
  *                 elements.
- *   qtables       HOST uint16[2][64]: the luma and the chroma dequantisation
- *                 tables, natural order, entries 1..255.
+ *   qtables       HOST uint16[n_qtables][2][64]: luma and chroma dequantisation
+ *                 tables, natural order, entries 1..255; n_qtables = 1 (one
+ *                 pair for every frame) or n (frame i's pair at 128 i).
  *   widths, heights  HOST [n], 1 .. SMOL_MAX_DIM.
  *   rects         HOST [n][4] (x, y, w, h, luma pixels, inside the frame;
  *                 x and y even) or NULL for whole frames. A block is decoded
@@ -67,7 +68,7 @@ int smol_jpeg_mcu_rect(int32_t width, int32_t height, const smol_params *p,
  *   stream        as for smol_preprocess_batch.
  * Returns SMOL_OK, SMOL_ERR_INVALID_ARG (nothing enqueued) or SMOL_ERR_HIP. */
 int smol_jpeg_decode_i420(const int16_t *coef, int64_t coef_elems, const int64_t *coef_offsets,
-                          const uint16_t *qtables, const int32_t *widths,
+                          const uint16_t *qtables, int32_t n_qtables, const int32_t *widths,
                           const int32_t *heights, const int32_t *rects, int32_t n,
                           uint8_t *out, int64_t out_bytes, const int64_t *y_offsets,
                           const int64_t *cb_offsets, const int64_t *cr_offsets, void *stream);
@@ -92,10 +93,65 @@ int64_t smol_jpeg_workspace_bytes(int32_t n, const int32_t *widths, const int32_
  * smol_jpeg_decode_i420. */
 int smol_jpeg_roi_preprocess_batch(const int16_t *coef, int64_t coef_elems,
                                    const int64_t *coef_offsets, const uint16_t *qtables,
-                                   const int32_t *widths, const int32_t *heights, int32_t n,
+                                   int32_t n_qtables, const int32_t *widths,
+                                   const int32_t *heights, int32_t n,
                                    const smol_params *p, const smol_options *opts,
                                    void *workspace, int64_t workspace_bytes, void *out,
                                    void *stream);
+
+/* ------------------------------------------------------------------------
+ * Entropy decoding on the host (ITU-T T.81: Annex B stream syntax, Annex C
+ * Huffman tables, Annex F sequential decoding). Accepted streams: baseline
+ * (SOF0) or extended sequential (SOF1) Huffman coding, 8-bit samples, three
+ * components sampled 2x2, 1x1, 1x1 (4:2:0) in one interleaved scan, Cb and
+ * Cr on one quantisation table, 8-bit table entries, optional restart
+ * intervals. Other JPEGs (progressive, arithmetic, other subsampling,
+ * grayscale) fail with SMOL_ERR_UNSUPPORTED; malformed streams with
+ * SMOL_ERR_INVALID_ARG.
+ * ---------------------------------------------------------------------- */
+
+/* What the headers of one stream say. */
+typedef struct smol_jpeg_info {
+    int32_t width, height;      /* luma pixels                             */
+    int32_t restart_interval;   /* MCUs per restart interval, 0: none      */
+    int32_t reserved;
+    int64_t scan_offset;        /* first byte of the entropy-coded data    */
+    uint16_t qtables[2][64];    /* luma, chroma tables, natural order      */
+} smol_jpeg_info;
+
+/* smol_jpeg_read_info -- parse the markers of one stream (HOST, `bytes`
+ * bytes) up to the start of its scan. Host only. */
+int smol_jpeg_read_info(const uint8_t *data, int64_t bytes, smol_jpeg_info *info);
+
+/* smol_jpeg_entropy_decode_batch -- entropy-decode n streams into the
+ * coefficient layout above, one stream per host thread at a time.
+ *
+ *   data          HOST: stream i is bytes offsets[i] .. offsets[i] + sizes[i]
+ *                 - 1 (HOST [n] tables), all inside data_bytes.
+ *   rects         HOST [n][4] (x, y, w, h in luma pixels, inside the frame)
+ *                 or NULL. With a rectangle only the MCUs from the first to
+ *                 the last that hold one of its pixels are decoded (restart
+ *                 intervals wholly before the first are skipped unread), and
+ *                 only blocks of the MCU rows and columns it spans are
+ *                 written: every block smol_jpeg_decode_i420 reads for the
+ *                 same rectangle (or for any rectangle inside those MCUs).
+ *                 Other blocks are left as they were.
+ *   coef          HOST int16: stream i's coefficients at element
+ *                 coef_offsets[i] (HOST [n]), smol_jpeg_coef_count of its
+ *                 size, inside coef_elems. Pinned memory lets the copy to the
+ *                 device run asynchronously.
+ *   qtables       HOST uint16 [n][2][64] receiving each stream's luma and
+ *                 chroma tables (natural order), or NULL.
+ *   threads       worker threads (<= 0: one per hardware thread); at most n
+ *                 and 256 run.
+ * Every stream is decoded; the call then returns SMOL_OK or the status of
+ * the lowest-numbered failing stream (its coefficients are incomplete), with
+ * "image i: ..." in smol_last_error(). */
+int smol_jpeg_entropy_decode_batch(const uint8_t *data, int64_t data_bytes,
+                                   const int64_t *offsets, const int64_t *sizes, int32_t n,
+                                   const int32_t *rects, int16_t *coef, int64_t coef_elems,
+                                   const int64_t *coef_offsets, uint16_t *qtables,
+                                   int32_t threads);
 
 #ifdef __cplusplus
 }

@@ -38,6 +38,7 @@ SOURCES = [
     "smol_pipeline.cpp",
     "smol_jpeg_kernels.hip",
     "smol_jpeg.cpp",
+    "smol_jpeg_entropy.cpp",
 ]
 HEADERS = ["smol_internal.h", "smol_device.h", "smol_rows.h"]
 

@@ -74,31 +74,34 @@ constexpr int kRowsMaxGroups = 4;
 constexpr int kRowsMaxWavesPerGroup = 4;
 
 // Block decoding (smol_jpeg_kernels.hip). A launch decodes up to
-// kJpegMaxRuns runs; a run is `frames` frames of one geometry whose
-// coefficients start at element coef (from JpegArgs::coef) and step by
-// coef_stride, and whose Y planes start at byte out (from JpegArgs::out) and
-// step by out_stride, the Cb and Cr planes cboff / croff bytes after the Y
-// plane. Coefficients: luma blocks bw x bh, then Cb and Cr (bw/2) x (bh/2),
-// 64 each, natural order; planes W x H and ceil(W/2) x ceil(H/2), tightly
-// pitched. Luma blocks lbx0 .. lbx0 + lnbx - 1 (rows likewise) and chroma
-// blocks cbx0 .. are decoded; jobs_end counts the kernel's jobs (groups of up
-// to eight blocks along a block row) of this and the earlier runs.
+// kJpegMaxRuns runs; a run is `frames` frames of one geometry and one pair of
+// dequantisation tables (q[qt]) whose coefficients start at element coef
+// (from JpegArgs::coef) and step by coef_stride, and whose Y planes start at
+// byte out (from JpegArgs::out) and step by out_stride, the Cb and Cr planes
+// cboff / croff bytes after the Y plane. Coefficients: luma blocks bw x bh,
+// then Cb and Cr (bw/2) x (bh/2), 64 each, natural order; planes W x H and
+// ceil(W/2) x ceil(H/2), tightly pitched. Luma blocks lbx0 .. lbx0 + lnbx - 1
+// (rows likewise) and chroma blocks cbx0 .. are decoded; jobs_end counts the
+// kernel's jobs (groups of up to eight blocks along a block row) of this and
+// the earlier runs.
 constexpr int kJpegMaxRuns = 24;
+constexpr int kJpegMaxTables = 8;
 struct JpegRun {
     long long coef, coef_stride, out, out_stride, cboff, croff;
     int32_t W, H, bw, bh;
     int16_t lbx0, lby0, lnbx, lnby, cbx0, cby0, cnbx, cnby;
-    int32_t frames, pad;
+    int32_t frames, qt;
     long long jobs_end;
 };
 struct JpegArgs {
     const int16_t *coef;
     uint8_t *out;
     int32_t runs, pad;
-    uint8_t q[2][64];  // luma, chroma dequantisation (entries 1..255)
-    float c[64];       // c[k * 8 + n] = fp32(C(k)/2 cos((2n + 1) k pi / 16))
+    uint8_t q[kJpegMaxTables][2][64];  // luma, chroma dequantisation (entries 1..255)
+    float c[64];                       // c[k * 8 + n] = fp32(C(k)/2 cos((2n + 1) k pi / 16))
     JpegRun run[kJpegMaxRuns];
 };
+static_assert(sizeof(JpegArgs) <= 4096, "kernel arguments of block decoding");
 int launch_jpeg_idct(const JpegArgs &a, int grid, void *stream);
 
 // The MCU-aligned rectangle (x, y, w, h) holding every luma and chroma sample

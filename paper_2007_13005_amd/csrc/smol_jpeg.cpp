@@ -82,7 +82,7 @@ int smol_jpeg_mcu_rect(int32_t width, int32_t height, const smol_params *p,
 }
 
 int smol_jpeg_decode_i420(const int16_t *coef, int64_t coef_elems, const int64_t *coef_offsets,
-                          const uint16_t *qtables, const int32_t *widths,
+                          const uint16_t *qtables, int32_t n_qtables, const int32_t *widths,
                           const int32_t *heights, const int32_t *rects, int32_t n,
                           uint8_t *out, int64_t out_bytes, const int64_t *y_offsets,
                           const int64_t *cb_offsets, const int64_t *cr_offsets, void *stream)
@@ -97,9 +97,13 @@ int smol_jpeg_decode_i420(const int16_t *coef, int64_t coef_elems, const int64_t
         return smol::set_error(SMOL_ERR_INVALID_ARG, "a NULL pointer or table");
     if (((uintptr_t)coef & 15) != 0)
         return smol::set_error(SMOL_ERR_INVALID_ARG, "coef must be 16-byte aligned");
-    for (int i = 0; i < 128; ++i)
+    if (n_qtables != 1 && n_qtables != n)
+        return smol::set_error(SMOL_ERR_INVALID_ARG, "n_qtables = %d: 1 or n (%d)", n_qtables,
+                               n);
+    for (int64_t i = 0; i < 128LL * n_qtables; ++i)
         if (qtables[i] < 1 || qtables[i] > 255)
-            return smol::set_error(SMOL_ERR_INVALID_ARG, "table entry %d = %d outside 1..255", i,
+            return smol::set_error(SMOL_ERR_INVALID_ARG, "table %lld entry %lld = %d outside "
+                                   "1..255", (long long)(i / 128), (long long)(i % 128),
                                    qtables[i]);
     std::vector<Blocks> blk((size_t)n);
     for (int32_t i = 0; i < n; ++i) {
@@ -139,9 +143,13 @@ int smol_jpeg_decode_i420(const int16_t *coef, int64_t coef_elems, const int64_t
 
     smol::JpegArgs a;
     std::memset(&a, 0, sizeof a);
-    for (int t = 0; t < 2; ++t)
-        for (int i = 0; i < 64; ++i)
-            a.q[t][i] = qtables[64 * t + i];
+    // frame i's luma and chroma tables
+    auto tables = [&](int32_t i) { return qtables + (n_qtables == 1 ? 0 : 128 * (size_t)i); };
+    auto same_tables = [&](int32_t i, int32_t j) {
+        return n_qtables == 1 || std::memcmp(tables(i), tables(j), 128 * sizeof(uint16_t)) == 0;
+    };
+    int ntables = 0;
+    int32_t table_frame[smol::kJpegMaxTables];  // a frame using each of the launch's tables
     const double pi = 3.14159265358979323846;
     for (int k = 0; k < 8; ++k)
         for (int m = 0; m < 8; ++m)
@@ -150,8 +158,8 @@ int smol_jpeg_decode_i420(const int16_t *coef, int64_t coef_elems, const int64_t
     const int cus = smol::device_cus();
     a.coef = coef;
     a.out = out;
-    // Runs of frames with one geometry and constant strides; up to
-    // kJpegMaxRuns runs share a launch.
+    // Runs of frames with one geometry, one pair of tables and constant
+    // strides; up to kJpegMaxRuns runs and kJpegMaxTables pairs share a launch.
     long long jobs = 0;
     auto flush = [&]() -> int {
         if (a.runs == 0)
@@ -160,6 +168,7 @@ int smol_jpeg_decode_i420(const int16_t *coef, int64_t coef_elems, const int64_t
         const int rc = smol::launch_jpeg_idct(a, grid, stream);
         a.runs = 0;
         jobs = 0;
+        ntables = 0;
         if (rc != (int)hipSuccess)
             return smol::set_error(SMOL_ERR_HIP, "block decoding launch: %s",
                                    hipGetErrorString((hipError_t)rc));
@@ -173,8 +182,24 @@ int smol_jpeg_decode_i420(const int16_t *coef, int64_t coef_elems, const int64_t
                coef_offsets[e] - coef_offsets[e - 1] == cs &&
                y_offsets[e] - y_offsets[e - 1] == os &&
                cb_offsets[e] - y_offsets[e] == cb_offsets[b] - y_offsets[b] &&
-               cr_offsets[e] - y_offsets[e] == cr_offsets[b] - y_offsets[b])
+               cr_offsets[e] - y_offsets[e] == cr_offsets[b] - y_offsets[b] &&
+               same_tables(e, b))
             ++e;
+        int qt = 0;
+        while (qt < ntables && !same_tables(table_frame[qt], b))
+            ++qt;
+        if (qt == smol::kJpegMaxTables) {
+            const int rc = flush();
+            if (rc != SMOL_OK)
+                return rc;
+            qt = 0;
+        }
+        if (qt == ntables) {
+            table_frame[ntables++] = b;
+            const uint16_t *t = tables(b);
+            for (int k = 0; k < 128; ++k)
+                a.q[qt][k / 64][k % 64] = (uint8_t)t[k];
+        }
         const Blocks &g = blk[(size_t)b];
         smol::JpegRun &r = a.run[a.runs];
         r.coef = coef_offsets[b];
@@ -196,7 +221,7 @@ int smol_jpeg_decode_i420(const int16_t *coef, int64_t coef_elems, const int64_t
         r.cnbx = (int16_t)g.cnbx;
         r.cnby = (int16_t)g.cnby;
         r.frames = e - b;
-        r.pad = 0;
+        r.qt = qt;
         // jobs of the kernel: groups of up to eight blocks along block rows
         jobs += ((long long)(g.lnbx + 7) / 8 * g.lnby + 2LL * ((g.cnbx + 7) / 8) * g.cnby) *
                 (long long)(e - b);
@@ -229,7 +254,8 @@ int64_t smol_jpeg_workspace_bytes(int32_t n, const int32_t *widths, const int32_
 
 int smol_jpeg_roi_preprocess_batch(const int16_t *coef, int64_t coef_elems,
                                    const int64_t *coef_offsets, const uint16_t *qtables,
-                                   const int32_t *widths, const int32_t *heights, int32_t n,
+                                   int32_t n_qtables, const int32_t *widths,
+                                   const int32_t *heights, int32_t n,
                                    const smol_params *p, const smol_options *opts,
                                    void *workspace, int64_t workspace_bytes, void *out,
                                    void *stream)
@@ -272,9 +298,9 @@ int smol_jpeg_roi_preprocess_batch(const int16_t *coef, int64_t coef_elems,
         ro[(size_t)i] = bo[(size_t)i] + ((W + 1) / 2) * ((H + 1) / 2);
         cur += frame_bytes(W, H);
     }
-    int rc = smol_jpeg_decode_i420(coef, coef_elems, coef_offsets, qtables, widths, heights,
-                                   rects.data(), n, (uint8_t *)workspace, workspace_bytes,
-                                   yo.data(), bo.data(), ro.data(), stream);
+    int rc = smol_jpeg_decode_i420(coef, coef_elems, coef_offsets, qtables, n_qtables, widths,
+                                   heights, rects.data(), n, (uint8_t *)workspace,
+                                   workspace_bytes, yo.data(), bo.data(), ro.data(), stream);
     if (rc)
         return rc;
     return smol_yuv420_preprocess_batch_ex((const uint8_t *)workspace, workspace_bytes,

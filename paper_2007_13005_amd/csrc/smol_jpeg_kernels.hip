@@ -77,7 +77,7 @@ __global__ void __launch_bounds__(64) jpeg_idct_kernel(JpegArgs a)
                              64LL * ((long long)by * gw + bx0 + bb);
         typedef short short8 __attribute__((ext_vector_type(8)));
         const short8 raw = *(const short8 *)(blk + 8 * row);
-        const uint8_t *q = comp == 0 ? a.q[0] : a.q[1];
+        const uint8_t *q = a.q[r.qt][comp == 0 ? 0 : 1];
         float d[8];
 #pragma unroll
         for (int u = 0; u < 8; ++u)

@@ -94,6 +94,12 @@ class PipelineStats(ctypes.Structure):
         return {name: getattr(self, name) for name, _ in self._fields_ if name != "reserved"}
 
 
+class JpegInfo(ctypes.Structure):
+    _fields_ = [("width", ctypes.c_int32), ("height", ctypes.c_int32),
+                ("restart_interval", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("scan_offset", ctypes.c_int64), ("qtables", ctypes.c_uint16 * 128)]
+
+
 # smol_consumer_fn: int (*)(void *user, const void *output, int32_t n, void *stream)
 CONSUMER = ctypes.CFUNCTYPE(ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
                             ctypes.c_void_p)
@@ -146,14 +152,19 @@ SIGNATURES = {
     "smol_jpeg_coef_count": (ctypes.c_int64, [ctypes.c_int32, ctypes.c_int32]),
     "smol_jpeg_mcu_rect": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(Params),
                                           ctypes.POINTER(Options), _vp]),
-    "smol_jpeg_decode_i420": (ctypes.c_int, [_vp, ctypes.c_int64, _vp, _vp, _vp, _vp, _vp,
-                                             ctypes.c_int32, _vp, ctypes.c_int64, _vp, _vp, _vp,
-                                             _vp]),
+    "smol_jpeg_decode_i420": (ctypes.c_int, [_vp, ctypes.c_int64, _vp, _vp, ctypes.c_int32,
+                                             _vp, _vp, _vp, ctypes.c_int32, _vp, ctypes.c_int64,
+                                             _vp, _vp, _vp, _vp]),
     "smol_jpeg_workspace_bytes": (ctypes.c_int64, [ctypes.c_int32, _vp, _vp]),
-    "smol_jpeg_roi_preprocess_batch": (ctypes.c_int, [_vp, ctypes.c_int64, _vp, _vp, _vp, _vp,
+    "smol_jpeg_roi_preprocess_batch": (ctypes.c_int, [_vp, ctypes.c_int64, _vp, _vp,
+                                                      ctypes.c_int32, _vp, _vp,
                                                       ctypes.c_int32, ctypes.POINTER(Params),
                                                       ctypes.POINTER(Options), _vp,
                                                       ctypes.c_int64, _vp, _vp]),
+    "smol_jpeg_read_info": (ctypes.c_int, [_vp, ctypes.c_int64, ctypes.POINTER(JpegInfo)]),
+    "smol_jpeg_entropy_decode_batch": (ctypes.c_int, [_vp, ctypes.c_int64, _vp, _vp,
+                                                      ctypes.c_int32, _vp, _vp, ctypes.c_int64,
+                                                      _vp, _vp, ctypes.c_int32]),
     "smol_set_tuning": (ctypes.c_int, [ctypes.POINTER(Tuning)]),
     "smol_last_plan": (ctypes.c_int, [ctypes.POINTER(Plan)]),
     "smol_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -465,11 +476,16 @@ def jpeg_mcu_rect(width: int, height: int, params: Params,
     return tuple(int(v) for v in r)
 
 
-def _qtables(qtables) -> np.ndarray:
+def _qtables(qtables, n: int) -> tuple[np.ndarray, int]:
+    """(flat uint16 tables, n_qtables): one (luma, chroma) pair for every
+    frame, shape (2, 64) or (128,), or one per frame, shape (n, 2, 64) or
+    (n, 128)."""
     q = _table(qtables, np.uint16).reshape(-1)
-    if q.size != 128:
-        raise ValueError("qtables must hold 2 x 64 entries (luma, chroma)")
-    return q
+    if q.size == 128:
+        return q, 1
+    if q.size == 128 * n:
+        return q, n
+    raise ValueError("qtables must hold 2 x 64 entries (luma, chroma), once or per frame")
 
 
 def jpeg_decode_i420(coef, coef_offsets, qtables, widths, heights, out, y_offsets, cb_offsets,
@@ -486,9 +502,9 @@ def jpeg_decode_i420(coef, coef_offsets, qtables, widths, heights, out, y_offset
     yo, bo, ro = (_table(v, np.int64) for v in (y_offsets, cb_offsets, cr_offsets))
     n = len(co)
     r = None if rects is None else _rois(rects, n)
-    q = _qtables(qtables)
+    q, nq = _qtables(qtables, n)
     _check(lib().smol_jpeg_decode_i420(
-        coef.data_ptr(), coef.numel(), co.ctypes.data, q.ctypes.data, w.ctypes.data,
+        coef.data_ptr(), coef.numel(), co.ctypes.data, q.ctypes.data, nq, w.ctypes.data,
         h.ctypes.data, None if r is None else r.ctypes.data, n, out.data_ptr(), out.numel(),
         yo.ctypes.data, bo.ctypes.data, ro.ctypes.data, _stream_handle(stream)))
 
@@ -509,17 +525,85 @@ def jpeg_roi_preprocess_batch(coef, coef_offsets, qtables, widths, heights, para
     co = _table(coef_offsets, np.int64)
     w, h = _table(widths, np.int32), _table(heights, np.int32)
     n = len(co)
-    q = _qtables(qtables)
+    q, nq = _qtables(qtables, n)
     need = jpeg_workspace_bytes(w, h)
     if workspace is None:
         workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=coef.device)
     out = _out_tensor(out, n, params, coef.device, options.layout if options else LAYOUT_NCHW)
     _check(lib().smol_jpeg_roi_preprocess_batch(
-        coef.data_ptr(), coef.numel(), co.ctypes.data, q.ctypes.data, w.ctypes.data,
+        coef.data_ptr(), coef.numel(), co.ctypes.data, q.ctypes.data, nq, w.ctypes.data,
         h.ctypes.data, n, ctypes.byref(params),
         None if options is None else ctypes.byref(options), workspace.data_ptr(),
         workspace.numel(), out.data_ptr(), _stream_handle(stream)))
     return out
+
+
+def jpeg_read_info(data: bytes) -> JpegInfo:
+    """The headers of one JPEG stream: size, restart interval, tables."""
+    buf = np.frombuffer(data, np.uint8)
+    info = JpegInfo()
+    _check(lib().smol_jpeg_read_info(buf.ctypes.data, buf.size, ctypes.byref(info)))
+    return info
+
+
+class JpegBatch:
+    """Entropy-decoded JPEG streams: ``coef`` (int16, host; a pinned torch
+    tensor when asked for), ``coef_offsets``, ``qtables`` (n, 2, 64),
+    ``widths``, ``heights`` and the ``rects`` they were decoded for."""
+
+    def __init__(self, coef, coef_offsets, qtables, widths, heights, rects):
+        self.coef, self.coef_offsets, self.qtables = coef, coef_offsets, qtables
+        self.widths, self.heights, self.rects = widths, heights, rects
+
+    @property
+    def n(self) -> int:
+        return len(self.widths)
+
+
+def jpeg_entropy_decode_batch(streams, rects=None, threads: int = 0,
+                              pinned: bool = False) -> JpegBatch:
+    """Entropy-decode JPEG streams (a list of bytes) on host threads into the
+    coefficient layout of the GPU calls. ``rects`` (n, 4) limits each stream
+    to the MCUs its rectangle needs (blocks outside stay zero)."""
+    n = len(streams)
+    sizes = np.asarray([len(b) for b in streams], np.int64)
+    offs = np.concatenate([[0], np.cumsum(sizes)[:-1]]).astype(np.int64) if n else sizes
+    data = np.frombuffer(b"".join(streams), np.uint8) if n else np.zeros(1, np.uint8)
+    infos = [jpeg_read_info(b) for b in streams]
+    w = np.asarray([i.width for i in infos], np.int32)
+    h = np.asarray([i.height for i in infos], np.int32)
+    counts = np.asarray([jpeg_coef_count(int(a), int(b)) for a, b in zip(w, h)], np.int64)
+    co = np.concatenate([[0], np.cumsum(counts)[:-1]]).astype(np.int64) if n else counts
+    total = max(int(counts.sum()), 8)
+    if pinned:
+        import torch
+        coef = torch.zeros(total, dtype=torch.int16, pin_memory=True)
+        ptr = coef.data_ptr()
+    else:
+        coef = np.zeros(total, np.int16)
+        ptr = coef.ctypes.data
+    q = np.zeros((max(n, 1), 2, 64), np.uint16)
+    r = None if rects is None else _rois(rects, n)
+    _check(lib().smol_jpeg_entropy_decode_batch(
+        data.ctypes.data, data.size, offs.ctypes.data, sizes.ctypes.data, n,
+        None if r is None else r.ctypes.data, ptr, total, co.ctypes.data, q.ctypes.data,
+        threads))
+    return JpegBatch(coef, co, q[:n], w, h, r)
+
+
+def jpeg_files_preprocess(streams, params: Params, options: Options | None = None,
+                          threads: int = 0, out=None, stream=None):
+    """Algorithm 1 from JPEG files: per stream the MCU rectangle of the
+    preprocessing, entropy decoding of only the MCUs it needs (host threads,
+    pinned memory), the copy to the device, then the partial block decoding
+    and the fused preprocessing on the GPU."""
+    import torch
+    infos = [jpeg_read_info(b) for b in streams]
+    rects = [jpeg_mcu_rect(i.width, i.height, params, options) for i in infos]
+    b = jpeg_entropy_decode_batch(streams, rects, threads, pinned=True)
+    dev = b.coef.to("cuda", non_blocking=True)
+    return jpeg_roi_preprocess_batch(dev, b.coef_offsets, b.qtables, b.widths, b.heights, params,
+                                     options, None, out, stream)
 
 
 def torch_int16():
@@ -572,12 +656,14 @@ class PreparedCall:
         self._jpeg = None
         if wl.kind == "jpeg":
             import torch
-            tabs = [_table(wl.coef_offsets, np.int64), _qtables(wl.qtables),
-                    _table(wl.widths, np.int32), _table(wl.heights, np.int32)]
+            q, nq = _qtables(wl.qtables, wl.n)
+            tabs = [_table(wl.coef_offsets, np.int64), q, _table(wl.widths, np.int32),
+                    _table(wl.heights, np.int32)]
             ws = torch.empty(max(jpeg_workspace_bytes(wl.widths, wl.heights), 16),
                              dtype=torch.uint8, device="cuda")
             self._keep = tabs
-            self._jpeg = ([t.ctypes.data for t in tabs], ws, ws.data_ptr(), ws.numel())
+            ptrs = [t.ctypes.data for t in tabs]
+            self._jpeg = (ptrs[:2] + [nq] + ptrs[2:], ws, ws.data_ptr(), ws.numel())
             self._fn = lib().smol_jpeg_roi_preprocess_batch
             self._pref = ctypes.byref(self.params)
             self._tail = [ctypes.byref(self.options)] if ex else [None]

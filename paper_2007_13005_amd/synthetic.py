@@ -342,8 +342,8 @@ def photo_ycbcr(rng, W: int, H: int) -> np.ndarray:
     """A W x H x 3 YCbCr uint8 image with photo-like structure: smooth
     luminance and colour fields, a few hard-edged rectangles and fine
     Gaussian grain."""
-    yy, xx = np.mgrid[0:H, 0:W].astype(np.float64)
-    img = np.empty((H, W, 3))
+    yy, xx = np.mgrid[0:H, 0:W].astype(np.float32)
+    img = np.empty((H, W, 3), np.float32)
     for c, amp in enumerate((70.0, 35.0, 35.0)):
         a, b, ph = rng.uniform(0.005, 0.08, 2), rng.uniform(0.005, 0.08, 2), rng.uniform(0, 6.3, 2)
         img[..., c] = 128 + amp * np.sin(a[0] * xx + b[0] * yy + ph[0]) * np.cos(
@@ -351,29 +351,43 @@ def photo_ycbcr(rng, W: int, H: int) -> np.ndarray:
     for _ in range(int(rng.integers(2, 6))):
         x0, y0 = int(rng.integers(0, W)), int(rng.integers(0, H))
         x1, y1 = x0 + int(rng.integers(1, max(2, W // 3))), y0 + int(rng.integers(1, max(2, H // 3)))
-        img[y0:y1, x0:x1] += rng.uniform(-50, 50, 3)
-    img += rng.normal(0.0, 4.0, img.shape)
+        img[y0:y1, x0:x1] += rng.uniform(-50, 50, 3).astype(np.float32)
+    img += rng.standard_normal(img.shape, dtype=np.float32) * 4.0
     return np.clip(np.rint(img), 0, 255).astype(np.uint8)
 
 
-def jpeg_files(sizes, seed: int, quality=75, restart_blocks: int = 0) -> list[bytes]:
+def jpeg_files(sizes, seed: int, quality=75, restart_blocks: int = 0,
+               distinct: int = 0) -> list[bytes]:
     """Baseline 4:2:0 JPEG streams of seeded photo-like images, encoded by
     libjpeg through PIL, standing in for a JPEG dataset. ``quality`` is one
     libjpeg quality for all or one per image; ``restart_blocks`` > 0 puts a
-    restart marker every that many MCUs."""
+    restart marker every that many MCUs; ``distinct`` > 0 encodes only the
+    first that many streams and repeats them in turn (same sizes needed)."""
     import io
 
     from PIL import Image
     rng = np.random.default_rng(seed)
     qs = [quality] * len(sizes) if np.isscalar(quality) else list(quality)
     out = []
-    for (W, H), q in zip(sizes, qs):
+    for i, ((W, H), q) in enumerate(zip(sizes, qs)):
+        if distinct and i >= distinct:
+            assert tuple(sizes[i % distinct]) == (W, H)
+            out.append(out[i % distinct])
+            continue
         b = io.BytesIO()
         kw = {"restart_marker_blocks": int(restart_blocks)} if restart_blocks else {}
         Image.fromarray(photo_ycbcr(rng, int(W), int(H)), "YCbCr").save(
             b, "JPEG", quality=int(q), subsampling=2, **kw)
         out.append(b.getvalue())
     return out
+
+
+def jpeg_file_batch(n: int = 128, width: int = 1280, height: int = 720, quality: int = 75,
+                    restart_blocks: int = 80, distinct: int = 32) -> list[bytes]:
+    """The file benchmark's batch: n photo-like width x height streams at one
+    libjpeg quality, a restart marker every MCU row of a 1280-wide frame,
+    ``distinct`` different images repeated."""
+    return jpeg_files([(width, height)] * n, SEED_BASE + 9, quality, restart_blocks, distinct)
 
 
 def c8(n: int = 128, height: int = 720, width: int = 1280) -> Workload:

@@ -33,7 +33,7 @@ def jpeg_planes(wl: synthetic.Workload):
         W, H = int(wl.widths[i]), int(wl.heights[i])
         k = oracle.jpeg_coef_count(W, H)
         c = coef[int(wl.coef_offsets[i]):int(wl.coef_offsets[i]) + k]
-        y, cb, cr = oracle.jpeg_decode_i420(c, wl.qtables[0], wl.qtables[1], W, H)
+        y, cb, cr = oracle.jpeg_decode_i420(c, *wl.frame_qtables(i), W, H)
         yo.append(cur)
         bo.append(cur + y.size)
         ro.append(cur + y.size + cb.size)

@@ -54,7 +54,7 @@ def _oracle_decode(wl, i, rect=None, fill=7):
     W, H = int(wl.widths[i]), int(wl.heights[i])
     k = oracle.jpeg_coef_count(W, H)
     c = wl.src.view(np.int16)[int(wl.coef_offsets[i]):int(wl.coef_offsets[i]) + k]
-    return oracle.jpeg_decode_i420(c, wl.qtables[0], wl.qtables[1], W, H, rect, fill=fill)
+    return oracle.jpeg_decode_i420(c, *wl.frame_qtables(i), W, H, rect, fill=fill)
 
 
 def test_whole_frame_decode_bit_exact():

@@ -1,0 +1,98 @@
+"""JPEG files end to end on the GPU: the library's host entropy decoding
+(partial, Algorithm 1's rectangles), per-frame dequantisation tables, block
+decoding and the fused preprocessing, against the oracle's whole-stream
+entropy decoding, whole-frame block decoding and preprocessing (marked gpu;
+run on an MI355X)."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2007_13005_amd import smol, synthetic
+from tests.gpu_util import assert_parity, note, run_oracle
+
+pytestmark = pytest.mark.gpu
+
+F32, F16 = synthetic.OUT_F32, synthetic.OUT_F16
+
+
+def _oracle_workload(name, files, S, C, dtype) -> synthetic.Workload:
+    """The oracle's entropy decoding of the streams, packed as a coefficient
+    workload (per-frame tables) for the oracle's block decoding and
+    preprocessing."""
+    coefs, qs, ws, hs = [], [], [], []
+    for f in files:
+        c, qy, qc, W, H = oracle.jpeg_entropy_decode(f)
+        coefs.append(c)
+        qs.append(np.stack([qy, qc]))
+        ws.append(W)
+        hs.append(H)
+    offs = np.cumsum([0] + [c.size for c in coefs[:-1]]).astype(np.int64)
+    return synthetic.Workload(name=name, kind="jpeg", src=np.concatenate(coefs).view(np.uint8),
+                              widths=np.asarray(ws, np.int32), heights=np.asarray(hs, np.int32),
+                              resize_short=S, crop_h=C, crop_w=C, out_dtype=dtype,
+                              coef_offsets=offs, qtables=np.stack(qs))
+
+
+def test_per_frame_tables_whole_decode():
+    """Twenty streams of twenty qualities (more table pairs than one launch
+    holds), decoded whole on the GPU with each frame's own tables."""
+    import torch
+    rng = np.random.default_rng(100)
+    sizes = [(int(rng.integers(1, 300)), int(rng.integers(1, 200))) for _ in range(20)]
+    quals = [5 * (k + 1) for k in range(20)]
+    files = synthetic.jpeg_files(sizes, 100, quals, restart_blocks=4)
+    b = smol.jpeg_entropy_decode_batch(files, threads=8)
+    assert len({q.tobytes() for q in b.qtables}) == 20
+    yo, bo, ro, cur = [], [], [], 0
+    for W, H in sizes:
+        Wc, Hc = (W + 1) // 2, (H + 1) // 2
+        yo.append(cur)
+        bo.append(cur + W * H)
+        ro.append(cur + W * H + Wc * Hc)
+        cur += W * H + 2 * Wc * Hc
+    out = torch.full((cur,), 3, dtype=torch.uint8, device="cuda:0")
+    coef = torch.from_numpy(b.coef).to("cuda:0")
+    smol.jpeg_decode_i420(coef, b.coef_offsets, b.qtables, b.widths, b.heights, out, yo, bo, ro)
+    torch.cuda.synchronize()
+    flat = out.cpu().numpy()
+    for i, f in enumerate(files):
+        c, qy, qc, W, H = oracle.jpeg_entropy_decode(f)
+        y, cb, cr = oracle.jpeg_decode_i420(c, qy, qc, W, H)
+        assert np.array_equal(flat[yo[i]:bo[i]], y.reshape(-1)), (i, sizes[i])
+        assert np.array_equal(flat[bo[i]:ro[i]], cb.reshape(-1)), (i, sizes[i])
+        assert np.array_equal(flat[ro[i]:ro[i] + cb.size], cr.reshape(-1)), (i, sizes[i])
+    note(f"    {len(files)} streams, {len(quals)} table pairs, decoded bit for bit")
+
+
+@pytest.mark.parametrize("layout", [smol.LAYOUT_NCHW, smol.LAYOUT_NHWC])
+@pytest.mark.parametrize("dtype", [F32, F16])
+@pytest.mark.parametrize("restart", [0, 2])
+def test_files_preprocess_end_to_end(dtype, layout, restart):
+    sizes = [(640, 480), (333, 517), (1280, 720), (300, 600), (451, 302), (257, 256)]
+    files = synthetic.jpeg_files(sizes, 101, [75, 90, 60, 75, 95, 80], restart_blocks=restart)
+    p = smol.make_params(256, 224, 224, synthetic.IMAGENET_MEAN_255, synthetic.IMAGENET_STD_255,
+                         dtype)
+    o = smol.make_options(layout=layout) if layout else None
+    got = smol.jpeg_files_preprocess(files, p, o, threads=4)
+    import torch
+    torch.cuda.synchronize()
+    wl = _oracle_workload("jpeg-files", files, 256, 224, dtype)
+    wl.layout = layout
+    stats = assert_parity(got.cpu().numpy(), run_oracle(wl), dtype, wl.name)
+    note(f"    files restart={restart}: {stats}")
+
+
+def test_files_at_benchmark_size():
+    """The file benchmark's batch: 128 streams of 1280x720 at quality 75,
+    restart markers every MCU row."""
+    files = synthetic.jpeg_file_batch()
+    p = smol.make_params(256, 224, 224, synthetic.IMAGENET_MEAN_255, synthetic.IMAGENET_STD_255,
+                         F16)
+    got = smol.jpeg_files_preprocess(files, p, threads=16)
+    import torch
+    torch.cuda.synchronize()
+    wl = _oracle_workload("jpeg-files-128", files, 256, 224, F16)
+    stats = assert_parity(got.cpu().numpy(), run_oracle(wl), F16, wl.name)
+    note(f"    {wl.name}: {stats}")
