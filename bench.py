@@ -563,14 +563,23 @@ def jpeg_files_experiment(args) -> int:
     data = np.frombuffer(b"".join(files), np.uint8)
     counts = np.asarray([smol.jpeg_coef_count(int(a), int(b)) for a, b in zip(w, h)], np.int64)
     co = np.concatenate([[0], np.cumsum(counts)[:-1]]).astype(np.int64)
-    total = int(counts.sum())
-    slots = [torch.zeros(total, dtype=torch.int16, pin_memory=True) for _ in range(3)]
+    total_frame = int(counts.sum())
+    # partial decoding stores each rectangle's MCU window only
+    wcounts = np.asarray([smol.jpeg_window_coef_count(int(a), int(b), r)
+                          for a, b, r in zip(w, h, rects)], np.int64)
+    cow = np.concatenate([[0], np.cumsum(wcounts)[:-1]]).astype(np.int64)
+    total = int(wcounts.sum())
+    slots = [torch.zeros(total_frame, dtype=torch.int16, pin_memory=True) for _ in range(3)]
     q = np.zeros((n, 2, 64), np.uint16)
     fn = smol.lib().smol_jpeg_entropy_decode_batch
 
     def entropy(slot, rect_ptr):
+        whole = rect_ptr is None
         rc = fn(data.ctypes.data, data.size, offs.ctypes.data, sizes.ctypes.data, n, rect_ptr,
-                slot.data_ptr(), total, co.ctypes.data, q.ctypes.data, threads)
+                slot.data_ptr(), total_frame if whole else total,
+                (co if whole else cow).ctypes.data,
+                smol.JPEG_COEF_FRAME if whole else smol.JPEG_COEF_WINDOW, q.ctypes.data,
+                threads)
         if rc:
             raise smol.SmolError(smol.lib().smol_last_error().decode())
 
@@ -595,9 +604,9 @@ def jpeg_files_experiment(args) -> int:
     pref = ctypes.byref(params)
 
     def gpu(src):
-        rc = gpu_fn(src.data_ptr(), total, co.ctypes.data, qp.ctypes.data, n, w.ctypes.data,
-                    h.ctypes.data, n, pref, None, ws.data_ptr(), ws.numel(), out.data_ptr(),
-                    stream.cuda_stream)
+        rc = gpu_fn(src.data_ptr(), total, cow.ctypes.data, qp.ctypes.data, n, w.ctypes.data,
+                    h.ctypes.data, n, smol.JPEG_COEF_WINDOW, pref, None, ws.data_ptr(),
+                    ws.numel(), out.data_ptr(), stream.cuda_stream)
         if rc:
             raise smol.SmolError(smol.lib().smol_last_error().decode())
 
@@ -614,7 +623,7 @@ def jpeg_files_experiment(args) -> int:
 
     entropy(slots[0], rects.ctypes.data)
     qp[:] = q
-    h2d_s = timed_gpu(lambda: dev.copy_(slots[0], non_blocking=True))
+    h2d_s = timed_gpu(lambda: dev.copy_(slots[0][:total], non_blocking=True))
     gpu_s = timed_gpu(lambda: gpu(dev))
     stages = {"entropy_partial": partial, "h2d": n / h2d_s, "gpu_decode_preprocess": n / gpu_s}
     # pipelined: host decoding of the next batch runs while the copy and the
@@ -627,7 +636,7 @@ def jpeg_files_experiment(args) -> int:
         s_ = k % len(slots)
         evs[s_].synchronize()
         entropy(slots[s_], rects.ctypes.data)
-        devs[s_].copy_(slots[s_], non_blocking=True)
+        devs[s_].copy_(slots[s_][:total], non_blocking=True)
         evs[s_].record()
         gpu(devs[s_])
         k += 1
@@ -651,7 +660,8 @@ def jpeg_files_experiment(args) -> int:
                                "75, restart marker every MCU row; Algorithm 1's rectangles for "
                                "short side 256, crop 224x224, NCHW fp16",
                    "avg_stream_bytes": int(sizes.mean()), "host_threads": threads,
-                   "coef_bytes_per_batch": 2 * total, "phase_seconds": secs},
+                   "coef_bytes_per_batch_frame_layout": 2 * total_frame,
+                   "coef_bytes_per_batch_window_layout": 2 * total, "phase_seconds": secs},
         "entropy_whole_images_per_s": round(whole, 1),
         "entropy_partial_images_per_s": round(partial, 1),
         "partial_speedup": round(partial / whole, 3),

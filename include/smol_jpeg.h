@@ -32,8 +32,24 @@
 extern "C" {
 #endif
 
+/* Coefficient layouts of a frame:
+ *   SMOL_JPEG_COEF_FRAME   the whole MCU-padded frame, as above;
+ *   SMOL_JPEG_COEF_WINDOW  only the MCU window of the frame's rectangle (MCU
+ *                          columns x/16 .. (x+w-1)/16 and rows likewise, for
+ *                          a rectangle x, y, w, h): its luma blocks in raster
+ *                          order (2 columns and 2 rows per MCU), then its Cb
+ *                          blocks, then its Cr blocks. Partial decoding needs
+ *                          nothing else, so this is what crosses to the GPU. */
+#define SMOL_JPEG_COEF_FRAME 0
+#define SMOL_JPEG_COEF_WINDOW 1
+
 /* int16 coefficients of one width x height frame (0 if a size is < 1). */
 int64_t smol_jpeg_coef_count(int32_t width, int32_t height);
+
+/* int16 coefficients of the MCU window of rect (HOST int32[4]; NULL: the
+ * whole frame) in a width x height frame; 0 if a size is < 1 or the
+ * rectangle leaves the frame. */
+int64_t smol_jpeg_window_coef_count(int32_t width, int32_t height, const int32_t *rect);
 
 /* smol_jpeg_mcu_rect -- Algorithm 1: the smallest rectangle aligned to the
  * 16 x 16 MCU grid (clipped to the frame) that holds every luma and chroma
@@ -49,9 +65,11 @@ int smol_jpeg_mcu_rect(int32_t width, int32_t height, const smol_params *p,
  * rectangle into I420 planes.
  *
  *   coef          DEVICE int16 coefficients, 16-byte aligned; frame i's at
- *                 element coef_offsets[i] (HOST [n], multiples of 8),
- *                 smol_jpeg_coef_count of its size, all inside coef_elems
- *                 elements.
+ *                 element coef_offsets[i] (HOST [n], multiples of 8), in
+ *                 coef_layout: SMOL_JPEG_COEF_FRAME (smol_jpeg_coef_count
+ *                 elements) or SMOL_JPEG_COEF_WINDOW (the MCU window of its
+ *                 rectangle, smol_jpeg_window_coef_count elements; rects
+ *                 needed), all inside coef_elems elements.
  *   qtables       HOST uint16[n_qtables][2][64]: luma and chroma dequantisation
  *                 tables, natural order, entries 1..255; n_qtables = 1 (one
  *                 pair for every frame) or n (frame i's pair at 128 i).
@@ -70,8 +88,9 @@ int smol_jpeg_mcu_rect(int32_t width, int32_t height, const smol_params *p,
 int smol_jpeg_decode_i420(const int16_t *coef, int64_t coef_elems, const int64_t *coef_offsets,
                           const uint16_t *qtables, int32_t n_qtables, const int32_t *widths,
                           const int32_t *heights, const int32_t *rects, int32_t n,
-                          uint8_t *out, int64_t out_bytes, const int64_t *y_offsets,
-                          const int64_t *cb_offsets, const int64_t *cr_offsets, void *stream);
+                          int32_t coef_layout, uint8_t *out, int64_t out_bytes,
+                          const int64_t *y_offsets, const int64_t *cb_offsets,
+                          const int64_t *cr_offsets, void *stream);
 
 /* Bytes of workspace smol_jpeg_roi_preprocess_batch needs: the n I420
  * frames packed back to back (frame i's Y, Cb, Cr planes at the running
@@ -84,6 +103,11 @@ int64_t smol_jpeg_workspace_bytes(int32_t n, const int32_t *widths, const int32_
  * smol_yuv420_preprocess_batch_ex over the workspace (no ROI; centred chroma
  * only). The output equals that of decoding whole frames.
  *
+ *   coef_layout SMOL_JPEG_COEF_FRAME, or SMOL_JPEG_COEF_WINDOW for
+ *               coefficients of each frame's MCU window, the rectangle being
+ *               smol_jpeg_mcu_rect under the same p and opts (as
+ *               smol_jpeg_entropy_decode_batch writes them given those
+ *               rectangles).
  *   workspace   DEVICE, 16-byte aligned, at least smol_jpeg_workspace_bytes;
  *               overlaps neither coef nor out.
  *   opts        resize_mode and layout as for the _ex calls; chroma_siting
@@ -94,7 +118,7 @@ int64_t smol_jpeg_workspace_bytes(int32_t n, const int32_t *widths, const int32_
 int smol_jpeg_roi_preprocess_batch(const int16_t *coef, int64_t coef_elems,
                                    const int64_t *coef_offsets, const uint16_t *qtables,
                                    int32_t n_qtables, const int32_t *widths,
-                                   const int32_t *heights, int32_t n,
+                                   const int32_t *heights, int32_t n, int32_t coef_layout,
                                    const smol_params *p, const smol_options *opts,
                                    void *workspace, int64_t workspace_bytes, void *out,
                                    void *stream);
@@ -137,9 +161,9 @@ int smol_jpeg_read_info(const uint8_t *data, int64_t bytes, smol_jpeg_info *info
  *                 same rectangle (or for any rectangle inside those MCUs).
  *                 Other blocks are left as they were.
  *   coef          HOST int16: stream i's coefficients at element
- *                 coef_offsets[i] (HOST [n]), smol_jpeg_coef_count of its
- *                 size, inside coef_elems. Pinned memory lets the copy to the
- *                 device run asynchronously.
+ *                 coef_offsets[i] (HOST [n]) in coef_layout (the window
+ *                 layout needs rects), inside coef_elems. Pinned memory lets
+ *                 the copy to the device run asynchronously.
  *   qtables       HOST uint16 [n][2][64] receiving each stream's luma and
  *                 chroma tables (natural order), or NULL.
  *   threads       worker threads (<= 0: one per hardware thread); at most n
@@ -150,8 +174,8 @@ int smol_jpeg_read_info(const uint8_t *data, int64_t bytes, smol_jpeg_info *info
 int smol_jpeg_entropy_decode_batch(const uint8_t *data, int64_t data_bytes,
                                    const int64_t *offsets, const int64_t *sizes, int32_t n,
                                    const int32_t *rects, int16_t *coef, int64_t coef_elems,
-                                   const int64_t *coef_offsets, uint16_t *qtables,
-                                   int32_t threads);
+                                   const int64_t *coef_offsets, int32_t coef_layout,
+                                   uint16_t *qtables, int32_t threads);
 
 #ifdef __cplusplus
 }

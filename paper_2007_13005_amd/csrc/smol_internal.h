@@ -78,9 +78,11 @@ constexpr int kRowsMaxWavesPerGroup = 4;
 // dequantisation tables (q[qt]) whose coefficients start at element coef
 // (from JpegArgs::coef) and step by coef_stride, and whose Y planes start at
 // byte out (from JpegArgs::out) and step by out_stride, the Cb and Cr planes
-// cboff / croff bytes after the Y plane. Coefficients: luma blocks bw x bh,
-// then Cb and Cr (bw/2) x (bh/2), 64 each, natural order; planes W x H and
-// ceil(W/2) x ceil(H/2), tightly pitched. Luma blocks lbx0 .. lbx0 + lnbx - 1
+// cboff / croff bytes after the Y plane (W x H and ceil(W/2) x ceil(H/2),
+// tightly pitched). The coefficients hold the blocks of MCU columns wx0 ..
+// wx0 + wmx - 1 and rows wy0 .. wy0 + wmy - 1 (the whole frame, or a
+// rectangle's MCU window): luma blocks 2 wmx x 2 wmy, then Cb and Cr
+// wmx x wmy, 64 each in natural order. Luma blocks lbx0 .. lbx0 + lnbx - 1
 // (rows likewise) and chroma blocks cbx0 .. are decoded; jobs_end counts the
 // kernel's jobs (groups of up to eight blocks along a block row) of this and
 // the earlier runs.
@@ -88,7 +90,8 @@ constexpr int kJpegMaxRuns = 24;
 constexpr int kJpegMaxTables = 8;
 struct JpegRun {
     long long coef, coef_stride, out, out_stride, cboff, croff;
-    int32_t W, H, bw, bh;
+    int32_t W, H;
+    int16_t wx0, wy0, wmx, wmy;
     int16_t lbx0, lby0, lnbx, lnby, cbx0, cby0, cnbx, cnby;
     int32_t frames, qt;
     long long jobs_end;

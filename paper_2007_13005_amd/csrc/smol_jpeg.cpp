@@ -18,10 +18,11 @@ namespace {
 struct Blocks {
     int32_t W, H, bw, bh;
     int32_t lbx0, lby0, lnbx, lnby, cbx0, cby0, cnbx, cnby;
+    int32_t wx0, wy0, wmx, wmy;  // MCU window the coefficients hold
     bool same_geometry(const Blocks &o) const
     {
         return W == o.W && H == o.H && lbx0 == o.lbx0 && lby0 == o.lby0 && lnbx == o.lnbx &&
-               lnby == o.lnby;
+               lnby == o.lnby && wx0 == o.wx0 && wy0 == o.wy0 && wmx == o.wmx && wmy == o.wmy;
     }
 };
 
@@ -50,6 +51,21 @@ int64_t coef_count(int64_t W, int64_t H)
     return 64 * (bw * bh + 2 * (bw / 2) * (bh / 2));
 }
 
+// MCU window of a rectangle: first column and row, columns, rows
+void mcu_window(int64_t W, int64_t H, const int32_t *rect, int64_t win[4])
+{
+    if (!rect) {
+        win[0] = win[1] = 0;
+        win[2] = (W + 15) / 16;
+        win[3] = (H + 15) / 16;
+        return;
+    }
+    win[0] = rect[0] / 16;
+    win[1] = rect[1] / 16;
+    win[2] = ((int64_t)rect[0] + rect[2] - 1) / 16 - win[0] + 1;
+    win[3] = ((int64_t)rect[1] + rect[3] - 1) / 16 - win[1] + 1;
+}
+
 int64_t frame_bytes(int64_t W, int64_t H)
 {
     return W * H + 2 * ((W + 1) / 2) * ((H + 1) / 2);
@@ -64,6 +80,18 @@ int64_t smol_jpeg_coef_count(int32_t width, int32_t height)
     if (width < 1 || height < 1)
         return 0;
     return coef_count(width, height);
+}
+
+int64_t smol_jpeg_window_coef_count(int32_t width, int32_t height, const int32_t *rect)
+{
+    if (width < 1 || height < 1)
+        return 0;
+    if (rect && (rect[0] < 0 || rect[1] < 0 || rect[2] < 1 || rect[3] < 1 ||
+                 (int64_t)rect[0] + rect[2] > width || (int64_t)rect[1] + rect[3] > height))
+        return 0;
+    int64_t win[4];
+    mcu_window(width, height, rect, win);
+    return 64 * 6 * win[2] * win[3];
 }
 
 int smol_jpeg_mcu_rect(int32_t width, int32_t height, const smol_params *p,
@@ -84,8 +112,9 @@ int smol_jpeg_mcu_rect(int32_t width, int32_t height, const smol_params *p,
 int smol_jpeg_decode_i420(const int16_t *coef, int64_t coef_elems, const int64_t *coef_offsets,
                           const uint16_t *qtables, int32_t n_qtables, const int32_t *widths,
                           const int32_t *heights, const int32_t *rects, int32_t n,
-                          uint8_t *out, int64_t out_bytes, const int64_t *y_offsets,
-                          const int64_t *cb_offsets, const int64_t *cr_offsets, void *stream)
+                          int32_t coef_layout, uint8_t *out, int64_t out_bytes,
+                          const int64_t *y_offsets, const int64_t *cb_offsets,
+                          const int64_t *cr_offsets, void *stream)
 {
     smol::clear_error();
     if (n < 0 || n > SMOL_MAX_BATCH)
@@ -105,16 +134,16 @@ int smol_jpeg_decode_i420(const int16_t *coef, int64_t coef_elems, const int64_t
             return smol::set_error(SMOL_ERR_INVALID_ARG, "table %lld entry %lld = %d outside "
                                    "1..255", (long long)(i / 128), (long long)(i % 128),
                                    qtables[i]);
+    if (coef_layout != SMOL_JPEG_COEF_FRAME && coef_layout != SMOL_JPEG_COEF_WINDOW)
+        return smol::set_error(SMOL_ERR_INVALID_ARG, "coef_layout %d unknown", coef_layout);
+    if (coef_layout == SMOL_JPEG_COEF_WINDOW && !rects)
+        return smol::set_error(SMOL_ERR_INVALID_ARG, "the window layout needs rects");
     std::vector<Blocks> blk((size_t)n);
     for (int32_t i = 0; i < n; ++i) {
         const int64_t W = widths[i], H = heights[i];
         if (W < 1 || H < 1 || W > SMOL_MAX_DIM || H > SMOL_MAX_DIM)
             return smol::set_error(SMOL_ERR_INVALID_ARG, "frame %d: size %lldx%lld outside 1..%d",
                                    i, (long long)W, (long long)H, SMOL_MAX_DIM);
-        if (coef_offsets[i] < 0 || coef_offsets[i] > coef_elems ||
-            coef_count(W, H) > coef_elems - coef_offsets[i])
-            return smol::set_error(SMOL_ERR_INVALID_ARG, "frame %d: coefficients outside coef",
-                                   i);
         if (coef_offsets[i] % 8 != 0)
             return smol::set_error(SMOL_ERR_INVALID_ARG, "frame %d: coefficient offset not a "
                                    "multiple of 8", i);
@@ -138,7 +167,19 @@ int smol_jpeg_decode_i420(const int16_t *coef, int64_t coef_elems, const int64_t
                                        (long long)rx, (long long)ry, (long long)rw,
                                        (long long)rh);
         }
-        blk[(size_t)i] = blocks_of(W, H, rx, ry, rw, rh);
+        Blocks &g = blk[(size_t)i];
+        g = blocks_of(W, H, rx, ry, rw, rh);
+        int64_t win[4];
+        mcu_window(W, H, coef_layout == SMOL_JPEG_COEF_WINDOW ? rects + 4 * (size_t)i : nullptr,
+                   win);
+        g.wx0 = (int32_t)win[0];
+        g.wy0 = (int32_t)win[1];
+        g.wmx = (int32_t)win[2];
+        g.wmy = (int32_t)win[3];
+        if (coef_offsets[i] < 0 || coef_offsets[i] > coef_elems ||
+            64 * 6 * win[2] * win[3] > coef_elems - coef_offsets[i])
+            return smol::set_error(SMOL_ERR_INVALID_ARG, "frame %d: coefficients outside coef",
+                                   i);
     }
 
     smol::JpegArgs a;
@@ -210,8 +251,10 @@ int smol_jpeg_decode_i420(const int16_t *coef, int64_t coef_elems, const int64_t
         r.croff = cr_offsets[b] - y_offsets[b];
         r.W = (int32_t)g.W;
         r.H = (int32_t)g.H;
-        r.bw = (int32_t)g.bw;
-        r.bh = (int32_t)g.bh;
+        r.wx0 = (int16_t)g.wx0;
+        r.wy0 = (int16_t)g.wy0;
+        r.wmx = (int16_t)g.wmx;
+        r.wmy = (int16_t)g.wmy;
         r.lbx0 = (int16_t)g.lbx0;
         r.lby0 = (int16_t)g.lby0;
         r.lnbx = (int16_t)g.lnbx;
@@ -256,9 +299,9 @@ int smol_jpeg_roi_preprocess_batch(const int16_t *coef, int64_t coef_elems,
                                    const int64_t *coef_offsets, const uint16_t *qtables,
                                    int32_t n_qtables, const int32_t *widths,
                                    const int32_t *heights, int32_t n,
-                                   const smol_params *p, const smol_options *opts,
-                                   void *workspace, int64_t workspace_bytes, void *out,
-                                   void *stream)
+                                   int32_t coef_layout, const smol_params *p,
+                                   const smol_options *opts, void *workspace,
+                                   int64_t workspace_bytes, void *out, void *stream)
 {
     smol::clear_error();
     if (n < 0 || n > SMOL_MAX_BATCH)
@@ -299,8 +342,9 @@ int smol_jpeg_roi_preprocess_batch(const int16_t *coef, int64_t coef_elems,
         cur += frame_bytes(W, H);
     }
     int rc = smol_jpeg_decode_i420(coef, coef_elems, coef_offsets, qtables, n_qtables, widths,
-                                   heights, rects.data(), n, (uint8_t *)workspace,
-                                   workspace_bytes, yo.data(), bo.data(), ro.data(), stream);
+                                   heights, rects.data(), n, coef_layout,
+                                   (uint8_t *)workspace, workspace_bytes, yo.data(), bo.data(),
+                                   ro.data(), stream);
     if (rc)
         return rc;
     return smol_yuv420_preprocess_batch_ex((const uint8_t *)workspace, workspace_bytes,

@@ -360,7 +360,7 @@ int64_t find_restart(const uint8_t *d, int64_t n, int64_t from, int64_t k)
 // Decode one stream's coefficients into `coef` (the library's layout). With
 // `rect`, only MCUs up to the last one holding its blocks are decoded, and
 // only blocks of the MCU columns and rows it spans are stored.
-int decode_image(const uint8_t *d, int64_t n, const int32_t *rect, int16_t *coef,
+int decode_image(const uint8_t *d, int64_t n, const int32_t *rect, bool window, int16_t *coef,
                  int64_t coef_room, uint16_t *q_out, Failure &f)
 {
     Header h;
@@ -369,10 +369,7 @@ int decode_image(const uint8_t *d, int64_t n, const int32_t *rect, int16_t *coef
         return rc;
     if (q_out)
         std::memcpy(q_out, h.q, sizeof h.q);
-    const int64_t mx = (h.W + 15) / 16, my = (h.H + 15) / 16, bw = 2 * mx;
-    if (coef_room < 64 * (4 * mx * my + 2 * mx * my))
-        return fail(f, SMOL_ERR_INVALID_ARG, "coefficients of a %dx%d frame outside coef", h.W,
-                    h.H);
+    const int64_t mx = (h.W + 15) / 16, my = (h.H + 15) / 16;
     int64_t x0 = 0, x1 = mx - 1, y0 = 0, y1 = my - 1;
     if (rect) {
         if (rect[0] < 0 || rect[1] < 0 || rect[2] < 1 || rect[3] < 1 ||
@@ -384,7 +381,13 @@ int decode_image(const uint8_t *d, int64_t n, const int32_t *rect, int16_t *coef
         y1 = ((int64_t)rect[1] + rect[3] - 1) / 16;
     }
     const int64_t first = y0 * mx + x0, last = y1 * mx + x1;
-    int16_t *planes[3] = {coef, coef + 64 * 4 * mx * my, coef + 64 * 5 * mx * my};
+    // the stored MCU grid: the whole frame or the rectangle's window
+    const int64_t gx0 = window ? x0 : 0, gy0 = window ? y0 : 0;
+    const int64_t gmx = window ? x1 - x0 + 1 : mx, gmy = window ? y1 - y0 + 1 : my;
+    if (coef_room < 64 * 6 * gmx * gmy)
+        return fail(f, SMOL_ERR_INVALID_ARG, "coefficients of a %dx%d frame outside coef", h.W,
+                    h.H);
+    int16_t *planes[3] = {coef, coef + 64 * 4 * gmx * gmy, coef + 64 * 5 * gmx * gmy};
     const Huff *dct[3], *act[3];
     for (int c = 0; c < 3; ++c) {
         dct[c] = &h.dc[h.dc_tab[c]];
@@ -429,9 +432,11 @@ int decode_image(const uint8_t *d, int64_t n, const int32_t *rect, int16_t *coef
         for (int b = 0; b < 6; ++b) {
             const int c = b < 4 ? 0 : b - 3;
             int16_t *z = scratch;
-            if (keep)
-                z = c == 0 ? planes[0] + 64 * ((2 * r + (b >> 1)) * bw + 2 * c0 + (b & 1))
-                           : planes[c] + 64 * mcu;
+            if (keep) {
+                const int64_t gr = r - gy0, gc = c0 - gx0;
+                z = c == 0 ? planes[0] + 64 * ((2 * gr + (b >> 1)) * 2 * gmx + 2 * gc + (b & 1))
+                           : planes[c] + 64 * (gr * gmx + gc);
+            }
             std::memset(z, 0, 64 * sizeof(int16_t));
             const int t = decode(s, *dct[c]);
             if (t < 0 || t > 11)
@@ -506,8 +511,8 @@ int smol_jpeg_read_info(const uint8_t *data, int64_t bytes, smol_jpeg_info *info
 int smol_jpeg_entropy_decode_batch(const uint8_t *data, int64_t data_bytes,
                                    const int64_t *offsets, const int64_t *sizes, int32_t n,
                                    const int32_t *rects, int16_t *coef, int64_t coef_elems,
-                                   const int64_t *coef_offsets, uint16_t *qtables,
-                                   int32_t threads)
+                                   const int64_t *coef_offsets, int32_t coef_layout,
+                                   uint16_t *qtables, int32_t threads)
 {
     smol::clear_error();
     if (n < 0 || n > SMOL_MAX_BATCH)
@@ -516,6 +521,10 @@ int smol_jpeg_entropy_decode_batch(const uint8_t *data, int64_t data_bytes,
         return SMOL_OK;
     if (!data || !offsets || !sizes || !coef || !coef_offsets)
         return smol::set_error(SMOL_ERR_INVALID_ARG, "a NULL pointer or table");
+    if (coef_layout != SMOL_JPEG_COEF_FRAME && coef_layout != SMOL_JPEG_COEF_WINDOW)
+        return smol::set_error(SMOL_ERR_INVALID_ARG, "coef_layout %d unknown", coef_layout);
+    if (coef_layout == SMOL_JPEG_COEF_WINDOW && !rects)
+        return smol::set_error(SMOL_ERR_INVALID_ARG, "the window layout needs rects");
     for (int32_t i = 0; i < n; ++i) {
         if (offsets[i] < 0 || sizes[i] < 0 || offsets[i] > data_bytes ||
             sizes[i] > data_bytes - offsets[i])
@@ -532,7 +541,8 @@ int smol_jpeg_entropy_decode_batch(const uint8_t *data, int64_t data_bytes,
     auto work = [&]() {
         for (int32_t i; (i = next.fetch_add(1)) < n;)
             decode_image(data + offsets[i], sizes[i], rects ? rects + 4 * (size_t)i : nullptr,
-                         coef + coef_offsets[i], coef_elems - coef_offsets[i],
+                         coef_layout == SMOL_JPEG_COEF_WINDOW, coef + coef_offsets[i],
+                         coef_elems - coef_offsets[i],
                          qtables ? qtables + 128 * (size_t)i : nullptr, fails[(size_t)i]);
     };
     if (t == 1) {

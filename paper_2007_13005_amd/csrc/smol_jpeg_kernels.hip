@@ -44,7 +44,7 @@ __global__ void __launch_bounds__(64) jpeg_idct_kernel(JpegArgs a)
         const long long local = job - (ri ? a.run[ri - 1].jobs_end : 0);
         const int f = (int)(local / per_frame);
         long long k = local - (long long)f * per_frame;
-        int comp, by, bx0, nb, gw, pw, ph;
+        int comp, by, bx0, nb, gw, ox, oy, pw, ph;  // (ox, oy): the stored grid's first block
         long long cbase, pbase;
         if (k < lum) {
             comp = 0;
@@ -52,7 +52,9 @@ __global__ void __launch_bounds__(64) jpeg_idct_kernel(JpegArgs a)
             const int gi = (int)(k % lg);
             bx0 = r.lbx0 + gi * kBlocksPerWave;
             nb = min(kBlocksPerWave, r.lnbx - gi * kBlocksPerWave);
-            gw = r.bw;
+            gw = 2 * r.wmx;
+            ox = 2 * r.wx0;
+            oy = 2 * r.wy0;
             cbase = 0;
             pbase = 0;
             pw = r.W;
@@ -65,8 +67,10 @@ __global__ void __launch_bounds__(64) jpeg_idct_kernel(JpegArgs a)
             const int gi = (int)(k % cg);
             bx0 = r.cbx0 + gi * kBlocksPerWave;
             nb = min(kBlocksPerWave, r.cnbx - gi * kBlocksPerWave);
-            gw = r.bw >> 1;
-            cbase = 64LL * r.bw * r.bh + (comp == 2 ? 64LL * (r.bw >> 1) * (r.bh >> 1) : 0);
+            gw = r.wmx;
+            ox = r.wx0;
+            oy = r.wy0;
+            cbase = 64LL * r.wmx * r.wmy * (comp == 1 ? 4 : 5);
             pbase = comp == 1 ? r.cboff : r.croff;
             pw = (r.W + 1) >> 1;
             ph = (r.H + 1) >> 1;
@@ -74,7 +78,7 @@ __global__ void __launch_bounds__(64) jpeg_idct_kernel(JpegArgs a)
         // lanes of blocks past the group's end repeat its last block
         const int bb = min(b, nb - 1);
         const int16_t *blk = a.coef + r.coef + f * r.coef_stride + cbase +
-                             64LL * ((long long)by * gw + bx0 + bb);
+                             64LL * ((long long)(by - oy) * gw + bx0 + bb - ox);
         typedef short short8 __attribute__((ext_vector_type(8)));
         const short8 raw = *(const short8 *)(blk + 8 * row);
         const uint8_t *q = a.q[r.qt][comp == 0 ? 0 : 1];

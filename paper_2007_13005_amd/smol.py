@@ -34,6 +34,8 @@ RESIZE_SHORT_CROP = 0
 RESIZE_DIRECT = 1
 LAYOUT_NCHW = 0
 LAYOUT_NHWC = 1
+JPEG_COEF_FRAME = 0
+JPEG_COEF_WINDOW = 1
 CHROMA_CENTER = 0
 CHROMA_LEFT = 1
 
@@ -153,18 +155,19 @@ SIGNATURES = {
     "smol_jpeg_mcu_rect": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(Params),
                                           ctypes.POINTER(Options), _vp]),
     "smol_jpeg_decode_i420": (ctypes.c_int, [_vp, ctypes.c_int64, _vp, _vp, ctypes.c_int32,
-                                             _vp, _vp, _vp, ctypes.c_int32, _vp, ctypes.c_int64,
-                                             _vp, _vp, _vp, _vp]),
+                                             _vp, _vp, _vp, ctypes.c_int32, ctypes.c_int32, _vp,
+                                             ctypes.c_int64, _vp, _vp, _vp, _vp]),
+    "smol_jpeg_window_coef_count": (ctypes.c_int64, [ctypes.c_int32, ctypes.c_int32, _vp]),
     "smol_jpeg_workspace_bytes": (ctypes.c_int64, [ctypes.c_int32, _vp, _vp]),
     "smol_jpeg_roi_preprocess_batch": (ctypes.c_int, [_vp, ctypes.c_int64, _vp, _vp,
-                                                      ctypes.c_int32, _vp, _vp,
+                                                      ctypes.c_int32, _vp, _vp, ctypes.c_int32,
                                                       ctypes.c_int32, ctypes.POINTER(Params),
                                                       ctypes.POINTER(Options), _vp,
                                                       ctypes.c_int64, _vp, _vp]),
     "smol_jpeg_read_info": (ctypes.c_int, [_vp, ctypes.c_int64, ctypes.POINTER(JpegInfo)]),
     "smol_jpeg_entropy_decode_batch": (ctypes.c_int, [_vp, ctypes.c_int64, _vp, _vp,
                                                       ctypes.c_int32, _vp, _vp, ctypes.c_int64,
-                                                      _vp, _vp, ctypes.c_int32]),
+                                                      _vp, ctypes.c_int32, _vp, ctypes.c_int32]),
     "smol_set_tuning": (ctypes.c_int, [ctypes.POINTER(Tuning)]),
     "smol_last_plan": (ctypes.c_int, [ctypes.POINTER(Plan)]),
     "smol_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -488,8 +491,14 @@ def _qtables(qtables, n: int) -> tuple[np.ndarray, int]:
     raise ValueError("qtables must hold 2 x 64 entries (luma, chroma), once or per frame")
 
 
+def jpeg_window_coef_count(width: int, height: int, rect=None) -> int:
+    r = None if rect is None else np.ascontiguousarray(rect, np.int32)
+    return int(lib().smol_jpeg_window_coef_count(width, height,
+                                                 None if r is None else r.ctypes.data))
+
+
 def jpeg_decode_i420(coef, coef_offsets, qtables, widths, heights, out, y_offsets, cb_offsets,
-                     cr_offsets, rects=None, stream=None):
+                     cr_offsets, rects=None, stream=None, coef_layout: int = JPEG_COEF_FRAME):
     """Decode the blocks of each frame meeting its rectangle (``rects`` (n, 4)
     or None for whole frames) from the int16 device tensor ``coef`` into the
     uint8 device tensor ``out`` at the given plane offsets."""
@@ -505,7 +514,8 @@ def jpeg_decode_i420(coef, coef_offsets, qtables, widths, heights, out, y_offset
     q, nq = _qtables(qtables, n)
     _check(lib().smol_jpeg_decode_i420(
         coef.data_ptr(), coef.numel(), co.ctypes.data, q.ctypes.data, nq, w.ctypes.data,
-        h.ctypes.data, None if r is None else r.ctypes.data, n, out.data_ptr(), out.numel(),
+        h.ctypes.data, None if r is None else r.ctypes.data, n, coef_layout, out.data_ptr(),
+        out.numel(),
         yo.ctypes.data, bo.ctypes.data, ro.ctypes.data, _stream_handle(stream)))
 
 
@@ -516,7 +526,7 @@ def jpeg_workspace_bytes(widths, heights) -> int:
 
 def jpeg_roi_preprocess_batch(coef, coef_offsets, qtables, widths, heights, params: Params,
                               options: Options | None = None, workspace=None, out=None,
-                              stream=None):
+                              stream=None, coef_layout: int = JPEG_COEF_FRAME):
     """Algorithm 1 end to end: only each frame's MCU rectangle decoded (into
     ``workspace``, allocated if omitted), then the I420 preprocessing."""
     import torch
@@ -532,7 +542,7 @@ def jpeg_roi_preprocess_batch(coef, coef_offsets, qtables, widths, heights, para
     out = _out_tensor(out, n, params, coef.device, options.layout if options else LAYOUT_NCHW)
     _check(lib().smol_jpeg_roi_preprocess_batch(
         coef.data_ptr(), coef.numel(), co.ctypes.data, q.ctypes.data, nq, w.ctypes.data,
-        h.ctypes.data, n, ctypes.byref(params),
+        h.ctypes.data, n, coef_layout, ctypes.byref(params),
         None if options is None else ctypes.byref(options), workspace.data_ptr(),
         workspace.numel(), out.data_ptr(), _stream_handle(stream)))
     return out
@@ -551,20 +561,22 @@ class JpegBatch:
     tensor when asked for), ``coef_offsets``, ``qtables`` (n, 2, 64),
     ``widths``, ``heights`` and the ``rects`` they were decoded for."""
 
-    def __init__(self, coef, coef_offsets, qtables, widths, heights, rects):
+    def __init__(self, coef, coef_offsets, qtables, widths, heights, rects, coef_layout):
         self.coef, self.coef_offsets, self.qtables = coef, coef_offsets, qtables
         self.widths, self.heights, self.rects = widths, heights, rects
+        self.coef_layout = coef_layout
 
     @property
     def n(self) -> int:
         return len(self.widths)
 
 
-def jpeg_entropy_decode_batch(streams, rects=None, threads: int = 0,
-                              pinned: bool = False) -> JpegBatch:
+def jpeg_entropy_decode_batch(streams, rects=None, threads: int = 0, pinned: bool = False,
+                              coef_layout: int = JPEG_COEF_FRAME) -> JpegBatch:
     """Entropy-decode JPEG streams (a list of bytes) on host threads into the
     coefficient layout of the GPU calls. ``rects`` (n, 4) limits each stream
-    to the MCUs its rectangle needs (blocks outside stay zero)."""
+    to the MCUs its rectangle needs (other blocks stay zero); with
+    ``JPEG_COEF_WINDOW`` only those MCUs are stored."""
     n = len(streams)
     sizes = np.asarray([len(b) for b in streams], np.int64)
     offs = np.concatenate([[0], np.cumsum(sizes)[:-1]]).astype(np.int64) if n else sizes
@@ -572,7 +584,14 @@ def jpeg_entropy_decode_batch(streams, rects=None, threads: int = 0,
     infos = [jpeg_read_info(b) for b in streams]
     w = np.asarray([i.width for i in infos], np.int32)
     h = np.asarray([i.height for i in infos], np.int32)
-    counts = np.asarray([jpeg_coef_count(int(a), int(b)) for a, b in zip(w, h)], np.int64)
+    r = None if rects is None else _rois(rects, n)
+    if coef_layout == JPEG_COEF_WINDOW:
+        if r is None:
+            raise ValueError("the window layout needs rects")
+        counts = np.asarray([jpeg_window_coef_count(int(a), int(b), r[i])
+                             for i, (a, b) in enumerate(zip(w, h))], np.int64)
+    else:
+        counts = np.asarray([jpeg_coef_count(int(a), int(b)) for a, b in zip(w, h)], np.int64)
     co = np.concatenate([[0], np.cumsum(counts)[:-1]]).astype(np.int64) if n else counts
     total = max(int(counts.sum()), 8)
     if pinned:
@@ -583,27 +602,27 @@ def jpeg_entropy_decode_batch(streams, rects=None, threads: int = 0,
         coef = np.zeros(total, np.int16)
         ptr = coef.ctypes.data
     q = np.zeros((max(n, 1), 2, 64), np.uint16)
-    r = None if rects is None else _rois(rects, n)
     _check(lib().smol_jpeg_entropy_decode_batch(
         data.ctypes.data, data.size, offs.ctypes.data, sizes.ctypes.data, n,
-        None if r is None else r.ctypes.data, ptr, total, co.ctypes.data, q.ctypes.data,
-        threads))
-    return JpegBatch(coef, co, q[:n], w, h, r)
+        None if r is None else r.ctypes.data, ptr, total, co.ctypes.data, coef_layout,
+        q.ctypes.data, threads))
+    return JpegBatch(coef, co, q[:n], w, h, r, coef_layout)
 
 
 def jpeg_files_preprocess(streams, params: Params, options: Options | None = None,
                           threads: int = 0, out=None, stream=None):
     """Algorithm 1 from JPEG files: per stream the MCU rectangle of the
     preprocessing, entropy decoding of only the MCUs it needs (host threads,
-    pinned memory), the copy to the device, then the partial block decoding
-    and the fused preprocessing on the GPU."""
-    import torch
+    pinned memory, only the rectangle's MCU window stored), the copy to the
+    device, then the partial block decoding and the fused preprocessing on
+    the GPU."""
     infos = [jpeg_read_info(b) for b in streams]
     rects = [jpeg_mcu_rect(i.width, i.height, params, options) for i in infos]
-    b = jpeg_entropy_decode_batch(streams, rects, threads, pinned=True)
+    b = jpeg_entropy_decode_batch(streams, rects, threads, pinned=True,
+                                  coef_layout=JPEG_COEF_WINDOW)
     dev = b.coef.to("cuda", non_blocking=True)
     return jpeg_roi_preprocess_batch(dev, b.coef_offsets, b.qtables, b.widths, b.heights, params,
-                                     options, None, out, stream)
+                                     options, None, out, stream, JPEG_COEF_WINDOW)
 
 
 def torch_int16():
@@ -702,8 +721,8 @@ class PreparedCall:
     def __call__(self, src_ptr: int, src_bytes: int, out_ptr: int, stream_handle) -> None:
         if self._jpeg:
             args, _, ws, ws_bytes = self._jpeg
-            _check(self._fn(src_ptr, src_bytes // 2, *args, self.n, self._pref, *self._tail, ws,
-                            ws_bytes, out_ptr, stream_handle))
+            _check(self._fn(src_ptr, src_bytes // 2, *args, self.n, JPEG_COEF_FRAME, self._pref,
+                            *self._tail, ws, ws_bytes, out_ptr, stream_handle))
             return
         if self._low:
             low, _, ws, ws_bytes = self._low

@@ -405,13 +405,15 @@ def test_jpeg_sizes_match_oracle():
     assert smol.jpeg_workspace_bytes(w, h) == ((15 + 2 * 2 * 3 + 256 + 2 * 64 + 15) // 16) * 16 + 16
 
 
-def _jpeg_decode_call(qt=None, rect=(0, 0, 16, 16), out_bytes=16 * 16 + 2 * 64, n=1, nq=1):
+def _jpeg_decode_call(qt=None, rect=(0, 0, 16, 16), out_bytes=16 * 16 + 2 * 64, n=1, nq=1,
+                      layout=0, coef_elems=10**6):
     q = np.ones(128, np.uint16) if qt is None else np.asarray(qt, np.uint16)
     w = np.asarray([16], np.int32)
     z = np.zeros(1, np.int64)
-    r = np.asarray(rect, np.int32)
-    rc = smol.lib().smol_jpeg_decode_i420(FAKE_SRC, 10**6, z.ctypes.data, q.ctypes.data, nq,
-                                          w.ctypes.data, w.ctypes.data, r.ctypes.data, n,
+    r = None if rect is None else np.asarray(rect, np.int32)
+    rc = smol.lib().smol_jpeg_decode_i420(FAKE_SRC, coef_elems, z.ctypes.data, q.ctypes.data, nq,
+                                          w.ctypes.data, w.ctypes.data,
+                                          None if r is None else r.ctypes.data, n, layout,
                                           FAKE_OUT, out_bytes, z.ctypes.data,
                                           np.asarray([256], np.int64).ctypes.data,
                                           np.asarray([320], np.int64).ctypes.data, None)
@@ -421,6 +423,9 @@ def _jpeg_decode_call(qt=None, rect=(0, 0, 16, 16), out_bytes=16 * 16 + 2 * 64, 
 @pytest.mark.parametrize("kw,needle", [
     (dict(qt=[0] + [1] * 127), "entry 0 = 0"), (dict(qt=[1] * 127 + [256]), "entry 127"),
     (dict(nq=2), "n_qtables = 2"), (dict(nq=0), "n_qtables = 0"),
+    (dict(layout=2), "coef_layout 2"), (dict(layout=1, rect=None), "needs rects"),
+    (dict(coef_elems=6 * 64 - 1), "outside coef"),
+    (dict(layout=1, rect=(0, 0, 8, 8), coef_elems=6 * 64 - 1), "outside coef"),
     (dict(rect=(1, 0, 8, 8)), "odd origin"), (dict(rect=(0, 0, 17, 16)), "rectangle"),
     (dict(out_bytes=383), "outside out"), (dict(n=-1), "n = -1"),
 ])
@@ -437,7 +442,7 @@ def _jpeg_roi_call(opts=None, ws=FAKE_OUT + 4096, ws_bytes=None, params=None):
     z = np.zeros(1, np.int64)
     need = smol.lib().smol_jpeg_workspace_bytes(1, w.ctypes.data, h.ctypes.data)
     rc = smol.lib().smol_jpeg_roi_preprocess_batch(
-        FAKE_SRC, 10**6, z.ctypes.data, q.ctypes.data, 1, w.ctypes.data, h.ctypes.data, 1,
+        FAKE_SRC, 10**6, z.ctypes.data, q.ctypes.data, 1, w.ctypes.data, h.ctypes.data, 1, 0,
         ctypes.byref(p), None if opts is None else ctypes.byref(opts), ws,
         need if ws_bytes is None else ws_bytes, FAKE_OUT, None)
     return rc, smol.lib().smol_last_error().decode()

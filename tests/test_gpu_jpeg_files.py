@@ -66,6 +66,46 @@ def test_per_frame_tables_whole_decode():
     note(f"    {len(files)} streams, {len(quals)} table pairs, decoded bit for bit")
 
 
+def test_window_layout_decode():
+    """Coefficients of only each rectangle's MCU window (the layout the file
+    path copies to the device) decode to the oracle's pixels inside the
+    rectangle and leave the rest of the planes alone; runs share launches."""
+    import torch
+    rng = np.random.default_rng(103)
+    sizes = [(int(rng.integers(1, 400)), int(rng.integers(1, 300))) for _ in range(40)]
+    sizes += [(640, 480)] * 8
+    files = synthetic.jpeg_files(sizes, 103, 80, restart_blocks=3)
+    rects = []
+    for W, H in sizes:
+        x, y = 2 * int(rng.integers(0, (W + 1) // 2)), 2 * int(rng.integers(0, (H + 1) // 2))
+        rects.append((x, y, int(rng.integers(1, W - x + 1)), int(rng.integers(1, H - y + 1))))
+    rects[-8:] = [rects[-8]] * 8
+    b = smol.jpeg_entropy_decode_batch(files, rects, threads=8,
+                                       coef_layout=smol.JPEG_COEF_WINDOW)
+    yo, bo, ro, cur = [], [], [], 0
+    for W, H in sizes:
+        Wc, Hc = (W + 1) // 2, (H + 1) // 2
+        yo.append(cur)
+        bo.append(cur + W * H)
+        ro.append(cur + W * H + Wc * Hc)
+        cur += W * H + 2 * Wc * Hc
+    out = torch.full((cur,), 7, dtype=torch.uint8, device="cuda:0")
+    smol.jpeg_decode_i420(torch.from_numpy(b.coef).to("cuda:0"), b.coef_offsets, b.qtables,
+                          b.widths, b.heights, out, yo, bo, ro, rects,
+                          coef_layout=smol.JPEG_COEF_WINDOW)
+    torch.cuda.synchronize()
+    flat = out.cpu().numpy()
+    for i, f in enumerate(files):
+        c, qy, qc, W, H = oracle.jpeg_entropy_decode(f)
+        exp = oracle.jpeg_decode_i420(c, qy, qc, W, H, rects[i], fill=7)
+        Wc, Hc = (W + 1) // 2, (H + 1) // 2
+        got = (flat[yo[i]:bo[i]].reshape(H, W), flat[bo[i]:ro[i]].reshape(Hc, Wc),
+               flat[ro[i]:ro[i] + Wc * Hc].reshape(Hc, Wc))
+        for k in range(3):
+            assert np.array_equal(got[k], exp[k]), (i, sizes[i], rects[i], k)
+    note(f"    {len(files)} frames decoded from their MCU windows")
+
+
 @pytest.mark.parametrize("layout", [smol.LAYOUT_NCHW, smol.LAYOUT_NHWC])
 @pytest.mark.parametrize("dtype", [F32, F16])
 @pytest.mark.parametrize("restart", [0, 2])

@@ -19,7 +19,7 @@ SIZES = [(203, 77), (64, 48), (33, 21), (1, 1), (17, 3), (640, 480), (16, 16), (
 SENTINEL = 0x5A5A
 
 
-def _decode_raw(files, rects=None, threads=0, fill=SENTINEL):
+def _decode_raw(files, rects=None, threads=0, fill=SENTINEL, layout=smol.JPEG_COEF_FRAME):
     """The C call on a sentinel-filled buffer: (rc, message, coef, offsets,
     qtables)."""
     n = len(files)
@@ -27,10 +27,12 @@ def _decode_raw(files, rects=None, threads=0, fill=SENTINEL):
     offs = np.concatenate([[0], np.cumsum(sizes)[:-1]]).astype(np.int64)
     data = np.frombuffer(b"".join(files), np.uint8)
     counts = []
-    for f in files:
+    for k, f in enumerate(files):
         try:
             i = smol.jpeg_read_info(f)
-            counts.append(smol.jpeg_coef_count(i.width, i.height))
+            counts.append(smol.jpeg_window_coef_count(i.width, i.height, rects[k])
+                          if layout == smol.JPEG_COEF_WINDOW else
+                          smol.jpeg_coef_count(i.width, i.height))
         except smol.SmolError:
             counts.append(64)
     co = np.concatenate([[0], np.cumsum(counts)[:-1]]).astype(np.int64)
@@ -40,7 +42,7 @@ def _decode_raw(files, rects=None, threads=0, fill=SENTINEL):
     rc = smol.lib().smol_jpeg_entropy_decode_batch(
         data.ctypes.data, data.size, offs.ctypes.data, sizes.ctypes.data, n,
         None if r is None else r.ctypes.data, coef.ctypes.data, coef.size, co.ctypes.data,
-        q.ctypes.data, threads)
+        layout, q.ctypes.data, threads)
     return rc, smol.lib().smol_last_error().decode(), coef, co, q
 
 
@@ -98,6 +100,32 @@ def test_partial_streams_write_only_their_mcus(restart):
         mask = np.ones(got[0].shape[:2], bool)
         mask[inside] = False
         assert (got[0][mask] == SENTINEL).all(), (i, rects[i])
+
+
+@pytest.mark.parametrize("restart", [0, 3])
+def test_window_layout_holds_the_mcu_window(restart):
+    """The window layout stores exactly the frame layout's blocks of the
+    rectangle's MCU window, packed."""
+    rng = np.random.default_rng(96 + restart)
+    files = synthetic.jpeg_files(SIZES, 96, 75, restart_blocks=restart)
+    rects = _random_rects(rng, SIZES)
+    rc, msg, coef, co, _ = _decode_raw(files, rects, threads=3, layout=smol.JPEG_COEF_WINDOW)
+    assert rc == 0, msg
+    for i, f in enumerate(files):
+        c, _, _, W, H = oracle.jpeg_entropy_decode(f)
+        x, y, w, h = rects[i]
+        mx0, mx1, my0, my1 = x // 16, (x + w - 1) // 16, y // 16, (y + h - 1) // 16
+        nx, ny = mx1 - mx0 + 1, my1 - my0 + 1
+        exp = _blocks(c, W, H)
+        k = smol.jpeg_window_coef_count(W, H, rects[i])
+        assert k == 64 * 6 * nx * ny
+        win = coef[co[i]:co[i] + k]
+        luma = win[:64 * 4 * nx * ny].reshape(2 * ny, 2 * nx, 64)
+        cb = win[64 * 4 * nx * ny:64 * 5 * nx * ny].reshape(ny, nx, 64)
+        cr = win[64 * 5 * nx * ny:].reshape(ny, nx, 64)
+        assert np.array_equal(luma, exp[0][2 * my0:2 * my1 + 2, 2 * mx0:2 * mx1 + 2]), i
+        assert np.array_equal(cb, exp[1][my0:my1 + 1, mx0:mx1 + 1]), i
+        assert np.array_equal(cr, exp[2][my0:my1 + 1, mx0:mx1 + 1]), i
 
 
 def test_algorithm1_rectangles_feed_the_block_decoder():
@@ -169,13 +197,13 @@ def test_argument_errors():
     coef = np.zeros(smol.jpeg_coef_count(16, 16), np.int16)
     z = np.zeros(1, np.int64)
 
-    def call(size=len(f), coef_elems=coef.size, n=1, rect=None):
+    def call(size=len(f), coef_elems=coef.size, n=1, rect=None, layout=0):
         s = np.asarray([size], np.int64)
         r = None if rect is None else np.asarray(rect, np.int32)
         rc = smol.lib().smol_jpeg_entropy_decode_batch(
             data.ctypes.data, data.size, z.ctypes.data, s.ctypes.data, n,
             None if r is None else r.ctypes.data, coef.ctypes.data, coef_elems, z.ctypes.data,
-            None, 1)
+            layout, None, 1)
         return rc, smol.lib().smol_last_error().decode()
 
     assert call()[0] == 0
@@ -184,6 +212,13 @@ def test_argument_errors():
     assert rc == smol.ERR_INVALID_ARG and "outside coef" in msg
     rc, msg = call(rect=(8, 8, 9, 8))
     assert rc == smol.ERR_INVALID_ARG and "rectangle" in msg
+    rc, msg = call(layout=1)
+    assert rc == smol.ERR_INVALID_ARG and "needs rects" in msg
+    rc, msg = call(layout=3, rect=(0, 0, 16, 16))
+    assert rc == smol.ERR_INVALID_ARG and "coef_layout 3" in msg
+    assert call(layout=1, rect=(0, 0, 16, 16), coef_elems=6 * 64)[0] == 0
+    rc, msg = call(layout=1, rect=(0, 0, 16, 16), coef_elems=6 * 64 - 1)
+    assert rc == smol.ERR_INVALID_ARG and "outside coef" in msg
     assert call(n=-1)[0] == smol.ERR_INVALID_ARG
     assert call(n=0)[0] == 0
     info = smol.JpegInfo()
