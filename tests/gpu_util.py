@@ -42,6 +42,24 @@ def jpeg_planes(wl: synthetic.Workload):
     return np.concatenate(bufs), yo, bo, ro
 
 
+def files_workload(name, files, S, C, dtype) -> synthetic.Workload:
+    """The oracle's entropy decoding of JPEG streams, packed as a coefficient
+    workload (per-frame tables) for the oracle's block decoding and
+    preprocessing (``run_oracle``)."""
+    coefs, qs, ws, hs = [], [], [], []
+    for f in files:
+        c, qy, qc, W, H = oracle.jpeg_entropy_decode(f)
+        coefs.append(c)
+        qs.append(np.stack([qy, qc]))
+        ws.append(W)
+        hs.append(H)
+    offs = np.cumsum([0] + [c.size for c in coefs[:-1]]).astype(np.int64)
+    return synthetic.Workload(name=name, kind="jpeg", src=np.concatenate(coefs).view(np.uint8),
+                              widths=np.asarray(ws, np.int32), heights=np.asarray(hs, np.int32),
+                              resize_short=S, crop_h=C, crop_w=C, out_dtype=dtype,
+                              coef_offsets=offs, qtables=np.stack(qs))
+
+
 def run_oracle(wl: synthetic.Workload) -> np.ndarray:
     if wl.kind == "jpeg":
         flat, yo, bo, ro = jpeg_planes(wl)

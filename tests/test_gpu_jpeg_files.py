@@ -10,29 +10,11 @@ import pytest
 
 import oracle
 from paper_2007_13005_amd import smol, synthetic
-from tests.gpu_util import assert_parity, note, run_oracle
+from tests.gpu_util import assert_parity, files_workload, note, run_oracle
 
 pytestmark = pytest.mark.gpu
 
 F32, F16 = synthetic.OUT_F32, synthetic.OUT_F16
-
-
-def _oracle_workload(name, files, S, C, dtype) -> synthetic.Workload:
-    """The oracle's entropy decoding of the streams, packed as a coefficient
-    workload (per-frame tables) for the oracle's block decoding and
-    preprocessing."""
-    coefs, qs, ws, hs = [], [], [], []
-    for f in files:
-        c, qy, qc, W, H = oracle.jpeg_entropy_decode(f)
-        coefs.append(c)
-        qs.append(np.stack([qy, qc]))
-        ws.append(W)
-        hs.append(H)
-    offs = np.cumsum([0] + [c.size for c in coefs[:-1]]).astype(np.int64)
-    return synthetic.Workload(name=name, kind="jpeg", src=np.concatenate(coefs).view(np.uint8),
-                              widths=np.asarray(ws, np.int32), heights=np.asarray(hs, np.int32),
-                              resize_short=S, crop_h=C, crop_w=C, out_dtype=dtype,
-                              coef_offsets=offs, qtables=np.stack(qs))
 
 
 def test_per_frame_tables_whole_decode():
@@ -118,7 +100,7 @@ def test_files_preprocess_end_to_end(dtype, layout, restart):
     got = smol.jpeg_files_preprocess(files, p, o, threads=4)
     import torch
     torch.cuda.synchronize()
-    wl = _oracle_workload("jpeg-files", files, 256, 224, dtype)
+    wl = files_workload("jpeg-files", files, 256, 224, dtype)
     wl.layout = layout
     stats = assert_parity(got.cpu().numpy(), run_oracle(wl), dtype, wl.name)
     note(f"    files restart={restart}: {stats}")
@@ -133,6 +115,6 @@ def test_files_at_benchmark_size():
     got = smol.jpeg_files_preprocess(files, p, threads=16)
     import torch
     torch.cuda.synchronize()
-    wl = _oracle_workload("jpeg-files-128", files, 256, 224, F16)
+    wl = files_workload("jpeg-files-128", files, 256, 224, F16)
     stats = assert_parity(got.cpu().numpy(), run_oracle(wl), F16, wl.name)
     note(f"    {wl.name}: {stats}")
