@@ -94,7 +94,7 @@ struct JpegRun {
     int16_t wx0, wy0, wmx, wmy;
     int16_t lbx0, lby0, lnbx, lnby, cbx0, cby0, cnbx, cnby;
     int32_t frames, qt;
-    long long jobs_end;
+    uint32_t jobs_end, pad;  // jobs_end < 2^31
 };
 struct JpegArgs {
     const int16_t *coef;

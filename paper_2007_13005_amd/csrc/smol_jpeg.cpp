@@ -226,6 +226,17 @@ int smol_jpeg_decode_i420(const int16_t *coef, int64_t coef_elems, const int64_t
                cr_offsets[e] - y_offsets[e] == cr_offsets[b] - y_offsets[b] &&
                same_tables(e, b))
             ++e;
+        // the kernel's job indices stay below 2^31: split runs and launches
+        const Blocks &g0 = blk[(size_t)b];
+        const long long per_frame =
+            (long long)(g0.lnbx + 7) / 8 * g0.lnby + 2LL * ((g0.cnbx + 7) / 8) * g0.cnby;
+        const long long max_jobs = 0x7fffffffLL;
+        if (jobs + per_frame > max_jobs) {
+            const int rc = flush();
+            if (rc != SMOL_OK)
+                return rc;
+        }
+        e = (int32_t)std::min<long long>(e, b + (max_jobs - jobs) / per_frame);
         int qt = 0;
         while (qt < ntables && !same_tables(table_frame[qt], b))
             ++qt;
@@ -266,9 +277,9 @@ int smol_jpeg_decode_i420(const int16_t *coef, int64_t coef_elems, const int64_t
         r.frames = e - b;
         r.qt = qt;
         // jobs of the kernel: groups of up to eight blocks along block rows
-        jobs += ((long long)(g.lnbx + 7) / 8 * g.lnby + 2LL * ((g.cnbx + 7) / 8) * g.cnby) *
-                (long long)(e - b);
-        r.jobs_end = jobs;
+        jobs += per_frame * (e - b);
+        r.jobs_end = (uint32_t)jobs;
+        r.pad = 0;
         if (++a.runs == smol::kJpegMaxRuns) {
             const int rc = flush();
             if (rc != SMOL_OK)

@@ -30,26 +30,28 @@ __global__ void __launch_bounds__(64) jpeg_idct_kernel(JpegArgs a)
 #pragma unroll
     for (int k = 0; k < 8; ++k)
         cr[k] = a.c[k * 8 + row];
-    const long long jobs = a.run[a.runs - 1].jobs_end;
+    // job indices stay below 2^31 (the host splits launches), so the job
+    // mapping runs in 32-bit unsigned arithmetic
+    const uint32_t jobs = a.run[a.runs - 1].jobs_end;
     int ri = 0;  // run of the current job (jobs ascend within a workgroup)
-    for (long long job = blockIdx.x; job < jobs; job += gridDim.x) {
+    for (uint32_t job = blockIdx.x; job < jobs; job += gridDim.x) {
         while (a.run[ri].jobs_end <= job)
             ++ri;
         const JpegRun &r = a.run[ri];
         // groups of up to eight blocks along each block row of the rectangle
-        const int lg = (r.lnbx + kBlocksPerWave - 1) / kBlocksPerWave;
-        const int cg = (r.cnbx + kBlocksPerWave - 1) / kBlocksPerWave;
-        const long long lum = (long long)lg * r.lnby, chr = (long long)cg * r.cnby;
-        const long long per_frame = lum + 2 * chr;
-        const long long local = job - (ri ? a.run[ri - 1].jobs_end : 0);
-        const int f = (int)(local / per_frame);
-        long long k = local - (long long)f * per_frame;
+        const uint32_t lg = ((uint32_t)r.lnbx + kBlocksPerWave - 1) / kBlocksPerWave;
+        const uint32_t cg = ((uint32_t)r.cnbx + kBlocksPerWave - 1) / kBlocksPerWave;
+        const uint32_t lum = lg * (uint32_t)r.lnby, chr = cg * (uint32_t)r.cnby;
+        const uint32_t per_frame = lum + 2 * chr;
+        const uint32_t local = job - (ri ? a.run[ri - 1].jobs_end : 0);
+        const uint32_t f = local / per_frame;
+        uint32_t k = local - f * per_frame;
         int comp, by, bx0, nb, gw, ox, oy, pw, ph;  // (ox, oy): the stored grid's first block
         long long cbase, pbase;
         if (k < lum) {
             comp = 0;
             by = r.lby0 + (int)(k / lg);
-            const int gi = (int)(k % lg);
+            const int gi = (int)(k - (k / lg) * lg);
             bx0 = r.lbx0 + gi * kBlocksPerWave;
             nb = min(kBlocksPerWave, r.lnbx - gi * kBlocksPerWave);
             gw = 2 * r.wmx;
@@ -64,7 +66,7 @@ __global__ void __launch_bounds__(64) jpeg_idct_kernel(JpegArgs a)
             comp = k < chr ? 1 : 2;
             k -= comp == 1 ? 0 : chr;
             by = r.cby0 + (int)(k / cg);
-            const int gi = (int)(k % cg);
+            const int gi = (int)(k - (k / cg) * cg);
             bx0 = r.cbx0 + gi * kBlocksPerWave;
             nb = min(kBlocksPerWave, r.cnbx - gi * kBlocksPerWave);
             gw = r.wmx;
