@@ -58,15 +58,18 @@ typedef struct smol_pipeline smol_pipeline;
  *   input_bytes   bytes of each host / device input buffer, >= 1
  *   output_bytes  bytes of each device output buffer, >= 16
  *   copy_streams  copy streams, 0 .. 4 (0: one)
- * Device memory held: slots * (input_bytes + output_bytes); pinned host
- * memory: slots * input_bytes. */
+ *   workspace_bytes  device workspace per slot for smol_pipeline_submit_jpeg
+ *                 (at least smol_jpeg_workspace_bytes of its batches), >= 0
+ * Device memory held: slots * (input_bytes + output_bytes + workspace_bytes);
+ * pinned host memory: slots * input_bytes. */
 typedef struct smol_pipeline_config {
     int32_t slots;
     int32_t streams;
     int64_t input_bytes;
     int64_t output_bytes;
     int32_t copy_streams;
-    int32_t reserved[3];  /* must be zero */
+    int32_t reserved;  /* must be zero */
+    int64_t workspace_bytes;
 } smol_pipeline_config;
 
 /* The DNN stage, called on the submitting thread right after the
@@ -120,6 +123,19 @@ int smol_pipeline_submit_yuv420(smol_pipeline *p, int32_t slot, int64_t bytes,
                                 const int32_t *heights, const int32_t *rois, int32_t n,
                                 const smol_params *params, const smol_options *opts,
                                 smol_consumer_fn consumer, void *user);
+
+/* smol_pipeline_submit_jpeg -- the same for entropy-decoded JPEG batches
+ * (smol_jpeg_roi_preprocess_batch): the slot's host buffer holds the int16
+ * coefficients (`bytes` even) as smol_jpeg_entropy_decode_batch wrote them,
+ * tables relative to its start; the slot's workspace (workspace_bytes at
+ * creation, nonzero) takes the decoded planes. Producer threads can thus
+ * entropy-decode straight into the pinned slot they acquired (section 6.1's
+ * decoder threads feeding the queue). */
+int smol_pipeline_submit_jpeg(smol_pipeline *p, int32_t slot, int64_t bytes,
+                              const int64_t *coef_offsets, const uint16_t *qtables,
+                              int32_t n_qtables, const int32_t *widths, const int32_t *heights,
+                              int32_t n, int32_t coef_layout, const smol_params *params,
+                              const smol_options *opts, smol_consumer_fn consumer, void *user);
 
 /* smol_pipeline_drain -- wait until every submission so far has completed
  * and its slot is free. */

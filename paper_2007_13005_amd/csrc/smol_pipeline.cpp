@@ -15,6 +15,7 @@
 
 #include "smol.h"
 #include "smol_internal.h"
+#include "smol_jpeg.h"
 #include "smol_pipeline.h"
 
 namespace {
@@ -25,6 +26,7 @@ struct Slot {
     uint8_t *host = nullptr;    // pinned, input_bytes
     uint8_t *dev_in = nullptr;  // input_bytes
     uint8_t *dev_out = nullptr; // output_bytes
+    uint8_t *dev_ws = nullptr;  // workspace_bytes (JPEG submissions)
     hipEvent_t copied = nullptr; // after the slot's input copy
     hipEvent_t done = nullptr;  // after the slot's last consumer
     SlotState state = kFree;
@@ -41,6 +43,7 @@ struct smol_pipeline {
     int device = 0;
     int64_t input_bytes = 0;
     int64_t output_bytes = 0;
+    int64_t workspace_bytes = 0;
     std::vector<hipStream_t> streams;       // preprocessing and consumers
     std::vector<hipStream_t> copy_streams;  // host-to-device copies
     std::vector<Slot> slots;
@@ -70,6 +73,8 @@ void free_all(smol_pipeline *p)
             (void)hipFree(s.dev_in);
         if (s.dev_out)
             (void)hipFree(s.dev_out);
+        if (s.dev_ws)
+            (void)hipFree(s.dev_ws);
     }
     for (hipStream_t st : p->streams)
         if (st)
@@ -147,9 +152,9 @@ int64_t output_bytes_of(const smol_params *params, int32_t n)
     return (int64_t)n * 3 * params->crop_h * params->crop_w * esz;
 }
 
-// Shared part of both submissions: argument checks, the copy, the
-// preprocessing call `pre(src, bytes, out, stream)`, the consumer and the
-// completion event.
+// Shared part of the submissions: argument checks, the copy, the
+// preprocessing call `pre(src, bytes, out, workspace, stream)`, the consumer
+// and the completion event.
 template <class Pre>
 int submit(smol_pipeline *p, int32_t slot, int64_t bytes, int32_t n, const smol_params *params,
            smol_consumer_fn consumer, void *user, Pre pre)
@@ -197,7 +202,7 @@ int submit(smol_pipeline *p, int32_t slot, int64_t bytes, int32_t n, const smol_
         p->cv.notify_all();
         return hip_error(e2 != hipSuccess ? e2 : e, "copy event");
     }
-    int rc = pre(sl.dev_in, bytes, sl.dev_out, s);
+    int rc = pre(sl.dev_in, bytes, sl.dev_out, sl.dev_ws, s);
     std::string msg = rc ? smol_last_error() : "";
     if (!rc && consumer) {
         const int c = consumer(user, sl.dev_out, n, s);
@@ -253,12 +258,15 @@ int smol_pipeline_create(const smol_pipeline_config *c, smol_pipeline **out)
     if (c->input_bytes < 1 || c->output_bytes < 16)
         return smol::set_error(SMOL_ERR_INVALID_ARG, "input_bytes %lld < 1 or output_bytes %lld "
                                "< 16", (long long)c->input_bytes, (long long)c->output_bytes);
-    for (int i = 0; i < 3; ++i)
-        if (c->reserved[i])
-            return smol::set_error(SMOL_ERR_INVALID_ARG, "reserved[%d] is not zero", i);
+    if (c->reserved)
+        return smol::set_error(SMOL_ERR_INVALID_ARG, "reserved is not zero");
+    if (c->workspace_bytes < 0)
+        return smol::set_error(SMOL_ERR_INVALID_ARG, "workspace_bytes %lld < 0",
+                               (long long)c->workspace_bytes);
     smol_pipeline *p = new smol_pipeline();
     p->input_bytes = c->input_bytes;
     p->output_bytes = c->output_bytes;
+    p->workspace_bytes = c->workspace_bytes;
     hipError_t e = hipGetDevice(&p->device);
     p->slots.resize((size_t)c->slots);
     p->streams.resize((size_t)c->streams, nullptr);
@@ -274,6 +282,8 @@ int smol_pipeline_create(const smol_pipeline_config *c, smol_pipeline **out)
             e = hipMalloc((void **)&s.dev_in, (size_t)c->input_bytes);
         if (e == hipSuccess)
             e = hipMalloc((void **)&s.dev_out, (size_t)c->output_bytes);
+        if (e == hipSuccess && c->workspace_bytes > 0)
+            e = hipMalloc((void **)&s.dev_ws, (size_t)c->workspace_bytes);
         if (e == hipSuccess)
             e = hipEventCreateWithFlags(&s.done, hipEventDisableTiming);
         if (e == hipSuccess)
@@ -363,7 +373,7 @@ int smol_pipeline_submit(smol_pipeline *p, int32_t slot, int64_t bytes, const in
                          smol_consumer_fn consumer, void *user)
 {
     return submit(p, slot, bytes, n, params, consumer, user,
-                  [&](const uint8_t *src, int64_t nb, void *out, hipStream_t s) {
+                  [&](const uint8_t *src, int64_t nb, void *out, void *, hipStream_t s) {
                       return smol_preprocess_batch_ex(src, nb, offsets, widths, heights,
                                                       row_pitch, rois, n, params, opts, out, s);
                   });
@@ -377,10 +387,33 @@ int smol_pipeline_submit_yuv420(smol_pipeline *p, int32_t slot, int64_t bytes,
                                 smol_consumer_fn consumer, void *user)
 {
     return submit(p, slot, bytes, n, params, consumer, user,
-                  [&](const uint8_t *src, int64_t nb, void *out, hipStream_t s) {
+                  [&](const uint8_t *src, int64_t nb, void *out, void *, hipStream_t s) {
                       return smol_yuv420_preprocess_batch_ex(src, nb, y_offsets, cb_offsets,
                                                              cr_offsets, widths, heights, rois,
                                                              n, params, opts, out, s);
+                  });
+}
+
+int smol_pipeline_submit_jpeg(smol_pipeline *p, int32_t slot, int64_t bytes,
+                              const int64_t *coef_offsets, const uint16_t *qtables,
+                              int32_t n_qtables, const int32_t *widths, const int32_t *heights,
+                              int32_t n, int32_t coef_layout, const smol_params *params,
+                              const smol_options *opts, smol_consumer_fn consumer, void *user)
+{
+    if (p && p->workspace_bytes == 0) {
+        smol::clear_error();
+        return smol::set_error(SMOL_ERR_INVALID_ARG, "the pipeline has no workspace "
+                               "(workspace_bytes 0 at creation)");
+    }
+    if (bytes % 2)
+        return smol::set_error(SMOL_ERR_INVALID_ARG, "bytes %lld: whole int16 coefficients "
+                               "needed", (long long)bytes);
+    return submit(p, slot, bytes, n, params, consumer, user,
+                  [&](const uint8_t *src, int64_t nb, void *out, void *ws, hipStream_t s) {
+                      return smol_jpeg_roi_preprocess_batch(
+                          (const int16_t *)src, nb / 2, coef_offsets, qtables, n_qtables,
+                          widths, heights, n, coef_layout, params, opts, ws,
+                          p->workspace_bytes, out, s);
                   });
 }
 

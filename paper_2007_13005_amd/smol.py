@@ -84,7 +84,8 @@ class Plan(ctypes.Structure):
 class PipelineConfig(ctypes.Structure):
     _fields_ = [("slots", ctypes.c_int32), ("streams", ctypes.c_int32),
                 ("input_bytes", ctypes.c_int64), ("output_bytes", ctypes.c_int64),
-                ("copy_streams", ctypes.c_int32), ("reserved", ctypes.c_int32 * 3)]
+                ("copy_streams", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("workspace_bytes", ctypes.c_int64)]
 
 
 class PipelineStats(ctypes.Structure):
@@ -149,6 +150,10 @@ SIGNATURES = {
                                                    _vp, _vp, _vp, _vp, ctypes.c_int32,
                                                    ctypes.POINTER(Params),
                                                    ctypes.POINTER(Options), CONSUMER, _vp]),
+    "smol_pipeline_submit_jpeg": (ctypes.c_int, [_vp, ctypes.c_int32, ctypes.c_int64, _vp, _vp,
+                                                 ctypes.c_int32, _vp, _vp, ctypes.c_int32,
+                                                 ctypes.c_int32, ctypes.POINTER(Params),
+                                                 ctypes.POINTER(Options), CONSUMER, _vp]),
     "smol_pipeline_drain": (ctypes.c_int, [_vp]),
     "smol_pipeline_get_stats": (ctypes.c_int, [_vp, ctypes.POINTER(PipelineStats)]),
     "smol_jpeg_coef_count": (ctypes.c_int64, [ctypes.c_int32, ctypes.c_int32]),
@@ -742,10 +747,11 @@ class Pipeline:
     stream) run in stream order while other slots are filled."""
 
     def __init__(self, slots: int, streams: int, input_bytes: int, output_bytes: int,
-                 copy_streams: int = 1):
+                 copy_streams: int = 1, workspace_bytes: int = 0):
         cfg = PipelineConfig()
         cfg.slots, cfg.streams, cfg.copy_streams = slots, streams, copy_streams
         cfg.input_bytes, cfg.output_bytes = input_bytes, output_bytes
+        cfg.workspace_bytes = workspace_bytes
         h = ctypes.c_void_p()
         _check(lib().smol_pipeline_create(ctypes.byref(cfg), ctypes.byref(h)))
         self._h = h
@@ -799,6 +805,49 @@ class Pipeline:
             h.ctypes.data, None if r is None else r.ctypes.data, n, ctypes.byref(params),
             None if options is None else ctypes.byref(options),
             CONSUMER() if consumer is None else consumer, user))
+
+    def submit_jpeg(self, slot: int, nbytes: int, coef_offsets, qtables, widths, heights,
+                    params: Params, coef_layout: int = JPEG_COEF_WINDOW,
+                    options: Options | None = None, consumer=None,
+                    user: int | None = None) -> None:
+        """Submit entropy-decoded JPEG coefficients in the slot's host buffer
+        (``decode_jpeg_into``) for partial block decoding and preprocessing."""
+        co = _table(coef_offsets, np.int64)
+        w = _table(widths, np.int32)
+        h = _table(heights, np.int32)
+        n = len(co)
+        q, nq = _qtables(qtables, n)
+        _check(lib().smol_pipeline_submit_jpeg(
+            self._h, slot, nbytes, co.ctypes.data, q.ctypes.data, nq, w.ctypes.data,
+            h.ctypes.data, n, coef_layout, ctypes.byref(params),
+            None if options is None else ctypes.byref(options),
+            CONSUMER() if consumer is None else consumer, user))
+
+    def decode_jpeg_into(self, slot: int, streams, params: Params,
+                         options: Options | None = None, threads: int = 0):
+        """Entropy-decode JPEG streams into the acquired slot's pinned buffer,
+        only the MCU windows of Algorithm 1's rectangles: (bytes,
+        coef_offsets, qtables, widths, heights) for ``submit_jpeg``."""
+        n = len(streams)
+        infos = [jpeg_read_info(b) for b in streams]
+        w = np.asarray([i.width for i in infos], np.int32)
+        h = np.asarray([i.height for i in infos], np.int32)
+        rects = _rois([jpeg_mcu_rect(i.width, i.height, params, options) for i in infos], n)
+        counts = np.asarray([jpeg_window_coef_count(int(w[i]), int(h[i]), rects[i])
+                             for i in range(n)], np.int64)
+        co = np.concatenate([[0], np.cumsum(counts)[:-1]]).astype(np.int64)
+        total = int(counts.sum())
+        if 2 * total > self.input_bytes:
+            raise ValueError(f"{2 * total} coefficient bytes exceed the slot's {self.input_bytes}")
+        sizes = np.asarray([len(b) for b in streams], np.int64)
+        offs = np.concatenate([[0], np.cumsum(sizes)[:-1]]).astype(np.int64)
+        data = np.frombuffer(b"".join(streams), np.uint8)
+        q = np.zeros((n, 2, 64), np.uint16)
+        _check(lib().smol_jpeg_entropy_decode_batch(
+            data.ctypes.data, data.size, offs.ctypes.data, sizes.ctypes.data, n,
+            rects.ctypes.data, self._host[slot], total, co.ctypes.data, JPEG_COEF_WINDOW,
+            q.ctypes.data, threads))
+        return 2 * total, co, q, w, h
 
     def drain(self) -> None:
         _check(lib().smol_pipeline_drain(self._h))

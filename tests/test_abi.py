@@ -361,15 +361,13 @@ def test_lowres_empty_batch_is_a_no_op():
     (dict(streams=17), "streams"), (dict(input_bytes=0), "input_bytes"),
     (dict(output_bytes=8), "output_bytes"), (dict(reserved=1), "reserved"),
     (dict(copy_streams=5), "copy_streams"), (dict(copy_streams=-1), "copy_streams"),
+    (dict(workspace_bytes=-1), "workspace_bytes"),
 ])
 def test_pipeline_config_validation(kw, needle):
     cfg = smol.PipelineConfig()
     cfg.slots, cfg.streams, cfg.input_bytes, cfg.output_bytes = 2, 1, 1024, 1024
     for k, v in kw.items():
-        if k == "reserved":
-            cfg.reserved[0] = v
-        else:
-            setattr(cfg, k, v)
+        setattr(cfg, k, v)
     h = ctypes.c_void_p(1)
     rc = smol.lib().smol_pipeline_create(ctypes.byref(cfg), ctypes.byref(h))
     assert rc == smol.ERR_INVALID_ARG and h.value is None

@@ -138,3 +138,50 @@ def test_bad_submission_keeps_the_slot_and_failed_consumer_recycles_it():
         pl.drain()
         st = pl.stats()
         assert st["submitted"] == st["completed"] == 1
+
+
+def test_jpeg_batches_decoded_into_slots():
+    """Producer threads entropy-decode JPEG batches straight into the pinned
+    slots they acquired; the copy, partial block decoding and preprocessing
+    run in stream order; every batch equals the oracle's chain."""
+    import torch
+    from tests.gpu_util import files_workload
+    rng = np.random.default_rng(43)
+    batches = []
+    for b in range(4):
+        sizes = [(int(rng.integers(200, 700)), int(rng.integers(200, 500))) for _ in range(5)]
+        batches.append(synthetic.jpeg_files(sizes, 43 + b, [60, 75, 90, 75, 85],
+                                            restart_blocks=b % 3))
+    p = smol.make_params(128, 112, 112, synthetic.IMAGENET_MEAN_255,
+                         synthetic.IMAGENET_STD_255, F16)
+    results = [torch.empty((5, 3, 112, 112), dtype=torch.float16, device="cuda:0")
+               for _ in range(8)]
+    cb = _copy_consumer(results)
+    ws = max(smol.jpeg_workspace_bytes(*zip(*[(smol.jpeg_read_info(f).width,
+                                                smol.jpeg_read_info(f).height) for f in bt]))
+             for bt in batches)
+    errors = []
+    with smol.Pipeline(4, 2, 8 << 20, 5 * 3 * 112 * 112 * 2, workspace_bytes=ws) as pl:
+
+        def producer(t):
+            try:
+                for j in range(t, 8, 2):
+                    slot, _, _ = pl.acquire()
+                    nb, co, q, w, h = pl.decode_jpeg_into(slot, batches[j % 4], p, threads=2)
+                    pl.submit_jpeg(slot, nb, co, q, w, h, p, consumer=cb, user=j)
+            except Exception as e:  # noqa: BLE001 -- reported below
+                errors.append(e)
+
+        ths = [threading.Thread(target=producer, args=(t,)) for t in range(2)]
+        for th in ths:
+            th.start()
+        for th in ths:
+            th.join()
+        pl.drain()
+        assert pl.stats()["submitted"] == 8
+    assert not errors, errors
+    torch.cuda.synchronize()
+    for j in range(8):
+        wl = files_workload(f"pipe-jpeg{j}", batches[j % 4], 128, 112, F16)
+        assert_parity(results[j].cpu().numpy(), run_oracle(wl), F16, wl.name)
+    note("    8 JPEG batches through the pipeline match the oracle")
