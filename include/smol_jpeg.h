@@ -166,8 +166,8 @@ int smol_jpeg_read_info(const uint8_t *data, int64_t bytes, smol_jpeg_info *info
  *                 the copy to the device run asynchronously.
  *   qtables       HOST uint16 [n][2][64] receiving each stream's luma and
  *                 chroma tables (natural order), or NULL.
- *   threads       worker threads (<= 0: one per hardware thread); at most n
- *                 and 256 run.
+ *   threads       worker threads (<= 0: one per CPU in the process's
+ *                 affinity mask); at most n and 256 run.
  * Every stream is decoded; the call then returns SMOL_OK or the status of
  * the lowest-numbered failing stream (its coefficients are incomplete), with
  * "image i: ..." in smol_last_error(). */

@@ -12,6 +12,8 @@
 //
 // Stream format: ITU-T T.81 (Annex B syntax, Annex C Huffman tables, Annex F
 // sequential Huffman decoding).
+#include <sched.h>
+
 #include <algorithm>
 #include <atomic>
 #include <cstdarg>
@@ -486,6 +488,19 @@ int decode_image(const uint8_t *d, int64_t n, const int32_t *rect, bool window, 
     return SMOL_OK;
 }
 
+// CPUs this process may run on (its affinity mask), else the hardware's.
+int usable_cpus()
+{
+    cpu_set_t set;
+    if (sched_getaffinity(0, sizeof set, &set) == 0) {
+        const int k = CPU_COUNT(&set);
+        if (k > 0)
+            return k;
+    }
+    const unsigned hw = std::thread::hardware_concurrency();
+    return hw ? (int)hw : 1;
+}
+
 }  // namespace
 
 extern "C" {
@@ -533,8 +548,7 @@ int smol_jpeg_entropy_decode_batch(const uint8_t *data, int64_t data_bytes,
             return smol::set_error(SMOL_ERR_INVALID_ARG, "image %d: coefficient offset outside "
                                    "coef", i);
     }
-    unsigned hw = std::thread::hardware_concurrency();
-    int t = threads > 0 ? threads : (int)(hw ? hw : 1);
+    int t = threads > 0 ? threads : usable_cpus();
     t = std::max(1, std::min({t, (int)n, 256}));
     std::vector<Failure> fails((size_t)n);
     std::atomic<int32_t> next{0};
