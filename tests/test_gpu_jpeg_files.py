@@ -118,3 +118,37 @@ def test_files_at_benchmark_size():
     wl = files_workload("jpeg-files-128", files, 256, 224, F16)
     stats = assert_parity(got.cpu().numpy(), run_oracle(wl), F16, wl.name)
     note(f"    {wl.name}: {stats}")
+
+
+def test_widest_and_tallest_streams():
+    """65500 x 17 and 17 x 65500 (libjpeg's largest size): block indices and
+    windows near the 16-bit limits of the run table, restart skipping on
+    4094-MCU rows; whole frames and Algorithm 1's windows, bit for bit."""
+    import torch
+    sizes = [(65500, 17), (17, 65500)]
+    files = synthetic.jpeg_files(sizes, 111, 75, restart_blocks=100)
+    p = smol.make_params(224, 224, 224, synthetic.IMAGENET_MEAN_255, synthetic.IMAGENET_STD_255,
+                         F16)
+    rects = [smol.jpeg_mcu_rect(W, H, p) for W, H in sizes]
+    yo, bo, ro, cur = [], [], [], 0
+    for W, H in sizes:
+        Wc, Hc = (W + 1) // 2, (H + 1) // 2
+        yo.append(cur)
+        bo.append(cur + W * H)
+        ro.append(cur + W * H + Wc * Hc)
+        cur += W * H + 2 * Wc * Hc
+    for layout, rr in ((smol.JPEG_COEF_FRAME, None), (smol.JPEG_COEF_WINDOW, rects)):
+        b = smol.jpeg_entropy_decode_batch(files, rr, threads=2, coef_layout=layout)
+        out = torch.full((cur,), 7, dtype=torch.uint8, device="cuda:0")
+        smol.jpeg_decode_i420(torch.from_numpy(b.coef).to("cuda:0"), b.coef_offsets, b.qtables,
+                              b.widths, b.heights, out, yo, bo, ro, rr, coef_layout=layout)
+        torch.cuda.synchronize()
+        flat = out.cpu().numpy()
+        for i, f in enumerate(files):
+            c, qy, qc, W, H = oracle.jpeg_entropy_decode(f)
+            exp = oracle.jpeg_decode_i420(c, qy, qc, W, H, None if rr is None else rr[i], fill=7)
+            Wc, Hc = (W + 1) // 2, (H + 1) // 2
+            got = (flat[yo[i]:bo[i]].reshape(H, W), flat[bo[i]:ro[i]].reshape(Hc, Wc),
+                   flat[ro[i]:ro[i] + Wc * Hc].reshape(Hc, Wc))
+            for k in range(3):
+                assert np.array_equal(got[k], exp[k]), (layout, sizes[i], k)

@@ -249,3 +249,25 @@ def test_corrupt_streams_fail_cleanly():
             assert np.array_equal(coef[:c.size], c)
         counts[c is not None] += 1
     assert counts[True] >= 20 and counts[False] >= 20, counts
+
+
+def test_widest_and_tallest_streams_bit_exact():
+    """libjpeg's largest sizes, 65500 x 17 and 17 x 65500, with restart
+    intervals of 100 MCUs, whole and through narrow rectangles at the far
+    end (most intervals skipped)."""
+    sizes = [(65500, 17), (17, 65500)]
+    files = synthetic.jpeg_files(sizes, 111, 75, restart_blocks=100)
+    rects = [(65400, 2, 60, 13), (3, 65400, 12, 90)]
+    for rr in (None, rects):
+        rc, msg, coef, co, _ = _decode_raw(files, rr, threads=2)
+        assert rc == 0, msg
+        for i, f in enumerate(files):
+            c, _, _, W, H = oracle.jpeg_entropy_decode(f)
+            got, exp = _blocks(coef[co[i]:co[i] + c.size], W, H), _blocks(c, W, H)
+            if rr is None:
+                assert np.array_equal(coef[co[i]:co[i] + c.size], c), sizes[i]
+                continue
+            x, y, w, h = rr[i]
+            sl = (slice(2 * (y // 16), 2 * ((y + h - 1) // 16) + 2),
+                  slice(2 * (x // 16), 2 * ((x + w - 1) // 16) + 2))
+            assert np.array_equal(got[0][sl], exp[0][sl]), sizes[i]
