@@ -313,13 +313,23 @@ def _table(v, dtype) -> np.ndarray:
     return np.ascontiguousarray(np.asarray(v), dtype=dtype)
 
 
-def _stream_handle(stream) -> int | None:
+def _launch_stream(stream, *tensors) -> int:
+    """The handle of the stream a call launches on. For a stream other than
+    torch's current one (a torch stream or a raw handle), the stream first
+    waits for the current stream's work (which made or filled the tensors),
+    and the device tensors are recorded on it so that torch's allocator does
+    not hand their memory out again before the call's work has finished."""
+    import torch
     if stream is None:
-        import torch
         return torch.cuda.current_stream().cuda_stream
-    if isinstance(stream, int):
-        return stream
-    return stream.cuda_stream
+    st = torch.cuda.ExternalStream(stream) if isinstance(stream, int) else stream
+    cur = torch.cuda.current_stream()
+    if st.cuda_stream != cur.cuda_stream:
+        st.wait_stream(cur)
+        for t in tensors:
+            if t is not None and getattr(t, "is_cuda", False):
+                t.record_stream(st)
+    return st.cuda_stream
 
 
 def _out_tensor(out, n: int, params: Params, device, layout: int = LAYOUT_NCHW):
@@ -368,13 +378,13 @@ def preprocess_batch(src, offsets, widths, heights, params: Params, pitches=None
                                            w.ctypes.data, h.ctypes.data,
                                            None if pt is None else pt.ctypes.data, n,
                                            ctypes.byref(params), out.data_ptr(),
-                                           _stream_handle(stream)))
+                                           _launch_stream(stream, src, out)))
     else:
         _check(lib().smol_preprocess_batch_ex(
             src.data_ptr(), src.numel(), off.ctypes.data, w.ctypes.data, h.ctypes.data,
             None if pt is None else pt.ctypes.data, None if r is None else r.ctypes.data, n,
             ctypes.byref(params), None if options is None else ctypes.byref(options),
-            out.data_ptr(), _stream_handle(stream)))
+            out.data_ptr(), _launch_stream(stream, src, out)))
     return out
 
 
@@ -399,13 +409,14 @@ def yuv420_preprocess_batch(src, y_offsets, cb_offsets, cr_offsets, widths, heig
         _check(lib().smol_yuv420_preprocess_batch(src.data_ptr(), src.numel(), yo.ctypes.data,
                                                   bo.ctypes.data, ro.ctypes.data, w.ctypes.data,
                                                   h.ctypes.data, n, ctypes.byref(params),
-                                                  out.data_ptr(), _stream_handle(stream)))
+                                                  out.data_ptr(),
+                                                  _launch_stream(stream, src, out)))
     else:
         _check(lib().smol_yuv420_preprocess_batch_ex(
             src.data_ptr(), src.numel(), yo.ctypes.data, bo.ctypes.data, ro.ctypes.data,
             w.ctypes.data, h.ctypes.data, None if r is None else r.ctypes.data, n,
             ctypes.byref(params), None if options is None else ctypes.byref(options),
-            out.data_ptr(), _stream_handle(stream)))
+            out.data_ptr(), _launch_stream(stream, src, out)))
     return out
 
 
@@ -443,7 +454,7 @@ def lowres_preprocess_batch(src, offsets, widths, heights, params: Params, low_r
     _check(lib().smol_lowres_preprocess_batch(
         src.data_ptr(), src.numel(), off.ctypes.data, w.ctypes.data, h.ctypes.data,
         None if pt is None else pt.ctypes.data, n, low_res, ctypes.byref(params), ws.data_ptr(),
-        ws.numel(), out.data_ptr(), _stream_handle(stream)))
+        ws.numel(), out.data_ptr(), _launch_stream(stream, src, out, ws)))
     return out
 
 
@@ -466,7 +477,7 @@ def yuv420_lowres_preprocess_batch(src, y_offsets, cb_offsets, cr_offsets, width
     _check(lib().smol_yuv420_lowres_preprocess_batch(
         src.data_ptr(), src.numel(), yo.ctypes.data, bo.ctypes.data, ro.ctypes.data,
         w.ctypes.data, h.ctypes.data, n, low_res, ctypes.byref(params), ws.data_ptr(),
-        ws.numel(), out.data_ptr(), _stream_handle(stream)))
+        ws.numel(), out.data_ptr(), _launch_stream(stream, src, out, ws)))
     return out
 
 
@@ -520,8 +531,8 @@ def jpeg_decode_i420(coef, coef_offsets, qtables, widths, heights, out, y_offset
     _check(lib().smol_jpeg_decode_i420(
         coef.data_ptr(), coef.numel(), co.ctypes.data, q.ctypes.data, nq, w.ctypes.data,
         h.ctypes.data, None if r is None else r.ctypes.data, n, coef_layout, out.data_ptr(),
-        out.numel(),
-        yo.ctypes.data, bo.ctypes.data, ro.ctypes.data, _stream_handle(stream)))
+        out.numel(), yo.ctypes.data, bo.ctypes.data, ro.ctypes.data,
+        _launch_stream(stream, coef, out)))
 
 
 def jpeg_workspace_bytes(widths, heights) -> int:
@@ -549,7 +560,7 @@ def jpeg_roi_preprocess_batch(coef, coef_offsets, qtables, widths, heights, para
         coef.data_ptr(), coef.numel(), co.ctypes.data, q.ctypes.data, nq, w.ctypes.data,
         h.ctypes.data, n, coef_layout, ctypes.byref(params),
         None if options is None else ctypes.byref(options), workspace.data_ptr(),
-        workspace.numel(), out.data_ptr(), _stream_handle(stream)))
+        workspace.numel(), out.data_ptr(), _launch_stream(stream, coef, out, workspace)))
     return out
 
 
@@ -625,9 +636,14 @@ def jpeg_files_preprocess(streams, params: Params, options: Options | None = Non
     rects = [jpeg_mcu_rect(i.width, i.height, params, options) for i in infos]
     b = jpeg_entropy_decode_batch(streams, rects, threads, pinned=True,
                                   coef_layout=JPEG_COEF_WINDOW)
-    dev = b.coef.to("cuda", non_blocking=True)
-    return jpeg_roi_preprocess_batch(dev, b.coef_offsets, b.qtables, b.widths, b.heights, params,
-                                     options, None, out, stream, JPEG_COEF_WINDOW)
+    import torch
+    st = (torch.cuda.current_stream() if stream is None else
+          torch.cuda.ExternalStream(stream) if isinstance(stream, int) else stream)
+    with torch.cuda.stream(st):
+        # the copy, the workspace and the output all belong to `st`
+        dev = b.coef.to("cuda", non_blocking=True)
+        return jpeg_roi_preprocess_batch(dev, b.coef_offsets, b.qtables, b.widths, b.heights,
+                                         params, options, None, out, None, JPEG_COEF_WINDOW)
 
 
 def torch_int16():

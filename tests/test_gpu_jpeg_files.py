@@ -152,3 +152,25 @@ def test_widest_and_tallest_streams():
                    flat[ro[i]:ro[i] + Wc * Hc].reshape(Hc, Wc))
             for k in range(3):
                 assert np.array_equal(got[k], exp[k]), (layout, sizes[i], k)
+
+
+def test_side_streams_match_the_current_stream():
+    """Calls given a stream other than torch's current one (a torch stream
+    or a raw handle) order themselves after the current stream's work and
+    keep their temporaries alive: same bytes as on the current stream."""
+    import torch
+    files = synthetic.jpeg_files([(640, 480), (333, 517), (1280, 720)], 104, 80,
+                                 restart_blocks=2)
+    p = smol.make_params(256, 224, 224, synthetic.IMAGENET_MEAN_255, synthetic.IMAGENET_STD_255,
+                         F16)
+    ref = smol.jpeg_files_preprocess(files, p, threads=4)
+    wl = synthetic.c7(n=6)
+    src = torch.from_numpy(wl.src).to("cuda:0")
+    low_ref = smol.run_workload(wl, src)
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    for st in (side, side.cuda_stream):
+        got = smol.jpeg_files_preprocess(files, p, threads=4, stream=st)
+        low = smol.run_workload(wl, src, stream=st)
+        torch.cuda.synchronize()
+        assert torch.equal(got, ref) and torch.equal(low, low_ref)
