@@ -35,7 +35,7 @@ constexpr uint8_t kNatural[64] = {
     35, 42, 49, 56, 57, 50, 43, 36, 29, 22, 15, 23, 30, 37, 44, 51,
     58, 59, 52, 45, 38, 31, 39, 46, 53, 60, 61, 54, 47, 55, 62, 63};
 
-constexpr int kLook = 9;  // bits resolved by one table lookup
+constexpr int kLook = 10;  // bits resolved by one table lookup
 
 // A Huffman table for decoding: codes of up to kLook bits resolve through
 // `fast` (entry = length << 8 | symbol, 0 = longer code); longer codes
@@ -44,9 +44,11 @@ constexpr int kLook = 9;  // bits resolved by one table lookup
 // first[l]].
 struct Huff {
     uint16_t fast[1 << kLook];
-    // AC tables: a code and the value bits that follow it, both within
-    // kLook bits, resolved at once: the value, the zero run before it and
-    // the bits used (0: not resolvable this way)
+    // A code and the value bits that follow it, both within kLook bits,
+    // resolved at once: the value, the zero run before it and the bits used
+    // (0: not resolvable this way). Symbol 0 (AC: end of block; DC:
+    // difference 0) has run 0xFF. DC tables use the entries of run 0 and
+    // 0xFF (their symbols are categories).
     struct Ac {
         int16_t value;
         uint8_t run, bits;
@@ -82,6 +84,10 @@ bool build_huff(Huff &h, const uint8_t *counts, const uint8_t *symbols, int nsym
     for (int e = 0; e < (1 << kLook); ++e) {
         h.fast_ac[e] = {0, 0, 0};
         const int l = h.fast[e] >> 8, rs = h.fast[e] & 0xFF, size = rs & 15;
+        if (l != 0 && rs == 0x00) {
+            h.fast_ac[e] = {0, 0xFF, (uint8_t)l};
+            continue;
+        }
         if (l == 0 || size == 0 || l + size > kLook)
             continue;
         int32_t v = (e >> (kLook - l - size)) & ((1 << size) - 1);
@@ -440,10 +446,19 @@ int decode_image(const uint8_t *d, int64_t n, const int32_t *rect, bool window, 
                            : planes[c] + 64 * (gr * gmx + gc);
             }
             std::memset(z, 0, 64 * sizeof(int16_t));
-            const int t = decode(s, *dct[c]);
-            if (t < 0 || t > 11)
-                return fail(f, SMOL_ERR_INVALID_ARG, "bad DC code at MCU %lld", (long long)mcu);
-            pred[c] += receive(s, t);
+            if (s.n < 32)
+                s.fill();
+            const Huff::Ac &fd = dct[c]->fast_ac[s.buf >> (64 - kLook)];
+            if (fd.bits && (fd.run == 0 || fd.run == 0xFF)) {
+                s.skip(fd.bits);  // a DC difference resolved at once
+                pred[c] += fd.run == 0xFF ? 0 : fd.value;
+            } else {
+                const int t = decode(s, *dct[c]);
+                if (t < 0 || t > 11)
+                    return fail(f, SMOL_ERR_INVALID_ARG, "bad DC code at MCU %lld",
+                                (long long)mcu);
+                pred[c] += receive(s, t);
+            }
             if (pred[c] < -32768 || pred[c] > 32767)
                 return fail(f, SMOL_ERR_INVALID_ARG, "DC value out of range at MCU %lld",
                             (long long)mcu);
@@ -454,6 +469,10 @@ int decode_image(const uint8_t *d, int64_t n, const int32_t *rect, bool window, 
                     s.fill();
                 const Huff::Ac &fa = ac.fast_ac[s.buf >> (64 - kLook)];
                 if (fa.bits) {
+                    if (fa.run == 0xFF) {
+                        s.skip(fa.bits);
+                        break;  // end of block
+                    }
                     k += fa.run;
                     if (k > 63)
                         return fail(f, SMOL_ERR_INVALID_ARG, "AC run past the block at MCU "
