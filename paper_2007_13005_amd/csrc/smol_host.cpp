@@ -1309,7 +1309,7 @@ const char *smol_status_string(int status)
 
 const char *smol_last_error(void) { return g_last_error.c_str(); }
 
-int smol_version(void) { return 100; }
+int smol_version(void) { return 200; }
 
 }  // extern "C"
 
