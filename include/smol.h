@@ -54,7 +54,7 @@ extern "C" {
 #define SMOL_OK 0
 #define SMOL_ERR_INVALID_ARG (-1) /* a null pointer, a size out of range, a   */
                                   /* buffer too small for its table entries  */
-#define SMOL_ERR_UNSUPPORTED (-2) /* valid in principle, beyond this build's  */
+#define SMOL_ERR_UNSUPPORTED (-2) /* valid in principle, beyond the library's */
                                   /* limits (see the per-call notes)          */
 #define SMOL_ERR_HIP (-3)         /* the HIP runtime reported an error        */
 

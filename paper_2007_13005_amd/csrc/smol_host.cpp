@@ -1299,7 +1299,7 @@ const char *smol_status_string(int status)
     case SMOL_ERR_INVALID_ARG:
         return "invalid argument";
     case SMOL_ERR_UNSUPPORTED:
-        return "unsupported by this build";
+        return "unsupported by this library";
     case SMOL_ERR_HIP:
         return "HIP runtime error";
     default:
