@@ -580,8 +580,7 @@ def jpeg_files_experiment(args) -> int:
                 (co if whole else cow).ctypes.data,
                 smol.JPEG_COEF_FRAME if whole else smol.JPEG_COEF_WINDOW, q.ctypes.data,
                 threads)
-        if rc:
-            raise smol.SmolError(smol.lib().smol_last_error().decode())
+        smol._check(rc)
 
     def rate(body) -> tuple[float, int]:
         body()
@@ -607,8 +606,7 @@ def jpeg_files_experiment(args) -> int:
         rc = gpu_fn(src.data_ptr(), total, cow.ctypes.data, qp.ctypes.data, n, w.ctypes.data,
                     h.ctypes.data, n, smol.JPEG_COEF_WINDOW, pref, None, ws.data_ptr(),
                     ws.numel(), out.data_ptr(), stream.cuda_stream)
-        if rc:
-            raise smol.SmolError(smol.lib().smol_last_error().decode())
+        smol._check(rc)
 
     def timed_gpu(body, reps=50) -> float:
         body()

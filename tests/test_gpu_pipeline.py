@@ -185,3 +185,20 @@ def test_jpeg_batches_decoded_into_slots():
         wl = files_workload(f"pipe-jpeg{j}", batches[j % 4], 128, 112, F16)
         assert_parity(results[j].cpu().numpy(), run_oracle(wl), F16, wl.name)
     note("    8 JPEG batches through the pipeline match the oracle")
+
+
+def test_jpeg_submission_errors_keep_the_slot():
+    """A JPEG submission to a pipeline created without a workspace, or with
+    an odd byte count, is rejected before anything is enqueued; the slot
+    stays acquired and can be released."""
+    p = smol.make_params(64, 56, 56, synthetic.IMAGENET_MEAN_255, synthetic.IMAGENET_STD_255,
+                         F16)
+    q = np.ones((1, 2, 64), np.uint16)
+    for ws, nbytes, needle in ((0, 6 * 128, "no workspace"), (1 << 20, 6 * 128 - 1, "int16")):
+        with smol.Pipeline(1, 1, 1 << 16, 3 * 56 * 56 * 2, workspace_bytes=ws) as pl:
+            slot, _, _ = pl.acquire()
+            with pytest.raises(smol.SmolError, match=needle):
+                pl.submit_jpeg(slot, nbytes, [0], q, [16], [16], p,
+                               coef_layout=smol.JPEG_COEF_FRAME)
+            pl.release(slot)
+            assert pl.stats()["submitted"] == 0
