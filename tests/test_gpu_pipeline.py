@@ -202,3 +202,14 @@ def test_jpeg_submission_errors_keep_the_slot():
                                coef_layout=smol.JPEG_COEF_FRAME)
             pl.release(slot)
             assert pl.stats()["submitted"] == 0
+
+
+def test_jpeg_batch_larger_than_the_slot_is_refused():
+    files = synthetic.jpeg_files([(640, 480)], 44, 75)
+    p = smol.make_params(256, 224, 224, synthetic.IMAGENET_MEAN_255, synthetic.IMAGENET_STD_255,
+                         F16)
+    with smol.Pipeline(1, 1, 1 << 10, 3 * 224 * 224 * 2, workspace_bytes=1 << 20) as pl:
+        slot, _, _ = pl.acquire()
+        with pytest.raises(ValueError, match="exceed the slot"):
+            pl.decode_jpeg_into(slot, files, p)
+        pl.release(slot)
