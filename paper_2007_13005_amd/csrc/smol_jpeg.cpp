@@ -205,7 +205,10 @@ int smol_jpeg_decode_i420(const int16_t *coef, int64_t coef_elems, const int64_t
     auto flush = [&]() -> int {
         if (a.runs == 0)
             return SMOL_OK;
-        const int grid = (int)std::min<long long>(jobs, (long long)(cus > 0 ? cus : 256) * 32);
+        // 128 one-wave workgroups per compute unit, each looping over jobs:
+        // measured faster than 32 (long-lived waves) and than one workgroup
+        // per job on 128 720p frames
+        const int grid = (int)std::min<long long>(jobs, (long long)(cus > 0 ? cus : 256) * 128);
         const int rc = smol::launch_jpeg_idct(a, grid, stream);
         a.runs = 0;
         jobs = 0;
