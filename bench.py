@@ -30,6 +30,15 @@ if ROOT not in sys.path:
 
 METRIC = "images/sec preprocessed + achieved HBM GB/s (% of MI355X peak), 1 GPU"
 HBM_PEAK_GBPS = 8000.0  # MI355X published HBM3E bandwidth
+# ALU ceilings from the unit counts and clock (256 compute units of 4 SIMDs at
+# 2.4 GHz). A SIMD executes a 64-lane fp32 VALU instruction in 4 clocks (16
+# lanes per clock), so the chip issues 256 * 4 / 4 * 2.4e9 wave instructions
+# per second; a separately rounded fp32 add, multiply, min or max (packed fp32
+# is not used) is one operation per lane per clock: 256 * 64 * 2.4e9 per
+# second. (The published 157.3 TFLOP/s counts packed fused multiply-adds, four
+# flops per lane per clock.)
+VALU_WAVE_INSTR_PER_S = 256 * 4 / 4 * 2.4e9
+ALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12
 MALL_BYTES = 256 * 1024 * 1024
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
@@ -61,6 +70,17 @@ def parse():
     ap.add_argument("--jpeg-files", action="store_true",
                     help="experiment: JPEG files through host entropy decoding (whole and "
                          "partial), the copy and the GPU stages, alone and pipelined")
+    ap.add_argument("--stream-probe", action="store_true",
+                    help="instead of the benchmark, the streaming probe's ceilings at the "
+                         "workload's read and write bytes (pure read, pure write, the mix, a "
+                         "copy), as one JSON line")
+    ap.add_argument("--stream-shape", default="all", choices=["all", "read", "write", "mix", "copy"],
+                    help="--stream-probe: only this read/write shape")
+    ap.add_argument("--stream-waves", type=int, default=0, help="--stream-probe: only this "
+                    "wave count (0: 2048, 4096 and 8192)")
+    ap.add_argument("--stream-flags", type=int, default=-1, help="--stream-probe: only these "
+                    "load/store flags (-1: nontemporal both, loads only, neither; 4 or 8 loads "
+                    "in flight)")
     ap.add_argument("--copy-probe", type=int, default=0,
                     help="instead of the benchmark, copy this many MiB with torch several "
                          "times (calibrates the FETCH_SIZE / WRITE_SIZE counters)")
@@ -140,6 +160,63 @@ def algorithmic_bytes(wl, smol) -> int:
             cache[key] = _read_bytes(g, wl.kind)
         total += cache[key]
     return total + wl.n * 3 * wl.crop_h * wl.crop_w * wl.out_elem_bytes
+
+
+# fp32 operations the definition performs per output pixel: the RGB path's
+# three lerps (subtract, multiply, add) per channel and the normalisation
+# (subtract, divide) per channel; I420 adds, at each of the four luma taps, the
+# chroma bilinear of both planes (3 lerps each), BT.601 (2 offsets, 8
+# products and sums) and the clamp of 3 channels (2 each).
+OPS_PER_PIXEL_RGB = 3 * 9 + 3 * 2
+OPS_PER_PIXEL_I420 = OPS_PER_PIXEL_RGB + 4 * (2 * 9 + 10 + 6)
+# Block decoding: dequantisation (64 products) and two passes of 64 outputs,
+# each a sum of 8 products (8 multiplies, 7 adds).
+OPS_PER_JPEG_BLOCK = 64 + 2 * 64 * 15
+
+
+def algorithmic_ops(wl, smol) -> int:
+    """fp32 operations of the definition per batch (see the constants)."""
+    pixels = wl.n * wl.crop_h * wl.crop_w
+    if wl.kind == "rgb":
+        return pixels * OPS_PER_PIXEL_RGB
+    ops = pixels * OPS_PER_PIXEL_I420
+    if wl.kind == "jpeg":
+        import math
+        p = smol.make_params(wl.resize_short, wl.crop_h, wl.crop_w, wl.mean, wl.std,
+                             wl.out_dtype)
+        o = smol.make_options(wl.resize_mode, wl.layout, 0)
+        for w, h in zip(wl.widths.tolist(), wl.heights.tolist()):
+            _, _, rw, rh = smol.jpeg_mcu_rect(w, h, p, o)
+            blocks = (math.ceil(rw / 8) * math.ceil(rh / 8) +
+                      2 * math.ceil(math.ceil(rw / 2) / 8) * math.ceil(math.ceil(rh / 2) / 8))
+            ops += blocks * OPS_PER_JPEG_BLOCK
+    return ops
+
+
+def roofline_of(wl, smol, algo: int, launches: int, avg_launch_s: float,
+                traffic: dict | None) -> dict:
+    """The roofline entry of the launch. The bound follows the counters of
+    the committed profile: issue time of its VALU instructions at the chip's
+    rate against its HBM bytes at the peak bandwidth; without counters, HBM."""
+    per_launch = algo / launches
+    mem_bytes = per_launch if traffic is None else max(per_launch, traffic["bytes_per_launch"])
+    t_mem = mem_bytes / (HBM_PEAK_GBPS * 1e9)
+    valu = None if traffic is None else traffic.get("valu_insts_per_launch")
+    t_alu = None if valu is None else valu / VALU_WAVE_INSTR_PER_S
+    bound = "alu" if t_alu is not None and t_alu > t_mem else "hbm"
+    if bound == "alu":
+        achieved = algorithmic_ops(wl, smol) / launches / avg_launch_s / 1e12
+        r = {"bound": "alu", "achieved": round(achieved, 3), "peak": round(ALU_PEAK_TOPS, 2),
+             "unit": "TFLOP/s", "frac": round(achieved / ALU_PEAK_TOPS, 4)}
+    else:
+        achieved = per_launch / avg_launch_s / 1e9
+        r = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
+             "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4)}
+    r["traffic"] = None if traffic is None else traffic["bytes_per_launch"]
+    r["bound_from"] = ("counters: VALU issue %.1f us vs HBM %.1f us per launch"
+                       % (t_alu * 1e6, t_mem * 1e6) if t_alu is not None
+                       else "no committed counters for this kernel: HBM assumed")
+    return r
 
 
 def touched_bytes(wl, smol) -> int:
@@ -256,29 +333,61 @@ def cpu_model() -> str:
     return "unknown"
 
 
-def stream_ceilings_gbps(torch, mib: int = 512, reps: int = 10) -> dict:
-    """GB/s of plain streaming kernels over `mib` MiB buffers: a device copy
-    (read + write bytes) and a fill (write), ceilings the kernel's traffic
-    mix is compared with."""
-    n = mib * 1024 * 1024
-    a = torch.empty(n, dtype=torch.uint8, device="cuda:0")
-    b = torch.empty_like(a)
-    a.fill_(1)
-
-    def rate(fn, nbytes: int) -> float:
-        for _ in range(2):
-            fn()
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        e0.record()
-        for _ in range(reps):
-            fn()
-        e1.record()
-        torch.cuda.synchronize()
-        return nbytes * reps / (e0.elapsed_time(e1) / 1e3) / 1e9
-
-    return {"copy": rate(lambda: b.copy_(a), 2 * n), "write": rate(lambda: b.fill_(3), n)}
+def stream_ceilings_gbps(torch, smol, read_bytes: int, write_bytes: int, rotate: int,
+                         reps: int = 40, only_shape: str = "all", only_waves: int = 0,
+                         only_flags: int = -1) -> dict:
+    """GB/s of the library's streaming probe (smol_stream_probe, 16-byte
+    accesses) at one preprocessing launch's own byte counts, sets rotated like
+    the benchmark's: a pure read of its read bytes, a pure write of its write
+    bytes, its read/write mix in one launch, and a copy of the same total.
+    Each is the best over load/store forms and wave counts; the mix is the
+    ceiling the launch is compared with."""
+    read_bytes -= read_bytes % 16
+    write_bytes -= write_bytes % 16
+    half = (read_bytes + write_bytes) // 32 * 16
+    shapes = {"read": (read_bytes, 0), "write": (0, write_bytes), "mix": (read_bytes, write_bytes),
+              "copy": (half, half)}
+    if only_shape != "all":
+        shapes = {only_shape: shapes[only_shape]}
+    rmax = max(r for r, _ in shapes.values())
+    wmax = max(w for _, w in shapes.values())
+    srcs = [torch.empty(rmax, dtype=torch.uint8, device="cuda:0") for _ in range(rotate)]
+    dsts = [torch.empty(wmax, dtype=torch.uint8, device="cuda:0") for _ in range(rotate)]
+    for t in srcs:
+        t.fill_(1)
+    sh = torch.cuda.current_stream().cuda_stream
+    nt = smol.STREAM_NT_LOADS | smol.STREAM_NT_STORES
+    flags_all = ([nt, smol.STREAM_NT_LOADS, 0, nt | smol.STREAM_DEEP,
+                  smol.STREAM_NT_LOADS | smol.STREAM_DEEP]
+                 if only_flags < 0 else [only_flags])
+    waves_all = (2048, 4096, 8192) if only_waves <= 0 else (only_waves,)
+    res, best_form = {}, {}
+    for name, (rb, wb) in shapes.items():
+        best = 0.0
+        for flags in flags_all:
+            for waves in waves_all:
+                def launch(i):
+                    smol.stream_probe(srcs[i % rotate].data_ptr() if rb else 0, rb,
+                                      dsts[i % rotate].data_ptr() if wb else 0, wb, waves, flags,
+                                      sh)
+                for i in range(4):
+                    launch(i)
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record()
+                for i in range(reps):
+                    launch(i)
+                e1.record()
+                torch.cuda.synchronize()
+                gbps = (rb + wb) * reps / (e0.elapsed_time(e1) / 1e3) / 1e9
+                if gbps > best:
+                    best, best_form[name] = gbps, {"flags": flags, "waves": waves,
+                                                   "us_per_launch": round(
+                                                       e0.elapsed_time(e1) * 1e3 / reps, 3)}
+        res[name] = best
+    res["forms"] = best_form
+    res["bytes"] = {k: list(v) for k, v in shapes.items()}
+    return res
 
 
 def load_traffic(config: str) -> dict | None:
@@ -744,6 +853,12 @@ def main() -> int:
     algo = algorithmic_bytes(wl, smol)
     out_bytes = wl.n * 3 * wl.crop_h * wl.crop_w * wl.out_elem_bytes
     rotate = args.rotate or max(2, -(-2 * MALL_BYTES // algo))
+    if args.stream_probe:
+        ceil = stream_ceilings_gbps(torch, smol, algo - out_bytes, out_bytes, rotate,
+                                    reps=200, only_shape=args.stream_shape,
+                                    only_waves=args.stream_waves, only_flags=args.stream_flags)
+        print(json.dumps({"workload": wl.name, "rotation_sets": rotate, **ceil}), flush=True)
+        return 0
     if (args.band_rows or args.path or args.wg_per_cu or args.lds_budget or args.row_order or
             args.upload):
         smol.set_tuning(path=args.path, band_rows=args.band_rows, lds_budget=args.lds_budget,
@@ -806,15 +921,14 @@ def main() -> int:
     e1.record(stream)
     torch.cuda.synchronize()
     mall_us = 1e3 * e0.elapsed_time(e1) / args.steps
-    ceil = None if args.profile_run else stream_ceilings_gbps(torch)
-    copy_gbps = None if ceil is None else ceil["copy"]
+    ceil = None if args.profile_run else stream_ceilings_gbps(torch, smol, algo - out_bytes,
+                                                              out_bytes, rotate)
 
     traffic = load_traffic(args.config)
     if traffic is not None and traffic.get("grid") != plan["grid"]:
         traffic = None  # counters taken on another launch shape
-    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
-                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                "traffic": None if traffic is None else traffic["bytes_per_launch"]}
+    roofline = roofline_of(wl, smol, algo, max(1, plan["launches"]), avg_launch_s, traffic)
+    hbm_gbps_launch = per_launch_bytes / avg_launch_s / 1e9
     res = {
         "metric": METRIC,
         "value": round(wl.n * args.steps / wall, 1),
@@ -838,10 +952,14 @@ def main() -> int:
                    "gpu_us_per_step_reps": [round(x, 3) for x in rep_us],
                    "hbm_gbps_wall": round(algo * args.steps / wall / 1e9, 1),
                    "mall_warm_us_per_step_one_set": round(mall_us, 3),
-                   "copy_ceiling_gbps": None if copy_gbps is None else round(copy_gbps, 1),
-                   "write_ceiling_gbps": None if ceil is None else round(ceil["write"], 1),
-                   "achieved_frac_of_copy_ceiling":
-                       None if copy_gbps is None else round(achieved / copy_gbps, 4)},
+                   "hbm_gbps_per_launch": round(hbm_gbps_launch, 1),
+                   "hbm_frac_per_launch": round(hbm_gbps_launch / HBM_PEAK_GBPS, 4),
+                   "stream_ceilings_gbps": None if ceil is None else {
+                       k: round(ceil[k], 1) for k in ("read", "write", "mix", "copy")},
+                   "stream_ceiling_forms": None if ceil is None else ceil["forms"],
+                   "achieved_frac_of_mix_ceiling":
+                       None if ceil is None else round(algo / (gpu_ms / 1e3 / args.steps) /
+                                                       1e9 / ceil["mix"], 4)},
         "roofline": roofline,
     }
     if not args.profile_run and args.cpu_seconds > 0:

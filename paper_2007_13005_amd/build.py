@@ -39,8 +39,9 @@ SOURCES = [
     "smol_jpeg_kernels.hip",
     "smol_jpeg.cpp",
     "smol_jpeg_entropy.cpp",
+    "smol_stream.hip",
 ]
-HEADERS = ["smol_internal.h", "smol_device.h", "smol_rows.h"]
+HEADERS = ["smol_internal.h", "smol_device.h", "smol_rows.h", "smol_rows_rgb.h", "smol_rows_yuv.h"]
 
 # -ffp-contract=off: the kernels round every multiply and add on their own, as
 # the definition does; fused multiply-adds are never formed implicitly.

@@ -597,15 +597,18 @@ int run_batch(const std::vector<Desc> &descs, size_t first, size_t count, int no
     }
 
     const int rc = launch(a, pl, stream);
+    if (st) {
+        // Recorded also when the launch failed: the table copy enqueued above
+        // still reads the pinned slot, and the slot's next use must wait for it.
+        e = hipEventRecord(st->ev[slot], s);
+        if (e == hipSuccess)
+            st->pending[slot] = true;
+        else if (rc == (int)hipSuccess)
+            return hip_fail(e, "hipEventRecord");
+    }
     if (rc != (int)hipSuccess)
         return hip_fail((hipError_t)rc, "kernel launch");
     info->launches += 1;
-    if (st) {
-        e = hipEventRecord(st->ev[slot], s);
-        if (e != hipSuccess)
-            return hip_fail(e, "hipEventRecord");
-        st->pending[slot] = true;
-    }
     return SMOL_OK;
 }
 

@@ -1,5 +1,5 @@
 // smol_rows_rgb_f16_range.hip -- RGB row-streaming kernels, fp16 output, contiguous row ranges, NCHW output.
-#include "smol_rows.h"
+#include "smol_rows_rgb.h"
 
 namespace smol {
 

@@ -1,5 +1,5 @@
 // smol_rows_rgb_f32_range_nhwc.hip -- RGB row-streaming kernels, fp32 output, contiguous row ranges, NHWC output.
-#include "smol_rows.h"
+#include "smol_rows_rgb.h"
 
 namespace smol {
 

@@ -1,5 +1,5 @@
 // smol_rows_rgb_f32_stride.hip -- RGB row-streaming kernels, fp32 output, rows strided across waves, NCHW output.
-#include "smol_rows.h"
+#include "smol_rows_rgb.h"
 
 namespace smol {
 

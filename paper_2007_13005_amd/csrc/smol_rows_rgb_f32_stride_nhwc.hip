@@ -1,5 +1,5 @@
 // smol_rows_rgb_f32_stride_nhwc.hip -- RGB row-streaming kernels, fp32 output, rows strided across waves, NHWC output.
-#include "smol_rows.h"
+#include "smol_rows_rgb.h"
 
 namespace smol {
 

@@ -1,5 +1,5 @@
 // smol_rows_rgb_u8_range.hip -- RGB row-streaming kernels, uint8 output (rounded resized values), contiguous row ranges.
-#include "smol_rows.h"
+#include "smol_rows_rgb.h"
 
 namespace smol {
 

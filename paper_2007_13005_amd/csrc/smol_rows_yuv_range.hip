@@ -1,5 +1,5 @@
 // smol_rows_yuv_range.hip -- I420 row-streaming kernels, contiguous row ranges, NCHW output.
-#include "smol_rows.h"
+#include "smol_rows_yuv.h"
 
 namespace smol {
 

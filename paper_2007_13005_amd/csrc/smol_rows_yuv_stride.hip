@@ -1,5 +1,5 @@
 // smol_rows_yuv_stride.hip -- I420 row-streaming kernels, rows strided across waves, NCHW output.
-#include "smol_rows.h"
+#include "smol_rows_yuv.h"
 
 namespace smol {
 

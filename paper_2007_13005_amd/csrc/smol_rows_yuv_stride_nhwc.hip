@@ -1,5 +1,5 @@
 // smol_rows_yuv_stride_nhwc.hip -- I420 row-streaming kernels, rows strided across waves, NHWC output.
-#include "smol_rows.h"
+#include "smol_rows_yuv.h"
 
 namespace smol {
 

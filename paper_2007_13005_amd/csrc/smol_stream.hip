@@ -1,0 +1,145 @@
+// smol_stream.hip -- the streaming-bandwidth probe (smol_stream_probe): one
+// launch that reads one buffer and writes another with coalesced 16-byte
+// accesses, every wave interleaving its reads and writes in the ratio of the
+// two sizes. It measures the memory ceiling that the preprocessing kernels'
+// byte mix can reach on the device.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "smol.h"
+#include "smol_internal.h"
+#include "smol_stream.h"
+
+namespace smol {
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(1))) const u32x4 GlobalIn;
+typedef __attribute__((address_space(1))) u32x4 GlobalOut;
+
+constexpr int kWavesPerGroup = 4;
+
+struct StreamArgs {
+    const u32x4 *src;
+    u32x4 *dst;
+    uint64_t nr, nw;  // 16-byte granules read and written
+    uint32_t waves;
+};
+
+template <int NTL>
+__device__ __forceinline__ u32x4 ld(const u32x4 *p, uint64_t i)
+{
+    GlobalIn *g = (GlobalIn *)p + i;
+    return NTL ? __builtin_nontemporal_load(g) : *g;
+}
+
+template <int NTS>
+__device__ __forceinline__ void st(u32x4 *p, uint64_t i, u32x4 v)
+{
+    GlobalOut *g = (GlobalOut *)p + i;
+    if (NTS)
+        __builtin_nontemporal_store(v, g);
+    else
+        *g = v;
+}
+
+// Wave w owns granules [n w / W, n (w + 1) / W) of each buffer. A read step
+// loads kUnroll * 64 granules (kUnroll 16-byte loads per lane in flight);
+// after each step the wave writes, 64 granules per store, until its writes
+// have kept pace with its reads (writes done = floor(reads done * its writes
+// / its reads)).
+template <int NTL, int NTS, int kUnroll>
+__global__ void __launch_bounds__(64 * kWavesPerGroup) stream_kernel(StreamArgs a)
+{
+    const uint32_t w = __builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerGroup +
+                                                      (threadIdx.x >> 6));
+    if (w >= a.waves)
+        return;
+    const uint32_t lane = threadIdx.x & 63;
+    const uint64_t r0 = a.nr * w / a.waves, r1 = a.nr * (w + 1) / a.waves;
+    const uint64_t w0 = a.nw * w / a.waves, w1 = a.nw * (w + 1) / a.waves;
+    const uint64_t nr = r1 - r0, nw = w1 - w0;
+    u32x4 acc = {0x9e3779b9u, 0x7f4a7c15u, 0x85ebca6bu, 0xc2b2ae35u};
+    // credit counts reads times the wave's writes; each 64-granule store
+    // spends 64 times its reads, so stores keep pace without a division
+    uint64_t written = 0, credit = 0;
+    const uint64_t unit = 64 * nr;
+    for (uint64_t done = 0; done < nr;) {
+        const uint64_t step = nr - done < (uint64_t)(64 * kUnroll) ? nr - done : 64 * kUnroll;
+        u32x4 v[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const uint64_t k = done + 64 * u + lane;
+            // past the wave's range a lane reloads its last granule
+            v[u] = ld<NTL>(a.src, r0 + (k < nr ? k : nr - 1));
+        }
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u)
+            acc ^= v[u];
+        done += step;
+        credit += step * nw;
+        while (written < nw && (credit >= unit || done == nr)) {
+            const uint64_t k = written + lane;
+            if (k < nw)
+                st<NTS>(a.dst, w0 + k, acc);
+            written += 64;
+            credit = credit >= unit ? credit - unit : 0;
+        }
+    }
+    if (nr == 0) {
+        for (; written < nw; written += 64 * kUnroll) {
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) {
+                const uint64_t k = written + 64 * u + lane;
+                if (k < nw)
+                    st<NTS>(a.dst, w0 + k, acc + (uint32_t)k);
+            }
+        }
+    }
+    // keep the loads of a pure read stream
+    asm volatile("" ::"v"(acc.x), "v"(acc.y), "v"(acc.z), "v"(acc.w));
+}
+
+}  // namespace
+}  // namespace smol
+
+extern "C" int smol_stream_probe(const void *src, uint64_t read_bytes, void *dst,
+                                 uint64_t write_bytes, int32_t waves, int32_t flags, void *stream)
+{
+    using namespace smol;
+    clear_error();
+    if (read_bytes % 16 || write_bytes % 16)
+        return set_error(SMOL_ERR_INVALID_ARG, "sizes must be multiples of 16 bytes");
+    if (read_bytes == 0 && write_bytes == 0)
+        return set_error(SMOL_ERR_INVALID_ARG, "nothing to read or write");
+    if ((read_bytes && (!src || (uintptr_t)src % 16)) ||
+        (write_bytes && (!dst || (uintptr_t)dst % 16)))
+        return set_error(SMOL_ERR_INVALID_ARG, "buffers must be non-null and 16-byte aligned");
+    if (waves < 1 || waves > (1 << 20))
+        return set_error(SMOL_ERR_INVALID_ARG, "waves must be in 1 .. 2^20");
+    if (flags & ~(SMOL_STREAM_NT_LOADS | SMOL_STREAM_NT_STORES | SMOL_STREAM_DEEP))
+        return set_error(SMOL_ERR_INVALID_ARG, "unknown flags");
+    StreamArgs a;
+    a.src = (const u32x4 *)src;
+    a.dst = (u32x4 *)dst;
+    a.nr = read_bytes / 16;
+    a.nw = write_bytes / 16;
+    a.waves = (uint32_t)waves;
+    const dim3 grid((unsigned)((waves + kWavesPerGroup - 1) / kWavesPerGroup)),
+        block(64 * kWavesPerGroup);
+    hipStream_t s = (hipStream_t)stream;
+    switch (flags) {
+    case 0: hipLaunchKernelGGL((stream_kernel<0, 0, 4>), grid, block, 0, s, a); break;
+    case 1: hipLaunchKernelGGL((stream_kernel<1, 0, 4>), grid, block, 0, s, a); break;
+    case 2: hipLaunchKernelGGL((stream_kernel<0, 1, 4>), grid, block, 0, s, a); break;
+    case 3: hipLaunchKernelGGL((stream_kernel<1, 1, 4>), grid, block, 0, s, a); break;
+    case 4: hipLaunchKernelGGL((stream_kernel<0, 0, 8>), grid, block, 0, s, a); break;
+    case 5: hipLaunchKernelGGL((stream_kernel<1, 0, 8>), grid, block, 0, s, a); break;
+    case 6: hipLaunchKernelGGL((stream_kernel<0, 1, 8>), grid, block, 0, s, a); break;
+    default: hipLaunchKernelGGL((stream_kernel<1, 1, 8>), grid, block, 0, s, a); break;
+    }
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess)
+        return set_error(SMOL_ERR_HIP, "stream probe launch: %s", hipGetErrorString(e));
+    return SMOL_OK;
+}

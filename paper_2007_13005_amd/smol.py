@@ -173,6 +173,8 @@ SIGNATURES = {
     "smol_jpeg_entropy_decode_batch": (ctypes.c_int, [_vp, ctypes.c_int64, _vp, _vp,
                                                       ctypes.c_int32, _vp, _vp, ctypes.c_int64,
                                                       _vp, ctypes.c_int32, _vp, ctypes.c_int32]),
+    "smol_stream_probe": (ctypes.c_int, [_vp, ctypes.c_uint64, _vp, ctypes.c_uint64,
+                                         ctypes.c_int32, ctypes.c_int32, _vp]),
     "smol_set_tuning": (ctypes.c_int, [ctypes.POINTER(Tuning)]),
     "smol_last_plan": (ctypes.c_int, [ctypes.POINTER(Plan)]),
     "smol_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -307,6 +309,19 @@ def last_plan() -> dict:
 
 def version() -> int:
     return int(lib().smol_version())
+
+
+STREAM_NT_LOADS = 1
+STREAM_NT_STORES = 2
+STREAM_DEEP = 4
+
+
+def stream_probe(src: int, read_bytes: int, dst: int, write_bytes: int, waves: int,
+                 flags: int = STREAM_NT_LOADS | STREAM_NT_STORES, stream: int = 0) -> None:
+    """One launch of the streaming probe (raw device addresses, a raw stream
+    handle): reads read_bytes at src, writes write_bytes at dst."""
+    _check(lib().smol_stream_probe(src or None, read_bytes, dst or None, write_bytes, waves,
+                                   flags, stream or None))
 
 
 def _table(v, dtype) -> np.ndarray:
@@ -639,6 +654,14 @@ def jpeg_files_preprocess(streams, params: Params, options: Options | None = Non
     import torch
     st = (torch.cuda.current_stream() if stream is None else
           torch.cuda.ExternalStream(stream) if isinstance(stream, int) else stream)
+    cur = torch.cuda.current_stream()
+    if st.cuda_stream != cur.cuda_stream:
+        # as for every call on another stream: wait for the current stream's
+        # work (which may still be making or using `out`), and keep `out` from
+        # being handed out again before the side stream is done with it
+        st.wait_stream(cur)
+        if out is not None and getattr(out, "is_cuda", False):
+            out.record_stream(st)
     with torch.cuda.stream(st):
         # the copy, the workspace and the output all belong to `st`
         dev = b.coef.to("cuda", non_blocking=True)

@@ -456,3 +456,24 @@ def _jpeg_roi_call(opts=None, ws=FAKE_OUT + 4096, ws_bytes=None, params=None):
 def test_jpeg_roi_preprocess_validation(kw, needle):
     rc, msg = _jpeg_roi_call(**kw)
     assert rc == smol.ERR_INVALID_ARG and needle in msg, (rc, msg)
+
+
+@pytest.mark.parametrize("kw, needle", [
+    (dict(read_bytes=24), "multiples of 16"),
+    (dict(write_bytes=8), "multiples of 16"),
+    (dict(read_bytes=0, write_bytes=0), "nothing"),
+    (dict(src=0), "non-null"),
+    (dict(src=FAKE_SRC + 8), "aligned"),
+    (dict(dst=0, write_bytes=64), "non-null"),
+    (dict(waves=0), "waves"),
+    (dict(waves=(1 << 20) + 1), "waves"),
+    (dict(flags=8), "flags"),
+])
+def test_stream_probe_validation(kw, needle):
+    a = dict(src=FAKE_SRC, read_bytes=1024, dst=FAKE_OUT, write_bytes=0, waves=64, flags=3)
+    a.update(kw)
+    rc = smol.lib().smol_stream_probe(a["src"] or None, a["read_bytes"], a["dst"] or None,
+                                      a["write_bytes"], a["waves"], a["flags"], None)
+    assert rc == smol.ERR_INVALID_ARG
+    assert needle in smol.lib().smol_last_error().decode()
+

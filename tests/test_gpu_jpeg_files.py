@@ -174,3 +174,10 @@ def test_side_streams_match_the_current_stream():
         low = smol.run_workload(wl, src, stream=st)
         torch.cuda.synchronize()
         assert torch.equal(got, ref) and torch.equal(low, low_ref)
+        # a caller-supplied output filled on the current stream just before:
+        # the side-stream call must overwrite it only after that fill
+        out = torch.empty_like(ref)
+        out.fill_(7.0)
+        got = smol.jpeg_files_preprocess(files, p, threads=4, stream=st, out=out)
+        torch.cuda.synchronize()
+        assert got.data_ptr() == out.data_ptr() and torch.equal(out, ref)
