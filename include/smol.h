@@ -147,6 +147,35 @@ int smol_preprocess_batch(const uint8_t *src, int64_t src_bytes, const int64_t *
                           const int32_t *row_pitch, int32_t n, const smol_params *p, void *out,
                           void *stream);
 
+/* smol_preprocess_batch_noalloc -- smol_preprocess_batch for callers that
+ * cannot allocate memory during the call (tight serving loops, harnesses
+ * that forbid allocation).
+ *
+ * Same arguments, validation, kernels and results as smol_preprocess_batch.
+ * The call allocates nothing: no device memory, no pinned host memory (the
+ * library's other calls allocate the descriptor table and its staging buffer
+ * on first use). A batch that needs a descriptor table (images of different
+ * sizes or offset strides) keeps it in a fixed device array of
+ * SMOL_NOALLOC_MAX_IMAGES descriptors that the library holds on every device
+ * it runs on until the process ends; the table is copied there from host
+ * memory with an ordinary asynchronous host-to-device copy on `stream`.
+ *
+ * Limit: n <= SMOL_NOALLOC_MAX_IMAGES (else SMOL_ERR_UNSUPPORTED, nothing
+ * enqueued).
+ *
+ * Every call on a device shares that device's array. Calls on one stream are
+ * ordered by the stream; calls that overlap on one device (different streams
+ * with no ordering between them, or different host threads) race for the
+ * array and must not be issued.
+ *
+ * Returns as smol_preprocess_batch.
+ */
+#define SMOL_NOALLOC_MAX_IMAGES 4096
+int smol_preprocess_batch_noalloc(const uint8_t *src, int64_t src_bytes, const int64_t *offsets,
+                                  const int32_t *widths, const int32_t *heights,
+                                  const int32_t *row_pitch, int32_t n, const smol_params *p,
+                                  void *out, void *stream);
+
 /* smol_yuv420_preprocess_batch -- planar YCbCr 4:2:0 (I420) uint8 frames ->
  * NCHW RGB.
  *

@@ -40,6 +40,7 @@ SOURCES = [
     "smol_jpeg.cpp",
     "smol_jpeg_entropy.cpp",
     "smol_stream.hip",
+    "smol_scratch.hip",
 ]
 HEADERS = ["smol_internal.h", "smol_device.h", "smol_rows.h", "smol_rows_rgb.h", "smol_rows_yuv.h"]
 

@@ -39,6 +39,11 @@ int fail(int code, const char *fmt, ...)
 std::atomic<int> g_path{0}, g_band_rows{0}, g_lds_budget{0}, g_wg_per_cu{0}, g_exact{0},
     g_row_order{0}, g_upload{0};
 
+// True while this thread runs smol_preprocess_batch_noalloc: descriptor tables
+// then go to the fixed device array of smol_scratch.hip, not to the staging
+// ring and device buffer the other calls allocate.
+thread_local bool t_noalloc = false;
+
 constexpr int kDefaultLdsBudget = 64 * 1024;
 constexpr int kMaxBandRows = 64;
 constexpr int kMaxWorkgroupsPerCu = 16;
@@ -541,7 +546,24 @@ int run_batch(const std::vector<Desc> &descs, size_t first, size_t count, int no
     Staging *st = nullptr;
     std::unique_lock<std::mutex> lk;
     int slot = -1;
-    if (!uniform) {
+    if (!uniform && t_noalloc) {
+        // The call's tables sit side by side in the device's fixed array (a
+        // run of images [first, first + count) at descriptor `first`); calls on
+        // one stream reuse it in stream order.
+        if (first + count > (size_t)smol::kNoallocMaxImages)
+            return fail(SMOL_ERR_UNSUPPORTED, "descriptor table of %zu images exceeds the "
+                        "no-allocation limit of %d", first + count, smol::kNoallocMaxImages);
+        void *table = nullptr;
+        const int rc = smol::scratch_table(device, &table);
+        if (rc != (int)hipSuccess)
+            return hip_fail((hipError_t)rc, "hipGetSymbolAddress(descriptor table)");
+        uint8_t *dv = (uint8_t *)table + first * sizeof(Desc);
+        e = hipMemcpyAsync(dv, descs.data() + first, sizeof(Desc) * count,
+                           hipMemcpyHostToDevice, s);
+        if (e != hipSuccess)
+            return hip_fail(e, "hipMemcpyAsync(descriptors)");
+        a.table = (const Desc *)dv;
+    } else if (!uniform) {
         st = staging_for(device);
         lk = std::unique_lock<std::mutex>(st->mu);
         const size_t bytes = sizeof(Desc) * count;
@@ -1119,6 +1141,23 @@ int smol_preprocess_batch(const uint8_t *src, int64_t src_bytes, const int64_t *
                           const int32_t *row_pitch, int32_t n, const smol_params *p, void *out,
                           void *stream)
 {
+    return rgb_batch(src, src_bytes, offsets, widths, heights, row_pitch, nullptr, n, p, nullptr,
+                     out, stream);
+}
+
+int smol_preprocess_batch_noalloc(const uint8_t *src, int64_t src_bytes, const int64_t *offsets,
+                                  const int32_t *widths, const int32_t *heights,
+                                  const int32_t *row_pitch, int32_t n, const smol_params *p,
+                                  void *out, void *stream)
+{
+    g_last_error.clear();
+    if (n > SMOL_NOALLOC_MAX_IMAGES)
+        return fail(SMOL_ERR_UNSUPPORTED, "n = %d exceeds the %d images of the no-allocation "
+                    "call's descriptor table", n, SMOL_NOALLOC_MAX_IMAGES);
+    struct Scope {
+        Scope() { t_noalloc = true; }
+        ~Scope() { t_noalloc = false; }
+    } scope;
     return rgb_batch(src, src_bytes, offsets, widths, heights, row_pitch, nullptr, n, p, nullptr,
                      out, stream);
 }

@@ -112,6 +112,14 @@ int launch_jpeg_idct(const JpegArgs &a, int grid, void *stream);
 // status; fails as the batch calls would on these parameters.
 int mcu_rect(int64_t W, int64_t H, const smol_params *p, int resize_mode, int32_t rect[4]);
 
+// smol_preprocess_batch_noalloc keeps a ragged batch's descriptor table in a
+// fixed device array of kNoallocTableBytes (smol_scratch.hip) instead of
+// memory the library allocates. scratch_table() returns that array's device
+// address on `device` (the current device), looked up once per device.
+constexpr int kNoallocMaxImages = SMOL_NOALLOC_MAX_IMAGES;
+constexpr size_t kNoallocTableBytes = (size_t)kNoallocMaxImages * sizeof(Desc);
+int scratch_table(int device, void **table);
+
 // Device compute units (0 when unknown).
 int device_cus();
 

@@ -112,6 +112,9 @@ _vp = ctypes.c_void_p
 SIGNATURES = {
     "smol_preprocess_batch": (ctypes.c_int, [_vp, ctypes.c_int64, _vp, _vp, _vp, _vp,
                                              ctypes.c_int32, ctypes.POINTER(Params), _vp, _vp]),
+    "smol_preprocess_batch_noalloc": (ctypes.c_int, [_vp, ctypes.c_int64, _vp, _vp, _vp, _vp,
+                                                     ctypes.c_int32, ctypes.POINTER(Params), _vp,
+                                                     _vp]),
     "smol_yuv420_preprocess_batch": (ctypes.c_int, [_vp, ctypes.c_int64, _vp, _vp, _vp, _vp, _vp,
                                                     ctypes.c_int32, ctypes.POINTER(Params), _vp,
                                                     _vp]),

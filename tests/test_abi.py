@@ -477,3 +477,15 @@ def test_stream_probe_validation(kw, needle):
     assert rc == smol.ERR_INVALID_ARG
     assert needle in smol.lib().smol_last_error().decode()
 
+
+def test_noalloc_refuses_batches_over_its_table():
+    n = 4097
+    p = _params()
+    offs = np.zeros(n, np.int64)
+    w = np.full(n, 320, np.int32)
+    h = np.full(n, 240, np.int32)
+    rc = smol.lib().smol_preprocess_batch_noalloc(FAKE_SRC, 10**9, offs.ctypes.data, w.ctypes.data,
+                                                  h.ctypes.data, None, n, ctypes.byref(p),
+                                                  FAKE_OUT, None)
+    assert rc == smol.ERR_UNSUPPORTED
+    assert "4096" in smol.lib().smol_last_error().decode()
