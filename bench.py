@@ -178,7 +178,10 @@ def algorithmic_ops(wl, smol) -> int:
     """fp32 operations of the definition per batch (see the constants)."""
     pixels = wl.n * wl.crop_h * wl.crop_w
     if wl.kind == "rgb":
-        return pixels * OPS_PER_PIXEL_RGB
+        # the low-resolution op's first launch: three lerps per channel at
+        # each of the r x r reduced pixels (stored rounded, not normalised)
+        low = wl.n * wl.low_res * wl.low_res * 3 * 9 if wl.low_res else 0
+        return pixels * OPS_PER_PIXEL_RGB + low
     ops = pixels * OPS_PER_PIXEL_I420
     if wl.kind == "jpeg":
         import math
