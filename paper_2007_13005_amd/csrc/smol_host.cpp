@@ -1370,8 +1370,13 @@ void smol::clear_error() { g_last_error.clear(); }
 
 int smol::mcu_rect(int64_t W, int64_t H, const smol_params *p, int resize_mode, int32_t rect[4])
 {
+    // the parameters as the batch calls check them (a zero crop would make
+    // the resized size of a direct resize zero)
+    int rc = check_params(p);
+    if (rc)
+        return rc;
     Geo g;
-    int rc = image_geo(W, H, p, resize_mode, &g, 0);
+    rc = image_geo(W, H, p, resize_mode, &g, 0);
     if (rc)
         return rc;
     int64_t xf, xl, yf, yl, a, b, c0, c1, d0, d1;

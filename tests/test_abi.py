@@ -489,3 +489,15 @@ def test_noalloc_refuses_batches_over_its_table():
                                                   FAKE_OUT, None)
     assert rc == smol.ERR_UNSUPPORTED
     assert "4096" in smol.lib().smol_last_error().decode()
+
+
+@pytest.mark.parametrize("kw", [dict(crop_h=0), dict(crop_w=0), dict(resize_short=0),
+                                dict(std=(0.0, 1.0, 1.0))])
+@pytest.mark.parametrize("mode", [smol.RESIZE_SHORT_CROP, smol.RESIZE_DIRECT])
+def test_mcu_rect_checks_params_like_the_batch_calls(kw, mode):
+    # a zero crop under a direct resize once reached a division by zero
+    p = _params(**kw)
+    rect = np.zeros(4, np.int32)
+    rc = smol.lib().smol_jpeg_mcu_rect(640, 480, ctypes.byref(p),
+                                       ctypes.byref(smol.make_options(mode)), rect.ctypes.data)
+    assert rc == smol.ERR_INVALID_ARG
