@@ -76,8 +76,21 @@ typedef struct smol_pipeline_config {
  * preprocessing launch: it must enqueue its work on `stream` (a hipStream_t)
  * reading the n preprocessed images at `output` (DEVICE, the slot's output
  * buffer, valid in stream order until the work enqueued here completes) and
- * return 0, or nonzero to report a failure. It must not synchronise the
- * stream's device work with the host. */
+ * return 0, or nonzero to report a failure.
+ *
+ * Contract (the submitting thread still holds the slot while the consumer
+ * runs):
+ *   - all of its device work goes on `stream`: the slot is recycled when the
+ *     work on `stream` up to the submission's end completes, so work put on
+ *     other streams is not covered by the slot and is not throttled by the
+ *     pool of slots;
+ *   - it must not wait on the host for device work, and must not call
+ *     smol_pipeline_acquire, _submit*, _drain or _destroy of the same
+ *     pipeline: with every slot held by producers inside their consumers, a
+ *     consumer waiting for a slot or for completions waits forever;
+ *   - it may call the library's batch calls on `stream` (they only enqueue).
+ * The Python binding runs Python consumers with torch's current stream set to
+ * `stream` and refuses those pipeline calls from inside a consumer. */
 typedef int (*smol_consumer_fn)(void *user, const void *output, int32_t n, void *stream);
 
 /* smol_pipeline_create -- allocate the buffers, streams and events on the

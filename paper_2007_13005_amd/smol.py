@@ -9,6 +9,8 @@ from __future__ import annotations
 
 import ctypes
 import os
+import sys
+import threading
 
 import numpy as np
 
@@ -210,11 +212,22 @@ def lib() -> ctypes.CDLL:
     runtimes = _mapped_hip_runtimes()
     if len(runtimes) > 1:
         raise RuntimeError(f"two HIP runtimes are loaded in this process: {runtimes}")
+    bind_signatures(handle)
+    _lib = handle
+    return handle
+
+
+def bind_signatures(handle: ctypes.CDLL, required: bool = True) -> ctypes.CDLL:
+    """Type every declared symbol of a loaded build of the library (a build
+    of only some of its files may skip the missing ones)."""
     for name, (res, args) in SIGNATURES.items():
-        fn = getattr(handle, name)
+        fn = getattr(handle, name, None)
+        if fn is None:
+            if required:
+                raise RuntimeError(f"{name} is missing from the library")
+            continue
         fn.restype = res
         fn.argtypes = args
-    _lib = handle
     return handle
 
 
@@ -780,31 +793,100 @@ class PreparedCall:
                         out_ptr, stream_handle))
 
 
+_consumer_state = threading.local()
+
+
 class Pipeline:
     """Pipelined ingest (``include/smol_pipeline.h``): ``slots`` reused buffer
     sets (pinned host input, device input, device output), ``streams`` compute
-    streams and ``copy_streams`` copy streams. Producer threads ``acquire`` a slot, fill ``host_view(slot)`` with
-    a batch and ``submit`` it; the copy, the preprocessing and the optional
-    consumer (a ``CONSUMER`` callback that enqueues the DNN on the given
-    stream) run in stream order while other slots are filled."""
+    streams and ``copy_streams`` copy streams. Producer threads ``acquire`` a
+    slot, fill ``host_view(slot)`` with a batch and ``submit`` it; the copy,
+    the preprocessing and the optional consumer run in stream order while
+    other slots are filled.
+
+    A consumer is a Python callable ``f(output, n, stream)`` (raw device
+    pointer of the slot's output, image count, raw stream handle) or a
+    ``CONSUMER`` callback ``f(user, output, n, stream)``. It runs on the
+    submitting thread during ``submit``, which still holds the slot. For a
+    Python callable, torch's current stream is the batch's stream while it
+    runs (when torch has a device), so torch work it starts is ordered behind
+    the preprocessing and covered by the slot's completion. From inside any
+    consumer, this pipeline's ``acquire``, ``submit``, ``drain`` and
+    ``close`` raise instead of waiting: the consumer's thread holds a slot,
+    and waiting there for a slot or for completions can wait forever (every
+    slot held by producers inside their consumers)."""
 
     def __init__(self, slots: int, streams: int, input_bytes: int, output_bytes: int,
-                 copy_streams: int = 1, workspace_bytes: int = 0):
+                 copy_streams: int = 1, workspace_bytes: int = 0, library=None):
+        self._lib = lib() if library is None else library
         cfg = PipelineConfig()
         cfg.slots, cfg.streams, cfg.copy_streams = slots, streams, copy_streams
         cfg.input_bytes, cfg.output_bytes = input_bytes, output_bytes
         cfg.workspace_bytes = workspace_bytes
         h = ctypes.c_void_p()
-        _check(lib().smol_pipeline_create(ctypes.byref(cfg), ctypes.byref(h)))
+        self._check(self._lib.smol_pipeline_create(ctypes.byref(cfg), ctypes.byref(h)))
         self._h = h
         self.input_bytes = input_bytes
         self.output_bytes = output_bytes
         self._host = {}
 
+    def _check(self, status: int) -> None:
+        if status != OK:
+            detail = (self._lib.smol_last_error().decode() or
+                      self._lib.smol_status_string(status).decode())
+            raise SmolError(status, detail)
+
+    def _not_in_consumer(self, what: str) -> None:
+        if getattr(_consumer_state, "pipeline", None) is self:
+            raise RuntimeError(f"{what} called from inside a consumer of the same pipeline: the "
+                               "consumer's thread holds a slot, and waiting there for slots or "
+                               "completions can deadlock")
+
+    def _consumer_fn(self, consumer):
+        """The CONSUMER the library calls: the caller's consumer inside the
+        re-entrancy guard (and, for a Python callable, on the batch's torch
+        stream); an exception becomes a failed consumer (nonzero)."""
+        if consumer is None:
+            return CONSUMER()
+        raw = isinstance(consumer, CONSUMER)
+
+        def call(user, output, n, stream):
+            prev = getattr(_consumer_state, "pipeline", None)
+            _consumer_state.pipeline = self
+            try:
+                if raw:
+                    return int(consumer(user, output, n, stream))
+                torch = sys.modules.get("torch")
+                if torch is not None and torch.cuda.is_available():
+                    with torch.cuda.stream(torch.cuda.ExternalStream(stream)):
+                        consumer(output, n, stream)
+                else:
+                    consumer(output, n, stream)
+                return 0
+            except Exception as e:  # noqa: BLE001 -- reported as a failed consumer
+                _consumer_state.error = e
+                return 1
+            finally:
+                _consumer_state.pipeline = prev
+
+        return CONSUMER(call)
+
+    def _submitted(self, status: int) -> None:
+        """Check a submission; a consumer's exception becomes the cause."""
+        err = getattr(_consumer_state, "error", None)
+        _consumer_state.error = None
+        try:
+            self._check(status)
+        except SmolError as e:
+            if err is not None:
+                raise e from err
+            raise
+
     def acquire(self) -> tuple[int, int, int]:
         """(slot, host pointer, device output pointer)."""
+        self._not_in_consumer("acquire")
         slot, host, out = ctypes.c_int32(), ctypes.c_void_p(), ctypes.c_void_p()
-        _check(lib().smol_pipeline_acquire(self._h, ctypes.byref(slot), ctypes.byref(host),
+        self._check(self._lib.smol_pipeline_acquire(self._h, ctypes.byref(slot), ctypes.byref(host),
                                            ctypes.byref(out)))
         self._host[slot.value] = host.value
         return slot.value, host.value, out.value
@@ -815,7 +897,7 @@ class Pipeline:
         return np.ctypeslib.as_array(buf)
 
     def release(self, slot: int) -> None:
-        _check(lib().smol_pipeline_release(self._h, slot))
+        self._check(self._lib.smol_pipeline_release(self._h, slot))
 
     def submit(self, slot: int, nbytes: int, offsets, widths, heights, params: Params,
                pitches=None, rois=None, options: Options | None = None, consumer=None,
@@ -826,11 +908,13 @@ class Pipeline:
         pt = None if pitches is None else _table(pitches, np.int32)
         n = len(off)
         r = _rois(rois, n)
-        _check(lib().smol_pipeline_submit(
+        self._not_in_consumer("submit")
+        _consumer_state.error = None
+        self._submitted(self._lib.smol_pipeline_submit(
             self._h, slot, nbytes, off.ctypes.data, w.ctypes.data, h.ctypes.data,
             None if pt is None else pt.ctypes.data, None if r is None else r.ctypes.data, n,
             ctypes.byref(params), None if options is None else ctypes.byref(options),
-            CONSUMER() if consumer is None else consumer, user))
+            self._consumer_fn(consumer), user))
 
     def submit_yuv420(self, slot: int, nbytes: int, y_offsets, cb_offsets, cr_offsets, widths,
                       heights, params: Params, rois=None, options: Options | None = None,
@@ -842,11 +926,13 @@ class Pipeline:
         h = _table(heights, np.int32)
         n = len(yo)
         r = _rois(rois, n)
-        _check(lib().smol_pipeline_submit_yuv420(
+        self._not_in_consumer("submit")
+        _consumer_state.error = None
+        self._submitted(self._lib.smol_pipeline_submit_yuv420(
             self._h, slot, nbytes, yo.ctypes.data, bo.ctypes.data, ro.ctypes.data, w.ctypes.data,
             h.ctypes.data, None if r is None else r.ctypes.data, n, ctypes.byref(params),
             None if options is None else ctypes.byref(options),
-            CONSUMER() if consumer is None else consumer, user))
+            self._consumer_fn(consumer), user))
 
     def submit_jpeg(self, slot: int, nbytes: int, coef_offsets, qtables, widths, heights,
                     params: Params, coef_layout: int = JPEG_COEF_WINDOW,
@@ -859,11 +945,13 @@ class Pipeline:
         h = _table(heights, np.int32)
         n = len(co)
         q, nq = _qtables(qtables, n)
-        _check(lib().smol_pipeline_submit_jpeg(
+        self._not_in_consumer("submit")
+        _consumer_state.error = None
+        self._submitted(self._lib.smol_pipeline_submit_jpeg(
             self._h, slot, nbytes, co.ctypes.data, q.ctypes.data, nq, w.ctypes.data,
             h.ctypes.data, n, coef_layout, ctypes.byref(params),
             None if options is None else ctypes.byref(options),
-            CONSUMER() if consumer is None else consumer, user))
+            self._consumer_fn(consumer), user))
 
     def decode_jpeg_into(self, slot: int, streams, params: Params,
                          options: Options | None = None, threads: int = 0):
@@ -885,24 +973,26 @@ class Pipeline:
         offs = np.concatenate([[0], np.cumsum(sizes)[:-1]]).astype(np.int64)
         data = np.frombuffer(b"".join(streams), np.uint8)
         q = np.zeros((n, 2, 64), np.uint16)
-        _check(lib().smol_jpeg_entropy_decode_batch(
+        self._check(self._lib.smol_jpeg_entropy_decode_batch(
             data.ctypes.data, data.size, offs.ctypes.data, sizes.ctypes.data, n,
             rects.ctypes.data, self._host[slot], total, co.ctypes.data, JPEG_COEF_WINDOW,
             q.ctypes.data, threads))
         return 2 * total, co, q, w, h
 
     def drain(self) -> None:
-        _check(lib().smol_pipeline_drain(self._h))
+        self._not_in_consumer("drain")
+        self._check(self._lib.smol_pipeline_drain(self._h))
 
     def stats(self) -> dict:
         st = PipelineStats()
-        _check(lib().smol_pipeline_get_stats(self._h, ctypes.byref(st)))
+        self._check(self._lib.smol_pipeline_get_stats(self._h, ctypes.byref(st)))
         return st.as_dict()
 
     def close(self) -> None:
         if self._h is not None and self._h.value:
+            self._not_in_consumer("close")
             h, self._h = self._h, None
-            _check(lib().smol_pipeline_destroy(h))
+            self._check(self._lib.smol_pipeline_destroy(h))
 
     def __enter__(self):
         return self
