@@ -134,10 +134,10 @@ typedef struct smol_geometry {
  *              stream.
  *
  * Host tables and p are read before the call returns. When the images do not
- * share one size and a constant offset stride, the call uploads a per-image
- * descriptor table (80 bytes per image) through a pinned staging buffer that
- * the library keeps per device and reuses in stream order (a small copy
- * kernel on `stream` moves it to device memory; see smol_tuning.upload).
+ * share one size and a constant offset stride, the call writes a per-image
+ * descriptor table (80 bytes per image) to a pinned staging buffer that the
+ * library keeps per device and reuses in stream order; the kernel reads it
+ * from there (see smol_tuning.upload).
  *
  * Returns SMOL_OK, SMOL_ERR_INVALID_ARG (nothing enqueued),
  * SMOL_ERR_UNSUPPORTED (resized side beyond SMOL_MAX_RESIZED) or SMOL_ERR_HIP.
@@ -377,11 +377,12 @@ int smol_image_geometry_ex(int32_t width, int32_t height, int32_t yuv420, const 
  *               0 (default): 2 for uniform RGB batches whose staged rows
  *               exceed 2 KiB, else 1
  *   upload      how a ragged batch's descriptor table reaches the device:
- *               1 a DMA copy on the library's copy stream, which the
- *               caller's stream waits for (overlaps earlier kernels; costs
- *               more host time per call); 0 (default) or 2: a small copy
- *               kernel on the caller's stream that reads the pinned staging
- *               slot (about a microsecond of GPU time) */
+ *               0 (default) or 3: no copy, the preprocessing kernel reads the
+ *               pinned staging slot itself (one launch per call); 1 a DMA
+ *               copy on the library's copy stream, which the caller's stream
+ *               waits for (overlaps earlier kernels; costs more host time per
+ *               call); 2: a small copy kernel on the caller's stream that
+ *               moves the pinned staging slot to device memory first */
 typedef struct smol_tuning {
     int32_t path;
     int32_t band_rows;

@@ -99,14 +99,23 @@ struct Geo {
 };
 
 // Short side -> S, long side floor(S * long / short).
+// a / b for a >= 0, b > 0: a 32-bit division when both fit (several times
+// cheaper than a 64-bit one on x86, and per image the host does five)
+inline int64_t udiv(int64_t a, int64_t b)
+{
+    if (((uint64_t)a | (uint64_t)b) >> 32 == 0)
+        return (int64_t)((uint32_t)a / (uint32_t)b);
+    return a / b;
+}
+
 void resized(int64_t W, int64_t H, int64_t S, int64_t *Wr, int64_t *Hr)
 {
     if (W <= H) {
         *Wr = S;
-        *Hr = S * H / W;
+        *Hr = udiv(S * H, W);
     } else {
         *Hr = S;
-        *Wr = S * W / H;
+        *Wr = udiv(S * W, H);
     }
 }
 
@@ -119,7 +128,7 @@ void tap_index(int64_t x, int64_t in, int64_t out, int64_t *x0, int64_t *x1)
         *x0 = *x1 = 0;
         return;
     }
-    const int64_t q = num / (2 * out);
+    const int64_t q = udiv(num, 2 * out);
     if (q >= in - 1) {
         *x0 = *x1 = in - 1;
         return;
@@ -586,14 +595,21 @@ int run_batch(const std::vector<Desc> &descs, size_t first, size_t count, int no
         uint8_t *h = st->host + (size_t)slot * st->slot_cap;
         uint8_t *dv = st->dev + (size_t)slot * st->slot_cap;
         std::memcpy(h, descs.data() + first, bytes);
-        // By default the table goes through a copy kernel on the caller's
-        // stream that reads the pinned slot over the bus: one launch more and
-        // about a microsecond of GPU time. The alternative, a DMA copy on the
-        // copy stream that the caller's stream waits for, overlaps earlier
-        // kernels but its cross-stream wait costs more host time per call
-        // than a short kernel takes (measured: 256 ROIs, 34 against 26 us
-        // of host time per call), and was not faster on long kernels either.
-        if (g_upload.load() != 1) {
+        // By default the kernel reads the table from the pinned slot over the
+        // bus (one launch per call; measured: 256 ROIs 24.6 against 26.2 us
+        // per call, 256 ragged images 52.9 against 53.9, with no slower
+        // kernel). The alternatives: a copy kernel on the caller's stream
+        // that moves the slot to device memory first (one launch more, about
+        // 4 us of GPU time under the tracer), or a DMA copy on the copy
+        // stream that the caller's stream waits for, which costs more host
+        // time per call than a short kernel takes (34 against 26 us of host
+        // time per call for 256 ROIs).
+        const int upload = g_upload.load();
+        if (upload == 0 || upload == 3) {
+            // the kernel reads the pinned slot itself, over the bus: one
+            // launch (the slot is reused only after that kernel completes)
+            dv = st->host_dev + (size_t)slot * st->slot_cap;
+        } else if (upload == 2) {
             const int rc = smol::launch_table_copy(st->host_dev + (size_t)slot * st->slot_cap, dv,
                                                    bytes, stream);
             if (rc != (int)hipSuccess)
@@ -699,6 +715,11 @@ static int rgb_batch(const uint8_t *src, int64_t src_bytes, const int64_t *offse
     std::vector<Desc> descs((size_t)n);
     std::vector<uint8_t> inside((size_t)n);  // every 8-byte source window lies in src
     int64_t max_span = 0;
+    // The geometry of a region depends on its size only: the previous
+    // image's is reused when the size repeats (a uniform batch computes it
+    // once).
+    int64_t memo_w = -1, memo_h = -1, memo_xf = 0, memo_xl = 0, memo_yf = 0, memo_yl = 0;
+    Geo memo_g{};
     for (int32_t i = 0; i < n; ++i) {
         Geo g;
         const int64_t FW = widths[i], FH = heights[i];
@@ -718,9 +739,30 @@ static int rgb_batch(const uint8_t *src, int64_t src_bytes, const int64_t *offse
         rc = region(rois, i, FW, FH, &rx, &ry, &W, &H);
         if (rc)
             return rc;
-        rc = image_geo(W, H, p, o.resize_mode, &g, i);
-        if (rc)
-            return rc;
+        int64_t xf, xl, yf, yl;
+        if (W == memo_w && H == memo_h) {
+            g = memo_g;
+            xf = memo_xf;
+            xl = memo_xl;
+            yf = memo_yf;
+            yl = memo_yl;
+        } else {
+            rc = image_geo(W, H, p, o.resize_mode, &g, i);
+            if (rc)
+                return rc;
+            int64_t a, b;
+            tap_index(g.left, W, g.Wr, &xf, &a);
+            tap_index(g.left + p->crop_w - 1, W, g.Wr, &b, &xl);
+            tap_index(g.top, H, g.Hr, &yf, &a);
+            tap_index(g.top + p->crop_h - 1, H, g.Hr, &b, &yl);
+            memo_w = W;
+            memo_h = H;
+            memo_g = g;
+            memo_xf = xf;
+            memo_xl = xl;
+            memo_yf = yf;
+            memo_yl = yl;
+        }
         const int64_t off = offsets[i] + ry * pitch + 3 * rx;  // the region's first pixel
         Desc &d = descs[i];
         std::memset(&d, 0, sizeof d);
@@ -733,15 +775,10 @@ static int rgb_batch(const uint8_t *src, int64_t src_bytes, const int64_t *offse
         d.Hr = (int32_t)g.Hr;
         d.left = (int32_t)g.left;
         d.top = (int32_t)g.top;
-        int64_t xf, xl;
-        x_span(d, p->crop_w, &xf, &xl);
         d.xf = (int32_t)xf;
         d.span = (int32_t)std::min<int64_t>(3 * (xl - xf + 1), INT32_MAX);
         {
             // every 16-byte chunk holding a staged byte lies inside src
-            int64_t yf, yd, yd2, yl;
-            tap_index(g.top, H, g.Hr, &yf, &yd);
-            tap_index(g.top + p->crop_h - 1, H, g.Hr, &yd2, &yl);
             const uintptr_t base = (uintptr_t)src + (uintptr_t)off + 3 * (uintptr_t)xf;
             const uintptr_t first = (base + (uintptr_t)yf * (uintptr_t)pitch) & ~(uintptr_t)15;
             const uintptr_t last = base + (uintptr_t)yl * (uintptr_t)pitch + 3 * (uintptr_t)(xl - xf + 1);
@@ -1313,8 +1350,8 @@ int smol_set_tuning(const smol_tuning *t)
         return fail(SMOL_ERR_INVALID_ARG, "exact %d is neither 0 nor 1", t->exact);
     if (t->row_order < 0 || t->row_order > 2)
         return fail(SMOL_ERR_INVALID_ARG, "row_order %d outside 0..2", t->row_order);
-    if (t->upload < 0 || t->upload > 2)
-        return fail(SMOL_ERR_INVALID_ARG, "upload %d outside 0..2", t->upload);
+    if (t->upload < 0 || t->upload > 3)
+        return fail(SMOL_ERR_INVALID_ARG, "upload %d outside 0..3", t->upload);
     g_path = t->path;
     g_band_rows = t->band_rows;
     g_lds_budget = t->lds_budget;

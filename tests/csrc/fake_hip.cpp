@@ -1,5 +1,5 @@
 // The thread-backed HIP stand-in declared in fake_hip/hip/hip_runtime.h, and
-// the library's kernel launchers as tasks on it (each takes kKernelUs), so
+// the library's kernel launchers as tasks on it (each takes kernel_us()), so
 // that the pipeline and the host code run on the CPU with real concurrency:
 // producer threads, stream workers, host waits on events.
 #include <hip/hip_runtime.h>
@@ -18,7 +18,16 @@
 
 namespace {
 
-constexpr unsigned kKernelUs = 200;
+// Duration of a kernel task: 200 us, or FAKE_HIP_KERNEL_US from the
+// environment.
+unsigned kernel_us()
+{
+    static const unsigned us = [] {
+        const char *e = std::getenv("FAKE_HIP_KERNEL_US");
+        return e ? (unsigned)std::atoi(e) : 200u;
+    }();
+    return us;
+}
 std::atomic<long> g_pending{0};
 
 }  // namespace
@@ -204,7 +213,10 @@ hipError_t hipHostGetDevicePointer(void **dev, void *host, unsigned)
 
 void fake_hip_enqueue_task(hipStream_t s, unsigned us)
 {
-    stream_of(s).push([us] { std::this_thread::sleep_for(std::chrono::microseconds(us)); });
+    stream_of(s).push([us] {
+        if (us)
+            std::this_thread::sleep_for(std::chrono::microseconds(us));
+    });
 }
 
 long fake_hip_pending(void) { return g_pending.load(); }
@@ -213,7 +225,7 @@ namespace smol {
 namespace {
 int task(void *stream)
 {
-    fake_hip_enqueue_task((hipStream_t)stream, kKernelUs);
+    fake_hip_enqueue_task((hipStream_t)stream, kernel_us());
     return hipSuccess;
 }
 uint8_t g_scratch[kNoallocTableBytes];

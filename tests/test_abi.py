@@ -155,8 +155,9 @@ def test_tuning_validation():
     with pytest.raises(smol.SmolError):
         smol.set_tuning(row_order=3)
     with pytest.raises(smol.SmolError):
-        smol.set_tuning(upload=3)
+        smol.set_tuning(upload=4)
     smol.set_tuning(path=1, band_rows=8, lds_budget=32768)
+    smol.set_tuning(upload=3)
     smol.set_tuning(upload=2)
     smol.set_tuning(path=4, exact=1)
     smol.reset_tuning()

@@ -175,11 +175,12 @@ def test_detection_crops_c6_full():
     _check(synthetic.c6())
 
 
-@pytest.mark.parametrize("upload", [0, 1, 2])
+@pytest.mark.parametrize("upload", [0, 1, 2, 3])
 def test_descriptor_upload_paths(upload):
-    """Both ways a ragged table reaches the device (DMA on the copy stream, or
-    the copy kernel on the caller's stream) give the oracle's results, over
-    more calls than the staging ring has slots."""
+    """Every way a ragged table reaches the device (DMA on the copy stream,
+    the copy kernel on the caller's stream, or the kernel reading the pinned
+    slot itself) gives the oracle's results, over more calls than the staging
+    ring has slots."""
     smol.set_tuning(upload=upload)
     wl = synthetic.c6(n=24)
     ref = run_oracle(wl)
@@ -187,4 +188,28 @@ def test_descriptor_upload_paths(upload):
         got = run_gpu(wl)
         assert_parity(got, ref, wl.out_dtype, f"c6 upload={upload}")
     assert smol.last_plan()["uploaded_descriptors"] == 1
-    assert smol.last_plan()["launches"] == (1 if upload == 1 else 2)
+    assert smol.last_plan()["launches"] == (2 if upload == 2 else 1)
+
+
+@pytest.mark.parametrize("upload", [0, 2])
+def test_back_to_back_ragged_calls_reuse_the_ring(upload):
+    """40 ragged calls enqueued back to back, each on its own images and
+    output, with no synchronisation between them (the 16-slot staging ring is
+    reused while earlier kernels may still read it): every output matches the
+    oracle."""
+    import torch
+    smol.set_tuning(upload=upload)
+    try:
+        wls = [synthetic.c6(n=8 + (k % 5)) for k in range(4)]
+        refs = [run_oracle(wl) for wl in wls]
+        srcs = [torch.from_numpy(wl.src).to("cuda:0") for wl in wls]
+        torch.cuda.synchronize()
+        outs = []
+        for k in range(40):
+            outs.append(smol.run_workload(wls[k % 4], srcs[k % 4]))
+        torch.cuda.synchronize()
+        for k, out in enumerate(outs):
+            assert_parity(out.cpu().numpy(), refs[k % 4], wls[k % 4].out_dtype,
+                          f"call {k} upload={upload}")
+    finally:
+        smol.reset_tuning()
