@@ -669,11 +669,17 @@ int smol_ref_yuv420_lowres_preprocess_batch(const uint8_t *src, int64_t src_byte
  *     raster order over the MCU-padded frame, luma then Cb then Cr;
  *   - dequantisation multiplies by the table entry; the inverse DCT is
  *     ITU-T T.81's A.3.3 formula, evaluated in fp32 as two 1-D passes
- *     (horizontal frequencies first), each sum over the frequency index in
- *     increasing order, every product and sum rounded on its own, with the
- *     table c[k][n] = C(k)/2 cos((2n+1) k pi / 16) (C(0) = 1/sqrt(2), else 1)
- *     formed in double and rounded once to fp32; then + 128, rounded to
- *     nearest (ties to even) and clamped to 0..255;
+ *     (horizontal frequencies first). T.81 fixes the real value only; each
+ *     1-D sum x[n] = sum_k c[k][n] d[k] is evaluated through the parity of
+ *     the cosine basis, c[k][7-n] = (-1)^k c[k][n] (an identity of the
+ *     formula): for n = 0..3, E = c[0][n] d[0] + c[2][n] d[2] + c[4][n] d[4]
+ *     + c[6][n] d[6] and O = c[1][n] d[1] + c[3][n] d[3] + c[5][n] d[5]
+ *     + c[7][n] d[7], each summed in increasing frequency, then
+ *     x[n] = E + O and x[7-n] = E - O; every product and sum is rounded on
+ *     its own, and the table c[k][n] = C(k)/2 cos((2n+1) k pi / 16)
+ *     (C(0) = 1/sqrt(2), else 1) for n = 0..3 is formed in double and
+ *     rounded once to fp32; then + 128, rounded to nearest (ties to even)
+ *     and clamped to 0..255;
  *   - Algorithm 1's rectangle: the smallest MCU-aligned rectangle holding
  *     every luma and chroma sample the resize taps read (the algorithm's
  *     scale = min(h, w) / 224 is replaced by the exact tap footprint, as for
@@ -690,30 +696,42 @@ static void jpeg_idct_table(float c[64])
         }
 }
 
+/* One 1-D inverse transform of the 8 values in[0], in[st], ..., in[7 st]
+ * into out[0], out[st], ...: the sum over k of c[k][n] in[k] for each n,
+ * through the parity identity (see the readings above). */
+static void idct_1d(const float c[64], const float *in, float *out, int st)
+{
+    for (int n = 0; n < 4; ++n) {
+        float e = c[0 * 8 + n] * in[0 * st];
+        e = e + c[2 * 8 + n] * in[2 * st];
+        e = e + c[4 * 8 + n] * in[4 * st];
+        e = e + c[6 * 8 + n] * in[6 * st];
+        float o = c[1 * 8 + n] * in[1 * st];
+        o = o + c[3 * 8 + n] * in[3 * st];
+        o = o + c[5 * 8 + n] * in[5 * st];
+        o = o + c[7 * 8 + n] * in[7 * st];
+        out[n * st] = e + o;
+        out[(7 - n) * st] = e - o;
+    }
+}
+
 /* One block: coef[v*8+u] times q[v*8+u], inverse DCT, level shift, round,
  * clamp; the w x h top-left pixels (w, h <= 8) are written to out (row
  * pitch `pitch` bytes). */
 void oracle_idct_block(const int16_t *coef, const uint16_t *q, uint8_t *out, int64_t pitch,
                        int32_t w, int32_t h)
 {
-    float c[64], d[64], g[64];
+    float c[64], d[64], g[64], f[64];
     jpeg_idct_table(c);
     for (int i = 0; i < 64; ++i)
         d[i] = (float)((int32_t)coef[i] * (int32_t)q[i]); /* exact: |.| < 2^24 */
     for (int v = 0; v < 8; ++v) /* horizontal pass: row v of frequencies */
-        for (int x = 0; x < 8; ++x) {
-            float s = 0.0f;
-            for (int u = 0; u < 8; ++u)
-                s = s + c[u * 8 + x] * d[v * 8 + u];
-            g[v * 8 + x] = s;
-        }
-    for (int y = 0; y < h; ++y) /* vertical pass */
-        for (int x = 0; x < w; ++x) {
-            float s = 0.0f;
-            for (int v = 0; v < 8; ++v)
-                s = s + c[v * 8 + y] * g[v * 8 + x];
-            out[y * pitch + x] = round_u8(s + 128.0f);
-        }
+        idct_1d(c, d + v * 8, g + v * 8, 1);
+    for (int x = 0; x < 8; ++x) /* vertical pass: column x */
+        idct_1d(c, g + x, f + x, 8);
+    for (int y = 0; y < h; ++y)
+        for (int x = 0; x < w; ++x)
+            out[y * pitch + x] = round_u8(f[y * 8 + x] + 128.0f);
 }
 
 /* Blocks of the MCU-padded frame: luma bw x bh, chroma bw/2 x bh/2 each. */

@@ -169,3 +169,31 @@ def test_partial_decode_equals_full_decode_inside_the_rect():
     # blocks along the right and bottom frame edges are clipped, not skipped
     edge = oracle.jpeg_decode_i420(coef, qy, qc, W, H, (192, 64, 11, 13), fill=7)
     assert np.array_equal(edge[0][64:, 192:], full[0][64:, 192:])
+
+
+def test_dense_blocks_match_the_double_formula():
+    """Blocks with every coefficient nonzero (Laplacian terms falling off with
+    frequency, as in coded photographs, and full-range noise): the oracle's
+    output equals T.81's formula evaluated in double and rounded, except
+    where the double value lies within 1e-3 of a rounding boundary or of the
+    clamp, and is never more than 1/2 + 1e-3 from it before clamping. This
+    pins the sum as a whole: a dropped or doubled term, a sign error in the
+    parity split or a transposed pass all move pixels by far more."""
+    rng = np.random.default_rng(24)
+    B = np.stack([_basis(u, v) for v in range(8) for u in range(8)])  # [k, y, x]
+    q = np.ones(64, np.uint16)
+    for trial in range(300):
+        if trial % 2:
+            c = rng.integers(-300, 301, 64)
+        else:
+            uu, vv = np.meshgrid(np.arange(8), np.arange(8))
+            c = np.rint(rng.laplace(0, 60 / (1 + uu + vv))).reshape(64)
+            c[0] = rng.integers(-400, 400)
+        c = np.clip(c, -1024, 1023).astype(np.int16)
+        exact = 128 + np.tensordot(c.astype(np.float64), B, axes=(0, 0))
+        got = oracle.idct_block(c, q).astype(np.float64)
+        inside = (exact > 0.001) & (exact < 254.999)
+        frac = np.abs(exact - np.floor(exact) - 0.5)
+        sure = inside & (frac > 1e-3)
+        assert np.array_equal(got[sure], np.rint(exact[sure])), trial
+        assert np.all(np.abs(got[inside] - exact[inside]) <= 0.5 + 1e-3), trial
