@@ -169,9 +169,10 @@ def algorithmic_bytes(wl, smol) -> int:
 # products and sums) and the clamp of 3 channels (2 each).
 OPS_PER_PIXEL_RGB = 3 * 9 + 3 * 2
 OPS_PER_PIXEL_I420 = OPS_PER_PIXEL_RGB + 4 * (2 * 9 + 10 + 6)
-# Block decoding: dequantisation (64 products) and two passes of 64 outputs,
-# each a sum of 8 products (8 multiplies, 7 adds).
-OPS_PER_JPEG_BLOCK = 64 + 2 * 64 * 15
+# Block decoding: dequantisation (64 products) and two passes of eight 1-D
+# transforms, each 4 output pairs of an even and an odd sum (4 multiplies and
+# 3 adds each) and their sum and difference.
+OPS_PER_JPEG_BLOCK = 64 + 2 * 8 * 4 * (2 * 7 + 2)
 
 
 def algorithmic_ops(wl, smol) -> int:

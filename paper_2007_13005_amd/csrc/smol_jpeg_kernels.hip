@@ -4,13 +4,16 @@
 // decoding that produces the coefficients is the CPU decoder's.
 //
 // A wave decodes up to eight horizontally adjacent blocks of one block row
-// at a time: lane l loads coefficient row v = l % 8 of block b = l / 8 (16
-// contiguous bytes), forms the horizontal pass G(v, x) = sum_u c(u, x) D(v, u)
-// for all x in registers, and, after an exchange through LDS, output row
-// y = l % 8 of block b: f(y, x) = sum_v c(v, y) G(v, x). Both sums run in
-// increasing frequency (T.81 A.3.3 evaluated separably), each product and
-// sum rounded on its own (no contraction); then + 128, rounded to nearest
-// even, clamped.
+// at a time. Each 1-D transform x(n) = sum_k c(k, n) D(k) is evaluated
+// through the parity of the cosine basis, c(k, 7 - n) = (-1)^k c(k, n): for
+// n < 4 the even-frequency sum E and the odd-frequency sum O (each in
+// increasing frequency), then x(n) = E + O and x(7 - n) = E - O (T.81 A.3.3
+// evaluated separably), each product and sum rounded on its own (no
+// contraction). Pass 1: lane l loads coefficient row v = l % 8 of block
+// b = l / 8 (16 contiguous bytes) and forms G(v, x) for all x in registers.
+// After an exchange through LDS, pass 2: lane l forms output rows y and 7 - y
+// (y = l % 4) of block b at columns 4 h .. 4 h + 3 (h = (l % 8) / 4). Then
+// + 128, rounded to nearest even, clamped.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -23,13 +26,14 @@ constexpr int kBlocksPerWave = 8;
 
 __global__ void __launch_bounds__(64) jpeg_idct_kernel(JpegArgs a)
 {
-    __shared__ float g[kBlocksPerWave][8][8];  // [block][v][x]
+    __shared__ __attribute__((aligned(16))) float g[kBlocksPerWave][8][8];  // [block][v][x]
     const int l = threadIdx.x;
-    const int b = l >> 3, row = l & 7;  // block of the group; v (pass 1) or y (pass 2)
-    float cr[8];                        // c(k, row) for pass 2
+    const int b = l >> 3, row = l & 7;  // block of the group; coefficient row v of pass 1
+    const int y = row & 3, h = row >> 2;  // pass 2: output rows y, 7 - y; columns 4h .. 4h + 3
+    float cy[8];                          // c(k, y) for pass 2
 #pragma unroll
     for (int k = 0; k < 8; ++k)
-        cr[k] = a.c[k * 8 + row];
+        cy[k] = a.c[k * 8 + y];
     // job indices stay below 2^31 (the host splits launches), so the job
     // mapping runs in 32-bit unsigned arithmetic
     const uint32_t jobs = a.run[a.runs - 1].jobs_end;
@@ -90,37 +94,59 @@ __global__ void __launch_bounds__(64) jpeg_idct_kernel(JpegArgs a)
             d[u] = (float)((int)raw[u] * (int)q[8 * row + u]);  // exact: |.| < 2^24
         // horizontal pass for row v = row of block bb
 #pragma unroll
-        for (int x = 0; x < 8; ++x) {
-            float s = 0.0f;
-#pragma unroll
-            for (int u = 0; u < 8; ++u)
-                s = s + a.c[u * 8 + x] * d[u];
-            g[b][row][x] = s;
+        for (int n = 0; n < 4; ++n) {
+            float e = a.c[0 * 8 + n] * d[0];
+            e = e + a.c[2 * 8 + n] * d[2];
+            e = e + a.c[4 * 8 + n] * d[4];
+            e = e + a.c[6 * 8 + n] * d[6];
+            float o = a.c[1 * 8 + n] * d[1];
+            o = o + a.c[3 * 8 + n] * d[3];
+            o = o + a.c[5 * 8 + n] * d[5];
+            o = o + a.c[7 * 8 + n] * d[7];
+            g[b][row][n] = e + o;
+            g[b][row][7 - n] = e - o;
         }
         __syncthreads();
-        // vertical pass for row y = row of block bb
-        uint32_t px4[2] = {0, 0};
-        uint8_t px[8];
+        // vertical pass: rows y and 7 - y of block bb at columns 4h .. 4h + 3
+        typedef float f32x4 __attribute__((ext_vector_type(4)));
+        f32x4 gv[8];
 #pragma unroll
-        for (int x = 0; x < 8; ++x) {
-            float t = 0.0f;
+        for (int v = 0; v < 8; ++v)
+            gv[v] = *(const f32x4 *)&g[b][v][4 * h];
+        uint32_t top = 0, bot = 0;  // four pixels of row y, four of row 7 - y
 #pragma unroll
-            for (int v = 0; v < 8; ++v)
-                t = t + cr[v] * g[b][v][x];
-            px[x] = (uint8_t)__builtin_rintf(fminf(fmaxf(t + 128.0f, 0.0f), 255.0f));
-            px4[x >> 2] |= (uint32_t)px[x] << (8 * (x & 3));
+        for (int i = 0; i < 4; ++i) {
+            float e = cy[0] * gv[0][i];
+            e = e + cy[2] * gv[2][i];
+            e = e + cy[4] * gv[4][i];
+            e = e + cy[6] * gv[6][i];
+            float o = cy[1] * gv[1][i];
+            o = o + cy[3] * gv[3][i];
+            o = o + cy[5] * gv[5][i];
+            o = o + cy[7] * gv[7][i];
+            const uint32_t p0 = (uint32_t)__builtin_rintf(fminf(fmaxf((e + o) + 128.0f, 0.0f), 255.0f));
+            const uint32_t p1 = (uint32_t)__builtin_rintf(fminf(fmaxf((e - o) + 128.0f, 0.0f), 255.0f));
+            top |= p0 << (8 * i);
+            bot |= p1 << (8 * i);
         }
-        const int gx = 8 * (bx0 + b), gy = 8 * by + row;
-        if (b < nb && gy < ph) {
-            uint8_t *dst = a.out + r.out + f * r.out_stride + pbase + (long long)gy * pw + gx;
-            if (gx + 8 <= pw && ((uintptr_t)dst & 7) == 0) {
-                typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-                *(u32x2 *)dst = u32x2{px4[0], px4[1]};
-            } else {
+        const int gx = 8 * (bx0 + b) + 4 * h;
+        if (b < nb && gx < pw) {
+            uint8_t *base = a.out + r.out + f * r.out_stride + pbase;
+            const int gy[2] = {8 * by + y, 8 * by + 7 - y};
+            const uint32_t pix[2] = {top, bot};
 #pragma unroll
-                for (int x = 0; x < 8; ++x)
-                    if (gx + x < pw)
-                        dst[x] = px[x];
+            for (int k = 0; k < 2; ++k) {
+                if (gy[k] >= ph)
+                    continue;
+                uint8_t *dst = base + (long long)gy[k] * pw + gx;
+                if (gx + 4 <= pw && ((uintptr_t)dst & 3) == 0) {
+                    *(uint32_t *)dst = pix[k];
+                } else {
+#pragma unroll
+                    for (int x = 0; x < 4; ++x)
+                        if (gx + x < pw)
+                            dst[x] = (uint8_t)(pix[k] >> (8 * x));
+                }
             }
         }
         __syncthreads();
