@@ -195,8 +195,14 @@ __device__ __forceinline__ void yuv_load(YuvStaged<GL> &st, const YuvCursor &c, 
         st.sh[s] = (int)(row[s] & 15);
         const int last = repeat ? 0 : (st.sh[s] + (s < 2 ? c.yspan : c.cspan) - 1) >> 4;
         GlobalByte *p = (GlobalByte *)(row[s] - (uintptr_t)st.sh[s]);
-        st.c[s] = __builtin_nontemporal_load(
-            (const __attribute__((address_space(1))) u32x4 *)(p + 16u * (uint32_t)min(lane, last)));
+        // chroma rows are shared by consecutive output rows (a chroma row
+        // covers two luma rows): ordinary loads, so the next row's loads of
+        // the same rows hit in the caches; luma rows are streamed once
+        if (s < 2)
+            st.c[s] = __builtin_nontemporal_load(
+                (const __attribute__((address_space(1))) u32x4 *)(p + 16u * (uint32_t)min(lane, last)));
+        else
+            st.c[s] = *(const __attribute__((address_space(1))) u32x4 *)(p + 16u * (uint32_t)min(lane, last));
         if (GL == 2 && s < 2)
             st.c2[s] = __builtin_nontemporal_load(
                 (const __attribute__((address_space(1))) u32x4 *)(p + 16u * (uint32_t)min(64 + lane,
