@@ -365,7 +365,12 @@ __device__ __forceinline__ void cursor_next(RowCursor &c, const BatchArgs &a, co
 // `repeat`: the row was loaded already (past the end of the wave's range);
 // every lane then loads the rows' first chunk, so the instruction stream is
 // unchanged but almost nothing is fetched.
-template <int G>
+// NT: nontemporal loads, for walks that read each source row once (the
+// strided walk of large frames); a contiguous walk meets a source row again
+// when consecutive output rows share it (upscales, downscales by less than
+// 2, and the rows of an image's neighbours in the walk), and ordinary loads
+// let those reads hit in the caches.
+template <int G, int NT = 1>
 __device__ __forceinline__ void load_rows(StagedRows<G> &st, const RowCursor &c, int lane,
                                           bool repeat)
 {
@@ -390,10 +395,14 @@ __device__ __forceinline__ void load_rows(StagedRows<G> &st, const RowCursor &c,
     for (int g = 0; g < G; ++g) {
         const uint32_t o0 = 16u * (uint32_t)min(64 * g + lane, last0);
         const uint32_t o1 = 16u * (uint32_t)min(64 * g + lane, last1);
-        st.c0[g] = __builtin_nontemporal_load(
-            (const __attribute__((address_space(1))) u32x4 *)(p0 + o0));
-        st.c1[g] = __builtin_nontemporal_load(
-            (const __attribute__((address_space(1))) u32x4 *)(p1 + o1));
+        typedef const __attribute__((address_space(1))) u32x4 GlobalChunk;
+        if (NT) {
+            st.c0[g] = __builtin_nontemporal_load((GlobalChunk *)(p0 + o0));
+            st.c1[g] = __builtin_nontemporal_load((GlobalChunk *)(p1 + o1));
+        } else {
+            st.c0[g] = *(GlobalChunk *)(p0 + o0);
+            st.c1[g] = *(GlobalChunk *)(p1 + o1);
+        }
     }
 }
 

@@ -71,10 +71,10 @@ __global__ void __launch_bounds__(64 * kRowsMaxWavesPerGroup) rgb_rows_kernel(Ba
     // outstanding but the prefetched row; the last row is interpolated after
     // it.
     StagedRows<G> A, B, C;
-    load_rows<G>(A, lc, lane, false);
+    load_rows<G, STRIDE>(A, lc, lane, false);
     advance();
     if (P == 2) {
-        load_rows<G>(B, lc, lane, at_end);
+        load_rows<G, STRIDE>(B, lc, lane, at_end);
         advance();
     }
     write_rows<G>(lds, A, lane);
@@ -98,7 +98,7 @@ __global__ void __launch_bounds__(64 * kRowsMaxWavesPerGroup) rgb_rows_kernel(Ba
     };
 #define SMOL_ROWS_STEP(NXT, FUT)                                                              \
     {                                                                                         \
-        load_rows<G>(FUT, lc, lane, at_end);                                                  \
+        load_rows<G, STRIDE>(FUT, lc, lane, at_end);                                                  \
         advance();                                                                            \
         compute();                                                                            \
         write_rows<G>(lds, NXT, lane);                                                        \
