@@ -1437,6 +1437,8 @@ int smol::mcu_rect(int64_t W, int64_t H, const smol_params *p, int resize_mode, 
     return SMOL_OK;
 }
 
+void smol::add_plan_launches(int k) { g_last_plan.launches += k; }
+
 int smol::device_cus()
 {
     int device = 0;

@@ -120,6 +120,10 @@ constexpr int kNoallocMaxImages = SMOL_NOALLOC_MAX_IMAGES;
 constexpr size_t kNoallocTableBytes = (size_t)kNoallocMaxImages * sizeof(Desc);
 int scratch_table(int device, void **table);
 
+// Adds k launches to the calling thread's last plan (smol_last_plan), for
+// calls made of several library calls (partial JPEG decoding).
+void add_plan_launches(int k);
+
 // Device compute units (0 when unknown).
 int device_cus();
 

@@ -14,6 +14,9 @@
 
 namespace {
 
+// launches of block decoding made by the calling thread's last decode
+thread_local int t_decode_launches = 0;
+
 // Block ranges of one frame's rectangle.
 struct Blocks {
     int32_t W, H, bw, bh;
@@ -210,6 +213,7 @@ int smol_jpeg_decode_i420(const int16_t *coef, int64_t coef_elems, const int64_t
         // per job on 128 720p frames
         const int grid = (int)std::min<long long>(jobs, (long long)(cus > 0 ? cus : 256) * 128);
         const int rc = smol::launch_jpeg_idct(a, grid, stream);
+        t_decode_launches += rc == (int)hipSuccess ? 1 : 0;
         a.runs = 0;
         jobs = 0;
         ntables = 0;
@@ -355,15 +359,20 @@ int smol_jpeg_roi_preprocess_batch(const int16_t *coef, int64_t coef_elems,
         ro[(size_t)i] = bo[(size_t)i] + ((W + 1) / 2) * ((H + 1) / 2);
         cur += frame_bytes(W, H);
     }
+    t_decode_launches = 0;
     int rc = smol_jpeg_decode_i420(coef, coef_elems, coef_offsets, qtables, n_qtables, widths,
                                    heights, rects.data(), n, coef_layout,
                                    (uint8_t *)workspace, workspace_bytes, yo.data(), bo.data(),
                                    ro.data(), stream);
     if (rc)
         return rc;
-    return smol_yuv420_preprocess_batch_ex((const uint8_t *)workspace, workspace_bytes,
-                                           yo.data(), bo.data(), ro.data(), widths, heights,
-                                           nullptr, n, p, &o, out, stream);
+    const int decode_launches = t_decode_launches;
+    rc = smol_yuv420_preprocess_batch_ex((const uint8_t *)workspace, workspace_bytes, yo.data(),
+                                         bo.data(), ro.data(), widths, heights, nullptr, n, p,
+                                         &o, out, stream);
+    if (rc == SMOL_OK)
+        smol::add_plan_launches(decode_launches);  // the plan reports both stages
+    return rc;
 }
 
 }  // extern "C"

@@ -113,7 +113,11 @@ def test_partial_decode_then_preprocess(dtype, layout):
     wl.layout = layout
     got = run_gpu(wl)
     stats = assert_parity(got, run_oracle(wl), dtype, wl.name)
-    note(f"    {wl.name}: {stats} plan={smol.last_plan()}")
+    plan = smol.last_plan()
+    note(f"    {wl.name}: {stats} plan={plan}")
+    # the plan counts the block decoding too (one launch for these five
+    # geometries) besides the preprocessing's launches
+    assert plan["launches"] >= 2
 
 
 def test_partial_decode_direct_resize():
