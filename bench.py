@@ -884,6 +884,17 @@ def main() -> int:
         call(sp, sb, op, sh)
     torch.cuda.synchronize()
     plan = smol.last_plan()
+    # Host time per call: a burst of calls shorter than the library's
+    # descriptor ring (16 slots), timed on the host from an idle device, so
+    # that no call waits for an earlier one (binding, validation, descriptors
+    # and the runtime's enqueue).
+    burst = 12
+    t_host = time.perf_counter()
+    for i in range(burst):
+        sp, sb, op = ptrs[i % rotate]
+        call(sp, sb, op, sh)
+    host_us = (time.perf_counter() - t_host) / burst * 1e6
+    torch.cuda.synchronize()
 
     # The timed region, split into 5 repetitions by events on the launch
     # stream (the median per-batch time is reported beside the average).
@@ -952,6 +963,7 @@ def main() -> int:
                    "band_rows": plan["band_rows"], "lds_bytes": plan["lds_bytes"],
                    "grid": plan["grid"], "launches_per_step": plan["launches"],
                    "gpu_ms_per_step": round(gpu_ms / args.steps, 5),
+                   "host_us_per_call": round(host_us, 2),
                    "gpu_us_per_step_median_of_5": round(median_us, 3),
                    "gpu_us_per_step_reps": [round(x, 3) for x in rep_us],
                    "hbm_gbps_wall": round(algo * args.steps / wall / 1e9, 1),
