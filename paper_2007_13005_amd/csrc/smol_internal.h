@@ -132,24 +132,26 @@ int device_cus();
 int set_error(int code, const char *fmt, ...);
 void clear_error();
 
-// Launchers (smol_kernels.hip). Return a hipError_t as int.
+// Launchers (smol_kernels.hip). Return a hipError_t as int. `done`, where
+// given, is an event (or null) that the launch itself signals when the kernel
+// completes.
 // Copies `bytes` (a multiple of 16) from src to dst with a small kernel on
 // `stream` (src may be pinned host memory as the device addresses it).
 int launch_table_copy(const void *src, void *dst, size_t bytes, void *stream);
 // Direct kernels: out_type 0 fp32, 1 fp16, 2 uint8 (rounded, not normalised).
-int launch_rgb_direct(const BatchArgs &a, int out_type, void *stream);
-int launch_rgb_lds(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream);
-int launch_rgb_gather(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream);
+int launch_rgb_direct(const BatchArgs &a, int out_type, void *stream, void *done);
+int launch_rgb_lds(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream, void *done);
+int launch_rgb_gather(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream, void *done);
 // Row-streaming launches: `lds_bytes` is one wave's slot; a workgroup holds
 // a.wpg waves and a.grid is the number of waves (a multiple of a.wpg).
-int launch_rgb_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream);
+int launch_rgb_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream, void *done);
 // Resident workgroups of a.wpg waves per compute unit.
 int occupancy_rgb_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, int *blocks_per_cu);
 // Resident workgroups per compute unit for the persistent kernels.
 int occupancy_rgb_gather(int out_f16, size_t lds_bytes, int *blocks_per_cu);
 int occupancy_rgb_lds(int out_f16, size_t lds_bytes, int *blocks_per_cu);
-int launch_yuv_direct(const BatchArgs &a, int out_type, void *stream);
-int launch_yuv_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream);
+int launch_yuv_direct(const BatchArgs &a, int out_type, void *stream, void *done);
+int launch_yuv_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream, void *done);
 int occupancy_yuv_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, int *blocks_per_cu);
 
 // Row-streaming kernels for the plan in the arguments (the file of each part:

@@ -22,6 +22,7 @@
 // rounded this gives RN(a / std) whenever the quotient is a normal number
 // (Markstein's correction step), which covers every value a = v - mean can
 // take here. fp16 outputs are the round-to-nearest-even of those fp32 values.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -748,6 +749,18 @@ dim3 direct_block(const BatchArgs &a)
     return dim3(64 * (waves < kThreads / 64 ? waves : kThreads / 64));
 }
 
+// Launches `kernel` with its one argument `a`. `done`, when not null, is an
+// event that the launch signals at the kernel's completion: it rides on the
+// dispatch itself, with no event packet of its own behind the kernel (such a
+// packet holds the queue about 5 us before the next dispatch).
+int launch_one(const void *kernel, dim3 grid, dim3 block, size_t lds, const BatchArgs &a,
+               void *stream, void *done)
+{
+    void *args[] = {(void *)&a};
+    return (int)hipExtLaunchKernel(kernel, grid, block, args, lds, (hipStream_t)stream, nullptr,
+                                   (hipEvent_t)done, 0);
+}
+
 }  // namespace
 
 int launch_table_copy(const void *src, void *dst, size_t bytes, void *stream)
@@ -759,39 +772,26 @@ int launch_table_copy(const void *src, void *dst, size_t bytes, void *stream)
     return (int)hipGetLastError();
 }
 
-int launch_rgb_direct(const BatchArgs &a, int out_type, void *stream)
+int launch_rgb_direct(const BatchArgs &a, int out_type, void *stream, void *done)
 {
-    hipStream_t s = (hipStream_t)stream;
-    const dim3 grid = direct_grid(a), block = direct_block(a);
-    if (out_type == 2)
-        hipLaunchKernelGGL(rgb_direct_kernel<2>, grid, block, 0, s, a);
-    else if (out_type == 1)
-        hipLaunchKernelGGL(rgb_direct_kernel<1>, grid, block, 0, s, a);
-    else
-        hipLaunchKernelGGL(rgb_direct_kernel<0>, grid, block, 0, s, a);
-    return (int)hipGetLastError();
+    const void *k = out_type == 2   ? (const void *)rgb_direct_kernel<2>
+                    : out_type == 1 ? (const void *)rgb_direct_kernel<1>
+                                    : (const void *)rgb_direct_kernel<0>;
+    return launch_one(k, direct_grid(a), direct_block(a), 0, a, stream, done);
 }
 
-int launch_rgb_lds(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream)
+int launch_rgb_lds(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream,
+                   void *done)
 {
-    hipStream_t s = (hipStream_t)stream;
-    const dim3 grid((unsigned)a.grid), block(kThreads);
-    if (out_f16)
-        hipLaunchKernelGGL(rgb_lds_kernel<1>, grid, block, lds_bytes, s, a);
-    else
-        hipLaunchKernelGGL(rgb_lds_kernel<0>, grid, block, lds_bytes, s, a);
-    return (int)hipGetLastError();
+    const void *k = out_f16 ? (const void *)rgb_lds_kernel<1> : (const void *)rgb_lds_kernel<0>;
+    return launch_one(k, dim3((unsigned)a.grid), dim3(kThreads), lds_bytes, a, stream, done);
 }
 
-int launch_rgb_gather(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream)
+int launch_rgb_gather(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream,
+                   void *done)
 {
-    hipStream_t s = (hipStream_t)stream;
-    const dim3 grid((unsigned)a.grid), block(kThreads);
-    if (out_f16)
-        hipLaunchKernelGGL(rgb_gather_kernel<1>, grid, block, lds_bytes, s, a);
-    else
-        hipLaunchKernelGGL(rgb_gather_kernel<0>, grid, block, lds_bytes, s, a);
-    return (int)hipGetLastError();
+    const void *k = out_f16 ? (const void *)rgb_gather_kernel<1> : (const void *)rgb_gather_kernel<0>;
+    return launch_one(k, dim3((unsigned)a.grid), dim3(kThreads), lds_bytes, a, stream, done);
 }
 
 // f16: the output type, 0 fp32, 1 fp16, 2 uint8 (contiguous ranges only)
@@ -806,12 +806,10 @@ const void *rows_kernel(const BatchArgs &a, int f16)
                : (a.interleave ? rows_rgb_f32_stride(a) : rows_rgb_f32_range(a));
 }
 
-int launch_rgb_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream)
+int launch_rgb_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream, void *done)
 {
-    hipStream_t s = (hipStream_t)stream;
-    const dim3 grid((unsigned)(a.grid / a.wpg)), block(64 * a.wpg);
-    void *args[] = {(void *)&a};
-    return (int)hipLaunchKernel(rows_kernel(a, out_f16), grid, block, args, lds_bytes * a.wpg, s);
+    return launch_one(rows_kernel(a, out_f16), dim3((unsigned)(a.grid / a.wpg)), dim3(64 * a.wpg),
+                      lds_bytes * a.wpg, a, stream, done);
 }
 
 // Resident workgroups per compute unit of a kernel at a block size and LDS
@@ -859,17 +857,12 @@ int occupancy_rgb_lds(int out_f16, size_t lds_bytes, int *blocks_per_cu)
                      kThreads, lds_bytes, blocks_per_cu);
 }
 
-int launch_yuv_direct(const BatchArgs &a, int out_type, void *stream)
+int launch_yuv_direct(const BatchArgs &a, int out_type, void *stream, void *done)
 {
-    hipStream_t s = (hipStream_t)stream;
-    const dim3 grid = direct_grid(a), block = direct_block(a);
-    if (out_type == 2)
-        hipLaunchKernelGGL(yuv_direct_kernel<2>, grid, block, 0, s, a);
-    else if (out_type == 1)
-        hipLaunchKernelGGL(yuv_direct_kernel<1>, grid, block, 0, s, a);
-    else
-        hipLaunchKernelGGL(yuv_direct_kernel<0>, grid, block, 0, s, a);
-    return (int)hipGetLastError();
+    const void *k = out_type == 2   ? (const void *)yuv_direct_kernel<2>
+                    : out_type == 1 ? (const void *)yuv_direct_kernel<1>
+                                    : (const void *)yuv_direct_kernel<0>;
+    return launch_one(k, direct_grid(a), direct_block(a), 0, a, stream, done);
 }
 
 const void *yuv_rows_kernel_for(const BatchArgs &a, int f16)
@@ -879,12 +872,10 @@ const void *yuv_rows_kernel_for(const BatchArgs &a, int f16)
     return a.interleave ? rows_yuv_stride(a, f16) : rows_yuv_range(a, f16);
 }
 
-int launch_yuv_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream)
+int launch_yuv_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream, void *done)
 {
-    hipStream_t s = (hipStream_t)stream;
-    const dim3 grid((unsigned)(a.grid / a.wpg)), block(64 * a.wpg);
-    void *args[] = {(void *)&a};
-    return (int)hipLaunchKernel(yuv_rows_kernel_for(a, out_f16), grid, block, args, lds_bytes * a.wpg, s);
+    return launch_one(yuv_rows_kernel_for(a, out_f16), dim3((unsigned)(a.grid / a.wpg)),
+                      dim3(64 * a.wpg), lds_bytes * a.wpg, a, stream, done);
 }
 
 int occupancy_yuv_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, int *blocks_per_cu)

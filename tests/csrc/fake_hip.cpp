@@ -223,10 +223,11 @@ long fake_hip_pending(void) { return g_pending.load(); }
 
 namespace smol {
 namespace {
-int task(void *stream)
+int task(void *stream, void *done = nullptr)
 {
     fake_hip_enqueue_task((hipStream_t)stream, kernel_us());
-    return hipSuccess;
+    // the completion event of the launch: recorded right behind the task
+    return done ? hipEventRecord((hipEvent_t)done, (hipStream_t)stream) : hipSuccess;
 }
 uint8_t g_scratch[kNoallocTableBytes];
 }  // namespace
@@ -241,10 +242,10 @@ int launch_table_copy(const void *src, void *dst, size_t bytes, void *s)
 {
     return hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, (hipStream_t)s);
 }
-int launch_rgb_direct(const BatchArgs &, int, void *s) { return task(s); }
-int launch_rgb_lds(const BatchArgs &, int, size_t, void *s) { return task(s); }
-int launch_rgb_gather(const BatchArgs &, int, size_t, void *s) { return task(s); }
-int launch_rgb_rows(const BatchArgs &, int, size_t, void *s) { return task(s); }
+int launch_rgb_direct(const BatchArgs &, int, void *s, void *d) { return task(s, d); }
+int launch_rgb_lds(const BatchArgs &, int, size_t, void *s, void *d) { return task(s, d); }
+int launch_rgb_gather(const BatchArgs &, int, size_t, void *s, void *d) { return task(s, d); }
+int launch_rgb_rows(const BatchArgs &, int, size_t, void *s, void *d) { return task(s, d); }
 int occupancy_rgb_rows(const BatchArgs &, int, size_t, int *b)
 {
     *b = 2;
@@ -260,8 +261,8 @@ int occupancy_rgb_lds(int, size_t, int *b)
     *b = 2;
     return hipSuccess;
 }
-int launch_yuv_direct(const BatchArgs &, int, void *s) { return task(s); }
-int launch_yuv_rows(const BatchArgs &, int, size_t, void *s) { return task(s); }
+int launch_yuv_direct(const BatchArgs &, int, void *s, void *d) { return task(s, d); }
+int launch_yuv_rows(const BatchArgs &, int, size_t, void *s, void *d) { return task(s, d); }
 int occupancy_yuv_rows(const BatchArgs &, int, size_t, int *b)
 {
     *b = 2;

@@ -28,14 +28,14 @@ namespace smol {
 int launch_jpeg_idct(const JpegArgs &, int, void *) { return hipErrorNoDevice; }
 int scratch_table(int, void **) { return hipErrorNoDevice; }
 int launch_table_copy(const void *, void *, size_t, void *) { return hipErrorNoDevice; }
-int launch_rgb_direct(const BatchArgs &, int, void *) { return hipErrorNoDevice; }
-int launch_rgb_lds(const BatchArgs &, int, size_t, void *) { return hipErrorNoDevice; }
-int launch_rgb_gather(const BatchArgs &, int, size_t, void *) { return hipErrorNoDevice; }
-int launch_rgb_rows(const BatchArgs &, int, size_t, void *) { return hipErrorNoDevice; }
+int launch_rgb_direct(const BatchArgs &, int, void *, void *) { return hipErrorNoDevice; }
+int launch_rgb_lds(const BatchArgs &, int, size_t, void *, void *) { return hipErrorNoDevice; }
+int launch_rgb_gather(const BatchArgs &, int, size_t, void *, void *) { return hipErrorNoDevice; }
+int launch_rgb_rows(const BatchArgs &, int, size_t, void *, void *) { return hipErrorNoDevice; }
 int occupancy_rgb_rows(const BatchArgs &, int, size_t, int *) { return hipErrorNoDevice; }
 int occupancy_rgb_gather(int, size_t, int *) { return hipErrorNoDevice; }
 int occupancy_rgb_lds(int, size_t, int *) { return hipErrorNoDevice; }
-int launch_yuv_direct(const BatchArgs &, int, void *) { return hipErrorNoDevice; }
-int launch_yuv_rows(const BatchArgs &, int, size_t, void *) { return hipErrorNoDevice; }
+int launch_yuv_direct(const BatchArgs &, int, void *, void *) { return hipErrorNoDevice; }
+int launch_yuv_rows(const BatchArgs &, int, size_t, void *, void *) { return hipErrorNoDevice; }
 int occupancy_yuv_rows(const BatchArgs &, int, size_t, int *) { return hipErrorNoDevice; }
 }  // namespace smol

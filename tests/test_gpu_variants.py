@@ -213,3 +213,33 @@ def test_back_to_back_ragged_calls_reuse_the_ring(upload):
                           f"call {k} upload={upload}")
     finally:
         smol.reset_tuning()
+
+
+@pytest.mark.parametrize("upload", [0, 1, 2])
+def test_ring_waits_for_kernels_held_behind_a_busy_stream(upload):
+    """The staging ring's reuse wait on kernels that have not started: a
+    bounded spin kernel holds the stream while 40 ragged calls are enqueued
+    (the ring has 16 slots, so the 17th call must wait for the 1st kernel's
+    completion event before it rewrites that slot); every output matches the
+    oracle."""
+    import torch
+    smol.set_tuning(upload=upload)
+    try:
+        wls = [synthetic.c6(n=8 + (k % 5)) for k in range(4)]
+        refs = [run_oracle(wl) for wl in wls]
+        srcs = [torch.from_numpy(wl.src).to("cuda:0") for wl in wls]
+        torch.cuda.synchronize()
+        held = torch.cuda.Event()
+        torch.cuda._sleep(200_000_000)
+        held.record()
+        outs = [smol.run_workload(wls[k % 4], srcs[k % 4]) for k in range(16)]
+        # the ring is full and the stream still held: the calls below reuse
+        # slots whose kernels have not run yet
+        assert not held.query(), "the spin kernel ended before the ring filled"
+        outs += [smol.run_workload(wls[k % 4], srcs[k % 4]) for k in range(16, 40)]
+        torch.cuda.synchronize()
+        for k, out in enumerate(outs):
+            assert_parity(out.cpu().numpy(), refs[k % 4], wls[k % 4].out_dtype,
+                          f"call {k} upload={upload}")
+    finally:
+        smol.reset_tuning()
