@@ -527,6 +527,14 @@ int run_batch(const std::vector<Desc> &descs, size_t first, size_t count, int no
             else
                 a.wpg = 1;
             pl.grid = (int)w;
+            // the rows each wave walks, and the strided walk's step
+            const long long q = items / w;
+            if (q >= INT32_MAX)
+                return fail(SMOL_ERR_UNSUPPORTED, "%lld output rows for %lld waves", items, w);
+            a.rows_q = (int)q;
+            a.rows_r = (int)(items - q * w);
+            a.step_di = (int)(w / a.Ch);
+            a.step_dr = (int)(w % a.Ch);
         } else {
             if (forced > 0)
                 per_cu = std::min(per_cu, forced);

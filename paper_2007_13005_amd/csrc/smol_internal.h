@@ -53,6 +53,11 @@ struct BatchArgs {
     int32_t interleave;  // row streaming: wave q takes rows q, q + G, ... (else a range)
     int32_t exact;       // 1: operation-by-operation fp32 arithmetic (row-streaming kernel)
     int32_t wpg;         // row streaming: waves per workgroup (grid = waves / wpg)
+    // Row streaming, from the host: the n * Ch rows are rows_q * grid + rows_r
+    // (wave w walks rows_q rows, one more when w < rows_r), and a strided walk
+    // steps by grid rows = step_di images and step_dr rows.
+    int32_t rows_q, rows_r;
+    int32_t step_di, step_dr;
     int32_t nhwc;        // 1: output n x Ch x Cw x 3 (row-streaming and direct kernels)
     int32_t siting;      // I420 chroma columns: 0 centred (x/2 - 1/4), 1 co-sited (x/2)
     float mean[3];   // per channel, 0..255 units

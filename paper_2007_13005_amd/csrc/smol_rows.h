@@ -6,6 +6,8 @@
 // in parallel.
 #pragma once
 
+#include <limits.h>
+
 #include "smol_device.h"
 
 namespace smol {
@@ -206,22 +208,33 @@ struct RowStep {
 };
 
 template <int STRIDE>
-__device__ __forceinline__ RowStep row_step_of(int waves, int Ch)
+__device__ __forceinline__ RowStep row_step_of(const BatchArgs &a)
 {
-    return STRIDE ? RowStep{waves / Ch, waves % Ch, Ch} : RowStep{0, 1, Ch};
+    return STRIDE ? RowStep{a.step_di, a.step_dr, a.Ch} : RowStep{0, 1, a.Ch};
 }
 
-// First row and row count of wave `w` (of `waves`) over T rows.
+// First row and row count of wave `w`: the host splits the n * Ch rows as
+// rows_q * grid + rows_r, so every wave walks rows_q rows and waves
+// w < rows_r one more. STRIDE = 1: wave w starts at row w; STRIDE = 0: at the
+// end of the ranges of waves 0 .. w - 1.
 template <int STRIDE>
-__device__ __forceinline__ void wave_rows(long long T, int w, int waves, long long &r0,
-                                          int &n_rows)
+__device__ __forceinline__ void wave_rows(const BatchArgs &a, int w, long long &r0, int &n_rows)
+{
+    n_rows = a.rows_q + (w < a.rows_r ? 1 : 0);
+    r0 = STRIDE ? (long long)w : (long long)w * a.rows_q + min(w, a.rows_r);
+}
+
+// Image and crop row of batch row r (r < 2^31 in a strided walk, where it is
+// a wave index).
+template <int STRIDE>
+__device__ __forceinline__ void split_row(long long r, int Ch, int &img, int &rr)
 {
     if (STRIDE) {
-        r0 = w;
-        n_rows = w < T ? (int)((T - w + waves - 1) / waves) : 0;
+        img = (int)((unsigned)r / (unsigned)Ch);
+        rr = (int)r - img * Ch;
     } else {
-        r0 = T * w / waves;
-        n_rows = (int)(T * (w + 1) / waves - r0);
+        img = (int)(r / Ch);
+        rr = (int)(r - (long long)img * Ch);
     }
 }
 
@@ -233,29 +246,35 @@ __device__ __forceinline__ int xcd_position(int g, int G)
     return G % 8 == 0 ? (g % 8) * (G / 8) + g / 8 : g;
 }
 
-// A workgroup holds blockDim.x / 64 independent waves (no barriers), each
-// with its own LDS slot of `slot_bytes`; several waves per workgroup cut the
-// cost of dispatching the grid. Returns the wave's slot and sets its lane,
-// the number of waves and the wave's rows.
+// A workgroup holds a.wpg independent waves (no barriers), each with its own
+// LDS slot of `slot_bytes`; several waves per workgroup cut the cost of
+// dispatching the grid. Returns the wave's slot and sets its lane and rows.
+// (The wave count comes from the arguments: blockDim would be a memory read
+// that every wave waits for before its first address is known.)
 template <int STRIDE>
-__device__ __forceinline__ uint8_t *rows_wave(uint8_t *lds_all, int slot_bytes, long long T,
-                                              int &lane, int &nw, long long &r0, int &n_rows)
+__device__ __forceinline__ uint8_t *rows_wave(uint8_t *lds_all, int slot_bytes, const BatchArgs &a,
+                                              int &lane, long long &r0, int &n_rows)
 {
-    const int wpg = (int)(blockDim.x >> 6);
+    const int wpg = a.wpg;
     const int wid = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
     lane = (int)(threadIdx.x & 63);
-    const int ng = (int)gridDim.x;
-    nw = ng * wpg;
-    const int g = STRIDE ? xcd_position((int)blockIdx.x, ng) : (int)blockIdx.x;
-    wave_rows<STRIDE>(T, g * wpg + wid, nw, r0, n_rows);
+    const int g = STRIDE ? xcd_position((int)blockIdx.x, (int)gridDim.x) : (int)blockIdx.x;
+    wave_rows<STRIDE>(a, g * wpg + wid, r0, n_rows);
     return lds_all + wid * slot_bytes;
 }
 
+// floor(n / d) and n - d floor(n / d) for d > 0: one truncating division (a
+// 32-bit one when n fits), then the correction for negative n.
 __device__ __forceinline__ void floor_divmod(long long n, int d, int &q, int &r)
 {
-    const long long qq = n >= 0 ? n / d : -((-n + d - 1) / d);
+    long long qq = (n >= INT_MIN && n <= INT_MAX) ? (long long)((int)n / d) : n / d;
+    long long rr = n - qq * d;
+    if (rr < 0) {
+        --qq;
+        rr += d;
+    }
     q = (int)qq;
-    r = (int)(n - qq * d);
+    r = (int)rr;
 }
 
 // Vertical half-pixel taps along a walk over rows of one geometry:

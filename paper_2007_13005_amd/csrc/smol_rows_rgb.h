@@ -14,19 +14,43 @@ __global__ void __launch_bounds__(64 * kRowsMaxWavesPerGroup) rgb_rows_kernel(Ba
 {
     constexpr int NHWC = FORM & kFormNhwc, ODD = (FORM & kFormOdd) ? 1 : 0;
     extern __shared__ __attribute__((aligned(16))) uint8_t lds_all[];
-    int lane, nw;
+    int lane;
     long long r0;
     int n_rows;
     const int Ch = a.Ch;
-    uint8_t *const lds = rows_wave<STRIDE>(lds_all, 2048 * G, (long long)a.n * Ch, lane, nw, r0,
-                                           n_rows);
+    uint8_t *const lds = rows_wave<STRIDE>(lds_all, 2048 * G, a, lane, r0, n_rows);
     if (n_rows <= 0)
         return;
-    const RowStep step = row_step_of<STRIDE>(nw, Ch);
+    const RowStep step = row_step_of<STRIDE>(a);
     constexpr int kEsz = F16 == 2 ? 1 : F16 ? 2 : 4;
-    int c_img = (int)(r0 / Ch), c_rr = (int)(r0 - (long long)c_img * Ch);  // row to interpolate
-    RowCursor lc;                                                          // next row to load
+    int c_img, c_rr;  // row to interpolate
+    split_row<STRIDE>(r0, Ch, c_img, c_rr);
+    RowCursor lc;  // next row to load
     cursor_image<STRIDE>(lc, a, c_img, c_rr, step);
+
+    // The load cursor stops at the wave's last row: past the end the loads
+    // repeat that row (fetching one chunk), so every step issues the same
+    // loads and the compiler can count exactly what is outstanding when a
+    // row is written to LDS.
+    int lrow = 0;
+    bool at_end = false;  // the cursor sits on the wave's last row, already loaded
+    auto advance = [&]() {
+        if (lrow + 1 < n_rows) {
+            cursor_next<STRIDE>(lc, a, step);
+            ++lrow;
+        } else {
+            at_end = true;
+        }
+    };
+    // The first row (two with P = 2) is requested before the column taps
+    // and the rest of the set-up are computed.
+    StagedRows<G> A, B, C;
+    load_rows<G, STRIDE>(A, lc, lane, false);
+    advance();
+    if (P == 2) {
+        load_rows<G, STRIDE>(B, lc, lane, at_end);
+        advance();
+    }
 
     // Output row pointer of the row to interpolate: a step adds 3 Ch di + dr
     // rows, plus 2 Ch (planes 1 and 2 of the image left) when it wraps.
@@ -49,20 +73,6 @@ __global__ void __launch_bounds__(64 * kRowsMaxWavesPerGroup) rgb_rows_kernel(Ba
     const NormK nk = norm_consts(a);
     const uint32_t lds0 = lds_addr(lds);
 
-    // The load cursor stops at the wave's last row: past the end the loads
-    // repeat that row (fetching one chunk), so every step issues the same
-    // loads and the compiler can count exactly what is outstanding when a
-    // row is written to LDS.
-    int lrow = 0;
-    bool at_end = false;  // the cursor sits on the wave's last row, already loaded
-    auto advance = [&]() {
-        if (lrow + 1 < n_rows) {
-            cursor_next<STRIDE>(lc, a, step);
-            ++lrow;
-        } else {
-            at_end = true;
-        }
-    };
     // P = 2: a step loads row k + 2 into FUT, interpolates row k (staged in
     // LDS), writes row k + 1 (in NXT) into the slot; the three register sets
     // rotate over three steps without copies. P = 1: one register set, loaded
@@ -70,13 +80,6 @@ __global__ void __launch_bounds__(64 * kRowsMaxWavesPerGroup) rgb_rows_kernel(Ba
     // steps that stage a next row and leaves only at its end, with nothing
     // outstanding but the prefetched row; the last row is interpolated after
     // it.
-    StagedRows<G> A, B, C;
-    load_rows<G, STRIDE>(A, lc, lane, false);
-    advance();
-    if (P == 2) {
-        load_rows<G, STRIDE>(B, lc, lane, at_end);
-        advance();
-    }
     write_rows<G>(lds, A, lane);
     int csh0 = A.sh0, csh1 = A.sh1, cy0 = A.y0, cy1 = A.y1;
     float cwy = A.wy;

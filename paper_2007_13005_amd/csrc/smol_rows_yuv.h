@@ -362,19 +362,35 @@ yuv_rows_kernel(BatchArgs a)
 {
     constexpr int NHWC = FORM & kFormNhwc, ODD = (FORM & kFormOdd) ? 1 : 0;
     extern __shared__ __attribute__((aligned(16))) uint8_t lds_all[];
-    int lane, nw;
+    int lane;
     long long r0;
     int n_rows;
     const int Ch = a.Ch;
-    uint8_t *const lds = rows_wave<STRIDE>(lds_all, yuv_seg<GL>(8), (long long)a.n * Ch, lane,
-                                           nw, r0, n_rows);
+    uint8_t *const lds = rows_wave<STRIDE>(lds_all, yuv_seg<GL>(8), a, lane, r0, n_rows);
     if (n_rows <= 0)
         return;
-    const RowStep step = row_step_of<STRIDE>(nw, Ch);
+    const RowStep step = row_step_of<STRIDE>(a);
     constexpr int kEsz = F16 == 2 ? 1 : F16 ? 2 : 4;
-    int c_img = (int)(r0 / Ch), c_rr = (int)(r0 - (long long)c_img * Ch);  // row to interpolate
-    YuvCursor lc;                                                          // next row to load
+    int c_img, c_rr;  // row to interpolate
+    split_row<STRIDE>(r0, Ch, c_img, c_rr);
+    YuvCursor lc;  // next row to load
     yuv_cursor_image<STRIDE>(lc, a, c_img, c_rr, step);
+
+    // One register set: row k + 1 is loaded before row k is interpolated.
+    // The loop runs the n_rows - 1 steps that stage a next row and leaves
+    // only at its end; the last row is interpolated after it. The first row
+    // is requested before the column taps and the rest of the set-up are
+    // computed.
+    int lrow = 0;
+    auto advance = [&]() {
+        if (lrow + 1 < n_rows) {
+            yuv_cursor_next<STRIDE>(lc, a, step);
+            ++lrow;
+        }
+    };
+    YuvStaged<GL> R;
+    yuv_load<GL>(R, lc, lane, false);
+    advance();
     // bytes between an image's output rows: Cw elements per plane (NCHW) or
     // 3 Cw (NHWC); a wrap to the next image skips the rest of the image.
     const long long rb = (long long)a.Cw * kEsz, rowb = NHWC ? 3 * rb : rb;
@@ -394,21 +410,8 @@ yuv_rows_kernel(BatchArgs a)
     const NormK nk = norm_consts(a);
     const uint32_t lds0 = lds_addr(lds);
 
-    // One register set: row k + 1 is loaded before row k is interpolated.
-    // The loop runs the n_rows - 1 steps that stage a next row and leaves
-    // only at its end; the last row is interpolated after it.
-    int lrow = 0;
-    auto advance = [&]() {
-        if (lrow + 1 < n_rows) {
-            yuv_cursor_next<STRIDE>(lc, a, step);
-            ++lrow;
-        }
-    };
     const long long plane = (long long)Ch * a.Cw * kEsz;
     RowOut<F16, J> out;
-    YuvStaged<GL> R;
-    yuv_load<GL>(R, lc, lane, false);
-    advance();
     yuv_write<GL>(lds, R, lane);
     int csh[8];
 #pragma unroll
