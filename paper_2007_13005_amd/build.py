@@ -5,6 +5,7 @@ Usage: python -m paper_2007_13005_amd.build [-v]
 from __future__ import annotations
 
 import os
+import re
 import shutil
 import subprocess
 import sys
@@ -77,8 +78,27 @@ def _jobs() -> int:
 
 
 def _noise_free(stderr: str) -> str:
-    noise = "is not a recognized feature for this target"
-    return "\n".join(line for line in stderr.splitlines() if noise not in line)
+    noise = ("is not a recognized feature for this target", "kernel-resource-usage")
+    return "\n".join(line for line in stderr.splitlines() if not any(n in line for n in noise))
+
+
+# Device code is compiled with the compiler's per-kernel resource remarks; a
+# kernel that spills to or keeps a struct in private memory (scratch) fails the
+# build: every access would be a memory round trip on the hot path.
+RESOURCE_REMARKS = "-Rpass-analysis=kernel-resource-usage"
+
+
+def _scratch_users(stderr: str) -> list:
+    users, name = [], None
+    for line in stderr.splitlines():
+        m = re.search(r"Function Name: (\S+)", line)
+        if m:
+            name = m.group(1)
+            continue
+        m = re.search(r"ScratchSize \[bytes/lane\]: (\d+)", line)
+        if m and int(m.group(1)) > 0:
+            users.append(f"{name}: {m.group(1)} bytes/lane")
+    return users
 
 
 def build(verbose: bool = False) -> str:
@@ -88,8 +108,9 @@ def build(verbose: bool = False) -> str:
         cmds = []
         for src in SOURCES:
             obj = os.path.join(objdir, os.path.splitext(src)[0] + ".o")
-            cmds.append((obj, [cc, *HIPCC_FLAGS, "-I", INCLUDE, "-I", CSRC, "-c", "-o", obj,
-                               os.path.join(CSRC, src)]))
+            remarks = [RESOURCE_REMARKS] if src.endswith(".hip") else []
+            cmds.append((obj, [cc, *HIPCC_FLAGS, *remarks, "-I", INCLUDE, "-I", CSRC, "-c", "-o",
+                               obj, os.path.join(CSRC, src)]))
         pending = list(cmds)
         running = []
         errors = []
@@ -102,9 +123,12 @@ def build(verbose: bool = False) -> str:
                                                       stderr=subprocess.PIPE, text=True)))
             cmd, proc = running.pop(0)
             _, err = proc.communicate()
+            scratch = _scratch_users(err)
             err = _noise_free(err)
             if proc.returncode != 0:
                 errors.append(f"{cmd[-1]} ({proc.returncode}):\n{err}")
+            elif scratch:
+                errors.append(f"{cmd[-1]}: kernels using scratch memory:\n" + "\n".join(scratch))
             elif verbose and err.strip():
                 print(err, file=sys.stderr)
         if errors:

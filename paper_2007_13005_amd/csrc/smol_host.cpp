@@ -535,6 +535,27 @@ int run_batch(const std::vector<Desc> &descs, size_t first, size_t count, int no
             a.rows_r = (int)(items - q * w);
             a.step_di = (int)(w / a.Ch);
             a.step_dr = (int)(w % a.Ch);
+            if (uniform) {
+                // |quotients| <= H + 1: |step_dr - Ch| <= Ch <= Hr
+                const Desc &d = descs[first];
+                const int64_t den = 2 * (int64_t)d.Hr;
+                const int64_t nums[2] = {2 * (int64_t)d.H * a.step_dr,
+                                         2 * (int64_t)d.H * (a.step_dr - a.Ch)};
+                int32_t qr[4];
+                for (int k = 0; k < 2; ++k) {
+                    int64_t q = nums[k] / den, r = nums[k] - q * den;
+                    if (r < 0) {
+                        --q;
+                        r += den;
+                    }
+                    qr[2 * k] = (int32_t)q;
+                    qr[2 * k + 1] = (int32_t)r;
+                }
+                a.vq_s = qr[0];
+                a.vr_s = qr[1];
+                a.vq_w = qr[2];
+                a.vr_w = qr[3];
+            }
         } else {
             if (forced > 0)
                 per_cu = std::min(per_cu, forced);

@@ -58,6 +58,10 @@ struct BatchArgs {
     // steps by grid rows = step_di images and step_dr rows.
     int32_t rows_q, rows_r;
     int32_t step_di, step_dr;
+    // Strided walk of a uniform batch: floor quotient and remainder of
+    // 2 H step_dr and of 2 H (step_dr - Ch) by 2 Hr (the vertical map's
+    // steps within an image and across a wrap), from the host.
+    int32_t vq_s, vr_s, vq_w, vr_w;
     int32_t nhwc;        // 1: output n x Ch x Cw x 3 (row-streaming and direct kernels)
     int32_t siting;      // I420 chroma columns: 0 centred (x/2 - 1/4), 1 co-sited (x/2)
     float mean[3];   // per channel, 0..255 units

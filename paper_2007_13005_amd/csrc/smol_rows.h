@@ -290,18 +290,29 @@ struct VCursor {
 };
 
 template <int STRIDE>
-__device__ __forceinline__ void vcursor_init(VCursor &v, const RowImg &g, int rr, const RowStep &s)
+__device__ __forceinline__ void vcursor_init(VCursor &v, const BatchArgs &a, const RowImg &g, int rr,
+                                             const RowStep &s)
 {
-    v.H = g.H;
-    v.den = 2 * g.Hr;
-    floor_divmod((long long)(2 * (g.top + rr) + 1) * g.H - g.Hr, v.den, v.q, v.rem);
-    if (STRIDE) {
-        floor_divmod(2LL * g.H * s.dr, v.den, v.qs, v.rs);
-        floor_divmod(2LL * g.H * (s.dr - s.Ch), v.den, v.qw, v.rw);
+    const int den = 2 * g.Hr;
+    int q, rem, qs, rs, qw = 0, rw = 0;
+    floor_divmod((long long)(2 * (g.top + rr) + 1) * g.H - g.Hr, den, q, rem);
+    if (STRIDE && !a.table) {
+        // one geometry for the whole launch: the host computed the steps
+        qs = a.vq_s;
+        rs = a.vr_s;
+        qw = a.vq_w;
+        rw = a.vr_w;
+    } else if (STRIDE) {
+        // a walk over a table reads the next image's descriptor on a wrap
+        floor_divmod(2LL * g.H * s.dr, den, qs, rs);
     } else {
-        v.qs = (2 * g.H) / v.den;
-        v.rs = 2 * g.H - v.qs * v.den;
+        qs = (2 * g.H) / den;
+        rs = 2 * g.H - qs * den;
     }
+    // (every field stored on every path: stores that differ by branch can be
+    // merged into one store to a chosen field, which keeps the cursor in
+    // memory)
+    v = VCursor{q, rem, den, g.H, qs, rs, qw, rw};
 }
 
 __device__ __forceinline__ void vcursor_add(VCursor &v, int dq, int dr)
@@ -344,7 +355,7 @@ __device__ __forceinline__ void cursor_image(RowCursor &c, const BatchArgs &a, i
     const RowImg g = row_img(a, img);
     c.img = img;
     c.rr = rr;
-    vcursor_init<STRIDE>(c.v, g, rr, s);
+    vcursor_init<STRIDE>(c.v, a, g, rr, s);
     c.base = (uintptr_t)(a.src + g.off) + 3 * (uintptr_t)g.xf;
     c.pitch = g.pitch;
     c.span = g.span;
@@ -644,13 +655,15 @@ __device__ __forceinline__ void store_row(uint8_t *orow, long long plane, int Cw
                     __builtin_nontemporal_store((w1 >> 16) | (w2 & 0xffff0000u),
                                                 (uint32_t *)dst + 2);
                 } else {
-                    typedef uint32_t u32x2v __attribute__((ext_vector_type(2)));
-                    const u32x2v q0 = {out.w[j][0][0], out.w[j][1][0]};
-                    const u32x2v q1 = {out.w[j][2][0], out.w[j][0][F16 ? 0 : 1]};
-                    const u32x2v q2 = {out.w[j][1][F16 ? 0 : 1], out.w[j][2][F16 ? 0 : 1]};
-                    __builtin_nontemporal_store(q0, (u32x2v *)dst);
-                    __builtin_nontemporal_store(q1, (u32x2v *)dst + 1);
-                    __builtin_nontemporal_store(q2, (u32x2v *)dst + 2);
+                    // pixel c: r g b, pixel c + 1: r g b, as three 8-byte
+                    // words (built from scalars: a vector gathered from the
+                    // array's elements would keep the array in memory)
+                    const uint64_t r0 = out.w[j][0][0], g0 = out.w[j][1][0], b0 = out.w[j][2][0];
+                    const uint64_t r1 = out.w[j][0][F16 ? 0 : 1], g1 = out.w[j][1][F16 ? 0 : 1],
+                                   b1 = out.w[j][2][F16 ? 0 : 1];
+                    __builtin_nontemporal_store(r0 | (g0 << 32), (uint64_t *)dst);
+                    __builtin_nontemporal_store(b0 | (r1 << 32), (uint64_t *)dst + 1);
+                    __builtin_nontemporal_store(g1 | (b1 << 32), (uint64_t *)dst + 2);
                 }
             } else {
                 // odd Cw: element by element, pixel c + 1 is the last

@@ -19,8 +19,9 @@ __global__ void __launch_bounds__(64 * kRowsMaxWavesPerGroup) rgb_rows_kernel(Ba
     int n_rows;
     const int Ch = a.Ch;
     uint8_t *const lds = rows_wave<STRIDE>(lds_all, 2048 * G, a, lane, r0, n_rows);
-    if (n_rows <= 0)
-        return;
+    // The host launches at most one wave per row, so every wave has rows (an
+    // early exit here would hold the remaining argument loads behind it).
+    __builtin_assume(n_rows > 0);
     const RowStep step = row_step_of<STRIDE>(a);
     constexpr int kEsz = F16 == 2 ? 1 : F16 ? 2 : 4;
     int c_img, c_rr;  // row to interpolate

@@ -121,7 +121,7 @@ __device__ __forceinline__ void yuv_cursor_image(YuvCursor &c, const BatchArgs &
     lg.H = g.H;
     lg.Hr = g.Hr;
     lg.top = g.top;
-    vcursor_init<STRIDE>(c.v, lg, rr, s);
+    vcursor_init<STRIDE>(c.v, a, lg, rr, s);
     c.W = g.fw;
     c.Wc = (g.fw + 1) >> 1;
     c.Hc = (g.fh + 1) >> 1;
@@ -367,8 +367,9 @@ yuv_rows_kernel(BatchArgs a)
     int n_rows;
     const int Ch = a.Ch;
     uint8_t *const lds = rows_wave<STRIDE>(lds_all, yuv_seg<GL>(8), a, lane, r0, n_rows);
-    if (n_rows <= 0)
-        return;
+    // The host launches at most one wave per row, so every wave has rows (an
+    // early exit here would hold the remaining argument loads behind it).
+    __builtin_assume(n_rows > 0);
     const RowStep step = row_step_of<STRIDE>(a);
     constexpr int kEsz = F16 == 2 ? 1 : F16 ? 2 : 4;
     int c_img, c_rr;  // row to interpolate
