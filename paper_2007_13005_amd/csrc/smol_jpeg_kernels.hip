@@ -13,7 +13,7 @@
 // b = l / 8 (16 contiguous bytes) and forms G(v, x) for all x in registers.
 // After an exchange through LDS, pass 2: lane l forms output rows y and 7 - y
 // (y = l % 4) of block b at columns 4 h .. 4 h + 3 (h = (l % 8) / 4). Then
-// + 128, rounded to nearest even, clamped.
+// + 128, clamped to [0, 255] and rounded to nearest even.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -23,10 +23,14 @@ namespace smol {
 namespace {
 
 constexpr int kBlocksPerWave = 8;
+constexpr int kBlockWords = 68;
 
 __global__ void __launch_bounds__(64) jpeg_idct_kernel(JpegArgs a)
 {
-    __shared__ __attribute__((aligned(16))) float g[kBlocksPerWave][8][8];  // [block][v][x]
+    // G(v, x) of block b at word b * kBlockWords + 8 v + x: the 4-word pad
+    // per block spreads the eight blocks' rows over the LDS banks (with 64
+    // words per block every block's row v sits in the same banks)
+    __shared__ __attribute__((aligned(16))) float g[kBlocksPerWave * kBlockWords];
     const int l = threadIdx.x;
     const int b = l >> 3, row = l & 7;  // block of the group; coefficient row v of pass 1
     const int y = row & 3, h = row >> 2;  // pass 2: output rows y, 7 - y; columns 4h .. 4h + 3
@@ -92,7 +96,10 @@ __global__ void __launch_bounds__(64) jpeg_idct_kernel(JpegArgs a)
 #pragma unroll
         for (int u = 0; u < 8; ++u)
             d[u] = (float)((int)raw[u] * (int)q[8 * row + u]);  // exact: |.| < 2^24
-        // horizontal pass for row v = row of block bb
+        // horizontal pass for row v = row of block bb: x = 0..3 and 7..4,
+        // written as two 16-byte stores
+        typedef float f32x4 __attribute__((ext_vector_type(4)));
+        f32x4 lo, hi;
 #pragma unroll
         for (int n = 0; n < 4; ++n) {
             float e = a.c[0 * 8 + n] * d[0];
@@ -103,16 +110,18 @@ __global__ void __launch_bounds__(64) jpeg_idct_kernel(JpegArgs a)
             o = o + a.c[3 * 8 + n] * d[3];
             o = o + a.c[5 * 8 + n] * d[5];
             o = o + a.c[7 * 8 + n] * d[7];
-            g[b][row][n] = e + o;
-            g[b][row][7 - n] = e - o;
+            lo[n] = e + o;
+            hi[3 - n] = e - o;
         }
+        f32x4 *grow = (f32x4 *)&g[b * kBlockWords + 8 * row];
+        grow[0] = lo;
+        grow[1] = hi;
         __syncthreads();
         // vertical pass: rows y and 7 - y of block bb at columns 4h .. 4h + 3
-        typedef float f32x4 __attribute__((ext_vector_type(4)));
         f32x4 gv[8];
 #pragma unroll
         for (int v = 0; v < 8; ++v)
-            gv[v] = *(const f32x4 *)&g[b][v][4 * h];
+            gv[v] = *(const f32x4 *)&g[b * kBlockWords + 8 * v + 4 * h];
         uint32_t top = 0, bot = 0;  // four pixels of row y, four of row 7 - y
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
@@ -124,10 +133,11 @@ __global__ void __launch_bounds__(64) jpeg_idct_kernel(JpegArgs a)
             o = o + cy[3] * gv[3][i];
             o = o + cy[5] * gv[5][i];
             o = o + cy[7] * gv[7][i];
-            const uint32_t p0 = (uint32_t)__builtin_rintf(fminf(fmaxf((e + o) + 128.0f, 0.0f), 255.0f));
-            const uint32_t p1 = (uint32_t)__builtin_rintf(fminf(fmaxf((e - o) + 128.0f, 0.0f), 255.0f));
-            top |= p0 << (8 * i);
-            bot |= p1 << (8 * i);
+            // v_cvt_pk_u8_f32: byte i = the value clamped to [0, 255] and
+            // rounded to nearest even (one instruction for clamp, round,
+            // convert and insert)
+            top = __builtin_amdgcn_cvt_pk_u8_f32((e + o) + 128.0f, (uint32_t)i, top);
+            bot = __builtin_amdgcn_cvt_pk_u8_f32((e - o) + 128.0f, (uint32_t)i, bot);
         }
         const int gx = 8 * (bx0 + b) + 4 * h;
         if (b < nb && gx < pw) {

@@ -573,10 +573,10 @@ __device__ __forceinline__ void pack_pair(RowOut<F16, J> &out, int j, const floa
 #pragma unroll
     for (int ch = 0; ch < 3; ++ch) {
         if (F16 == 2) {
-            // nearest, ties to even (v_rndne_f32), of a value in [0, 255]
-            const uint32_t b0 = (uint32_t)__builtin_rintf(clamp255(o[ch][0]));
-            const uint32_t b1 = (uint32_t)__builtin_rintf(clamp255(o[ch][1]));
-            out.w[j][ch][0] = b0 | (b1 << 8);
+            // clamped to [0, 255] and rounded to nearest even, into bytes 0
+            // and 1 (v_cvt_pk_u8_f32 does clamp, round, convert and insert)
+            out.w[j][ch][0] = __builtin_amdgcn_cvt_pk_u8_f32(
+                o[ch][1], 1u, __builtin_amdgcn_cvt_pk_u8_f32(o[ch][0], 0u, 0u));
         } else if (F16 && !EXACT) {
             // The conversion may fuse with the last product (one rounding
             // to fp16 instead of two).
