@@ -102,8 +102,17 @@ struct JpegRun {
     int32_t W, H;
     int16_t wx0, wy0, wmx, wmy;
     int16_t lbx0, lby0, lnbx, lnby, cbx0, cby0, cnbx, cnby;
-    int32_t frames, qt;
-    uint32_t jobs_end, pad;  // jobs_end < 2^31
+    // Jobs of a frame: lum = lg * lnby luma groups (lg groups of up to eight
+    // blocks per block row), then chr = cg * cnby groups of each chroma
+    // plane; a row's last group holds lrem (cg: crem) blocks.
+    uint32_t lum, chr;
+    uint32_t jobs_end;  // < 2^31
+    // Division by a divisor d of the run (jobs per frame, lg, cg) as
+    // floor(n m / 2^s) with m = ceil(2^s / d), s = 31 + ceil(log2 d): exact
+    // for every n < 2^31.
+    uint32_t m_pf, m_lg, m_cg;
+    uint32_t groups;  // lg | cg << 11 | lrem << 22 | crem << 26
+    uint32_t shifts;  // s of the frame's jobs | s of lg << 8 | s of cg << 16 | qt << 24
 };
 struct JpegArgs {
     const int16_t *coef;
@@ -113,6 +122,7 @@ struct JpegArgs {
     float c[64];                       // c[k * 8 + n] = fp32(C(k)/2 cos((2n + 1) k pi / 16))
     JpegRun run[kJpegMaxRuns];
 };
+static_assert(sizeof(JpegRun) == 112, "run table entry of block decoding");
 static_assert(sizeof(JpegArgs) <= 4096, "kernel arguments of block decoding");
 int launch_jpeg_idct(const JpegArgs &a, int grid, void *stream);
 

@@ -74,6 +74,19 @@ int64_t frame_bytes(int64_t W, int64_t H)
     return W * H + 2 * ((W + 1) / 2) * ((H + 1) / 2);
 }
 
+// m = ceil(2^s / d), s = 31 + ceil(log2 d), for 1 <= d < 2^31: then
+// floor(n / d) = floor(n m / 2^s) for every 0 <= n < 2^31 (m = (2^s + e) / d
+// with 0 <= e < d, so n m / 2^s exceeds n / d by less than 2^-ceil(log2 d)
+// <= 1 / d, which cannot reach the next integer), and m < 2^32.
+void magic_divisor(uint32_t d, uint32_t *m, uint32_t *s)
+{
+    int l = 0;
+    while (((uint64_t)1 << l) < d)
+        ++l;
+    *s = (uint32_t)(31 + l);
+    *m = (uint32_t)((((uint64_t)1 << (31 + l)) + d - 1) / d);
+}
+
 }  // namespace
 
 extern "C" {
@@ -281,12 +294,21 @@ int smol_jpeg_decode_i420(const int16_t *coef, int64_t coef_elems, const int64_t
         r.cby0 = (int16_t)g.cby0;
         r.cnbx = (int16_t)g.cnbx;
         r.cnby = (int16_t)g.cnby;
-        r.frames = e - b;
-        r.qt = qt;
+
         // jobs of the kernel: groups of up to eight blocks along block rows
         jobs += per_frame * (e - b);
         r.jobs_end = (uint32_t)jobs;
-        r.pad = 0;
+        // lg, cg <= 1025 (11 bits each); the last group of a row holds 1..8
+        const uint32_t lg = (uint32_t)((g.lnbx + 7) / 8), cg = (uint32_t)((g.cnbx + 7) / 8);
+        const uint32_t lrem = (uint32_t)g.lnbx - 8 * (lg - 1), crem = (uint32_t)g.cnbx - 8 * (cg - 1);
+        r.lum = lg * (uint32_t)g.lnby;
+        r.chr = cg * (uint32_t)g.cnby;
+        r.groups = lg | cg << 11 | lrem << 22 | crem << 26;
+        uint32_t s_pf, s_lg, s_cg;
+        magic_divisor((uint32_t)per_frame, &r.m_pf, &s_pf);
+        magic_divisor(lg, &r.m_lg, &s_lg);
+        magic_divisor(cg, &r.m_cg, &s_cg);
+        r.shifts = s_pf | s_lg << 8 | s_cg << 16 | (uint32_t)qt << 24;
         if (++a.runs == smol::kJpegMaxRuns) {
             const int rc = flush();
             if (rc != SMOL_OK)

@@ -25,6 +25,22 @@ namespace {
 constexpr int kBlocksPerWave = 8;
 constexpr int kBlockWords = 68;
 
+// The 32-bit word at a 4-byte aligned field, and its two 16-bit halves.
+__device__ __forceinline__ uint32_t word_of(const int16_t *p)
+{
+    uint32_t w;
+    __builtin_memcpy(&w, p, 4);
+    return w;
+}
+__device__ __forceinline__ int lo16(uint32_t w) { return (int)(int16_t)(w & 0xffffu); }
+__device__ __forceinline__ int hi16(uint32_t w) { return (int)(int16_t)(w >> 16); }
+
+// floor(n / d) from the run's m = ceil(2^s / d) (exact for n < 2^31)
+__device__ __forceinline__ uint32_t magic_div(uint32_t n, uint32_t m, uint32_t s)
+{
+    return (uint32_t)(((uint64_t)n * m) >> s);
+}
+
 __global__ void __launch_bounds__(64) jpeg_idct_kernel(JpegArgs a)
 {
     // G(v, x) of block b at word b * kBlockWords + 8 v + x: the 4-word pad
@@ -39,7 +55,8 @@ __global__ void __launch_bounds__(64) jpeg_idct_kernel(JpegArgs a)
     for (int k = 0; k < 8; ++k)
         cy[k] = a.c[k * 8 + y];
     // job indices stay below 2^31 (the host splits launches), so the job
-    // mapping runs in 32-bit unsigned arithmetic
+    // mapping runs in 32-bit unsigned arithmetic, its divisions by the run's
+    // divisors as multiplications (JpegRun)
     const uint32_t jobs = a.run[a.runs - 1].jobs_end;
     int ri = 0;  // run of the current job (jobs ascend within a workgroup)
     for (uint32_t job = blockIdx.x; job < jobs; job += gridDim.x) {
@@ -47,24 +64,27 @@ __global__ void __launch_bounds__(64) jpeg_idct_kernel(JpegArgs a)
             ++ri;
         const JpegRun &r = a.run[ri];
         // groups of up to eight blocks along each block row of the rectangle
-        const uint32_t lg = ((uint32_t)r.lnbx + kBlocksPerWave - 1) / kBlocksPerWave;
-        const uint32_t cg = ((uint32_t)r.cnbx + kBlocksPerWave - 1) / kBlocksPerWave;
-        const uint32_t lum = lg * (uint32_t)r.lnby, chr = cg * (uint32_t)r.cnby;
-        const uint32_t per_frame = lum + 2 * chr;
+        const uint32_t lg = r.groups & 0x7ffu, cg = (r.groups >> 11) & 0x7ffu;
+        const uint32_t lum = r.lum, chr = r.chr, per_frame = lum + 2 * chr;
         const uint32_t local = job - (ri ? a.run[ri - 1].jobs_end : 0);
-        const uint32_t f = local / per_frame;
+        const uint32_t f = magic_div(local, r.m_pf, r.shifts & 0xffu);
         uint32_t k = local - f * per_frame;
+        // the 16-bit fields in pairs, as the words that hold them (a 16-bit
+        // field read alone becomes a vector load that the wave waits for)
+        const uint32_t wxy = word_of(&r.wx0), wm = word_of(&r.wmx);
         int comp, by, bx0, nb, gw, ox, oy, pw, ph;  // (ox, oy): the stored grid's first block
         long long cbase, pbase;
         if (k < lum) {
             comp = 0;
-            by = r.lby0 + (int)(k / lg);
-            const int gi = (int)(k - (k / lg) * lg);
-            bx0 = r.lbx0 + gi * kBlocksPerWave;
-            nb = min(kBlocksPerWave, r.lnbx - gi * kBlocksPerWave);
-            gw = 2 * r.wmx;
-            ox = 2 * r.wx0;
-            oy = 2 * r.wy0;
+            const uint32_t kr = magic_div(k, r.m_lg, (r.shifts >> 8) & 0xffu);
+            const uint32_t lb = word_of(&r.lbx0);
+            by = hi16(lb) + (int)kr;
+            const uint32_t gi = k - kr * lg;
+            bx0 = lo16(lb) + (int)gi * kBlocksPerWave;
+            nb = gi + 1 == lg ? (int)((r.groups >> 22) & 0xfu) : kBlocksPerWave;
+            gw = 2 * lo16(wm);
+            ox = 2 * lo16(wxy);
+            oy = 2 * hi16(wxy);
             cbase = 0;
             pbase = 0;
             pw = r.W;
@@ -73,14 +93,16 @@ __global__ void __launch_bounds__(64) jpeg_idct_kernel(JpegArgs a)
             k -= lum;
             comp = k < chr ? 1 : 2;
             k -= comp == 1 ? 0 : chr;
-            by = r.cby0 + (int)(k / cg);
-            const int gi = (int)(k - (k / cg) * cg);
-            bx0 = r.cbx0 + gi * kBlocksPerWave;
-            nb = min(kBlocksPerWave, r.cnbx - gi * kBlocksPerWave);
-            gw = r.wmx;
-            ox = r.wx0;
-            oy = r.wy0;
-            cbase = 64LL * r.wmx * r.wmy * (comp == 1 ? 4 : 5);
+            const uint32_t kr = magic_div(k, r.m_cg, (r.shifts >> 16) & 0xffu);
+            const uint32_t cb = word_of(&r.cbx0);
+            by = hi16(cb) + (int)kr;
+            const uint32_t gi = k - kr * cg;
+            bx0 = lo16(cb) + (int)gi * kBlocksPerWave;
+            nb = gi + 1 == cg ? (int)(r.groups >> 26) : kBlocksPerWave;
+            gw = lo16(wm);
+            ox = lo16(wxy);
+            oy = hi16(wxy);
+            cbase = 64LL * lo16(wm) * hi16(wm) * (comp == 1 ? 4 : 5);
             pbase = comp == 1 ? r.cboff : r.croff;
             pw = (r.W + 1) >> 1;
             ph = (r.H + 1) >> 1;
@@ -91,7 +113,7 @@ __global__ void __launch_bounds__(64) jpeg_idct_kernel(JpegArgs a)
                              64LL * ((long long)(by - oy) * gw + bx0 + bb - ox);
         typedef short short8 __attribute__((ext_vector_type(8)));
         const short8 raw = *(const short8 *)(blk + 8 * row);
-        const uint8_t *q = a.q[r.qt][comp == 0 ? 0 : 1];
+        const uint8_t *q = a.q[r.shifts >> 24][comp == 0 ? 0 : 1];
         float d[8];
 #pragma unroll
         for (int u = 0; u < 8; ++u)
