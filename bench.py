@@ -49,6 +49,12 @@ def parse():
     ap.add_argument("--steps", type=int, default=400)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", default="c4", choices=["c1", "c2", "c3", "c4", "c5", "c6", "c7", "c8"])
+    ap.add_argument("--frames", type=int, default=0,
+                    help="images per batch instead of the configuration's (0: the "
+                         "configuration's); with --stream-probe, the probe moves that batch's "
+                         "bytes. Timing several batch sizes splits a launch's fixed cost from "
+                         "its cost per image; the line then describes that batch, not the "
+                         "configuration's")
     ap.add_argument("--rotate", type=int, default=0,
                     help="input/output sets cycled through (0: enough to defeat the MALL)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
@@ -853,7 +859,7 @@ def main() -> int:
         print("bench.py needs a HIP device", file=sys.stderr)
         return 1
     dev = torch.device("cuda:0")
-    wl = synthetic.make(args.config)
+    wl = synthetic.make(args.config, **({"n": args.frames} if args.frames > 0 else {}))
     algo = algorithmic_bytes(wl, smol)
     out_bytes = wl.n * 3 * wl.crop_h * wl.crop_w * wl.out_elem_bytes
     rotate = args.rotate or max(2, -(-2 * MALL_BYTES // algo))
