@@ -43,7 +43,8 @@ SOURCES = [
     "smol_stream.hip",
     "smol_scratch.hip",
 ]
-HEADERS = ["smol_internal.h", "smol_device.h", "smol_rows.h", "smol_rows_rgb.h", "smol_rows_yuv.h"]
+HEADERS = ["smol_internal.h", "smol_device.h", "smol_rows.h", "smol_rows_rgb.h", "smol_rows_yuv.h",
+           "smol_magic.h"]
 
 # -ffp-contract=off: the kernels round every multiply and add on their own, as
 # the definition does; fused multiply-adds are never formed implicitly.

@@ -10,6 +10,7 @@
 
 #include "smol.h"
 #include "smol_internal.h"
+#include "smol_magic.h"
 #include "smol_jpeg.h"
 
 namespace {
@@ -72,19 +73,6 @@ void mcu_window(int64_t W, int64_t H, const int32_t *rect, int64_t win[4])
 int64_t frame_bytes(int64_t W, int64_t H)
 {
     return W * H + 2 * ((W + 1) / 2) * ((H + 1) / 2);
-}
-
-// m = ceil(2^s / d), s = 31 + ceil(log2 d), for 1 <= d < 2^31: then
-// floor(n / d) = floor(n m / 2^s) for every 0 <= n < 2^31 (m = (2^s + e) / d
-// with 0 <= e < d, so n m / 2^s exceeds n / d by less than 2^-ceil(log2 d)
-// <= 1 / d, which cannot reach the next integer), and m < 2^32.
-void magic_divisor(uint32_t d, uint32_t *m, uint32_t *s)
-{
-    int l = 0;
-    while (((uint64_t)1 << l) < d)
-        ++l;
-    *s = (uint32_t)(31 + l);
-    *m = (uint32_t)((((uint64_t)1 << (31 + l)) + d - 1) / d);
 }
 
 }  // namespace
@@ -305,9 +293,9 @@ int smol_jpeg_decode_i420(const int16_t *coef, int64_t coef_elems, const int64_t
         r.chr = cg * (uint32_t)g.cnby;
         r.groups = lg | cg << 11 | lrem << 22 | crem << 26;
         uint32_t s_pf, s_lg, s_cg;
-        magic_divisor((uint32_t)per_frame, &r.m_pf, &s_pf);
-        magic_divisor(lg, &r.m_lg, &s_lg);
-        magic_divisor(cg, &r.m_cg, &s_cg);
+        smol::magic_divisor((uint32_t)per_frame, &r.m_pf, &s_pf);
+        smol::magic_divisor(lg, &r.m_lg, &s_lg);
+        smol::magic_divisor(cg, &r.m_cg, &s_cg);
         r.shifts = s_pf | s_lg << 8 | s_cg << 16 | (uint32_t)qt << 24;
         if (++a.runs == smol::kJpegMaxRuns) {
             const int rc = flush();
