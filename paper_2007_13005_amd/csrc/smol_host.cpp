@@ -527,7 +527,8 @@ int run_batch(const std::vector<Desc> &descs, size_t first, size_t count, int no
             else
                 a.wpg = 1;
             pl.grid = (int)w;
-            // the rows each wave walks, and the strided walk's step
+            // the rows each wave walks (q >= 1: w <= items, and the kernels
+            // rely on every wave having a row), and the strided walk's step
             const long long q = items / w;
             if (q >= INT32_MAX)
                 return fail(SMOL_ERR_UNSUPPORTED, "%lld output rows for %lld waves", items, w);

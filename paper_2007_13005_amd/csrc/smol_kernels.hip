@@ -780,17 +780,16 @@ int launch_rgb_direct(const BatchArgs &a, int out_type, void *stream, void *done
     return launch_one(k, direct_grid(a), direct_block(a), 0, a, stream, done);
 }
 
-int launch_rgb_lds(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream,
-                   void *done)
+int launch_rgb_lds(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream, void *done)
 {
     const void *k = out_f16 ? (const void *)rgb_lds_kernel<1> : (const void *)rgb_lds_kernel<0>;
     return launch_one(k, dim3((unsigned)a.grid), dim3(kThreads), lds_bytes, a, stream, done);
 }
 
-int launch_rgb_gather(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream,
-                   void *done)
+int launch_rgb_gather(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream, void *done)
 {
-    const void *k = out_f16 ? (const void *)rgb_gather_kernel<1> : (const void *)rgb_gather_kernel<0>;
+    const void *k =
+        out_f16 ? (const void *)rgb_gather_kernel<1> : (const void *)rgb_gather_kernel<0>;
     return launch_one(k, dim3((unsigned)a.grid), dim3(kThreads), lds_bytes, a, stream, done);
 }
 
