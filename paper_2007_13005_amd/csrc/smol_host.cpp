@@ -48,6 +48,7 @@ constexpr int kDefaultLdsBudget = 64 * 1024;
 constexpr int kMaxBandRows = 64;
 constexpr int kMaxWorkgroupsPerCu = 16;
 constexpr int kDefaultBandRows = 2;
+constexpr long long kRowsMinPerWave = 3;  // rows per wave a launch aims for (row streaming)
 constexpr int kGatherPassPixels = 2048;  // 256 threads x 4 pairs x 2 pixels
 // Row-streaming waves per compute unit for long staged rows (4 KiB chunk
 // groups): more waves would each walk fewer rows, and every wave pays its
@@ -513,14 +514,24 @@ int run_batch(const std::vector<Desc> &descs, size_t first, size_t count, int no
         if (rows) {
             // Waves per compute unit (the tuning knob counts waves here).
             int waves = per_cu * a.wpg;
-            if (forced > 0)
+            items = (long long)n * a.Ch;
+            if (forced > 0) {
                 waves = std::min(waves, forced);
-            else if (pl.path == smol::PATH_ROWS && a.row_groups >= 4)
-                waves = std::min(waves, kRowsWavesPerCu);
+            } else {
+                if (pl.path == smol::PATH_ROWS && a.row_groups >= 4)
+                    waves = std::min(waves, kRowsWavesPerCu);
+                // Small launches: at least about three rows per wave, in
+                // multiples of 4 waves per compute unit (a wave's set-up and
+                // first load cost about a row; 7,168 rows of 224 columns take
+                // 8.1 us on 5,120 waves and 6.7 us on 2,048).
+                const long long by_rows = items / kRowsMinPerWave / di.cus;
+                if (by_rows < waves)
+                    waves = (int)std::min<long long>(waves,
+                                                     std::max<long long>(4, by_rows & ~3LL));
+            }
             // Workgroups of 4 (or 2) waves when that count allows, so each
             // compute unit still holds at most `waves` of them.
             a.wpg = waves % 4 == 0 ? 4 : waves % 2 == 0 ? 2 : 1;
-            items = (long long)n * a.Ch;
             long long w = std::min<long long>(items, (long long)di.cus * waves);
             if (w >= a.wpg)
                 w -= w % a.wpg;
@@ -817,7 +828,8 @@ static int rgb_batch(const uint8_t *src, int64_t src_bytes, const int64_t *offse
             // every 16-byte chunk holding a staged byte lies inside src
             const uintptr_t base = (uintptr_t)src + (uintptr_t)off + 3 * (uintptr_t)xf;
             const uintptr_t first = (base + (uintptr_t)yf * (uintptr_t)pitch) & ~(uintptr_t)15;
-            const uintptr_t last = base + (uintptr_t)yl * (uintptr_t)pitch + 3 * (uintptr_t)(xl - xf + 1);
+            const uintptr_t last =
+                base + (uintptr_t)yl * (uintptr_t)pitch + 3 * (uintptr_t)(xl - xf + 1);
             const uintptr_t end = (last + 15) & ~(uintptr_t)15;
             d.safe = first >= (uintptr_t)src && end <= (uintptr_t)src + (uintptr_t)src_bytes;
         }
