@@ -15,8 +15,12 @@ namespace {
 // then into its LDS slot (1 KiB each): luma rows y0 and y1 over the crop's
 // luma column span and, for each chroma plane, the chroma rows that the
 // vertical chroma taps of y0 and y1 read over the matching chroma span. Those
-// are at most three rows: the first chroma row of y1 is always one of the two
-// of y0 (y1 = y0 + 1 or the clamped y0).
+// are at most three rows, staged so that y0 reads chroma rows (r0, r1) and y1
+// reads (r1, r2): the taps of consecutive luma rows (y1 = y0 + 1 or the
+// clamped y0) either move on by one chroma row (y1's first row is y0's
+// second; r2 is y1's second) or stay on y0's pair (y1's second row is y0's
+// second; r2 is then y1's first row and y1's weights are swapped, which gives
+// the same exact integer sums).
 //
 // Every luma tap is converted as defined: chroma bilinear at centred siting,
 // BT.601 full range, clamp; then the four converted taps are interpolated
@@ -84,20 +88,18 @@ __device__ __forceinline__ YuvImg yuv_img(const BatchArgs &a, int img)
 }
 
 // One output row's eight segments in registers: Y y0, Y y1, Cb r0, Cb r1,
-// Cb r2, Cr r0, Cr r1, Cr r2 (r0, r1: the chroma rows of y0; r2: the second
-// chroma row of y1), with each segment's offset in its first chunk, the luma
-// vertical weight, the chroma vertical weights of y0 and y1, and which of r0,
-// r1 is y1's first chroma row. A lane holds one 16-byte chunk of each
-// segment, and with GL = 2 a second chunk of each luma segment (luma rows of
-// up to 2 KiB).
+// Cb r2, Cr r0, Cr r1, Cr r2 (y0 reads chroma rows r0, r1 and y1 reads r1,
+// r2), with each segment's offset in its first chunk, the luma vertical
+// weight and the chroma weights of rows r1 (for y0) and r2 (for y1), in
+// quarters. A lane holds one 16-byte chunk of each segment, and with GL = 2 a
+// second chunk of each luma segment (luma rows of up to 2 KiB).
 template <int GL>
 struct YuvStaged {
     u32x4 c[8];
     u32x4 c2[2];  // second luma chunks (GL = 2)
     int sh[8];
     float wy;
-    int fy0, fy1;  // vertical chroma weights of luma rows y0, y1, in quarters
-    int b0;
+    int fy0, fy1;  // weights of chroma rows r1 (in y0's pair) and r2 (in y1's), in quarters
 };
 
 // Load cursor over the output rows of I420 frames (the walk of the RGB
@@ -181,14 +183,17 @@ __device__ __forceinline__ void yuv_load(YuvStaged<GL> &st, const YuvCursor &c, 
     int y0, y1;
     vcursor_tap(c.v, y0, y1, st.wy);
     const Tap t0 = chroma_tap(c.ry + y0, c.Hc), t1 = chroma_tap(c.ry + y1, c.Hc);
+    // y1's taps move on by one chroma row (t1.x0 == t0.x1) or keep y0's
+    // second row (t1.x1 == t0.x1); y1 reads (r1 = t0.x1, r2) either way
+    const bool next = t1.x0 == t0.x1;
+    const int r2 = next ? t1.x1 : t1.x0;
     st.fy0 = (int)(4.0f * t0.w);  // exact: 0, 1 or 3
-    st.fy1 = (int)(4.0f * t1.w);
-    st.b0 = t1.x0 == t0.x0 ? 0 : 1;
+    st.fy1 = next ? (int)(4.0f * t1.w) : 4 - (int)(4.0f * t1.w);
     const uintptr_t row[8] = {
         c.base[0] + (uintptr_t)y0 * (uintptr_t)c.W,     c.base[0] + (uintptr_t)y1 * (uintptr_t)c.W,
         c.base[1] + (uintptr_t)t0.x0 * (uintptr_t)c.Wc, c.base[1] + (uintptr_t)t0.x1 * (uintptr_t)c.Wc,
-        c.base[1] + (uintptr_t)t1.x1 * (uintptr_t)c.Wc, c.base[2] + (uintptr_t)t0.x0 * (uintptr_t)c.Wc,
-        c.base[2] + (uintptr_t)t0.x1 * (uintptr_t)c.Wc, c.base[2] + (uintptr_t)t1.x1 * (uintptr_t)c.Wc};
+        c.base[1] + (uintptr_t)r2 * (uintptr_t)c.Wc,    c.base[2] + (uintptr_t)t0.x0 * (uintptr_t)c.Wc,
+        c.base[2] + (uintptr_t)t0.x1 * (uintptr_t)c.Wc, c.base[2] + (uintptr_t)r2 * (uintptr_t)c.Wc};
     typedef __attribute__((address_space(1))) const uint8_t GlobalByte;
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
@@ -291,6 +296,47 @@ __device__ __forceinline__ void lds_read_quads<8>(const uint32_t (&A)[8], uint32
 }
 #undef SMOL_RD2
 
+// The reads of one output pixel when both luma segments start at one offset
+// in their first chunk and all six chroma segments at another (planes whose
+// pitches and offsets are multiples of 16 give that on every row). aY: LDS
+// byte address of luma column x0 in segment Y y0; aC: of the pixel's first
+// chroma column in segment Cb r0. The other segments lie whole KiB further
+// (yuv_seg). lum: luma bytes x0, x0 + 1 of row y0, then of row y1 (byte reads,
+// zero-extended); q[2 .. 7]: bytes aC .. aC + 3 of Cb r0 .. r2, Cr r0 .. r2,
+// from dword reads of two segments at a time (offsets in units of 256 bytes)
+// at the aligned address and the next dword, realigned. (Byte reads into
+// register halves would save registers, but with ECC-protected registers the
+// hardware clears the other half, so each byte gets a register of its own.)
+template <int GL>
+__device__ __forceinline__ void yuv_read_px(uint32_t aY, uint32_t aC, uint32_t (&lum)[4],
+                                            uint32_t (&q)[8])
+{
+    constexpr int kY1 = (int)(yuv_seg<GL>(1) - yuv_seg<GL>(0));
+    static_assert(yuv_seg<GL>(7) - yuv_seg<GL>(2) == 5 * 1024, "chroma segments 1 KiB apart");
+    const uint32_t m = aC & ~3u, m4 = m + 4;
+    u32x2 d[3], e[3];
+    asm volatile("ds_read_u8 %0, %10\n\t"
+                 "ds_read_u8 %1, %10 offset:1\n\t"
+                 "ds_read_u8 %2, %10 offset:%13\n\t"
+                 "ds_read_u8 %3, %10 offset:%14\n\t"
+                 "ds_read2st64_b32 %4, %11 offset1:4\n\t"
+                 "ds_read2st64_b32 %5, %11 offset0:8 offset1:12\n\t"
+                 "ds_read2st64_b32 %6, %11 offset0:16 offset1:20\n\t"
+                 "ds_read2st64_b32 %7, %12 offset1:4\n\t"
+                 "ds_read2st64_b32 %8, %12 offset0:8 offset1:12\n\t"
+                 "ds_read2st64_b32 %9, %12 offset0:16 offset1:20\n\t"
+                 "s_waitcnt lgkmcnt(0)"
+                 : "=&v"(lum[0]), "=&v"(lum[1]), "=&v"(lum[2]), "=&v"(lum[3]), "=&v"(d[0]),
+                   "=&v"(d[1]), "=&v"(d[2]), "=&v"(e[0]), "=&v"(e[1]), "=&v"(e[2])
+                 : "v"(aY), "v"(m), "v"(m4), "i"(kY1), "i"(kY1 + 1)
+                 : "memory");
+#pragma unroll
+    for (int t = 0; t < 3; ++t) {
+        q[2 + 2 * t] = __builtin_amdgcn_alignbyte(e[t].x, d[t].x, aC);
+        q[3 + 2 * t] = __builtin_amdgcn_alignbyte(e[t].y, d[t].y, aC);
+    }
+}
+
 // 16 * (chroma - 128) at one luma tap: the tap's four chroma samples
 // (selected from chroma rows ra and rb) dotted with its weight bytes, minus
 // 2048, exact in integers.
@@ -300,38 +346,48 @@ __device__ __forceinline__ float chroma16(uint32_t ra, uint32_t rb, uint32_t sel
     return (float)(int)__builtin_amdgcn_udot4(smp, wts, (uint32_t)-2048, false);
 }
 
-template <int F16, int J, int EXACT, int GL>
+// One output row from the staged segments. SAME: every luma segment of the
+// row starts at offset sh[0] in its first chunk and every chroma segment at
+// sh[2] (the reads of yuv_read_px); otherwise each segment is addressed on
+// its own.
+template <int F16, int J, int EXACT, int GL, int SAME>
 __device__ __forceinline__ void yuv_compute(const NormK &nk, uint32_t slot, const int (&sh)[8],
-                                            float wy, int fy0, int fy1, int b0,
-                                            const YuvCols<J> &k, RowOut<F16, J> &out)
+                                            float wy, int fy0, int fy1, const YuvCols<J> &k,
+                                            RowOut<F16, J> &out)
 {
     // weight bytes of luma row yi and column xi: hw(xi) * (4 + 65535 fy(yi))
     // = (4 - fy) * [4 - fx, fx, 0, 0] + fy * [0, 0, 4 - fx, fx] (no carries)
     const uint32_t vm[2] = {4u + 65535u * (uint32_t)fy0, 4u + 65535u * (uint32_t)fy1};
+    const uint32_t baseY = slot + yuv_seg<GL>(0) + (uint32_t)sh[0];
+    const uint32_t baseC = slot + yuv_seg<GL>(2) + (uint32_t)sh[2];
 #pragma unroll
     for (int j = 0; j < J; ++j) {
         float o[3][2];
 #pragma unroll
         for (int px = 0; px < 2; ++px) {
             // reads: Y y0, Y y1, Cb r0..r2, Cr r0..r2
-            uint32_t A[8], q[8];
+            uint32_t q[8], lum[4];
+            if (SAME) {
+                yuv_read_px<GL>(baseY + (uint32_t)k.ox[j][px], baseC + (uint32_t)k.oc[j][px], lum,
+                                q);
+            } else {
+                uint32_t A[8];
 #pragma unroll
-            for (int s = 0; s < 8; ++s)
-                A[s] = slot + yuv_seg<GL>(s) + (uint32_t)sh[s] +
-                       (uint32_t)(s < 2 ? k.ox[j][px] : k.oc[j][px]);
-            lds_read_quads<8>(A, q);
+                for (int s = 0; s < 8; ++s)
+                    A[s] = slot + yuv_seg<GL>(s) + (uint32_t)sh[s] +
+                           (uint32_t)(s < 2 ? k.ox[j][px] : k.oc[j][px]);
+                lds_read_quads<8>(A, q);
+            }
             // 16 * (chroma - 128) at (y0, y1) x (x0, x1) for both planes:
-            // luma row y0 reads chroma rows r0, r1; y1 reads r0 or r1 (b0),
-            // and r2
+            // luma row y0 reads chroma rows r0, r1 and y1 reads r1, r2
             float cc[2][2][2];  // [plane][luma row][luma col]
 #pragma unroll
             for (int pl = 0; pl < 2; ++pl) {
                 const uint32_t r0 = q[2 + 3 * pl], r1 = q[3 + 3 * pl], r2 = q[4 + 3 * pl];
-                const uint32_t ra1 = b0 ? r1 : r0;
 #pragma unroll
                 for (int xi = 0; xi < 2; ++xi) {
                     cc[pl][0][xi] = chroma16(r0, r1, k.sel[j][px][xi], __umul24(k.hw[j][px][xi], vm[0]));
-                    cc[pl][1][xi] = chroma16(ra1, r2, k.sel[j][px][xi], __umul24(k.hw[j][px][xi], vm[1]));
+                    cc[pl][1][xi] = chroma16(r1, r2, k.sel[j][px][xi], __umul24(k.hw[j][px][xi], vm[1]));
                 }
             }
             float rgb[2][2][3];  // [luma row][luma col][channel]
@@ -339,7 +395,8 @@ __device__ __forceinline__ void yuv_compute(const NormK &nk, uint32_t slot, cons
             for (int yi = 0; yi < 2; ++yi)
 #pragma unroll
                 for (int xi = 0; xi < 2; ++xi) {
-                    const float Y = xi ? cvt_ubyte1(q[yi]) : cvt_ubyte0(q[yi]);
+                    const float Y = SAME ? cvt_ubyte0(lum[2 * yi + xi])
+                                         : xi ? cvt_ubyte1(q[yi]) : cvt_ubyte0(q[yi]);
                     ycbcr16_to_rgb(Y, cc[0][yi][xi], cc[1][yi][xi], rgb[yi][xi][0],
                                    rgb[yi][xi][1], rgb[yi][xi][2]);
                 }
@@ -352,6 +409,25 @@ __device__ __forceinline__ void yuv_compute(const NormK &nk, uint32_t slot, cons
         }
         pack_pair<F16, EXACT, J>(out, j, o);
     }
+}
+
+// Whether every luma segment of a row starts at one offset in its first
+// chunk and every chroma segment at another.
+__device__ __forceinline__ bool yuv_same_offsets(const int (&sh)[8])
+{
+    return sh[1] == sh[0] && sh[3] == sh[2] && sh[4] == sh[2] && sh[5] == sh[2] &&
+           sh[6] == sh[2] && sh[7] == sh[2];
+}
+
+template <int F16, int J, int EXACT, int GL>
+__device__ __forceinline__ void yuv_compute_row(const NormK &nk, uint32_t slot, const int (&sh)[8],
+                                                float wy, int fy0, int fy1, const YuvCols<J> &k,
+                                                RowOut<F16, J> &out)
+{
+    if (yuv_same_offsets(sh))
+        yuv_compute<F16, J, EXACT, GL, 1>(nk, slot, sh, wy, fy0, fy1, k, out);
+    else
+        yuv_compute<F16, J, EXACT, GL, 0>(nk, slot, sh, wy, fy0, fy1, k, out);
 }
 
 // FORM as for rgb_rows_kernel; GL: chunks per lane of a luma segment (staged
@@ -420,11 +496,10 @@ yuv_rows_kernel(BatchArgs a)
         csh[s] = R.sh[s];
     float cwy = R.wy;
     int cfy0 = R.fy0, cfy1 = R.fy1;
-    int cb0 = R.b0;
     for (int left = n_rows - 1; left > 0; --left) {
         yuv_load<GL>(R, lc, lane, false);
         advance();
-        yuv_compute<F16, J, EXACT, GL>(nk, lds0, csh, cwy, cfy0, cfy1, cb0, cols, out);
+        yuv_compute_row<F16, J, EXACT, GL>(nk, lds0, csh, cwy, cfy0, cfy1, cols, out);
         yuv_write<GL>(lds, R, lane);
         store_row<F16, J, ODD>(orow, plane, a.Cw, lane, out, NHWC);
 #pragma unroll
@@ -433,7 +508,6 @@ yuv_rows_kernel(BatchArgs a)
         cwy = R.wy;
         cfy0 = R.fy0;
         cfy1 = R.fy1;
-        cb0 = R.b0;
         const int pimg = c_img;
         c_img += step.di;
         c_rr += step.dr;
@@ -453,7 +527,7 @@ yuv_rows_kernel(BatchArgs a)
             }
         }
     }
-    yuv_compute<F16, J, EXACT, GL>(nk, lds0, csh, cwy, cfy0, cfy1, cb0, cols, out);
+    yuv_compute_row<F16, J, EXACT, GL>(nk, lds0, csh, cwy, cfy0, cfy1, cols, out);
     store_row<F16, J, ODD>(orow, plane, a.Cw, lane, out, NHWC);
 }
 

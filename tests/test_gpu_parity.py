@@ -386,6 +386,28 @@ def test_yuv_row_streaming_exact(name, sizes, S, C, dtype):
                                   ref.view(np.uint32 if dtype == F32 else np.uint16))
 
 
+# Frames whose row segments all start at one offset per plane (pitches and
+# plane offsets multiples of 16: the row kernel's shared-address reads) and
+# frames where they do not (luma pitch 1288: consecutive luma rows 8 bytes
+# apart in their chunks; chroma pitch 648 likewise), alone and mixed in one
+# ragged batch.
+YUV_OFFSETS = [
+    ("same", [(1280, 720)]),
+    ("luma-mixed", [(1288, 720)]),
+    ("chroma-mixed", [(1296, 720)]),
+    ("all", [(1280, 720), (1288, 720), (1296, 720), (1280, 720)]),
+]
+
+
+@pytest.mark.parametrize("dtype", [F32, F16])
+@pytest.mark.parametrize("name,sizes", YUV_OFFSETS, ids=[e[0] for e in YUV_OFFSETS])
+def test_yuv_row_segment_offsets_exact(name, sizes, dtype):
+    smol.set_tuning(path=smol.PATH_ROWS, exact=1)
+    got, ref = _check(_yuv(name, sizes, 256, 224, dtype, seed=len(name)))
+    np.testing.assert_array_equal(got.view(np.uint32 if dtype == F32 else np.uint16),
+                                  ref.view(np.uint32 if dtype == F32 else np.uint16))
+
+
 @pytest.mark.parametrize("path", [smol.PATH_AUTO, smol.PATH_ROWS])
 def test_yuv_frame_at_end_of_src_first_in_batch(path):
     """Batch order reverses memory order: the frame whose planes end at the
