@@ -107,6 +107,7 @@ struct YuvStaged {
 struct YuvCursor {
     int img, rr;
     VCursor v;          // luma vertical map over the region's rows
+    double rcp;         // 1 / v.den, rounded to nearest
     uintptr_t base[3];  // first staged byte of the region's row 0 (Y), of chroma row 0 (Cb, Cr)
     int W, Wc, Hc, yspan, cspan;  // frame luma pitch, chroma pitch and rows
     int ry;             // the region's first frame row
@@ -124,6 +125,7 @@ __device__ __forceinline__ void yuv_cursor_image(YuvCursor &c, const BatchArgs &
     lg.Hr = g.Hr;
     lg.top = g.top;
     vcursor_init<STRIDE>(c.v, a, lg, rr, s);
+    c.rcp = 1.0 / (double)c.v.den;
     c.W = g.fw;
     c.Wc = (g.fw + 1) >> 1;
     c.Hc = (g.fh + 1) >> 1;
@@ -176,42 +178,80 @@ __device__ __forceinline__ constexpr uint32_t yuv_seg(int s)
     return s < 2 ? 1024u * GL * (uint32_t)s : 2048u * GL + 1024u * (uint32_t)(s - 2);
 }
 
+// The vertical chroma taps of frame luma row y (centred siting; the rows
+// and weight of chroma_tap) with the weight of the second row in quarters.
+__device__ __forceinline__ void chroma_rows(int y, int n, int &r0, int &r1, int &f)
+{
+    const int num = 2 * y - 1;
+    const int q = num >> 2;
+    if (num <= 0) {
+        r0 = r1 = 0;
+        f = 0;
+    } else if (q >= n - 1) {
+        r0 = r1 = n - 1;
+        f = 0;
+    } else {
+        r0 = q;
+        r1 = q + 1;
+        f = num & 3;
+    }
+}
+
 template <int GL>
 __device__ __forceinline__ void yuv_load(YuvStaged<GL> &st, const YuvCursor &c, int lane,
                                          bool repeat)
 {
     int y0, y1;
-    vcursor_tap(c.v, y0, y1, st.wy);
-    const Tap t0 = chroma_tap(c.ry + y0, c.Hc), t1 = chroma_tap(c.ry + y1, c.Hc);
-    // y1's taps move on by one chroma row (t1.x0 == t0.x1) or keep y0's
-    // second row (t1.x1 == t0.x1); y1 reads (r1 = t0.x1, r2) either way
-    const bool next = t1.x0 == t0.x1;
-    const int r2 = next ? t1.x1 : t1.x0;
-    st.fy0 = (int)(4.0f * t0.w);  // exact: 0, 1 or 3
-    st.fy1 = next ? (int)(4.0f * t1.w) : 4 - (int)(4.0f * t1.w);
+    if (c.v.q < 0 || (c.v.q == 0 && c.v.rem == 0)) {
+        y0 = y1 = 0;
+        st.wy = 0.0f;
+    } else if (c.v.q >= c.v.H - 1) {
+        y0 = y1 = c.v.H - 1;
+        st.wy = 0.0f;
+    } else {
+        y0 = c.v.q;
+        y1 = y0 + 1;
+        // rem / den rounded to nearest fp32 (0 < rem < den <= 2^24): the
+        // fp64 product rem * RN(1 / den) is within 2^-52 (relative) of the
+        // quotient, and no such quotient lies within 2^-49 (relative) of a
+        // midpoint between fp32 values (that would need 2^25 | den), so
+        // both round to the same fp32 value
+        st.wy = (float)((double)c.v.rem * c.rcp);
+    }
+    int a0, a1, f0, b0, b1, f1;
+    chroma_rows(c.ry + y0, c.Hc, a0, a1, f0);
+    chroma_rows(c.ry + y1, c.Hc, b0, b1, f1);
+    // y1's taps move on by one chroma row (b0 == a1) or keep y0's second row
+    // (b1 == a1); y1 reads (r1 = a1, r2) either way
+    const bool next = b0 == a1;
+    const int r2 = next ? b1 : b0;
+    st.fy0 = f0;
+    st.fy1 = next ? f1 : 4 - f1;
     const uintptr_t row[8] = {
-        c.base[0] + (uintptr_t)y0 * (uintptr_t)c.W,     c.base[0] + (uintptr_t)y1 * (uintptr_t)c.W,
-        c.base[1] + (uintptr_t)t0.x0 * (uintptr_t)c.Wc, c.base[1] + (uintptr_t)t0.x1 * (uintptr_t)c.Wc,
-        c.base[1] + (uintptr_t)r2 * (uintptr_t)c.Wc,    c.base[2] + (uintptr_t)t0.x0 * (uintptr_t)c.Wc,
-        c.base[2] + (uintptr_t)t0.x1 * (uintptr_t)c.Wc, c.base[2] + (uintptr_t)r2 * (uintptr_t)c.Wc};
+        c.base[0] + (uintptr_t)y0 * (uintptr_t)c.W,  c.base[0] + (uintptr_t)y1 * (uintptr_t)c.W,
+        c.base[1] + (uintptr_t)a0 * (uintptr_t)c.Wc, c.base[1] + (uintptr_t)a1 * (uintptr_t)c.Wc,
+        c.base[1] + (uintptr_t)r2 * (uintptr_t)c.Wc, c.base[2] + (uintptr_t)a0 * (uintptr_t)c.Wc,
+        c.base[2] + (uintptr_t)a1 * (uintptr_t)c.Wc, c.base[2] + (uintptr_t)r2 * (uintptr_t)c.Wc};
     typedef __attribute__((address_space(1))) const uint8_t GlobalByte;
+    typedef const __attribute__((address_space(1))) u32x4 GlobalChunk;
+    const uint32_t lane16 = 16u * (uint32_t)lane;
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
         st.sh[s] = (int)(row[s] & 15);
-        const int last = repeat ? 0 : (st.sh[s] + (s < 2 ? c.yspan : c.cspan) - 1) >> 4;
+        // byte offset of the lane's chunk: lanes past the segment's last
+        // chunk load that chunk again
+        const uint32_t last16 =
+            repeat ? 0u : (uint32_t)(st.sh[s] + (s < 2 ? c.yspan : c.cspan) - 1) & ~15u;
         GlobalByte *p = (GlobalByte *)(row[s] - (uintptr_t)st.sh[s]);
         // chroma rows are shared by consecutive output rows (a chroma row
         // covers two luma rows): ordinary loads, so the next row's loads of
         // the same rows hit in the caches; luma rows are streamed once
         if (s < 2)
-            st.c[s] = __builtin_nontemporal_load(
-                (const __attribute__((address_space(1))) u32x4 *)(p + 16u * (uint32_t)min(lane, last)));
+            st.c[s] = __builtin_nontemporal_load((GlobalChunk *)(p + min(lane16, last16)));
         else
-            st.c[s] = *(const __attribute__((address_space(1))) u32x4 *)(p + 16u * (uint32_t)min(lane, last));
+            st.c[s] = *(GlobalChunk *)(p + min(lane16, last16));
         if (GL == 2 && s < 2)
-            st.c2[s] = __builtin_nontemporal_load(
-                (const __attribute__((address_space(1))) u32x4 *)(p + 16u * (uint32_t)min(64 + lane,
-                                                                                           last)));
+            st.c2[s] = __builtin_nontemporal_load((GlobalChunk *)(p + min(1024u + lane16, last16)));
     }
 }
 
