@@ -871,16 +871,28 @@ const void *yuv_rows_kernel_for(const BatchArgs &a, int f16)
     return a.interleave ? rows_yuv_stride(a, f16) : rows_yuv_range(a, f16);
 }
 
+// LDS bytes of the column table that the waves of an I420 row-streaming
+// workgroup share when the batch is uniform (no descriptor table) and the
+// group has more than one wave: 32 bytes per lane and pixel of the lane's
+// 2 J columns (the kernel's yuv_col_table_bytes).
+static size_t yuv_rows_table_lds(const BatchArgs &a, bool uniform)
+{
+    const size_t J = a.col_iters <= 1 ? 1 : a.col_iters <= 2 ? 2 : 4;
+    return uniform && a.wpg > 1 ? 2 * J * 64 * 32 : 0;
+}
+
 int launch_yuv_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, void *stream, void *done)
 {
     return launch_one(yuv_rows_kernel_for(a, out_f16), dim3((unsigned)(a.grid / a.wpg)),
-                      dim3(64 * a.wpg), lds_bytes * a.wpg, a, stream, done);
+                      dim3(64 * a.wpg), lds_bytes * a.wpg + yuv_rows_table_lds(a, !a.table), a,
+                      stream, done);
 }
 
 int occupancy_yuv_rows(const BatchArgs &a, int out_f16, size_t lds_bytes, int *blocks_per_cu)
 {
-    return occupancy(yuv_rows_kernel_for(a, out_f16), 64 * a.wpg, lds_bytes * a.wpg,
-                     blocks_per_cu);
+    // queried before the batch's table is known: counts the shared table
+    return occupancy(yuv_rows_kernel_for(a, out_f16), 64 * a.wpg,
+                     lds_bytes * a.wpg + yuv_rows_table_lds(a, true), blocks_per_cu);
 }
 
 }  // namespace smol

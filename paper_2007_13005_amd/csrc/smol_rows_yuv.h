@@ -276,36 +276,93 @@ struct YuvCols {
     uint32_t hw[J][2][2];    // per luma column: horizontal weight bytes (4 - fx, fx)
 };
 
+// The column data of pixel px of column iteration j (one column of the lane)
+// as 8 words: ox, wx (bits), oc, sel[0], sel[1], hw[0], hw[1], 0.
+__device__ __forceinline__ void yuv_col(uint32_t (&w)[8], const YuvImg &g, int Cw, int lane,
+                                        int siting, int j, int px)
+{
+    const int Wc = (g.fw + 1) >> 1;
+    const int cxf = chroma_tap(g.rx + g.xf, Wc, siting).x0;
+    const int c = min(pair_col(lane, j, Cw) + px, Cw - 1);
+    const Tap t = axis_tap(g.left + c, g.W, g.Wr);
+    const Tap a0 = chroma_tap(g.rx + t.x0, Wc, siting), a1 = chroma_tap(g.rx + t.x1, Wc, siting);
+    w[0] = (uint32_t)(t.x0 - g.xf);
+    w[1] = __builtin_bit_cast(uint32_t, t.w);
+    w[2] = (uint32_t)(a0.x0 - cxf);
+    // the samples of luma column xi are bytes d0, d1 of the 4 read from each
+    // chroma row; perm(row b, row a) yields a[d0], a[d1], b[d0], b[d1]
+    const Tap ax[2] = {a0, a1};
+#pragma unroll
+    for (int xi = 0; xi < 2; ++xi) {
+        const uint32_t d0 = (uint32_t)(ax[xi].x0 - a0.x0);
+        const uint32_t d1 = (uint32_t)(ax[xi].x1 - a0.x0);
+        w[3 + xi] = d0 | d1 << 8 | (4 + d0) << 16 | (4 + d1) << 24;
+        const uint32_t fx = (uint32_t)(4.0f * ax[xi].w);  // exact: 0 .. 3
+        w[5 + xi] = (4 - fx) | fx << 8;
+    }
+    w[7] = 0;
+}
+
+template <int J>
+__device__ __forceinline__ void yuv_col_set(YuvCols<J> &k, int j, int px, const uint32_t (&w)[8])
+{
+    k.ox[j][px] = (int)w[0];
+    k.wx[j][px] = __builtin_bit_cast(float, w[1]);
+    k.oc[j][px] = (int)w[2];
+    k.sel[j][px][0] = w[3];
+    k.sel[j][px][1] = w[4];
+    k.hw[j][px][0] = w[5];
+    k.hw[j][px][1] = w[6];
+}
+
 template <int J>
 __device__ __forceinline__ void yuv_cols(YuvCols<J> &k, const YuvImg &g, int Cw, int lane,
                                          int siting)
 {
-    const int Wc = (g.fw + 1) >> 1;
-    const int cxf = chroma_tap(g.rx + g.xf, Wc, siting).x0;
 #pragma unroll
     for (int j = 0; j < J; ++j)
 #pragma unroll
         for (int px = 0; px < 2; ++px) {
-            const int c = min(pair_col(lane, j, Cw) + px, Cw - 1);
-            const Tap t = axis_tap(g.left + c, g.W, g.Wr);
-            const Tap a0 = chroma_tap(g.rx + t.x0, Wc, siting),
-                      a1 = chroma_tap(g.rx + t.x1, Wc, siting);
-            k.ox[j][px] = t.x0 - g.xf;
-            k.wx[j][px] = t.w;
-            k.oc[j][px] = a0.x0 - cxf;
-            // the samples of luma column xi are bytes d0, d1 of the 4 read
-            // from each chroma row; perm(row b, row a) yields a[d0], a[d1],
-            // b[d0], b[d1]
-            const Tap ax[2] = {a0, a1};
-#pragma unroll
-            for (int xi = 0; xi < 2; ++xi) {
-                const uint32_t d0 = (uint32_t)(ax[xi].x0 - a0.x0);
-                const uint32_t d1 = (uint32_t)(ax[xi].x1 - a0.x0);
-                k.sel[j][px][xi] = d0 | d1 << 8 | (4 + d0) << 16 | (4 + d1) << 24;
-                const uint32_t fx = (uint32_t)(4.0f * ax[xi].w);  // exact: 0 .. 3
-                k.hw[j][px][xi] = (4 - fx) | fx << 8;
-            }
+            uint32_t w[8];
+            yuv_col(w, g, Cw, lane, siting, j, px);
+            yuv_col_set<J>(k, j, px, w);
         }
+}
+
+// LDS bytes of the column table that the waves of a workgroup share when a
+// uniform batch gives them all one geometry: 32 bytes per lane and pixel.
+template <int J>
+__device__ __host__ constexpr uint32_t yuv_col_table_bytes()
+{
+    return 2u * J * 64u * 32u;  // the host adds the same to a uniform launch's LDS
+}
+
+// yuv_cols for the waves of a workgroup that share one geometry: wave wid
+// computes the pixels (j, px) with (2 j + px) % wpg == wid into the table,
+// then every wave reads all of them (each pixel's data is the same for every
+// wave's lane). The barrier waits for this wave's LDS writes only, not for
+// the row loads already in flight.
+template <int J>
+__device__ __forceinline__ void yuv_cols_shared(YuvCols<J> &k, uint8_t *table, const YuvImg &g,
+                                                int Cw, int lane, int siting, int wid, int wpg)
+{
+#pragma unroll
+    for (int t = 0; t < 2 * J; ++t)
+        if (t % wpg == wid) {
+            uint32_t w[8];
+            yuv_col(w, g, Cw, lane, siting, t / 2, t & 1);
+            u32x4 *e = (u32x4 *)(table + 32u * (64u * (uint32_t)t + (uint32_t)lane));
+            e[0] = u32x4{w[0], w[1], w[2], w[3]};
+            e[1] = u32x4{w[4], w[5], w[6], w[7]};
+        }
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+#pragma unroll
+    for (int t = 0; t < 2 * J; ++t) {
+        const u32x4 *e = (const u32x4 *)(table + 32u * (64u * (uint32_t)t + (uint32_t)lane));
+        const u32x4 lo = e[0], hi = e[1];
+        const uint32_t w[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+        yuv_col_set<J>(k, t / 2, t & 1, w);
+    }
 }
 
 // Dword-aligned reads of N byte groups (at LDS byte addresses A), realigned:
@@ -519,7 +576,11 @@ yuv_rows_kernel(BatchArgs a)
     int cW, cWr, cleft;
     {
         const YuvImg g = yuv_img(a, c_img);
-        yuv_cols<J>(cols, g, a.Cw, lane, a.siting);
+        if (!a.table && a.wpg > 1)
+            yuv_cols_shared<J>(cols, lds_all + a.wpg * yuv_seg<GL>(8), g, a.Cw, lane, a.siting,
+                               __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)), a.wpg);
+        else
+            yuv_cols<J>(cols, g, a.Cw, lane, a.siting);
         cW = g.W;
         cWr = g.Wr;
         cleft = g.left;
