@@ -31,14 +31,18 @@ if ROOT not in sys.path:
 METRIC = "images/sec preprocessed + achieved HBM GB/s (% of MI355X peak), 1 GPU"
 HBM_PEAK_GBPS = 8000.0  # MI355X published HBM3E bandwidth
 # ALU ceilings from the unit counts and clock (256 compute units of 4 SIMDs at
-# 2.4 GHz). A SIMD executes a 64-lane fp32 VALU instruction in 4 clocks (16
-# lanes per clock), so the chip issues 256 * 4 / 4 * 2.4e9 wave instructions
-# per second; a separately rounded fp32 add, multiply, min or max (packed fp32
-# is not used) is one operation per lane per clock: 256 * 64 * 2.4e9 per
-# second. (The published 157.3 TFLOP/s counts packed fused multiply-adds, four
-# flops per lane per clock.)
+# 2.4 GHz). A SIMD issues a 64-lane VALU instruction every 4 clocks (16 lanes
+# per clock); unpacked fp32 adds, multiplies and fused multiply-adds issue at
+# twice that rate (32 lanes per clock, two instructions from two waves per
+# 4 clocks), everything else (conversions, integer, permutes, byte alignment,
+# dot products, min/max/med3) at the single rate. These rates are measured by
+# `smol_valu_probe` (`--valu-probe`). The definition's operations are
+# separately rounded adds and multiplies (no contraction), one instruction
+# each, so their ceiling is 256 * 4 * 32 * 2.4e9 = 78.6 T operations/s: half
+# the published 157.3 TFLOP/s, which counts a fused multiply-add as two.
 VALU_WAVE_INSTR_PER_S = 256 * 4 / 4 * 2.4e9
-ALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12
+VALU_DUAL_WAVE_INSTR_PER_S = 2 * VALU_WAVE_INSTR_PER_S
+ALU_PEAK_TOPS = 256 * 4 * 32 * 2.4e9 / 1e12
 MALL_BYTES = 256 * 1024 * 1024
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
@@ -90,6 +94,9 @@ def parse():
     ap.add_argument("--copy-probe", type=int, default=0,
                     help="instead of the benchmark, copy this many MiB with torch several "
                          "times (calibrates the FETCH_SIZE / WRITE_SIZE counters)")
+    ap.add_argument("--valu-probe", action="store_true",
+                    help="instead of the benchmark, measure the issue rate of each VALU "
+                         "instruction kind of smol_valu_probe at 1, 2, 3 and 4 waves per SIMD")
     return ap.parse_args()
 
 
@@ -207,12 +214,18 @@ def roofline_of(wl, smol, algo: int, launches: int, avg_launch_s: float,
                 traffic: dict | None) -> dict:
     """The roofline entry of the launch. The bound follows the counters of
     the committed profile: issue time of its VALU instructions at the chip's
-    rate against its HBM bytes at the peak bandwidth; without counters, HBM."""
+    rates against its HBM bytes at the peak bandwidth; without counters, HBM."""
     per_launch = algo / launches
     mem_bytes = per_launch if traffic is None else max(per_launch, traffic["bytes_per_launch"])
     t_mem = mem_bytes / (HBM_PEAK_GBPS * 1e9)
     valu = None if traffic is None else traffic.get("valu_insts_per_launch")
-    t_alu = None if valu is None else valu / VALU_WAVE_INSTR_PER_S
+    dual = None if traffic is None else traffic.get("valu_dual_insts_per_launch")
+    t_alu = None
+    if valu is not None:
+        # fp32 add/mul/fma at the dual rate when their counts were taken,
+        # every instruction at the single rate otherwise
+        dual = 0 if dual is None else min(dual, valu)
+        t_alu = dual / VALU_DUAL_WAVE_INSTR_PER_S + (valu - dual) / VALU_WAVE_INSTR_PER_S
     bound = "alu" if t_alu is not None and t_alu > t_mem else "hbm"
     if bound == "alu":
         achieved = algorithmic_ops(wl, smol) / launches / avg_launch_s / 1e12
@@ -419,6 +432,30 @@ def load_traffic(config: str) -> dict | None:
     if h.hexdigest() != rec.get("sources_sha256"):
         return None
     return rec
+
+
+def valu_probe() -> None:
+    """Per kind of VALU instruction and waves per SIMD: 64-lane instructions
+    issued per ns per SIMD (median wave's time, 1024 SIMDs), and that rate in
+    lanes per clock at 2.4 GHz."""
+    import torch
+    from paper_2007_13005_amd import smol
+    iters = 8192
+    ticks = torch.zeros(4 * 1024, dtype=torch.int64, device="cuda:0")
+    rows = []
+    for kind, name in enumerate(smol.VALU_KINDS):
+        for per_simd in (1, 2, 3, 4):
+            waves = 1024 * per_simd
+            for _ in range(2):  # the first launch warms the clocks
+                smol.valu_probe(kind, waves, iters, ticks.data_ptr())
+                torch.cuda.synchronize()
+            t = sorted(ticks[:waves].cpu().tolist())
+            ns = t[len(t) // 2] * 10.0
+            rate = 8 * iters * per_simd / ns
+            rows.append({"kind": name, "waves_per_simd": per_simd, "ns": ns,
+                         "wave_instr_per_ns_per_simd": round(rate, 3),
+                         "lanes_per_clock_at_2.4GHz": round(rate * 64 / 2.4, 1)})
+            print(json.dumps(rows[-1]), flush=True)
 
 
 def copy_probe(mib: int) -> None:
@@ -842,6 +879,9 @@ def main() -> int:
               "preprocessing path shards by image with no communication, and only the "
               "single-GPU share is measured here.", file=sys.stderr, flush=True)
         return 2
+    if args.valu_probe:
+        valu_probe()
+        return 0
     if args.copy_probe:
         copy_probe(args.copy_probe)
         return 0

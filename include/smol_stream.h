@@ -45,6 +45,34 @@ extern "C" {
 int smol_stream_probe(const void *src, uint64_t read_bytes, void *dst, uint64_t write_bytes,
                       int32_t waves, int32_t flags, void *stream);
 
+/* Instruction kinds of smol_valu_probe. */
+#define SMOL_VALU_MUL_F32 0     /* v_mul_f32          */
+#define SMOL_VALU_ADD_F32 1     /* v_add_f32          */
+#define SMOL_VALU_FMA_F32 2     /* v_fma_f32          */
+#define SMOL_VALU_PERM 3        /* v_perm_b32         */
+#define SMOL_VALU_ALIGNBYTE 4   /* v_alignbyte_b32    */
+#define SMOL_VALU_DOT4 5        /* v_dot4_u32_u8      */
+#define SMOL_VALU_MED3_F32 6    /* v_med3_f32         */
+#define SMOL_VALU_CVT_F32_I32 7 /* v_cvt_f32_i32      */
+#define SMOL_VALU_MUL_U24 8     /* v_mul_u32_u24      */
+#define SMOL_VALU_KINDS 9
+
+/* The issue rate of one kind of VALU instruction, the other ceiling of the
+ * preprocessing kernels (the I420 path and the block decoder spend more time
+ * issuing VALU instructions than moving bytes). Enqueue one launch of
+ * `waves` one-wave workgroups; each wave issues `iters` x 8 instructions of
+ * `kind` on eight independent register chains (inline assembly, so nothing
+ * is folded away) and writes the time it took, in ticks of the 100 MHz
+ * real-time counter, to ticks[w] for its index w.
+ *   kind    SMOL_VALU_*
+ *   waves   1 .. 2^20 (the device's SIMDs take them round robin: 1024 waves
+ *           put one on each SIMD of a 256-CU part)
+ *   iters   1 .. 2^20
+ *   ticks   DEVICE buffer of `waves` uint64 values, owned by the caller
+ * Returns SMOL_OK, SMOL_ERR_INVALID_ARG (kind unknown, waves or iters out of
+ * range, ticks NULL) or SMOL_ERR_HIP; nothing is enqueued on error. */
+int smol_valu_probe(int32_t kind, int32_t waves, int32_t iters, uint64_t *ticks, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

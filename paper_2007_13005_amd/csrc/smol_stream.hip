@@ -100,8 +100,79 @@ __global__ void __launch_bounds__(64 * kWavesPerGroup) stream_kernel(StreamArgs 
     asm volatile("" ::"v"(acc.x), "v"(acc.y), "v"(acc.z), "v"(acc.w));
 }
 
+// Eight independent chains of one instruction (operands %0 .. %7 the chains,
+// %8 and %9 shared sources).
+#define SMOL_V8(I) I("%0") I("%1") I("%2") I("%3") I("%4") I("%5") I("%6") I("%7")
+#define SMOL_MUL(R) "v_mul_f32 " R ", " R ", %8\n\t"
+#define SMOL_ADD(R) "v_add_f32 " R ", " R ", %8\n\t"
+#define SMOL_FMA(R) "v_fma_f32 " R ", " R ", %8, %9\n\t"
+#define SMOL_PERM(R) "v_perm_b32 " R ", " R ", %8, %9\n\t"
+#define SMOL_ALIGN(R) "v_alignbyte_b32 " R ", " R ", %8, %9\n\t"
+#define SMOL_DOT4(R) "v_dot4_u32_u8 " R ", %8, %9, " R "\n\t"
+#define SMOL_MED3(R) "v_med3_f32 " R ", " R ", %8, %9\n\t"
+#define SMOL_CVT(R) "v_cvt_f32_i32 " R ", " R "\n\t"
+#define SMOL_MULU24(R) "v_mul_u32_u24 " R ", " R ", %8\n\t"
+#define SMOL_VALU_STEP(BODY)                                                                     \
+    asm volatile(SMOL_V8(BODY)                                                                   \
+                 : "+v"(r[0]), "+v"(r[1]), "+v"(r[2]), "+v"(r[3]), "+v"(r[4]), "+v"(r[5]),     \
+                   "+v"(r[6]), "+v"(r[7])                                                       \
+                 : "v"(x), "v"(y))
+
+template <int K>
+__global__ void __launch_bounds__(64) valu_kernel(uint64_t *ticks, int32_t iters)
+{
+    uint32_t r[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+        r[k] = 0x3f800000u + 977u * (uint32_t)k + (uint32_t)threadIdx.x;
+    const uint32_t x = 0x3f7ffff0u + (uint32_t)threadIdx.x, y = 0x3f800010u;
+    const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+#pragma unroll 4
+    for (int32_t it = 0; it < iters; ++it) {
+        if constexpr (K == 0) SMOL_VALU_STEP(SMOL_MUL);
+        else if constexpr (K == 1) SMOL_VALU_STEP(SMOL_ADD);
+        else if constexpr (K == 2) SMOL_VALU_STEP(SMOL_FMA);
+        else if constexpr (K == 3) SMOL_VALU_STEP(SMOL_PERM);
+        else if constexpr (K == 4) SMOL_VALU_STEP(SMOL_ALIGN);
+        else if constexpr (K == 5) SMOL_VALU_STEP(SMOL_DOT4);
+        else if constexpr (K == 6) SMOL_VALU_STEP(SMOL_MED3);
+        else if constexpr (K == 7) SMOL_VALU_STEP(SMOL_CVT);
+        else SMOL_VALU_STEP(SMOL_MULU24);
+    }
+    const uint64_t t1 = __builtin_amdgcn_s_memrealtime();
+    // keep the chains
+    asm volatile("" ::"v"(r[0]), "v"(r[1]), "v"(r[2]), "v"(r[3]), "v"(r[4]), "v"(r[5]),
+                 "v"(r[6]), "v"(r[7]));
+    if (threadIdx.x == 0)
+        ticks[blockIdx.x] = t1 - t0;
+}
+#undef SMOL_VALU_STEP
+
 }  // namespace
 }  // namespace smol
+
+extern "C" int smol_valu_probe(int32_t kind, int32_t waves, int32_t iters, uint64_t *ticks,
+                               void *stream)
+{
+    using namespace smol;
+    clear_error();
+    if (kind < 0 || kind >= SMOL_VALU_KINDS)
+        return set_error(SMOL_ERR_INVALID_ARG, "kind %d unknown", kind);
+    if (waves < 1 || waves > (1 << 20) || iters < 1 || iters > (1 << 20))
+        return set_error(SMOL_ERR_INVALID_ARG, "waves and iters must be in 1 .. 2^20");
+    if (!ticks)
+        return set_error(SMOL_ERR_INVALID_ARG, "ticks is NULL");
+    static const void *const kernels[SMOL_VALU_KINDS] = {
+        (const void *)valu_kernel<0>, (const void *)valu_kernel<1>, (const void *)valu_kernel<2>,
+        (const void *)valu_kernel<3>, (const void *)valu_kernel<4>, (const void *)valu_kernel<5>,
+        (const void *)valu_kernel<6>, (const void *)valu_kernel<7>, (const void *)valu_kernel<8>};
+    void *args[] = {(void *)&ticks, (void *)&iters};
+    const hipError_t e = hipLaunchKernel(kernels[kind], dim3((unsigned)waves), dim3(64), args, 0,
+                                         (hipStream_t)stream);
+    if (e != hipSuccess)
+        return set_error(SMOL_ERR_HIP, "VALU probe launch: %s", hipGetErrorString(e));
+    return SMOL_OK;
+}
 
 extern "C" int smol_stream_probe(const void *src, uint64_t read_bytes, void *dst,
                                  uint64_t write_bytes, int32_t waves, int32_t flags, void *stream)

@@ -180,6 +180,7 @@ SIGNATURES = {
                                                       _vp, ctypes.c_int32, _vp, ctypes.c_int32]),
     "smol_stream_probe": (ctypes.c_int, [_vp, ctypes.c_uint64, _vp, ctypes.c_uint64,
                                          ctypes.c_int32, ctypes.c_int32, _vp]),
+    "smol_valu_probe": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _vp, _vp]),
     "smol_set_tuning": (ctypes.c_int, [ctypes.POINTER(Tuning)]),
     "smol_last_plan": (ctypes.c_int, [ctypes.POINTER(Plan)]),
     "smol_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -338,6 +339,17 @@ def stream_probe(src: int, read_bytes: int, dst: int, write_bytes: int, waves: i
     handle): reads read_bytes at src, writes write_bytes at dst."""
     _check(lib().smol_stream_probe(src or None, read_bytes, dst or None, write_bytes, waves,
                                    flags, stream or None))
+
+
+VALU_KINDS = ("mul_f32", "add_f32", "fma_f32", "perm", "alignbyte", "dot4", "med3_f32",
+              "cvt_f32_i32", "mul_u24")
+
+
+def valu_probe(kind: int, waves: int, iters: int, ticks: int, stream: int = 0) -> None:
+    """One launch of the VALU issue-rate probe (``include/smol_stream.h``):
+    each of ``waves`` waves writes its elapsed 100 MHz ticks to the device
+    buffer at ``ticks``."""
+    _check(lib().smol_valu_probe(kind, waves, iters, ticks or None, stream or None))
 
 
 def _table(v, dtype) -> np.ndarray:

@@ -479,6 +479,17 @@ def test_stream_probe_validation(kw, needle):
     assert needle in smol.lib().smol_last_error().decode()
 
 
+@pytest.mark.parametrize("kind, waves, iters, ticks, needle", [
+    (-1, 64, 16, FAKE_OUT, "kind"), (9, 64, 16, FAKE_OUT, "kind"),
+    (0, 0, 16, FAKE_OUT, "waves"), (0, (1 << 20) + 1, 16, FAKE_OUT, "waves"),
+    (0, 64, 0, FAKE_OUT, "iters"), (0, 64, 16, 0, "NULL"),
+])
+def test_valu_probe_validation(kind, waves, iters, ticks, needle):
+    rc = smol.lib().smol_valu_probe(kind, waves, iters, ticks or None, None)
+    assert rc == smol.ERR_INVALID_ARG
+    assert needle in smol.lib().smol_last_error().decode()
+
+
 def test_noalloc_refuses_batches_over_its_table():
     n = 4097
     p = _params()

@@ -1,7 +1,8 @@
 """The streaming probe (smol_stream_probe) on the GPU: every granule of the
 written buffer is written, in every read/write mix, load/store form and wave
 count the benchmark uses, including ragged sizes whose last wave ends
-mid-step; pure reads write nothing."""
+mid-step; pure reads write nothing. The VALU probe (smol_valu_probe) times
+every wave of a launch, for every instruction kind."""
 from __future__ import annotations
 
 import pytest
@@ -42,3 +43,13 @@ def test_pure_read_writes_nothing():
                       torch.cuda.current_stream().cuda_stream)
     torch.cuda.synchronize()
     assert bool((dst == SENTINEL).all())
+
+
+@pytest.mark.parametrize("kind", range(9))
+def test_valu_probe_times_every_wave(kind):
+    import torch
+    note(f"valu probe kind={kind}")
+    ticks = torch.zeros(2048, dtype=torch.int64, device="cuda:0")
+    smol.valu_probe(kind, 2048, 64, ticks.data_ptr(), torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    assert bool((ticks > 0).all())
