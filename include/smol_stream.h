@@ -55,7 +55,13 @@ int smol_stream_probe(const void *src, uint64_t read_bytes, void *dst, uint64_t 
 #define SMOL_VALU_MED3_F32 6    /* v_med3_f32         */
 #define SMOL_VALU_CVT_F32_I32 7 /* v_cvt_f32_i32      */
 #define SMOL_VALU_MUL_U24 8     /* v_mul_u32_u24      */
-#define SMOL_VALU_KINDS 9
+#define SMOL_VALU_MUL_LO_U32 9  /* v_mul_lo_u32       */
+#define SMOL_VALU_MAX_F32 10    /* v_max_f32          */
+#define SMOL_VALU_ADD_U32 11    /* v_add_u32          */
+#define SMOL_VALU_CNDMASK 12    /* v_cndmask_b32      */
+#define SMOL_VALU_CVT_UBYTE0 13 /* v_cvt_f32_ubyte0   */
+#define SMOL_VALU_AND_B32 14    /* v_and_b32          */
+#define SMOL_VALU_KINDS 15
 
 /* The issue rate of one kind of VALU instruction, the other ceiling of the
  * preprocessing kernels (the I420 path and the block decoder spend more time

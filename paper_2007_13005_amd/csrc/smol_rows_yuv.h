@@ -434,13 +434,29 @@ __device__ __forceinline__ void yuv_read_px(uint32_t aY, uint32_t aC, uint32_t (
     }
 }
 
+// s * v for factors below 2^24 as one v_mul_u32_u24. (__umul24 of a factor
+// computed in another basic block reaches instruction selection as a plain
+// 32-bit multiply, v_mul_lo_u32, which issues at a quarter of the rate.)
+// s must be the same in every lane.
+__device__ __forceinline__ uint32_t mul_u24_sv(uint32_t s, uint32_t v)
+{
+    uint32_t r;
+    asm("v_mul_u32_u24 %0, %1, %2" : "=v"(r) : "s"(s), "v"(v));
+    return r;
+}
+
 // 16 * (chroma - 128) at one luma tap: the tap's four chroma samples
 // (selected from chroma rows ra and rb) dotted with its weight bytes, minus
-// 2048, exact in integers.
+// 2048, exact in integers. The sum, in [-2048, 2032], is accumulated onto the
+// bit pattern of 1.5 * 2^23, where consecutive floats are 1 apart, so the
+// result reads as the float 1.5 * 2^23 + (S - 2048); subtracting 1.5 * 2^23
+// is exact. (One fp32 subtraction instead of an integer conversion, which
+// issues at half the rate.)
 __device__ __forceinline__ float chroma16(uint32_t ra, uint32_t rb, uint32_t sel, uint32_t wts)
 {
     const uint32_t smp = __builtin_amdgcn_perm(rb, ra, sel);
-    return (float)(int)__builtin_amdgcn_udot4(smp, wts, (uint32_t)-2048, false);
+    return __uint_as_float(__builtin_amdgcn_udot4(smp, wts, 0x4B400000u - 2048u, false)) -
+           12582912.0f;
 }
 
 // One output row from the staged segments. SAME: every luma segment of the
@@ -454,7 +470,9 @@ __device__ __forceinline__ void yuv_compute(const NormK &nk, uint32_t slot, cons
 {
     // weight bytes of luma row yi and column xi: hw(xi) * (4 + 65535 fy(yi))
     // = (4 - fy) * [4 - fx, fx, 0, 0] + fy * [0, 0, 4 - fx, fx] (no carries)
-    const uint32_t vm[2] = {4u + 65535u * (uint32_t)fy0, 4u + 65535u * (uint32_t)fy1};
+    const uint32_t vm[2] = {
+        (uint32_t)__builtin_amdgcn_readfirstlane((int)(4u + 65535u * (uint32_t)fy0)),
+        (uint32_t)__builtin_amdgcn_readfirstlane((int)(4u + 65535u * (uint32_t)fy1))};
     const uint32_t baseY = slot + yuv_seg<GL>(0) + (uint32_t)sh[0];
     const uint32_t baseC = slot + yuv_seg<GL>(2) + (uint32_t)sh[2];
 #pragma unroll
@@ -483,8 +501,8 @@ __device__ __forceinline__ void yuv_compute(const NormK &nk, uint32_t slot, cons
                 const uint32_t r0 = q[2 + 3 * pl], r1 = q[3 + 3 * pl], r2 = q[4 + 3 * pl];
 #pragma unroll
                 for (int xi = 0; xi < 2; ++xi) {
-                    cc[pl][0][xi] = chroma16(r0, r1, k.sel[j][px][xi], __umul24(k.hw[j][px][xi], vm[0]));
-                    cc[pl][1][xi] = chroma16(r1, r2, k.sel[j][px][xi], __umul24(k.hw[j][px][xi], vm[1]));
+                    cc[pl][0][xi] = chroma16(r0, r1, k.sel[j][px][xi], mul_u24_sv(vm[0], k.hw[j][px][xi]));
+                    cc[pl][1][xi] = chroma16(r1, r2, k.sel[j][px][xi], mul_u24_sv(vm[1], k.hw[j][px][xi]));
                 }
             }
             float rgb[2][2][3];  // [luma row][luma col][channel]

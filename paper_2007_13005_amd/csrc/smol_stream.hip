@@ -101,7 +101,7 @@ __global__ void __launch_bounds__(64 * kWavesPerGroup) stream_kernel(StreamArgs 
 }
 
 // Eight independent chains of one instruction (operands %0 .. %7 the chains,
-// %8 and %9 shared sources).
+// %8 and %9 shared sources, %10 a lane mask).
 #define SMOL_V8(I) I("%0") I("%1") I("%2") I("%3") I("%4") I("%5") I("%6") I("%7")
 #define SMOL_MUL(R) "v_mul_f32 " R ", " R ", %8\n\t"
 #define SMOL_ADD(R) "v_add_f32 " R ", " R ", %8\n\t"
@@ -112,11 +112,17 @@ __global__ void __launch_bounds__(64 * kWavesPerGroup) stream_kernel(StreamArgs 
 #define SMOL_MED3(R) "v_med3_f32 " R ", " R ", %8, %9\n\t"
 #define SMOL_CVT(R) "v_cvt_f32_i32 " R ", " R "\n\t"
 #define SMOL_MULU24(R) "v_mul_u32_u24 " R ", " R ", %8\n\t"
+#define SMOL_MULLO(R) "v_mul_lo_u32 " R ", " R ", %8\n\t"
+#define SMOL_MAX(R) "v_max_f32 " R ", " R ", %8\n\t"
+#define SMOL_ADDU(R) "v_add_u32 " R ", " R ", %8\n\t"
+#define SMOL_CND(R) "v_cndmask_b32_e64 " R ", " R ", %8, %10\n\t"
+#define SMOL_UBYTE(R) "v_cvt_f32_ubyte0 " R ", " R "\n\t"
+#define SMOL_AND(R) "v_and_b32 " R ", " R ", %8\n\t"
 #define SMOL_VALU_STEP(BODY)                                                                     \
     asm volatile(SMOL_V8(BODY)                                                                   \
                  : "+v"(r[0]), "+v"(r[1]), "+v"(r[2]), "+v"(r[3]), "+v"(r[4]), "+v"(r[5]),     \
                    "+v"(r[6]), "+v"(r[7])                                                       \
-                 : "v"(x), "v"(y))
+                 : "v"(x), "v"(y), "s"(m))
 
 template <int K>
 __global__ void __launch_bounds__(64) valu_kernel(uint64_t *ticks, int32_t iters)
@@ -126,6 +132,7 @@ __global__ void __launch_bounds__(64) valu_kernel(uint64_t *ticks, int32_t iters
     for (int k = 0; k < 8; ++k)
         r[k] = 0x3f800000u + 977u * (uint32_t)k + (uint32_t)threadIdx.x;
     const uint32_t x = 0x3f7ffff0u + (uint32_t)threadIdx.x, y = 0x3f800010u;
+    const uint64_t m = 0x5555555555555555ull;
     const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
 #pragma unroll 4
     for (int32_t it = 0; it < iters; ++it) {
@@ -137,7 +144,13 @@ __global__ void __launch_bounds__(64) valu_kernel(uint64_t *ticks, int32_t iters
         else if constexpr (K == 5) SMOL_VALU_STEP(SMOL_DOT4);
         else if constexpr (K == 6) SMOL_VALU_STEP(SMOL_MED3);
         else if constexpr (K == 7) SMOL_VALU_STEP(SMOL_CVT);
-        else SMOL_VALU_STEP(SMOL_MULU24);
+        else if constexpr (K == 8) SMOL_VALU_STEP(SMOL_MULU24);
+        else if constexpr (K == 9) SMOL_VALU_STEP(SMOL_MULLO);
+        else if constexpr (K == 10) SMOL_VALU_STEP(SMOL_MAX);
+        else if constexpr (K == 11) SMOL_VALU_STEP(SMOL_ADDU);
+        else if constexpr (K == 12) SMOL_VALU_STEP(SMOL_CND);
+        else if constexpr (K == 13) SMOL_VALU_STEP(SMOL_UBYTE);
+        else SMOL_VALU_STEP(SMOL_AND);
     }
     const uint64_t t1 = __builtin_amdgcn_s_memrealtime();
     // keep the chains
@@ -165,7 +178,9 @@ extern "C" int smol_valu_probe(int32_t kind, int32_t waves, int32_t iters, uint6
     static const void *const kernels[SMOL_VALU_KINDS] = {
         (const void *)valu_kernel<0>, (const void *)valu_kernel<1>, (const void *)valu_kernel<2>,
         (const void *)valu_kernel<3>, (const void *)valu_kernel<4>, (const void *)valu_kernel<5>,
-        (const void *)valu_kernel<6>, (const void *)valu_kernel<7>, (const void *)valu_kernel<8>};
+        (const void *)valu_kernel<6>, (const void *)valu_kernel<7>, (const void *)valu_kernel<8>,
+        (const void *)valu_kernel<9>, (const void *)valu_kernel<10>, (const void *)valu_kernel<11>,
+        (const void *)valu_kernel<12>, (const void *)valu_kernel<13>, (const void *)valu_kernel<14>};
     void *args[] = {(void *)&ticks, (void *)&iters};
     const hipError_t e = hipLaunchKernel(kernels[kind], dim3((unsigned)waves), dim3(64), args, 0,
                                          (hipStream_t)stream);

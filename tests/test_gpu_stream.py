@@ -45,7 +45,7 @@ def test_pure_read_writes_nothing():
     assert bool((dst == SENTINEL).all())
 
 
-@pytest.mark.parametrize("kind", range(9))
+@pytest.mark.parametrize("kind", range(len(smol.VALU_KINDS)))
 def test_valu_probe_times_every_wave(kind):
     import torch
     note(f"valu probe kind={kind}")
