@@ -434,10 +434,10 @@ __device__ __forceinline__ void yuv_read_px(uint32_t aY, uint32_t aC, uint32_t (
     }
 }
 
-// s * v for factors below 2^24 as one v_mul_u32_u24. (__umul24 of a factor
-// computed in another basic block reaches instruction selection as a plain
-// 32-bit multiply, v_mul_lo_u32, which issues at a quarter of the rate.)
-// s must be the same in every lane.
+// s * v for factors below 2^24 as one v_mul_u32_u24 with s in a scalar
+// register. (__umul24 of a factor computed in another basic block reaches
+// instruction selection as a plain 32-bit multiply, v_mul_lo_u32.) s must be
+// the same in every lane.
 __device__ __forceinline__ uint32_t mul_u24_sv(uint32_t s, uint32_t v)
 {
     uint32_t r;
