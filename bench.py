@@ -34,9 +34,12 @@ HBM_PEAK_GBPS = 8000.0  # MI355X published HBM3E bandwidth
 # 2.4 GHz). A SIMD issues a 64-lane VALU instruction every 4 clocks (16 lanes
 # per clock); unpacked fp32 adds, multiplies and fused multiply-adds issue at
 # twice that rate (32 lanes per clock, two instructions from two waves per
-# 4 clocks), everything else (conversions, integer, permutes, byte alignment,
-# dot products, min/max/med3) at the single rate. These rates are measured by
-# `smol_valu_probe` (`--valu-probe`). The definition's operations are
+# 4 clocks), and so do 32-bit integer adds and bitwise operations; conversions,
+# integer products, permutes, byte alignment, dot products, min/max/med3 and
+# lane selects issue at the single rate. These rates are measured by
+# `smol_valu_probe` (`--valu-probe`). The counters separate fp32 adds,
+# multiplies and fused multiply-adds only, so every other instruction is
+# priced at the single rate (an upper bound). The definition's operations are
 # separately rounded adds and multiplies (no contraction), one instruction
 # each, so their ceiling is 256 * 4 * 32 * 2.4e9 = 78.6 T operations/s: half
 # the published 157.3 TFLOP/s, which counts a fused multiply-add as two.
