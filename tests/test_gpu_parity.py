@@ -408,6 +408,22 @@ def test_yuv_row_segment_offsets_exact(name, sizes, dtype):
                                   ref.view(np.uint32 if dtype == F32 else np.uint16))
 
 
+@pytest.mark.parametrize("cb,cr", [(0, 255), (255, 0), (0, 0), (255, 255)])
+def test_yuv_extreme_chroma_exact(cb, cr):
+    """Chroma planes at 0 and 255: the chroma sums at their extremes (16 x
+    (0 - 128) and 16 x (255 - 128)), where the row kernel's conversion of the
+    sum to fp32 must still be exact; bit-identical to the oracle."""
+    rng = np.random.default_rng(cb * 7 + cr)
+    planes = []
+    for w, h in [(1280, 720), (641, 359)]:
+        ch, cw = (h + 1) // 2, (w + 1) // 2
+        planes.append((rng.integers(0, 256, size=(h, w), dtype=np.uint8),
+                       np.full((ch, cw), cb, np.uint8), np.full((ch, cw), cr, np.uint8)))
+    smol.set_tuning(path=smol.PATH_ROWS, exact=1)
+    got, ref = _check(synthetic.yuv420_workload("extreme", planes, 256, 224, F32))
+    np.testing.assert_array_equal(got.view(np.uint32), ref.view(np.uint32))
+
+
 @pytest.mark.parametrize("path", [smol.PATH_AUTO, smol.PATH_ROWS])
 def test_yuv_frame_at_end_of_src_first_in_batch(path):
     """Batch order reverses memory order: the frame whose planes end at the
