@@ -362,7 +362,8 @@ int smol_image_geometry_ex(int32_t width, int32_t height, int32_t yuv420, const 
  *               for the row-streaming kernels, whose workgroups hold 1, 2
  *               or 4 independent waves, the cap counts waves; by default as
  *               many as can be resident (row streaming with 4 KiB staged
- *               rows: 8 waves)
+ *               rows: 8 waves); for block decoding (smol_jpeg.h) the
+ *               launch's one-wave workgroups per compute unit (default 128)
  *   exact       1: the row-streaming kernels form the normalisation as the
  *               correctly rounded quotient (v - mean) / std and round to
  *               fp16 from that fp32 value, bit-identical to a scalar fp32

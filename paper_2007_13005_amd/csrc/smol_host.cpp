@@ -1487,6 +1487,12 @@ int smol::mcu_rect(int64_t W, int64_t H, const smol_params *p, int resize_mode, 
 
 void smol::add_plan_launches(int k) { g_last_plan.launches += k; }
 
+namespace smol {
+// The workgroups_per_cu knob (0: automatic), read by block decoding's launch
+// (smol_jpeg.cpp).
+int tuned_workgroups_per_cu() { return g_wg_per_cu.load(); }
+}  // namespace smol
+
 int smol::device_cus()
 {
     int device = 0;

@@ -13,6 +13,12 @@
 #include "smol_magic.h"
 #include "smol_jpeg.h"
 
+namespace smol {
+// The workgroups_per_cu knob of smol_set_tuning, 0 when automatic
+// (smol_host.cpp).
+int tuned_workgroups_per_cu();
+}  // namespace smol
+
 namespace {
 
 // launches of block decoding made by the calling thread's last decode
@@ -209,10 +215,12 @@ int smol_jpeg_decode_i420(const int16_t *coef, int64_t coef_elems, const int64_t
     auto flush = [&]() -> int {
         if (a.runs == 0)
             return SMOL_OK;
-        // 128 one-wave workgroups per compute unit, each looping over jobs:
-        // measured faster than 32 (long-lived waves) and than one workgroup
-        // per job on 128 720p frames
-        const int grid = (int)std::min<long long>(jobs, (long long)(cus > 0 ? cus : 256) * 128);
+        // 128 one-wave workgroups per compute unit, each looping over jobs
+        // (or the workgroups_per_cu knob): measured faster than 32
+        // (long-lived waves) and than one workgroup per job on 128 720p
+        // frames
+        const int per_cu = smol::tuned_workgroups_per_cu() > 0 ? smol::tuned_workgroups_per_cu() : 128;
+        const int grid = (int)std::min<long long>(jobs, (long long)(cus > 0 ? cus : 256) * per_cu);
         const int rc = smol::launch_jpeg_idct(a, grid, stream);
         t_decode_launches += rc == (int)hipSuccess ? 1 : 0;
         a.runs = 0;

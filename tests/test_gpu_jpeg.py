@@ -149,3 +149,17 @@ def test_jpeg_c8_full():
     got = run_gpu(wl)
     stats = assert_parity(got, run_oracle(wl), wl.out_dtype, wl.name)
     note(f"    c8: {stats} plan={smol.last_plan()}")
+
+
+@pytest.mark.parametrize("wg", [1, 3])
+def test_block_decoder_walks_many_groups_per_wave(wg):
+    """A launch of `wg` one-wave workgroups per compute unit: every wave
+    walks many groups of blocks, across runs of different geometries,
+    reading each next group's rows while it computes the current one; the
+    decodes of the whole-frame and many-runs cases stay bit for bit."""
+    smol.set_tuning(workgroups_per_cu=wg)
+    try:
+        test_whole_frame_decode_bit_exact()
+        test_ragged_batch_spans_several_launches()
+    finally:
+        smol.reset_tuning()
