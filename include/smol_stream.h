@@ -61,7 +61,8 @@ int smol_stream_probe(const void *src, uint64_t read_bytes, void *dst, uint64_t 
 #define SMOL_VALU_CNDMASK 12    /* v_cndmask_b32      */
 #define SMOL_VALU_CVT_UBYTE0 13 /* v_cvt_f32_ubyte0   */
 #define SMOL_VALU_AND_B32 14    /* v_and_b32          */
-#define SMOL_VALU_KINDS 15
+#define SMOL_VALU_ADD_F32_SALU 15 /* v_add_f32, each followed by an s_add_u32 */
+#define SMOL_VALU_KINDS 16
 
 /* The issue rate of one kind of VALU instruction, the other ceiling of the
  * preprocessing kernels (the I420 path and the block decoder spend more time

@@ -124,6 +124,16 @@ __global__ void __launch_bounds__(64 * kWavesPerGroup) stream_kernel(StreamArgs 
                    "+v"(r[6]), "+v"(r[7])                                                       \
                  : "v"(x), "v"(y), "s"(m))
 
+// v_add_f32 on the eight chains, each followed by an s_add_u32 on one scalar
+// chain (%8): whether scalar instructions take a wave's VALU issue slots.
+#define SMOL_ADD_SALU(R) "v_add_f32 " R ", " R ", %9\n\ts_add_u32 %8, %8, 1\n\t"
+#define SMOL_VALU_SALU_STEP                                                                      \
+    asm volatile(SMOL_V8(SMOL_ADD_SALU)                                                          \
+                 : "+v"(r[0]), "+v"(r[1]), "+v"(r[2]), "+v"(r[3]), "+v"(r[4]), "+v"(r[5]),     \
+                   "+v"(r[6]), "+v"(r[7]), "+s"(sc)                                             \
+                 : "v"(x)                                                                       \
+                 : "scc")
+
 template <int K>
 __global__ void __launch_bounds__(64) valu_kernel(uint64_t *ticks, int32_t iters)
 {
@@ -133,6 +143,7 @@ __global__ void __launch_bounds__(64) valu_kernel(uint64_t *ticks, int32_t iters
         r[k] = 0x3f800000u + 977u * (uint32_t)k + (uint32_t)threadIdx.x;
     const uint32_t x = 0x3f7ffff0u + (uint32_t)threadIdx.x, y = 0x3f800010u;
     const uint64_t m = 0x5555555555555555ull;
+    uint32_t sc = 0;
     const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
 #pragma unroll 4
     for (int32_t it = 0; it < iters; ++it) {
@@ -150,16 +161,18 @@ __global__ void __launch_bounds__(64) valu_kernel(uint64_t *ticks, int32_t iters
         else if constexpr (K == 11) SMOL_VALU_STEP(SMOL_ADDU);
         else if constexpr (K == 12) SMOL_VALU_STEP(SMOL_CND);
         else if constexpr (K == 13) SMOL_VALU_STEP(SMOL_UBYTE);
-        else SMOL_VALU_STEP(SMOL_AND);
+        else if constexpr (K == 14) SMOL_VALU_STEP(SMOL_AND);
+        else SMOL_VALU_SALU_STEP;
     }
     const uint64_t t1 = __builtin_amdgcn_s_memrealtime();
     // keep the chains
     asm volatile("" ::"v"(r[0]), "v"(r[1]), "v"(r[2]), "v"(r[3]), "v"(r[4]), "v"(r[5]),
-                 "v"(r[6]), "v"(r[7]));
+                 "v"(r[6]), "v"(r[7]), "s"(sc));
     if (threadIdx.x == 0)
         ticks[blockIdx.x] = t1 - t0;
 }
 #undef SMOL_VALU_STEP
+#undef SMOL_VALU_SALU_STEP
 
 }  // namespace
 }  // namespace smol
@@ -180,7 +193,8 @@ extern "C" int smol_valu_probe(int32_t kind, int32_t waves, int32_t iters, uint6
         (const void *)valu_kernel<3>, (const void *)valu_kernel<4>, (const void *)valu_kernel<5>,
         (const void *)valu_kernel<6>, (const void *)valu_kernel<7>, (const void *)valu_kernel<8>,
         (const void *)valu_kernel<9>, (const void *)valu_kernel<10>, (const void *)valu_kernel<11>,
-        (const void *)valu_kernel<12>, (const void *)valu_kernel<13>, (const void *)valu_kernel<14>};
+        (const void *)valu_kernel<12>, (const void *)valu_kernel<13>, (const void *)valu_kernel<14>,
+        (const void *)valu_kernel<15>};
     void *args[] = {(void *)&ticks, (void *)&iters};
     const hipError_t e = hipLaunchKernel(kernels[kind], dim3((unsigned)waves), dim3(64), args, 0,
                                          (hipStream_t)stream);

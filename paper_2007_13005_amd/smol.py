@@ -343,7 +343,7 @@ def stream_probe(src: int, read_bytes: int, dst: int, write_bytes: int, waves: i
 
 VALU_KINDS = ("mul_f32", "add_f32", "fma_f32", "perm", "alignbyte", "dot4", "med3_f32",
               "cvt_f32_i32", "mul_u24", "mul_lo_u32", "max_f32", "add_u32", "cndmask",
-              "cvt_f32_ubyte0", "and_b32")
+              "cvt_f32_ubyte0", "and_b32", "add_f32_salu")
 
 
 def valu_probe(kind: int, waves: int, iters: int, ticks: int, stream: int = 0) -> None:

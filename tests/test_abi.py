@@ -480,7 +480,7 @@ def test_stream_probe_validation(kw, needle):
 
 
 @pytest.mark.parametrize("kind, waves, iters, ticks, needle", [
-    (-1, 64, 16, FAKE_OUT, "kind"), (15, 64, 16, FAKE_OUT, "kind"),
+    (-1, 64, 16, FAKE_OUT, "kind"), (16, 64, 16, FAKE_OUT, "kind"),
     (0, 0, 16, FAKE_OUT, "waves"), (0, (1 << 20) + 1, 16, FAKE_OUT, "waves"),
     (0, 64, 0, FAKE_OUT, "iters"), (0, 64, 16, 0, "NULL"),
 ])
