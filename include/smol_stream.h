@@ -59,7 +59,7 @@ int smol_stream_probe(const void *src, uint64_t read_bytes, void *dst, uint64_t 
 #define SMOL_VALU_MAX_F32 10    /* v_max_f32          */
 #define SMOL_VALU_ADD_U32 11    /* v_add_u32          */
 #define SMOL_VALU_CNDMASK 12    /* v_cndmask_b32      */
-#define SMOL_VALU_CVT_UBYTE0 13 /* v_cvt_f32_ubyte0   */
+#define SMOL_VALU_CVT_F32_UBYTE0 13 /* v_cvt_f32_ubyte0 */
 #define SMOL_VALU_AND_B32 14    /* v_and_b32          */
 #define SMOL_VALU_ADD_F32_SALU 15 /* v_add_f32, each followed by an s_add_u32 */
 #define SMOL_VALU_KINDS 16

@@ -490,6 +490,17 @@ def test_valu_probe_validation(kind, waves, iters, ticks, needle):
     assert needle in smol.lib().smol_last_error().decode()
 
 
+def test_valu_probe_kinds_match_the_header():
+    """The binding's kind names follow the header's SMOL_VALU_* numbering."""
+    hdr = open(os.path.join(os.path.dirname(__file__), "..", "include", "smol_stream.h")).read()
+    kinds = {int(v): n for n, v in re.findall(r"#define SMOL_VALU_(\w+) (\d+)", hdr)}
+    count = kinds.pop(len(smol.VALU_KINDS), None)
+    assert count == "KINDS"
+    assert sorted(kinds) == list(range(len(smol.VALU_KINDS)))
+    for k, name in kinds.items():
+        assert name.lower().replace("_", "") == smol.VALU_KINDS[k].replace("_", ""), (k, name)
+
+
 def test_noalloc_refuses_batches_over_its_table():
     n = 4097
     p = _params()
